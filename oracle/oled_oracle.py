@@ -1,0 +1,244 @@
+"""CPU oracle of the block-MoE expert layer under partial expert residency.
+
+TEST INFRASTRUCTURE ONLY. Only the tests, the smoke check of the build entry
+point and the CPU-baseline leg of the benchmark may import this module. The
+product path never calls it, and it shares no code with the HIP library.
+
+What it computes, for one MoE layer l in one denoising iteration i of a
+semi-autoregressive dLLM (OLED-MoE, Sec. 2.1 and Sec. 4), step by step and in
+float64 from the exact input bits:
+
+  O1 route      top-k experts per token and their gate scores (Sec. 2.1, 4.1)
+  O2 permute    expert histogram, offsets, stable token permutation
+  O3 classify   active set A, hits A & R, misses M = A \\ R (Sec. 4.2)
+  O4 expert_ffn SwiGLU expert FFN
+  O5 moe_output y[t] = sum_j g[t][j] * FFN_{idx[t][j]}(x[t]); it does not
+                depend on R (the system is lossless, Sec. 5.1)
+  O6 score      reuse-priority numerators (the priority equation of Sec. 4.3)
+  O7            stale residents (resident, not activated) score zero (Sec. 4.3)
+  O8 retain     R^{i+1} = Top_C(R^i u G^i, p) (the retention rule, Sec. 4.2),
+                with G = M (every miss is transferred to the GPU)
+  O9            R^{i+1} feeds the same layer at iteration i+1 (Sec. 4.1)
+
+Readings where the paper is silent (each is restated in the design notes):
+  * gate function: softmax over the k selected logits (equal to a full softmax
+    renormalised over the top-k); exp and the sum in float64, sum in slot
+    order, one round-to-nearest to float32;
+  * ties in top-k: lower expert id first; slot order is (logit desc, id asc);
+  * the gate score in the priority is the renormalised float32 gate;
+  * psi(c) = c, the paper's default;
+  * the priority numerator is accumulated exactly as integers,
+    S[e] = sum floor(g * c * 2^48): g*c is exact in float64 (24+24 bits) and
+    the floor is exact, so any summation order gives the same S. Ranking by S
+    equals ranking by p_e because the denominator is one per-layer constant;
+  * Top-C ties: (S desc, previously resident first, id asc); candidates with
+    S = 0 are kept while capacity remains (eviction only when over capacity);
+  * utilisation = hits / C (fraction of cache capacity serving activated
+    experts, Sec. 3.2 and Sec. 5.1).
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+SCORE_SHIFT = 48
+SCORE_SCALE = float(2 ** SCORE_SHIFT)
+
+
+# ------------------------------------------------------------ input decoding
+def bf16_bits_to_f64(bits: np.ndarray) -> np.ndarray:
+    """uint16 bf16 bit patterns -> float64 (exact)."""
+    u32 = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+    return u32.view(np.float32).astype(np.float64)
+
+
+def decode(a: np.ndarray) -> np.ndarray:
+    """Workload-encoded array (float32, or uint16 bf16 bits) -> float64."""
+    if a.dtype == np.uint16:
+        return bf16_bits_to_f64(a)
+    return np.asarray(a, dtype=np.float32).astype(np.float64)
+
+
+# ----------------------------------------------------------------- O1 route
+def route(logits: np.ndarray, k: int):
+    """O1. Top-k routing of every token of the block, with gate scores.
+
+    logits: float32 [T][E]. Returns idx int32 [T][k] ordered by
+    (logit desc, expert id asc) and gates float32 [T][k]:
+      gate[t][j] = fl32( e_j / (e_0 + ... + e_{k-1}) ),
+      e_j = exp(logit[t][idx[t][j]] - logit[t][idx[t][0]]) in float64.
+    """
+    logits = np.asarray(logits, dtype=np.float32)
+    if not np.all(np.isfinite(logits)):
+        raise ValueError("non-finite router logit")
+    T, E = logits.shape
+    if not 1 <= k <= E:
+        raise ValueError("top_k out of range")
+    # stable sort on -logit keeps lower ids first among equal logits
+    order = np.argsort(-logits.astype(np.float64), axis=1, kind="stable")
+    idx = order[:, :k].astype(np.int32)
+    gates = np.empty((T, k), dtype=np.float32)
+    for t in range(T):
+        sel = [float(logits[t, e]) for e in idx[t]]
+        ex = [math.exp(v - sel[0]) for v in sel]
+        s = 0.0
+        for v in ex:
+            s += v
+        for j in range(k):
+            gates[t, j] = np.float32(ex[j] / s)
+    return idx, gates
+
+
+# --------------------------------------------------------------- O2 permute
+def permute(idx: np.ndarray, n_experts: int):
+    """O2. Expert histogram, exclusive offsets and stable counting-sort permutation.
+
+    Route r = t*k + j goes to position offsets[e] + #{t' < t : e in idx[t']}.
+    Returns counts [E], offsets [E+1], perm [T*k] (position -> route) and
+    inv_perm [T*k] (route -> position), all int32.
+    """
+    flat = np.asarray(idx, dtype=np.int64).ravel()
+    counts = np.zeros(n_experts, dtype=np.int64)
+    for e in flat:
+        counts[e] += 1
+    offsets = np.zeros(n_experts + 1, dtype=np.int64)
+    for e in range(n_experts):
+        offsets[e + 1] = offsets[e] + counts[e]
+    seen = np.zeros(n_experts, dtype=np.int64)
+    inv_perm = np.empty(flat.size, dtype=np.int64)
+    for r, e in enumerate(flat):
+        inv_perm[r] = offsets[e] + seen[e]
+        seen[e] += 1
+    perm = np.empty(flat.size, dtype=np.int64)
+    perm[inv_perm] = np.arange(flat.size)
+    return (counts.astype(np.int32), offsets.astype(np.int32),
+            perm.astype(np.int32), inv_perm.astype(np.int32))
+
+
+# -------------------------------------------------------------- O3 classify
+def classify(counts: np.ndarray, resident: np.ndarray):
+    """O3. Active set A, hit mask A & R, miss mask M = A \\ R (Sec. 4.2)."""
+    active = np.asarray(counts) > 0
+    resident = np.asarray(resident, dtype=bool)
+    return active, active & resident, active & ~resident
+
+
+# ------------------------------------------------------------ O4/O5 outputs
+def silu(z: np.ndarray) -> np.ndarray:
+    return z / (1.0 + np.exp(-z))
+
+
+def expert_ffn(x: np.ndarray, w13: np.ndarray, w2: np.ndarray) -> np.ndarray:
+    """O4. SwiGLU expert FFN in float64: W2 (silu(W1 x) * (W3 x)).
+
+    x [n][H]; w13 [2I][H] (W1 rows, then W3 rows); w2 [H][I]. No biases.
+    """
+    inter = w2.shape[1]
+    a = x @ w13[:inter].T
+    b = x @ w13[inter:].T
+    return (silu(a) * b) @ w2.T
+
+
+def moe_output(x: np.ndarray, idx: np.ndarray, gates: np.ndarray, expert_weights,
+               tokens=None) -> np.ndarray:
+    """O5. y[t] = sum_j gate[t][j] * FFN_{idx[t][j]}(x[t]) in float64.
+
+    x float64 [T][H]; expert_weights(e) -> (w13, w2) float64. `tokens`
+    restricts the evaluation to a subset of token rows (returned in that order).
+    """
+    T = x.shape[0]
+    rows = np.arange(T) if tokens is None else np.asarray(tokens)
+    y = np.zeros((rows.size, x.shape[1]), dtype=np.float64)
+    sub = idx[rows]
+    for e in np.unique(sub):
+        w13, w2 = expert_weights(int(e))
+        for j in range(idx.shape[1]):
+            sel = np.nonzero(sub[:, j] == e)[0]
+            if sel.size:
+                out = expert_ffn(x[rows[sel]], w13, w2)
+                y[sel] += gates[rows[sel], j].astype(np.float64)[:, None] * out
+    return y
+
+
+# ---------------------------------------------------------------- O6 score
+def score(idx: np.ndarray, gates: np.ndarray, conf: np.ndarray, n_experts: int):
+    """O6/O7. Reuse-priority numerators of Sec. 4.3 with psi(c) = c.
+
+    S[e] = sum over routes (t, j) with idx[t][j] == e of
+           floor(float64(gate[t][j]) * float64(conf[t]) * 2^48).
+    Experts routed by no token (stale residents included) get 0.
+    Returns (S as Python ints in a uint64 array, p = S / sum(S) in float64).
+    """
+    conf = np.asarray(conf, dtype=np.float32)
+    if not np.all((conf >= 0.0) & (conf <= 1.0)):
+        raise ValueError("confidence outside [0, 1]")
+    T, k = idx.shape
+    S = [0] * n_experts
+    for t in range(T):
+        c = float(conf[t])
+        for j in range(k):
+            term = math.floor(float(gates[t, j]) * c * SCORE_SCALE)
+            S[int(idx[t, j])] += int(term)
+    total = sum(S)
+    p = np.array([s / total if total else 0.0 for s in S], dtype=np.float64)
+    return np.array(S, dtype=np.uint64), p
+
+
+# --------------------------------------------------------------- O8 retain
+def retain(S: np.ndarray, resident: np.ndarray, miss: np.ndarray, capacity: int):
+    """O8. R^{i+1} = Top_C(R^i u G^i, p) with G = M (retention rule, Sec. 4.2).
+
+    Candidates are ordered by (S desc, previously resident first, id asc) and
+    the first min(C, |cand|) are kept. Returns the new resident mask (bool [E]).
+    """
+    resident = np.asarray(resident, dtype=bool)
+    cand = [e for e in range(len(S)) if resident[e] or miss[e]]
+    cand.sort(key=lambda e: (-int(S[e]), 0 if resident[e] else 1, e))
+    keep = np.zeros(len(S), dtype=bool)
+    for e in cand[: max(0, min(capacity, len(cand)))]:
+        keep[e] = True
+    return keep
+
+
+# --------------------------------------------------- O1..O9, one layer-step
+def layer_step(logits, conf, resident, top_k: int, capacity: int):
+    """Control path of one layer-iteration (O1-O3, O6-O8): no expert outputs.
+
+    Returns a dict with idx, gates, counts, offsets, perm, inv_perm, active,
+    hit, miss, n_hits, n_misses, util, S, p and the new resident mask.
+    """
+    E = logits.shape[1]
+    idx, gates = route(logits, top_k)
+    counts, offsets, perm, inv_perm = permute(idx, E)
+    active, hit, miss = classify(counts, resident)
+    S, p = score(idx, gates, conf, E)
+    new_res = retain(S, resident, miss, capacity)
+    n_hits = int(hit.sum())
+    return dict(idx=idx, gates=gates, counts=counts, offsets=offsets, perm=perm,
+                inv_perm=inv_perm, active=active, hit=hit, miss=miss,
+                n_active=int(active.sum()), n_hits=n_hits, n_misses=int(miss.sum()),
+                util=(n_hits / capacity if capacity > 0 else 0.0),
+                S=S, p=p, resident_before=np.asarray(resident, dtype=bool).copy(),
+                resident_after=new_res)
+
+
+def run_schedule(logits_fn, conf_fn, n_layers: int, n_iters: int, n_experts: int,
+                 top_k: int, capacity: int, resident0=None):
+    """O9. Replays the cache state of every layer over iterations 0..n_iters-1.
+
+    logits_fn(l, i) -> float32 [T][E]; conf_fn(l, i) -> float32 [T].
+    The cache starts empty (R^0 = {} per layer) unless resident0 is given.
+    Returns steps[i][l] (the layer_step dicts).
+    """
+    res = [np.zeros(n_experts, dtype=bool) if resident0 is None
+           else np.asarray(resident0[l], dtype=bool) for l in range(n_layers)]
+    steps = []
+    for i in range(n_iters):
+        row = []
+        for l in range(n_layers):
+            st = layer_step(logits_fn(l, i), conf_fn(l, i), res[l], top_k, capacity)
+            res[l] = st["resident_after"]
+            row.append(st)
+        steps.append(row)
+    return steps
