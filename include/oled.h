@@ -1,0 +1,242 @@
+/*
+ * oled.h - C ABI of the OLED-MoE block-MoE layer hot path for MI355X (gfx950).
+ *
+ * One MoE layer l in one denoising iteration i of a semi-autoregressive dLLM,
+ * run with a fixed-capacity per-layer GPU expert cache (OLED-MoE, Sec. 4.1):
+ *
+ *   route_block        the gate's routed expert ids and gate scores for every
+ *                      token of the block (Sec. 4.1), plus the expert
+ *                      histogram, offsets and stable token permutation
+ *   apply_misses       active set A, hits A & R and misses M = A \ R of the
+ *                      layer (Sec. 4.2); every miss is transferred host->device
+ *                      into a staging slot on a copy stream (G = M)
+ *   moe_forward_cached the SwiGLU experts over the cached (hit) experts, then
+ *                      over the transferred misses once their copies land,
+ *                      and the gate-weighted combine (Sec. 4.1)
+ *   score_and_retain   reuse priorities p_e (the priority equation of
+ *                      Sec. 4.3, psi(c) = c; stale residents score zero) and
+ *                      the retention rule R' = Top_C(R u G, p) of Sec. 4.2
+ *
+ * Call order per (layer, iteration): route_block -> apply_misses ->
+ * [moe_forward_cached] -> score_and_retain. Exactly one layer is in flight per
+ * context; any other order returns OLED_ERR_STATE and changes nothing.
+ * moe_forward_cached may be skipped (control path only); the cache state does
+ * not depend on expert outputs.
+ *
+ * Conventions
+ *  - Every function returns an oled_status and never aborts. Host-detected
+ *    errors (OLED_ERR_INVALID_ARG, OLED_ERR_STATE, OLED_ERR_UNSUPPORTED) leave
+ *    all host and device state unchanged. oled_last_error() describes the last
+ *    failure of a context.
+ *  - "_dev" pointers are device memory on the context's GPU, "host" pointers
+ *    are host memory. Streams are hipStream_t passed as void* (NULL = the null
+ *    stream). The caller keeps every buffer it passes alive until the stream
+ *    work that reads it has completed.
+ *  - Layouts are row-major and dense. Token t of the block is row t.
+ *  - One host thread per context. The four calls of a layer must use the same
+ *    compute stream; a new stream at route_block is ordered after the old one.
+ *  - Routing indices, permutations, hit/miss counts and retained sets are
+ *    deterministic integers; layer outputs are bitwise identical for any cache
+ *    residency (the cache only changes where weights are read from).
+ */
+#ifndef OLED_H_
+#define OLED_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  OLED_OK = 0,
+  OLED_ERR_INVALID_ARG = 1,  /* bad argument, or bad data found on the device */
+  OLED_ERR_OUT_OF_MEMORY = 2,
+  OLED_ERR_HIP = 3,          /* a HIP runtime call failed */
+  OLED_ERR_STATE = 4,        /* call out of order for this context */
+  OLED_ERR_UNSUPPORTED = 5   /* shape outside the supported range */
+} oled_status;
+
+typedef enum { OLED_F32 = 0, OLED_BF16 = 1 } oled_dtype;
+
+/* Context flags. */
+#define OLED_FLAG_PROFILE 1 /* time every kernel and copy with HIP events */
+
+/*
+ * Shape and resources of one MoE layer stack.
+ *  hidden H, inter I: multiples of 128. n_experts E in [1, 256]. top_k k in
+ *  [1, min(E, 16)]. n_layers L >= 1. capacity C >= 0 experts per layer (C = 0:
+ *  every active expert misses; C >= E: full residency). max_tokens Tmax in
+ *  [1, 65535] (bounds the integer priority sums, see score_and_retain).
+ *  dtype: activations, weights and outputs; accumulation is fp32.
+ *
+ *  host_pool: caller-owned pinned host memory (hipHostMalloc, oled_host_alloc
+ *  or a pinned torch tensor) of host_pool_blocks expert blocks, each
+ *  3*H*I*elem bytes: w13 [2I][H] (gate projection W1 rows, then up projection
+ *  W3 rows) followed by w2 [H][I]. host_block_of[l*E + e] in
+ *  [0, host_pool_blocks) names the block of expert e of layer l; several
+ *  experts may share one block. The pool must outlive the context; the table
+ *  is copied at creation.
+ */
+typedef struct {
+  int32_t hidden;
+  int32_t inter;
+  int32_t n_experts;
+  int32_t top_k;
+  int32_t n_layers;
+  int32_t capacity;
+  int32_t max_tokens;
+  int32_t dtype;            /* oled_dtype */
+  int32_t device;           /* HIP device ordinal */
+  int32_t flags;            /* OLED_FLAG_* */
+  const void* host_pool;
+  int64_t host_pool_blocks;
+  const int64_t* host_block_of;
+} oled_config;
+
+/* Result of apply_misses for the layer (Sec. 4.2). Counts are experts. */
+typedef struct {
+  int32_t n_active;       /* |A| */
+  int32_t n_hits;         /* |A & R| */
+  int32_t n_misses;       /* |M| = |A \ R|, all transferred */
+  int32_t n_resident;     /* |R| before execution */
+  int32_t rejected_layer; /* a layer whose last retention was rejected for an
+                             invalid confidence since the previous report, else -1 */
+  int32_t reserved;
+  int64_t h2d_bytes;      /* bytes enqueued on the copy stream */
+} oled_miss_report;
+
+/*
+ * Inspection of a layer (synchronises the device). Every pointer is a
+ * caller-owned host array or NULL (skipped). The routing arrays describe the
+ * most recent route_block call of the context; they are filled only if that
+ * call was for `layer` (then `tokens` = its T, else 0).
+ */
+typedef struct {
+  int32_t* topk_idx;          /* [T*k] expert of route r = t*k + j, slot order (logit desc, id asc) */
+  float* gates;               /* [T*k] gate of route r (fp32) */
+  int32_t* counts;            /* [E] routes per expert */
+  int32_t* offsets;           /* [E+1] exclusive prefix sum of counts */
+  int32_t* perm;              /* [T*k] sorted position -> route */
+  int32_t* inv_perm;          /* [T*k] route -> sorted position */
+  uint64_t* score_q;          /* [E] priority numerators of the last score_and_retain of `layer` */
+  uint8_t* resident_before;   /* [E] R of the layer before its last execution */
+  uint8_t* resident_after;    /* [E] committed R of the layer now */
+  int32_t* slot_of;           /* [E] committed cache slot per expert, -1 if absent */
+  int32_t tokens;
+  int32_t n_active, n_hits, n_misses;
+} oled_layer_state;
+
+/* One timed operation (OLED_FLAG_PROFILE). */
+typedef struct {
+  int32_t kind;      /* oled_op_kind */
+  int32_t layer;
+  float ms;          /* device time between the events around the operation */
+  int64_t bytes;     /* algorithmic bytes moved */
+  int64_t flops;     /* algorithmic flops */
+} oled_op_time;
+
+typedef enum {
+  OLED_OP_ROUTE_TOPK = 0,
+  OLED_OP_PERMUTE = 1,
+  OLED_OP_FFN_UP = 2,        /* grouped gate/up GEMM + SiLU*up epilogue */
+  OLED_OP_FFN_DOWN = 3,      /* grouped down GEMM */
+  OLED_OP_COMBINE = 4,
+  OLED_OP_SCORE_RETAIN = 5,
+  OLED_OP_H2D = 6            /* miss copies of one apply_misses */
+} oled_op_kind;
+
+/* Creates a context: allocates the slot pool (L*min(C,E) + min(E, Tmax*k)
+ * expert slots), routing scratch, pinned summaries, a copy stream and events
+ * on cfg->device. The cache starts empty (R = {} for every layer).
+ * Errors: INVALID_ARG (bad field, host pool not pinned), UNSUPPORTED (shape),
+ * OUT_OF_MEMORY, HIP. On error *ctx_out is NULL. */
+oled_status oled_create(const oled_config* cfg, void** ctx_out);
+
+/* Waits for outstanding work and frees everything the context owns. NULL ok. */
+void oled_destroy(void* ctx);
+
+/* Text of the last error of ctx (never NULL; empty if none). With ctx NULL,
+ * the last oled_create failure of the calling thread. */
+const char* oled_last_error(const void* ctx);
+
+/* Empties every layer's cache (R := {}), as at creation. Synchronises. */
+oled_status oled_reset_cache(void* ctx);
+
+/*
+ * route_block: the gate of Sec. 4.1 for the T tokens of the block.
+ *  logits_dev: float [T][E] router logits. For each token the k largest
+ *  logits are selected, ordered by (logit desc, expert id asc) (-0.0 equals
+ *  +0.0); gate[t][j] = e_j / sum_j' e_j' with e_j = exp(l_j - l_0) in fp64,
+ *  summed in slot order, rounded once to fp32. Then the expert histogram,
+ *  exclusive offsets and the stable counting-sort permutation of the T*k
+ *  routes by (expert, token). Asynchronous on `stream`.
+ *  Errors: INVALID_ARG (layer outside [0,L), T outside [1,Tmax], NULL logits),
+ *  STATE. A non-finite logit is detected on the device and reported by the
+ *  following apply_misses.
+ */
+oled_status route_block(void* ctx, int32_t layer, const float* logits_dev, int32_t T,
+                        void* stream);
+
+/*
+ * apply_misses: misses M = A \ R of the routed layer (Sec. 4.2) and their
+ *  transfer (G = M). Waits for route_block's results (the one host sync of a
+ *  layer), gives every miss a free staging slot and enqueues one
+ *  host-to-device copy of the expert's block per miss on copy_stream (NULL:
+ *  the context's own copy stream), overlapping the hit experts' compute.
+ *  Fills *out (may be NULL).
+ *  Errors: STATE; INVALID_ARG if the logits held a non-finite value (no copy
+ *  is issued; the layer returns to idle with its cache unchanged); HIP if a
+ *  copy could not be enqueued (staged slots are released, cache unchanged).
+ *  Retentions enqueued earlier are committed here; one rejected for an
+ *  invalid confidence is named in out->rejected_layer (the call still
+ *  returns OLED_OK for its own work).
+ */
+oled_status apply_misses(void* ctx, int32_t layer, void* copy_stream, oled_miss_report* out);
+
+/*
+ * moe_forward_cached: the layer output (Sec. 4.1; lossless, Sec. 5.1)
+ *  y[t] = sum_j gate[t][j] * W2_e (silu(W1_e x[t]) * (W3_e x[t])), e = idx[t][j].
+ *  x_dev: [T][H] dtype (read); y_dev: [T][H] dtype (overwritten). Hit experts
+ *  run first from their cache slots; the misses run after their copies
+ *  complete (the stream waits on the copy events). Accumulation is fp32; the
+ *  intermediate silu(W1 x) * (W3 x) is stored in dtype.
+ *  Errors: STATE, INVALID_ARG (NULL pointers).
+ */
+oled_status moe_forward_cached(void* ctx, int32_t layer, const void* x_dev, void* y_dev,
+                               void* stream);
+
+/*
+ * score_and_retain: priorities of Sec. 4.3 and the retention rule of Sec. 4.2.
+ *  conf_dev: float [T] token confidence in [0, 1]. For each expert,
+ *  S[e] = sum over its routes of floor(fp64(gate) * fp64(conf[t]) * 2^48)
+ *  (exact; p_e = S[e] / sum S). Residents that no token routed to score 0.
+ *  Candidates R u M are ranked by (S desc, previously resident first, id asc)
+ *  and the first min(C, |R u M|) stay cached for the next iteration of this
+ *  layer; the rest release their slots. The new cache state is committed on
+ *  the host at the next synchronising call.
+ *  Errors: STATE, INVALID_ARG (NULL conf). A confidence outside [0,1] (or NaN)
+ *  is detected on the device: the layer keeps its previous R, its transferred
+ *  misses are dropped, and the rejection is reported by the next
+ *  apply_misses (rejected_layer) and by oled_read_layer_state.
+ */
+oled_status score_and_retain(void* ctx, int32_t layer, const float* conf_dev, void* stream);
+
+/* Inspection (synchronises; see oled_layer_state). Returns INVALID_ARG (with
+ * the arrays filled) if the layer's last retention was rejected. */
+oled_status oled_read_layer_state(void* ctx, int32_t layer, oled_layer_state* out);
+
+/* Operation timings recorded since the last collection (OLED_FLAG_PROFILE).
+ * Synchronises. Writes at most cap entries to out, sets *n_out; entries that
+ * did not fit are dropped. */
+oled_status oled_profile_collect(void* ctx, oled_op_time* out, int32_t cap, int32_t* n_out);
+
+/* Pinned host memory for expert pools (hipHostMalloc). *ptr_out NULL on error. */
+oled_status oled_host_alloc(int64_t bytes, void** ptr_out);
+void oled_host_free(void* ptr);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OLED_H_ */

@@ -1,0 +1,85 @@
+"""Builds the gfx950 HIP library (liboled.so) and the host-only cache test library.
+
+    python -m paper_2609_33385_amd.build
+
+Compiles every source each time it is called. Objects go to csrc/_build/.
+"""
+from __future__ import annotations
+
+import concurrent.futures
+import os
+import shutil
+import subprocess
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+INCLUDE = os.path.join(ROOT, "include")
+OBJ = os.path.join(CSRC, "_build")
+LIB = os.path.join(PKG, "liboled.so")
+CACHE_LIB = os.path.join(PKG, "liboled_cache_host.so")
+
+ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
+HIPCC = os.path.join(ROCM, "bin", "hipcc")
+ARCH = "gfx950"
+
+HIP_SOURCES = ["route.hip", "ffn.hip", "score.hip"]
+HOST_SOURCES = ["oled.cpp", "cache_state.cpp"]
+
+HIP_FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
+             # keep hand-written and compiler-generated fp32 code off packed-fp32 ops
+             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+             f"-I{INCLUDE}", f"-I{CSRC}"]
+HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-D__HIP_PLATFORM_AMD__",
+              f"-I{ROCM}/include", f"-I{INCLUDE}", f"-I{CSRC}"]
+
+
+def _run(cmd):
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("build step failed:\n" + " ".join(cmd) + "\n" + r.stdout + r.stderr)
+    return r
+
+
+def _compile(src: str) -> str:
+    path = os.path.join(CSRC, src)
+    obj = os.path.join(OBJ, src + ".o")
+    if src.endswith(".hip"):
+        _run([HIPCC, *HIP_FLAGS, "-c", path, "-o", obj])
+    else:
+        _run(["g++", *HOST_FLAGS, "-c", path, "-o", obj])
+    return obj
+
+
+def build(verbose: bool = False) -> str:
+    """Compiles the HIP library for gfx950 and the host-only cache library."""
+    if not os.path.exists(HIPCC):
+        raise RuntimeError(f"hipcc not found at {HIPCC}")
+    os.makedirs(OBJ, exist_ok=True)
+    srcs = HIP_SOURCES + HOST_SOURCES
+    with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
+        objs = list(ex.map(_compile, srcs))
+    tmp = LIB + ".tmp"
+    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp])
+    os.replace(tmp, LIB)
+    tmp = CACHE_LIB + ".tmp"
+    _run(["g++", "-O2", "-std=c++17", "-fPIC", "-shared", f"-I{CSRC}",
+          os.path.join(CSRC, "cache_state.cpp"), os.path.join(CSRC, "cache_state_capi.cpp"),
+          "-o", tmp])
+    os.replace(tmp, CACHE_LIB)
+    if verbose:
+        print("built", LIB, "and", CACHE_LIB)
+    return LIB
+
+
+def clean() -> None:
+    shutil.rmtree(OBJ, ignore_errors=True)
+    for p in (LIB, CACHE_LIB):
+        if os.path.exists(p):
+            os.remove(p)
+
+
+if __name__ == "__main__":
+    build(verbose=True)
+    sys.exit(0)

@@ -1,0 +1,297 @@
+"""ctypes binding of the C ABI in include/oled.h (argument marshalling only).
+
+Every step of the hot path runs in the HIP library liboled.so; this module
+only converts Python/PyTorch arguments into the ABI's pointers and sizes. It
+raises if the library is missing: there is no fallback.
+
+Module-level functions carry the ABI's names (route_block, apply_misses,
+moe_forward_cached, score_and_retain, ...) and take the context handle first;
+`Context` wraps them for convenience.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liboled.so")
+
+OLED_OK = 0
+OLED_ERR_INVALID_ARG = 1
+OLED_ERR_OUT_OF_MEMORY = 2
+OLED_ERR_HIP = 3
+OLED_ERR_STATE = 4
+OLED_ERR_UNSUPPORTED = 5
+STATUS_NAMES = {0: "OK", 1: "INVALID_ARG", 2: "OUT_OF_MEMORY", 3: "HIP", 4: "STATE",
+                5: "UNSUPPORTED"}
+
+OLED_F32 = 0
+OLED_BF16 = 1
+OLED_FLAG_PROFILE = 1
+
+OP_NAMES = {0: "route_topk", 1: "permute", 2: "ffn_up", 3: "ffn_down", 4: "combine",
+            5: "score_retain", 6: "h2d"}
+
+EXPORTED = ["oled_create", "oled_destroy", "oled_last_error", "oled_reset_cache", "route_block",
+            "apply_misses", "moe_forward_cached", "score_and_retain", "oled_read_layer_state",
+            "oled_profile_collect", "oled_host_alloc", "oled_host_free"]
+
+
+class OledConfig(ctypes.Structure):
+    _fields_ = [("hidden", ctypes.c_int32), ("inter", ctypes.c_int32),
+                ("n_experts", ctypes.c_int32), ("top_k", ctypes.c_int32),
+                ("n_layers", ctypes.c_int32), ("capacity", ctypes.c_int32),
+                ("max_tokens", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("device", ctypes.c_int32), ("flags", ctypes.c_int32),
+                ("host_pool", ctypes.c_void_p), ("host_pool_blocks", ctypes.c_int64),
+                ("host_block_of", ctypes.POINTER(ctypes.c_int64))]
+
+
+class MissReport(ctypes.Structure):
+    _fields_ = [("n_active", ctypes.c_int32), ("n_hits", ctypes.c_int32),
+                ("n_misses", ctypes.c_int32), ("n_resident", ctypes.c_int32),
+                ("rejected_layer", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("h2d_bytes", ctypes.c_int64)]
+
+
+class LayerState(ctypes.Structure):
+    _fields_ = [("topk_idx", ctypes.c_void_p), ("gates", ctypes.c_void_p),
+                ("counts", ctypes.c_void_p), ("offsets", ctypes.c_void_p),
+                ("perm", ctypes.c_void_p), ("inv_perm", ctypes.c_void_p),
+                ("score_q", ctypes.c_void_p), ("resident_before", ctypes.c_void_p),
+                ("resident_after", ctypes.c_void_p), ("slot_of", ctypes.c_void_p),
+                ("tokens", ctypes.c_int32), ("n_active", ctypes.c_int32),
+                ("n_hits", ctypes.c_int32), ("n_misses", ctypes.c_int32)]
+
+
+class OpTime(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("layer", ctypes.c_int32), ("ms", ctypes.c_float),
+                ("bytes", ctypes.c_int64), ("flops", ctypes.c_int64)]
+
+
+class OledError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Loads liboled.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is missing: build it with `python -m paper_2609_33385_amd.build`")
+    lib = ctypes.CDLL(path)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    sig = {
+        "oled_create": (i32, [ctypes.POINTER(OledConfig), ctypes.POINTER(vp)]),
+        "oled_destroy": (None, [vp]),
+        "oled_last_error": (ctypes.c_char_p, [vp]),
+        "oled_reset_cache": (i32, [vp]),
+        "route_block": (i32, [vp, i32, vp, i32, vp]),
+        "apply_misses": (i32, [vp, i32, vp, ctypes.POINTER(MissReport)]),
+        "moe_forward_cached": (i32, [vp, i32, vp, vp, vp]),
+        "score_and_retain": (i32, [vp, i32, vp, vp]),
+        "oled_read_layer_state": (i32, [vp, i32, ctypes.POINTER(LayerState)]),
+        "oled_profile_collect": (i32, [vp, ctypes.POINTER(OpTime), i32, ctypes.POINTER(i32)]),
+        "oled_host_alloc": (i32, [i64, ctypes.POINTER(vp)]),
+        "oled_host_free": (None, [vp]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _ptr(x) -> int | None:
+    """Device/host address of a torch tensor, numpy array, int or None."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    if hasattr(x, "data_ptr"):
+        return x.data_ptr()
+    if isinstance(x, np.ndarray):
+        return x.ctypes.data
+    raise TypeError(f"cannot take the address of {type(x)}")
+
+
+def _stream(s) -> int | None:
+    if s is None:
+        return None
+    if isinstance(s, int):
+        return s
+    return s.cuda_stream  # torch.cuda.Stream
+
+
+def last_error(ctx) -> str:
+    return load().oled_last_error(ctx).decode()
+
+
+def _check(ctx, status: int):
+    if status != OLED_OK:
+        raise OledError(status, last_error(ctx))
+
+
+# ------------------------------------------------------------ ABI functions
+def oled_create(cfg: OledConfig) -> int:
+    lib = load()
+    h = ctypes.c_void_p()
+    st = lib.oled_create(ctypes.byref(cfg), ctypes.byref(h))
+    if st != OLED_OK:
+        raise OledError(st, lib.oled_last_error(None).decode())
+    return h.value
+
+
+def oled_destroy(ctx) -> None:
+    load().oled_destroy(ctx)
+
+
+def oled_reset_cache(ctx) -> None:
+    _check(ctx, load().oled_reset_cache(ctx))
+
+
+def route_block(ctx, layer: int, logits, T: int, stream=None) -> int:
+    return load().route_block(ctx, layer, _ptr(logits), T, _stream(stream))
+
+
+def apply_misses(ctx, layer: int, copy_stream=None, report: MissReport | None = None) -> int:
+    return load().apply_misses(ctx, layer, _stream(copy_stream),
+                               ctypes.byref(report) if report is not None else None)
+
+
+def moe_forward_cached(ctx, layer: int, x, y, stream=None) -> int:
+    return load().moe_forward_cached(ctx, layer, _ptr(x), _ptr(y), _stream(stream))
+
+
+def score_and_retain(ctx, layer: int, conf, stream=None) -> int:
+    return load().score_and_retain(ctx, layer, _ptr(conf), _stream(stream))
+
+
+def oled_read_layer_state(ctx, layer: int, state: LayerState) -> int:
+    return load().oled_read_layer_state(ctx, layer, ctypes.byref(state))
+
+
+def oled_profile_collect(ctx, cap: int = 1 << 16):
+    arr = (OpTime * cap)()
+    n = ctypes.c_int32()
+    _check(ctx, load().oled_profile_collect(ctx, arr, cap, ctypes.byref(n)))
+    return [(OP_NAMES[arr[i].kind], arr[i].layer, arr[i].ms, arr[i].bytes, arr[i].flops)
+            for i in range(n.value)]
+
+
+def oled_host_alloc(nbytes: int) -> int:
+    p = ctypes.c_void_p()
+    st = load().oled_host_alloc(nbytes, ctypes.byref(p))
+    if st != OLED_OK:
+        raise OledError(st, f"pinned host allocation of {nbytes} bytes failed")
+    return p.value
+
+
+def oled_host_free(ptr: int) -> None:
+    load().oled_host_free(ptr)
+
+
+# ---------------------------------------------------------------- helpers
+class PinnedPool:
+    """Pinned host expert pool of n_blocks blocks of block_bytes (oled_host_alloc)."""
+
+    def __init__(self, n_blocks: int, block_bytes: int):
+        self.n_blocks, self.block_bytes = n_blocks, block_bytes
+        self.ptr = oled_host_alloc(n_blocks * block_bytes)
+
+    def view(self, dtype=np.uint8) -> np.ndarray:
+        buf = (ctypes.c_char * (self.n_blocks * self.block_bytes)).from_address(self.ptr)
+        return np.frombuffer(buf, dtype=dtype)
+
+    def block(self, b: int, dtype) -> np.ndarray:
+        n = self.block_bytes // np.dtype(dtype).itemsize
+        return self.view(dtype)[b * n:(b + 1) * n]
+
+    def free(self):
+        if self.ptr:
+            oled_host_free(self.ptr)
+            self.ptr = 0
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+
+class Context:
+    """One layer stack with its expert caches (wraps the ABI functions)."""
+
+    def __init__(self, hidden, inter, n_experts, top_k, n_layers, capacity, max_tokens,
+                 dtype: str, host_pool: int, host_pool_blocks: int, host_block_of,
+                 device: int = 0, profile: bool = False):
+        self._hbo = np.ascontiguousarray(host_block_of, dtype=np.int64)
+        cfg = OledConfig(hidden, inter, n_experts, top_k, n_layers, capacity, max_tokens,
+                         OLED_F32 if dtype == "f32" else OLED_BF16, device,
+                         OLED_FLAG_PROFILE if profile else 0, host_pool, host_pool_blocks,
+                         self._hbo.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)))
+        self.E, self.k, self.L, self.C, self.Tmax = n_experts, top_k, n_layers, capacity, max_tokens
+        self.ctx = oled_create(cfg)
+
+    def close(self):
+        if self.ctx:
+            oled_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def reset_cache(self):
+        oled_reset_cache(self.ctx)
+
+    def route_block(self, layer, logits, T, stream=None):
+        _check(self.ctx, route_block(self.ctx, layer, logits, T, stream))
+
+    def apply_misses(self, layer, copy_stream=None) -> MissReport:
+        rep = MissReport()
+        _check(self.ctx, apply_misses(self.ctx, layer, copy_stream, rep))
+        return rep
+
+    def moe_forward_cached(self, layer, x, y, stream=None):
+        _check(self.ctx, moe_forward_cached(self.ctx, layer, x, y, stream))
+
+    def score_and_retain(self, layer, conf, stream=None):
+        _check(self.ctx, score_and_retain(self.ctx, layer, conf, stream))
+
+    def read_layer_state(self, layer, T=None) -> dict:
+        E, k = self.E, self.k
+        R = (T if T is not None else self.Tmax) * k
+        out = dict(topk_idx=np.zeros(R, np.int32), gates=np.zeros(R, np.float32),
+                   counts=np.zeros(E, np.int32), offsets=np.zeros(E + 1, np.int32),
+                   perm=np.zeros(R, np.int32), inv_perm=np.zeros(R, np.int32),
+                   score_q=np.zeros(E, np.uint64), resident_before=np.zeros(E, np.uint8),
+                   resident_after=np.zeros(E, np.uint8), slot_of=np.zeros(E, np.int32))
+        st = LayerState(*[a.ctypes.data for a in out.values()], 0, 0, 0, 0)
+        status = oled_read_layer_state(self.ctx, layer, st)
+        if status not in (OLED_OK, OLED_ERR_INVALID_ARG):
+            _check(self.ctx, status)
+        Tn = st.tokens
+        for key in ("topk_idx", "gates", "perm", "inv_perm"):
+            out[key] = out[key][: Tn * k]
+        out["topk_idx"] = out["topk_idx"].reshape(Tn, k)
+        out["gates"] = out["gates"].reshape(Tn, k)
+        out.update(tokens=Tn, n_active=st.n_active, n_hits=st.n_hits, n_misses=st.n_misses,
+                   rejected=(status == OLED_ERR_INVALID_ARG))
+        out["resident_before"] = out["resident_before"].astype(bool)
+        out["resident_after"] = out["resident_after"].astype(bool)
+        return out
+
+    def profile_collect(self):
+        return oled_profile_collect(self.ctx)

@@ -1,0 +1,201 @@
+"""GPU parity of the HIP path (through the C ABI) against the CPU oracle.
+
+Integer results (routing indices, permutation, counts, hits/misses, priority
+numerators, retained sets) and the fp32 gates must match bit for bit; layer
+outputs within relative L2 1e-5 (fp32) or 2e-2 (bf16).
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import oled_oracle as O
+from paper_2609_33385_amd import harness as HN
+from paper_2609_33385_amd import oled
+from paper_2609_33385_amd import workload as W
+
+from gpu_common import (OracleWeights, compare_control, oracle_schedule, rel_l2,
+                        run_schedule_gpu, tol)
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    oled.load()
+
+
+def _chain(w, seed, layers, n_iters, n_blocks, out_at=None, out_tokens=None, capacity=None,
+           forward=True):
+    """Runs a schedule on both sides and compares every layer-iteration.
+
+    out_at: set of (layer index, iteration) whose outputs are checked (None: all).
+    out_tokens: token rows checked there (None: all).
+    """
+    C = w.capacity if capacity is None else capacity
+    _say(f"[chain] {w.name} layers={list(layers)} iters={n_iters} C={C} P={n_blocks}")
+    pool = HN.fill_pool(w, seed, n_blocks)
+    ctx = HN.make_context(w, pool, capacity=C, n_layers=len(layers))
+    ref = oracle_schedule(w, seed, layers, n_iters, C)
+    ow = OracleWeights(w, seed, n_blocks, len(layers))
+    worst = [0.0]
+
+    def check(i, li, st, y):
+        where = f"{w.name} l={layers[li]} i={i}"
+        compare_control(st, ref[i][li], w.tokens, where)
+        if y is None or (out_at is not None and (li, i) not in out_at):
+            return
+        o = ref[i][li]
+        x = O.decode(W.activations(w, seed, layers[li], 0, i))
+        rows = np.arange(w.tokens) if out_tokens is None else np.asarray(out_tokens)
+        y_ref = O.moe_output(x, o["idx"], o["gates"], ow.fn(li), tokens=rows)
+        err = rel_l2(O.decode(y)[rows], y_ref)
+        worst[0] = max(worst[0], err)
+        assert err <= tol(w), f"{where}: rel L2 {err:.3e} > {tol(w)}"
+
+    try:
+        run_schedule_gpu(ctx, w, seed, layers, n_iters, forward, check)
+    finally:
+        ctx.close()
+        pool.free()
+    _say(f"[chain] {w.name} ok, worst rel L2 {worst[0]:.3e}")
+
+
+def test_cfg1_full_schedule():
+    w = W.WORKLOADS[1]
+    _chain(w, 0, range(w.n_layers), w.n_iters, w.n_layers * w.n_experts)
+
+
+SMALL = [  # (E, k, T, C, dtype, H, I)
+    (1, 1, 1, 0, "f32", 128, 128),
+    (5, 2, 37, 2, "f32", 128, 256),
+    (64, 8, 65, 26, "bf16", 256, 128),
+    (128, 8, 200, 51, "bf16", 128, 384),
+    (256, 16, 33, 100, "bf16", 128, 128),
+    (33, 3, 600, 33, "f32", 128, 128),
+    (64, 8, 130, 0, "bf16", 256, 256),
+    (16, 4, 1025, 40, "bf16", 128, 128),
+]
+
+
+@pytest.mark.parametrize("E,k,T,C,dt,H,I", SMALL)
+def test_small_shapes(E, k, T, C, dt, H, I):
+    w = W.WORKLOADS[1].replace(wid=100 + E, name=f"small-E{E}-k{k}-T{T}", dtype=dt, batch=1,
+                               block=T, n_experts=E, top_k=k, hidden=H, inter=I, n_layers=2,
+                               n_iters=3, capacity=C)
+    _chain(w, 1, range(2), 3, min(2 * E, 24))
+
+
+def test_ties_and_signed_zero():
+    """Tied logits (small integer alphabet) and -0.0 / +0.0 through the ABI."""
+    rng = np.random.default_rng(5)
+    E, k, T, H, I = 12, 3, 70, 128, 128
+    w = W.WORKLOADS[1].replace(wid=200, name="ties", batch=1, block=T, n_experts=E, top_k=k,
+                               hidden=H, inter=I, n_layers=1, n_iters=1, capacity=4)
+    lg = rng.integers(-2, 3, size=(T, E)).astype(np.float32)
+    lg[::5, 0] = -0.0
+    lg[::5, 1] = 0.0
+    conf = rng.uniform(0, 1, T).astype(np.float32)
+    pool = HN.fill_pool(w, 0, E)
+    ctx = HN.make_context(w, pool)
+    try:
+        HN.layer_step(ctx, 0, torch.from_numpy(lg).cuda(), torch.from_numpy(conf).cuda())
+        st = ctx.read_layer_state(0, T)
+        ref = O.layer_step(lg, conf, np.zeros(E, bool), k, 4)
+        compare_control(st, ref, T, "ties")
+    finally:
+        ctx.close()
+        pool.free()
+
+
+def test_cfg2_chain():
+    w = W.WORKLOADS[2]
+    L, N = w.n_layers, w.n_iters
+    out_at = {(l, i) for l in (0, L // 2, L - 1) for i in (0, 1, N - 1)}
+    _chain(w, 0, range(L), N, 64, out_at=out_at)
+
+
+def test_cfg3_chain():
+    w = W.WORKLOADS[3]
+    L, N = w.n_layers, w.n_iters
+    _chain(w, 0, range(L), N, 64, out_at={(0, 0), (L - 1, N - 1)})
+
+
+@pytest.mark.parametrize("wid", [4, 5])
+def test_cfg45_chain(wid):
+    w = W.WORKLOADS[wid]
+    layers = [0, w.n_layers // 2, w.n_layers - 1]
+    rows = np.random.default_rng(wid).choice(w.tokens, 16, replace=False)
+    _chain(w, 0, layers, w.n_iters, 8, out_at={(0, 0), (2, w.n_iters - 1)}, out_tokens=rows)
+
+
+def test_cross_residency_bitwise():
+    """Outputs do not depend on the cache state (lossless): C = E, 40%, 0."""
+    w = W.WORKLOADS[2]
+    layers, N = [0, 1], 4
+    pool = HN.fill_pool(w, 0, 16)
+    outs = {}
+    for C in (w.n_experts, w.capacity, 0):
+        ctx = HN.make_context(w, pool, capacity=C, n_layers=len(layers))
+        got = []
+        run_schedule_gpu(ctx, w, 0, layers, N, True,
+                         lambda i, li, st, y: got.append((st["n_hits"], y.copy())))
+        ctx.close()
+        outs[C] = got
+    pool.free()
+    base = outs[w.n_experts]
+    for C, got in outs.items():
+        for (h0, y0), (h1, y1) in zip(base, got):
+            assert np.array_equal(y0, y1), f"C={C}: outputs differ from full residency"
+    assert sum(h for h, _ in outs[0]) == 0
+
+
+def test_error_paths():
+    w = W.WORKLOADS[1]
+    pool = HN.fill_pool(w, 0, 8)
+    ctx = HN.make_context(w, pool)
+    T, E = w.tokens, w.n_experts
+    s = torch.cuda.current_stream()
+    try:
+        lg = torch.from_numpy(W.logits(w, 0, 0, 0, 0)).cuda()
+        conf = torch.from_numpy(W.confidence(w, 0, 0, 0)).cuda()
+        # out of order
+        assert oled.apply_misses(ctx.ctx, 0, None, None) == oled.OLED_ERR_STATE
+        assert oled.score_and_retain(ctx.ctx, 0, conf, s) == oled.OLED_ERR_STATE
+        assert oled.route_block(ctx.ctx, 0, lg, 0, s) == oled.OLED_ERR_INVALID_ARG
+        assert oled.route_block(ctx.ctx, 0, lg, T + 1, s) == oled.OLED_ERR_INVALID_ARG
+        assert oled.route_block(ctx.ctx, 5, lg, T, s) == oled.OLED_ERR_INVALID_ARG
+        # one good step fills the cache
+        HN.layer_step(ctx, 0, lg, conf)
+        before = ctx.read_layer_state(0, T)["resident_after"].copy()
+        assert before.any()
+        # a non-finite logit: apply_misses refuses, nothing changes
+        bad = lg.clone()
+        bad[3, 2] = float("nan")
+        ctx.route_block(0, bad, T, s)
+        rep = oled.MissReport()
+        assert oled.apply_misses(ctx.ctx, 0, None, rep) == oled.OLED_ERR_INVALID_ARG
+        assert np.array_equal(ctx.read_layer_state(0, T)["resident_after"], before)
+        # confidence outside [0, 1]: retention rejected, R kept, reported
+        lg1 = torch.from_numpy(W.logits(w, 0, 0, 0, 1)).cuda()
+        badc = conf.clone()
+        badc[0] = 1.5
+        HN.layer_step(ctx, 0, lg1, badc)
+        st = ctx.read_layer_state(0, T)
+        assert st["rejected"]
+        assert np.array_equal(st["resident_after"], before)
+        ctx.route_block(0, lg1, T, s)
+        rep = ctx.apply_misses(0)
+        assert rep.rejected_layer == 0   # reported once, by the next apply_misses
+        ctx.score_and_retain(0, conf, s)
+        assert not ctx.read_layer_state(0, T)["rejected"]
+    finally:
+        ctx.close()
+        pool.free()

@@ -1,0 +1,196 @@
+"""CPU-only checks of the library: it loads and exports every symbol of the
+header, validates arguments before touching a GPU, and its host cache
+bookkeeping keeps the oracle's resident sets with conserved slots."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+from oracle import oled_oracle as O
+from paper_2609_33385_amd import oled
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "oled.h")
+CSRC = os.path.join(ROOT, "paper_2609_33385_amd", "csrc")
+CACHE_LIB = os.path.join(ROOT, "paper_2609_33385_amd", "liboled_cache_host.so")
+
+
+def header_functions():
+    text = open(HEADER).read()
+    return re.findall(r"^\s*(?:oled_status|void|const char\s*\*)\s+(\w+)\s*\(", text, re.M)
+
+
+def test_library_exports_header_symbols():
+    names = header_functions()
+    assert set(names) == set(oled.EXPORTED), names
+    lib = oled.load()
+    out = subprocess.run(["nm", "-D", "--defined-only", oled.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = {ln.split()[-1] for ln in out.splitlines() if ln.strip()}
+    for n in names:
+        assert n in exported, n
+        assert getattr(lib, n) is not None
+
+
+def test_library_targets_gfx950():
+    out = subprocess.run(["/opt/rocm/bin/roc-obj-ls", oled.LIB_PATH], capture_output=True,
+                         text=True)
+    if out.returncode != 0:
+        pytest.skip("roc-obj-ls unavailable")
+    assert "gfx950" in out.stdout
+
+
+def _cfg(**kw):
+    base = dict(hidden=256, inter=512, n_experts=8, top_k=2, n_layers=1, capacity=4,
+                max_tokens=32, dtype=oled.OLED_F32, device=0, flags=0, host_pool=None,
+                host_pool_blocks=0, host_block_of=None)
+    base.update(kw)
+    hbo = np.zeros(base["n_layers"] * base["n_experts"], np.int64)
+    c = oled.OledConfig(base["hidden"], base["inter"], base["n_experts"], base["top_k"],
+                        base["n_layers"], base["capacity"], base["max_tokens"], base["dtype"],
+                        base["device"], base["flags"], base["host_pool"] or 0,
+                        base["host_pool_blocks"],
+                        hbo.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)))
+    return c, hbo
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(hidden=0), oled.OLED_ERR_INVALID_ARG),
+    (dict(top_k=9), oled.OLED_ERR_INVALID_ARG),
+    (dict(dtype=7), oled.OLED_ERR_INVALID_ARG),
+    (dict(hidden=200, host_pool=1, host_pool_blocks=1), oled.OLED_ERR_UNSUPPORTED),
+    (dict(n_experts=300, top_k=2, host_pool=1, host_pool_blocks=1), oled.OLED_ERR_UNSUPPORTED),
+    (dict(max_tokens=70000, host_pool=1, host_pool_blocks=1), oled.OLED_ERR_UNSUPPORTED),
+    (dict(capacity=-1), oled.OLED_ERR_INVALID_ARG),
+    (dict(), oled.OLED_ERR_INVALID_ARG),  # no host pool
+])
+def test_create_validates_before_device(kw, status):
+    lib = oled.load()
+    cfg, _hbo = _cfg(**kw)
+    h = ctypes.c_void_p()
+    assert lib.oled_create(ctypes.byref(cfg), ctypes.byref(h)) == status
+    assert h.value is None
+    assert lib.oled_last_error(None)
+
+
+def test_null_context_calls():
+    lib = oled.load()
+    assert lib.route_block(None, 0, None, 1, None) == oled.OLED_ERR_INVALID_ARG
+    assert lib.apply_misses(None, 0, None, None) == oled.OLED_ERR_INVALID_ARG
+    assert lib.moe_forward_cached(None, 0, None, None, None) == oled.OLED_ERR_INVALID_ARG
+    assert lib.score_and_retain(None, 0, None, None) == oled.OLED_ERR_INVALID_ARG
+    assert lib.oled_reset_cache(None) == oled.OLED_ERR_INVALID_ARG
+    lib.oled_destroy(None)
+
+
+# -------------------------------------------------- host cache bookkeeping
+class HostCache:
+    def __init__(self, L, E, C, n_slots):
+        self.lib = ctypes.CDLL(CACHE_LIB)
+        vp, i = ctypes.c_void_p, ctypes.c_int
+        sigs = {"oled_cs_create": (vp, [i, i, i, i]), "oled_cs_destroy": (None, [vp]),
+                "oled_cs_reset": (None, [vp]), "oled_cs_check": (i, [vp]),
+                "oled_cs_free_slots": (i, [vp]),
+                "oled_cs_classify": (None, [vp, i, vp, vp, vp, vp]),
+                "oled_cs_stage": (i, [vp, i, vp, vp, vp]), "oled_cs_drop": (None, [vp, i]),
+                "oled_cs_commit": (i, [vp, i, vp]), "oled_cs_resident": (None, [vp, i, vp]),
+                "oled_cs_slots": (None, [vp, i, vp])}
+        for n, (res, args) in sigs.items():
+            getattr(self.lib, n).restype = res
+            getattr(self.lib, n).argtypes = args
+        self.p = ctypes.c_void_p(self.lib.oled_cs_create(L, E, C, n_slots))
+        self.E = E
+
+    def __del__(self):
+        self.lib.oled_cs_destroy(self.p)
+
+    def classify(self, l, counts):
+        c = np.ascontiguousarray(counts, np.int32)
+        hit, miss, n3 = np.zeros(self.E, np.uint8), np.zeros(self.E, np.uint8), np.zeros(3, np.int32)
+        self.lib.oled_cs_classify(self.p, l, c.ctypes.data, hit.ctypes.data, miss.ctypes.data,
+                                  n3.ctypes.data)
+        return hit.astype(bool), miss.astype(bool), n3
+
+    def stage(self, l, miss):
+        m = np.ascontiguousarray(miss, np.uint8)
+        ex, sl = np.zeros(self.E, np.int32), np.zeros(self.E, np.int32)
+        n = self.lib.oled_cs_stage(self.p, l, m.ctypes.data, ex.ctypes.data, sl.ctypes.data)
+        return n, ex[:max(n, 0)], sl[:max(n, 0)]
+
+    def commit(self, l, keep):
+        k = np.ascontiguousarray(keep, np.uint8)
+        return self.lib.oled_cs_commit(self.p, l, k.ctypes.data) == 1
+
+    def resident(self, l):
+        r = np.zeros(self.E, np.uint8)
+        self.lib.oled_cs_resident(self.p, l, r.ctypes.data)
+        return r.astype(bool)
+
+    def slots(self, l):
+        s = np.zeros(self.E, np.int32)
+        self.lib.oled_cs_slots(self.p, l, s.ctypes.data)
+        return s
+
+    def check(self):
+        return self.lib.oled_cs_check(self.p) == 1
+
+
+@pytest.mark.parametrize("C", [0, 2, 4, 8])
+def test_host_cache_follows_oracle(C):
+    """The bookkeeping stages the oracle's misses and commits its retained sets."""
+    rng = np.random.default_rng(C)
+    L, E, k, T, N = 3, 8, 2, 16, 8
+    hc = HostCache(L, E, C, L * min(C, E) + E)
+    res = [np.zeros(E, bool) for _ in range(L)]
+    walk = np.cumsum(rng.standard_normal((N, L, T, E)) * 0.5, axis=0) + 2 * rng.standard_normal((L, T, E))
+    for i in range(N):
+        conf = rng.uniform(0, 1, T).astype(np.float32)
+        for l in range(L):
+            st = O.layer_step(walk[i, l].astype(np.float32), conf, res[l], k, C)
+            hit, miss, n3 = hc.classify(l, st["counts"])
+            assert np.array_equal(hit, st["hit"]) and np.array_equal(miss, st["miss"])
+            assert tuple(n3) == (st["n_active"], st["n_hits"], st["n_misses"])
+            assert np.array_equal(hc.resident(l), res[l])
+            n, ex, sl = hc.stage(l, miss)
+            assert n == st["n_misses"] and len(set(sl.tolist())) == n
+            before = hc.slots(l)
+            assert hc.commit(l, st["resident_after"])
+            after = hc.slots(l)
+            kept = st["resident_after"]
+            # retained experts keep their slot (residents and staged misses alike)
+            assert np.array_equal(after[kept], before[kept])
+            assert np.all(after[~kept] == -1)
+            assert hc.check()
+            res[l] = st["resident_after"]
+
+
+def test_host_cache_rollback_and_refusals():
+    hc = HostCache(2, 6, 2, 2 * 2 + 6)
+    miss = np.array([1, 1, 1, 0, 0, 0], bool)
+    n, ex, sl = hc.stage(0, miss)
+    assert n == 3 and hc.check()
+    assert hc.stage(0, miss)[0] == -1                       # already staged
+    assert not hc.commit(0, np.array([1, 1, 1, 0, 0, 0]))   # more than C
+    assert not hc.commit(0, np.array([0, 0, 0, 1, 0, 0]))   # not a candidate
+    hc.lib.oled_cs_drop(hc.p, 0)                             # failed copy: roll back
+    assert hc.check() and not hc.resident(0).any()
+    assert hc.lib.oled_cs_free_slots(hc.p) == 10
+    n, ex, sl = hc.stage(0, miss)
+    assert hc.commit(0, np.array([1, 0, 1, 0, 0, 0])) and hc.check()
+    assert hc.lib.oled_cs_free_slots(hc.p) == 8
+
+
+def test_host_cache_sanitized_selftest(tmp_path):
+    exe = tmp_path / "cache_selftest"
+    src = os.path.join(ROOT, "tests", "native", "cache_state_selftest.cpp")
+    r = subprocess.run(["g++", "-std=c++17", "-O1", "-g", "-fsanitize=address,undefined",
+                        "-fno-sanitize-recover=all", f"-I{CSRC}", src,
+                        os.path.join(CSRC, "cache_state.cpp"), "-o", str(exe)],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "selftest ok" in r.stdout
