@@ -1,0 +1,253 @@
+"""Block-MoE layer throughput on one MI355X under 40% expert residency.
+
+Workload: LLaDA-MoE-like layer stack in bf16 - hidden 2048, 64 experts,
+top-8, expert SwiGLU intermediate 1024, 16 MoE layers, batch 1 x block 32
+tokens, 8 denoising iterations per block, expert cache 26 of 64 experts per
+layer (40%). One step is one denoising iteration through all 16 layers: per
+layer route_block -> moe_forward_cached (cached experts) -> apply_misses
+(host-to-device copies of missed experts on a side stream, their GEMMs, the
+combine) -> score_and_retain. Blocks follow each
+other without resetting the caches; the warm-up steps cover the cold start.
+
+Inputs (router logits, activations, confidence) are generated before timing
+and resident in HBM; the expert weights live in a pinned host pool (all
+16 x 64 experts, 12 GiB) and reach the GPU only through cache misses.
+
+Prints one JSON line with the layer-token throughput, the roofline of the
+dominant kernel (grouped gate/up GEMM, timed with HIP events on its stream
+during the timed steps) and the CPU oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 MFMA
+METRIC = "block-MoE layer tokens/s at 40% expert residency; grouped-GEMM MFMA util"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def fill_pool_device(pool, w, seed: int, chunk: int = 64):
+    """Fills the pinned pool with N(0, 0.02^2) bf16 weights drawn on the GPU."""
+    import torch
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    host = torch.from_numpy(pool.view(np.int16))
+    per = w.expert_elems
+    for b0 in range(0, pool.n_blocks, chunk):
+        n = min(chunk, pool.n_blocks - b0)
+        v = (torch.randn(n * per, generator=g, device="cuda") * 0.02).to(torch.bfloat16)
+        host[b0 * per:(b0 + n) * per].copy_(v.view(torch.int16))
+    torch.cuda.synchronize()
+
+
+def make_inputs(w, seed: int, n_steps: int):
+    """Device tensors: logits[g][l] [T][E] fp32, x[g][l] [T][H] bf16, conf[g] [T]."""
+    import torch
+    from paper_2609_33385_amd import harness as HN
+    from paper_2609_33385_amd import workload as W
+    N, L = w.n_iters, w.n_layers
+    n_blocks = (n_steps + N - 1) // N
+    lg = np.empty((n_blocks * N, L, w.tokens, w.n_experts), np.float32)
+    for b in range(n_blocks):
+        for l in range(L):
+            lg[b * N:(b + 1) * N, l] = W.logits_block(w, seed, l, b)
+    xs = np.empty((n_steps, L, w.tokens, w.hidden), np.uint16)
+    cf = np.empty((n_steps, w.tokens), np.float32)
+    for g in range(n_steps):
+        b, it = divmod(g, N)
+        cf[g] = W.confidence(w, seed, b, it)
+        for l in range(L):
+            xs[g, l] = W.activations(w, seed, l, b, it)
+    return (torch.from_numpy(lg[:n_steps]).cuda(), HN.to_device(xs), torch.from_numpy(cf).cuda())
+
+
+def cpu_baseline(w, seed: int):
+    """The oracle on host cores: every layer of block 0, iteration 1, with the FFN."""
+    from threadpoolctl import threadpool_info
+
+    from oracle import oled_oracle as O
+    from paper_2609_33385_amd import workload as W
+    P = 64
+    raw = {b: W.expert_block(w, seed, b) for b in range(P)}   # drawn outside the timing
+    hbo = W.host_block_of(w, P)
+    res0 = [np.zeros(w.n_experts, bool) for _ in range(w.n_layers)]
+    for l in range(w.n_layers):                               # iteration 0 fills R (untimed)
+        res0[l] = O.layer_step(W.logits(w, seed, l, 0, 0), W.confidence(w, seed, 0, 0), res0[l],
+                               w.top_k, w.capacity)["resident_after"]
+    iters = (1, 2)
+    inputs = {it: (W.confidence(w, seed, 0, it),
+                   [(W.logits(w, seed, l, 0, it), O.decode(W.activations(w, seed, l, 0, it)))
+                    for l in range(w.n_layers)]) for it in iters}
+    t0 = time.perf_counter()
+    for it in iters:
+        conf, rows = inputs[it]
+        for l, (lg, x) in enumerate(rows):
+            st = O.layer_step(lg, conf, res0[l], w.top_k, w.capacity)
+            res0[l] = st["resident_after"]
+
+            def weights(e, l=l):
+                return W.split_expert(w, O.decode(raw[int(hbo[l * w.n_experts + e])]))
+
+            O.moe_output(x, st["idx"], st["gates"], weights)
+    dt = time.perf_counter() - t0
+    n = len(iters) * w.n_layers
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {"value": n * w.tokens / dt, "unit": "layer-tokens/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": (f"{n} layer-iterations (all {w.n_layers} layers of block 0, iterations 1-2) "
+                       f"of the same workload: routing, permutation, hit/miss sets, priorities, "
+                       f"retention and the float64 SwiGLU experts + combine; {dt:.1f} s, BLAS on "
+                       f"{threads} threads of {os.cpu_count()} host CPUs")}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=64)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--capacity", type=int, default=None, help="experts cached per layer")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-ops", default="ffn_up,ffn_down,h2d",
+                    help="operations timed with HIP events during the timed steps ('' for none)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: the expert-offloading layer path has no multi-GPU "
+              "mode in this build (run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_33385_amd import oled
+    from paper_2609_33385_amd import workload as W
+
+    w = W.WORKLOADS[2]
+    if args.capacity is not None:
+        w = w.replace(capacity=args.capacity)
+    L, T, E = w.n_layers, w.tokens, w.n_experts
+    torch.cuda.set_device(0)
+    lib = oled.load()
+
+    t0 = time.time()
+    pool = oled.PinnedPool(L * E, w.expert_bytes)
+    fill_pool_device(pool, w, args.seed)
+    n_total = args.warmup + args.steps
+    logits, xs, conf = make_inputs(w, args.seed, n_total)
+    y = torch.empty((T, w.hidden), dtype=torch.bfloat16, device="cuda")
+    prof = oled.profile_mask(*[o for o in args.profile_ops.split(",") if o])
+    ctx = oled.Context(w.hidden, w.inter, E, w.top_k, L, w.capacity, T, w.dtype, pool.ptr,
+                       pool.n_blocks, W.host_block_of(w, pool.n_blocks), profile_ops=prof)
+    log(f"setup {time.time() - t0:.1f}s: pool {pool.n_blocks} x {w.expert_bytes >> 20} MiB pinned")
+
+    h = ctx.ctx
+    s = torch.cuda.current_stream()
+    sp = s.cuda_stream
+    lg_p = [[logits[g, l].data_ptr() for l in range(L)] for g in range(n_total)]
+    x_p = [[xs[g, l].data_ptr() for l in range(L)] for g in range(n_total)]
+    c_p = [conf[g].data_ptr() for g in range(n_total)]
+    y_p = y.data_ptr()
+    rep = oled.MissReport()
+    rep_ref = ctypes.byref(rep)
+    stats = {"hits": 0, "misses": 0, "active": 0, "h2d_bytes": 0, "layer_iters": 0}
+
+    def step(g, count):
+        for l in range(L):
+            if lib.route_block(h, l, lg_p[g][l], T, sp):
+                raise oled.OledError(1, oled.last_error(h))
+            if lib.moe_forward_cached(h, l, x_p[g][l], y_p, sp):
+                raise oled.OledError(1, oled.last_error(h))
+            if lib.apply_misses(h, l, None, rep_ref):
+                raise oled.OledError(1, oled.last_error(h))
+            if lib.score_and_retain(h, l, c_p[g], sp):
+                raise oled.OledError(1, oled.last_error(h))
+            if count:
+                stats["hits"] += rep.n_hits
+                stats["misses"] += rep.n_misses
+                stats["active"] += rep.n_active
+                stats["h2d_bytes"] += rep.h2d_bytes
+                stats["layer_iters"] += 1
+
+    for g in range(args.warmup):
+        step(g, False)
+    torch.cuda.synchronize()
+    ctx.profile_collect()            # drop warm-up timings
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for g in range(args.warmup, n_total):
+        step(g, True)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    ops = ctx.profile_collect()
+
+    def agg(name):
+        sel = [o for o in ops if o[0] == name]
+        ms = sum(o[2] for o in sel)
+        return dict(n=len(sel), ms=ms, bytes=sum(o[3] for o in sel), flops=sum(o[4] for o in sel))
+
+    up, down, h2d = agg("ffn_up"), agg("ffn_down"), agg("h2d")
+    up_gbs = (up["bytes"] / 1e9) / (up["ms"] / 1e3) if up["ms"] > 0 else 0.0
+    ffn_ms = up["ms"] + down["ms"]
+    ffn_tflops = ((up["flops"] + down["flops"]) / 1e12) / (ffn_ms / 1e3) if ffn_ms > 0 else 0.0
+    ffn_gbs = ((up["bytes"] + down["bytes"]) / 1e9) / (ffn_ms / 1e3) if ffn_ms > 0 else 0.0
+    value = args.steps * L * T / elapsed
+    li = max(1, stats["layer_iters"])
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "layer-tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded router logits, activations, confidence; random-init bf16 experts)",
+        "config": {"workload": "LLaDA-MoE-like layer stack, bf16: hidden 2048, 64 experts, top-8, "
+                               "expert intermediate 1024, 16 MoE layers, batch 1 x block 32 tokens, "
+                               "8 denoising iterations per block, expert cache 26/64 (40%) per layer",
+                   "hidden": w.hidden, "n_experts": E, "top_k": w.top_k, "inter": w.inter,
+                   "n_layers": L, "tokens_per_iteration": T, "iterations_per_block": w.n_iters,
+                   "capacity": w.capacity},
+        "roofline": {"kernel": "grouped gate/up SwiGLU GEMM (k_ffn up)", "bound": "hbm",
+                     "achieved": round(up_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(up_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "launches": up["n"], "avg_launch_us": round(up["ms"] / max(1, up["n"]) * 1e3, 2),
+                     "bytes_per_launch": int(up["bytes"] / max(1, up["n"]))},
+        "detail": {
+            "ffn_up_down_GBps": round(ffn_gbs, 1),
+            "ffn_mfma_util": round(ffn_tflops / MFMA_BF16_PEAK_TFLOPS, 5),
+            "ffn_tflops": round(ffn_tflops, 2),
+            "ffn_ms_per_step": round(ffn_ms / args.steps, 4),
+            "h2d_GBps": round((h2d["bytes"] / 1e9) / (h2d["ms"] / 1e3), 2) if h2d["ms"] > 0 else None,
+            "h2d_ms_per_step": round(h2d["ms"] / args.steps, 4),
+            "hits_per_layer_iter": round(stats["hits"] / li, 3),
+            "misses_per_layer_iter": round(stats["misses"] / li, 3),
+            "active_per_layer_iter": round(stats["active"] / li, 3),
+            "cache_util": round(stats["hits"] / li / max(1, w.capacity), 4),
+            "h2d_MiB_per_step": round(stats["h2d_bytes"] / args.steps / 2 ** 20, 2),
+        },
+    }
+    ctx.close()
+    pool.free()
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, args.seed)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

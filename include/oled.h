@@ -7,21 +7,24 @@
  *   route_block        the gate's routed expert ids and gate scores for every
  *                      token of the block (Sec. 4.1), plus the expert
  *                      histogram, offsets and stable token permutation
- *   apply_misses       active set A, hits A & R and misses M = A \ R of the
- *                      layer (Sec. 4.2); every miss is transferred host->device
- *                      into a staging slot on a copy stream (G = M)
- *   moe_forward_cached the SwiGLU experts over the cached (hit) experts, then
- *                      over the transferred misses once their copies land,
- *                      and the gate-weighted combine (Sec. 4.1)
+ *   moe_forward_cached the SwiGLU experts that are cached (hits, A & R) run
+ *                      directly on the GPU (Sec. 4.1); enqueued without
+ *                      waiting for the routing result on the host
+ *   apply_misses       active set A, hits and misses M = A \ R of the layer
+ *                      (Sec. 4.2); every miss is transferred host->device into
+ *                      a staging slot on a copy stream (G = M) and computed on
+ *                      the GPU once its copy lands; then the gate-weighted
+ *                      combine of all k routes of every token
  *   score_and_retain   reuse priorities p_e (the priority equation of
  *                      Sec. 4.3, psi(c) = c; stale residents score zero) and
  *                      the retention rule R' = Top_C(R u G, p) of Sec. 4.2
  *
- * Call order per (layer, iteration): route_block -> apply_misses ->
- * [moe_forward_cached] -> score_and_retain. Exactly one layer is in flight per
+ * Call order per (layer, iteration): route_block -> [moe_forward_cached] ->
+ * apply_misses -> score_and_retain. Exactly one layer is in flight per
  * context; any other order returns OLED_ERR_STATE and changes nothing.
- * moe_forward_cached may be skipped (control path only); the cache state does
- * not depend on expert outputs.
+ * moe_forward_cached may be skipped (control path only: apply_misses then
+ * only transfers); the cache state does not depend on expert outputs. The
+ * layer output y is complete once the work apply_misses enqueued has run.
  *
  * Conventions
  *  - Every function returns an oled_status and never aborts. Host-detected
@@ -59,8 +62,6 @@ typedef enum {
 
 typedef enum { OLED_F32 = 0, OLED_BF16 = 1 } oled_dtype;
 
-/* Context flags. */
-#define OLED_FLAG_PROFILE 1 /* time every kernel and copy with HIP events */
 
 /*
  * Shape and resources of one MoE layer stack.
@@ -88,7 +89,8 @@ typedef struct {
   int32_t max_tokens;
   int32_t dtype;            /* oled_dtype */
   int32_t device;           /* HIP device ordinal */
-  int32_t flags;            /* OLED_FLAG_* */
+  int32_t profile_ops;      /* bit (1 << oled_op_kind) set: time that operation with HIP
+                               events on its stream (oled_profile_collect); 0: off */
   const void* host_pool;
   int64_t host_pool_blocks;
   const int64_t* host_block_of;
@@ -127,7 +129,7 @@ typedef struct {
   int32_t n_active, n_hits, n_misses;
 } oled_layer_state;
 
-/* One timed operation (OLED_FLAG_PROFILE). */
+/* One timed operation (see oled_config.profile_ops). */
 typedef struct {
   int32_t kind;      /* oled_op_kind */
   int32_t layer;
@@ -179,32 +181,38 @@ oled_status route_block(void* ctx, int32_t layer, const float* logits_dev, int32
                         void* stream);
 
 /*
- * apply_misses: misses M = A \ R of the routed layer (Sec. 4.2) and their
- *  transfer (G = M). Waits for route_block's results (the one host sync of a
- *  layer), gives every miss a free staging slot and enqueues one
- *  host-to-device copy of the expert's block per miss on copy_stream (NULL:
- *  the context's own copy stream), overlapping the hit experts' compute.
- *  Fills *out (may be NULL).
- *  Errors: STATE; INVALID_ARG if the logits held a non-finite value (no copy
- *  is issued; the layer returns to idle with its cache unchanged); HIP if a
- *  copy could not be enqueued (staged slots are released, cache unchanged).
- *  Retentions enqueued earlier are committed here; one rejected for an
- *  invalid confidence is named in out->rejected_layer (the call still
- *  returns OLED_OK for its own work).
- */
-oled_status apply_misses(void* ctx, int32_t layer, void* copy_stream, oled_miss_report* out);
-
-/*
- * moe_forward_cached: the layer output (Sec. 4.1; lossless, Sec. 5.1)
- *  y[t] = sum_j gate[t][j] * W2_e (silu(W1_e x[t]) * (W3_e x[t])), e = idx[t][j].
- *  x_dev: [T][H] dtype (read); y_dev: [T][H] dtype (overwritten). Hit experts
- *  run first from their cache slots; the misses run after their copies
- *  complete (the stream waits on the copy events). Accumulation is fp32; the
- *  intermediate silu(W1 x) * (W3 x) is stored in dtype.
- *  Errors: STATE, INVALID_ARG (NULL pointers).
+ * moe_forward_cached: the cached experts of the routed layer (Sec. 4.1).
+ *  x_dev: [T][H] dtype (read); y_dev: [T][H] dtype, written by the combine
+ *  that apply_misses enqueues: y[t] = sum_j gate[t][j] *
+ *  W2_e (silu(W1_e x[t]) * (W3_e x[t])), e = idx[t][j] (lossless, Sec. 5.1).
+ *  Enqueues the grouped GEMMs of the hit experts (A & R, weights read from
+ *  their cache slots) on `stream` right away; their work list and count come
+ *  from route_block's kernels on the device, so no host synchronisation is
+ *  needed. Accumulation is fp32; silu(W1 x) * (W3 x) is stored in dtype.
+ *  Both buffers must stay valid until the layer's work has run.
+ *  Errors: STATE (not right after route_block), INVALID_ARG (NULL pointers,
+ *  a stream other than route_block's).
  */
 oled_status moe_forward_cached(void* ctx, int32_t layer, const void* x_dev, void* y_dev,
                                void* stream);
+
+/*
+ * apply_misses: misses M = A \ R of the routed layer (Sec. 4.2) and their
+ *  compensation by transfer (G = M). Waits for route_block's result (the one
+ *  host synchronisation of a layer; it overlaps the hit experts' GEMMs),
+ *  gives every miss a free staging slot and enqueues its host-to-device copy
+ *  on copy_stream (NULL: the context's own copy stream), gate/up weights of
+ *  all misses first, then their down weights. If moe_forward_cached was
+ *  called, it then enqueues on the compute stream the misses' GEMMs (each
+ *  half after its copies) and the combine into y. Fills *out (may be NULL).
+ *  Errors: STATE; INVALID_ARG if the logits held a non-finite value (no copy
+ *  is issued, y is not written; the layer returns to idle with its cache
+ *  unchanged); HIP if a copy could not be enqueued (staged slots are
+ *  released, cache unchanged). Retentions enqueued earlier are committed
+ *  here; one rejected for an invalid confidence is named in
+ *  out->rejected_layer (the call still returns OLED_OK for its own work).
+ */
+oled_status apply_misses(void* ctx, int32_t layer, void* copy_stream, oled_miss_report* out);
 
 /*
  * score_and_retain: priorities of Sec. 4.3 and the retention rule of Sec. 4.2.
@@ -226,7 +234,7 @@ oled_status score_and_retain(void* ctx, int32_t layer, const float* conf_dev, vo
  * the arrays filled) if the layer's last retention was rejected. */
 oled_status oled_read_layer_state(void* ctx, int32_t layer, oled_layer_state* out);
 
-/* Operation timings recorded since the last collection (OLED_FLAG_PROFILE).
+/* Operation timings recorded since the last collection (oled_config.profile_ops).
  * Synchronises. Writes at most cap entries to out, sets *n_out; entries that
  * did not fit are dropped. */
 oled_status oled_profile_collect(void* ctx, oled_op_time* out, int32_t cap, int32_t* n_out);

@@ -3,16 +3,30 @@
 // gate-weighted combine (OLED-MoE Sec. 4.1: cache-hit experts execute on the
 // GPU; the output does not depend on where an expert's weights came from).
 //
-// Work decomposition: a work item is up to 64 routes (rows of the
-// expert-sorted order) of one expert; grid = (feature tiles of 64, items).
-// Each of the 4 wavefronts owns 16 output features and multiplies its 16
-// weight rows, streamed straight from HBM into registers, with up to four
-// 16-row token tiles staged per 128-wide K chunk in LDS. The weights are the
-// A operand (M = features) and the tokens the B operand (N = tokens) of
-// v_mfma_f32_16x16x32_bf16 (v_mfma_f32_16x16x4_f32 for fp32), so each weight
-// byte is read once per item and reused across the token tiles in registers.
-// Results per expert depend only on that expert's rows, never on the other
+// The GEMMs are weight-streaming: a layer iteration routes few tokens to each
+// expert (tens of rows), so every weight byte should be read from HBM once
+// while enough wavefronts are in flight to cover HBM latency.
+//
+// Tile = one work item (up to 64 expert-sorted routes of one expert) x
+// 16 * 4 / KS output features. The 4 wavefronts of a workgroup form 4 / KS
+// feature groups of 16 and split K in KS contiguous parts (KS = 4, 2 or 1 by
+// the size of K); each streams its 16 (gate/up: 2 x 16) weight rows from HBM
+// straight into registers (A operand, M = features) and the token rows of its
+// K part from L2 (B operand, N = 16 tokens per MFMA tile); the KS partial
+// tiles are summed in LDS in a fixed order (deterministic).
+// MFMA: v_mfma_f32_16x16x32_bf16 (bf16) or v_mfma_f32_16x16x4_f32 (fp32).
+//
+// One tile per workgroup over a grid sized for every possible tile; tiles past
+// the live count exit at once, and the hardware dispatcher balances the rest
+// over the CUs. Workgroup b runs on XCD b % 8; tiles are renumbered so that
+// each XCD takes a contiguous range (consecutive feature tiles of the same
+// expert share its token rows in that XCD's L2). The number of items can come
+// from device memory, so the hit experts can be launched before the host has
+// seen the routing result.
+//
+// Results for an expert depend only on its own rows, never on the other
 // experts of the launch, so hit and miss launches give identical bits.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include "kernels.h"
@@ -42,7 +56,7 @@ struct TrBF16 {
   __device__ static float silu(float a) { return a / (1.f + __expf(-a)); }
 };
 
-// fp32: a 16-byte vector holds 4 consecutive k (16g + 4g' + q); MFMA q of the
+// fp32: a 16-byte vector holds 4 consecutive k (16v + 4g + q); MFMA q of the
 // vector takes element q from every lane group.
 struct TrF32 {
   using T = float;
@@ -58,117 +72,202 @@ struct TrF32 {
 };
 
 constexpr int kThreads = 256;
-constexpr int kKC = 128;  // K elements per chunk
+constexpr int kWaves = 4;
+constexpr int kFeat = 16;                  // output features per tile
+constexpr int kMaxNT = kItemRows / 16;     // token tiles per item
 
-template <class TR, bool UP>
-__global__ __launch_bounds__(kThreads) void k_ffn(
-    const char* __restrict__ pool, int64_t slot_bytes, SlotTable st,
-    const WorkItem* __restrict__ items, int item_base, const typename TR::T* __restrict__ src,
-    const int32_t* __restrict__ perm, int k, int H, int I, typename TR::T* __restrict__ hout,
-    float* __restrict__ oout) {
-  using T = typename TR::T;
-  constexpr int EPV = TR::EPV;
+__device__ __forceinline__ u32x4_t ldg16(const void* p) {
+  return *reinterpret_cast<const u32x4_t*>(p);
+}
+
+// Bijection on [0, total): tile t (XCD t % 8) -> contiguous range per XCD.
+__device__ __forceinline__ int xcd_order(int t, int total) {
+  const int x = t & 7, local = t >> 3;
+  const int q = total >> 3, r = total & 7;
+  return x * q + (x < r ? x : r) + local;
+}
+
+// Streams one K range of a tile: NT token tiles, groups of U MFMA steps with
+// the next group's loads in flight while the current group multiplies (U is
+// smaller for more token tiles to keep registers, and so occupancy, in check).
+template <class TR, bool UP, int NT>
+__device__ __forceinline__ void stream_k(const typename TR::T* a1, const typename TR::T* a3,
+                                         const typename TR::T* const* b, int steps,
+                                         floatx4_t* acc1, floatx4_t* acc3) {
   constexpr int SPAN = TR::SPAN;
-  constexpr int NV = kKC / SPAN;          // vectors per lane per chunk
-  constexpr int VPR = kKC / EPV;          // vectors per LDS row
-  constexpr int NQ = 64 * VPR / kThreads; // B vectors loaded per thread per chunk
-  constexpr int RS = kKC + EPV;           // LDS row stride (elements), +16 bytes
-  __shared__ __attribute__((aligned(16))) T s_b[64 * RS];
+  constexpr int U = NT == 1 ? 4 : 2;
+  const int groups = steps / U;
+  u32x4_t ra1[2][U], ra3[2][U], rb[2][U][NT];
+  auto load = [&](int buf, int g0) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int kk = (g0 * U + u) * SPAN;
+      ra1[buf][u] = ldg16(a1 + kk);
+      if (UP) ra3[buf][u] = ldg16(a3 + kk);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) rb[buf][u][nt] = ldg16(b[nt] + kk);
+    }
+  };
+  auto mult = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        TR::mma(acc1[nt], ra1[buf][u], rb[buf][u][nt]);
+        if (UP) TR::mma(acc3[nt], ra3[buf][u], rb[buf][u][nt]);
+      }
+    }
+  };
+  if (groups > 0) load(0, 0);
+  int gi = 0;
+  for (; gi + 2 <= groups; gi += 2) {
+    load(1, gi + 1);
+    mult(0);
+    if (gi + 2 < groups) load(0, gi + 2);
+    mult(1);
+  }
+  if (gi < groups) mult(0);
+  // remaining steps (K range not a multiple of U steps)
+  for (int st = groups * U; st < steps; ++st) {
+    const int kk = st * SPAN;
+    const u32x4_t x1 = ldg16(a1 + kk);
+    u32x4_t x3;
+    if (UP) x3 = ldg16(a3 + kk);
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const u32x4_t bv = ldg16(b[nt] + kk);
+      TR::mma(acc1[nt], x1, bv);
+      if (UP) TR::mma(acc3[nt], x3, bv);
+    }
+  }
+}
 
-  const WorkItem it = items[item_base + blockIdx.y];
-  const int rows = it.rows;
-  const T* W = reinterpret_cast<const T*>(pool + static_cast<int64_t>(st.slot[it.expert]) * slot_bytes);
-  const int Kdim = UP ? H : I;
+// Epilogue of one 16x16 output tile held in D layout: lane (lr, g), register
+// r -> feature f0 + 4g + r, token row 16 nt + lr of the item.
+template <class TR, bool UP>
+__device__ __forceinline__ void store_tile(const WorkItem& it, int nt, int f0, const floatx4_t& s1,
+                                           const floatx4_t& s3, int H, int I,
+                                           typename TR::T* __restrict__ hout,
+                                           float* __restrict__ oout) {
+  using T = typename TR::T;
   const int lane = threadIdx.x & 63;
   const int lr = lane & 15, g = lane >> 4;
-  const int fw = blockIdx.x * kFeatTile + (threadIdx.x >> 6) * 16;
+  const int row = 16 * nt + lr;
+  if (row >= it.rows) return;
+  const size_t pos = static_cast<size_t>(it.row_begin + row);
+  if (UP) {
+    float hv[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) hv[r] = TR::silu(s1[r]) * s3[r];
+    if constexpr (sizeof(T) == 2) {
+      uint2 packed;
+      packed.x = f32_to_bf16_rne(hv[0]) | (static_cast<uint32_t>(f32_to_bf16_rne(hv[1])) << 16);
+      packed.y = f32_to_bf16_rne(hv[2]) | (static_cast<uint32_t>(f32_to_bf16_rne(hv[3])) << 16);
+      *reinterpret_cast<uint2*>(hout + pos * I + f0 + 4 * g) = packed;
+    } else {
+      *reinterpret_cast<float4*>(hout + pos * I + f0 + 4 * g) = make_float4(hv[0], hv[1], hv[2], hv[3]);
+    }
+  } else {
+    *reinterpret_cast<float4*>(oout + pos * H + f0 + 4 * g) = make_float4(s1[0], s1[1], s1[2], s1[3]);
+  }
+}
+
+// One tile of 16 * (4 / KS) output features. Wavefront w takes feature group
+// w / KS and K part w % KS; with KS > 1 the KS partial tiles of a feature
+// group are summed in LDS in a fixed order and the parts share the epilogue.
+template <class TR, bool UP, int KS, int NT>
+__device__ __forceinline__ void run_tile(const WorkItem& it, int tile_f0, const typename TR::T* W,
+                                         const typename TR::T* __restrict__ src,
+                                         const int32_t* __restrict__ perm, int k, int H, int I,
+                                         typename TR::T* __restrict__ hout,
+                                         float* __restrict__ oout,
+                                         floatx4_t (*s_red)[(UP ? 2 : 1) * kMaxNT][64]) {
+  using T = typename TR::T;
+  constexpr int EPV = TR::EPV;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lr = lane & 15, g = lane >> 4;
+  const int fg = wave / KS, kp = wave % KS;
+  const int f0 = tile_f0 + kFeat * fg;
+  const int Kdim = UP ? H : I;
+  const int kw = Kdim / KS;
+  const int kbeg = kp * kw;
+  const int rows = it.rows;
 
   const T* a1;
   const T* a3;
   if (UP) {
-    a1 = W + static_cast<size_t>(fw + lr) * H + EPV * g;
-    a3 = W + static_cast<size_t>(I + fw + lr) * H + EPV * g;
+    a1 = W + static_cast<size_t>(f0 + lr) * H + kbeg + EPV * g;
+    a3 = W + static_cast<size_t>(I + f0 + lr) * H + kbeg + EPV * g;
   } else {
-    a1 = W + static_cast<size_t>(2) * I * H + static_cast<size_t>(fw + lr) * I + EPV * g;
+    a1 = W + static_cast<size_t>(2) * I * H + static_cast<size_t>(f0 + lr) * I + kbeg + EPV * g;
     a3 = a1;
   }
-
-  const int bcol = threadIdx.x % VPR;
-  const T* bsrc[NQ];
-  int brow[NQ];
+  // token rows past the item's end read its last row; their results are dropped
+  const T* b[NT];
 #pragma unroll
-  for (int q = 0; q < NQ; ++q) {
-    brow[q] = threadIdx.x / VPR + q * (kThreads / VPR);
-    bsrc[q] = nullptr;
-    if (brow[q] < rows) {
-      const int pos = it.row_begin + brow[q];
-      bsrc[q] = (UP ? src + static_cast<size_t>(perm[pos] / k) * H : src + static_cast<size_t>(pos) * I) +
-                bcol * EPV;
-    }
+  for (int nt = 0; nt < NT; ++nt) {
+    const int r = min(16 * nt + lr, rows - 1);
+    const int pos = it.row_begin + r;
+    b[nt] = (UP ? src + static_cast<size_t>(perm[pos] / k) * H : src + static_cast<size_t>(pos) * I) +
+            kbeg + EPV * g;
   }
-  const int NT = (rows + 15) >> 4;
-
-  floatx4_t acc1[4], acc3[4];
+  floatx4_t acc1[NT], acc3[NT];
 #pragma unroll
-  for (int nt = 0; nt < 4; ++nt) {
+  for (int nt = 0; nt < NT; ++nt) {
     acc1[nt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
     acc3[nt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
   }
+  stream_k<TR, UP, NT>(a1, a3, b, kw / TR::SPAN, acc1, acc3);
 
-  for (int kc = 0; kc < Kdim; kc += kKC) {
-    u32x4_t av1[NV], av3[NV];
+  if constexpr (KS == 1) {
 #pragma unroll
-    for (int v = 0; v < NV; ++v) {
-      av1[v] = *reinterpret_cast<const u32x4_t*>(a1 + kc + SPAN * v);
-      if (UP) av3[v] = *reinterpret_cast<const u32x4_t*>(a3 + kc + SPAN * v);
+    for (int nt = 0; nt < NT; ++nt) store_tile<TR, UP>(it, nt, f0, acc1[nt], acc3[nt], H, I, hout, oout);
+  } else {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      s_red[wave][nt][lane] = acc1[nt];
+      if (UP) s_red[wave][kMaxNT + nt][lane] = acc3[nt];
     }
-    u32x4_t bv[NQ];
-#pragma unroll
-    for (int q = 0; q < NQ; ++q)
-      bv[q] = bsrc[q] ? *reinterpret_cast<const u32x4_t*>(bsrc[q] + kc) : u32x4_t{0u, 0u, 0u, 0u};
     __syncthreads();
+    for (int nt = kp; nt < NT; nt += KS) {
+      floatx4_t s1 = s_red[fg * KS][nt][lane];
+      floatx4_t s3 = UP ? s_red[fg * KS][kMaxNT + nt][lane] : floatx4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int q = 0; q < NQ; ++q)
-      *reinterpret_cast<u32x4_t*>(&s_b[brow[q] * RS + bcol * EPV]) = bv[q];
-    __syncthreads();
-#pragma unroll
-    for (int v = 0; v < NV; ++v) {
-#pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
-        if (nt < NT) {
-          const u32x4_t b =
-              *reinterpret_cast<const u32x4_t*>(&s_b[(16 * nt + lr) * RS + SPAN * v + EPV * g]);
-          TR::mma(acc1[nt], av1[v], b);
-          if (UP) TR::mma(acc3[nt], av3[v], b);
-        }
+      for (int j = 1; j < KS; ++j) {
+        s1 += s_red[fg * KS + j][nt][lane];
+        if (UP) s3 += s_red[fg * KS + j][kMaxNT + nt][lane];
       }
+      store_tile<TR, UP>(it, nt, f0, s1, s3, H, I, hout, oout);
     }
+    __syncthreads();  // s_red is reused by the next tile
   }
+}
 
-  // D layout: lane (lr, g), register r -> feature fw + 4g + r, token row 16 nt + lr.
-#pragma unroll
-  for (int nt = 0; nt < 4; ++nt) {
-    const int row = 16 * nt + lr;
-    if (nt < NT && row < rows) {
-      const size_t pos = static_cast<size_t>(it.row_begin + row);
-      if (UP) {
-        float hv[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) hv[r] = TR::silu(acc1[nt][r]) * acc3[nt][r];
-        if constexpr (sizeof(T) == 2) {
-          uint2 packed;
-          packed.x = f32_to_bf16_rne(hv[0]) | (static_cast<uint32_t>(f32_to_bf16_rne(hv[1])) << 16);
-          packed.y = f32_to_bf16_rne(hv[2]) | (static_cast<uint32_t>(f32_to_bf16_rne(hv[3])) << 16);
-          *reinterpret_cast<uint2*>(hout + pos * I + fw + 4 * g) = packed;
-        } else {
-          *reinterpret_cast<float4*>(hout + pos * I + fw + 4 * g) =
-              make_float4(hv[0], hv[1], hv[2], hv[3]);
-        }
-      } else {
-        *reinterpret_cast<float4*>(oout + pos * H + fw + 4 * g) =
-            make_float4(acc1[nt][0], acc1[nt][1], acc1[nt][2], acc1[nt][3]);
-      }
-    }
+template <class TR, bool UP, int KS>
+__global__ __launch_bounds__(kThreads) void k_ffn(
+    const char* __restrict__ pool, int64_t slot_bytes, SlotTable st,
+    const WorkItem* __restrict__ items, const int32_t* __restrict__ n_items_dev, int item_base,
+    int n_items_host, const typename TR::T* __restrict__ src, const int32_t* __restrict__ perm,
+    int k, int H, int I, typename TR::T* __restrict__ hout, float* __restrict__ oout) {
+  using T = typename TR::T;
+  constexpr int FEAT = kFeat * (kWaves / KS);  // output features per tile
+  __shared__ floatx4_t s_red[KS > 1 ? kWaves : 1][(UP ? 2 : 1) * kMaxNT][64];
+
+  const int n_items = n_items_host >= 0 ? n_items_host : *n_items_dev;
+  const int nf = (UP ? I : H) / FEAT;
+  const int total = n_items * nf;
+  const int t = blockIdx.x;  // one tile per workgroup; the grid covers every possible tile
+  if (t >= total) return;
+  const int v = xcd_order(t, total);
+  const int ii = v / nf;
+  const int f0 = (v - ii * nf) * FEAT;
+  const WorkItem it = items[item_base + ii];
+  const T* W = reinterpret_cast<const T*>(pool + static_cast<int64_t>(st.slot[it.expert]) * slot_bytes);
+  switch ((it.rows + 15) >> 4) {
+    case 1: run_tile<TR, UP, KS, 1>(it, f0, W, src, perm, k, H, I, hout, oout, s_red); break;
+    case 2: run_tile<TR, UP, KS, 2>(it, f0, W, src, perm, k, H, I, hout, oout, s_red); break;
+    case 3: run_tile<TR, UP, KS, 3>(it, f0, W, src, perm, k, H, I, hout, oout, s_red); break;
+    default: run_tile<TR, UP, KS, 4>(it, f0, W, src, perm, k, H, I, hout, oout, s_red); break;
   }
 }
 
@@ -202,49 +301,57 @@ __global__ __launch_bounds__(256) void k_combine(const float* __restrict__ O,
   }
 }
 
-}  // namespace
+// K split of the wavefronts of a tile: a function of K alone, so every launch
+// over an expert reduces in the same order. Each wavefront keeps a K range of
+// at least 512 where K allows.
+inline int k_split(int K) { return K >= 2048 ? 4 : (K >= 1024 ? 2 : 1); }
 
-hipError_t launch_ffn_up(bool bf16, const void* pool, int64_t slot_bytes, const SlotTable& slots,
-                         const WorkItem* items, int item_base, int n_items, const void* x,
-                         const int32_t* perm, int k, int H, int I, void* h, hipStream_t s) {
-  if (n_items <= 0) return hipSuccess;
-  const dim3 grid(I / kFeatTile, n_items);
-  const char* p = static_cast<const char*>(pool);
-  if (bf16)
-    hipLaunchKernelGGL((k_ffn<TrBF16, true>), grid, dim3(kThreads), 0, s, p, slot_bytes, slots,
-                       items, item_base, static_cast<const uint16_t*>(x), perm, k, H, I,
-                       static_cast<uint16_t*>(h), nullptr);
-  else
-    hipLaunchKernelGGL((k_ffn<TrF32, true>), grid, dim3(kThreads), 0, s, p, slot_bytes, slots,
-                       items, item_base, static_cast<const float*>(x), perm, k, H, I,
-                       static_cast<float*>(h), nullptr);
+template <class TR, bool UP, int KS>
+hipError_t launch_ffn_ks(const FfnLaunch& a, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
+  auto kern = k_ffn<TR, UP, KS>;
+  const int nf = (UP ? a.I : a.H) / (kFeat * (kWaves / KS));
+  const int grid = a.max_items * nf;
+  if (grid <= 0) return hipSuccess;
+  using T = typename TR::T;
+  hipExtLaunchKernelGGL(kern, dim3(grid), dim3(kThreads), 0, s, ev0, ev1, 0,
+                        static_cast<const char*>(a.pool), a.slot_bytes, *a.slots, a.items,
+                        a.n_items_dev, a.item_base, a.n_items_host, static_cast<const T*>(a.src),
+                        a.perm, a.k, a.H, a.I, static_cast<T*>(a.hout), a.oout);
   return hipGetLastError();
 }
 
-hipError_t launch_ffn_down(bool bf16, const void* pool, int64_t slot_bytes, const SlotTable& slots,
-                           const WorkItem* items, int item_base, int n_items, const void* h,
-                           int H, int I, float* O, hipStream_t s) {
-  if (n_items <= 0) return hipSuccess;
-  const dim3 grid(H / kFeatTile, n_items);
-  const char* p = static_cast<const char*>(pool);
-  if (bf16)
-    hipLaunchKernelGGL((k_ffn<TrBF16, false>), grid, dim3(kThreads), 0, s, p, slot_bytes, slots,
-                       items, item_base, static_cast<const uint16_t*>(h), nullptr, 1, H, I,
-                       nullptr, O);
-  else
-    hipLaunchKernelGGL((k_ffn<TrF32, false>), grid, dim3(kThreads), 0, s, p, slot_bytes, slots,
-                       items, item_base, static_cast<const float*>(h), nullptr, 1, H, I, nullptr,
-                       O);
-  return hipGetLastError();
+template <class TR, bool UP>
+hipError_t launch_ffn_t(const FfnLaunch& a, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
+  switch (k_split(UP ? a.H : a.I)) {
+    case 4: return launch_ffn_ks<TR, UP, 4>(a, ev0, ev1, s);
+    case 2: return launch_ffn_ks<TR, UP, 2>(a, ev0, ev1, s);
+    default: return launch_ffn_ks<TR, UP, 1>(a, ev0, ev1, s);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_ffn_up(bool bf16, const FfnLaunch& a, hipEvent_t ev0, hipEvent_t ev1,
+                         hipStream_t s) {
+  return bf16 ? launch_ffn_t<TrBF16, true>(a, ev0, ev1, s) : launch_ffn_t<TrF32, true>(a, ev0, ev1, s);
+}
+
+hipError_t launch_ffn_down(bool bf16, const FfnLaunch& a, hipEvent_t ev0, hipEvent_t ev1,
+                           hipStream_t s) {
+  return bf16 ? launch_ffn_t<TrBF16, false>(a, ev0, ev1, s)
+              : launch_ffn_t<TrF32, false>(a, ev0, ev1, s);
 }
 
 hipError_t launch_combine(bool bf16, const float* O, const float* gates, const int32_t* inv_perm,
-                          int T, int k, int H, void* y, hipStream_t s) {
+                          int T, int k, int H, void* y, hipEvent_t ev0, hipEvent_t ev1,
+                          hipStream_t s) {
   const dim3 grid((H + 1023) / 1024, T);
   if (bf16)
-    hipLaunchKernelGGL(k_combine<true>, grid, dim3(256), 0, s, O, gates, inv_perm, k, H, y);
+    hipExtLaunchKernelGGL(k_combine<true>, grid, dim3(256), 0, s, ev0, ev1, 0, O, gates, inv_perm,
+                          k, H, y);
   else
-    hipLaunchKernelGGL(k_combine<false>, grid, dim3(256), 0, s, O, gates, inv_perm, k, H, y);
+    hipExtLaunchKernelGGL(k_combine<false>, grid, dim3(256), 0, s, ev0, ev1, 0, O, gates, inv_perm,
+                          k, H, y);
   return hipGetLastError();
 }
 

@@ -1,10 +1,22 @@
 // Host runtime of the C ABI declared in include/oled.h: the context, the call
 // state machine, the per-layer cache bookkeeping, the host-to-device miss
 // copies on a side stream and the kernel launches.
+//
+// Per layer: route_block enqueues the gate kernels; moe_forward_cached
+// enqueues the hit experts at once (their work list and count stay on the
+// device); apply_misses is the one host synchronisation of the layer - it
+// polls the routing summary the permute kernel publishes in coherent pinned
+// memory, commits earlier retentions, stages and copies the misses and
+// enqueues their GEMMs behind the copies, then the combine; score_and_retain
+// enqueues the priority/retention kernel, whose result is committed at the
+// next synchronising call.
 #include "oled.h"
 
 #include <hip/hip_runtime.h>
+#include <immintrin.h>
 
+#include <algorithm>
+#include <atomic>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -17,6 +29,7 @@
 namespace {
 
 using oled::ExpertMask;
+using oled::FfnLaunch;
 using oled::RetainOut;
 using oled::RouteSummary;
 using oled::SlotTable;
@@ -24,7 +37,7 @@ using oled::WorkItem;
 
 thread_local std::string g_create_error;
 
-enum class Stage { kIdle, kRouted, kApplied, kForwarded };
+enum class Stage { kIdle, kRouted, kHitsQueued, kApplied };
 
 struct OpRec {
   int kind, layer;
@@ -34,8 +47,10 @@ struct OpRec {
 
 struct Ctx {
   // shape
-  int H = 0, I = 0, E = 0, K = 0, L = 0, C = 0, Tmax = 0, dtype = 0, esz = 0, device = 0, flags = 0;
-  int64_t eb = 0;   // bytes of one expert block
+  int H = 0, I = 0, E = 0, K = 0, L = 0, C = 0, Tmax = 0, dtype = 0, esz = 0, device = 0;
+  uint32_t profile_ops = 0;
+  int64_t eb = 0;    // bytes of one expert block
+  int64_t e13 = 0;   // bytes of its w13 part
   int n_slots = 0;
   int max_items = 0;
   const char* host_pool = nullptr;
@@ -50,34 +65,36 @@ struct Ctx {
   int32_t* d_perm = nullptr;
   int32_t* d_inv = nullptr;
   int32_t* d_flag = nullptr;
+  int32_t* d_item_counts = nullptr;
+  int32_t* d_sync = nullptr;       // completion counter + bad-logit flag of the routing launch
   WorkItem* d_items = nullptr;
   void* d_h = nullptr;
   float* d_O = nullptr;
   uint64_t* d_score = nullptr;  // [L][E]
-  // pinned host memory written by kernels
+  // coherent pinned host memory written by kernels
   RouteSummary* h_sum = nullptr;
-  RetainOut* h_ret = nullptr;  // [L]
+  RetainOut* h_ret = nullptr;   // [L]
   // streams and events
   hipStream_t own_copy = nullptr;
-  hipEvent_t ev_route = nullptr, ev_copy = nullptr, ev_order = nullptr;
-  std::vector<hipEvent_t> ev_retain;
+  hipEvent_t ev_up = nullptr, ev_down = nullptr, ev_order = nullptr;
   // cache state
   oled::CacheState cs;
   std::vector<uint8_t> pending;     // [L] retention result not yet committed
   std::vector<int> ret_seq;         // [L] sequence number of that result
+  std::vector<hipStream_t> ret_stream;
   std::vector<uint8_t> rejected;    // [L] last retention rejected (bad confidence)
   std::vector<uint8_t> res_before;  // [L][E] R before the layer's last execution
   std::vector<int> last_counts;     // [L][3] n_active, n_hits, n_misses of the last apply
   // the layer in flight
   Stage stage = Stage::kIdle;
-  int cur_layer = -1, cur_T = 0;
+  int cur_layer = -1, cur_T = 0, cur_res = 0;
   hipStream_t cur_stream = nullptr;
   bool have_stream = false;
+  const void* fwd_x = nullptr;
+  void* fwd_y = nullptr;
   int last_routed_layer = -1, last_routed_T = 0;
   std::vector<int32_t> counts;      // [E] route counts of the layer in flight
   std::vector<uint8_t> hit, miss;
-  int n_active = 0, n_hits = 0, n_misses = 0, n_hit_items = 0, n_miss_items = 0;
-  int64_t hit_rows = 0, miss_rows = 0;
   bool copies_outstanding = false;
   int seq = 0, route_seq = 0;
   int rejected_layer = -1;          // reported by the next apply_misses
@@ -101,9 +118,9 @@ oled_status hip_fail(Ctx* c, hipError_t e, const char* what) {
   return fail(c, OLED_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
-#define HIP_TRY(c, expr)                                 \
-  do {                                                   \
-    hipError_t e_ = (expr);                              \
+#define HIP_TRY(c, expr)                                   \
+  do {                                                     \
+    hipError_t e_ = (expr);                                \
     if (e_ != hipSuccess) return hip_fail((c), e_, #expr); \
   } while (0)
 
@@ -113,31 +130,33 @@ hipEvent_t take_event(Ctx* c) {
     c->ev_free.pop_back();
     return e;
   }
+  // timing only: no system-scope fence, so the event adds no cache flush
   hipEvent_t e = nullptr;
-  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
   return e;
 }
 
-// Event pair around one operation when profiling is on.
-struct OpTimer {
-  Ctx* c;
-  hipStream_t s;
-  hipEvent_t a = nullptr;
-  OpTimer(Ctx* c_, hipStream_t s_) : c(c_), s(s_) {
-    if (c->flags & OLED_FLAG_PROFILE) {
-      a = take_event(c);
-      if (a) hipEventRecord(a, s);
-    }
-  }
-  void done(int kind, int layer, int64_t bytes, int64_t flops) {
-    if (!a) return;
-    hipEvent_t b = take_event(c);
-    if (!b) return;
-    hipEventRecord(b, s);
-    c->ops.push_back(OpRec{kind, layer, bytes, flops, a, b});
-    a = nullptr;
-  }
+// Timing events of one operation when its kind is profiled (else null).
+struct OpEvents {
+  hipEvent_t a = nullptr, b = nullptr;
 };
+
+OpEvents op_begin(Ctx* c, int kind) {
+  OpEvents ev;
+  if (!(c->profile_ops & (1u << kind))) return ev;
+  ev.a = take_event(c);
+  ev.b = take_event(c);
+  if (!ev.a || !ev.b) {
+    if (ev.a) c->ev_free.push_back(ev.a);
+    if (ev.b) c->ev_free.push_back(ev.b);
+    return OpEvents{};
+  }
+  return ev;
+}
+
+void op_end(Ctx* c, const OpEvents& ev, int kind, int layer, int64_t bytes, int64_t flops) {
+  if (ev.a) c->ops.push_back(OpRec{kind, layer, bytes, flops, ev.a, ev.b});
+}
 
 ExpertMask mask_of(const uint8_t* m, int E) {
   ExpertMask x;
@@ -147,16 +166,40 @@ ExpertMask mask_of(const uint8_t* m, int E) {
   return x;
 }
 
-// Commits the retention result of layer l (waits for its event).
+// Waits until a kernel has published `want` into *flag (coherent pinned
+// memory). Checks the stream now and then so a failed launch cannot hang.
+oled_status wait_published(Ctx* c, const int32_t* flag, int want, hipStream_t s, const char* what) {
+  const volatile int32_t* p = flag;
+  for (uint64_t spin = 1;; ++spin) {
+    if (*p == want) {
+      std::atomic_thread_fence(std::memory_order_acquire);
+      return OLED_OK;
+    }
+    if ((spin & 255) == 0) {
+      const hipError_t e = hipStreamQuery(s);
+      if (e == hipSuccess) {  // the stream is idle: the value must be visible now
+        if (*p == want) {
+          std::atomic_thread_fence(std::memory_order_acquire);
+          return OLED_OK;
+        }
+        return fail(c, OLED_ERR_HIP, "%s: result was not published", what);
+      }
+      if (e != hipErrorNotReady) return hip_fail(c, e, what);
+    }
+    _mm_pause();
+  }
+}
+
+// Commits the retention result of layer l.
 oled_status consume_layer(Ctx* c, int l) {
   if (!c->pending[l]) return OLED_OK;
-  HIP_TRY(c, hipEventSynchronize(c->ev_retain[l]));
-  const RetainOut& o = c->h_ret[l];
+  oled_status st = wait_published(c, &c->h_ret[l].seq, c->ret_seq[l], c->ret_stream[l], "retention");
   c->pending[l] = 0;
-  if (o.seq != c->ret_seq[l]) {
+  if (st != OLED_OK) {
     c->cs.drop_staged(l);
-    return fail(c, OLED_ERR_HIP, "stale retention result for layer %d", l);
+    return st;
   }
+  const RetainOut& o = c->h_ret[l];
   if (o.bad_conf) {
     c->cs.drop_staged(l);
     c->rejected[l] = 1;
@@ -164,7 +207,9 @@ oled_status consume_layer(Ctx* c, int l) {
     return fail(c, OLED_ERR_INVALID_ARG, "confidence outside [0,1] at layer %d: retention skipped", l);
   }
   c->rejected[l] = 0;
-  if (!c->cs.commit(l, o.retained)) {
+  uint8_t keep[oled::kMaxExperts];
+  for (int e = 0; e < c->E; ++e) keep[e] = (o.retained[e >> 5] >> (e & 31)) & 1u;
+  if (!c->cs.commit(l, keep)) {
     c->cs.drop_staged(l);
     return fail(c, OLED_ERR_HIP, "inconsistent retention result for layer %d", l);
   }
@@ -190,10 +235,8 @@ void free_ctx(Ctx* c) {
     hipEventDestroy(op.b);
   }
   for (auto e : c->ev_free) hipEventDestroy(e);
-  for (auto e : c->ev_retain)
-    if (e) hipEventDestroy(e);
-  if (c->ev_route) hipEventDestroy(c->ev_route);
-  if (c->ev_copy) hipEventDestroy(c->ev_copy);
+  if (c->ev_up) hipEventDestroy(c->ev_up);
+  if (c->ev_down) hipEventDestroy(c->ev_down);
   if (c->ev_order) hipEventDestroy(c->ev_order);
   if (c->own_copy) hipStreamDestroy(c->own_copy);
   hipFree(c->d_pool);
@@ -204,6 +247,8 @@ void free_ctx(Ctx* c) {
   hipFree(c->d_perm);
   hipFree(c->d_inv);
   hipFree(c->d_flag);
+  hipFree(c->d_item_counts);
+  hipFree(c->d_sync);
   hipFree(c->d_items);
   hipFree(c->d_h);
   hipFree(c->d_O);
@@ -218,16 +263,49 @@ hipError_t dev_alloc(T** p, size_t n) {
   return hipMalloc(reinterpret_cast<void**>(p), n * sizeof(T) > 0 ? n * sizeof(T) : 16);
 }
 
-oled_status check_call(Ctx* c, int layer, Stage want) {
+oled_status check_layer(Ctx* c, int layer) {
   if (layer < 0 || layer >= c->L)
     return fail(c, OLED_ERR_INVALID_ARG, "layer %d outside [0,%d)", layer, c->L);
-  if (c->stage != want)
-    return fail(c, OLED_ERR_STATE, "call out of order (layer %d, stage %d)", layer,
-                static_cast<int>(c->stage));
-  if (want != Stage::kIdle && layer != c->cur_layer)
-    return fail(c, OLED_ERR_STATE, "layer %d is not the layer in flight (%d)", layer, c->cur_layer);
   return OLED_OK;
 }
+
+oled_status check_in_flight(Ctx* c, int layer, hipStream_t s, const char* call) {
+  if (layer != c->cur_layer)
+    return fail(c, OLED_ERR_STATE, "%s: layer %d is not the layer in flight (%d)", call, layer,
+                c->cur_layer);
+  if (s != c->cur_stream)
+    return fail(c, OLED_ERR_INVALID_ARG, "%s: stream differs from route_block's", call);
+  return OLED_OK;
+}
+
+FfnLaunch ffn_args(Ctx* c, const SlotTable* tab, int base, int n_host, int max_items) {
+  FfnLaunch a;
+  a.pool = c->d_pool;
+  a.slot_bytes = c->eb;
+  a.slots = tab;
+  a.items = c->d_items;
+  a.n_items_dev = c->d_item_counts;
+  a.item_base = base;
+  a.n_items_host = n_host;
+  a.max_items = max_items;
+  a.src = nullptr;
+  a.perm = c->d_perm;
+  a.k = c->K;
+  a.H = c->H;
+  a.I = c->I;
+  a.hout = c->d_h;
+  a.oout = c->d_O;
+  return a;
+}
+
+int64_t up_bytes(const Ctx* c, int64_t n_exp, int64_t rows) {
+  return n_exp * c->e13 + rows * c->H * c->esz + rows * c->I * c->esz;
+}
+int64_t down_bytes(const Ctx* c, int64_t n_exp, int64_t rows) {
+  return n_exp * (c->eb - c->e13) + rows * c->I * c->esz + rows * c->H * 4;
+}
+int64_t up_flops(const Ctx* c, int64_t rows) { return rows * 4 * static_cast<int64_t>(c->H) * c->I; }
+int64_t down_flops(const Ctx* c, int64_t rows) { return rows * 2 * static_cast<int64_t>(c->H) * c->I; }
 
 }  // namespace
 
@@ -282,8 +360,9 @@ oled_status oled_create(const oled_config* cfg, void** ctx_out) {
   c->dtype = cfg->dtype;
   c->esz = cfg->dtype == OLED_F32 ? 4 : 2;
   c->device = cfg->device;
-  c->flags = cfg->flags;
+  c->profile_ops = static_cast<uint32_t>(cfg->profile_ops);
   c->eb = static_cast<int64_t>(3) * c->H * c->I * c->esz;
+  c->e13 = static_cast<int64_t>(2) * c->H * c->I * c->esz;
   const int cap = c->C < c->E ? c->C : c->E;
   const int64_t routes = static_cast<int64_t>(c->Tmax) * c->K;
   const int staging = routes < c->E ? static_cast<int>(routes) : c->E;
@@ -305,37 +384,34 @@ oled_status oled_create(const oled_config* cfg, void** ctx_out) {
   if (dev_alloc(&c->d_topk, routes) || dev_alloc(&c->d_gates, routes) ||
       dev_alloc(&c->d_counts, c->E) || dev_alloc(&c->d_offsets, c->E + 1) ||
       dev_alloc(&c->d_perm, routes) || dev_alloc(&c->d_inv, routes) || dev_alloc(&c->d_flag, 1) ||
+      dev_alloc(&c->d_item_counts, 2) || dev_alloc(&c->d_sync, 2) ||
       dev_alloc(&c->d_items, c->max_items) ||
       dev_alloc(reinterpret_cast<char**>(&c->d_h), routes * c->I * c->esz) ||
       dev_alloc(&c->d_O, routes * c->H) ||
       dev_alloc(&c->d_score, static_cast<size_t>(c->L) * c->E))
     return oom("routing scratch");
   if (hipMemset(c->d_flag, 0, sizeof(int32_t)) != hipSuccess ||
+      hipMemset(c->d_item_counts, 0, 2 * sizeof(int32_t)) != hipSuccess ||
+      hipMemset(c->d_sync, 0, 2 * sizeof(int32_t)) != hipSuccess ||
       hipMemset(c->d_score, 0, sizeof(uint64_t) * c->L * c->E) != hipSuccess)
     return oom("scratch init");
-  if (hipHostMalloc(reinterpret_cast<void**>(&c->h_sum), sizeof(RouteSummary), hipHostMallocDefault) ||
-      hipHostMalloc(reinterpret_cast<void**>(&c->h_ret), sizeof(RetainOut) * c->L, hipHostMallocDefault))
+  if (hipHostMalloc(reinterpret_cast<void**>(&c->h_sum), sizeof(RouteSummary), hipHostMallocCoherent) ||
+      hipHostMalloc(reinterpret_cast<void**>(&c->h_ret), sizeof(RetainOut) * c->L, hipHostMallocCoherent))
     return oom("pinned summaries");
   std::memset(c->h_sum, 0, sizeof(RouteSummary));
   std::memset(c->h_ret, 0, sizeof(RetainOut) * c->L);
   if (hipStreamCreateWithFlags(&c->own_copy, hipStreamNonBlocking) != hipSuccess ||
-      hipEventCreateWithFlags(&c->ev_route, hipEventDisableTiming) != hipSuccess ||
-      hipEventCreateWithFlags(&c->ev_copy, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&c->ev_up, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&c->ev_down, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&c->ev_order, hipEventDisableTiming) != hipSuccess) {
     g_create_error = "stream/event creation failed";
     free_ctx(c);
     return OLED_ERR_HIP;
   }
-  c->ev_retain.assign(c->L, nullptr);
-  for (int l = 0; l < c->L; ++l)
-    if (hipEventCreateWithFlags(&c->ev_retain[l], hipEventDisableTiming) != hipSuccess) {
-      g_create_error = "event creation failed";
-      free_ctx(c);
-      return OLED_ERR_HIP;
-    }
   c->cs = oled::CacheState(c->L, c->E, c->C, c->n_slots);
   c->pending.assign(c->L, 0);
   c->ret_seq.assign(c->L, 0);
+  c->ret_stream.assign(c->L, nullptr);
   c->rejected.assign(c->L, 0);
   c->res_before.assign(static_cast<size_t>(c->L) * c->E, 0);
   c->last_counts.assign(static_cast<size_t>(c->L) * 3, 0);
@@ -365,7 +441,7 @@ oled_status oled_reset_cache(void* ctx) {
   if (c->stage != Stage::kIdle) return fail(c, OLED_ERR_STATE, "reset while a layer is in flight");
   HIP_TRY(c, hipSetDevice(c->device));
   HIP_TRY(c, hipDeviceSynchronize());
-  for (int l = 0; l < c->L; ++l) c->pending[l] = 0;
+  std::fill(c->pending.begin(), c->pending.end(), 0);
   c->cs.reset();
   std::fill(c->rejected.begin(), c->rejected.end(), 0);
   std::fill(c->res_before.begin(), c->res_before.end(), 0);
@@ -376,8 +452,10 @@ oled_status oled_reset_cache(void* ctx) {
 oled_status route_block(void* ctx, int32_t layer, const float* logits_dev, int32_t T, void* stream) {
   Ctx* c = static_cast<Ctx*>(ctx);
   if (!c) return OLED_ERR_INVALID_ARG;
-  oled_status st = check_call(c, layer, Stage::kIdle);
+  oled_status st = check_layer(c, layer);
   if (st != OLED_OK) return st;
+  if (c->stage != Stage::kIdle)
+    return fail(c, OLED_ERR_STATE, "route_block while layer %d is in flight", c->cur_layer);
   if (!logits_dev) return fail(c, OLED_ERR_INVALID_ARG, "NULL logits");
   if (T < 1 || T > c->Tmax) return fail(c, OLED_ERR_INVALID_ARG, "T=%d outside [1,%d]", T, c->Tmax);
   HIP_TRY(c, hipSetDevice(c->device));
@@ -392,39 +470,98 @@ oled_status route_block(void* ctx, int32_t layer, const float* logits_dev, int32
   }
   const ExpertMask res = mask_of(c->cs.resident(layer), c->E);
   const int seq = ++c->seq;
-  {
-    OpTimer tm(c, s);
-    HIP_TRY(c, oled::launch_route_topk(logits_dev, T, c->E, c->K, c->d_topk, c->d_gates, c->d_flag, s));
-    tm.done(OLED_OP_ROUTE_TOPK, layer, static_cast<int64_t>(T) * c->E * 4 + static_cast<int64_t>(T) * c->K * 8, 0);
-  }
-  {
-    OpTimer tm(c, s);
+  const int64_t route_bytes = static_cast<int64_t>(T) * c->E * 4 + static_cast<int64_t>(T) * c->K * 8;
+  const int64_t perm_bytes = static_cast<int64_t>(T) * c->K * 12 + static_cast<int64_t>(c->E) * 8;
+  if (oled::route_fused(T, c->K)) {
+    OpEvents ev = op_begin(c, OLED_OP_ROUTE_TOPK);
+    HIP_TRY(c, oled::launch_route_fused(logits_dev, T, c->E, c->K, res, c->d_topk, c->d_gates,
+                                        c->d_counts, c->d_offsets, c->d_perm, c->d_inv, c->d_items,
+                                        c->d_item_counts, c->d_sync, c->h_sum, seq, ev.a, ev.b, s));
+    op_end(c, ev, OLED_OP_ROUTE_TOPK, layer, route_bytes + perm_bytes, 0);
+  } else {
+    {
+      OpEvents ev = op_begin(c, OLED_OP_ROUTE_TOPK);
+      HIP_TRY(c, oled::launch_route_topk(logits_dev, T, c->E, c->K, c->d_topk, c->d_gates,
+                                         c->d_flag, ev.a, ev.b, s));
+      op_end(c, ev, OLED_OP_ROUTE_TOPK, layer, route_bytes, 0);
+    }
+    OpEvents ev = op_begin(c, OLED_OP_PERMUTE);
     HIP_TRY(c, oled::launch_permute(c->d_topk, T, c->K, c->E, res, c->d_counts, c->d_offsets,
-                                    c->d_perm, c->d_inv, c->d_items, c->d_flag, c->h_sum, seq, s));
-    tm.done(OLED_OP_PERMUTE, layer, static_cast<int64_t>(T) * c->K * 12 + static_cast<int64_t>(c->E) * 8, 0);
+                                    c->d_perm, c->d_inv, c->d_items, c->d_item_counts, c->d_flag,
+                                    c->h_sum, seq, ev.a, ev.b, s));
+    op_end(c, ev, OLED_OP_PERMUTE, layer, perm_bytes, 0);
   }
-  HIP_TRY(c, hipEventRecord(c->ev_route, s));
   c->route_seq = seq;
   c->stage = Stage::kRouted;
   c->cur_layer = layer;
   c->cur_T = T;
+  c->cur_res = c->cs.resident_count(layer);
   c->cur_stream = s;
   c->have_stream = true;
+  c->fwd_x = nullptr;
+  c->fwd_y = nullptr;
   c->last_routed_layer = layer;
   c->last_routed_T = T;
+  return OLED_OK;
+}
+
+oled_status moe_forward_cached(void* ctx, int32_t layer, const void* x_dev, void* y_dev, void* stream) {
+  Ctx* c = static_cast<Ctx*>(ctx);
+  if (!c) return OLED_ERR_INVALID_ARG;
+  oled_status st = check_layer(c, layer);
+  if (st != OLED_OK) return st;
+  if (c->stage != Stage::kRouted)
+    return fail(c, OLED_ERR_STATE, "moe_forward_cached must follow route_block");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  st = check_in_flight(c, layer, s, "moe_forward_cached");
+  if (st != OLED_OK) return st;
+  if (!x_dev || !y_dev) return fail(c, OLED_ERR_INVALID_ARG, "NULL x or y");
+  HIP_TRY(c, hipSetDevice(c->device));
+  if (c->cur_res > 0) {
+    // hits: the active residents; the item count stays on the device, the
+    // byte and flop accounting is completed in apply_misses
+    SlotTable tab;
+    std::memset(&tab, 0xff, sizeof(tab));
+    c->cs.launch_slots(layer, tab.slot);
+    const int64_t routes = static_cast<int64_t>(c->cur_T) * c->K;
+    const int max_hit_items =
+        static_cast<int>(std::min<int64_t>(c->cur_res, routes) + routes / oled::kItemRows);
+    const bool bf16 = c->dtype == OLED_BF16;
+    FfnLaunch a = ffn_args(c, &tab, 0, -1, max_hit_items);
+    a.src = x_dev;
+    {
+      OpEvents ev = op_begin(c, OLED_OP_FFN_UP);
+      HIP_TRY(c, oled::launch_ffn_up(bf16, a, ev.a, ev.b, s));
+      op_end(c, ev, OLED_OP_FFN_UP, layer, -1, -1);
+    }
+    a.src = c->d_h;
+    {
+      OpEvents ev = op_begin(c, OLED_OP_FFN_DOWN);
+      HIP_TRY(c, oled::launch_ffn_down(bf16, a, ev.a, ev.b, s));
+      op_end(c, ev, OLED_OP_FFN_DOWN, layer, -1, -1);
+    }
+  }
+  c->fwd_x = x_dev;
+  c->fwd_y = y_dev;
+  c->stage = Stage::kHitsQueued;
   return OLED_OK;
 }
 
 oled_status apply_misses(void* ctx, int32_t layer, void* copy_stream, oled_miss_report* out) {
   Ctx* c = static_cast<Ctx*>(ctx);
   if (!c) return OLED_ERR_INVALID_ARG;
-  oled_status st = check_call(c, layer, Stage::kRouted);
+  oled_status st = check_layer(c, layer);
   if (st != OLED_OK) return st;
+  if (c->stage != Stage::kRouted && c->stage != Stage::kHitsQueued)
+    return fail(c, OLED_ERR_STATE, "apply_misses must follow route_block or moe_forward_cached");
+  if (layer != c->cur_layer)
+    return fail(c, OLED_ERR_STATE, "apply_misses: layer %d is not the layer in flight (%d)", layer,
+                c->cur_layer);
   HIP_TRY(c, hipSetDevice(c->device));
-  HIP_TRY(c, hipEventSynchronize(c->ev_route));
-  if (c->h_sum->seq != c->route_seq) {
+  st = wait_published(c, &c->h_sum->seq, c->route_seq, c->cur_stream, "routing summary");
+  if (st != OLED_OK) {
     c->stage = Stage::kIdle;
-    return fail(c, OLED_ERR_HIP, "stale route summary");
+    return st;
   }
   // every retention enqueued before this route has completed: commit them
   st = consume_all(c);
@@ -437,27 +574,26 @@ oled_status apply_misses(void* ctx, int32_t layer, void* copy_stream, oled_miss_
     return fail(c, OLED_ERR_INVALID_ARG, "non-finite router logit at layer %d", layer);
   }
   std::memcpy(c->counts.data(), c->h_sum->counts, sizeof(int32_t) * c->E);
-  c->cs.classify(layer, c->counts.data(), c->hit.data(), c->miss.data(), &c->n_active, &c->n_hits,
-                 &c->n_misses);
+  int n_active = 0, n_hits = 0, n_misses = 0;
+  c->cs.classify(layer, c->counts.data(), c->hit.data(), c->miss.data(), &n_active, &n_hits,
+                 &n_misses);
   int nhi = 0, nmi = 0;
-  c->hit_rows = c->miss_rows = 0;
+  int64_t hit_rows = 0, miss_rows = 0;
   for (int e = 0; e < c->E; ++e) {
     const int ni = (c->counts[e] + oled::kItemRows - 1) / oled::kItemRows;
     if (c->hit[e]) {
       nhi += ni;
-      c->hit_rows += c->counts[e];
+      hit_rows += c->counts[e];
     }
     if (c->miss[e]) {
       nmi += ni;
-      c->miss_rows += c->counts[e];
+      miss_rows += c->counts[e];
     }
   }
   if (nhi != c->h_sum->n_hit_items || nmi != c->h_sum->n_miss_items) {
     c->stage = Stage::kIdle;
     return fail(c, OLED_ERR_HIP, "work list disagrees with the host cache state");
   }
-  c->n_hit_items = nhi;
-  c->n_miss_items = nmi;
   std::memcpy(&c->res_before[static_cast<size_t>(layer) * c->E], c->cs.resident(layer), c->E);
   const int n_res = c->cs.resident_count(layer);
 
@@ -469,38 +605,90 @@ oled_status apply_misses(void* ctx, int32_t layer, void* copy_stream, oled_miss_
   hipStream_t cs = copy_stream ? static_cast<hipStream_t>(copy_stream) : c->own_copy;
   int64_t bytes = 0;
   if (!exps.empty()) {
-    OpTimer tm(c, cs);
-    for (size_t i = 0; i < exps.size(); ++i) {
-      const int64_t blk = c->host_block_of[static_cast<size_t>(layer) * c->E + exps[i]];
-      const hipError_t e = hipMemcpyAsync(c->d_pool + static_cast<int64_t>(slots[i]) * c->eb,
-                                          c->host_pool + blk * c->eb, c->eb,
-                                          hipMemcpyHostToDevice, cs);
-      if (e != hipSuccess) {
-        hipStreamSynchronize(cs);
-        c->cs.drop_staged(layer);
-        c->stage = Stage::kIdle;
-        return hip_fail(c, e, "hipMemcpyAsync of a missed expert");
+    // gate/up weights of every miss first, then the down weights, so the miss
+    // gate/up GEMM can run while the down weights are still in flight
+    OpEvents ev = op_begin(c, OLED_OP_H2D);
+    hipError_t e = hipSuccess;
+    if (ev.a) e = hipEventRecord(ev.a, cs);
+    for (int part = 0; part < 2 && e == hipSuccess; ++part) {
+      const int64_t off = part == 0 ? 0 : c->e13;
+      const int64_t len = part == 0 ? c->e13 : c->eb - c->e13;
+      for (size_t i = 0; i < exps.size() && e == hipSuccess; ++i) {
+        const int64_t blk = c->host_block_of[static_cast<size_t>(layer) * c->E + exps[i]];
+        e = hipMemcpyAsync(c->d_pool + static_cast<int64_t>(slots[i]) * c->eb + off,
+                           c->host_pool + blk * c->eb + off, len, hipMemcpyHostToDevice, cs);
+        bytes += len;
       }
-      bytes += c->eb;
+      if (e == hipSuccess) e = hipEventRecord(part == 0 ? c->ev_up : c->ev_down, cs);
     }
-    tm.done(OLED_OP_H2D, layer, bytes, 0);
-    const hipError_t e = hipEventRecord(c->ev_copy, cs);
+    if (e == hipSuccess && ev.b) e = hipEventRecord(ev.b, cs);
     if (e != hipSuccess) {
       hipStreamSynchronize(cs);
       c->cs.drop_staged(layer);
       c->stage = Stage::kIdle;
-      return hip_fail(c, e, "hipEventRecord after the miss copies");
+      if (ev.a) c->ev_free.push_back(ev.a);
+      if (ev.b) c->ev_free.push_back(ev.b);
+      return hip_fail(c, e, "enqueueing the miss copies");
     }
+    op_end(c, ev, OLED_OP_H2D, layer, bytes, 0);
     c->copies_outstanding = true;
   }
+  // complete the accounting of this layer's hit launches
+  for (auto it = c->ops.rbegin(); it != c->ops.rend() && it->layer == layer; ++it) {
+    if (it->kind == OLED_OP_FFN_UP && it->bytes < 0) {
+      it->bytes = up_bytes(c, n_hits, hit_rows);
+      it->flops = up_flops(c, hit_rows);
+    } else if (it->kind == OLED_OP_FFN_DOWN && it->bytes < 0) {
+      it->bytes = down_bytes(c, n_hits, hit_rows);
+      it->flops = down_flops(c, hit_rows);
+    }
+  }
+  if (c->stage == Stage::kHitsQueued) {
+    hipStream_t s = c->cur_stream;
+    const bool bf16 = c->dtype == OLED_BF16;
+    if (nmi > 0) {
+      SlotTable tab;
+      std::memset(&tab, 0xff, sizeof(tab));
+      c->cs.launch_slots(layer, tab.slot);
+      for (int e = 0; e < c->E; ++e)
+        if (c->miss[e] && (tab.slot[e] < 0 || tab.slot[e] >= c->n_slots))
+          return fail(c, OLED_ERR_HIP, "missed expert %d has no slot (internal accounting error)", e);
+      FfnLaunch a = ffn_args(c, &tab, nhi, nmi, nmi);
+      a.src = c->fwd_x;
+      HIP_TRY(c, hipStreamWaitEvent(s, c->ev_up, 0));
+      {
+        OpEvents ev = op_begin(c, OLED_OP_FFN_UP);
+        HIP_TRY(c, oled::launch_ffn_up(bf16, a, ev.a, ev.b, s));
+        op_end(c, ev, OLED_OP_FFN_UP, layer, up_bytes(c, n_misses, miss_rows), up_flops(c, miss_rows));
+      }
+      a.src = c->d_h;
+      HIP_TRY(c, hipStreamWaitEvent(s, c->ev_down, 0));
+      c->copies_outstanding = false;
+      {
+        OpEvents ev = op_begin(c, OLED_OP_FFN_DOWN);
+        HIP_TRY(c, oled::launch_ffn_down(bf16, a, ev.a, ev.b, s));
+        op_end(c, ev, OLED_OP_FFN_DOWN, layer, down_bytes(c, n_misses, miss_rows),
+               down_flops(c, miss_rows));
+      }
+    }
+    {
+      OpEvents ev = op_begin(c, OLED_OP_COMBINE);
+      const int T = c->cur_T;
+      HIP_TRY(c, oled::launch_combine(bf16, c->d_O, c->d_gates, c->d_inv, T, c->K, c->H, c->fwd_y,
+                                      ev.a, ev.b, s));
+      op_end(c, ev, OLED_OP_COMBINE, layer,
+             static_cast<int64_t>(T) * c->K * (c->H * 4 + 8) + static_cast<int64_t>(T) * c->H * c->esz,
+             0);
+    }
+  }
   int* lc = &c->last_counts[static_cast<size_t>(layer) * 3];
-  lc[0] = c->n_active;
-  lc[1] = c->n_hits;
-  lc[2] = c->n_misses;
+  lc[0] = n_active;
+  lc[1] = n_hits;
+  lc[2] = n_misses;
   if (out) {
-    out->n_active = c->n_active;
-    out->n_hits = c->n_hits;
-    out->n_misses = c->n_misses;
+    out->n_active = n_active;
+    out->n_hits = n_hits;
+    out->n_misses = n_misses;
     out->n_resident = n_res;
     out->rejected_layer = c->rejected_layer;
     out->reserved = 0;
@@ -511,94 +699,38 @@ oled_status apply_misses(void* ctx, int32_t layer, void* copy_stream, oled_miss_
   return OLED_OK;
 }
 
-oled_status moe_forward_cached(void* ctx, int32_t layer, const void* x_dev, void* y_dev, void* stream) {
-  Ctx* c = static_cast<Ctx*>(ctx);
-  if (!c) return OLED_ERR_INVALID_ARG;
-  oled_status st = check_call(c, layer, Stage::kApplied);
-  if (st != OLED_OK) return st;
-  if (!x_dev || !y_dev) return fail(c, OLED_ERR_INVALID_ARG, "NULL x or y");
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  if (s != c->cur_stream) return fail(c, OLED_ERR_INVALID_ARG, "stream differs from route_block's");
-  HIP_TRY(c, hipSetDevice(c->device));
-  SlotTable tab;
-  std::memset(&tab, 0xff, sizeof(tab));
-  c->cs.launch_slots(layer, tab.slot);
-  for (int e = 0; e < c->E; ++e)
-    if (c->counts[e] > 0 && (tab.slot[e] < 0 || tab.slot[e] >= c->n_slots))
-      return fail(c, OLED_ERR_HIP, "active expert %d has no slot (internal accounting error)", e);
-  const bool bf16 = c->dtype == OLED_BF16;
-  const int T = c->cur_T;
-  const int64_t e13 = static_cast<int64_t>(2) * c->I * c->H * c->esz;
-  const int64_t e2 = static_cast<int64_t>(c->H) * c->I * c->esz;
-  auto run = [&](int base, int n, int n_exp, int64_t rows) -> oled_status {
-    if (n <= 0) return OLED_OK;
-    {
-      OpTimer tm(c, s);
-      HIP_TRY(c, oled::launch_ffn_up(bf16, c->d_pool, c->eb, tab, c->d_items, base, n, x_dev,
-                                     c->d_perm, c->K, c->H, c->I, c->d_h, s));
-      tm.done(OLED_OP_FFN_UP, layer,
-              n_exp * e13 + rows * c->H * c->esz + rows * c->I * c->esz,
-              rows * 2 * 2 * static_cast<int64_t>(c->H) * c->I);
-    }
-    {
-      OpTimer tm(c, s);
-      HIP_TRY(c, oled::launch_ffn_down(bf16, c->d_pool, c->eb, tab, c->d_items, base, n, c->d_h,
-                                       c->H, c->I, c->d_O, s));
-      tm.done(OLED_OP_FFN_DOWN, layer, n_exp * e2 + rows * c->I * c->esz + rows * c->H * 4,
-              rows * 2 * static_cast<int64_t>(c->H) * c->I);
-    }
-    return OLED_OK;
-  };
-  st = run(0, c->n_hit_items, c->n_hits, c->hit_rows);
-  if (st != OLED_OK) return st;
-  if (c->copies_outstanding) {
-    HIP_TRY(c, hipStreamWaitEvent(s, c->ev_copy, 0));
-    c->copies_outstanding = false;
-  }
-  st = run(c->n_hit_items, c->n_miss_items, c->n_misses, c->miss_rows);
-  if (st != OLED_OK) return st;
-  {
-    OpTimer tm(c, s);
-    HIP_TRY(c, oled::launch_combine(bf16, c->d_O, c->d_gates, c->d_inv, T, c->K, c->H, y_dev, s));
-    tm.done(OLED_OP_COMBINE, layer,
-            static_cast<int64_t>(T) * c->K * (c->H * 4 + 8) + static_cast<int64_t>(T) * c->H * c->esz, 0);
-  }
-  c->stage = Stage::kForwarded;
-  return OLED_OK;
-}
-
 oled_status score_and_retain(void* ctx, int32_t layer, const float* conf_dev, void* stream) {
   Ctx* c = static_cast<Ctx*>(ctx);
   if (!c) return OLED_ERR_INVALID_ARG;
-  if (layer < 0 || layer >= c->L)
-    return fail(c, OLED_ERR_INVALID_ARG, "layer %d outside [0,%d)", layer, c->L);
-  // the forward pass is optional: the cache state does not depend on outputs
-  if ((c->stage != Stage::kApplied && c->stage != Stage::kForwarded) || layer != c->cur_layer)
-    return fail(c, OLED_ERR_STATE, "score_and_retain out of order (layer %d)", layer);
-  if (!conf_dev) return fail(c, OLED_ERR_INVALID_ARG, "NULL confidence");
+  oled_status st = check_layer(c, layer);
+  if (st != OLED_OK) return st;
+  if (c->stage != Stage::kApplied)
+    return fail(c, OLED_ERR_STATE, "score_and_retain must follow apply_misses");
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (s != c->cur_stream) return fail(c, OLED_ERR_INVALID_ARG, "stream differs from route_block's");
+  st = check_in_flight(c, layer, s, "score_and_retain");
+  if (st != OLED_OK) return st;
+  if (!conf_dev) return fail(c, OLED_ERR_INVALID_ARG, "NULL confidence");
   HIP_TRY(c, hipSetDevice(c->device));
   if (c->copies_outstanding) {  // later reads of these slots must see the copies
-    HIP_TRY(c, hipStreamWaitEvent(s, c->ev_copy, 0));
+    HIP_TRY(c, hipStreamWaitEvent(s, c->ev_down, 0));
     c->copies_outstanding = false;
   }
   const ExpertMask res = mask_of(c->cs.resident(layer), c->E);
   const int seq = ++c->seq;
   {
-    OpTimer tm(c, s);
+    OpEvents ev = op_begin(c, OLED_OP_SCORE_RETAIN);
     HIP_TRY(c, oled::launch_score_retain(c->d_gates, static_cast<const float*>(conf_dev), c->d_perm,
                                          c->d_offsets, c->d_counts, c->cur_T, c->K, c->E, c->C, res,
                                          c->d_score + static_cast<size_t>(layer) * c->E,
-                                         &c->h_ret[layer], seq, s));
-    tm.done(OLED_OP_SCORE_RETAIN, layer,
-            static_cast<int64_t>(c->cur_T) * c->K * 12 + static_cast<int64_t>(c->cur_T) * 4 +
-                static_cast<int64_t>(c->E) * 16,
-            0);
+                                         &c->h_ret[layer], seq, ev.a, ev.b, s));
+    op_end(c, ev, OLED_OP_SCORE_RETAIN, layer,
+           static_cast<int64_t>(c->cur_T) * c->K * 12 + static_cast<int64_t>(c->cur_T) * 4 +
+               static_cast<int64_t>(c->E) * 16,
+           0);
   }
-  HIP_TRY(c, hipEventRecord(c->ev_retain[layer], s));
   c->pending[layer] = 1;
   c->ret_seq[layer] = seq;
+  c->ret_stream[layer] = s;
   c->stage = Stage::kIdle;
   c->cur_layer = -1;
   return OLED_OK;
@@ -610,9 +742,8 @@ oled_status oled_read_layer_state(void* ctx, int32_t layer, oled_layer_state* ou
   if (layer < 0 || layer >= c->L) return fail(c, OLED_ERR_INVALID_ARG, "layer out of range");
   HIP_TRY(c, hipSetDevice(c->device));
   HIP_TRY(c, hipDeviceSynchronize());
-  oled_status st = OLED_OK;
   if (c->stage == Stage::kIdle) {
-    st = consume_all(c);
+    const oled_status st = consume_all(c);
     if (st == OLED_ERR_HIP) return st;
   }
   const int T = (c->last_routed_layer == layer) ? c->last_routed_T : 0;

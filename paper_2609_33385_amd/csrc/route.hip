@@ -1,23 +1,13 @@
 // K1 top-k routing and K2 histogram / prefix-sum / stable permutation for one
 // denoising block (OLED-MoE Sec. 4.1: the gate yields routed expert ids and
 // gate scores for every token of the block; Sec. 4.2: the active set A).
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include "kernels.h"
 
 namespace oled {
 namespace {
-
-__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const uint32_t lo = __shfl_xor(static_cast<uint32_t>(v), off);
-    const uint32_t hi = __shfl_xor(static_cast<uint32_t>(v >> 32), off);
-    const uint64_t o = (static_cast<uint64_t>(hi) << 32) | lo;
-    v = o > v ? o : v;
-  }
-  return v;
-}
 
 // Orderable 64-bit key: (logit as an order-preserving uint32, ~expert id).
 // The larger key is the larger logit, and on equal logits the lower id.
@@ -33,84 +23,113 @@ __device__ __forceinline__ float key_value(uint64_t key) {
   return __uint_as_float((ord & 0x80000000u) ? (ord & 0x7FFFFFFFu) : ~ord);
 }
 
-// One wavefront per token; lane l holds logits l, l+64, ... (EPL per lane).
-// k rounds of a wavefront arg-max over the keys, then the gates in fp64:
-// e_j = exp(l_j - l_0), s = e_0 + ... + e_{k-1} in slot order, g_j = fl32(e_j / s).
+__device__ __forceinline__ uint64_t bcast_u64(uint64_t v, int lane) {
+  const uint32_t lo = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(v)), lane);
+  const uint32_t hi = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(v >> 32)), lane);
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+// Routes one token with one wavefront; lane l holds logits l, l+64, ... (EPL
+// per lane). Each key's rank is the number of keys above it (all E keys are
+// broadcast lane by lane); the keys of rank j < k fill slot j, so the slots
+// are ordered by (logit desc, id asc). Slot j's expert and logit pass through
+// LDS (s_e, s_v: this wavefront's k entries); lane j < k takes
+// e_j = exp(l_j - l_0) in fp64, every lane sums e_0 + ... + e_{k-1} in slot
+// order (through s_x), and lane j returns g_j = fl32(e_j / s) and its expert
+// (else -1). `bad` collects non-finite logits.
+template <int EPL>
+__device__ __forceinline__ int route_token(const float* __restrict__ row, int E, int k,
+                                           int32_t* s_e, float* s_v, double* s_x,
+                                           float* __restrict__ gate_out, int* bad) {
+  const int lane = threadIdx.x & 63;
+  uint64_t key[EPL];
+  int rank[EPL];
+  int nonfinite = 0;
+#pragma unroll
+  for (int q = 0; q < EPL; ++q) {
+    const int e = lane + 64 * q;
+    key[q] = 0;
+    rank[q] = 0;
+    if (e < E) {
+      const float v = row[e];
+      nonfinite |= !__builtin_isfinite(v);
+      key[q] = route_key(v, e);
+    }
+  }
+  *bad |= __any(nonfinite);
+#pragma unroll
+  for (int qs = 0; qs < EPL; ++qs) {
+    if (64 * qs >= E) break;
+#pragma unroll 8
+    for (int src = 0; src < 64; ++src) {
+      const uint64_t other = bcast_u64(key[qs], src);
+#pragma unroll
+      for (int q = 0; q < EPL; ++q) rank[q] += other > key[q] ? 1 : 0;
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < EPL; ++q) {
+    if (key[q] != 0 && rank[q] < k) {
+      s_e[rank[q]] = static_cast<int32_t>(0xFFFFFFFFu - static_cast<uint32_t>(key[q]));
+      s_v[rank[q]] = key_value(key[q]);
+    }
+  }
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+  const float v0 = s_v[0];
+  const int my_e = lane < k ? s_e[lane] : -1;
+  const double ex = lane < k ? exp(static_cast<double>(s_v[lane]) - static_cast<double>(v0)) : 0.0;
+  if (lane < k) s_x[lane] = ex;
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+  double s = 0.0;
+  for (int j = 0; j < k; ++j) s += s_x[j];
+  *gate_out = static_cast<float>(ex / s);
+  __builtin_amdgcn_wave_barrier();  // s_* are reused by this wavefront's next token
+  return my_e;
+}
+
 template <int EPL>
 __global__ __launch_bounds__(256) void k_route_topk(const float* __restrict__ logits, int T, int E,
                                                     int k, int32_t* __restrict__ topk_idx,
                                                     float* __restrict__ gates,
                                                     int32_t* __restrict__ bad_flag) {
-  const int lane = threadIdx.x & 63;
+  __shared__ int32_t s_e[4][kMaxTopK];
+  __shared__ float s_v[4][kMaxTopK];
+  __shared__ double s_x[4][kMaxTopK];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nwaves = gridDim.x * 4;
-  for (int t = blockIdx.x * 4 + (threadIdx.x >> 6); t < T; t += nwaves) {
-    const float* row = logits + static_cast<size_t>(t) * E;
-    uint64_t key[EPL];
-    int bad = 0;
-#pragma unroll
-    for (int q = 0; q < EPL; ++q) {
-      const int e = lane + 64 * q;
-      key[q] = 0;
-      if (e < E) {
-        const float v = row[e];
-        bad |= !__builtin_isfinite(v);
-        key[q] = route_key(v, e);
-      }
-    }
-    if (__any(bad) && lane == 0) atomicOr(bad_flag, 1);
-
-    float sel_v[kMaxTopK];
-    int32_t sel_e[kMaxTopK];
-#pragma unroll
-    for (int j = 0; j < kMaxTopK; ++j) {
-      sel_v[j] = 0.f;
-      sel_e[j] = 0;
-      if (j < k) {
-        uint64_t best = 0;
-#pragma unroll
-        for (int q = 0; q < EPL; ++q) best = key[q] > best ? key[q] : best;
-        const uint64_t m = wave_max_u64(best);
-#pragma unroll
-        for (int q = 0; q < EPL; ++q)
-          if (key[q] == m) key[q] = 0;  // keys are unique: exactly one owner
-        sel_v[j] = key_value(m);
-        sel_e[j] = static_cast<int32_t>(0xFFFFFFFFu - static_cast<uint32_t>(m));
-      }
-    }
-    double ex[kMaxTopK];
-    double s = 0.0;
-#pragma unroll
-    for (int j = 0; j < kMaxTopK; ++j) {
-      ex[j] = 0.0;
-      if (j < k) {
-        ex[j] = exp(static_cast<double>(sel_v[j]) - static_cast<double>(sel_v[0]));
-        s += ex[j];
-      }
-    }
-#pragma unroll
-    for (int j = 0; j < kMaxTopK; ++j) {
-      if (j < k && lane == j) {
-        topk_idx[static_cast<size_t>(t) * k + j] = sel_e[j];
-        gates[static_cast<size_t>(t) * k + j] = static_cast<float>(ex[j] / s);
-      }
+  int bad = 0;
+  for (int t = blockIdx.x * 4 + wave; t < T; t += nwaves) {
+    float g;
+    const int e = route_token<EPL>(logits + static_cast<size_t>(t) * E, E, k, s_e[wave], s_v[wave],
+                                   s_x[wave], &g, &bad);
+    if (lane < k) {
+      topk_idx[static_cast<size_t>(t) * k + lane] = e;
+      gates[static_cast<size_t>(t) * k + lane] = g;
     }
   }
+  if (bad && lane == 0) atomicOr(bad_flag, 1);
 }
 
 constexpr int kPermThreads = 1024;
 constexpr int kChunkWords = 16;               // bitmask words per expert per chunk
 constexpr int kChunkTokens = kChunkWords * 32;
 
-// Single workgroup. Pass 1: per-expert counts (LDS atomics). Scan: offsets
-// and the work list, hit experts first. Pass 2, chunk by chunk of 512 tokens:
-// a per-expert token bitmask (the ballot of the tokens that chose the
-// expert), a running popcount prefix per 32-token word, and each route's
-// stable position = offsets[e] + tokens before it that chose e.
-__global__ __launch_bounds__(kPermThreads) void k_permute(
-    const int32_t* __restrict__ topk_idx, int T, int k, int E, ExpertMask resident,
+constexpr int kFusedMaxRoutes = 1024;       // fused routing path: T * k routes kept in LDS
+
+// Histogram, offsets, work list and stable permutation of the T*k routes in
+// `idx` (global or LDS), by one workgroup. Pass 1: per-expert counts (LDS
+// atomics). Scan: offsets and the work list, hit experts first. Pass 2,
+// chunk by chunk of 512 tokens: a per-expert token bitmask (the ballot of the
+// tokens that chose the expert), a running popcount prefix per 32-token word,
+// and each route's stable position = offsets[e] + tokens before it that chose e.
+// Then one wavefront publishes the summary (fields, system fence, seq).
+__device__ __forceinline__ void permute_body(
+    const int32_t* idx, int T, int k, int E, const ExpertMask& resident,
     int32_t* __restrict__ counts, int32_t* __restrict__ offsets, int32_t* __restrict__ perm,
-    int32_t* __restrict__ inv_perm, WorkItem* __restrict__ items, int32_t* __restrict__ bad_flag,
-    RouteSummary* __restrict__ summary, int seq) {
+    int32_t* __restrict__ inv_perm, WorkItem* __restrict__ items, int32_t* __restrict__ item_counts,
+    int bad, RouteSummary* __restrict__ summary, int seq) {
   __shared__ int32_t s_cnt[kMaxExperts];
   __shared__ int32_t s_off[kMaxExperts + 1];
   __shared__ int32_t s_item_base[kMaxExperts];
@@ -120,10 +139,11 @@ __global__ __launch_bounds__(kPermThreads) void k_permute(
   __shared__ int32_t s_pre[kMaxExperts * kChunkWords];
 
   const int tid = threadIdx.x;
+  const int nthr = blockDim.x;
   const int R = T * k;
-  for (int e = tid; e < kMaxExperts; e += kPermThreads) s_cnt[e] = 0;
+  for (int e = tid; e < kMaxExperts; e += nthr) s_cnt[e] = 0;
   __syncthreads();
-  for (int r = tid; r < R; r += kPermThreads) atomicAdd(&s_cnt[topk_idx[r]], 1);
+  for (int r = tid; r < R; r += nthr) atomicAdd(&s_cnt[idx[r]], 1);
   __syncthreads();
 
   if (tid < 64) {  // wave 0: scans over experts, 4 per lane
@@ -173,11 +193,10 @@ __global__ __launch_bounds__(kPermThreads) void k_permute(
   }
   __syncthreads();
 
-  for (int e = tid; e < E; e += kPermThreads) {
+  for (int e = tid; e < E; e += nthr) {
     const int c = s_cnt[e];
     counts[e] = c;
     offsets[e] = s_off[e];
-    summary->counts[e] = c;
     s_run[e] = s_off[e];
     const int base = s_item_base[e];
     for (int m = 0; m * kItemRows < c; ++m) {
@@ -193,15 +212,15 @@ __global__ __launch_bounds__(kPermThreads) void k_permute(
 
   for (int t0 = 0; t0 < T; t0 += kChunkTokens) {
     const int t1 = min(T, t0 + kChunkTokens);
-    for (int i = tid; i < E * kChunkWords; i += kPermThreads) s_mask[i] = 0u;
+    for (int i = tid; i < E * kChunkWords; i += nthr) s_mask[i] = 0u;
     __syncthreads();
-    for (int r = t0 * k + tid; r < t1 * k; r += kPermThreads) {
-      const int e = topk_idx[r];
+    for (int r = t0 * k + tid; r < t1 * k; r += nthr) {
+      const int e = idx[r];
       const int lt = r / k - t0;
       atomicOr(&s_mask[e * kChunkWords + (lt >> 5)], 1u << (lt & 31));
     }
     __syncthreads();
-    for (int e = tid; e < E; e += kPermThreads) {
+    for (int e = tid; e < E; e += nthr) {
       int run = s_run[e];
 #pragma unroll
       for (int w = 0; w < kChunkWords; ++w) {
@@ -211,8 +230,8 @@ __global__ __launch_bounds__(kPermThreads) void k_permute(
       s_run[e] = run;
     }
     __syncthreads();
-    for (int r = t0 * k + tid; r < t1 * k; r += kPermThreads) {
-      const int e = topk_idx[r];
+    for (int r = t0 * k + tid; r < t1 * k; r += nthr) {
+      const int e = idx[r];
       const int lt = r / k - t0;
       const int w = lt >> 5;
       const uint32_t below = s_mask[e * kChunkWords + w] & ((1u << (lt & 31)) - 1u);
@@ -223,39 +242,127 @@ __global__ __launch_bounds__(kPermThreads) void k_permute(
     __syncthreads();
   }
 
-  if (tid == 0) {
-    summary->n_hit_items = s_tot[0];
-    summary->n_miss_items = s_tot[1];
-    summary->bad_logits = *bad_flag;
-    *bad_flag = 0;
+  if (tid < 64) {
+    for (int e = tid; e < E; e += 64) summary->counts[e] = s_cnt[e];
+    if (tid == 0) {
+      item_counts[0] = s_tot[0];
+      item_counts[1] = s_tot[1];
+      summary->n_hit_items = s_tot[0];
+      summary->n_miss_items = s_tot[1];
+      summary->bad_logits = bad;
+    }
     __threadfence_system();
-    summary->seq = seq;
+    if (tid == 0) *reinterpret_cast<volatile int32_t*>(&summary->seq) = seq;
   }
+}
+
+__global__ __launch_bounds__(kPermThreads) void k_permute(
+    const int32_t* __restrict__ topk_idx, int T, int k, int E, ExpertMask resident,
+    int32_t* __restrict__ counts, int32_t* __restrict__ offsets, int32_t* __restrict__ perm,
+    int32_t* __restrict__ inv_perm, WorkItem* __restrict__ items, int32_t* __restrict__ item_counts,
+    int32_t* __restrict__ bad_flag, RouteSummary* __restrict__ summary, int seq) {
+  const int bad = *bad_flag;
+  __syncthreads();
+  if (threadIdx.x == 0) *bad_flag = 0;
+  permute_body(topk_idx, T, k, E, resident, counts, offsets, perm, inv_perm, items, item_counts,
+               bad, summary, seq);
+}
+
+// Small blocks (T*k <= 1024): routing on many CUs, one token per wavefront,
+// then the last workgroup to finish (a fenced counter; no workgroup ever
+// waits for another) permutes all routes. Workgroups hold 256 threads and
+// the permutation below is written for any workgroup size.
+template <int EPL>
+__global__ __launch_bounds__(256) void k_route_fused(
+    const float* __restrict__ logits, int T, int E, int k, ExpertMask resident,
+    int32_t* __restrict__ topk_idx, float* __restrict__ gates, int32_t* __restrict__ counts,
+    int32_t* __restrict__ offsets, int32_t* __restrict__ perm, int32_t* __restrict__ inv_perm,
+    WorkItem* __restrict__ items, int32_t* __restrict__ item_counts,
+    int32_t* __restrict__ sync, RouteSummary* __restrict__ summary, int seq) {
+  __shared__ int32_t s_e[4][kMaxTopK];
+  __shared__ float s_v[4][kMaxTopK];
+  __shared__ double s_x[4][kMaxTopK];
+  __shared__ int32_t s_idx[kFusedMaxRoutes];
+  __shared__ int32_t s_last;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int bad = 0;
+  for (int t = blockIdx.x * 4 + wave; t < T; t += gridDim.x * 4) {
+    float g;
+    const int e = route_token<EPL>(logits + static_cast<size_t>(t) * E, E, k, s_e[wave], s_v[wave],
+                                   s_x[wave], &g, &bad);
+    if (lane < k) {
+      topk_idx[static_cast<size_t>(t) * k + lane] = e;
+      gates[static_cast<size_t>(t) * k + lane] = g;
+    }
+  }
+  if (bad && lane == 0) atomicOr(&sync[1], 1);
+  __threadfence();   // this workgroup's routes are visible device-wide
+  __syncthreads();
+  if (threadIdx.x == 0) s_last = atomicAdd(&sync[0], 1) == static_cast<int>(gridDim.x) - 1;
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();   // see every other workgroup's routes
+  for (int r = threadIdx.x; r < T * k; r += blockDim.x) s_idx[r] = __hip_atomic_load(
+      &topk_idx[r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const int any_bad = __hip_atomic_load(&sync[1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();
+  if (threadIdx.x == 0) {  // re-arm for the next launch (stream order)
+    sync[0] = 0;
+    sync[1] = 0;
+  }
+  permute_body(s_idx, T, k, E, resident, counts, offsets, perm, inv_perm, items, item_counts,
+               any_bad, summary, seq);
 }
 
 }  // namespace
 
+bool route_fused(int T, int k) { return T * k <= kFusedMaxRoutes; }
+
 hipError_t launch_route_topk(const float* logits, int T, int E, int k, int32_t* topk_idx,
-                             float* gates, int32_t* bad_flag, hipStream_t s) {
+                             float* gates, int32_t* bad_flag, hipEvent_t ev0, hipEvent_t ev1,
+                             hipStream_t s) {
   const int blocks = (T + 3) / 4 < 4096 ? (T + 3) / 4 : 4096;
   if (E <= 64)
-    hipLaunchKernelGGL(k_route_topk<1>, dim3(blocks), dim3(256), 0, s, logits, T, E, k, topk_idx,
-                       gates, bad_flag);
+    hipExtLaunchKernelGGL(k_route_topk<1>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits, T,
+                          E, k, topk_idx, gates, bad_flag);
   else if (E <= 128)
-    hipLaunchKernelGGL(k_route_topk<2>, dim3(blocks), dim3(256), 0, s, logits, T, E, k, topk_idx,
-                       gates, bad_flag);
+    hipExtLaunchKernelGGL(k_route_topk<2>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits, T,
+                          E, k, topk_idx, gates, bad_flag);
   else
-    hipLaunchKernelGGL(k_route_topk<4>, dim3(blocks), dim3(256), 0, s, logits, T, E, k, topk_idx,
-                       gates, bad_flag);
+    hipExtLaunchKernelGGL(k_route_topk<4>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits, T,
+                          E, k, topk_idx, gates, bad_flag);
   return hipGetLastError();
 }
 
 hipError_t launch_permute(const int32_t* topk_idx, int T, int k, int E, const ExpertMask& resident,
                           int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* inv_perm,
-                          WorkItem* items, int32_t* bad_flag, RouteSummary* summary, int seq,
+                          WorkItem* items, int32_t* item_counts, int32_t* bad_flag,
+                          RouteSummary* summary, int seq, hipEvent_t ev0, hipEvent_t ev1,
                           hipStream_t s) {
-  hipLaunchKernelGGL(k_permute, dim3(1), dim3(kPermThreads), 0, s, topk_idx, T, k, E, resident,
-                     counts, offsets, perm, inv_perm, items, bad_flag, summary, seq);
+  hipExtLaunchKernelGGL(k_permute, dim3(1), dim3(kPermThreads), 0, s, ev0, ev1, 0, topk_idx, T, k,
+                        E, resident, counts, offsets, perm, inv_perm, items, item_counts, bad_flag,
+                        summary, seq);
+  return hipGetLastError();
+}
+
+hipError_t launch_route_fused(const float* logits, int T, int E, int k, const ExpertMask& resident,
+                              int32_t* topk_idx, float* gates, int32_t* counts, int32_t* offsets,
+                              int32_t* perm, int32_t* inv_perm, WorkItem* items,
+                              int32_t* item_counts, int32_t* sync, RouteSummary* summary, int seq,
+                              hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
+  const int blocks = (T + 3) / 4;
+  if (E <= 64)
+    hipExtLaunchKernelGGL(k_route_fused<1>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits, T,
+                          E, k, resident, topk_idx, gates, counts, offsets, perm, inv_perm, items,
+                          item_counts, sync, summary, seq);
+  else if (E <= 128)
+    hipExtLaunchKernelGGL(k_route_fused<2>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits, T,
+                          E, k, resident, topk_idx, gates, counts, offsets, perm, inv_perm, items,
+                          item_counts, sync, summary, seq);
+  else
+    hipExtLaunchKernelGGL(k_route_fused<4>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits, T,
+                          E, k, resident, topk_idx, gates, counts, offsets, perm, inv_perm, items,
+                          item_counts, sync, summary, seq);
   return hipGetLastError();
 }
 

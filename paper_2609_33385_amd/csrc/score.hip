@@ -7,6 +7,7 @@
 // is a segmented reduction over the expert-sorted route order with integer
 // LDS atomics between segments, so any order gives the same bits. Ranking by
 // the numerator equals ranking by p_e (one normaliser per layer).
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include "kernels.h"
@@ -16,6 +17,11 @@ namespace {
 
 constexpr int kThreads = 256;
 
+__device__ __forceinline__ bool ranks_above(unsigned long long sa, bool ra, int a,
+                                            unsigned long long sb, bool rb, int b) {
+  return sa > sb || (sa == sb && (ra > rb || (ra == rb && a < b)));
+}
+
 __global__ __launch_bounds__(kThreads) void k_score_retain(
     const float* __restrict__ gates, const float* __restrict__ conf,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ offsets,
@@ -24,14 +30,10 @@ __global__ __launch_bounds__(kThreads) void k_score_retain(
   __shared__ unsigned long long s_S[kMaxExperts];
   __shared__ int32_t s_off[kMaxExperts + 1];
   __shared__ int32_t s_bad;
-  __shared__ int32_t s_kept;
   const int tid = threadIdx.x;
   for (int e = tid; e < kMaxExperts; e += kThreads) s_S[e] = 0ull;
   for (int e = tid; e <= E; e += kThreads) s_off[e] = offsets[e];
-  if (tid == 0) {
-    s_bad = 0;
-    s_kept = 0;
-  }
+  if (tid == 0) s_bad = 0;
   __syncthreads();
 
   // segmented reduction: thread tid owns sorted positions [p0, p1)
@@ -67,33 +69,66 @@ __global__ __launch_bounds__(kThreads) void k_score_retain(
     if (bad) atomicOr(&s_bad, 1);
   }
   __syncthreads();
+  if (tid >= 64) return;
 
-  // Top-C over candidates R u A by (S desc, previously resident first, id asc)
-  for (int e = tid; e < E; e += kThreads) {
-    const bool res_e = resident.test(e);
-    const bool cand = res_e || counts[e] > 0;
-    const unsigned long long se = s_S[e];
-    int rank = 0;
-    for (int f = 0; f < E; ++f) {
-      const bool res_f = resident.test(f);
-      if (!(res_f || counts[f] > 0)) continue;
-      const unsigned long long sf = s_S[f];
-      const bool better = sf > se || (sf == se && (res_f && !res_e)) ||
-                          (sf == se && res_f == res_e && f < e);
-      rank += better ? 1 : 0;
+  // Top-C over candidates R u A by (S desc, previously resident first, id
+  // asc): one wavefront, lane l holds experts l, l+64, ...; a candidate's rank
+  // counts the candidates above it, broadcast from registers lane by lane.
+  const int lane = tid;
+  constexpr int Q = kMaxExperts / 64;
+  unsigned long long key_s[Q];
+  uint32_t key_rc[Q];  // bit 1: previously resident, bit 0: candidate
+  int rank[Q];
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int e = lane + 64 * q;
+    key_s[q] = s_S[e];
+    const bool r = e < E && resident.test(e);
+    const bool c = e < E && (r || counts[e] > 0);
+    key_rc[q] = (r ? 2u : 0u) | (c ? 1u : 0u);
+    rank[q] = 0;
+  }
+  const int nq = (E + 63) >> 6;
+  for (int qf = 0; qf < Q; ++qf) {
+    if (qf >= nq) break;
+    for (int src = 0; src < 64; ++src) {
+      const uint32_t rcf = __builtin_amdgcn_readlane(key_rc[qf], src);
+      if (!(rcf & 1u)) continue;  // not a candidate (uniform branch)
+      const uint32_t lo = __builtin_amdgcn_readlane(static_cast<uint32_t>(key_s[qf]), src);
+      const uint32_t hi = __builtin_amdgcn_readlane(static_cast<uint32_t>(key_s[qf] >> 32), src);
+      const unsigned long long sf = (static_cast<unsigned long long>(hi) << 32) | lo;
+      const int f = src + 64 * qf;
+#pragma unroll
+      for (int q = 0; q < Q; ++q)
+        rank[q] += ranks_above(sf, rcf & 2u, f, key_s[q], key_rc[q] & 2u, lane + 64 * q) ? 1 : 0;
     }
-    const bool keep = cand && rank < C;
-    out->retained[e] = keep ? 1 : 0;
-    score_out[e] = se;
-    if (keep) atomicAdd(&s_kept, 1);
   }
-  __syncthreads();
-  if (tid == 0) {
+  uint32_t word[kMaxExperts / 32];
+#pragma unroll
+  for (int w = 0; w < kMaxExperts / 32; ++w) word[w] = 0u;
+  int kept = 0;
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int e = lane + 64 * q;
+    const bool keep = (key_rc[q] & 1u) && rank[q] < C;
+    if (e < E) score_out[e] = key_s[q];
+    const uint64_t ballot = __ballot(keep);
+    word[2 * q] = static_cast<uint32_t>(ballot);
+    word[2 * q + 1] = static_cast<uint32_t>(ballot >> 32);
+    kept += __popcll(ballot);
+  }
+  // one wavefront publishes the result: fields, system-scope fence, then seq
+  uint32_t my_word = 0u;
+#pragma unroll
+  for (int w = 0; w < kMaxExperts / 32; ++w)
+    if (lane == w) my_word = word[w];
+  if (lane < kMaxExperts / 32) out->retained[lane] = my_word;
+  if (lane == 0) {
     out->bad_conf = s_bad;
-    out->n_retained = s_kept;
-    __threadfence_system();
-    out->seq = seq;
+    out->n_retained = kept;
   }
+  __threadfence_system();
+  if (lane == 0) *reinterpret_cast<volatile int32_t*>(&out->seq) = seq;
 }
 
 }  // namespace
@@ -101,9 +136,10 @@ __global__ __launch_bounds__(kThreads) void k_score_retain(
 hipError_t launch_score_retain(const float* gates, const float* conf, const int32_t* perm,
                                const int32_t* offsets, const int32_t* counts, int T, int k, int E,
                                int C, const ExpertMask& resident, uint64_t* score_out,
-                               RetainOut* out, int seq, hipStream_t s) {
-  hipLaunchKernelGGL(k_score_retain, dim3(1), dim3(kThreads), 0, s, gates, conf, perm, offsets,
-                     counts, T, k, E, C, resident, score_out, out, seq);
+                               RetainOut* out, int seq, hipEvent_t ev0, hipEvent_t ev1,
+                               hipStream_t s) {
+  hipExtLaunchKernelGGL(k_score_retain, dim3(1), dim3(kThreads), 0, s, ev0, ev1, 0, gates, conf,
+                        perm, offsets, counts, T, k, E, C, resident, score_out, out, seq);
   return hipGetLastError();
 }
 

@@ -29,10 +29,19 @@ STATUS_NAMES = {0: "OK", 1: "INVALID_ARG", 2: "OUT_OF_MEMORY", 3: "HIP", 4: "STA
 
 OLED_F32 = 0
 OLED_BF16 = 1
-OLED_FLAG_PROFILE = 1
+PROFILE_ALL = 0x7F
 
 OP_NAMES = {0: "route_topk", 1: "permute", 2: "ffn_up", 3: "ffn_down", 4: "combine",
             5: "score_retain", 6: "h2d"}
+OP_KIND = {v: k for k, v in OP_NAMES.items()}
+
+
+def profile_mask(*names) -> int:
+    """Bitmask of oled_op_kind for oled_config.profile_ops."""
+    m = 0
+    for n in names:
+        m |= 1 << OP_KIND[n]
+    return m
 
 EXPORTED = ["oled_create", "oled_destroy", "oled_last_error", "oled_reset_cache", "route_block",
             "apply_misses", "moe_forward_cached", "score_and_retain", "oled_read_layer_state",
@@ -44,7 +53,7 @@ class OledConfig(ctypes.Structure):
                 ("n_experts", ctypes.c_int32), ("top_k", ctypes.c_int32),
                 ("n_layers", ctypes.c_int32), ("capacity", ctypes.c_int32),
                 ("max_tokens", ctypes.c_int32), ("dtype", ctypes.c_int32),
-                ("device", ctypes.c_int32), ("flags", ctypes.c_int32),
+                ("device", ctypes.c_int32), ("profile_ops", ctypes.c_int32),
                 ("host_pool", ctypes.c_void_p), ("host_pool_blocks", ctypes.c_int64),
                 ("host_block_of", ctypes.POINTER(ctypes.c_int64))]
 
@@ -233,11 +242,11 @@ class Context:
 
     def __init__(self, hidden, inter, n_experts, top_k, n_layers, capacity, max_tokens,
                  dtype: str, host_pool: int, host_pool_blocks: int, host_block_of,
-                 device: int = 0, profile: bool = False):
+                 device: int = 0, profile_ops: int = 0):
         self._hbo = np.ascontiguousarray(host_block_of, dtype=np.int64)
         cfg = OledConfig(hidden, inter, n_experts, top_k, n_layers, capacity, max_tokens,
                          OLED_F32 if dtype == "f32" else OLED_BF16, device,
-                         OLED_FLAG_PROFILE if profile else 0, host_pool, host_pool_blocks,
+                         profile_ops, host_pool, host_pool_blocks,
                          self._hbo.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)))
         self.E, self.k, self.L, self.C, self.Tmax = n_experts, top_k, n_layers, capacity, max_tokens
         self.ctx = oled_create(cfg)

@@ -82,6 +82,8 @@ SMALL = [  # (E, k, T, C, dtype, H, I)
     (33, 3, 600, 33, "f32", 128, 128),
     (64, 8, 130, 0, "bf16", 256, 256),
     (16, 4, 1025, 40, "bf16", 128, 128),
+    (128, 16, 64, 51, "bf16", 128, 128),   # largest block routed by the fused path
+    (128, 8, 64, 51, "f32", 256, 1024),    # down GEMM with its K split in two
 ]
 
 

@@ -45,13 +45,13 @@ def test_library_targets_gfx950():
 
 def _cfg(**kw):
     base = dict(hidden=256, inter=512, n_experts=8, top_k=2, n_layers=1, capacity=4,
-                max_tokens=32, dtype=oled.OLED_F32, device=0, flags=0, host_pool=None,
+                max_tokens=32, dtype=oled.OLED_F32, device=0, profile_ops=0, host_pool=None,
                 host_pool_blocks=0, host_block_of=None)
     base.update(kw)
     hbo = np.zeros(base["n_layers"] * base["n_experts"], np.int64)
     c = oled.OledConfig(base["hidden"], base["inter"], base["n_experts"], base["top_k"],
                         base["n_layers"], base["capacity"], base["max_tokens"], base["dtype"],
-                        base["device"], base["flags"], base["host_pool"] or 0,
+                        base["device"], base["profile_ops"], base["host_pool"] or 0,
                         base["host_pool_blocks"],
                         hbo.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)))
     return c, hbo
