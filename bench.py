@@ -122,8 +122,9 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--capacity", type=int, default=None, help="experts cached per layer")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--profile-ops", default="ffn_up,ffn_down,h2d",
-                    help="operations timed with HIP events during the timed steps ('' for none)")
+    ap.add_argument("--profile-ops", default="ffn_up",
+                    help="operations timed with HIP events during the timed steps: any of "
+                         "ffn_up,ffn_down,h2d,combine,route_topk,permute,score_retain ('' for none)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: the expert-offloading layer path has no multi-GPU "
@@ -229,12 +230,14 @@ def main():
                      "launches": up["n"], "avg_launch_us": round(up["ms"] / max(1, up["n"]) * 1e3, 2),
                      "bytes_per_launch": int(up["bytes"] / max(1, up["n"]))},
         "detail": {
-            "ffn_up_down_GBps": round(ffn_gbs, 1),
-            "ffn_mfma_util": round(ffn_tflops / MFMA_BF16_PEAK_TFLOPS, 5),
-            "ffn_tflops": round(ffn_tflops, 2),
-            "ffn_ms_per_step": round(ffn_ms / args.steps, 4),
+            "ffn_up_down_GBps": round(ffn_gbs, 1) if down["n"] else None,
+            "ffn_up_mfma_util": round((up["flops"] / 1e12) / (up["ms"] / 1e3) / MFMA_BF16_PEAK_TFLOPS, 5)
+                                if up["ms"] > 0 else None,
+            "ffn_mfma_util": round(ffn_tflops / MFMA_BF16_PEAK_TFLOPS, 5) if down["n"] else None,
+            "ffn_ms_per_step": round(ffn_ms / args.steps, 4) if down["n"] else None,
             "h2d_GBps": round((h2d["bytes"] / 1e9) / (h2d["ms"] / 1e3), 2) if h2d["ms"] > 0 else None,
-            "h2d_ms_per_step": round(h2d["ms"] / args.steps, 4),
+            "h2d_ms_per_step": round(h2d["ms"] / args.steps, 4) if h2d["ms"] > 0 else None,
+            "profiled_ops": args.profile_ops,
             "hits_per_layer_iter": round(stats["hits"] / li, 3),
             "misses_per_layer_iter": round(stats["misses"] / li, 3),
             "active_per_layer_iter": round(stats["active"] / li, 3),

@@ -73,11 +73,10 @@ typedef enum { OLED_F32 = 0, OLED_BF16 = 1 } oled_dtype;
  *
  *  host_pool: caller-owned pinned host memory (hipHostMalloc, oled_host_alloc
  *  or a pinned torch tensor) of host_pool_blocks expert blocks, each
- *  3*H*I*elem bytes: w13 [2I][H] (gate projection W1 rows, then up projection
- *  W3 rows) followed by w2 [H][I]. host_block_of[l*E + e] in
- *  [0, host_pool_blocks) names the block of expert e of layer l; several
- *  experts may share one block. The pool must outlive the context; the table
- *  is copied at creation.
+ *  3*H*I*elem bytes in the packed layout written by oled_pack_expert.
+ *  host_block_of[l*E + e] in [0, host_pool_blocks) names the block of expert
+ *  e of layer l; several experts may share one block. The pool must outlive
+ *  the context; the table is copied at creation.
  */
 typedef struct {
   int32_t hidden;
@@ -203,8 +202,10 @@ oled_status moe_forward_cached(void* ctx, int32_t layer, const void* x_dev, void
  *  gives every miss a free staging slot and enqueues its host-to-device copy
  *  on copy_stream (NULL: the context's own copy stream), gate/up weights of
  *  all misses first, then their down weights. If moe_forward_cached was
- *  called, it then enqueues on the compute stream the misses' GEMMs (each
- *  half after its copies) and the combine into y. Fills *out (may be NULL).
+ *  called, it then enqueues on the compute stream the misses' GEMMs, each
+ *  half as soon as the host has seen its copies complete (the call returns
+ *  once the last miss copy has landed), and the combine into y. Fills *out
+ *  (may be NULL).
  *  Errors: STATE; INVALID_ARG if the logits held a non-finite value (no copy
  *  is issued, y is not written; the layer returns to idle with its cache
  *  unchanged); HIP if a copy could not be enqueued (staged slots are
@@ -238,6 +239,22 @@ oled_status oled_read_layer_state(void* ctx, int32_t layer, oled_layer_state* ou
  * Synchronises. Writes at most cap entries to out, sets *n_out; entries that
  * did not fit are dropped. */
 oled_status oled_profile_collect(void* ctx, oled_op_time* out, int32_t cap, int32_t* n_out);
+
+/*
+ * Packs one expert's logical weights into an expert block of the host pool.
+ *  w13: [2I][H] row-major (gate projection W1 rows 0..I-1, then up projection
+ *  W3 rows); w2: [H][I] row-major; elements of `dtype` (bf16 as raw 16-bit
+ *  patterns). block_out: 3*H*I elements, written in the order the grouped
+ *  GEMM reads them. With SPAN = 32 (bf16) or 16 (fp32), V = SPAN/4, S = H/SPAN
+ *  and S2 = I/SPAN, a fragment holds 16 rows x SPAN columns as element
+ *  l*V + i <- (row 16q + l%16, column SPAN*s + V*(l/16) + i), l < 64, i < V:
+ *    gate/up part: fragment ((q*S + s)*2 + m), m = 0 for W1, 1 for W3, q < I/16;
+ *    down part, after 2*I*H elements: fragment (q*S2 + s) of w2, q < H/16.
+ *  Host only; never fails for valid shapes (H, I multiples of 128).
+ *  Errors: INVALID_ARG (NULL pointer, bad dtype), UNSUPPORTED (shape).
+ */
+oled_status oled_pack_expert(int32_t dtype, int32_t hidden, int32_t inter, const void* w13,
+                             const void* w2, void* block_out);
 
 /* Pinned host memory for expert pools (hipHostMalloc). *ptr_out NULL on error. */
 oled_status oled_host_alloc(int64_t bytes, void** ptr_out);

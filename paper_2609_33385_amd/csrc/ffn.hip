@@ -13,7 +13,10 @@
 // the size of K); each streams its 16 (gate/up: 2 x 16) weight rows from HBM
 // straight into registers (A operand, M = features) and the token rows of its
 // K part from L2 (B operand, N = 16 tokens per MFMA tile); the KS partial
-// tiles are summed in LDS in a fixed order (deterministic).
+// tiles are summed in LDS in a fixed order (deterministic). Expert weights are
+// stored packed (see oled_pack_expert): the A fragment of one MFMA step is
+// 1 KiB of contiguous memory in lane order, so each wavefront streams one
+// contiguous range of its expert's block.
 // MFMA: v_mfma_f32_16x16x32_bf16 (bf16) or v_mfma_f32_16x16x4_f32 (fp32).
 //
 // One tile per workgroup over a grid sized for every possible tile; tiles past
@@ -80,6 +83,11 @@ __device__ __forceinline__ u32x4_t ldg16(const void* p) {
   return *reinterpret_cast<const u32x4_t*>(p);
 }
 
+// Expert weights are read once per work item: stream them past the caches.
+__device__ __forceinline__ u32x4_t ldw16(const void* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+}
+
 // Bijection on [0, total): tile t (XCD t % 8) -> contiguous range per XCD.
 __device__ __forceinline__ int xcd_order(int t, int total) {
   const int x = t & 7, local = t >> 3;
@@ -98,12 +106,13 @@ __device__ __forceinline__ void stream_k(const typename TR::T* a1, const typenam
   constexpr int U = NT == 1 ? 4 : 2;
   const int groups = steps / U;
   u32x4_t ra1[2][U], ra3[2][U], rb[2][U][NT];
+  constexpr int ASTEP = (UP ? 2 : 1) * 16 * SPAN;  // packed weights per MFMA step
   auto load = [&](int buf, int g0) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int kk = (g0 * U + u) * SPAN;
-      ra1[buf][u] = ldg16(a1 + kk);
-      if (UP) ra3[buf][u] = ldg16(a3 + kk);
+      ra1[buf][u] = ldw16(a1 + (g0 * U + u) * ASTEP);
+      if (UP) ra3[buf][u] = ldw16(a3 + (g0 * U + u) * ASTEP);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) rb[buf][u][nt] = ldg16(b[nt] + kk);
     }
@@ -130,9 +139,9 @@ __device__ __forceinline__ void stream_k(const typename TR::T* a1, const typenam
   // remaining steps (K range not a multiple of U steps)
   for (int st = groups * U; st < steps; ++st) {
     const int kk = st * SPAN;
-    const u32x4_t x1 = ldg16(a1 + kk);
+    const u32x4_t x1 = ldw16(a1 + st * ASTEP);
     u32x4_t x3;
-    if (UP) x3 = ldg16(a3 + kk);
+    if (UP) x3 = ldw16(a3 + st * ASTEP);
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const u32x4_t bv = ldg16(b[nt] + kk);
@@ -193,13 +202,17 @@ __device__ __forceinline__ void run_tile(const WorkItem& it, int tile_f0, const 
   const int kbeg = kp * kw;
   const int rows = it.rows;
 
+  // packed expert block: one 16-row x SPAN-k fragment per MFMA step, stored in
+  // the order the lanes consume it, so a wavefront load reads 1 KiB contiguously
+  constexpr int FRAG = 16 * TR::SPAN;
   const T* a1;
   const T* a3;
   if (UP) {
-    a1 = W + static_cast<size_t>(f0 + lr) * H + kbeg + EPV * g;
-    a3 = W + static_cast<size_t>(I + f0 + lr) * H + kbeg + EPV * g;
+    a1 = W + (static_cast<size_t>(f0 / 16) * (H / TR::SPAN) + kbeg / TR::SPAN) * 2 * FRAG + lane * EPV;
+    a3 = a1 + FRAG;
   } else {
-    a1 = W + static_cast<size_t>(2) * I * H + static_cast<size_t>(f0 + lr) * I + kbeg + EPV * g;
+    a1 = W + static_cast<size_t>(2) * I * H +
+         (static_cast<size_t>(f0 / 16) * (I / TR::SPAN) + kbeg / TR::SPAN) * FRAG + lane * EPV;
     a3 = a1;
   }
   // token rows past the item's end read its last row; their results are dropped
@@ -303,8 +316,8 @@ __global__ __launch_bounds__(256) void k_combine(const float* __restrict__ O,
 
 // K split of the wavefronts of a tile: a function of K alone, so every launch
 // over an expert reduces in the same order. Each wavefront keeps a K range of
-// at least 512 where K allows.
-inline int k_split(int K) { return K >= 2048 ? 4 : (K >= 1024 ? 2 : 1); }
+// at least 256.
+inline int k_split(int K) { return K >= 1024 ? 4 : (K >= 512 ? 2 : 1); }
 
 template <class TR, bool UP, int KS>
 hipError_t launch_ffn_ks(const FfnLaunch& a, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {

@@ -113,11 +113,10 @@ hipError_t launch_combine(bool bf16, const float* O, const float* gates, const i
                           int T, int k, int H, void* y, hipEvent_t ev0, hipEvent_t ev1,
                           hipStream_t s);
 
-// K6: priority numerators (segmented reduction) + Top-C retention.
-hipError_t launch_score_retain(const float* gates, const float* conf, const int32_t* perm,
-                               const int32_t* offsets, const int32_t* counts, int T, int k, int E,
-                               int C, const ExpertMask& resident, uint64_t* score_out,
-                               RetainOut* out, int seq, hipEvent_t ev0, hipEvent_t ev1,
-                               hipStream_t s);
+// K6: priority numerators (per-expert segment sums) + Top-C retention.
+hipError_t launch_score_retain(const float* gates, const float* conf, const int32_t* topk_idx,
+                               const int32_t* counts, int T, int k, int E, int C,
+                               const ExpertMask& resident, uint64_t* score_out, RetainOut* out,
+                               int seq, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s);
 
 }  // namespace oled

@@ -190,6 +190,19 @@ oled_status wait_published(Ctx* c, const int32_t* flag, int want, hipStream_t s,
   }
 }
 
+// Waits on the host for an event recorded on the copy stream. Launching the
+// dependent kernel after the host has seen the copy complete starts it within
+// a few microseconds; a GPU-side stream wait on a copy-engine event has been
+// measured to add tens of microseconds on this path.
+oled_status wait_event_spin(Ctx* c, hipEvent_t ev, const char* what) {
+  for (;;) {
+    const hipError_t e = hipEventQuery(ev);
+    if (e == hipSuccess) return OLED_OK;
+    if (e != hipErrorNotReady) return hip_fail(c, e, what);
+    _mm_pause();
+  }
+}
+
 // Commits the retention result of layer l.
 oled_status consume_layer(Ctx* c, int l) {
   if (!c->pending[l]) return OLED_OK;
@@ -306,6 +319,35 @@ int64_t down_bytes(const Ctx* c, int64_t n_exp, int64_t rows) {
 }
 int64_t up_flops(const Ctx* c, int64_t rows) { return rows * 4 * static_cast<int64_t>(c->H) * c->I; }
 int64_t down_flops(const Ctx* c, int64_t rows) { return rows * 2 * static_cast<int64_t>(c->H) * c->I; }
+
+// Expert block packing (see oled_pack_expert): fragment f holds 16 rows x SPAN
+// columns, element l*V + i <- (row 16q + l%16, column SPAN*s + V*(l/16) + i).
+template <class T, int SPAN>
+void pack_expert_t(int H, int I, const T* w13, const T* w2, T* out) {
+  constexpr int V = SPAN / 4;
+  constexpr int FRAG = 16 * SPAN;
+  const int S = H / SPAN, S2 = I / SPAN;
+  for (int q = 0; q < I / 16; ++q)
+    for (int s = 0; s < S; ++s)
+      for (int m = 0; m < 2; ++m) {
+        T* frag = out + (static_cast<size_t>(q * S + s) * 2 + m) * FRAG;
+        for (int l = 0; l < 64; ++l)
+          for (int i = 0; i < V; ++i) {
+            const size_t row = static_cast<size_t>(m) * I + 16 * q + (l & 15);
+            frag[l * V + i] = w13[row * H + SPAN * s + V * (l >> 4) + i];
+          }
+      }
+  T* down = out + static_cast<size_t>(2) * I * H;
+  for (int q = 0; q < H / 16; ++q)
+    for (int s = 0; s < S2; ++s) {
+      T* frag = down + static_cast<size_t>(q * S2 + s) * FRAG;
+      for (int l = 0; l < 64; ++l)
+        for (int i = 0; i < V; ++i) {
+          const size_t row = 16 * q + (l & 15);
+          frag[l * V + i] = w2[row * I + SPAN * s + V * (l >> 4) + i];
+        }
+    }
+}
 
 }  // namespace
 
@@ -655,14 +697,16 @@ oled_status apply_misses(void* ctx, int32_t layer, void* copy_stream, oled_miss_
           return fail(c, OLED_ERR_HIP, "missed expert %d has no slot (internal accounting error)", e);
       FfnLaunch a = ffn_args(c, &tab, nhi, nmi, nmi);
       a.src = c->fwd_x;
-      HIP_TRY(c, hipStreamWaitEvent(s, c->ev_up, 0));
+      st = wait_event_spin(c, c->ev_up, "gate/up weight copies");
+      if (st != OLED_OK) return st;
       {
         OpEvents ev = op_begin(c, OLED_OP_FFN_UP);
         HIP_TRY(c, oled::launch_ffn_up(bf16, a, ev.a, ev.b, s));
         op_end(c, ev, OLED_OP_FFN_UP, layer, up_bytes(c, n_misses, miss_rows), up_flops(c, miss_rows));
       }
       a.src = c->d_h;
-      HIP_TRY(c, hipStreamWaitEvent(s, c->ev_down, 0));
+      st = wait_event_spin(c, c->ev_down, "down weight copies");
+      if (st != OLED_OK) return st;
       c->copies_outstanding = false;
       {
         OpEvents ev = op_begin(c, OLED_OP_FFN_DOWN);
@@ -719,8 +763,8 @@ oled_status score_and_retain(void* ctx, int32_t layer, const float* conf_dev, vo
   const int seq = ++c->seq;
   {
     OpEvents ev = op_begin(c, OLED_OP_SCORE_RETAIN);
-    HIP_TRY(c, oled::launch_score_retain(c->d_gates, static_cast<const float*>(conf_dev), c->d_perm,
-                                         c->d_offsets, c->d_counts, c->cur_T, c->K, c->E, c->C, res,
+    HIP_TRY(c, oled::launch_score_retain(c->d_gates, static_cast<const float*>(conf_dev),
+                                         c->d_topk, c->d_counts, c->cur_T, c->K, c->E, c->C, res,
                                          c->d_score + static_cast<size_t>(layer) * c->E,
                                          &c->h_ret[layer], seq, ev.a, ev.b, s));
     op_end(c, ev, OLED_OP_SCORE_RETAIN, layer,
@@ -799,6 +843,20 @@ oled_status oled_profile_collect(void* ctx, oled_op_time* out, int32_t cap, int3
   }
   c->ops.clear();
   *n_out = n;
+  return OLED_OK;
+}
+
+oled_status oled_pack_expert(int32_t dtype, int32_t hidden, int32_t inter, const void* w13,
+                             const void* w2, void* block_out) {
+  if (!w13 || !w2 || !block_out) return OLED_ERR_INVALID_ARG;
+  if (dtype != OLED_F32 && dtype != OLED_BF16) return OLED_ERR_INVALID_ARG;
+  if (hidden <= 0 || inter <= 0 || hidden % 128 || inter % 128) return OLED_ERR_UNSUPPORTED;
+  if (dtype == OLED_BF16)
+    pack_expert_t<uint16_t, 32>(hidden, inter, static_cast<const uint16_t*>(w13),
+                                static_cast<const uint16_t*>(w2), static_cast<uint16_t*>(block_out));
+  else
+    pack_expert_t<uint32_t, 16>(hidden, inter, static_cast<const uint32_t*>(w13),
+                                static_cast<const uint32_t*>(w2), static_cast<uint32_t*>(block_out));
   return OLED_OK;
 }
 

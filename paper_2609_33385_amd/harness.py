@@ -15,11 +15,13 @@ from . import workload as W
 
 
 def fill_pool(w: W.Workload, seed: int, n_blocks: int) -> oled.PinnedPool:
-    """Pinned host pool of n_blocks expert blocks drawn by workload.expert_block."""
+    """Pinned host pool of n_blocks expert blocks drawn by workload.expert_block,
+    packed into the library's expert-block layout."""
     pool = oled.PinnedPool(n_blocks, w.expert_bytes)
     dt = np.float32 if w.dtype == "f32" else np.uint16
     for b in range(n_blocks):
-        pool.block(b, dt)[:] = W.expert_block(w, seed, b)
+        w13, w2 = W.split_expert(w, W.expert_block(w, seed, b))
+        oled.oled_pack_expert(w.dtype, w.hidden, w.inter, w13, w2, pool.block(b, dt))
     return pool
 
 

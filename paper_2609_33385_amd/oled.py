@@ -45,7 +45,7 @@ def profile_mask(*names) -> int:
 
 EXPORTED = ["oled_create", "oled_destroy", "oled_last_error", "oled_reset_cache", "route_block",
             "apply_misses", "moe_forward_cached", "score_and_retain", "oled_read_layer_state",
-            "oled_profile_collect", "oled_host_alloc", "oled_host_free"]
+            "oled_profile_collect", "oled_pack_expert", "oled_host_alloc", "oled_host_free"]
 
 
 class OledConfig(ctypes.Structure):
@@ -109,6 +109,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "score_and_retain": (i32, [vp, i32, vp, vp]),
         "oled_read_layer_state": (i32, [vp, i32, ctypes.POINTER(LayerState)]),
         "oled_profile_collect": (i32, [vp, ctypes.POINTER(OpTime), i32, ctypes.POINTER(i32)]),
+        "oled_pack_expert": (i32, [i32, i32, i32, vp, vp, vp]),
         "oled_host_alloc": (i32, [i64, ctypes.POINTER(vp)]),
         "oled_host_free": (None, [vp]),
     }
@@ -195,6 +196,18 @@ def oled_profile_collect(ctx, cap: int = 1 << 16):
     _check(ctx, load().oled_profile_collect(ctx, arr, cap, ctypes.byref(n)))
     return [(OP_NAMES[arr[i].kind], arr[i].layer, arr[i].ms, arr[i].bytes, arr[i].flops)
             for i in range(n.value)]
+
+
+def oled_pack_expert(dtype: str, hidden: int, inter: int, w13: np.ndarray, w2: np.ndarray,
+                     out: np.ndarray) -> None:
+    """Packs logical w13 [2I][H] and w2 [H][I] (float32 or bf16 bits) into `out`."""
+    w13 = np.ascontiguousarray(w13)
+    w2 = np.ascontiguousarray(w2)
+    assert out.flags.c_contiguous and out.size == 3 * hidden * inter
+    st = load().oled_pack_expert(OLED_F32 if dtype == "f32" else OLED_BF16, hidden, inter,
+                                 w13.ctypes.data, w2.ctypes.data, out.ctypes.data)
+    if st != OLED_OK:
+        raise OledError(st, "oled_pack_expert")
 
 
 def oled_host_alloc(nbytes: int) -> int:

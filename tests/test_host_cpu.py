@@ -194,3 +194,43 @@ def test_host_cache_sanitized_selftest(tmp_path):
     r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120)
     assert r.returncode == 0, r.stdout + r.stderr
     assert "selftest ok" in r.stdout
+
+
+# ------------------------------------------------------------ weight packing
+def _pack_ref(w13, w2, H, I, span):
+    """Documented packed layout, by reshape/transpose: fragment (q, s) holds
+    element (lane = g*16 + r, i) <- row 16q + r, column span*s + V*g + i."""
+    V = span // 4
+
+    def frags(M, rows, cols):
+        A = M.reshape(rows // 16, 16, cols // span, 4, V).transpose(0, 2, 3, 1, 4)
+        return A.reshape(rows // 16, cols // span, 64 * V)
+
+    up = np.stack([frags(w13[:I], I, H), frags(w13[I:], I, H)], axis=2)
+    return np.concatenate([up.ravel(), frags(w2, H, I).ravel()])
+
+
+@pytest.mark.parametrize("dtype,H,I", [("bf16", 256, 128), ("bf16", 128, 384), ("f32", 128, 256)])
+def test_pack_expert_layout(dtype, H, I):
+    rng = np.random.default_rng(H + I)
+    dt = np.uint16 if dtype == "bf16" else np.uint32
+    w13 = rng.integers(0, 2 ** 16 if dtype == "bf16" else 2 ** 31, size=(2 * I, H)).astype(dt)
+    w2 = rng.integers(0, 2 ** 16 if dtype == "bf16" else 2 ** 31, size=(H, I)).astype(dt)
+    out = np.zeros(3 * H * I, dt)
+    oled.oled_pack_expert(dtype, H, I, w13 if dtype == "bf16" else w13.view(np.float32),
+                          w2 if dtype == "bf16" else w2.view(np.float32),
+                          out if dtype == "bf16" else out.view(np.float32))
+    ref = _pack_ref(w13, w2, H, I, 32 if dtype == "bf16" else 16)
+    assert np.array_equal(out, ref)
+    assert sorted(out.tolist()) == sorted(np.concatenate([w13.ravel(), w2.ravel()]).tolist())
+
+
+def test_pack_expert_errors():
+    lib = oled.load()
+    a = np.zeros(3 * 128 * 128, np.uint16)
+    assert lib.oled_pack_expert(oled.OLED_BF16, 100, 128, a.ctypes.data, a.ctypes.data,
+                                a.ctypes.data) == oled.OLED_ERR_UNSUPPORTED
+    assert lib.oled_pack_expert(9, 128, 128, a.ctypes.data, a.ctypes.data,
+                                a.ctypes.data) == oled.OLED_ERR_INVALID_ARG
+    assert lib.oled_pack_expert(oled.OLED_BF16, 128, 128, None, a.ctypes.data,
+                                a.ctypes.data) == oled.OLED_ERR_INVALID_ARG
