@@ -75,8 +75,28 @@ def make_inputs(w, seed: int, n_steps: int):
     return (torch.from_numpy(lg[:n_steps]).cuda(), HN.to_device(xs), torch.from_numpy(cf).cuda())
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_ffn_up_llada40_traffic.json")
+FFN_SOURCE = os.path.join(ROOT, "paper_2609_33385_amd", "csrc", "ffn.hip")
+
+
+def measured_traffic():
+    """HBM bytes per gate/up GEMM launch from the committed counter summary, or
+    None if the kernel source changed since the counters were taken."""
+    import hashlib
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+        with open(FFN_SOURCE, "rb") as f:
+            sha = hashlib.sha256(f.read()).hexdigest()
+    except (OSError, ValueError):
+        return None
+    if rec.get("ffn_source_sha256") != sha:
+        return None
+    return rec.get("traffic_bytes_per_launch")
+
+
 def cpu_baseline(w, seed: int):
-    """The oracle on host cores: every layer of block 0, iteration 1, with the FFN."""
+    """The oracle on host cores: every layer of block 0, iterations 1-4, with the FFN."""
     from threadpoolctl import threadpool_info
 
     from oracle import oled_oracle as O
@@ -88,7 +108,7 @@ def cpu_baseline(w, seed: int):
     for l in range(w.n_layers):                               # iteration 0 fills R (untimed)
         res0[l] = O.layer_step(W.logits(w, seed, l, 0, 0), W.confidence(w, seed, 0, 0), res0[l],
                                w.top_k, w.capacity)["resident_after"]
-    iters = (1, 2)
+    iters = (1, 2, 3, 4)
     inputs = {it: (W.confidence(w, seed, 0, it),
                    [(W.logits(w, seed, l, 0, it), O.decode(W.activations(w, seed, l, 0, it)))
                     for l in range(w.n_layers)]) for it in iters}
@@ -108,7 +128,7 @@ def cpu_baseline(w, seed: int):
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     return {"value": n * w.tokens / dt, "unit": "layer-tokens/s", "cores": int(threads),
             "kind": "oracle",
-            "sample": (f"{n} layer-iterations (all {w.n_layers} layers of block 0, iterations 1-2) "
+            "sample": (f"{n} layer-iterations (all {w.n_layers} layers of block 0, iterations 1-4) "
                        f"of the same workload: routing, permutation, hit/miss sets, priorities, "
                        f"retention and the float64 SwiGLU experts + combine; {dt:.1f} s, BLAS on "
                        f"{threads} threads of {os.cpu_count()} host CPUs")}
@@ -122,6 +142,10 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--capacity", type=int, default=None, help="experts cached per layer")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibration", action="store_true",
+                    help="between warm-up and timed steps, run a plain streaming kernel of known traffic (torch "
+                         "negation over 256 MiB fp32: 256 MiB read, 256 MiB written) to scale "
+                         "hardware byte counters")
     ap.add_argument("--profile-ops", default="ffn_up",
                     help="operations timed with HIP events during the timed steps: any of "
                          "ffn_up,ffn_down,h2d,combine,route_topk,permute,score_retain ('' for none)")
@@ -184,6 +208,13 @@ def main():
     for g in range(args.warmup):
         step(g, False)
     torch.cuda.synchronize()
+    if args.calibration:
+        ca = torch.ones(64 << 20, dtype=torch.float32, device="cuda")
+        cb = torch.empty_like(ca)
+        for _ in range(2):
+            torch.neg(ca, out=cb)
+        torch.cuda.synchronize()
+        del ca, cb
     ctx.profile_collect()            # drop warm-up timings
     torch.cuda.synchronize()
     t_start = time.perf_counter()
@@ -226,7 +257,7 @@ def main():
                    "capacity": w.capacity},
         "roofline": {"kernel": "grouped gate/up SwiGLU GEMM (k_ffn up)", "bound": "hbm",
                      "achieved": round(up_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(up_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(up_gbs / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
                      "launches": up["n"], "avg_launch_us": round(up["ms"] / max(1, up["n"]) * 1e3, 2),
                      "bytes_per_launch": int(up["bytes"] / max(1, up["n"]))},
         "detail": {
