@@ -20,7 +20,6 @@ during the timed steps) and the CPU oracle timed on a bounded sample.
 from __future__ import annotations
 
 import argparse
-import ctypes
 import json
 import os
 import sys
@@ -146,6 +145,12 @@ def main():
                     help="between warm-up and timed steps, run a plain streaming kernel of known traffic (torch "
                          "negation over 256 MiB fp32: 256 MiB read, 256 MiB written) to scale "
                          "hardware byte counters")
+    ap.add_argument("--copy-mode", default="shader", choices=["shader", "sdma"],
+                    help="transfer of the misses: workgroups of the hit GEMM launches (shader) "
+                         "or hipMemcpyAsync on a copy stream (sdma)")
+    ap.add_argument("--launch-log", default=None,
+                    help="write the timed gate/up launches in order ([bytes, h2d bytes] each) "
+                         "to this JSON file, for matching them with profiler records")
     ap.add_argument("--profile-ops", default="ffn_up",
                     help="operations timed with HIP events during the timed steps: any of "
                          "ffn_up,ffn_down,h2d,combine,route_topk,permute,score_retain ('' for none)")
@@ -174,7 +179,8 @@ def main():
     y = torch.empty((T, w.hidden), dtype=torch.bfloat16, device="cuda")
     prof = oled.profile_mask(*[o for o in args.profile_ops.split(",") if o])
     ctx = oled.Context(w.hidden, w.inter, E, w.top_k, L, w.capacity, T, w.dtype, pool.ptr,
-                       pool.n_blocks, W.host_block_of(w, pool.n_blocks), profile_ops=prof)
+                       pool.n_blocks, W.host_block_of(w, pool.n_blocks), profile_ops=prof,
+                       copy_mode=args.copy_mode)
     log(f"setup {time.time() - t0:.1f}s: pool {pool.n_blocks} x {w.expert_bytes >> 20} MiB pinned")
 
     h = ctx.ctx
@@ -184,29 +190,20 @@ def main():
     x_p = [[xs[g, l].data_ptr() for l in range(L)] for g in range(n_total)]
     c_p = [conf[g].data_ptr() for g in range(n_total)]
     y_p = y.data_ptr()
-    rep = oled.MissReport()
-    rep_ref = ctypes.byref(rep)
-    stats = {"hits": 0, "misses": 0, "active": 0, "h2d_bytes": 0, "layer_iters": 0}
 
-    def step(g, count):
+    def step(g):
         for l in range(L):
             if lib.route_block(h, l, lg_p[g][l], T, sp):
                 raise oled.OledError(1, oled.last_error(h))
             if lib.moe_forward_cached(h, l, x_p[g][l], y_p, sp):
                 raise oled.OledError(1, oled.last_error(h))
-            if lib.apply_misses(h, l, None, rep_ref):
+            if lib.apply_misses(h, l, None, None):
                 raise oled.OledError(1, oled.last_error(h))
             if lib.score_and_retain(h, l, c_p[g], sp):
                 raise oled.OledError(1, oled.last_error(h))
-            if count:
-                stats["hits"] += rep.n_hits
-                stats["misses"] += rep.n_misses
-                stats["active"] += rep.n_active
-                stats["h2d_bytes"] += rep.h2d_bytes
-                stats["layer_iters"] += 1
 
     for g in range(args.warmup):
-        step(g, False)
+        step(g)
     torch.cuda.synchronize()
     if args.calibration:
         ca = torch.ones(64 << 20, dtype=torch.float32, device="cuda")
@@ -215,25 +212,44 @@ def main():
             torch.neg(ca, out=cb)
         torch.cuda.synchronize()
         del ca, cb
-    ctx.profile_collect()            # drop warm-up timings
+    ctx.profile_collect()            # drop warm-up timings and counts
+    ctx.collect_stats()
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for g in range(args.warmup, n_total):
-        step(g, True)
+        step(g)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     ops = ctx.profile_collect()
+    st = ctx.collect_stats()
+    stats = {"hits": st["n_hits"], "misses": st["n_misses"], "active": st["n_active"],
+             "h2d_bytes": st["h2d_bytes"], "layer_iters": st["layer_iters"]}
 
-    def agg(name):
-        sel = [o for o in ops if o[0] == name]
+    def agg(name, transfer=None):
+        """Launches of one kind; transfer True/False: only those that did / did
+        not also move miss weights host->device."""
+        sel = [o for o in ops if o[0] == name and
+               (transfer is None or (o[5] > 0) == transfer)]
         ms = sum(o[2] for o in sel)
-        return dict(n=len(sel), ms=ms, bytes=sum(o[3] for o in sel), flops=sum(o[4] for o in sel))
+        return dict(n=len(sel), ms=ms, bytes=sum(o[3] for o in sel), flops=sum(o[4] for o in sel),
+                    h2d=sum(max(0, o[5]) for o in sel))
 
-    up, down, h2d = agg("ffn_up"), agg("ffn_down"), agg("h2d")
+    # the gate/up GEMM's HBM roofline over the launches that moved no miss
+    # weights (a launch that also transfers misses runs as long as its PCIe reads)
+    up, down = agg("ffn_up", transfer=False), agg("ffn_down", transfer=False)
+    up_x, down_x, h2d = agg("ffn_up", transfer=True), agg("ffn_down", transfer=True), agg("h2d")
     up_gbs = (up["bytes"] / 1e9) / (up["ms"] / 1e3) if up["ms"] > 0 else 0.0
     ffn_ms = up["ms"] + down["ms"]
     ffn_tflops = ((up["flops"] + down["flops"]) / 1e12) / (ffn_ms / 1e3) if ffn_ms > 0 else 0.0
     ffn_gbs = ((up["bytes"] + down["bytes"]) / 1e9) / (ffn_ms / 1e3) if ffn_ms > 0 else 0.0
+    # host-to-device rate of the miss transfers: inside the gate/up and down
+    # launches that carried them (shader), or the copy-engine copies (sdma)
+    x_ms = up_x["ms"] + down_x["ms"] + h2d["ms"]
+    x_bytes = up_x["h2d"] + down_x["h2d"] + h2d["h2d"]
+    h2d_rate = round((x_bytes / 1e9) / (x_ms / 1e3), 2) if x_ms > 0 else None
+    if args.launch_log:
+        with open(args.launch_log, "w") as f:
+            json.dump({"ffn_up": [[o[3], o[5]] for o in ops if o[0] == "ffn_up"]}, f)
     value = args.steps * L * T / elapsed
     li = max(1, stats["layer_iters"])
     out = {
@@ -255,7 +271,8 @@ def main():
                    "hidden": w.hidden, "n_experts": E, "top_k": w.top_k, "inter": w.inter,
                    "n_layers": L, "tokens_per_iteration": T, "iterations_per_block": w.n_iters,
                    "capacity": w.capacity},
-        "roofline": {"kernel": "grouped gate/up SwiGLU GEMM (k_ffn up)", "bound": "hbm",
+        "roofline": {"kernel": "grouped gate/up SwiGLU GEMM (k_ffn up), launches that moved no "
+                               "miss weights", "bound": "hbm",
                      "achieved": round(up_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(up_gbs / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
                      "launches": up["n"], "avg_launch_us": round(up["ms"] / max(1, up["n"]) * 1e3, 2),
@@ -266,8 +283,9 @@ def main():
                                 if up["ms"] > 0 else None,
             "ffn_mfma_util": round(ffn_tflops / MFMA_BF16_PEAK_TFLOPS, 5) if down["n"] else None,
             "ffn_ms_per_step": round(ffn_ms / args.steps, 4) if down["n"] else None,
-            "h2d_GBps": round((h2d["bytes"] / 1e9) / (h2d["ms"] / 1e3), 2) if h2d["ms"] > 0 else None,
-            "h2d_ms_per_step": round(h2d["ms"] / args.steps, 4) if h2d["ms"] > 0 else None,
+            "copy_mode": args.copy_mode,
+            "h2d_GBps": h2d_rate,
+            "transfer_launches": up_x["n"] + down_x["n"] + h2d["n"],
             "profiled_ops": args.profile_ops,
             "hits_per_layer_iter": round(stats["hits"] / li, 3),
             "misses_per_layer_iter": round(stats["misses"] / li, 3),

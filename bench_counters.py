@@ -1,7 +1,7 @@
 """Summarises rocprofv3 runs of bench.py into the text summaries kept with the
 benchmark: per-kernel timings, and HBM traffic of the grouped gate/up GEMM.
 
-Input runs (CSV output, `-o run`):
+Input runs (CSV output, `-o run`), each with bench.py's --launch-log:
   trace  rocprofv3 --kernel-trace --stats   -- python3 bench.py
   fetch  rocprofv3 --pmc FETCH_SIZE         -- python3 bench.py --calibration --no-cpu-baseline
   write  rocprofv3 --pmc WRITE_SIZE         -- python3 bench.py --calibration --no-cpu-baseline
@@ -13,8 +13,11 @@ where the timed steps begin: the gate/up GEMM dispatches after it are the
 ones bench.py times.
 
 The gate/up GEMM is the k_ffn instance with UP = true (hit and miss launches
-use the same instance). Its traffic per launch is the mean over the timed
-dispatches of scaled FETCH_SIZE + WRITE_SIZE.
+use the same instance). The launch log lists the timed gate/up launches in
+dispatch order with the bytes each moved host-to-device; like bench.py's
+roofline, the summaries take the launches that moved none (a launch that
+transfers miss weights runs as long as its PCIe reads). Traffic per launch is
+the mean over those dispatches of scaled FETCH_SIZE + WRITE_SIZE.
 """
 from __future__ import annotations
 
@@ -57,12 +60,26 @@ def last_json_line(path: str) -> dict:
     return json.loads(lines[-1])
 
 
-def summarise_trace(d: str, bench: dict, plain: dict, cmd: str) -> str:
+def load_log(path: str):
+    with open(path) as f:
+        return json.load(f)["ffn_up"]
+
+
+def select(dispatches, log):
+    """The dispatches of the timed launches that moved no miss weights."""
+    if len(dispatches) != len(log):
+        raise SystemExit(f"{len(dispatches)} gate/up dispatches, launch log has {len(log)}")
+    return [d for d, (_, h2d) in zip(dispatches, log) if h2d <= 0]
+
+
+def summarise_trace(d: str, bench: dict, plain: dict, log, cmd: str) -> str:
     stats = read_csv(d, "kernel_stats")
     trace = read_csv(d, "kernel_trace")
     up = sorted((r for r in trace if is_up(r["Kernel_Name"])), key=lambda r: int(r["Dispatch_Id"]))
+    timed = select(up[-len(log):], log)
     n_timed = bench["roofline"]["launches"]
-    timed = up[-n_timed:]
+    if len(timed) != n_timed:
+        raise SystemExit(f"{len(timed)} launches without transfer, bench.py timed {n_timed}")
     dur = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in timed]
     timed_avg = sum(dur) / len(dur)
     up_stats = [r for r in stats if is_up(r["Name"])][0]
@@ -95,7 +112,7 @@ def summarise_trace(d: str, bench: dict, plain: dict, cmd: str) -> str:
         "|---|---|---|",
         f"| rocprofv3 stats, all dispatches | {up_stats['Calls']} | "
         f"{float(up_stats['AverageNs']) / 1e3:.2f} |",
-        f"| rocprofv3 trace, last {n_timed} dispatches (the timed steps) | {len(timed)} | "
+        f"| rocprofv3 trace, timed dispatches that moved no miss weights | {len(timed)} | "
         f"{timed_avg:.2f} |",
         f"| bench.py HIP events, timed steps, profiled run | {n_timed} | "
         f"{bench['roofline']['avg_launch_us']} |",
@@ -119,15 +136,16 @@ def counter_rows(d: str, counter: str):
     return rows
 
 
-def split_timed(rows, bench: dict):
+def split_timed(rows, bench: dict, log):
     cal = [i for i, r in enumerate(rows) if "neg_kernel" in r["Kernel_Name"]]
     if not cal:
         raise SystemExit("no calibration dispatch (torch neg) in the counter run")
     cal_val = float(rows[cal[-1]]["Counter_Value"])
     up = [float(r["Counter_Value"]) for r in rows[cal[-1] + 1:] if is_up(r["Kernel_Name"])]
+    up = select(up, log)
     if len(up) != bench["roofline"]["launches"]:
-        raise SystemExit(f"{len(up)} gate/up dispatches after calibration, bench.py timed "
-                         f"{bench['roofline']['launches']}")
+        raise SystemExit(f"{len(up)} gate/up dispatches without transfer after calibration, "
+                         f"bench.py timed {bench['roofline']['launches']}")
     return cal_val, up
 
 
@@ -135,6 +153,9 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--trace", required=True, help="rocprofv3 output dir of the kernel-trace run")
     ap.add_argument("--trace-bench", required=True, help="bench.py output of the kernel-trace run")
+    ap.add_argument("--trace-log", required=True, help="its --launch-log file")
+    ap.add_argument("--fetch-log", required=True)
+    ap.add_argument("--write-log", required=True)
     ap.add_argument("--plain-bench", required=True, help="bench.py output without the profiler")
     ap.add_argument("--fetch", required=True, help="rocprofv3 output dir of the FETCH_SIZE run")
     ap.add_argument("--fetch-bench", required=True)
@@ -144,14 +165,15 @@ def main():
     args = ap.parse_args()
 
     trace_cmd = ("rocprofv3 --kernel-trace --stats --output-format csv -d <dir> -o run "
-                 "-- python3 bench.py")
+                 "-- python3 bench.py --launch-log <dir>/launches.json")
     tb = last_json_line(args.trace_bench)
     with open(os.path.join(args.out, "k_ffn_up_llada40_kernel_stats.md"), "w") as f:
-        f.write(summarise_trace(args.trace, tb, last_json_line(args.plain_bench), trace_cmd))
+        f.write(summarise_trace(args.trace, tb, last_json_line(args.plain_bench),
+                                load_log(args.trace_log), trace_cmd))
 
     fb, wb = last_json_line(args.fetch_bench), last_json_line(args.write_bench)
-    cal_f, up_f = split_timed(counter_rows(args.fetch, "FETCH_SIZE"), fb)
-    cal_w, up_w = split_timed(counter_rows(args.write, "WRITE_SIZE"), wb)
+    cal_f, up_f = split_timed(counter_rows(args.fetch, "FETCH_SIZE"), fb, load_log(args.fetch_log))
+    cal_w, up_w = split_timed(counter_rows(args.write, "WRITE_SIZE"), wb, load_log(args.write_log))
     sf, sw = CAL_BYTES / cal_f, CAL_BYTES / cal_w       # bytes per counter KiB
     fetch_b = sum(up_f) / len(up_f) * sf
     write_b = sum(up_w) / len(up_w) * sw
@@ -159,7 +181,7 @@ def main():
     with open(FFN_SOURCE, "rb") as f:
         sha = hashlib.sha256(f.read()).hexdigest()
     pmc_cmd = ("timeout -s KILL 150 rocprofv3 --pmc {c} --output-format csv -d <dir> -o run "
-               "-- python3 bench.py --calibration --no-cpu-baseline")
+               "-- python3 bench.py --calibration --no-cpu-baseline --launch-log <dir>/launches.json")
     rec = {
         "kernel": "k_ffn UP=true (grouped gate/up SwiGLU GEMM)",
         "workload": "bf16 H2048 E64 k8 I1024, 16 layers, 32 tokens/iteration, cache 26/64",
@@ -190,8 +212,8 @@ def main():
         f"written) read FETCH_SIZE {cal_f:.0f} KiB and WRITE_SIZE {cal_w:.0f} KiB, so one "
         f"counter KiB is {sf:.1f} B fetched and {sw:.1f} B written.",
         "",
-        f"Over the {len(up_f)} timed gate/up launches (hit and miss, dispatches after the "
-        "calibration kernel):",
+        f"Over the {len(up_f)} timed gate/up launches that moved no miss weights (hit and miss "
+        "launches, dispatches after the calibration kernel):",
         "",
         "| per launch | bytes |",
         "|---|---|",

@@ -10,11 +10,10 @@
  *   moe_forward_cached the SwiGLU experts that are cached (hits, A & R) run
  *                      directly on the GPU (Sec. 4.1); enqueued without
  *                      waiting for the routing result on the host
- *   apply_misses       active set A, hits and misses M = A \ R of the layer
- *                      (Sec. 4.2); every miss is transferred host->device into
- *                      a staging slot on a copy stream (G = M) and computed on
- *                      the GPU once its copy lands; then the gate-weighted
- *                      combine of all k routes of every token
+ *   apply_misses       misses M = A \ R of the layer (Sec. 4.2): every miss
+ *                      is transferred host->device into a staging slot (G = M)
+ *                      and computed on the GPU once it has landed; then the
+ *                      gate-weighted combine of all k routes of every token
  *   score_and_retain   reuse priorities p_e (the priority equation of
  *                      Sec. 4.3, psi(c) = c; stale residents score zero) and
  *                      the retention rule R' = Top_C(R u G, p) of Sec. 4.2
@@ -25,6 +24,21 @@
  * moe_forward_cached may be skipped (control path only: apply_misses then
  * only transfers); the cache state does not depend on expert outputs. The
  * layer output y is complete once the work apply_misses enqueued has run.
+ *
+ * The cache state (resident sets, slot tables, free slots) lives in device
+ * memory and only the library's kernels change it, in stream order: the
+ * routing kernel gives every miss a free staging slot, the retention kernel
+ * commits. The transfer of the misses (oled_config.copy_mode):
+ *  OLED_COPY_SHADER  workgroups of the hit experts' GEMM launches copy the
+ *                    staged misses' weights from the pinned pool over PCIe
+ *                    while the other workgroups compute; no call of a layer
+ *                    waits for the device unless a report is asked for.
+ *  OLED_COPY_SDMA    apply_misses waits for the routing result and copies the
+ *                    misses with hipMemcpyAsync on a copy stream; the miss
+ *                    GEMMs are launched once the host has seen the copies land.
+ * Counts of a layer (hits, misses, bytes) are in the pinned routing records;
+ * apply_misses with a report, oled_read_layer_state and oled_collect_stats
+ * read them.
  *
  * Conventions
  *  - Every function returns an oled_status and never aborts. Host-detected
@@ -62,6 +76,9 @@ typedef enum {
 
 typedef enum { OLED_F32 = 0, OLED_BF16 = 1 } oled_dtype;
 
+/* How the misses reach their staging slots (see above). */
+typedef enum { OLED_COPY_SHADER = 0, OLED_COPY_SDMA = 1 } oled_copy_mode;
+
 
 /*
  * Shape and resources of one MoE layer stack.
@@ -76,7 +93,8 @@ typedef enum { OLED_F32 = 0, OLED_BF16 = 1 } oled_dtype;
  *  3*H*I*elem bytes in the packed layout written by oled_pack_expert.
  *  host_block_of[l*E + e] in [0, host_pool_blocks) names the block of expert
  *  e of layer l; several experts may share one block. The pool must outlive
- *  the context; the table is copied at creation.
+ *  the context; the table is copied at creation. The pool must be mapped for
+ *  device access (hipHostMalloc memory is).
  */
 typedef struct {
   int32_t hidden;
@@ -93,6 +111,8 @@ typedef struct {
   const void* host_pool;
   int64_t host_pool_blocks;
   const int64_t* host_block_of;
+  int32_t copy_mode;        /* oled_copy_mode */
+  int32_t reserved;
 } oled_config;
 
 /* Result of apply_misses for the layer (Sec. 4.2). Counts are experts. */
@@ -104,8 +124,19 @@ typedef struct {
   int32_t rejected_layer; /* a layer whose last retention was rejected for an
                              invalid confidence since the previous report, else -1 */
   int32_t reserved;
-  int64_t h2d_bytes;      /* bytes enqueued on the copy stream */
+  int64_t h2d_bytes;      /* bytes transferred host->device for the misses */
 } oled_miss_report;
+
+/* Totals over the routing calls since the last oled_collect_stats. */
+typedef struct {
+  int64_t layer_iters;    /* route_block calls */
+  int64_t n_active;       /* sum of |A| */
+  int64_t n_hits;         /* sum of |A & R| */
+  int64_t n_misses;       /* sum of |M| */
+  int64_t n_transferred;  /* misses given a staging slot and transferred */
+  int64_t h2d_bytes;      /* their bytes */
+  int64_t n_bad_blocks;   /* blocks with a non-finite logit (nothing staged) */
+} oled_stats;
 
 /*
  * Inspection of a layer (synchronises the device). Every pointer is a
@@ -133,8 +164,10 @@ typedef struct {
   int32_t kind;      /* oled_op_kind */
   int32_t layer;
   float ms;          /* device time between the events around the operation */
-  int64_t bytes;     /* algorithmic bytes moved */
+  int64_t bytes;     /* algorithmic device-memory bytes of the operation's compute */
   int64_t flops;     /* algorithmic flops */
+  int64_t h2d_bytes; /* bytes it transferred host->device (shader transfer inside a
+                        GEMM launch, a transfer-only launch, or copy-engine copies) */
 } oled_op_time;
 
 typedef enum {
@@ -144,12 +177,14 @@ typedef enum {
   OLED_OP_FFN_DOWN = 3,      /* grouped down GEMM */
   OLED_OP_COMBINE = 4,
   OLED_OP_SCORE_RETAIN = 5,
-  OLED_OP_H2D = 6            /* miss copies of one apply_misses */
+  OLED_OP_H2D = 6            /* copy-engine copies of one apply_misses, or a
+                                transfer-only launch */
 } oled_op_kind;
 
 /* Creates a context: allocates the slot pool (L*min(C,E) + min(E, Tmax*k)
- * expert slots), routing scratch, pinned summaries, a copy stream and events
- * on cfg->device. The cache starts empty (R = {} for every layer).
+ * expert slots), the device cache state, routing scratch, pinned records, a
+ * copy stream and events on cfg->device. The cache starts empty (R = {} for
+ * every layer).
  * Errors: INVALID_ARG (bad field, host pool not pinned), UNSUPPORTED (shape),
  * OUT_OF_MEMORY, HIP. On error *ctx_out is NULL. */
 oled_status oled_create(const oled_config* cfg, void** ctx_out);
@@ -161,7 +196,9 @@ void oled_destroy(void* ctx);
  * the last oled_create failure of the calling thread. */
 const char* oled_last_error(const void* ctx);
 
-/* Empties every layer's cache (R := {}), as at creation. Synchronises. */
+/* Empties every layer's cache (R := {}), as at creation. Synchronises. Also
+ * the way out after OLED_ERR_HIP, which leaves the context refusing
+ * route_block (OLED_ERR_STATE) until it is reset. */
 oled_status oled_reset_cache(void* ctx);
 
 /*
@@ -172,9 +209,13 @@ oled_status oled_reset_cache(void* ctx);
  *  summed in slot order, rounded once to fp32. Then the expert histogram,
  *  exclusive offsets and the stable counting-sort permutation of the T*k
  *  routes by (expert, token). Asynchronous on `stream`.
+ *  The same kernel splits the active experts into hits and misses against
+ *  the layer's resident set and gives every miss a free staging slot.
  *  Errors: INVALID_ARG (layer outside [0,L), T outside [1,Tmax], NULL logits),
- *  STATE. A non-finite logit is detected on the device and reported by the
- *  following apply_misses.
+ *  STATE. A non-finite logit is detected on the device: nothing is staged and
+ *  the layer's retention commits nothing; it is reported by apply_misses when
+ *  a report is asked for, else by the next oled_read_layer_state of the layer
+ *  (and counted by oled_collect_stats).
  */
 oled_status route_block(void* ctx, int32_t layer, const float* logits_dev, int32_t T,
                         void* stream);
@@ -187,7 +228,9 @@ oled_status route_block(void* ctx, int32_t layer, const float* logits_dev, int32
  *  Enqueues the grouped GEMMs of the hit experts (A & R, weights read from
  *  their cache slots) on `stream` right away; their work list and count come
  *  from route_block's kernels on the device, so no host synchronisation is
- *  needed. Accumulation is fp32; silu(W1 x) * (W3 x) is stored in dtype.
+ *  needed. With OLED_COPY_SHADER the same launches also transfer the staged
+ *  misses (gate/up weights with the gate/up GEMM, down weights with the
+ *  down GEMM). Accumulation is fp32; silu(W1 x) * (W3 x) is stored in dtype.
  *  Both buffers must stay valid until the layer's work has run.
  *  Errors: STATE (not right after route_block), INVALID_ARG (NULL pointers,
  *  a stream other than route_block's).
@@ -197,20 +240,25 @@ oled_status moe_forward_cached(void* ctx, int32_t layer, const void* x_dev, void
 
 /*
  * apply_misses: misses M = A \ R of the routed layer (Sec. 4.2) and their
- *  compensation by transfer (G = M). Waits for route_block's result (the one
- *  host synchronisation of a layer; it overlaps the hit experts' GEMMs),
- *  gives every miss a free staging slot and enqueues its host-to-device copy
- *  on copy_stream (NULL: the context's own copy stream), gate/up weights of
- *  all misses first, then their down weights. If moe_forward_cached was
- *  called, it then enqueues on the compute stream the misses' GEMMs, each
- *  half as soon as the host has seen its copies complete (the call returns
- *  once the last miss copy has landed), and the combine into y. Fills *out
- *  (may be NULL).
- *  Errors: STATE; INVALID_ARG if the logits held a non-finite value (no copy
- *  is issued, y is not written; the layer returns to idle with its cache
- *  unchanged); HIP if a copy could not be enqueued (staged slots are
- *  released, cache unchanged). Retentions enqueued earlier are committed
- *  here; one rejected for an invalid confidence is named in
+ *  compensation by transfer (G = M), then the combine.
+ *  OLED_COPY_SHADER: if moe_forward_cached was called, enqueues the misses'
+ *  grouped GEMMs (their weights were transferred by the hit launches) and the
+ *  combine into y; else a transfer-only launch. Nothing waits for the device
+ *  unless out is non-NULL. copy_stream is not used.
+ *  OLED_COPY_SDMA: waits for route_block's result, copies every staged miss
+ *  with hipMemcpyAsync on copy_stream (NULL: the context's own copy stream),
+ *  gate/up weights of all misses first, then their down weights; if
+ *  moe_forward_cached was called, launches the misses' GEMMs on the compute
+ *  stream as the host sees each half of the copies land (the call returns
+ *  once the last copy has landed), then the combine.
+ *  out (may be NULL): filled from the layer's routing record, which makes the
+ *  call wait for route_block's kernel.
+ *  Errors: STATE; INVALID_ARG if the record shows a non-finite logit (only
+ *  seen when the record is read: with a report, or always with
+ *  OLED_COPY_SDMA): nothing was staged, y is not written, the layer returns
+ *  to idle with its cache unchanged; HIP if a launch or copy could not be
+ *  enqueued (the context then needs oled_reset_cache). Retentions enqueued
+ *  earlier that were rejected for an invalid confidence are named in
  *  out->rejected_layer (the call still returns OLED_OK for its own work).
  */
 oled_status apply_misses(void* ctx, int32_t layer, void* copy_stream, oled_miss_report* out);
@@ -222,18 +270,25 @@ oled_status apply_misses(void* ctx, int32_t layer, void* copy_stream, oled_miss_
  *  (exact; p_e = S[e] / sum S). Residents that no token routed to score 0.
  *  Candidates R u M are ranked by (S desc, previously resident first, id asc)
  *  and the first min(C, |R u M|) stay cached for the next iteration of this
- *  layer; the rest release their slots. The new cache state is committed on
- *  the host at the next synchronising call.
+ *  layer; the rest release their slots. The same kernel commits the new
+ *  state in device memory (retained misses keep their staging slot).
  *  Errors: STATE, INVALID_ARG (NULL conf). A confidence outside [0,1] (or NaN)
  *  is detected on the device: the layer keeps its previous R, its transferred
- *  misses are dropped, and the rejection is reported by the next
+ *  misses are dropped, and the rejection is reported by the next report of
  *  apply_misses (rejected_layer) and by oled_read_layer_state.
  */
 oled_status score_and_retain(void* ctx, int32_t layer, const float* conf_dev, void* stream);
 
-/* Inspection (synchronises; see oled_layer_state). Returns INVALID_ARG (with
- * the arrays filled) if the layer's last retention was rejected. */
+/* Inspection (synchronises; see oled_layer_state). With no layer in flight it
+ * also checks slot conservation over the whole device cache state (every
+ * slot free or held by exactly one resident expert, |R| <= C per layer) and
+ * returns HIP if it does not hold. Returns INVALID_ARG (with the arrays
+ * filled) if the layer's last retention was rejected, or once after a bad
+ * block of the layer that no report has named. */
 oled_status oled_read_layer_state(void* ctx, int32_t layer, oled_layer_state* out);
+
+/* Totals of the routing records since the last call (synchronises). */
+oled_status oled_collect_stats(void* ctx, oled_stats* out);
 
 /* Operation timings recorded since the last collection (oled_config.profile_ops).
  * Synchronises. Writes at most cap entries to out, sets *n_out; entries that

@@ -1,4 +1,4 @@
-"""Builds the gfx950 HIP library (liboled.so) and the host-only cache test library.
+"""Builds the gfx950 HIP library (liboled.so).
 
     python -m paper_2609_33385_amd.build
 
@@ -18,14 +18,13 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 OBJ = os.path.join(CSRC, "_build")
 LIB = os.path.join(PKG, "liboled.so")
-CACHE_LIB = os.path.join(PKG, "liboled_cache_host.so")
 
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.path.join(ROCM, "bin", "hipcc")
 ARCH = "gfx950"
 
 HIP_SOURCES = ["route.hip", "ffn.hip", "score.hip"]
-HOST_SOURCES = ["oled.cpp", "cache_state.cpp"]
+HOST_SOURCES = ["oled.cpp"]
 
 HIP_FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
              # keep hand-written and compiler-generated fp32 code off packed-fp32 ops
@@ -53,7 +52,7 @@ def _compile(src: str) -> str:
 
 
 def build(verbose: bool = False) -> str:
-    """Compiles the HIP library for gfx950 and the host-only cache library."""
+    """Compiles the HIP library for gfx950."""
     if not os.path.exists(HIPCC):
         raise RuntimeError(f"hipcc not found at {HIPCC}")
     os.makedirs(OBJ, exist_ok=True)
@@ -63,21 +62,15 @@ def build(verbose: bool = False) -> str:
     tmp = LIB + ".tmp"
     _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp])
     os.replace(tmp, LIB)
-    tmp = CACHE_LIB + ".tmp"
-    _run(["g++", "-O2", "-std=c++17", "-fPIC", "-shared", f"-I{CSRC}",
-          os.path.join(CSRC, "cache_state.cpp"), os.path.join(CSRC, "cache_state_capi.cpp"),
-          "-o", tmp])
-    os.replace(tmp, CACHE_LIB)
     if verbose:
-        print("built", LIB, "and", CACHE_LIB)
+        print("built", LIB)
     return LIB
 
 
 def clean() -> None:
     shutil.rmtree(OBJ, ignore_errors=True)
-    for p in (LIB, CACHE_LIB):
-        if os.path.exists(p):
-            os.remove(p)
+    if os.path.exists(LIB):
+        os.remove(LIB)
 
 
 if __name__ == "__main__":

@@ -1,6 +1,6 @@
 // K4 grouped SwiGLU expert FFN over the experts of one layer (hits from their
-// cache slots, transferred misses from their staging slots) and K5 the
-// gate-weighted combine (OLED-MoE Sec. 4.1: cache-hit experts execute on the
+// cache slots, transferred misses from their staging slots), the transfer of
+// the misses, and K5 the gate-weighted combine (OLED-MoE Sec. 4.1: cache-hit experts execute on the
 // GPU; the output does not depend on where an expert's weights came from).
 //
 // The GEMMs are weight-streaming: a layer iteration routes few tokens to each
@@ -19,13 +19,18 @@
 // contiguous range of its expert's block.
 // MFMA: v_mfma_f32_16x16x32_bf16 (bf16) or v_mfma_f32_16x16x4_f32 (fp32).
 //
-// One tile per workgroup over a grid sized for every possible tile; tiles past
-// the live count exit at once, and the hardware dispatcher balances the rest
-// over the CUs. Workgroup b runs on XCD b % 8; tiles are renumbered so that
-// each XCD takes a contiguous range (consecutive feature tiles of the same
-// expert share its token rows in that XCD's L2). The number of items can come
-// from device memory, so the hit experts can be launched before the host has
-// seen the routing result.
+// One tile per workgroup over a grid sized for every possible tile (capped;
+// workgroups then loop over tiles); tiles past the live count exit at once,
+// and the hardware dispatcher balances the rest over the CUs. Workgroup b runs
+// on XCD b % 8; tiles are renumbered so that each XCD takes a contiguous range
+// (consecutive feature tiles of the same expert share its token rows in that
+// XCD's L2). The number of items comes from device memory, so the launches
+// are enqueued before the host has seen the routing result.
+//
+// A launch may also carry the host-to-device transfer of the layer's misses
+// (Sec. 4.2, every miss is transferred): its first workgroups copy a byte
+// range of each staged expert's pinned host block into the expert's staging
+// slot over PCIe while the other workgroups compute the hit experts' tiles.
 //
 // Results for an expert depend only on its own rows, never on the other
 // experts of the launch, so hit and miss launches give identical bits.
@@ -256,32 +261,88 @@ __device__ __forceinline__ void run_tile(const WorkItem& it, int tile_f0, const 
   }
 }
 
+// Copies bytes [off, off + len) of every staged expert's host block into its
+// slot: workgroup b of nblk takes 16-byte vectors b*256 + tid + m*nblk*256,
+// four loads in flight per thread. The loads cross PCIe; the stores bypass
+// the caches.
+__device__ __forceinline__ void fetch_blocks(const FetchArgs& f, char* pool, int64_t slot_bytes,
+                                             int n_slots, int b) {
+  const int n = min(f.hdr->staged_n, kMaxExperts);
+  if (n <= 0) return;
+  const int64_t per = f.len >> 4;
+  const int64_t total = static_cast<int64_t>(n) * per;
+  const int64_t stride = static_cast<int64_t>(f.nblk) * kThreads;
+  for (int64_t i0 = static_cast<int64_t>(b) * kThreads + threadIdx.x; i0 < total; i0 += 4 * stride) {
+    u32x4_t v[4];
+    char* dst[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int64_t i = i0 + u * stride;
+      dst[u] = nullptr;
+      if (i < total) {
+        const int j = static_cast<int>(i / per);
+        const int64_t o = f.off + ((i - j * per) << 4);
+        const int slot = f.hdr->staged_slot[j];
+        const int e = f.hdr->staged_exp[j];
+        if (slot >= 0 && slot < n_slots && e >= 0 && e < f.E) {
+          v[u] = ldw16(reinterpret_cast<const char*>(f.host_addr[e]) + o);
+          dst[u] = pool + static_cast<int64_t>(slot) * slot_bytes + o;
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (dst[u]) __builtin_nontemporal_store(v[u], reinterpret_cast<u32x4_t*>(dst[u]));
+  }
+}
+
 template <class TR, bool UP, int KS>
-__global__ __launch_bounds__(kThreads) void k_ffn(
-    const char* __restrict__ pool, int64_t slot_bytes, SlotTable st,
-    const WorkItem* __restrict__ items, const int32_t* __restrict__ n_items_dev, int item_base,
-    int n_items_host, const typename TR::T* __restrict__ src, const int32_t* __restrict__ perm,
-    int k, int H, int I, typename TR::T* __restrict__ hout, float* __restrict__ oout) {
+__global__ __launch_bounds__(kThreads) void k_ffn(FfnLaunch a) {
   using T = typename TR::T;
   constexpr int FEAT = kFeat * (kWaves / KS);  // output features per tile
   __shared__ floatx4_t s_red[KS > 1 ? kWaves : 1][(UP ? 2 : 1) * kMaxNT][64];
 
-  const int n_items = n_items_host >= 0 ? n_items_host : *n_items_dev;
-  const int nf = (UP ? I : H) / FEAT;
-  const int total = n_items * nf;
-  const int t = blockIdx.x;  // one tile per workgroup; the grid covers every possible tile
-  if (t >= total) return;
-  const int v = xcd_order(t, total);
-  const int ii = v / nf;
-  const int f0 = (v - ii * nf) * FEAT;
-  const WorkItem it = items[item_base + ii];
-  const T* W = reinterpret_cast<const T*>(pool + static_cast<int64_t>(st.slot[it.expert]) * slot_bytes);
-  switch ((it.rows + 15) >> 4) {
-    case 1: run_tile<TR, UP, KS, 1>(it, f0, W, src, perm, k, H, I, hout, oout, s_red); break;
-    case 2: run_tile<TR, UP, KS, 2>(it, f0, W, src, perm, k, H, I, hout, oout, s_red); break;
-    case 3: run_tile<TR, UP, KS, 3>(it, f0, W, src, perm, k, H, I, hout, oout, s_red); break;
-    default: run_tile<TR, UP, KS, 4>(it, f0, W, src, perm, k, H, I, hout, oout, s_red); break;
+  const int nfetch = a.fetch.nblk;
+  if (static_cast<int>(blockIdx.x) < nfetch) {
+    fetch_blocks(a.fetch, static_cast<char*>(const_cast<void*>(a.pool)), a.slot_bytes, a.n_slots,
+                 blockIdx.x);
+    return;
   }
+  int base, n_items;
+  if (a.n_items_host >= 0) {
+    base = a.item_base;
+    n_items = a.n_items_host;
+  } else {
+    const int c0 = a.item_counts[0];
+    base = a.which ? c0 : 0;
+    n_items = a.which ? a.item_counts[1] : c0;
+  }
+  const int nf = (UP ? a.I : a.H) / FEAT;
+  const int total = n_items * nf;
+  const int stride = static_cast<int>(gridDim.x) - nfetch;  // a multiple of 8 (XCD count)
+  const T* src = static_cast<const T*>(a.src);
+  T* hout = static_cast<T*>(a.hout);
+  for (int t = static_cast<int>(blockIdx.x) - nfetch; t < total; t += stride) {
+    const int v = xcd_order(t, total);
+    const int ii = v / nf;
+    const int f0 = (v - ii * nf) * FEAT;
+    const WorkItem it = a.items[base + ii];
+    const int slot = a.slot_of[it.expert];
+    if (slot < 0 || slot >= a.n_slots) continue;  // no weights on the device (bad block)
+    const T* W = reinterpret_cast<const T*>(static_cast<const char*>(a.pool) +
+                                            static_cast<int64_t>(slot) * a.slot_bytes);
+    switch ((it.rows + 15) >> 4) {
+      case 1: run_tile<TR, UP, KS, 1>(it, f0, W, src, a.perm, a.k, a.H, a.I, hout, a.oout, s_red); break;
+      case 2: run_tile<TR, UP, KS, 2>(it, f0, W, src, a.perm, a.k, a.H, a.I, hout, a.oout, s_red); break;
+      case 3: run_tile<TR, UP, KS, 3>(it, f0, W, src, a.perm, a.k, a.H, a.I, hout, a.oout, s_red); break;
+      default: run_tile<TR, UP, KS, 4>(it, f0, W, src, a.perm, a.k, a.H, a.I, hout, a.oout, s_red); break;
+    }
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void k_fetch(char* pool, int64_t slot_bytes, int n_slots,
+                                                    FetchArgs f) {
+  fetch_blocks(f, pool, slot_bytes, n_slots, blockIdx.x);
 }
 
 // One thread per 4 consecutive outputs of a token; sums its k routes in slot
@@ -321,15 +382,15 @@ inline int k_split(int K) { return K >= 1024 ? 4 : (K >= 512 ? 2 : 1); }
 
 template <class TR, bool UP, int KS>
 hipError_t launch_ffn_ks(const FfnLaunch& a, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
-  auto kern = k_ffn<TR, UP, KS>;
+  if (a.fetch.nblk % 8) return hipErrorInvalidValue;
   const int nf = (UP ? a.I : a.H) / (kFeat * (kWaves / KS));
-  const int grid = a.max_items * nf;
+  int64_t tiles = static_cast<int64_t>(a.max_items) * nf;
+  if (a.max_grid > 0 && tiles > a.max_grid) tiles = a.max_grid;
+  tiles = (tiles + 7) & ~static_cast<int64_t>(7);
+  const int64_t grid = a.fetch.nblk + tiles;
   if (grid <= 0) return hipSuccess;
-  using T = typename TR::T;
-  hipExtLaunchKernelGGL(kern, dim3(grid), dim3(kThreads), 0, s, ev0, ev1, 0,
-                        static_cast<const char*>(a.pool), a.slot_bytes, *a.slots, a.items,
-                        a.n_items_dev, a.item_base, a.n_items_host, static_cast<const T*>(a.src),
-                        a.perm, a.k, a.H, a.I, static_cast<T*>(a.hout), a.oout);
+  hipExtLaunchKernelGGL(k_ffn<TR, UP, KS>, dim3(static_cast<unsigned>(grid)), dim3(kThreads), 0, s,
+                        ev0, ev1, 0, a);
   return hipGetLastError();
 }
 
@@ -353,6 +414,14 @@ hipError_t launch_ffn_down(bool bf16, const FfnLaunch& a, hipEvent_t ev0, hipEve
                            hipStream_t s) {
   return bf16 ? launch_ffn_t<TrBF16, false>(a, ev0, ev1, s)
               : launch_ffn_t<TrF32, false>(a, ev0, ev1, s);
+}
+
+hipError_t launch_fetch(const void* pool, int64_t slot_bytes, int n_slots, const FetchArgs& f,
+                        hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
+  if (f.nblk <= 0) return hipSuccess;
+  hipExtLaunchKernelGGL(k_fetch, dim3(f.nblk), dim3(kThreads), 0, s, ev0, ev1, 0,
+                        static_cast<char*>(const_cast<void*>(pool)), slot_bytes, n_slots, f);
+  return hipGetLastError();
 }
 
 hipError_t launch_combine(bool bf16, const float* O, const float* gates, const int32_t* inv_perm,

@@ -1,6 +1,6 @@
 // Launchers of the gfx950 kernels of the block-MoE layer, and the small
-// structs that travel between host and device (pinned summaries, kernel
-// argument tables). Internal to the library.
+// structs that travel between host and device (device-resident cache state,
+// pinned summaries, kernel argument tables). Internal to the library.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -11,38 +11,73 @@ namespace oled {
 
 constexpr int kMaxExperts = 256;
 constexpr int kMaxTopK = 16;
-constexpr int kItemRows = 64;   // routes (token rows) per grouped-GEMM work item
-constexpr int kScoreShift = 48; // priority numerators are floor(g * c * 2^48)
+constexpr int kItemRows = 64;    // routes (token rows) per grouped-GEMM work item
+constexpr int kScoreShift = 48;  // priority numerators are floor(g * c * 2^48)
+constexpr int kStatsRing = 4096; // routing records kept in pinned memory
 
-// Written by the permute kernel into coherent pinned host memory (seq last,
-// after a system-scope fence); the host polls seq.
-struct RouteSummary {
-  int32_t counts[kMaxExperts];
-  int32_t n_hit_items;
-  int32_t n_miss_items;
-  int32_t bad_logits;  // a non-finite router logit was seen
-  int32_t seq;         // call sequence number, for freshness checks
-};
-
-// Written by the score/retain kernel into coherent pinned host memory, one
-// per layer (seq last, after a system-scope fence).
-struct RetainOut {
-  uint32_t retained[kMaxExperts / 32];  // bit e: expert e stays cached
-  int32_t bad_conf;    // a confidence outside [0, 1] was seen
-  int32_t n_retained;
-  int32_t seq;
-  int32_t pad;
-};
-
-// Expert mask passed by value as a kernel argument.
+// Expert mask (one bit per expert).
 struct ExpertMask {
   uint32_t bits[kMaxExperts / 32];
   __host__ __device__ bool test(int e) const { return (bits[e >> 5] >> (e & 31)) & 1u; }
 };
 
-// Cache slot of every expert of the layer (-1: not on the device), by value.
-struct SlotTable {
+// Device-resident cache state of a layer stack. Only the routing kernel
+// (staging) and the retention kernel (commit) change it, both on the compute
+// stream, so every layer sees the previous layer's result in stream order.
+struct CacheHdr {
+  int32_t free_top;    // free slots: free_list[0, free_top)
+  int32_t staged_n;    // misses of the layer in flight, each given a free slot
+  int32_t route_bad;   // the layer in flight staged nothing and commits nothing
+  int32_t fault;       // sticky: 1 no free slot for a miss, 2 free list overflow,
+                       // 4 retained expert without a slot
+  int32_t staged_exp[kMaxExperts];
+  int32_t staged_slot[kMaxExperts];
+};
+
+struct CacheView {
+  CacheHdr* hdr;
+  int32_t* slot_of;        // [L][E] slot of a resident or staged expert, else -1
+  ExpertMask* res;         // [L] committed resident set R
+  ExpertMask* res_before;  // [L] R when the layer was last routed
+  int32_t* last_counts;    // [L][4] n_active, n_hits, n_misses, |R| of the last routing
+  int32_t* free_list;      // [n_slots]
+  int n_slots;
+};
+
+// One routing call, written by the permute stage into a pinned ring at
+// seq % kStatsRing (fields, system-scope fence, then seq).
+struct RouteStats {
+  int32_t layer;
+  int32_t n_active;
+  int32_t n_hits;
+  int32_t n_misses;
+  int32_t n_resident;
+  int32_t hit_rows;
+  int32_t miss_rows;
+  int32_t n_staged;
+  int32_t bad;         // non-finite logit, or no free slot: nothing staged
+  int32_t n_hit_items;
+  int32_t n_miss_items;
+  int32_t seq;
+};
+
+// Staged misses of the last routing call, for host-issued copies (written by
+// the permute stage when asked; seq last, after a system-scope fence).
+struct StagedList {
+  int32_t n;
+  int32_t exp[kMaxExperts];
   int32_t slot[kMaxExperts];
+  int32_t seq;
+};
+
+// Written by the retention kernel into coherent pinned host memory, one per
+// layer (seq last, after a system-scope fence).
+struct RetainOut {
+  uint32_t retained[kMaxExperts / 32];  // bit e: expert e stays cached
+  int32_t bad_conf;    // a confidence outside [0, 1] was seen: nothing changed
+  int32_t n_retained;
+  int32_t seq;
+  int32_t pad;
 };
 
 // One grouped-GEMM work item: rows [row_begin, row_begin + rows) of the
@@ -54,24 +89,40 @@ struct WorkItem {
   int32_t pad;
 };
 
-// Arguments of a grouped-GEMM launch over work items [item_base, item_base + n).
-// n = n_items_host if >= 0, else read from n_items_dev on the device (the
-// launch may then be enqueued before the host knows the routing result);
-// max_items bounds n and sizes the persistent grid.
+// Host-to-device transfer of the staged misses done by workgroups of a GEMM
+// launch: bytes [off, off + len) of every staged expert's host block into its
+// slot. Workgroups [0, nblk) of the launch copy; the GEMM tiles follow.
+struct FetchArgs {
+  const uint64_t* host_addr;  // [E] device-visible address of each expert's host block
+  const CacheHdr* hdr;        // staged list
+  int64_t off, len;
+  int nblk;
+  int E;
+};
+
+// Arguments of a grouped-GEMM launch. Work items: hits are items
+// [0, c0), misses [c0, c0 + c1) with (c0, c1) = item_counts on the device;
+// `which` selects them. With n_items_host >= 0 the host's (item_base,
+// n_items_host) are used instead. max_items bounds the count and sizes the
+// grid (capped at max_grid workgroups; tiles beyond are looped over).
 struct FfnLaunch {
   const void* pool;
   int64_t slot_bytes;
-  const SlotTable* slots;
+  const int32_t* slot_of;  // [E] of the layer
+  int n_slots;
   const WorkItem* items;
-  const int32_t* n_items_dev;
+  const int32_t* item_counts;
+  int which;
   int item_base;
   int n_items_host;
   int max_items;
+  int max_grid;
   const void* src;        // up: x [T][H]; down: h [T*k][I]
   const int32_t* perm;    // up: route of each sorted position (token = route / k)
   int k, H, I;
   void* hout;             // up: h [T*k][I]
   float* oout;            // down: O [T*k][H]
+  FetchArgs fetch;
 };
 
 // Every launcher takes optional (ev0, ev1): if non-null they record the
@@ -82,23 +133,32 @@ hipError_t launch_route_topk(const float* logits, int T, int E, int k, int32_t* 
                              float* gates, int32_t* bad_flag, hipEvent_t ev0, hipEvent_t ev1,
                              hipStream_t s);
 
-// K2: histogram, offsets, stable permutation, hit-first work list, item counts
-// (device: item_counts[0] hits, [1] misses) and the pinned host summary.
-hipError_t launch_permute(const int32_t* topk_idx, int T, int k, int E, const ExpertMask& resident,
-                          int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* inv_perm,
-                          WorkItem* items, int32_t* item_counts, int32_t* bad_flag,
-                          RouteSummary* summary, int seq, hipEvent_t ev0, hipEvent_t ev1,
-                          hipStream_t s);
+// Outputs of the permute stage for one layer.
+struct PermuteOut {
+  int32_t* counts;
+  int32_t* offsets;
+  int32_t* perm;
+  int32_t* inv_perm;
+  WorkItem* items;
+  int32_t* item_counts;   // [2] hit items, miss items
+  RouteStats* ring;       // pinned
+  StagedList* staged;     // pinned, or null
+  int layer, E, seq;
+  CacheView cv;
+};
+
+// K2: histogram, offsets, stable permutation, hit-first work list, and the
+// staging of the misses into free slots (device cache state).
+hipError_t launch_permute(const int32_t* topk_idx, int T, int k, int32_t* bad_flag,
+                          const PermuteOut& o, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s);
 
 // K1+K2 as one launch for blocks with T*k <= 1024 (route_fused true): the
 // last workgroup to finish routing permutes. sync: 2 device ints, zero
 // before the first launch; the kernel leaves them zero.
 bool route_fused(int T, int k);
-hipError_t launch_route_fused(const float* logits, int T, int E, int k, const ExpertMask& resident,
-                              int32_t* topk_idx, float* gates, int32_t* counts, int32_t* offsets,
-                              int32_t* perm, int32_t* inv_perm, WorkItem* items,
-                              int32_t* item_counts, int32_t* sync, RouteSummary* summary, int seq,
-                              hipEvent_t ev0, hipEvent_t ev1, hipStream_t s);
+hipError_t launch_route_fused(const float* logits, int T, int k, int32_t* topk_idx, float* gates,
+                              int32_t* sync, const PermuteOut& o, hipEvent_t ev0, hipEvent_t ev1,
+                              hipStream_t s);
 
 // K4a: grouped gate/up GEMM with SiLU*up epilogue (h = silu(W1 x) * (W3 x)).
 hipError_t launch_ffn_up(bool bf16, const FfnLaunch& a, hipEvent_t ev0, hipEvent_t ev1,
@@ -108,15 +168,20 @@ hipError_t launch_ffn_up(bool bf16, const FfnLaunch& a, hipEvent_t ev0, hipEvent
 hipError_t launch_ffn_down(bool bf16, const FfnLaunch& a, hipEvent_t ev0, hipEvent_t ev1,
                            hipStream_t s);
 
+// Transfer of the staged misses alone (no GEMM tiles).
+hipError_t launch_fetch(const void* pool, int64_t slot_bytes, int n_slots, const FetchArgs& f,
+                        hipEvent_t ev0, hipEvent_t ev1, hipStream_t s);
+
 // K5: y[t] = sum_j gate[t][j] * O[inv_perm[t*k + j]], fp32, rounded once to dtype.
 hipError_t launch_combine(bool bf16, const float* O, const float* gates, const int32_t* inv_perm,
                           int T, int k, int H, void* y, hipEvent_t ev0, hipEvent_t ev1,
                           hipStream_t s);
 
-// K6: priority numerators (per-expert segment sums) + Top-C retention.
+// K6: priority numerators (per-expert segment sums), Top-C retention and the
+// commit into the device cache state.
 hipError_t launch_score_retain(const float* gates, const float* conf, const int32_t* topk_idx,
-                               const int32_t* counts, int T, int k, int E, int C,
-                               const ExpertMask& resident, uint64_t* score_out, RetainOut* out,
-                               int seq, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s);
+                               const int32_t* counts, int T, int k, int E, int C, int layer,
+                               const CacheView& cv, uint64_t* score_out, RetainOut* out, int seq,
+                               hipEvent_t ev0, hipEvent_t ev1, hipStream_t s);
 
 }  // namespace oled

@@ -1,15 +1,21 @@
 // Host runtime of the C ABI declared in include/oled.h: the context, the call
-// state machine, the per-layer cache bookkeeping, the host-to-device miss
-// copies on a side stream and the kernel launches.
+// state machine, the device-resident cache state, the transfer of the misses
+// and the kernel launches.
 //
-// Per layer: route_block enqueues the gate kernels; moe_forward_cached
-// enqueues the hit experts at once (their work list and count stay on the
-// device); apply_misses is the one host synchronisation of the layer - it
-// polls the routing summary the permute kernel publishes in coherent pinned
-// memory, commits earlier retentions, stages and copies the misses and
-// enqueues their GEMMs behind the copies, then the combine; score_and_retain
-// enqueues the priority/retention kernel, whose result is committed at the
-// next synchronising call.
+// The cache state of every layer (resident sets, slot tables, the free-slot
+// list, the staged misses of the layer in flight) lives in device memory and
+// only kernels change it: the routing kernel stages the misses into free
+// slots, the retention kernel commits. With the default shader transfer a
+// layer needs no host synchronisation at all: route_block enqueues the
+// routing kernel; moe_forward_cached the hit experts' gate/up and down GEMMs,
+// whose first workgroups copy the staged misses' weights from the pinned host
+// pool over PCIe meanwhile; apply_misses the misses' GEMMs and the combine;
+// score_and_retain the priority / retention / commit kernel. The host reads
+// the pinned routing records when a caller asks for counts.
+//
+// With the copy-engine transfer (OLED_COPY_SDMA) apply_misses waits for the
+// routing record, copies the staged misses with hipMemcpyAsync on a side
+// stream and launches their GEMMs once the host has seen the copies land.
 #include "oled.h"
 
 #include <hip/hip_runtime.h>
@@ -23,35 +29,46 @@
 #include <string>
 #include <vector>
 
-#include "cache_state.h"
 #include "kernels.h"
 
 namespace {
 
+using oled::CacheHdr;
+using oled::CacheView;
 using oled::ExpertMask;
+using oled::FetchArgs;
 using oled::FfnLaunch;
+using oled::PermuteOut;
 using oled::RetainOut;
-using oled::RouteSummary;
-using oled::SlotTable;
+using oled::RouteStats;
+using oled::StagedList;
 using oled::WorkItem;
 
 thread_local std::string g_create_error;
+
+constexpr int kFetchBlocks = 64;    // workgroups of a launch that copy misses (multiple of 8)
+constexpr int kMissGridCap = 1024;  // GEMM workgroups of a miss launch (they loop over tiles)
 
 enum class Stage { kIdle, kRouted, kHitsQueued, kApplied };
 
 struct OpRec {
   int kind, layer;
-  int64_t bytes, flops;
+  int route_seq;          // routing record that completes the accounting (0: complete)
+  int part;               // 0 gate/up, 1 down, -1 other
+  bool hits;              // hit-expert launch (else miss launch)
+  int64_t bytes, flops, h2d;
   hipEvent_t a, b;
 };
 
 struct Ctx {
   // shape
   int H = 0, I = 0, E = 0, K = 0, L = 0, C = 0, Tmax = 0, dtype = 0, esz = 0, device = 0;
+  int copy_mode = OLED_COPY_SHADER;
   uint32_t profile_ops = 0;
   int64_t eb = 0;    // bytes of one expert block
-  int64_t e13 = 0;   // bytes of its w13 part
+  int64_t e13 = 0;   // bytes of its gate/up part
   int n_slots = 0;
+  int cap = 0;       // min(C, E)
   int max_items = 0;
   const char* host_pool = nullptr;
   int64_t P = 0;
@@ -66,38 +83,48 @@ struct Ctx {
   int32_t* d_inv = nullptr;
   int32_t* d_flag = nullptr;
   int32_t* d_item_counts = nullptr;
-  int32_t* d_sync = nullptr;       // completion counter + bad-logit flag of the routing launch
+  int32_t* d_sync = nullptr;       // completion counter + bad-logit flag of the fused routing
   WorkItem* d_items = nullptr;
   void* d_h = nullptr;
   float* d_O = nullptr;
-  uint64_t* d_score = nullptr;  // [L][E]
+  uint64_t* d_score = nullptr;     // [L][E]
+  // device-resident cache state
+  CacheHdr* d_hdr = nullptr;
+  int32_t* d_slot_of = nullptr;    // [L][E]
+  ExpertMask* d_res = nullptr;     // [L]
+  ExpertMask* d_res_before = nullptr;
+  int32_t* d_last_counts = nullptr;  // [L][4]
+  int32_t* d_free = nullptr;       // [n_slots]
+  uint64_t* d_host_addr = nullptr; // [L][E]
   // coherent pinned host memory written by kernels
-  RouteSummary* h_sum = nullptr;
-  RetainOut* h_ret = nullptr;   // [L]
+  RouteStats* h_ring = nullptr;    // [kStatsRing]
+  StagedList* h_staged = nullptr;
+  RetainOut* h_ret = nullptr;      // [L]
   // streams and events
   hipStream_t own_copy = nullptr;
   hipEvent_t ev_up = nullptr, ev_down = nullptr, ev_order = nullptr;
-  // cache state
-  oled::CacheState cs;
-  std::vector<uint8_t> pending;     // [L] retention result not yet committed
-  std::vector<int> ret_seq;         // [L] sequence number of that result
-  std::vector<hipStream_t> ret_stream;
-  std::vector<uint8_t> rejected;    // [L] last retention rejected (bad confidence)
-  std::vector<uint8_t> res_before;  // [L][E] R before the layer's last execution
-  std::vector<int> last_counts;     // [L][3] n_active, n_hits, n_misses of the last apply
+  // routing records consumed by the host
+  int route_n = 0;                 // sequence number of the last routing call
+  int next_stat = 1;               // first record not yet consumed
+  std::vector<RouteStats> recs;    // consumed records kept for the profile accounting
+  oled_stats acc{};                // accumulated since the last oled_collect_stats
+  int bad_route_layer = -1;        // a bad block seen in a record, not yet reported
+  // retention results
+  int seq = 0;
+  std::vector<int> ret_seq;        // [L] sequence number of the last retention (0: none)
+  std::vector<uint8_t> ret_seen;   // [L] that result has been read
+  std::vector<uint8_t> rejected;   // [L] the last retention read was rejected
+  int rejected_layer = -1;         // reported by the next report
   // the layer in flight
   Stage stage = Stage::kIdle;
-  int cur_layer = -1, cur_T = 0, cur_res = 0;
+  int cur_layer = -1, cur_T = 0, cur_route = 0;
   hipStream_t cur_stream = nullptr;
   bool have_stream = false;
   const void* fwd_x = nullptr;
   void* fwd_y = nullptr;
   int last_routed_layer = -1, last_routed_T = 0;
-  std::vector<int32_t> counts;      // [E] route counts of the layer in flight
-  std::vector<uint8_t> hit, miss;
   bool copies_outstanding = false;
-  int seq = 0, route_seq = 0;
-  int rejected_layer = -1;          // reported by the next apply_misses
+  bool broken = false;             // a HIP failure left the device state unknown
   std::string err;
   // profiling
   std::vector<OpRec> ops;
@@ -115,6 +142,7 @@ oled_status fail(Ctx* c, oled_status st, const char* fmt, ...) {
 }
 
 oled_status hip_fail(Ctx* c, hipError_t e, const char* what) {
+  c->broken = true;
   return fail(c, OLED_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
@@ -154,19 +182,24 @@ OpEvents op_begin(Ctx* c, int kind) {
   return ev;
 }
 
-void op_end(Ctx* c, const OpEvents& ev, int kind, int layer, int64_t bytes, int64_t flops) {
-  if (ev.a) c->ops.push_back(OpRec{kind, layer, bytes, flops, ev.a, ev.b});
+void op_end(Ctx* c, const OpEvents& ev, OpRec r) {
+  if (!ev.a) return;
+  r.a = ev.a;
+  r.b = ev.b;
+  c->ops.push_back(r);
 }
 
-ExpertMask mask_of(const uint8_t* m, int E) {
-  ExpertMask x;
-  std::memset(&x, 0, sizeof(x));
-  for (int e = 0; e < E; ++e)
-    if (m[e]) x.bits[e >> 5] |= 1u << (e & 31);
-  return x;
+OpRec rec(int kind, int layer, int64_t bytes, int64_t flops = 0) {
+  OpRec r{};
+  r.kind = kind;
+  r.layer = layer;
+  r.part = -1;
+  r.bytes = bytes;
+  r.flops = flops;
+  return r;
 }
 
-// Waits until a kernel has published `want` into *flag (coherent pinned
+// Spins until a kernel has published `want` into *flag (coherent pinned
 // memory). Checks the stream now and then so a failed launch cannot hang.
 oled_status wait_published(Ctx* c, const int32_t* flag, int want, hipStream_t s, const char* what) {
   const volatile int32_t* p = flag;
@@ -203,77 +236,121 @@ oled_status wait_event_spin(Ctx* c, hipEvent_t ev, const char* what) {
   }
 }
 
-// Commits the retention result of layer l.
-oled_status consume_layer(Ctx* c, int l) {
-  if (!c->pending[l]) return OLED_OK;
-  oled_status st = wait_published(c, &c->h_ret[l].seq, c->ret_seq[l], c->ret_stream[l], "retention");
-  c->pending[l] = 0;
-  if (st != OLED_OK) {
-    c->cs.drop_staged(l);
-    return st;
-  }
-  const RetainOut& o = c->h_ret[l];
-  if (o.bad_conf) {
-    c->cs.drop_staged(l);
-    c->rejected[l] = 1;
-    c->rejected_layer = l;
-    return fail(c, OLED_ERR_INVALID_ARG, "confidence outside [0,1] at layer %d: retention skipped", l);
-  }
-  c->rejected[l] = 0;
-  uint8_t keep[oled::kMaxExperts];
-  for (int e = 0; e < c->E; ++e) keep[e] = (o.retained[e >> 5] >> (e & 31)) & 1u;
-  if (!c->cs.commit(l, keep)) {
-    c->cs.drop_staged(l);
-    return fail(c, OLED_ERR_HIP, "inconsistent retention result for layer %d", l);
+// Consumes routing records in order: all that are already published, and
+// every record up to `until`, waiting for those.
+oled_status drain_records(Ctx* c, int until) {
+  while (c->next_stat <= c->route_n) {
+    const RouteStats& r = c->h_ring[c->next_stat % oled::kStatsRing];
+    const volatile int32_t* ps = &r.seq;
+    if (*ps != c->next_stat) {
+      if (c->next_stat > until) return OLED_OK;
+      const oled_status st = wait_published(c, &r.seq, c->next_stat, c->cur_stream, "routing record");
+      if (st != OLED_OK) return st;
+    }
+    std::atomic_thread_fence(std::memory_order_acquire);
+    RouteStats v = r;
+    v.seq = c->next_stat;
+    c->acc.layer_iters += 1;
+    c->acc.n_active += v.n_active;
+    c->acc.n_hits += v.n_hits;
+    c->acc.n_misses += v.n_misses;
+    c->acc.n_transferred += v.n_staged;
+    c->acc.h2d_bytes += static_cast<int64_t>(v.n_staged) * c->eb;
+    if (v.bad) {
+      c->acc.n_bad_blocks += 1;
+      c->bad_route_layer = v.layer;
+    }
+    if (c->profile_ops) c->recs.push_back(v);
+    ++c->next_stat;
   }
   return OLED_OK;
 }
 
-oled_status consume_all(Ctx* c) {
-  oled_status worst = OLED_OK;
+const RouteStats* find_record(const Ctx* c, int seq) {
+  for (auto it = c->recs.rbegin(); it != c->recs.rend(); ++it)
+    if (it->seq == seq) return &*it;
+  return nullptr;
+}
+
+// Reads the retention results that have been published (every retention
+// enqueued before a published routing record, or before a synchronisation).
+void read_retentions(Ctx* c) {
   for (int l = 0; l < c->L; ++l) {
-    const oled_status st = consume_layer(c, l);
-    if (st == OLED_ERR_HIP) return st;
-    if (st != OLED_OK) worst = st;
+    if (c->ret_seq[l] == 0 || c->ret_seen[l]) continue;
+    const volatile int32_t* ps = &c->h_ret[l].seq;
+    if (*ps != c->ret_seq[l]) continue;
+    std::atomic_thread_fence(std::memory_order_acquire);
+    c->ret_seen[l] = 1;
+    if (c->h_ret[l].bad_conf) {
+      c->rejected[l] = 1;
+      c->rejected_layer = l;
+    } else {
+      c->rejected[l] = 0;
+    }
   }
-  return worst;
 }
 
 void free_ctx(Ctx* c) {
   if (!c) return;
-  hipSetDevice(c->device);
-  hipDeviceSynchronize();
+  (void)hipSetDevice(c->device);
+  (void)hipDeviceSynchronize();
   for (auto& op : c->ops) {
-    hipEventDestroy(op.a);
-    hipEventDestroy(op.b);
+    (void)hipEventDestroy(op.a);
+    (void)hipEventDestroy(op.b);
   }
-  for (auto e : c->ev_free) hipEventDestroy(e);
-  if (c->ev_up) hipEventDestroy(c->ev_up);
-  if (c->ev_down) hipEventDestroy(c->ev_down);
-  if (c->ev_order) hipEventDestroy(c->ev_order);
-  if (c->own_copy) hipStreamDestroy(c->own_copy);
-  hipFree(c->d_pool);
-  hipFree(c->d_topk);
-  hipFree(c->d_gates);
-  hipFree(c->d_counts);
-  hipFree(c->d_offsets);
-  hipFree(c->d_perm);
-  hipFree(c->d_inv);
-  hipFree(c->d_flag);
-  hipFree(c->d_item_counts);
-  hipFree(c->d_sync);
-  hipFree(c->d_items);
-  hipFree(c->d_h);
-  hipFree(c->d_O);
-  hipFree(c->d_score);
-  if (c->h_sum) hipHostFree(c->h_sum);
-  if (c->h_ret) hipHostFree(c->h_ret);
+  for (auto e : c->ev_free) (void)hipEventDestroy(e);
+  if (c->ev_up) (void)hipEventDestroy(c->ev_up);
+  if (c->ev_down) (void)hipEventDestroy(c->ev_down);
+  if (c->ev_order) (void)hipEventDestroy(c->ev_order);
+  if (c->own_copy) (void)hipStreamDestroy(c->own_copy);
+  void* dev[] = {c->d_pool, c->d_topk, c->d_gates, c->d_counts, c->d_offsets, c->d_perm,
+                 c->d_inv, c->d_flag, c->d_item_counts, c->d_sync, c->d_items, c->d_h, c->d_O,
+                 c->d_score, c->d_hdr, c->d_slot_of, c->d_res, c->d_res_before,
+                 c->d_last_counts, c->d_free, c->d_host_addr};
+  for (void* p : dev)
+    if (p) (void)hipFree(p);
+  if (c->h_ring) (void)hipHostFree(c->h_ring);
+  if (c->h_staged) (void)hipHostFree(c->h_staged);
+  if (c->h_ret) (void)hipHostFree(c->h_ret);
   delete c;
 }
 
 template <class T>
 hipError_t dev_alloc(T** p, size_t n) {
   return hipMalloc(reinterpret_cast<void**>(p), n * sizeof(T) > 0 ? n * sizeof(T) : 16);
+}
+
+// Empty caches: every slot free, no expert resident or staged.
+oled_status init_cache_state(Ctx* c) {
+  CacheHdr hdr;
+  std::memset(&hdr, 0, sizeof(hdr));
+  hdr.free_top = c->n_slots;
+  std::vector<int32_t> free_list(c->n_slots);
+  for (int i = 0; i < c->n_slots; ++i) free_list[i] = c->n_slots - 1 - i;  // slot 0 taken first
+  std::vector<int32_t> slots(static_cast<size_t>(c->L) * c->E, -1);
+  HIP_TRY(c, hipMemcpy(c->d_hdr, &hdr, sizeof(hdr), hipMemcpyHostToDevice));
+  HIP_TRY(c, hipMemcpy(c->d_free, free_list.data(), sizeof(int32_t) * c->n_slots,
+                       hipMemcpyHostToDevice));
+  HIP_TRY(c, hipMemcpy(c->d_slot_of, slots.data(), sizeof(int32_t) * slots.size(),
+                       hipMemcpyHostToDevice));
+  HIP_TRY(c, hipMemset(c->d_res, 0, sizeof(ExpertMask) * c->L));
+  HIP_TRY(c, hipMemset(c->d_res_before, 0, sizeof(ExpertMask) * c->L));
+  HIP_TRY(c, hipMemset(c->d_last_counts, 0, sizeof(int32_t) * 4 * c->L));
+  HIP_TRY(c, hipMemset(c->d_score, 0, sizeof(uint64_t) * c->L * c->E));
+  HIP_TRY(c, hipDeviceSynchronize());
+  return OLED_OK;
+}
+
+CacheView view(const Ctx* c) {
+  CacheView v;
+  v.hdr = c->d_hdr;
+  v.slot_of = c->d_slot_of;
+  v.res = c->d_res;
+  v.res_before = c->d_res_before;
+  v.last_counts = c->d_last_counts;
+  v.free_list = c->d_free;
+  v.n_slots = c->n_slots;
+  return v;
 }
 
 oled_status check_layer(Ctx* c, int layer) {
@@ -291,23 +368,30 @@ oled_status check_in_flight(Ctx* c, int layer, hipStream_t s, const char* call) 
   return OLED_OK;
 }
 
-FfnLaunch ffn_args(Ctx* c, const SlotTable* tab, int base, int n_host, int max_items) {
+FfnLaunch ffn_args(Ctx* c, int layer, int which, int max_items, int max_grid) {
   FfnLaunch a;
+  std::memset(&a, 0, sizeof(a));
   a.pool = c->d_pool;
   a.slot_bytes = c->eb;
-  a.slots = tab;
+  a.slot_of = c->d_slot_of + static_cast<size_t>(layer) * c->E;
+  a.n_slots = c->n_slots;
   a.items = c->d_items;
-  a.n_items_dev = c->d_item_counts;
-  a.item_base = base;
-  a.n_items_host = n_host;
+  a.item_counts = c->d_item_counts;
+  a.which = which;
+  a.item_base = 0;
+  a.n_items_host = -1;
   a.max_items = max_items;
-  a.src = nullptr;
+  a.max_grid = max_grid;
   a.perm = c->d_perm;
   a.k = c->K;
   a.H = c->H;
   a.I = c->I;
   a.hout = c->d_h;
   a.oout = c->d_O;
+  a.fetch.host_addr = c->d_host_addr + static_cast<size_t>(layer) * c->E;
+  a.fetch.hdr = c->d_hdr;
+  a.fetch.nblk = 0;
+  a.fetch.E = c->E;
   return a;
 }
 
@@ -319,6 +403,27 @@ int64_t down_bytes(const Ctx* c, int64_t n_exp, int64_t rows) {
 }
 int64_t up_flops(const Ctx* c, int64_t rows) { return rows * 4 * static_cast<int64_t>(c->H) * c->I; }
 int64_t down_flops(const Ctx* c, int64_t rows) { return rows * 2 * static_cast<int64_t>(c->H) * c->I; }
+
+// Completes the byte / flop accounting of a launch from its routing record.
+void complete_op(const Ctx* c, OpRec& op, const RouteStats& r) {
+  if (op.kind == OLED_OP_H2D) {  // transfer-only launch (no GEMM tiles)
+    op.bytes = static_cast<int64_t>(r.n_staged) * c->eb;
+    op.h2d = op.bytes;
+    op.flops = 0;
+    return;
+  }
+  const int64_t n = op.hits ? r.n_hits : r.n_misses;
+  const int64_t rows = op.hits ? r.hit_rows : r.miss_rows;
+  if (op.part == 0) {
+    op.bytes = up_bytes(c, n, rows);
+    op.flops = up_flops(c, rows);
+    if (op.h2d < 0) op.h2d = static_cast<int64_t>(r.n_staged) * c->e13;
+  } else {
+    op.bytes = down_bytes(c, n, rows);
+    op.flops = down_flops(c, rows);
+    if (op.h2d < 0) op.h2d = static_cast<int64_t>(r.n_staged) * (c->eb - c->e13);
+  }
+}
 
 // Expert block packing (see oled_pack_expert): fragment f holds 16 rows x SPAN
 // columns, element l*V + i <- (row 16q + l%16, column SPAN*s + V*(l/16) + i).
@@ -349,6 +454,46 @@ void pack_expert_t(int H, int I, const T* w13, const T* w2, T* out) {
     }
 }
 
+// Slot conservation over the device cache state (no layer in flight): every
+// slot is free or held by exactly one resident expert, and no layer holds
+// more than C experts.
+oled_status check_slots(Ctx* c) {
+  CacheHdr hdr;
+  std::vector<int32_t> slots(static_cast<size_t>(c->L) * c->E), free_list(c->n_slots);
+  std::vector<ExpertMask> res(c->L);
+  HIP_TRY(c, hipMemcpy(&hdr, c->d_hdr, sizeof(hdr), hipMemcpyDeviceToHost));
+  HIP_TRY(c, hipMemcpy(slots.data(), c->d_slot_of, sizeof(int32_t) * slots.size(),
+                       hipMemcpyDeviceToHost));
+  HIP_TRY(c, hipMemcpy(free_list.data(), c->d_free, sizeof(int32_t) * c->n_slots,
+                       hipMemcpyDeviceToHost));
+  HIP_TRY(c, hipMemcpy(res.data(), c->d_res, sizeof(ExpertMask) * c->L, hipMemcpyDeviceToHost));
+  if (hdr.fault) return fail(c, OLED_ERR_HIP, "device cache state fault %d", hdr.fault);
+  if (hdr.free_top < 0 || hdr.free_top > c->n_slots)
+    return fail(c, OLED_ERR_HIP, "free list top %d outside [0,%d]", hdr.free_top, c->n_slots);
+  std::vector<int> owner(c->n_slots, 0);
+  for (int i = 0; i < hdr.free_top; ++i) {
+    const int s = free_list[i];
+    if (s < 0 || s >= c->n_slots || owner[s]++)
+      return fail(c, OLED_ERR_HIP, "free slot %d listed twice or out of range", s);
+  }
+  for (int l = 0; l < c->L; ++l) {
+    int n_res = 0;
+    for (int e = 0; e < c->E; ++e) {
+      const int s = slots[static_cast<size_t>(l) * c->E + e];
+      const bool r = res[l].test(e);
+      n_res += r;
+      if (r != (s >= 0))
+        return fail(c, OLED_ERR_HIP, "expert %d of layer %d: resident %d but slot %d", e, l, r, s);
+      if (s < 0) continue;
+      if (s >= c->n_slots || owner[s]++) return fail(c, OLED_ERR_HIP, "slot %d held twice", s);
+    }
+    if (n_res > c->cap) return fail(c, OLED_ERR_HIP, "layer %d holds %d > C experts", l, n_res);
+  }
+  for (int s = 0; s < c->n_slots; ++s)
+    if (!owner[s]) return fail(c, OLED_ERR_HIP, "slot %d lost", s);
+  return OLED_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -365,6 +510,8 @@ oled_status oled_create(const oled_config* cfg, void** ctx_out) {
     return bad(OLED_ERR_INVALID_ARG, "non-positive shape field");
   if (cfg->dtype != OLED_F32 && cfg->dtype != OLED_BF16)
     return bad(OLED_ERR_INVALID_ARG, "dtype must be OLED_F32 or OLED_BF16");
+  if (cfg->copy_mode != OLED_COPY_SHADER && cfg->copy_mode != OLED_COPY_SDMA)
+    return bad(OLED_ERR_INVALID_ARG, "copy_mode must be OLED_COPY_SHADER or OLED_COPY_SDMA");
   if (cfg->top_k > cfg->n_experts) return bad(OLED_ERR_INVALID_ARG, "top_k > n_experts");
   if (cfg->hidden % 128 || cfg->inter % 128)
     return bad(OLED_ERR_UNSUPPORTED, "hidden and inter must be multiples of 128");
@@ -390,6 +537,13 @@ oled_status oled_create(const oled_config* cfg, void** ctx_out) {
     (void)hipGetLastError();
     return bad(OLED_ERR_INVALID_ARG, "host_pool is not pinned host memory");
   }
+  // the address kernels use to read the pool (same allocation, device view)
+  void* dev_view = nullptr;
+  if (hipHostGetDevicePointer(&dev_view, const_cast<void*>(cfg->host_pool), 0) != hipSuccess ||
+      !dev_view) {
+    (void)hipGetLastError();
+    return bad(OLED_ERR_INVALID_ARG, "host_pool is not mapped for device access");
+  }
 
   Ctx* c = new Ctx();
   c->H = cfg->hidden;
@@ -400,15 +554,16 @@ oled_status oled_create(const oled_config* cfg, void** ctx_out) {
   c->C = cfg->capacity;
   c->Tmax = cfg->max_tokens;
   c->dtype = cfg->dtype;
+  c->copy_mode = cfg->copy_mode;
   c->esz = cfg->dtype == OLED_F32 ? 4 : 2;
   c->device = cfg->device;
   c->profile_ops = static_cast<uint32_t>(cfg->profile_ops);
   c->eb = static_cast<int64_t>(3) * c->H * c->I * c->esz;
   c->e13 = static_cast<int64_t>(2) * c->H * c->I * c->esz;
-  const int cap = c->C < c->E ? c->C : c->E;
+  c->cap = c->C < c->E ? c->C : c->E;
   const int64_t routes = static_cast<int64_t>(c->Tmax) * c->K;
   const int staging = routes < c->E ? static_cast<int>(routes) : c->E;
-  c->n_slots = c->L * cap + staging;
+  c->n_slots = c->L * c->cap + staging;
   c->max_items = static_cast<int>(routes / oled::kItemRows) + c->E + 1;
   c->host_pool = static_cast<const char*>(cfg->host_pool);
   c->P = cfg->host_pool_blocks;
@@ -432,15 +587,30 @@ oled_status oled_create(const oled_config* cfg, void** ctx_out) {
       dev_alloc(&c->d_O, routes * c->H) ||
       dev_alloc(&c->d_score, static_cast<size_t>(c->L) * c->E))
     return oom("routing scratch");
+  if (dev_alloc(&c->d_hdr, 1) || dev_alloc(&c->d_slot_of, nb) || dev_alloc(&c->d_res, c->L) ||
+      dev_alloc(&c->d_res_before, c->L) || dev_alloc(&c->d_last_counts, 4 * c->L) ||
+      dev_alloc(&c->d_free, c->n_slots) || dev_alloc(&c->d_host_addr, nb))
+    return oom("cache state");
   if (hipMemset(c->d_flag, 0, sizeof(int32_t)) != hipSuccess ||
       hipMemset(c->d_item_counts, 0, 2 * sizeof(int32_t)) != hipSuccess ||
-      hipMemset(c->d_sync, 0, 2 * sizeof(int32_t)) != hipSuccess ||
-      hipMemset(c->d_score, 0, sizeof(uint64_t) * c->L * c->E) != hipSuccess)
+      hipMemset(c->d_sync, 0, 2 * sizeof(int32_t)) != hipSuccess)
     return oom("scratch init");
-  if (hipHostMalloc(reinterpret_cast<void**>(&c->h_sum), sizeof(RouteSummary), hipHostMallocCoherent) ||
+  {
+    std::vector<uint64_t> addr(nb);
+    for (int64_t i = 0; i < nb; ++i)
+      addr[i] = reinterpret_cast<uint64_t>(dev_view) +
+                static_cast<uint64_t>(c->host_block_of[i]) * static_cast<uint64_t>(c->eb);
+    if (hipMemcpy(c->d_host_addr, addr.data(), sizeof(uint64_t) * nb, hipMemcpyHostToDevice) !=
+        hipSuccess)
+      return oom("host block table");
+  }
+  if (hipHostMalloc(reinterpret_cast<void**>(&c->h_ring), sizeof(RouteStats) * oled::kStatsRing,
+                    hipHostMallocCoherent) ||
+      hipHostMalloc(reinterpret_cast<void**>(&c->h_staged), sizeof(StagedList), hipHostMallocCoherent) ||
       hipHostMalloc(reinterpret_cast<void**>(&c->h_ret), sizeof(RetainOut) * c->L, hipHostMallocCoherent))
-    return oom("pinned summaries");
-  std::memset(c->h_sum, 0, sizeof(RouteSummary));
+    return oom("pinned records");
+  std::memset(c->h_ring, 0, sizeof(RouteStats) * oled::kStatsRing);
+  std::memset(c->h_staged, 0, sizeof(StagedList));
   std::memset(c->h_ret, 0, sizeof(RetainOut) * c->L);
   if (hipStreamCreateWithFlags(&c->own_copy, hipStreamNonBlocking) != hipSuccess ||
       hipEventCreateWithFlags(&c->ev_up, hipEventDisableTiming) != hipSuccess ||
@@ -450,18 +620,11 @@ oled_status oled_create(const oled_config* cfg, void** ctx_out) {
     free_ctx(c);
     return OLED_ERR_HIP;
   }
-  c->cs = oled::CacheState(c->L, c->E, c->C, c->n_slots);
-  c->pending.assign(c->L, 0);
   c->ret_seq.assign(c->L, 0);
-  c->ret_stream.assign(c->L, nullptr);
+  c->ret_seen.assign(c->L, 0);
   c->rejected.assign(c->L, 0);
-  c->res_before.assign(static_cast<size_t>(c->L) * c->E, 0);
-  c->last_counts.assign(static_cast<size_t>(c->L) * 3, 0);
-  c->counts.assign(c->E, 0);
-  c->hit.assign(c->E, 0);
-  c->miss.assign(c->E, 0);
-  if (hipDeviceSynchronize() != hipSuccess) {
-    g_create_error = "device synchronisation failed";
+  if (init_cache_state(c) != OLED_OK) {
+    g_create_error = c->err;
     free_ctx(c);
     return OLED_ERR_HIP;
   }
@@ -483,11 +646,16 @@ oled_status oled_reset_cache(void* ctx) {
   if (c->stage != Stage::kIdle) return fail(c, OLED_ERR_STATE, "reset while a layer is in flight");
   HIP_TRY(c, hipSetDevice(c->device));
   HIP_TRY(c, hipDeviceSynchronize());
-  std::fill(c->pending.begin(), c->pending.end(), 0);
-  c->cs.reset();
+  oled_status st = drain_records(c, c->route_n);
+  if (st != OLED_OK) return st;
+  st = init_cache_state(c);
+  if (st != OLED_OK) return st;
+  c->broken = false;
+  std::fill(c->ret_seq.begin(), c->ret_seq.end(), 0);
+  std::fill(c->ret_seen.begin(), c->ret_seen.end(), 0);
   std::fill(c->rejected.begin(), c->rejected.end(), 0);
-  std::fill(c->res_before.begin(), c->res_before.end(), 0);
   c->rejected_layer = -1;
+  c->bad_route_layer = -1;
   return OLED_OK;
 }
 
@@ -496,6 +664,9 @@ oled_status route_block(void* ctx, int32_t layer, const float* logits_dev, int32
   if (!c) return OLED_ERR_INVALID_ARG;
   oled_status st = check_layer(c, layer);
   if (st != OLED_OK) return st;
+  if (c->broken)
+    return fail(c, OLED_ERR_STATE, "an earlier HIP failure left the cache state unknown: "
+                                   "call oled_reset_cache");
   if (c->stage != Stage::kIdle)
     return fail(c, OLED_ERR_STATE, "route_block while layer %d is in flight", c->cur_layer);
   if (!logits_dev) return fail(c, OLED_ERR_INVALID_ARG, "NULL logits");
@@ -506,38 +677,47 @@ oled_status route_block(void* ctx, int32_t layer, const float* logits_dev, int32
     HIP_TRY(c, hipEventRecord(c->ev_order, c->cur_stream));
     HIP_TRY(c, hipStreamWaitEvent(s, c->ev_order, 0));
   }
-  if (c->pending[layer]) {  // the hit/miss split needs this layer's committed R
-    st = consume_layer(c, layer);
-    if (st == OLED_ERR_HIP) return st;
-  }
-  const ExpertMask res = mask_of(c->cs.resident(layer), c->E);
-  const int seq = ++c->seq;
+  // consume what has been published; this call's ring entry must be free
+  const int n = c->route_n + 1;
+  st = drain_records(c, n - oled::kStatsRing);
+  if (st != OLED_OK) return st;
+
+  PermuteOut o;
+  o.counts = c->d_counts;
+  o.offsets = c->d_offsets;
+  o.perm = c->d_perm;
+  o.inv_perm = c->d_inv;
+  o.items = c->d_items;
+  o.item_counts = c->d_item_counts;
+  o.ring = c->h_ring;
+  o.staged = c->copy_mode == OLED_COPY_SDMA ? c->h_staged : nullptr;
+  o.layer = layer;
+  o.E = c->E;
+  o.seq = n;
+  o.cv = view(c);
   const int64_t route_bytes = static_cast<int64_t>(T) * c->E * 4 + static_cast<int64_t>(T) * c->K * 8;
   const int64_t perm_bytes = static_cast<int64_t>(T) * c->K * 12 + static_cast<int64_t>(c->E) * 8;
   if (oled::route_fused(T, c->K)) {
     OpEvents ev = op_begin(c, OLED_OP_ROUTE_TOPK);
-    HIP_TRY(c, oled::launch_route_fused(logits_dev, T, c->E, c->K, res, c->d_topk, c->d_gates,
-                                        c->d_counts, c->d_offsets, c->d_perm, c->d_inv, c->d_items,
-                                        c->d_item_counts, c->d_sync, c->h_sum, seq, ev.a, ev.b, s));
-    op_end(c, ev, OLED_OP_ROUTE_TOPK, layer, route_bytes + perm_bytes, 0);
+    HIP_TRY(c, oled::launch_route_fused(logits_dev, T, c->K, c->d_topk, c->d_gates, c->d_sync, o,
+                                        ev.a, ev.b, s));
+    op_end(c, ev, rec(OLED_OP_ROUTE_TOPK, layer, route_bytes + perm_bytes));
   } else {
     {
       OpEvents ev = op_begin(c, OLED_OP_ROUTE_TOPK);
       HIP_TRY(c, oled::launch_route_topk(logits_dev, T, c->E, c->K, c->d_topk, c->d_gates,
                                          c->d_flag, ev.a, ev.b, s));
-      op_end(c, ev, OLED_OP_ROUTE_TOPK, layer, route_bytes, 0);
+      op_end(c, ev, rec(OLED_OP_ROUTE_TOPK, layer, route_bytes));
     }
     OpEvents ev = op_begin(c, OLED_OP_PERMUTE);
-    HIP_TRY(c, oled::launch_permute(c->d_topk, T, c->K, c->E, res, c->d_counts, c->d_offsets,
-                                    c->d_perm, c->d_inv, c->d_items, c->d_item_counts, c->d_flag,
-                                    c->h_sum, seq, ev.a, ev.b, s));
-    op_end(c, ev, OLED_OP_PERMUTE, layer, perm_bytes, 0);
+    HIP_TRY(c, oled::launch_permute(c->d_topk, T, c->K, c->d_flag, o, ev.a, ev.b, s));
+    op_end(c, ev, rec(OLED_OP_PERMUTE, layer, perm_bytes));
   }
-  c->route_seq = seq;
+  c->route_n = n;
+  c->cur_route = n;
   c->stage = Stage::kRouted;
   c->cur_layer = layer;
   c->cur_T = T;
-  c->cur_res = c->cs.resident_count(layer);
   c->cur_stream = s;
   c->have_stream = true;
   c->fwd_x = nullptr;
@@ -559,33 +739,133 @@ oled_status moe_forward_cached(void* ctx, int32_t layer, const void* x_dev, void
   if (st != OLED_OK) return st;
   if (!x_dev || !y_dev) return fail(c, OLED_ERR_INVALID_ARG, "NULL x or y");
   HIP_TRY(c, hipSetDevice(c->device));
-  if (c->cur_res > 0) {
-    // hits: the active residents; the item count stays on the device, the
-    // byte and flop accounting is completed in apply_misses
-    SlotTable tab;
-    std::memset(&tab, 0xff, sizeof(tab));
-    c->cs.launch_slots(layer, tab.slot);
-    const int64_t routes = static_cast<int64_t>(c->cur_T) * c->K;
-    const int max_hit_items =
-        static_cast<int>(std::min<int64_t>(c->cur_res, routes) + routes / oled::kItemRows);
-    const bool bf16 = c->dtype == OLED_BF16;
-    FfnLaunch a = ffn_args(c, &tab, 0, -1, max_hit_items);
-    a.src = x_dev;
-    {
-      OpEvents ev = op_begin(c, OLED_OP_FFN_UP);
-      HIP_TRY(c, oled::launch_ffn_up(bf16, a, ev.a, ev.b, s));
-      op_end(c, ev, OLED_OP_FFN_UP, layer, -1, -1);
-    }
-    a.src = c->d_h;
-    {
-      OpEvents ev = op_begin(c, OLED_OP_FFN_DOWN);
-      HIP_TRY(c, oled::launch_ffn_down(bf16, a, ev.a, ev.b, s));
-      op_end(c, ev, OLED_OP_FFN_DOWN, layer, -1, -1);
-    }
+  // hits: the active residents, at most min(C, E) experts; their item count
+  // stays on the device. With the shader transfer the first workgroups of
+  // each launch copy the staged misses (gate/up part, then down part).
+  const int64_t routes = static_cast<int64_t>(c->cur_T) * c->K;
+  const int max_hit_items =
+      c->cap > 0 ? static_cast<int>(std::min<int64_t>(c->cap, routes) + routes / oled::kItemRows) : 0;
+  const bool shader = c->copy_mode == OLED_COPY_SHADER;
+  const bool bf16 = c->dtype == OLED_BF16;
+  FfnLaunch a = ffn_args(c, layer, 0, max_hit_items, 0);
+  a.src = x_dev;
+  if (shader) {
+    a.fetch.nblk = kFetchBlocks;
+    a.fetch.off = 0;
+    a.fetch.len = c->e13;
+  }
+  {
+    OpEvents ev = op_begin(c, OLED_OP_FFN_UP);
+    HIP_TRY(c, oled::launch_ffn_up(bf16, a, ev.a, ev.b, s));
+    OpRec r = rec(OLED_OP_FFN_UP, layer, -1);
+    r.route_seq = c->cur_route;
+    r.part = 0;
+    r.hits = true;
+    r.h2d = shader ? -1 : 0;
+    op_end(c, ev, r);
+  }
+  a.src = c->d_h;
+  if (shader) {
+    a.fetch.off = c->e13;
+    a.fetch.len = c->eb - c->e13;
+  }
+  {
+    OpEvents ev = op_begin(c, OLED_OP_FFN_DOWN);
+    HIP_TRY(c, oled::launch_ffn_down(bf16, a, ev.a, ev.b, s));
+    OpRec r = rec(OLED_OP_FFN_DOWN, layer, -1);
+    r.route_seq = c->cur_route;
+    r.part = 1;
+    r.hits = true;
+    r.h2d = shader ? -1 : 0;
+    op_end(c, ev, r);
   }
   c->fwd_x = x_dev;
   c->fwd_y = y_dev;
   c->stage = Stage::kHitsQueued;
+  return OLED_OK;
+}
+
+// Copy-engine transfer: the staged misses (from the routing kernel's list)
+// are copied with hipMemcpyAsync on the copy stream, gate/up parts of all
+// first, then the down parts; if the hits were queued, the misses' GEMMs are
+// launched as the host sees their copies land.
+oled_status apply_misses_sdma(Ctx* c, int layer, hipStream_t cs, const RouteStats& r,
+                              int64_t* bytes_out) {
+  hipStream_t s = c->cur_stream;
+  oled_status st = wait_published(c, &c->h_staged->seq, c->cur_route, s, "staged misses");
+  if (st != OLED_OK) return st;
+  const int n = c->h_staged->n;
+  if (n != r.n_staged || n < 0 || n > c->E)
+    return fail(c, OLED_ERR_HIP, "staged list disagrees with the routing record");
+  int64_t bytes = 0;
+  if (n > 0) {
+    OpEvents ev = op_begin(c, OLED_OP_H2D);
+    hipError_t e = hipSuccess;
+    if (ev.a) e = hipEventRecord(ev.a, cs);
+    for (int part = 0; part < 2 && e == hipSuccess; ++part) {
+      const int64_t off = part == 0 ? 0 : c->e13;
+      const int64_t len = part == 0 ? c->e13 : c->eb - c->e13;
+      for (int i = 0; i < n && e == hipSuccess; ++i) {
+        const int ex = c->h_staged->exp[i], sl = c->h_staged->slot[i];
+        if (ex < 0 || ex >= c->E || sl < 0 || sl >= c->n_slots) {
+          e = hipErrorInvalidValue;
+          break;
+        }
+        const int64_t blk = c->host_block_of[static_cast<size_t>(layer) * c->E + ex];
+        e = hipMemcpyAsync(c->d_pool + static_cast<int64_t>(sl) * c->eb + off,
+                           c->host_pool + blk * c->eb + off, len, hipMemcpyHostToDevice, cs);
+        bytes += len;
+      }
+      if (e == hipSuccess) e = hipEventRecord(part == 0 ? c->ev_up : c->ev_down, cs);
+    }
+    if (e == hipSuccess && ev.b) e = hipEventRecord(ev.b, cs);
+    if (e != hipSuccess) {
+      (void)hipStreamSynchronize(cs);
+      if (ev.a) c->ev_free.push_back(ev.a);
+      if (ev.b) c->ev_free.push_back(ev.b);
+      return hip_fail(c, e, "enqueueing the miss copies");
+    }
+    OpRec o = rec(OLED_OP_H2D, layer, bytes);
+    o.h2d = bytes;
+    op_end(c, ev, o);
+    c->copies_outstanding = true;
+  }
+  *bytes_out = bytes;
+  if (c->stage != Stage::kHitsQueued || r.n_miss_items <= 0) return OLED_OK;
+  const bool bf16 = c->dtype == OLED_BF16;
+  FfnLaunch a = ffn_args(c, layer, 1, r.n_miss_items, 0);
+  a.item_base = r.n_hit_items;
+  a.n_items_host = r.n_miss_items;
+  a.src = c->fwd_x;
+  st = wait_event_spin(c, c->ev_up, "gate/up weight copies");
+  if (st != OLED_OK) return st;
+  {
+    OpEvents ev = op_begin(c, OLED_OP_FFN_UP);
+    HIP_TRY(c, oled::launch_ffn_up(bf16, a, ev.a, ev.b, s));
+    op_end(c, ev, rec(OLED_OP_FFN_UP, layer, up_bytes(c, r.n_misses, r.miss_rows),
+                      up_flops(c, r.miss_rows)));
+  }
+  a.src = c->d_h;
+  st = wait_event_spin(c, c->ev_down, "down weight copies");
+  if (st != OLED_OK) return st;
+  c->copies_outstanding = false;
+  {
+    OpEvents ev = op_begin(c, OLED_OP_FFN_DOWN);
+    HIP_TRY(c, oled::launch_ffn_down(bf16, a, ev.a, ev.b, s));
+    op_end(c, ev, rec(OLED_OP_FFN_DOWN, layer, down_bytes(c, r.n_misses, r.miss_rows),
+                      down_flops(c, r.miss_rows)));
+  }
+  return OLED_OK;
+}
+
+oled_status launch_combine_of(Ctx* c, int layer) {
+  OpEvents ev = op_begin(c, OLED_OP_COMBINE);
+  const int T = c->cur_T;
+  HIP_TRY(c, oled::launch_combine(c->dtype == OLED_BF16, c->d_O, c->d_gates, c->d_inv, T, c->K,
+                                  c->H, c->fwd_y, ev.a, ev.b, c->cur_stream));
+  op_end(c, ev, rec(OLED_OP_COMBINE, layer,
+                    static_cast<int64_t>(T) * c->K * (c->H * 4 + 8) +
+                        static_cast<int64_t>(T) * c->H * c->esz));
   return OLED_OK;
 }
 
@@ -600,145 +880,90 @@ oled_status apply_misses(void* ctx, int32_t layer, void* copy_stream, oled_miss_
     return fail(c, OLED_ERR_STATE, "apply_misses: layer %d is not the layer in flight (%d)", layer,
                 c->cur_layer);
   HIP_TRY(c, hipSetDevice(c->device));
-  st = wait_published(c, &c->h_sum->seq, c->route_seq, c->cur_stream, "routing summary");
-  if (st != OLED_OK) {
-    c->stage = Stage::kIdle;
-    return st;
-  }
-  // every retention enqueued before this route has completed: commit them
-  st = consume_all(c);
-  if (st == OLED_ERR_HIP) {
-    c->stage = Stage::kIdle;
-    return st;
-  }
-  if (c->h_sum->bad_logits) {
-    c->stage = Stage::kIdle;
-    return fail(c, OLED_ERR_INVALID_ARG, "non-finite router logit at layer %d", layer);
-  }
-  std::memcpy(c->counts.data(), c->h_sum->counts, sizeof(int32_t) * c->E);
-  int n_active = 0, n_hits = 0, n_misses = 0;
-  c->cs.classify(layer, c->counts.data(), c->hit.data(), c->miss.data(), &n_active, &n_hits,
-                 &n_misses);
-  int nhi = 0, nmi = 0;
-  int64_t hit_rows = 0, miss_rows = 0;
-  for (int e = 0; e < c->E; ++e) {
-    const int ni = (c->counts[e] + oled::kItemRows - 1) / oled::kItemRows;
-    if (c->hit[e]) {
-      nhi += ni;
-      hit_rows += c->counts[e];
-    }
-    if (c->miss[e]) {
-      nmi += ni;
-      miss_rows += c->counts[e];
-    }
-  }
-  if (nhi != c->h_sum->n_hit_items || nmi != c->h_sum->n_miss_items) {
-    c->stage = Stage::kIdle;
-    return fail(c, OLED_ERR_HIP, "work list disagrees with the host cache state");
-  }
-  std::memcpy(&c->res_before[static_cast<size_t>(layer) * c->E], c->cs.resident(layer), c->E);
-  const int n_res = c->cs.resident_count(layer);
-
-  std::vector<int32_t> exps, slots;
-  if (!c->cs.stage_misses(layer, c->miss.data(), &exps, &slots)) {
-    c->stage = Stage::kIdle;
-    return fail(c, OLED_ERR_HIP, "no free staging slots (internal accounting error)");
-  }
-  hipStream_t cs = copy_stream ? static_cast<hipStream_t>(copy_stream) : c->own_copy;
-  int64_t bytes = 0;
-  if (!exps.empty()) {
-    // gate/up weights of every miss first, then the down weights, so the miss
-    // gate/up GEMM can run while the down weights are still in flight
-    OpEvents ev = op_begin(c, OLED_OP_H2D);
-    hipError_t e = hipSuccess;
-    if (ev.a) e = hipEventRecord(ev.a, cs);
-    for (int part = 0; part < 2 && e == hipSuccess; ++part) {
-      const int64_t off = part == 0 ? 0 : c->e13;
-      const int64_t len = part == 0 ? c->e13 : c->eb - c->e13;
-      for (size_t i = 0; i < exps.size() && e == hipSuccess; ++i) {
-        const int64_t blk = c->host_block_of[static_cast<size_t>(layer) * c->E + exps[i]];
-        e = hipMemcpyAsync(c->d_pool + static_cast<int64_t>(slots[i]) * c->eb + off,
-                           c->host_pool + blk * c->eb + off, len, hipMemcpyHostToDevice, cs);
-        bytes += len;
-      }
-      if (e == hipSuccess) e = hipEventRecord(part == 0 ? c->ev_up : c->ev_down, cs);
-    }
-    if (e == hipSuccess && ev.b) e = hipEventRecord(ev.b, cs);
-    if (e != hipSuccess) {
-      hipStreamSynchronize(cs);
-      c->cs.drop_staged(layer);
+  hipStream_t s = c->cur_stream;
+  const bool shader = c->copy_mode == OLED_COPY_SHADER;
+  const bool bf16 = c->dtype == OLED_BF16;
+  RouteStats r{};
+  if (!shader || out) {  // the layer's routing record is needed
+    st = drain_records(c, c->cur_route);
+    if (st != OLED_OK) {
       c->stage = Stage::kIdle;
-      if (ev.a) c->ev_free.push_back(ev.a);
-      if (ev.b) c->ev_free.push_back(ev.b);
-      return hip_fail(c, e, "enqueueing the miss copies");
+      return st;
     }
-    op_end(c, ev, OLED_OP_H2D, layer, bytes, 0);
-    c->copies_outstanding = true;
-  }
-  // complete the accounting of this layer's hit launches
-  for (auto it = c->ops.rbegin(); it != c->ops.rend() && it->layer == layer; ++it) {
-    if (it->kind == OLED_OP_FFN_UP && it->bytes < 0) {
-      it->bytes = up_bytes(c, n_hits, hit_rows);
-      it->flops = up_flops(c, hit_rows);
-    } else if (it->kind == OLED_OP_FFN_DOWN && it->bytes < 0) {
-      it->bytes = down_bytes(c, n_hits, hit_rows);
-      it->flops = down_flops(c, hit_rows);
+    r = c->h_ring[c->cur_route % oled::kStatsRing];
+    read_retentions(c);  // every retention enqueued before this routing has run
+    if (r.bad) {
+      if (c->bad_route_layer == layer) c->bad_route_layer = -1;  // reported here
+      c->stage = Stage::kIdle;
+      return fail(c, OLED_ERR_INVALID_ARG,
+                  "bad block at layer %d (non-finite router logit): nothing staged, cache "
+                  "unchanged", layer);
     }
   }
-  if (c->stage == Stage::kHitsQueued) {
-    hipStream_t s = c->cur_stream;
-    const bool bf16 = c->dtype == OLED_BF16;
-    if (nmi > 0) {
-      SlotTable tab;
-      std::memset(&tab, 0xff, sizeof(tab));
-      c->cs.launch_slots(layer, tab.slot);
-      for (int e = 0; e < c->E; ++e)
-        if (c->miss[e] && (tab.slot[e] < 0 || tab.slot[e] >= c->n_slots))
-          return fail(c, OLED_ERR_HIP, "missed expert %d has no slot (internal accounting error)", e);
-      FfnLaunch a = ffn_args(c, &tab, nhi, nmi, nmi);
+  int64_t bytes = 0;
+  if (shader) {
+    if (c->stage == Stage::kHitsQueued) {
+      // misses: bounded by the staging capacity; the item count is on the device
+      const int64_t routes = static_cast<int64_t>(c->cur_T) * c->K;
+      const int max_miss_items =
+          static_cast<int>(std::min<int64_t>(c->E, routes) + routes / oled::kItemRows);
+      FfnLaunch a = ffn_args(c, layer, 1, max_miss_items, kMissGridCap);
       a.src = c->fwd_x;
-      st = wait_event_spin(c, c->ev_up, "gate/up weight copies");
-      if (st != OLED_OK) return st;
       {
         OpEvents ev = op_begin(c, OLED_OP_FFN_UP);
         HIP_TRY(c, oled::launch_ffn_up(bf16, a, ev.a, ev.b, s));
-        op_end(c, ev, OLED_OP_FFN_UP, layer, up_bytes(c, n_misses, miss_rows), up_flops(c, miss_rows));
+        OpRec o = rec(OLED_OP_FFN_UP, layer, -1);
+        o.route_seq = c->cur_route;
+        o.part = 0;
+        op_end(c, ev, o);
       }
       a.src = c->d_h;
-      st = wait_event_spin(c, c->ev_down, "down weight copies");
-      if (st != OLED_OK) return st;
-      c->copies_outstanding = false;
       {
         OpEvents ev = op_begin(c, OLED_OP_FFN_DOWN);
         HIP_TRY(c, oled::launch_ffn_down(bf16, a, ev.a, ev.b, s));
-        op_end(c, ev, OLED_OP_FFN_DOWN, layer, down_bytes(c, n_misses, miss_rows),
-               down_flops(c, miss_rows));
+        OpRec o = rec(OLED_OP_FFN_DOWN, layer, -1);
+        o.route_seq = c->cur_route;
+        o.part = 1;
+        op_end(c, ev, o);
       }
+    } else {
+      // control path: transfer the whole blocks of the staged misses
+      FetchArgs f;
+      f.host_addr = c->d_host_addr + static_cast<size_t>(layer) * c->E;
+      f.hdr = c->d_hdr;
+      f.off = 0;
+      f.len = c->eb;
+      f.nblk = kFetchBlocks;
+      f.E = c->E;
+      OpEvents ev = op_begin(c, OLED_OP_H2D);
+      HIP_TRY(c, oled::launch_fetch(c->d_pool, c->eb, c->n_slots, f, ev.a, ev.b, s));
+      OpRec o = rec(OLED_OP_H2D, layer, -1);
+      o.route_seq = c->cur_route;
+      op_end(c, ev, o);
     }
-    {
-      OpEvents ev = op_begin(c, OLED_OP_COMBINE);
-      const int T = c->cur_T;
-      HIP_TRY(c, oled::launch_combine(bf16, c->d_O, c->d_gates, c->d_inv, T, c->K, c->H, c->fwd_y,
-                                      ev.a, ev.b, s));
-      op_end(c, ev, OLED_OP_COMBINE, layer,
-             static_cast<int64_t>(T) * c->K * (c->H * 4 + 8) + static_cast<int64_t>(T) * c->H * c->esz,
-             0);
+    bytes = static_cast<int64_t>(r.n_staged) * c->eb;
+  } else {
+    hipStream_t cs = copy_stream ? static_cast<hipStream_t>(copy_stream) : c->own_copy;
+    st = apply_misses_sdma(c, layer, cs, r, &bytes);
+    if (st != OLED_OK) {
+      c->stage = Stage::kIdle;
+      return st;
     }
   }
-  int* lc = &c->last_counts[static_cast<size_t>(layer) * 3];
-  lc[0] = n_active;
-  lc[1] = n_hits;
-  lc[2] = n_misses;
+  if (c->stage == Stage::kHitsQueued) {
+    st = launch_combine_of(c, layer);
+    if (st != OLED_OK) return st;
+  }
   if (out) {
-    out->n_active = n_active;
-    out->n_hits = n_hits;
-    out->n_misses = n_misses;
-    out->n_resident = n_res;
+    out->n_active = r.n_active;
+    out->n_hits = r.n_hits;
+    out->n_misses = r.n_misses;
+    out->n_resident = r.n_resident;
     out->rejected_layer = c->rejected_layer;
     out->reserved = 0;
     out->h2d_bytes = bytes;
+    c->rejected_layer = -1;
   }
-  c->rejected_layer = -1;
   c->stage = Stage::kApplied;
   return OLED_OK;
 }
@@ -759,22 +984,19 @@ oled_status score_and_retain(void* ctx, int32_t layer, const float* conf_dev, vo
     HIP_TRY(c, hipStreamWaitEvent(s, c->ev_down, 0));
     c->copies_outstanding = false;
   }
-  const ExpertMask res = mask_of(c->cs.resident(layer), c->E);
   const int seq = ++c->seq;
   {
     OpEvents ev = op_begin(c, OLED_OP_SCORE_RETAIN);
     HIP_TRY(c, oled::launch_score_retain(c->d_gates, static_cast<const float*>(conf_dev),
-                                         c->d_topk, c->d_counts, c->cur_T, c->K, c->E, c->C, res,
-                                         c->d_score + static_cast<size_t>(layer) * c->E,
+                                         c->d_topk, c->d_counts, c->cur_T, c->K, c->E, c->C, layer,
+                                         view(c), c->d_score + static_cast<size_t>(layer) * c->E,
                                          &c->h_ret[layer], seq, ev.a, ev.b, s));
-    op_end(c, ev, OLED_OP_SCORE_RETAIN, layer,
-           static_cast<int64_t>(c->cur_T) * c->K * 12 + static_cast<int64_t>(c->cur_T) * 4 +
-               static_cast<int64_t>(c->E) * 16,
-           0);
+    op_end(c, ev, rec(OLED_OP_SCORE_RETAIN, layer,
+                      static_cast<int64_t>(c->cur_T) * c->K * 12 +
+                          static_cast<int64_t>(c->cur_T) * 4 + static_cast<int64_t>(c->E) * 16));
   }
-  c->pending[layer] = 1;
   c->ret_seq[layer] = seq;
-  c->ret_stream[layer] = s;
+  c->ret_seen[layer] = 0;
   c->stage = Stage::kIdle;
   c->cur_layer = -1;
   return OLED_OK;
@@ -786,10 +1008,9 @@ oled_status oled_read_layer_state(void* ctx, int32_t layer, oled_layer_state* ou
   if (layer < 0 || layer >= c->L) return fail(c, OLED_ERR_INVALID_ARG, "layer out of range");
   HIP_TRY(c, hipSetDevice(c->device));
   HIP_TRY(c, hipDeviceSynchronize());
-  if (c->stage == Stage::kIdle) {
-    const oled_status st = consume_all(c);
-    if (st == OLED_ERR_HIP) return st;
-  }
+  oled_status st = drain_records(c, c->route_n);
+  if (st != OLED_OK) return st;
+  read_retentions(c);
   const int T = (c->last_routed_layer == layer) ? c->last_routed_T : 0;
   const size_t R = static_cast<size_t>(T) * c->K;
   out->tokens = T;
@@ -805,19 +1026,45 @@ oled_status oled_read_layer_state(void* ctx, int32_t layer, oled_layer_state* ou
   if (out->score_q)
     HIP_TRY(c, hipMemcpy(out->score_q, c->d_score + static_cast<size_t>(layer) * c->E, c->E * 8,
                          hipMemcpyDeviceToHost));
-  if (out->resident_before)
-    std::memcpy(out->resident_before, &c->res_before[static_cast<size_t>(layer) * c->E], c->E);
-  if (out->resident_after) std::memcpy(out->resident_after, c->cs.resident(layer), c->E);
-  if (out->slot_of) {
-    for (int e = 0; e < c->E; ++e)
-      out->slot_of[e] = c->cs.resident(layer)[e] ? c->cs.slot_of(layer)[e] : -1;
+  ExpertMask before, after;
+  int32_t lc[4];
+  std::vector<int32_t> slots(c->E);
+  HIP_TRY(c, hipMemcpy(&before, c->d_res_before + layer, sizeof(ExpertMask), hipMemcpyDeviceToHost));
+  HIP_TRY(c, hipMemcpy(&after, c->d_res + layer, sizeof(ExpertMask), hipMemcpyDeviceToHost));
+  HIP_TRY(c, hipMemcpy(lc, c->d_last_counts + 4 * layer, sizeof(lc), hipMemcpyDeviceToHost));
+  HIP_TRY(c, hipMemcpy(slots.data(), c->d_slot_of + static_cast<size_t>(layer) * c->E,
+                       sizeof(int32_t) * c->E, hipMemcpyDeviceToHost));
+  for (int e = 0; e < c->E; ++e) {
+    if (out->resident_before) out->resident_before[e] = before.test(e);
+    if (out->resident_after) out->resident_after[e] = after.test(e);
+    if (out->slot_of) out->slot_of[e] = after.test(e) ? slots[e] : -1;
   }
-  const int* lc = &c->last_counts[static_cast<size_t>(layer) * 3];
   out->n_active = lc[0];
   out->n_hits = lc[1];
   out->n_misses = lc[2];
+  if (c->stage == Stage::kIdle) {
+    st = check_slots(c);
+    if (st != OLED_OK) return st;
+  }
   if (c->rejected[layer])
     return fail(c, OLED_ERR_INVALID_ARG, "the last retention of layer %d was rejected", layer);
+  if (c->bad_route_layer == layer) {
+    c->bad_route_layer = -1;
+    return fail(c, OLED_ERR_INVALID_ARG, "a bad block (non-finite router logit) was seen at layer %d",
+                layer);
+  }
+  return OLED_OK;
+}
+
+oled_status oled_collect_stats(void* ctx, oled_stats* out) {
+  Ctx* c = static_cast<Ctx*>(ctx);
+  if (!c || !out) return OLED_ERR_INVALID_ARG;
+  HIP_TRY(c, hipSetDevice(c->device));
+  HIP_TRY(c, hipDeviceSynchronize());
+  const oled_status st = drain_records(c, c->route_n);
+  if (st != OLED_OK) return st;
+  *out = c->acc;
+  c->acc = oled_stats{};
   return OLED_OK;
 }
 
@@ -826,8 +1073,14 @@ oled_status oled_profile_collect(void* ctx, oled_op_time* out, int32_t cap, int3
   if (!c || !n_out || (cap > 0 && !out)) return OLED_ERR_INVALID_ARG;
   HIP_TRY(c, hipSetDevice(c->device));
   HIP_TRY(c, hipDeviceSynchronize());
+  const oled_status st = drain_records(c, c->route_n);
+  if (st != OLED_OK) return st;
   int n = 0;
   for (auto& op : c->ops) {
+    if (op.route_seq > 0) {
+      const RouteStats* r = find_record(c, op.route_seq);
+      if (r) complete_op(c, op, *r);
+    }
     float ms = 0.f;
     const hipError_t e = hipEventElapsedTime(&ms, op.a, op.b);
     if (n < cap) {
@@ -836,12 +1089,14 @@ oled_status oled_profile_collect(void* ctx, oled_op_time* out, int32_t cap, int3
       out[n].ms = e == hipSuccess ? ms : -1.f;
       out[n].bytes = op.bytes;
       out[n].flops = op.flops;
+      out[n].h2d_bytes = op.h2d;
       ++n;
     }
     c->ev_free.push_back(op.a);
     c->ev_free.push_back(op.b);
   }
   c->ops.clear();
+  c->recs.clear();
   *n_out = n;
   return OLED_OK;
 }
@@ -872,7 +1127,7 @@ oled_status oled_host_alloc(int64_t bytes, void** ptr_out) {
 }
 
 void oled_host_free(void* ptr) {
-  if (ptr) hipHostFree(ptr);
+  if (ptr) (void)hipHostFree(ptr);
 }
 
 }  // extern "C"

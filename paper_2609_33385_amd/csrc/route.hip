@@ -1,6 +1,7 @@
 // K1 top-k routing and K2 histogram / prefix-sum / stable permutation for one
 // denoising block (OLED-MoE Sec. 4.1: the gate yields routed expert ids and
-// gate scores for every token of the block; Sec. 4.2: the active set A).
+// gate scores for every token of the block; Sec. 4.2: the active set A, the
+// misses M = A \ R, each given a staging slot in the device cache state).
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
@@ -119,29 +120,35 @@ constexpr int kChunkTokens = kChunkWords * 32;
 constexpr int kFusedMaxRoutes = 1024;       // fused routing path: T * k routes kept in LDS
 
 // Histogram, offsets, work list and stable permutation of the T*k routes in
-// `idx` (global or LDS), by one workgroup. Pass 1: per-expert counts (LDS
-// atomics). Scan: offsets and the work list, hit experts first. Pass 2,
-// chunk by chunk of 512 tokens: a per-expert token bitmask (the ballot of the
-// tokens that chose the expert), a running popcount prefix per 32-token word,
-// and each route's stable position = offsets[e] + tokens before it that chose e.
-// Then one wavefront publishes the summary (fields, system fence, seq).
-__device__ __forceinline__ void permute_body(
-    const int32_t* idx, int T, int k, int E, const ExpertMask& resident,
-    int32_t* __restrict__ counts, int32_t* __restrict__ offsets, int32_t* __restrict__ perm,
-    int32_t* __restrict__ inv_perm, WorkItem* __restrict__ items, int32_t* __restrict__ item_counts,
-    int bad, RouteSummary* __restrict__ summary, int seq) {
+// `idx` (global or LDS), by one workgroup, plus the staging of the layer's
+// misses. Pass 1: per-expert counts (LDS atomics). Wave 0 then scans the
+// experts (4 per lane): offsets, the work list (hit experts first), the hit /
+// miss split against the layer's resident set, and the staging: miss j (in
+// expert order) takes the free slot free_list[free_top - 1 - j]. Pass 2,
+// chunk by chunk of 512 tokens: a per-expert token bitmask (the ballot of
+// the tokens that chose the expert), a running popcount prefix per 32-token
+// word, and each route's stable position = offsets[e] + tokens before it
+// that chose e. Finally one wavefront publishes the routing record (fields,
+// system-scope fence, seq).
+__device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, int bad,
+                                             const PermuteOut& o) {
   __shared__ int32_t s_cnt[kMaxExperts];
   __shared__ int32_t s_off[kMaxExperts + 1];
   __shared__ int32_t s_item_base[kMaxExperts];
   __shared__ int32_t s_run[kMaxExperts];
-  __shared__ int32_t s_tot[2];
+  __shared__ int32_t s_stat[12];
+  __shared__ int32_t s_sexp[kMaxExperts];
+  __shared__ int32_t s_sslot[kMaxExperts];
+  __shared__ uint32_t s_res[kMaxExperts / 32];
   __shared__ uint32_t s_mask[kMaxExperts * kChunkWords];
   __shared__ int32_t s_pre[kMaxExperts * kChunkWords];
 
   const int tid = threadIdx.x;
   const int nthr = blockDim.x;
+  const int E = o.E, layer = o.layer;
   const int R = T * k;
   for (int e = tid; e < kMaxExperts; e += nthr) s_cnt[e] = 0;
+  if (tid < kMaxExperts / 32) s_res[tid] = o.cv.res[layer].bits[tid];
   __syncthreads();
   for (int r = tid; r < R; r += nthr) atomicAdd(&s_cnt[idx[r]], 1);
   __syncthreads();
@@ -149,54 +156,108 @@ __device__ __forceinline__ void permute_body(
   if (tid < 64) {  // wave 0: scans over experts, 4 per lane
     const int lane = tid;
     int c[4], nh[4], nm[4];
-    int sc = 0, sh = 0, sm = 0;
+    bool hit[4], miss[4];
+    int sc = 0, sh = 0, sm = 0, sx = 0;
+    int n_act = 0, n_hit = 0, n_res = 0, hrows = 0, mrows = 0;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int e = 4 * lane + q;
       c[q] = e < E ? s_cnt[e] : 0;
       const int ni = (c[q] + kItemRows - 1) / kItemRows;
-      const bool res = e < E && resident.test(e);
-      nh[q] = res ? ni : 0;
-      nm[q] = res ? 0 : ni;
+      const bool res = e < E && ((s_res[e >> 5] >> (e & 31)) & 1u);
+      hit[q] = res && c[q] > 0;
+      miss[q] = !res && c[q] > 0;
+      nh[q] = hit[q] ? ni : 0;
+      nm[q] = miss[q] ? ni : 0;
       sc += c[q];
       sh += nh[q];
       sm += nm[q];
+      sx += miss[q] ? 1 : 0;
+      n_act += c[q] > 0 ? 1 : 0;
+      n_hit += hit[q] ? 1 : 0;
+      n_res += res ? 1 : 0;
+      hrows += hit[q] ? c[q] : 0;
+      mrows += miss[q] ? c[q] : 0;
     }
-    int ic = sc, ih = sh, im = sm;
+    int ic = sc, ih = sh, im = sm, ix = sx;
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
-      const int tc = __shfl_up(ic, off), th = __shfl_up(ih, off), tm = __shfl_up(im, off);
+      const int tc = __shfl_up(ic, off), th = __shfl_up(ih, off), tm = __shfl_up(im, off),
+                tx = __shfl_up(ix, off);
       if (lane >= off) {
         ic += tc;
         ih += th;
         im += tm;
+        ix += tx;
       }
     }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      n_act += __shfl_xor(n_act, off);
+      n_hit += __shfl_xor(n_hit, off);
+      n_res += __shfl_xor(n_res, off);
+      hrows += __shfl_xor(hrows, off);
+      mrows += __shfl_xor(mrows, off);
+    }
     const int tot_hit = __shfl(ih, 63);
-    int xc = ic - sc, xh = ih - sh, xm = im - sm;
+    const int n_miss = __shfl(ix, 63);
+    // staging: every miss takes a free slot, unless the block is bad
+    CacheHdr* hdr = o.cv.hdr;
+    const int free_top = hdr->free_top;
+    const bool stage = !bad && free_top >= 0 && free_top <= o.cv.n_slots && n_miss <= free_top;
+    int xc = ic - sc, xh = ih - sh, xm = im - sm, xx = ix - sx;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int e = 4 * lane + q;
       if (e < E) {
         s_off[e] = xc;
         s_item_base[e] = (nh[q] > 0) ? xh : tot_hit + xm;
+        if (stage && miss[q]) {
+          const int slot = o.cv.free_list[free_top - 1 - xx];
+          o.cv.slot_of[static_cast<size_t>(layer) * E + e] = slot;
+          hdr->staged_exp[xx] = e;
+          hdr->staged_slot[xx] = slot;
+          s_sexp[xx] = e;
+          s_sslot[xx] = slot;
+        }
       }
       xc += c[q];
       xh += nh[q];
       xm += nm[q];
+      xx += miss[q] ? 1 : 0;
     }
+    if (lane == 0) {
+      hdr->free_top = stage ? free_top - n_miss : free_top;
+      hdr->staged_n = stage ? n_miss : 0;
+      hdr->route_bad = stage ? 0 : 1;
+      if (!bad && !stage) hdr->fault |= 1;
+      int32_t* lc = o.cv.last_counts + 4 * layer;
+      lc[0] = n_act;
+      lc[1] = n_hit;
+      lc[2] = n_miss;
+      lc[3] = n_res;
+      s_stat[0] = n_act;
+      s_stat[1] = n_hit;
+      s_stat[2] = n_miss;
+      s_stat[3] = n_res;
+      s_stat[4] = hrows;
+      s_stat[5] = mrows;
+      s_stat[6] = stage ? n_miss : 0;
+      s_stat[7] = stage ? 0 : 1;
+    }
+    if (lane < kMaxExperts / 32) o.cv.res_before[layer].bits[lane] = s_res[lane];
     if (lane == 63) {
       s_off[E] = ic;
-      s_tot[0] = ih;
-      s_tot[1] = im;
+      s_stat[8] = ih;
+      s_stat[9] = im;
     }
   }
   __syncthreads();
 
   for (int e = tid; e < E; e += nthr) {
     const int c = s_cnt[e];
-    counts[e] = c;
-    offsets[e] = s_off[e];
+    o.counts[e] = c;
+    o.offsets[e] = s_off[e];
     s_run[e] = s_off[e];
     const int base = s_item_base[e];
     for (int m = 0; m * kItemRows < c; ++m) {
@@ -205,10 +266,10 @@ __device__ __forceinline__ void permute_body(
       it.row_begin = s_off[e] + m * kItemRows;
       it.rows = min(kItemRows, c - m * kItemRows);
       it.pad = 0;
-      items[base + m] = it;
+      o.items[base + m] = it;
     }
   }
-  if (tid == 0) offsets[E] = s_off[E];
+  if (tid == 0) o.offsets[E] = s_off[E];
 
   for (int t0 = 0; t0 < T; t0 += kChunkTokens) {
     const int t1 = min(T, t0 + kChunkTokens);
@@ -236,55 +297,71 @@ __device__ __forceinline__ void permute_body(
       const int w = lt >> 5;
       const uint32_t below = s_mask[e * kChunkWords + w] & ((1u << (lt & 31)) - 1u);
       const int pos = s_pre[e * kChunkWords + w] + __popc(below);
-      perm[pos] = r;
-      inv_perm[r] = pos;
+      o.perm[pos] = r;
+      o.inv_perm[r] = pos;
     }
     __syncthreads();
   }
 
   if (tid < 64) {
-    for (int e = tid; e < E; e += 64) summary->counts[e] = s_cnt[e];
+    const int n_staged = s_stat[6];
+    if (o.staged) {
+      for (int j = tid; j < n_staged; j += 64) {
+        o.staged->exp[j] = s_sexp[j];
+        o.staged->slot[j] = s_sslot[j];
+      }
+    }
+    RouteStats* rs = o.ring + (o.seq % kStatsRing);
     if (tid == 0) {
-      item_counts[0] = s_tot[0];
-      item_counts[1] = s_tot[1];
-      summary->n_hit_items = s_tot[0];
-      summary->n_miss_items = s_tot[1];
-      summary->bad_logits = bad;
+      o.item_counts[0] = s_stat[8];
+      o.item_counts[1] = s_stat[9];
+      rs->layer = layer;
+      rs->n_active = s_stat[0];
+      rs->n_hits = s_stat[1];
+      rs->n_misses = s_stat[2];
+      rs->n_resident = s_stat[3];
+      rs->hit_rows = s_stat[4];
+      rs->miss_rows = s_stat[5];
+      rs->n_staged = n_staged;
+      rs->bad = bad ? 1 : s_stat[7];
+      rs->n_hit_items = s_stat[8];
+      rs->n_miss_items = s_stat[9];
+      if (o.staged) o.staged->n = n_staged;
     }
     __threadfence_system();
-    if (tid == 0) *reinterpret_cast<volatile int32_t*>(&summary->seq) = seq;
+    if (tid == 0) {
+      *reinterpret_cast<volatile int32_t*>(&rs->seq) = o.seq;
+      if (o.staged) *reinterpret_cast<volatile int32_t*>(&o.staged->seq) = o.seq;
+    }
   }
 }
 
-__global__ __launch_bounds__(kPermThreads) void k_permute(
-    const int32_t* __restrict__ topk_idx, int T, int k, int E, ExpertMask resident,
-    int32_t* __restrict__ counts, int32_t* __restrict__ offsets, int32_t* __restrict__ perm,
-    int32_t* __restrict__ inv_perm, WorkItem* __restrict__ items, int32_t* __restrict__ item_counts,
-    int32_t* __restrict__ bad_flag, RouteSummary* __restrict__ summary, int seq) {
+__global__ __launch_bounds__(kPermThreads) void k_permute(const int32_t* __restrict__ topk_idx,
+                                                          int T, int k,
+                                                          int32_t* __restrict__ bad_flag,
+                                                          PermuteOut o) {
   const int bad = *bad_flag;
   __syncthreads();
   if (threadIdx.x == 0) *bad_flag = 0;
-  permute_body(topk_idx, T, k, E, resident, counts, offsets, perm, inv_perm, items, item_counts,
-               bad, summary, seq);
+  permute_body(topk_idx, T, k, bad, o);
 }
 
 // Small blocks (T*k <= 1024): routing on many CUs, one token per wavefront,
 // then the last workgroup to finish (a fenced counter; no workgroup ever
 // waits for another) permutes all routes. Workgroups hold 256 threads and
-// the permutation below is written for any workgroup size.
+// the permutation above is written for any workgroup size.
 template <int EPL>
-__global__ __launch_bounds__(256) void k_route_fused(
-    const float* __restrict__ logits, int T, int E, int k, ExpertMask resident,
-    int32_t* __restrict__ topk_idx, float* __restrict__ gates, int32_t* __restrict__ counts,
-    int32_t* __restrict__ offsets, int32_t* __restrict__ perm, int32_t* __restrict__ inv_perm,
-    WorkItem* __restrict__ items, int32_t* __restrict__ item_counts,
-    int32_t* __restrict__ sync, RouteSummary* __restrict__ summary, int seq) {
+__global__ __launch_bounds__(256) void k_route_fused(const float* __restrict__ logits, int T,
+                                                     int k, int32_t* __restrict__ topk_idx,
+                                                     float* __restrict__ gates,
+                                                     int32_t* __restrict__ sync, PermuteOut o) {
   __shared__ int32_t s_e[4][kMaxTopK];
   __shared__ float s_v[4][kMaxTopK];
   __shared__ double s_x[4][kMaxTopK];
   __shared__ int32_t s_idx[kFusedMaxRoutes];
   __shared__ int32_t s_last;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int E = o.E;
   int bad = 0;
   for (int t = blockIdx.x * 4 + wave; t < T; t += gridDim.x * 4) {
     float g;
@@ -310,8 +387,7 @@ __global__ __launch_bounds__(256) void k_route_fused(
     sync[0] = 0;
     sync[1] = 0;
   }
-  permute_body(s_idx, T, k, E, resident, counts, offsets, perm, inv_perm, items, item_counts,
-               any_bad, summary, seq);
+  permute_body(s_idx, T, k, any_bad, o);
 }
 
 }  // namespace
@@ -334,35 +410,26 @@ hipError_t launch_route_topk(const float* logits, int T, int E, int k, int32_t* 
   return hipGetLastError();
 }
 
-hipError_t launch_permute(const int32_t* topk_idx, int T, int k, int E, const ExpertMask& resident,
-                          int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* inv_perm,
-                          WorkItem* items, int32_t* item_counts, int32_t* bad_flag,
-                          RouteSummary* summary, int seq, hipEvent_t ev0, hipEvent_t ev1,
-                          hipStream_t s) {
+hipError_t launch_permute(const int32_t* topk_idx, int T, int k, int32_t* bad_flag,
+                          const PermuteOut& o, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
   hipExtLaunchKernelGGL(k_permute, dim3(1), dim3(kPermThreads), 0, s, ev0, ev1, 0, topk_idx, T, k,
-                        E, resident, counts, offsets, perm, inv_perm, items, item_counts, bad_flag,
-                        summary, seq);
+                        bad_flag, o);
   return hipGetLastError();
 }
 
-hipError_t launch_route_fused(const float* logits, int T, int E, int k, const ExpertMask& resident,
-                              int32_t* topk_idx, float* gates, int32_t* counts, int32_t* offsets,
-                              int32_t* perm, int32_t* inv_perm, WorkItem* items,
-                              int32_t* item_counts, int32_t* sync, RouteSummary* summary, int seq,
-                              hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
+hipError_t launch_route_fused(const float* logits, int T, int k, int32_t* topk_idx, float* gates,
+                              int32_t* sync, const PermuteOut& o, hipEvent_t ev0, hipEvent_t ev1,
+                              hipStream_t s) {
   const int blocks = (T + 3) / 4;
-  if (E <= 64)
+  if (o.E <= 64)
     hipExtLaunchKernelGGL(k_route_fused<1>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits, T,
-                          E, k, resident, topk_idx, gates, counts, offsets, perm, inv_perm, items,
-                          item_counts, sync, summary, seq);
-  else if (E <= 128)
+                          k, topk_idx, gates, sync, o);
+  else if (o.E <= 128)
     hipExtLaunchKernelGGL(k_route_fused<2>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits, T,
-                          E, k, resident, topk_idx, gates, counts, offsets, perm, inv_perm, items,
-                          item_counts, sync, summary, seq);
+                          k, topk_idx, gates, sync, o);
   else
     hipExtLaunchKernelGGL(k_route_fused<4>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits, T,
-                          E, k, resident, topk_idx, gates, counts, offsets, perm, inv_perm, items,
-                          item_counts, sync, summary, seq);
+                          k, topk_idx, gates, sync, o);
   return hipGetLastError();
 }
 

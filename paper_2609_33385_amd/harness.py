@@ -27,13 +27,14 @@ def fill_pool(w: W.Workload, seed: int, n_blocks: int) -> oled.PinnedPool:
 
 def make_context(w: W.Workload, pool: oled.PinnedPool, capacity: int | None = None,
                  n_layers: int | None = None, max_tokens: int | None = None,
-                 profile_ops: int = 0) -> oled.Context:
+                 profile_ops: int = 0, copy_mode: str = "shader") -> oled.Context:
     L = n_layers if n_layers is not None else w.n_layers
     return oled.Context(w.hidden, w.inter, w.n_experts, w.top_k, L,
                         w.capacity if capacity is None else capacity,
                         max_tokens if max_tokens is not None else w.tokens, w.dtype,
                         pool.ptr, pool.n_blocks,
-                        W.host_block_of(w.replace(n_layers=L), pool.n_blocks), profile_ops=profile_ops)
+                        W.host_block_of(w.replace(n_layers=L), pool.n_blocks), profile_ops=profile_ops,
+                        copy_mode=copy_mode)
 
 
 def torch_dtype(w: W.Workload):
@@ -59,13 +60,13 @@ def from_device(t: torch.Tensor) -> np.ndarray:
 
 def layer_step(ctx: oled.Context, layer: int, logits: torch.Tensor, conf: torch.Tensor,
                x: torch.Tensor | None = None, y: torch.Tensor | None = None,
-               stream=None) -> oled.MissReport:
+               stream=None, report: bool = True) -> oled.MissReport | None:
     """route_block -> [moe_forward_cached] -> apply_misses -> score_and_retain."""
     s = stream if stream is not None else torch.cuda.current_stream()
     T = logits.shape[0]
     ctx.route_block(layer, logits, T, s)
     if x is not None:
         ctx.moe_forward_cached(layer, x, y, s)
-    rep = ctx.apply_misses(layer)
+    rep = ctx.apply_misses(layer, report=report)
     ctx.score_and_retain(layer, conf, s)
     return rep

@@ -29,6 +29,9 @@ STATUS_NAMES = {0: "OK", 1: "INVALID_ARG", 2: "OUT_OF_MEMORY", 3: "HIP", 4: "STA
 
 OLED_F32 = 0
 OLED_BF16 = 1
+OLED_COPY_SHADER = 0
+OLED_COPY_SDMA = 1
+COPY_MODES = {"shader": OLED_COPY_SHADER, "sdma": OLED_COPY_SDMA}
 PROFILE_ALL = 0x7F
 
 OP_NAMES = {0: "route_topk", 1: "permute", 2: "ffn_up", 3: "ffn_down", 4: "combine",
@@ -45,7 +48,8 @@ def profile_mask(*names) -> int:
 
 EXPORTED = ["oled_create", "oled_destroy", "oled_last_error", "oled_reset_cache", "route_block",
             "apply_misses", "moe_forward_cached", "score_and_retain", "oled_read_layer_state",
-            "oled_profile_collect", "oled_pack_expert", "oled_host_alloc", "oled_host_free"]
+            "oled_collect_stats", "oled_profile_collect", "oled_pack_expert", "oled_host_alloc",
+            "oled_host_free"]
 
 
 class OledConfig(ctypes.Structure):
@@ -55,7 +59,8 @@ class OledConfig(ctypes.Structure):
                 ("max_tokens", ctypes.c_int32), ("dtype", ctypes.c_int32),
                 ("device", ctypes.c_int32), ("profile_ops", ctypes.c_int32),
                 ("host_pool", ctypes.c_void_p), ("host_pool_blocks", ctypes.c_int64),
-                ("host_block_of", ctypes.POINTER(ctypes.c_int64))]
+                ("host_block_of", ctypes.POINTER(ctypes.c_int64)),
+                ("copy_mode", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class MissReport(ctypes.Structure):
@@ -63,6 +68,16 @@ class MissReport(ctypes.Structure):
                 ("n_misses", ctypes.c_int32), ("n_resident", ctypes.c_int32),
                 ("rejected_layer", ctypes.c_int32), ("reserved", ctypes.c_int32),
                 ("h2d_bytes", ctypes.c_int64)]
+
+
+class Stats(ctypes.Structure):
+    _fields_ = [("layer_iters", ctypes.c_int64), ("n_active", ctypes.c_int64),
+                ("n_hits", ctypes.c_int64), ("n_misses", ctypes.c_int64),
+                ("n_transferred", ctypes.c_int64), ("h2d_bytes", ctypes.c_int64),
+                ("n_bad_blocks", ctypes.c_int64)]
+
+    def as_dict(self) -> dict:
+        return {name: getattr(self, name) for name, _ in self._fields_}
 
 
 class LayerState(ctypes.Structure):
@@ -77,7 +92,8 @@ class LayerState(ctypes.Structure):
 
 class OpTime(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("layer", ctypes.c_int32), ("ms", ctypes.c_float),
-                ("bytes", ctypes.c_int64), ("flops", ctypes.c_int64)]
+                ("bytes", ctypes.c_int64), ("flops", ctypes.c_int64),
+                ("h2d_bytes", ctypes.c_int64)]
 
 
 class OledError(RuntimeError):
@@ -108,6 +124,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "moe_forward_cached": (i32, [vp, i32, vp, vp, vp]),
         "score_and_retain": (i32, [vp, i32, vp, vp]),
         "oled_read_layer_state": (i32, [vp, i32, ctypes.POINTER(LayerState)]),
+        "oled_collect_stats": (i32, [vp, ctypes.POINTER(Stats)]),
         "oled_profile_collect": (i32, [vp, ctypes.POINTER(OpTime), i32, ctypes.POINTER(i32)]),
         "oled_pack_expert": (i32, [i32, i32, i32, vp, vp, vp]),
         "oled_host_alloc": (i32, [i64, ctypes.POINTER(vp)]),
@@ -190,12 +207,19 @@ def oled_read_layer_state(ctx, layer: int, state: LayerState) -> int:
     return load().oled_read_layer_state(ctx, layer, ctypes.byref(state))
 
 
+def oled_collect_stats(ctx) -> dict:
+    st = Stats()
+    _check(ctx, load().oled_collect_stats(ctx, ctypes.byref(st)))
+    return st.as_dict()
+
+
 def oled_profile_collect(ctx, cap: int = 1 << 16):
+    """[(op name, layer, ms, bytes, flops, h2d_bytes)] since the last collection."""
     arr = (OpTime * cap)()
     n = ctypes.c_int32()
     _check(ctx, load().oled_profile_collect(ctx, arr, cap, ctypes.byref(n)))
-    return [(OP_NAMES[arr[i].kind], arr[i].layer, arr[i].ms, arr[i].bytes, arr[i].flops)
-            for i in range(n.value)]
+    return [(OP_NAMES[arr[i].kind], arr[i].layer, arr[i].ms, arr[i].bytes, arr[i].flops,
+             arr[i].h2d_bytes) for i in range(n.value)]
 
 
 def oled_pack_expert(dtype: str, hidden: int, inter: int, w13: np.ndarray, w2: np.ndarray,
@@ -255,12 +279,13 @@ class Context:
 
     def __init__(self, hidden, inter, n_experts, top_k, n_layers, capacity, max_tokens,
                  dtype: str, host_pool: int, host_pool_blocks: int, host_block_of,
-                 device: int = 0, profile_ops: int = 0):
+                 device: int = 0, profile_ops: int = 0, copy_mode: str = "shader"):
         self._hbo = np.ascontiguousarray(host_block_of, dtype=np.int64)
         cfg = OledConfig(hidden, inter, n_experts, top_k, n_layers, capacity, max_tokens,
                          OLED_F32 if dtype == "f32" else OLED_BF16, device,
                          profile_ops, host_pool, host_pool_blocks,
-                         self._hbo.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)))
+                         self._hbo.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
+                         COPY_MODES[copy_mode], 0)
         self.E, self.k, self.L, self.C, self.Tmax = n_experts, top_k, n_layers, capacity, max_tokens
         self.ctx = oled_create(cfg)
 
@@ -281,8 +306,9 @@ class Context:
     def route_block(self, layer, logits, T, stream=None):
         _check(self.ctx, route_block(self.ctx, layer, logits, T, stream))
 
-    def apply_misses(self, layer, copy_stream=None) -> MissReport:
-        rep = MissReport()
+    def apply_misses(self, layer, copy_stream=None, report: bool = True) -> MissReport | None:
+        """With report=False nothing waits for the device (shader transfer)."""
+        rep = MissReport() if report else None
         _check(self.ctx, apply_misses(self.ctx, layer, copy_stream, rep))
         return rep
 
@@ -314,6 +340,9 @@ class Context:
         out["resident_before"] = out["resident_before"].astype(bool)
         out["resident_after"] = out["resident_after"].astype(bool)
         return out
+
+    def collect_stats(self) -> dict:
+        return oled_collect_stats(self.ctx)
 
     def profile_collect(self):
         return oled_profile_collect(self.ctx)

@@ -61,11 +61,12 @@ def compare_control(st_gpu: dict, st_or: dict, T: int, where: str):
 
 
 def run_schedule_gpu(ctx, w: W.Workload, seed: int, layers, n_iters: int, forward: bool,
-                     on_step=None):
+                     on_step=None, report: bool = True):
     """Runs iterations 0..n_iters-1 of block 0 over the given workload layers.
 
     Context layer li stands for workload layer layers[li]. on_step(i, li, state,
-    y) is called after each layer-iteration (state from oled_read_layer_state).
+    y, rep) is called after each layer-iteration (state from
+    oled_read_layer_state, rep the miss report or None).
     """
     dt = HN.torch_dtype(w)
     T = w.tokens
@@ -77,10 +78,20 @@ def run_schedule_gpu(ctx, w: W.Workload, seed: int, layers, n_iters: int, forwar
             if forward:
                 x = HN.to_device(W.activations(w, seed, l, 0, i))
                 y = torch.empty((T, w.hidden), dtype=dt, device="cuda")
-            HN.layer_step(ctx, li, logits, conf, x, y)
+            rep = HN.layer_step(ctx, li, logits, conf, x, y, report=report)
             state = ctx.read_layer_state(li, T)
             if on_step is not None:
-                on_step(i, li, state, None if y is None else HN.from_device(y))
+                on_step(i, li, state, None if y is None else HN.from_device(y), rep)
+
+
+def check_report(rep, st_or: dict, eb: int, where: str):
+    """A miss report against the oracle's layer step (every miss is transferred)."""
+    if rep is None:
+        return
+    assert (rep.n_active, rep.n_hits, rep.n_misses) == (
+        st_or["n_active"], st_or["n_hits"], st_or["n_misses"]), where
+    assert rep.n_resident == int(np.count_nonzero(st_or["resident_before"])), where
+    assert rep.h2d_bytes == st_or["n_misses"] * eb, where
 
 
 def oracle_schedule(w: W.Workload, seed: int, layers, n_iters: int, capacity: int):

@@ -2,7 +2,10 @@
 
 Integer results (routing indices, permutation, counts, hits/misses, priority
 numerators, retained sets) and the fp32 gates must match bit for bit; layer
-outputs within relative L2 1e-5 (fp32) or 2e-2 (bf16).
+outputs within relative L2 1e-5 (fp32) or 2e-2 (bf16). Every read of a
+layer's state also checks slot conservation over the device cache state.
+Both transfers of the misses are covered: workgroups of the hit launches
+("shader", the default) and hipMemcpyAsync on a copy stream ("sdma").
 """
 import sys
 
@@ -15,7 +18,7 @@ from paper_2609_33385_amd import harness as HN
 from paper_2609_33385_amd import oled
 from paper_2609_33385_amd import workload as W
 
-from gpu_common import (OracleWeights, compare_control, oracle_schedule, rel_l2,
+from gpu_common import (OracleWeights, check_report, compare_control, oracle_schedule, rel_l2,
                         run_schedule_gpu, tol)
 
 pytestmark = pytest.mark.gpu
@@ -33,23 +36,25 @@ def _gpu():
 
 
 def _chain(w, seed, layers, n_iters, n_blocks, out_at=None, out_tokens=None, capacity=None,
-           forward=True):
+           forward=True, copy_mode="shader", report=True):
     """Runs a schedule on both sides and compares every layer-iteration.
 
     out_at: set of (layer index, iteration) whose outputs are checked (None: all).
     out_tokens: token rows checked there (None: all).
     """
     C = w.capacity if capacity is None else capacity
-    _say(f"[chain] {w.name} layers={list(layers)} iters={n_iters} C={C} P={n_blocks}")
+    _say(f"[chain] {w.name} layers={list(layers)} iters={n_iters} C={C} P={n_blocks} "
+         f"copy={copy_mode} report={report}")
     pool = HN.fill_pool(w, seed, n_blocks)
-    ctx = HN.make_context(w, pool, capacity=C, n_layers=len(layers))
+    ctx = HN.make_context(w, pool, capacity=C, n_layers=len(layers), copy_mode=copy_mode)
     ref = oracle_schedule(w, seed, layers, n_iters, C)
     ow = OracleWeights(w, seed, n_blocks, len(layers))
     worst = [0.0]
 
-    def check(i, li, st, y):
+    def check(i, li, st, y, rep):
         where = f"{w.name} l={layers[li]} i={i}"
         compare_control(st, ref[i][li], w.tokens, where)
+        check_report(rep, ref[i][li], w.expert_bytes, where)
         if y is None or (out_at is not None and (li, i) not in out_at):
             return
         o = ref[i][li]
@@ -61,16 +66,23 @@ def _chain(w, seed, layers, n_iters, n_blocks, out_at=None, out_tokens=None, cap
         assert err <= tol(w), f"{where}: rel L2 {err:.3e} > {tol(w)}"
 
     try:
-        run_schedule_gpu(ctx, w, seed, layers, n_iters, forward, check)
+        run_schedule_gpu(ctx, w, seed, layers, n_iters, forward, check, report=report)
     finally:
         ctx.close()
         pool.free()
     _say(f"[chain] {w.name} ok, worst rel L2 {worst[0]:.3e}")
 
 
-def test_cfg1_full_schedule():
+@pytest.mark.parametrize("copy_mode", ["shader", "sdma"])
+def test_cfg1_full_schedule(copy_mode):
     w = W.WORKLOADS[1]
-    _chain(w, 0, range(w.n_layers), w.n_iters, w.n_layers * w.n_experts)
+    _chain(w, 0, range(w.n_layers), w.n_iters, w.n_layers * w.n_experts, copy_mode=copy_mode)
+
+
+def test_cfg1_control_path_without_reports():
+    """No forward and no reports: only the transfer-only launch moves misses."""
+    w = W.WORKLOADS[1]
+    _chain(w, 0, range(w.n_layers), w.n_iters, 8, forward=False, report=False)
 
 
 SMALL = [  # (E, k, T, C, dtype, H, I)
@@ -93,6 +105,8 @@ def test_small_shapes(E, k, T, C, dt, H, I):
                                block=T, n_experts=E, top_k=k, hidden=H, inter=I, n_layers=2,
                                n_iters=3, capacity=C)
     _chain(w, 1, range(2), 3, min(2 * E, 24))
+    if E in (5, 64):
+        _chain(w, 1, range(2), 3, min(2 * E, 24), copy_mode="sdma")
 
 
 def test_ties_and_signed_zero():
@@ -117,11 +131,62 @@ def test_ties_and_signed_zero():
         pool.free()
 
 
-def test_cfg2_chain():
+@pytest.mark.parametrize("copy_mode", ["shader", "sdma"])
+def test_cfg2_chain(copy_mode):
     w = W.WORKLOADS[2]
     L, N = w.n_layers, w.n_iters
     out_at = {(l, i) for l in (0, L // 2, L - 1) for i in (0, 1, N - 1)}
-    _chain(w, 0, range(L), N, 64, out_at=out_at)
+    _chain(w, 0, range(L), N, 64, out_at=out_at, copy_mode=copy_mode)
+
+
+def test_cfg2_no_sync_until_the_end():
+    """The bench's call pattern: no report and no host read between layers.
+    Every output, the final resident sets and the routing totals against the
+    oracle."""
+    w = W.WORKLOADS[2]
+    layers, N, T = [0, 5, 11, 15], w.n_iters, w.tokens
+    _say(f"[async] {w.name} layers={layers} iters={N}")
+    pool = HN.fill_pool(w, 0, 64)
+    ctx = HN.make_context(w, pool, n_layers=len(layers))
+    ref = oracle_schedule(w, 0, layers, N, w.capacity)
+    ow = OracleWeights(w, 0, 64, len(layers))
+    s = torch.cuda.current_stream()
+    dt = HN.torch_dtype(w)
+    try:
+        ins = []
+        for i in range(N):
+            conf = torch.from_numpy(W.confidence(w, 0, 0, i)).cuda()
+            for li, l in enumerate(layers):
+                lg = torch.from_numpy(W.logits(w, 0, l, 0, i)).cuda()
+                x = HN.to_device(W.activations(w, 0, l, 0, i))
+                ins.append((i, li, lg, conf, x, torch.empty((T, w.hidden), dtype=dt, device="cuda")))
+        torch.cuda.synchronize()
+        for i, li, lg, conf, x, y in ins:
+            HN.layer_step(ctx, li, lg, conf, x, y, stream=s, report=False)
+        stats = ctx.collect_stats()
+        for li in range(len(layers)):
+            st = ctx.read_layer_state(li, T)
+            np.testing.assert_array_equal(st["resident_after"], ref[N - 1][li]["resident_after"])
+        flat = [ref[i][li] for i in range(N) for li in range(len(layers))]
+        assert stats["layer_iters"] == N * len(layers)
+        assert stats["n_hits"] == sum(o["n_hits"] for o in flat)
+        assert stats["n_misses"] == sum(o["n_misses"] for o in flat)
+        assert stats["n_active"] == sum(o["n_active"] for o in flat)
+        assert stats["h2d_bytes"] == stats["n_misses"] * w.expert_bytes
+        worst = 0.0
+        for i, li, lg, conf, x, y in ins:
+            if (i, li) not in {(0, 0), (1, 2), (N - 1, 3), (N // 2, 1)}:
+                continue
+            o = ref[i][li]
+            xx = O.decode(W.activations(w, 0, layers[li], 0, i))
+            y_ref = O.moe_output(xx, o["idx"], o["gates"], ow.fn(li))
+            err = rel_l2(O.decode(HN.from_device(y)), y_ref)
+            worst = max(worst, err)
+            assert err <= tol(w), f"l={layers[li]} i={i}: rel L2 {err:.3e}"
+        _say(f"[async] ok, worst rel L2 {worst:.3e}")
+    finally:
+        ctx.close()
+        pool.free()
 
 
 def test_cfg3_chain():
@@ -139,30 +204,33 @@ def test_cfg45_chain(wid):
 
 
 def test_cross_residency_bitwise():
-    """Outputs do not depend on the cache state (lossless): C = E, 40%, 0."""
+    """Outputs do not depend on the cache state or the transfer (lossless):
+    C = E, 40% and 0 with the shader transfer, 40% with the copy engine."""
     w = W.WORKLOADS[2]
     layers, N = [0, 1], 4
     pool = HN.fill_pool(w, 0, 16)
     outs = {}
-    for C in (w.n_experts, w.capacity, 0):
-        ctx = HN.make_context(w, pool, capacity=C, n_layers=len(layers))
+    for C, mode in ((w.n_experts, "shader"), (w.capacity, "shader"), (0, "shader"),
+                    (w.capacity, "sdma")):
+        ctx = HN.make_context(w, pool, capacity=C, n_layers=len(layers), copy_mode=mode)
         got = []
         run_schedule_gpu(ctx, w, 0, layers, N, True,
-                         lambda i, li, st, y: got.append((st["n_hits"], y.copy())))
+                         lambda i, li, st, y, rep: got.append((st["n_hits"], y.copy())))
         ctx.close()
-        outs[C] = got
+        outs[(C, mode)] = got
     pool.free()
-    base = outs[w.n_experts]
-    for C, got in outs.items():
+    base = outs[(w.n_experts, "shader")]
+    for key, got in outs.items():
         for (h0, y0), (h1, y1) in zip(base, got):
-            assert np.array_equal(y0, y1), f"C={C}: outputs differ from full residency"
-    assert sum(h for h, _ in outs[0]) == 0
+            assert np.array_equal(y0, y1), f"{key}: outputs differ from full residency"
+    assert sum(h for h, _ in outs[(0, "shader")]) == 0
 
 
-def test_error_paths():
+@pytest.mark.parametrize("copy_mode", ["shader", "sdma"])
+def test_error_paths(copy_mode):
     w = W.WORKLOADS[1]
     pool = HN.fill_pool(w, 0, 8)
-    ctx = HN.make_context(w, pool)
+    ctx = HN.make_context(w, pool, copy_mode=copy_mode)
     T, E = w.tokens, w.n_experts
     s = torch.cuda.current_stream()
     try:
@@ -198,6 +266,34 @@ def test_error_paths():
         assert rep.rejected_layer == 0   # reported once, by the next apply_misses
         ctx.score_and_retain(0, conf, s)
         assert not ctx.read_layer_state(0, T)["rejected"]
+    finally:
+        ctx.close()
+        pool.free()
+
+
+def test_bad_block_without_report():
+    """A non-finite logit with nobody asking for a report: nothing is staged,
+    the retention commits nothing, and the next read of the layer says so once."""
+    w = W.WORKLOADS[1]
+    pool = HN.fill_pool(w, 0, 8)
+    ctx = HN.make_context(w, pool)
+    T = w.tokens
+    s = torch.cuda.current_stream()
+    try:
+        lg = torch.from_numpy(W.logits(w, 0, 0, 0, 0)).cuda()
+        conf = torch.from_numpy(W.confidence(w, 0, 0, 0)).cuda()
+        HN.layer_step(ctx, 0, lg, conf, report=False)
+        before = ctx.read_layer_state(0, T)["resident_after"].copy()
+        bad = torch.from_numpy(W.logits(w, 0, 0, 0, 1)).cuda()
+        bad[7, 1] = float("inf")
+        x = HN.to_device(W.activations(w, 0, 0, 0, 1))
+        y = torch.empty((T, w.hidden), dtype=torch.float32, device="cuda")
+        HN.layer_step(ctx, 0, bad, conf, x, y, report=False)
+        st = ctx.read_layer_state(0, T)
+        assert st["rejected"]                                  # reported once
+        assert np.array_equal(st["resident_after"], before)
+        assert not ctx.read_layer_state(0, T)["rejected"]
+        assert ctx.collect_stats()["n_bad_blocks"] == 1
     finally:
         ctx.close()
         pool.free()

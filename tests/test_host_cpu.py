@@ -1,6 +1,7 @@
 """CPU-only checks of the library: it loads and exports every symbol of the
-header, validates arguments before touching a GPU, and its host cache
-bookkeeping keeps the oracle's resident sets with conserved slots."""
+header, the binding's structures match the header's layout, it validates
+arguments before touching a GPU, and the expert packing follows its
+documented layout."""
 import ctypes
 import os
 import re
@@ -9,13 +10,10 @@ import subprocess
 import numpy as np
 import pytest
 
-from oracle import oled_oracle as O
 from paper_2609_33385_amd import oled
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "oled.h")
-CSRC = os.path.join(ROOT, "paper_2609_33385_amd", "csrc")
-CACHE_LIB = os.path.join(ROOT, "paper_2609_33385_amd", "liboled_cache_host.so")
 
 
 def header_functions():
@@ -53,7 +51,7 @@ def _cfg(**kw):
                         base["n_layers"], base["capacity"], base["max_tokens"], base["dtype"],
                         base["device"], base["profile_ops"], base["host_pool"] or 0,
                         base["host_pool_blocks"],
-                        hbo.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)))
+                        hbo.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), 0, 0)
     return c, hbo
 
 
@@ -86,114 +84,48 @@ def test_null_context_calls():
     lib.oled_destroy(None)
 
 
-# -------------------------------------------------- host cache bookkeeping
-class HostCache:
-    def __init__(self, L, E, C, n_slots):
-        self.lib = ctypes.CDLL(CACHE_LIB)
-        vp, i = ctypes.c_void_p, ctypes.c_int
-        sigs = {"oled_cs_create": (vp, [i, i, i, i]), "oled_cs_destroy": (None, [vp]),
-                "oled_cs_reset": (None, [vp]), "oled_cs_check": (i, [vp]),
-                "oled_cs_free_slots": (i, [vp]),
-                "oled_cs_classify": (None, [vp, i, vp, vp, vp, vp]),
-                "oled_cs_stage": (i, [vp, i, vp, vp, vp]), "oled_cs_drop": (None, [vp, i]),
-                "oled_cs_commit": (i, [vp, i, vp]), "oled_cs_resident": (None, [vp, i, vp]),
-                "oled_cs_slots": (None, [vp, i, vp])}
-        for n, (res, args) in sigs.items():
-            getattr(self.lib, n).restype = res
-            getattr(self.lib, n).argtypes = args
-        self.p = ctypes.c_void_p(self.lib.oled_cs_create(L, E, C, n_slots))
-        self.E = E
-
-    def __del__(self):
-        self.lib.oled_cs_destroy(self.p)
-
-    def classify(self, l, counts):
-        c = np.ascontiguousarray(counts, np.int32)
-        hit, miss, n3 = np.zeros(self.E, np.uint8), np.zeros(self.E, np.uint8), np.zeros(3, np.int32)
-        self.lib.oled_cs_classify(self.p, l, c.ctypes.data, hit.ctypes.data, miss.ctypes.data,
-                                  n3.ctypes.data)
-        return hit.astype(bool), miss.astype(bool), n3
-
-    def stage(self, l, miss):
-        m = np.ascontiguousarray(miss, np.uint8)
-        ex, sl = np.zeros(self.E, np.int32), np.zeros(self.E, np.int32)
-        n = self.lib.oled_cs_stage(self.p, l, m.ctypes.data, ex.ctypes.data, sl.ctypes.data)
-        return n, ex[:max(n, 0)], sl[:max(n, 0)]
-
-    def commit(self, l, keep):
-        k = np.ascontiguousarray(keep, np.uint8)
-        return self.lib.oled_cs_commit(self.p, l, k.ctypes.data) == 1
-
-    def resident(self, l):
-        r = np.zeros(self.E, np.uint8)
-        self.lib.oled_cs_resident(self.p, l, r.ctypes.data)
-        return r.astype(bool)
-
-    def slots(self, l):
-        s = np.zeros(self.E, np.int32)
-        self.lib.oled_cs_slots(self.p, l, s.ctypes.data)
-        return s
-
-    def check(self):
-        return self.lib.oled_cs_check(self.p) == 1
+# ------------------------------------------------------- ABI struct layout
+ABI_STRUCTS = {
+    "oled_config": oled.OledConfig,
+    "oled_miss_report": oled.MissReport,
+    "oled_stats": oled.Stats,
+    "oled_layer_state": oled.LayerState,
+    "oled_op_time": oled.OpTime,
+}
 
 
-@pytest.mark.parametrize("C", [0, 2, 4, 8])
-def test_host_cache_follows_oracle(C):
-    """The bookkeeping stages the oracle's misses and commits its retained sets."""
-    rng = np.random.default_rng(C)
-    L, E, k, T, N = 3, 8, 2, 16, 8
-    hc = HostCache(L, E, C, L * min(C, E) + E)
-    res = [np.zeros(E, bool) for _ in range(L)]
-    walk = np.cumsum(rng.standard_normal((N, L, T, E)) * 0.5, axis=0) + 2 * rng.standard_normal((L, T, E))
-    for i in range(N):
-        conf = rng.uniform(0, 1, T).astype(np.float32)
-        for l in range(L):
-            st = O.layer_step(walk[i, l].astype(np.float32), conf, res[l], k, C)
-            hit, miss, n3 = hc.classify(l, st["counts"])
-            assert np.array_equal(hit, st["hit"]) and np.array_equal(miss, st["miss"])
-            assert tuple(n3) == (st["n_active"], st["n_hits"], st["n_misses"])
-            assert np.array_equal(hc.resident(l), res[l])
-            n, ex, sl = hc.stage(l, miss)
-            assert n == st["n_misses"] and len(set(sl.tolist())) == n
-            before = hc.slots(l)
-            assert hc.commit(l, st["resident_after"])
-            after = hc.slots(l)
-            kept = st["resident_after"]
-            # retained experts keep their slot (residents and staged misses alike)
-            assert np.array_equal(after[kept], before[kept])
-            assert np.all(after[~kept] == -1)
-            assert hc.check()
-            res[l] = st["resident_after"]
-
-
-def test_host_cache_rollback_and_refusals():
-    hc = HostCache(2, 6, 2, 2 * 2 + 6)
-    miss = np.array([1, 1, 1, 0, 0, 0], bool)
-    n, ex, sl = hc.stage(0, miss)
-    assert n == 3 and hc.check()
-    assert hc.stage(0, miss)[0] == -1                       # already staged
-    assert not hc.commit(0, np.array([1, 1, 1, 0, 0, 0]))   # more than C
-    assert not hc.commit(0, np.array([0, 0, 0, 1, 0, 0]))   # not a candidate
-    hc.lib.oled_cs_drop(hc.p, 0)                             # failed copy: roll back
-    assert hc.check() and not hc.resident(0).any()
-    assert hc.lib.oled_cs_free_slots(hc.p) == 10
-    n, ex, sl = hc.stage(0, miss)
-    assert hc.commit(0, np.array([1, 0, 1, 0, 0, 0])) and hc.check()
-    assert hc.lib.oled_cs_free_slots(hc.p) == 8
-
-
-def test_host_cache_sanitized_selftest(tmp_path):
-    exe = tmp_path / "cache_selftest"
-    src = os.path.join(ROOT, "tests", "native", "cache_state_selftest.cpp")
-    r = subprocess.run(["g++", "-std=c++17", "-O1", "-g", "-fsanitize=address,undefined",
-                        "-fno-sanitize-recover=all", f"-I{CSRC}", src,
-                        os.path.join(CSRC, "cache_state.cpp"), "-o", str(exe)],
-                       capture_output=True, text=True)
+def test_binding_structs_match_header(tmp_path):
+    """The ctypes structures have the header's size and field offsets."""
+    lines = ['#include <stddef.h>', '#include <stdio.h>', '#include "oled.h"', 'int main(void) {']
+    for cname, py in ABI_STRUCTS.items():
+        lines.append(f'  printf("{cname} size %zu\\n", sizeof({cname}));')
+        for fname, _ in py._fields_:
+            lines.append(f'  printf("{cname} {fname} %zu\\n", offsetof({cname}, {fname}));')
+    lines += ["  return 0;", "}"]
+    src = tmp_path / "abi.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "abi"
+    r = subprocess.run(["gcc", "-std=c99", f"-I{os.path.join(ROOT, 'include')}", str(src), "-o",
+                        str(exe)], capture_output=True, text=True)
     assert r.returncode == 0, r.stderr
-    r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120)
-    assert r.returncode == 0, r.stdout + r.stderr
-    assert "selftest ok" in r.stdout
+    out = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout
+    got = {}
+    for ln in out.splitlines():
+        cname, key, val = ln.split()
+        got[(cname, key)] = int(val)
+    for cname, py in ABI_STRUCTS.items():
+        assert got[(cname, "size")] == ctypes.sizeof(py), cname
+        for fname, _ in py._fields_:
+            assert got[(cname, fname)] == getattr(py, fname).offset, (cname, fname)
+
+
+def test_create_rejects_bad_copy_mode():
+    lib = oled.load()
+    cfg, _hbo = _cfg(host_pool=1, host_pool_blocks=1)
+    cfg.copy_mode = 5
+    h = ctypes.c_void_p()
+    assert lib.oled_create(ctypes.byref(cfg), ctypes.byref(h)) == oled.OLED_ERR_INVALID_ARG
+    assert b"copy_mode" in lib.oled_last_error(None)
 
 
 # ------------------------------------------------------------ weight packing
