@@ -12,18 +12,19 @@
  *                      waiting for the routing result on the host
  *   apply_misses       misses M = A \ R of the layer (Sec. 4.2): every miss
  *                      is transferred host->device into a staging slot (G = M)
- *                      and computed on the GPU once it has landed; then the
- *                      gate-weighted combine of all k routes of every token
+ *                      and computed on the GPU once it has landed
  *   score_and_retain   reuse priorities p_e (the priority equation of
  *                      Sec. 4.3, psi(c) = c; stale residents score zero) and
- *                      the retention rule R' = Top_C(R u G, p) of Sec. 4.2
+ *                      the retention rule R' = Top_C(R u G, p) of Sec. 4.2;
+ *                      after a forward, in the same launch as the
+ *                      gate-weighted combine of all k routes of every token
  *
  * Call order per (layer, iteration): route_block -> [moe_forward_cached] ->
  * apply_misses -> score_and_retain. Exactly one layer is in flight per
  * context; any other order returns OLED_ERR_STATE and changes nothing.
  * moe_forward_cached may be skipped (control path only: apply_misses then
  * only transfers); the cache state does not depend on expert outputs. The
- * layer output y is complete once the work apply_misses enqueued has run.
+ * layer output y is complete once the work score_and_retain enqueued has run.
  *
  * The cache state (resident sets, slot tables, free slots) lives in device
  * memory and only the library's kernels change it, in stream order: the
@@ -175,7 +176,7 @@ typedef enum {
   OLED_OP_PERMUTE = 1,
   OLED_OP_FFN_UP = 2,        /* grouped gate/up GEMM + SiLU*up epilogue */
   OLED_OP_FFN_DOWN = 3,      /* grouped down GEMM */
-  OLED_OP_COMBINE = 4,
+  OLED_OP_COMBINE = 4,       /* combine + priority/retention launch after a forward */
   OLED_OP_SCORE_RETAIN = 5,
   OLED_OP_H2D = 6            /* copy-engine copies of one apply_misses, or a
                                 transfer-only launch */
@@ -223,14 +224,15 @@ oled_status route_block(void* ctx, int32_t layer, const float* logits_dev, int32
 /*
  * moe_forward_cached: the cached experts of the routed layer (Sec. 4.1).
  *  x_dev: [T][H] dtype (read); y_dev: [T][H] dtype, written by the combine
- *  that apply_misses enqueues: y[t] = sum_j gate[t][j] *
+ *  that score_and_retain enqueues: y[t] = sum_j gate[t][j] *
  *  W2_e (silu(W1_e x[t]) * (W3_e x[t])), e = idx[t][j] (lossless, Sec. 5.1).
  *  Enqueues the grouped GEMMs of the hit experts (A & R, weights read from
  *  their cache slots) on `stream` right away; their work list and count come
  *  from route_block's kernels on the device, so no host synchronisation is
- *  needed. With OLED_COPY_SHADER the same launches also transfer the staged
- *  misses (gate/up weights with the gate/up GEMM, down weights with the
- *  down GEMM). Accumulation is fp32; silu(W1 x) * (W3 x) is stored in dtype.
+ *  needed. With OLED_COPY_SHADER only their gate/up GEMM is enqueued here,
+ *  and its first workgroups transfer the staged misses' gate/up weights; the
+ *  hits' down GEMM follows in apply_misses. Accumulation is fp32;
+ *  silu(W1 x) * (W3 x) is stored in dtype.
  *  Both buffers must stay valid until the layer's work has run.
  *  Errors: STATE (not right after route_block), INVALID_ARG (NULL pointers,
  *  a stream other than route_block's).
@@ -241,16 +243,18 @@ oled_status moe_forward_cached(void* ctx, int32_t layer, const void* x_dev, void
 /*
  * apply_misses: misses M = A \ R of the routed layer (Sec. 4.2) and their
  *  compensation by transfer (G = M), then the combine.
- *  OLED_COPY_SHADER: if moe_forward_cached was called, enqueues the misses'
- *  grouped GEMMs (their weights were transferred by the hit launches) and the
- *  combine into y; else a transfer-only launch. Nothing waits for the device
- *  unless out is non-NULL. copy_stream is not used.
+ *  OLED_COPY_SHADER: if moe_forward_cached was called, enqueues one launch
+ *  holding the hits' down GEMM, the transfer of the misses' down weights and
+ *  the misses' gate/up GEMM (their gate/up weights landed with the hits'
+ *  gate/up launch), then the misses' down GEMM; else a transfer-only launch.
+ *  Nothing waits for the device unless out is non-NULL. copy_stream is not
+ *  used.
  *  OLED_COPY_SDMA: waits for route_block's result, copies every staged miss
  *  with hipMemcpyAsync on copy_stream (NULL: the context's own copy stream),
  *  gate/up weights of all misses first, then their down weights; if
  *  moe_forward_cached was called, launches the misses' GEMMs on the compute
  *  stream as the host sees each half of the copies land (the call returns
- *  once the last copy has landed), then the combine.
+ *  once the last copy has landed).
  *  out (may be NULL): filled from the layer's routing record, which makes the
  *  call wait for route_block's kernel.
  *  Errors: STATE; INVALID_ARG if the record shows a non-finite logit (only
@@ -271,7 +275,8 @@ oled_status apply_misses(void* ctx, int32_t layer, void* copy_stream, oled_miss_
  *  Candidates R u M are ranked by (S desc, previously resident first, id asc)
  *  and the first min(C, |R u M|) stay cached for the next iteration of this
  *  layer; the rest release their slots. The same kernel commits the new
- *  state in device memory (retained misses keep their staging slot).
+ *  state in device memory (retained misses keep their staging slot). After
+ *  moe_forward_cached its launch also holds the combine into y.
  *  Errors: STATE, INVALID_ARG (NULL conf). A confidence outside [0,1] (or NaN)
  *  is detected on the device: the layer keeps its previous R, its transferred
  *  misses are dropped, and the rejection is reported by the next report of

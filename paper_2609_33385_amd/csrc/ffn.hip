@@ -1,6 +1,6 @@
 // K4 grouped SwiGLU expert FFN over the experts of one layer (hits from their
-// cache slots, transferred misses from their staging slots), the transfer of
-// the misses, and K5 the gate-weighted combine (OLED-MoE Sec. 4.1: cache-hit experts execute on the
+// cache slots, transferred misses from their staging slots) and the transfer
+// of the misses (OLED-MoE Sec. 4.1: cache-hit experts execute on the
 // GPU; the output does not depend on where an expert's weights came from).
 //
 // The GEMMs are weight-streaming: a layer iteration routes few tokens to each
@@ -296,18 +296,13 @@ __device__ __forceinline__ void fetch_blocks(const FetchArgs& f, char* pool, int
   }
 }
 
+// The GEMM tiles of one launch part: tiles t0, t0 + stride, ... of the live
+// tile count (stride a multiple of 8, so a workgroup keeps its XCD).
 template <class TR, bool UP, int KS>
-__global__ __launch_bounds__(kThreads) void k_ffn(FfnLaunch a) {
+__device__ __forceinline__ void gemm_tiles(const FfnLaunch& a, int t0, int stride,
+                                           floatx4_t (*s_red)[(UP ? 2 : 1) * kMaxNT][64]) {
   using T = typename TR::T;
   constexpr int FEAT = kFeat * (kWaves / KS);  // output features per tile
-  __shared__ floatx4_t s_red[KS > 1 ? kWaves : 1][(UP ? 2 : 1) * kMaxNT][64];
-
-  const int nfetch = a.fetch.nblk;
-  if (static_cast<int>(blockIdx.x) < nfetch) {
-    fetch_blocks(a.fetch, static_cast<char*>(const_cast<void*>(a.pool)), a.slot_bytes, a.n_slots,
-                 blockIdx.x);
-    return;
-  }
   int base, n_items;
   if (a.n_items_host >= 0) {
     base = a.item_base;
@@ -319,10 +314,9 @@ __global__ __launch_bounds__(kThreads) void k_ffn(FfnLaunch a) {
   }
   const int nf = (UP ? a.I : a.H) / FEAT;
   const int total = n_items * nf;
-  const int stride = static_cast<int>(gridDim.x) - nfetch;  // a multiple of 8 (XCD count)
   const T* src = static_cast<const T*>(a.src);
   T* hout = static_cast<T*>(a.hout);
-  for (int t = static_cast<int>(blockIdx.x) - nfetch; t < total; t += stride) {
+  for (int t = t0; t < total; t += stride) {
     const int v = xcd_order(t, total);
     const int ii = v / nf;
     const int f0 = (v - ii * nf) * FEAT;
@@ -340,39 +334,42 @@ __global__ __launch_bounds__(kThreads) void k_ffn(FfnLaunch a) {
   }
 }
 
+template <class TR, bool UP, int KS>
+__global__ __launch_bounds__(kThreads) void k_ffn(FfnLaunch a) {
+  __shared__ floatx4_t s_red[KS > 1 ? kWaves : 1][(UP ? 2 : 1) * kMaxNT][64];
+  const int nfetch = a.fetch.nblk;
+  const int b = blockIdx.x;
+  if (b < nfetch) {
+    fetch_blocks(a.fetch, static_cast<char*>(const_cast<void*>(a.pool)), a.slot_bytes, a.n_slots, b);
+    return;
+  }
+  gemm_tiles<TR, UP, KS>(a, b - nfetch, static_cast<int>(gridDim.x) - nfetch, s_red);
+}
+
+// One launch for three independent parts: the transfer of the misses' down
+// weights (workgroups [0, nfetch)), the hit experts' down GEMM (the next gd
+// workgroups) and the misses' gate/up GEMM, whose weights the previous launch
+// transferred (the rest).
+template <class TR, int KSD, int KSU>
+__global__ __launch_bounds__(kThreads) void k_ffn_mix(FfnLaunch d, FfnLaunch u, int gd) {
+  __shared__ floatx4_t s_buf[kWaves][2 * kMaxNT][64];
+  const int nfetch = d.fetch.nblk;
+  const int b = blockIdx.x;
+  if (b < nfetch) {
+    fetch_blocks(d.fetch, static_cast<char*>(const_cast<void*>(d.pool)), d.slot_bytes, d.n_slots, b);
+    return;
+  }
+  if (b < nfetch + gd) {
+    gemm_tiles<TR, false, KSD>(d, b - nfetch, gd,
+                               reinterpret_cast<floatx4_t (*)[kMaxNT][64]>(&s_buf[0][0][0]));
+    return;
+  }
+  gemm_tiles<TR, true, KSU>(u, b - nfetch - gd, static_cast<int>(gridDim.x) - nfetch - gd, s_buf);
+}
+
 __global__ __launch_bounds__(kThreads) void k_fetch(char* pool, int64_t slot_bytes, int n_slots,
                                                     FetchArgs f) {
   fetch_blocks(f, pool, slot_bytes, n_slots, blockIdx.x);
-}
-
-// One thread per 4 consecutive outputs of a token; sums its k routes in slot
-// order in fp32 and rounds once.
-template <bool BF16>
-__global__ __launch_bounds__(256) void k_combine(const float* __restrict__ O,
-                                                 const float* __restrict__ gates,
-                                                 const int32_t* __restrict__ inv_perm, int k, int H,
-                                                 void* __restrict__ y) {
-  const int t = blockIdx.y;
-  const int h = (blockIdx.x * 256 + threadIdx.x) * 4;
-  if (h >= H) return;
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int j = 0; j < k; ++j) {
-    const float gj = gates[static_cast<size_t>(t) * k + j];
-    const int pos = inv_perm[static_cast<size_t>(t) * k + j];
-    const float4 o = *reinterpret_cast<const float4*>(O + static_cast<size_t>(pos) * H + h);
-    acc.x = fmaf(gj, o.x, acc.x);
-    acc.y = fmaf(gj, o.y, acc.y);
-    acc.z = fmaf(gj, o.z, acc.z);
-    acc.w = fmaf(gj, o.w, acc.w);
-  }
-  if (BF16) {
-    uint2 packed;
-    packed.x = f32_to_bf16_rne(acc.x) | (static_cast<uint32_t>(f32_to_bf16_rne(acc.y)) << 16);
-    packed.y = f32_to_bf16_rne(acc.z) | (static_cast<uint32_t>(f32_to_bf16_rne(acc.w)) << 16);
-    *reinterpret_cast<uint2*>(static_cast<uint16_t*>(y) + static_cast<size_t>(t) * H + h) = packed;
-  } else {
-    *reinterpret_cast<float4*>(static_cast<float*>(y) + static_cast<size_t>(t) * H + h) = acc;
-  }
 }
 
 // K split of the wavefronts of a tile: a function of K alone, so every launch
@@ -380,18 +377,58 @@ __global__ __launch_bounds__(256) void k_combine(const float* __restrict__ O,
 // at least 256.
 inline int k_split(int K) { return K >= 1024 ? 4 : (K >= 512 ? 2 : 1); }
 
+int part_grid(const FfnLaunch& a, int nf);
+
 template <class TR, bool UP, int KS>
 hipError_t launch_ffn_ks(const FfnLaunch& a, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
   if (a.fetch.nblk % 8) return hipErrorInvalidValue;
-  const int nf = (UP ? a.I : a.H) / (kFeat * (kWaves / KS));
-  int64_t tiles = static_cast<int64_t>(a.max_items) * nf;
-  if (a.max_grid > 0 && tiles > a.max_grid) tiles = a.max_grid;
-  tiles = (tiles + 7) & ~static_cast<int64_t>(7);
-  const int64_t grid = a.fetch.nblk + tiles;
+  const int64_t grid = static_cast<int64_t>(a.fetch.nblk) +
+                       part_grid(a, (UP ? a.I : a.H) / (kFeat * (kWaves / KS)));
   if (grid <= 0) return hipSuccess;
   hipExtLaunchKernelGGL(k_ffn<TR, UP, KS>, dim3(static_cast<unsigned>(grid)), dim3(kThreads), 0, s,
                         ev0, ev1, 0, a);
   return hipGetLastError();
+}
+
+// Workgroups of one GEMM part: max_items * tiles per item, capped at
+// max_grid, rounded up to a multiple of 8.
+int part_grid(const FfnLaunch& a, int nf) {
+  int64_t tiles = static_cast<int64_t>(a.max_items) * nf;
+  if (a.max_grid > 0 && tiles > a.max_grid) tiles = a.max_grid;
+  return static_cast<int>((tiles + 7) & ~static_cast<int64_t>(7));
+}
+
+template <class TR, int KSD, int KSU>
+hipError_t launch_mix_ks(const FfnLaunch& d, const FfnLaunch& u, hipEvent_t ev0, hipEvent_t ev1,
+                         hipStream_t s) {
+  if (d.fetch.nblk % 8) return hipErrorInvalidValue;
+  const int gd = part_grid(d, d.H / (kFeat * (kWaves / KSD)));
+  const int gu = part_grid(u, u.I / (kFeat * (kWaves / KSU)));
+  const int64_t grid = static_cast<int64_t>(d.fetch.nblk) + gd + gu;
+  if (grid <= 0) return hipSuccess;
+  hipExtLaunchKernelGGL(k_ffn_mix<TR, KSD, KSU>, dim3(static_cast<unsigned>(grid)), dim3(kThreads),
+                        0, s, ev0, ev1, 0, d, u, gd);
+  return hipGetLastError();
+}
+
+template <class TR, int KSD>
+hipError_t launch_mix_d(const FfnLaunch& d, const FfnLaunch& u, hipEvent_t ev0, hipEvent_t ev1,
+                        hipStream_t s) {
+  switch (k_split(u.H)) {
+    case 4: return launch_mix_ks<TR, KSD, 4>(d, u, ev0, ev1, s);
+    case 2: return launch_mix_ks<TR, KSD, 2>(d, u, ev0, ev1, s);
+    default: return launch_mix_ks<TR, KSD, 1>(d, u, ev0, ev1, s);
+  }
+}
+
+template <class TR>
+hipError_t launch_mix_t(const FfnLaunch& d, const FfnLaunch& u, hipEvent_t ev0, hipEvent_t ev1,
+                        hipStream_t s) {
+  switch (k_split(d.I)) {
+    case 4: return launch_mix_d<TR, 4>(d, u, ev0, ev1, s);
+    case 2: return launch_mix_d<TR, 2>(d, u, ev0, ev1, s);
+    default: return launch_mix_d<TR, 1>(d, u, ev0, ev1, s);
+  }
 }
 
 template <class TR, bool UP>
@@ -416,24 +453,16 @@ hipError_t launch_ffn_down(bool bf16, const FfnLaunch& a, hipEvent_t ev0, hipEve
               : launch_ffn_t<TrF32, false>(a, ev0, ev1, s);
 }
 
+hipError_t launch_ffn_mix(bool bf16, const FfnLaunch& d, const FfnLaunch& u, hipEvent_t ev0,
+                          hipEvent_t ev1, hipStream_t s) {
+  return bf16 ? launch_mix_t<TrBF16>(d, u, ev0, ev1, s) : launch_mix_t<TrF32>(d, u, ev0, ev1, s);
+}
+
 hipError_t launch_fetch(const void* pool, int64_t slot_bytes, int n_slots, const FetchArgs& f,
                         hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
   if (f.nblk <= 0) return hipSuccess;
   hipExtLaunchKernelGGL(k_fetch, dim3(f.nblk), dim3(kThreads), 0, s, ev0, ev1, 0,
                         static_cast<char*>(const_cast<void*>(pool)), slot_bytes, n_slots, f);
-  return hipGetLastError();
-}
-
-hipError_t launch_combine(bool bf16, const float* O, const float* gates, const int32_t* inv_perm,
-                          int T, int k, int H, void* y, hipEvent_t ev0, hipEvent_t ev1,
-                          hipStream_t s) {
-  const dim3 grid((H + 1023) / 1024, T);
-  if (bf16)
-    hipExtLaunchKernelGGL(k_combine<true>, grid, dim3(256), 0, s, ev0, ev1, 0, O, gates, inv_perm,
-                          k, H, y);
-  else
-    hipExtLaunchKernelGGL(k_combine<false>, grid, dim3(256), 0, s, ev0, ev1, 0, O, gates, inv_perm,
-                          k, H, y);
   return hipGetLastError();
 }
 

@@ -168,20 +168,42 @@ hipError_t launch_ffn_up(bool bf16, const FfnLaunch& a, hipEvent_t ev0, hipEvent
 hipError_t launch_ffn_down(bool bf16, const FfnLaunch& a, hipEvent_t ev0, hipEvent_t ev1,
                            hipStream_t s);
 
+// The hit experts' down GEMM with the transfer of the misses' down weights
+// (d.fetch), and the misses' gate/up GEMM (u), in one launch.
+hipError_t launch_ffn_mix(bool bf16, const FfnLaunch& d, const FfnLaunch& u, hipEvent_t ev0,
+                          hipEvent_t ev1, hipStream_t s);
+
 // Transfer of the staged misses alone (no GEMM tiles).
 hipError_t launch_fetch(const void* pool, int64_t slot_bytes, int n_slots, const FetchArgs& f,
                         hipEvent_t ev0, hipEvent_t ev1, hipStream_t s);
 
-// K5: y[t] = sum_j gate[t][j] * O[inv_perm[t*k + j]], fp32, rounded once to dtype.
-hipError_t launch_combine(bool bf16, const float* O, const float* gates, const int32_t* inv_perm,
-                          int T, int k, int H, void* y, hipEvent_t ev0, hipEvent_t ev1,
-                          hipStream_t s);
+// K6 arguments: priority numerators (per-expert segment sums), Top-C
+// retention and the commit into the device cache state of `layer`.
+struct ScoreArgs {
+  const float* gates;
+  const float* conf;
+  const int32_t* topk_idx;
+  const int32_t* counts;
+  int T, k, E, C, layer, seq;
+  CacheView cv;
+  uint64_t* score_out;
+  RetainOut* out;
+};
 
-// K6: priority numerators (per-expert segment sums), Top-C retention and the
-// commit into the device cache state.
-hipError_t launch_score_retain(const float* gates, const float* conf, const int32_t* topk_idx,
-                               const int32_t* counts, int T, int k, int E, int C, int layer,
-                               const CacheView& cv, uint64_t* score_out, RetainOut* out, int seq,
-                               hipEvent_t ev0, hipEvent_t ev1, hipStream_t s);
+// K5 arguments: y[t] = sum_j gate[t][j] * O[inv_perm[t*k + j]], fp32, rounded
+// once to dtype.
+struct CombineArgs {
+  const float* O;
+  const float* gates;
+  const int32_t* inv_perm;
+  int T, k, H;
+  void* y;
+};
+
+hipError_t launch_score_retain(const ScoreArgs& a, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s);
+
+// K5 and K6 in one launch (the layer's last).
+hipError_t launch_combine_score(bool bf16, const CombineArgs& c, const ScoreArgs& a,
+                                hipEvent_t ev0, hipEvent_t ev1, hipStream_t s);
 
 }  // namespace oled

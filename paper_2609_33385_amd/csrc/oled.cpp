@@ -7,11 +7,13 @@
 // only kernels change it: the routing kernel stages the misses into free
 // slots, the retention kernel commits. With the default shader transfer a
 // layer needs no host synchronisation at all: route_block enqueues the
-// routing kernel; moe_forward_cached the hit experts' gate/up and down GEMMs,
-// whose first workgroups copy the staged misses' weights from the pinned host
-// pool over PCIe meanwhile; apply_misses the misses' GEMMs and the combine;
-// score_and_retain the priority / retention / commit kernel. The host reads
-// the pinned routing records when a caller asks for counts.
+// routing kernel; moe_forward_cached the hit experts' gate/up GEMM, whose
+// first workgroups copy the staged misses' gate/up weights from the pinned
+// host pool over PCIe meanwhile; apply_misses one launch with the hit
+// experts' down GEMM, the copy of the misses' down weights and the misses'
+// gate/up GEMM, then the misses' down GEMM; score_and_retain one launch with
+// the combine and the priority / retention / commit. The host reads the
+// pinned routing records only when a caller asks for counts.
 //
 // With the copy-engine transfer (OLED_COPY_SDMA) apply_misses waits for the
 // routing record, copies the staged misses with hipMemcpyAsync on a side
@@ -54,7 +56,7 @@ enum class Stage { kIdle, kRouted, kHitsQueued, kApplied };
 struct OpRec {
   int kind, layer;
   int route_seq;          // routing record that completes the accounting (0: complete)
-  int part;               // 0 gate/up, 1 down, -1 other
+  int part;               // 0 gate/up, 1 down, 2 hit down + miss gate/up, -1 other
   bool hits;              // hit-expert launch (else miss launch)
   int64_t bytes, flops, h2d;
   hipEvent_t a, b;
@@ -412,6 +414,12 @@ void complete_op(const Ctx* c, OpRec& op, const RouteStats& r) {
     op.flops = 0;
     return;
   }
+  if (op.part == 2) {
+    op.bytes = down_bytes(c, r.n_hits, r.hit_rows) + up_bytes(c, r.n_misses, r.miss_rows);
+    op.flops = down_flops(c, r.hit_rows) + up_flops(c, r.miss_rows);
+    op.h2d = static_cast<int64_t>(r.n_staged) * (c->eb - c->e13);
+    return;
+  }
   const int64_t n = op.hits ? r.n_hits : r.n_misses;
   const int64_t rows = op.hits ? r.hit_rows : r.miss_rows;
   if (op.part == 0) {
@@ -740,8 +748,9 @@ oled_status moe_forward_cached(void* ctx, int32_t layer, const void* x_dev, void
   if (!x_dev || !y_dev) return fail(c, OLED_ERR_INVALID_ARG, "NULL x or y");
   HIP_TRY(c, hipSetDevice(c->device));
   // hits: the active residents, at most min(C, E) experts; their item count
-  // stays on the device. With the shader transfer the first workgroups of
-  // each launch copy the staged misses (gate/up part, then down part).
+  // stays on the device. With the shader transfer the first workgroups of the
+  // launch copy the staged misses' gate/up weights, and the hits' down GEMM
+  // is enqueued by apply_misses (sharing a launch with the misses' gate/up).
   const int64_t routes = static_cast<int64_t>(c->cur_T) * c->K;
   const int max_hit_items =
       c->cap > 0 ? static_cast<int>(std::min<int64_t>(c->cap, routes) + routes / oled::kItemRows) : 0;
@@ -764,19 +773,14 @@ oled_status moe_forward_cached(void* ctx, int32_t layer, const void* x_dev, void
     r.h2d = shader ? -1 : 0;
     op_end(c, ev, r);
   }
-  a.src = c->d_h;
-  if (shader) {
-    a.fetch.off = c->e13;
-    a.fetch.len = c->eb - c->e13;
-  }
-  {
+  if (!shader) {
+    a.src = c->d_h;
     OpEvents ev = op_begin(c, OLED_OP_FFN_DOWN);
     HIP_TRY(c, oled::launch_ffn_down(bf16, a, ev.a, ev.b, s));
     OpRec r = rec(OLED_OP_FFN_DOWN, layer, -1);
     r.route_seq = c->cur_route;
     r.part = 1;
     r.hits = true;
-    r.h2d = shader ? -1 : 0;
     op_end(c, ev, r);
   }
   c->fwd_x = x_dev;
@@ -858,17 +862,6 @@ oled_status apply_misses_sdma(Ctx* c, int layer, hipStream_t cs, const RouteStat
   return OLED_OK;
 }
 
-oled_status launch_combine_of(Ctx* c, int layer) {
-  OpEvents ev = op_begin(c, OLED_OP_COMBINE);
-  const int T = c->cur_T;
-  HIP_TRY(c, oled::launch_combine(c->dtype == OLED_BF16, c->d_O, c->d_gates, c->d_inv, T, c->K,
-                                  c->H, c->fwd_y, ev.a, ev.b, c->cur_stream));
-  op_end(c, ev, rec(OLED_OP_COMBINE, layer,
-                    static_cast<int64_t>(T) * c->K * (c->H * 4 + 8) +
-                        static_cast<int64_t>(T) * c->H * c->esz));
-  return OLED_OK;
-}
-
 oled_status apply_misses(void* ctx, int32_t layer, void* copy_stream, oled_miss_report* out) {
   Ctx* c = static_cast<Ctx*>(ctx);
   if (!c) return OLED_ERR_INVALID_ARG;
@@ -903,20 +896,32 @@ oled_status apply_misses(void* ctx, int32_t layer, void* copy_stream, oled_miss_
   int64_t bytes = 0;
   if (shader) {
     if (c->stage == Stage::kHitsQueued) {
-      // misses: bounded by the staging capacity; the item count is on the device
+      // one launch: the hits' down GEMM + the transfer of the misses' down
+      // weights + the misses' gate/up GEMM (their gate/up weights landed in
+      // the previous launch); then the misses' down GEMM. Miss items are
+      // bounded by the staging capacity; their count is on the device.
       const int64_t routes = static_cast<int64_t>(c->cur_T) * c->K;
+      const int max_hit_items =
+          c->cap > 0 ? static_cast<int>(std::min<int64_t>(c->cap, routes) + routes / oled::kItemRows)
+                     : 0;
       const int max_miss_items =
           static_cast<int>(std::min<int64_t>(c->E, routes) + routes / oled::kItemRows);
-      FfnLaunch a = ffn_args(c, layer, 1, max_miss_items, kMissGridCap);
-      a.src = c->fwd_x;
+      FfnLaunch d = ffn_args(c, layer, 0, max_hit_items, 0);
+      d.src = c->d_h;
+      d.fetch.nblk = kFetchBlocks;
+      d.fetch.off = c->e13;
+      d.fetch.len = c->eb - c->e13;
+      FfnLaunch u = ffn_args(c, layer, 1, max_miss_items, kMissGridCap);
+      u.src = c->fwd_x;
       {
-        OpEvents ev = op_begin(c, OLED_OP_FFN_UP);
-        HIP_TRY(c, oled::launch_ffn_up(bf16, a, ev.a, ev.b, s));
-        OpRec o = rec(OLED_OP_FFN_UP, layer, -1);
+        OpEvents ev = op_begin(c, OLED_OP_FFN_DOWN);
+        HIP_TRY(c, oled::launch_ffn_mix(bf16, d, u, ev.a, ev.b, s));
+        OpRec o = rec(OLED_OP_FFN_DOWN, layer, -1);
         o.route_seq = c->cur_route;
-        o.part = 0;
+        o.part = 2;
         op_end(c, ev, o);
       }
+      FfnLaunch a = ffn_args(c, layer, 1, max_miss_items, kMissGridCap);
       a.src = c->d_h;
       {
         OpEvents ev = op_begin(c, OLED_OP_FFN_DOWN);
@@ -950,10 +955,6 @@ oled_status apply_misses(void* ctx, int32_t layer, void* copy_stream, oled_miss_
       return st;
     }
   }
-  if (c->stage == Stage::kHitsQueued) {
-    st = launch_combine_of(c, layer);
-    if (st != OLED_OK) return st;
-  }
   if (out) {
     out->n_active = r.n_active;
     out->n_hits = r.n_hits;
@@ -985,15 +986,40 @@ oled_status score_and_retain(void* ctx, int32_t layer, const float* conf_dev, vo
     c->copies_outstanding = false;
   }
   const int seq = ++c->seq;
-  {
+  oled::ScoreArgs a;
+  a.gates = c->d_gates;
+  a.conf = static_cast<const float*>(conf_dev);
+  a.topk_idx = c->d_topk;
+  a.counts = c->d_counts;
+  a.T = c->cur_T;
+  a.k = c->K;
+  a.E = c->E;
+  a.C = c->C;
+  a.layer = layer;
+  a.seq = seq;
+  a.cv = view(c);
+  a.score_out = c->d_score + static_cast<size_t>(layer) * c->E;
+  a.out = &c->h_ret[layer];
+  const int64_t score_bytes = static_cast<int64_t>(c->cur_T) * c->K * 12 +
+                              static_cast<int64_t>(c->cur_T) * 4 + static_cast<int64_t>(c->E) * 16;
+  if (c->fwd_y) {  // the forward ran: the combine shares the launch
+    oled::CombineArgs cb;
+    cb.O = c->d_O;
+    cb.gates = c->d_gates;
+    cb.inv_perm = c->d_inv;
+    cb.T = c->cur_T;
+    cb.k = c->K;
+    cb.H = c->H;
+    cb.y = c->fwd_y;
+    OpEvents ev = op_begin(c, OLED_OP_COMBINE);
+    HIP_TRY(c, oled::launch_combine_score(c->dtype == OLED_BF16, cb, a, ev.a, ev.b, s));
+    op_end(c, ev, rec(OLED_OP_COMBINE, layer,
+                      static_cast<int64_t>(c->cur_T) * c->K * (c->H * 4 + 8) +
+                          static_cast<int64_t>(c->cur_T) * c->H * c->esz + score_bytes));
+  } else {
     OpEvents ev = op_begin(c, OLED_OP_SCORE_RETAIN);
-    HIP_TRY(c, oled::launch_score_retain(c->d_gates, static_cast<const float*>(conf_dev),
-                                         c->d_topk, c->d_counts, c->cur_T, c->K, c->E, c->C, layer,
-                                         view(c), c->d_score + static_cast<size_t>(layer) * c->E,
-                                         &c->h_ret[layer], seq, ev.a, ev.b, s));
-    op_end(c, ev, rec(OLED_OP_SCORE_RETAIN, layer,
-                      static_cast<int64_t>(c->cur_T) * c->K * 12 +
-                          static_cast<int64_t>(c->cur_T) * 4 + static_cast<int64_t>(c->E) * 16));
+    HIP_TRY(c, oled::launch_score_retain(a, ev.a, ev.b, s));
+    op_end(c, ev, rec(OLED_OP_SCORE_RETAIN, layer, score_bytes));
   }
   c->ret_seq[layer] = seq;
   c->ret_seen[layer] = 0;

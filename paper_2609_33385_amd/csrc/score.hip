@@ -1,4 +1,5 @@
-// K6 reuse priority and retention of one layer (OLED-MoE Sec. 4.3 priority
+// K5 the gate-weighted combine of the layer output and K6 the reuse priority
+// and retention of one layer (OLED-MoE Sec. 4.3 priority
 // p_e = sum_t g_te psi(c_t) / normaliser with psi(c) = c, stale residents at
 // zero; Sec. 4.2 retention R' = Top_C(R u G, p) with G = M), committed into
 // the device-resident cache state: slots of evicted residents and of misses
@@ -24,11 +25,15 @@ __device__ __forceinline__ bool ranks_above(unsigned long long sa, bool ra, int 
   return sa > sb || (sa == sb && (ra > rb || (ra == rb && a < b)));
 }
 
-__global__ __launch_bounds__(kThreads) void k_score_retain(
-    const float* __restrict__ gates, const float* __restrict__ conf,
-    const int32_t* __restrict__ topk_idx, const int32_t* __restrict__ counts, int T, int k, int E,
-    int C, int layer, CacheView cv, uint64_t* __restrict__ score_out, RetainOut* __restrict__ out,
-    int seq) {
+__device__ __forceinline__ void score_body(const ScoreArgs& a) {
+  const float* __restrict__ gates = a.gates;
+  const float* __restrict__ conf = a.conf;
+  const int32_t* __restrict__ topk_idx = a.topk_idx;
+  const int32_t* __restrict__ counts = a.counts;
+  const int T = a.T, k = a.k, E = a.E, C = a.C, layer = a.layer;
+  const CacheView& cv = a.cv;
+  uint64_t* __restrict__ score_out = a.score_out;
+  RetainOut* __restrict__ out = a.out;
   __shared__ unsigned long long s_S[kMaxExperts];
   __shared__ uint32_t s_rc[kMaxExperts];  // bit 1: previously resident, bit 0: candidate
   __shared__ int32_t s_rank[kMaxExperts];
@@ -146,17 +151,70 @@ __global__ __launch_bounds__(kThreads) void k_score_retain(
   }
   // publish: fields, system-scope fence, then seq
   __threadfence_system();
-  if (lane == 0) *reinterpret_cast<volatile int32_t*>(&out->seq) = seq;
+  if (lane == 0) *reinterpret_cast<volatile int32_t*>(&out->seq) = a.seq;
+}
+
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return static_cast<uint16_t>((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+
+// K5 for 1024 outputs of token t: one thread per 4 consecutive outputs sums
+// the token's k routes in slot order in fp32 and rounds once.
+template <bool BF16>
+__device__ __forceinline__ void combine_body(const CombineArgs& c, int t, int hb) {
+  const int h = (hb * 256 + static_cast<int>(threadIdx.x)) * 4;
+  if (h >= c.H) return;
+  const int k = c.k, H = c.H;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int j = 0; j < k; ++j) {
+    const float gj = c.gates[static_cast<size_t>(t) * k + j];
+    const int pos = c.inv_perm[static_cast<size_t>(t) * k + j];
+    const float4 o = *reinterpret_cast<const float4*>(c.O + static_cast<size_t>(pos) * H + h);
+    acc.x = fmaf(gj, o.x, acc.x);
+    acc.y = fmaf(gj, o.y, acc.y);
+    acc.z = fmaf(gj, o.z, acc.z);
+    acc.w = fmaf(gj, o.w, acc.w);
+  }
+  if (BF16) {
+    uint2 packed;
+    packed.x = f32_to_bf16_rne(acc.x) | (static_cast<uint32_t>(f32_to_bf16_rne(acc.y)) << 16);
+    packed.y = f32_to_bf16_rne(acc.z) | (static_cast<uint32_t>(f32_to_bf16_rne(acc.w)) << 16);
+    *reinterpret_cast<uint2*>(static_cast<uint16_t*>(c.y) + static_cast<size_t>(t) * H + h) = packed;
+  } else {
+    *reinterpret_cast<float4*>(static_cast<float*>(c.y) + static_cast<size_t>(t) * H + h) = acc;
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void k_score_retain(ScoreArgs a) { score_body(a); }
+
+// The layer's last launch: workgroup 0 scores and commits the retention,
+// workgroups 1.. combine (the two parts touch disjoint data).
+template <bool BF16>
+__global__ __launch_bounds__(kThreads) void k_combine_score(CombineArgs c, ScoreArgs a) {
+  const int b = blockIdx.x;
+  if (b == 0) {
+    score_body(a);
+    return;
+  }
+  const int hx = (c.H + 1023) / 1024;
+  combine_body<BF16>(c, (b - 1) / hx, (b - 1) % hx);
 }
 
 }  // namespace
 
-hipError_t launch_score_retain(const float* gates, const float* conf, const int32_t* topk_idx,
-                               const int32_t* counts, int T, int k, int E, int C, int layer,
-                               const CacheView& cv, uint64_t* score_out, RetainOut* out, int seq,
-                               hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
-  hipExtLaunchKernelGGL(k_score_retain, dim3(1), dim3(kThreads), 0, s, ev0, ev1, 0, gates, conf,
-                        topk_idx, counts, T, k, E, C, layer, cv, score_out, out, seq);
+hipError_t launch_score_retain(const ScoreArgs& a, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
+  hipExtLaunchKernelGGL(k_score_retain, dim3(1), dim3(kThreads), 0, s, ev0, ev1, 0, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_combine_score(bool bf16, const CombineArgs& c, const ScoreArgs& a,
+                                hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
+  const int grid = 1 + c.T * ((c.H + 1023) / 1024);
+  if (bf16)
+    hipExtLaunchKernelGGL(k_combine_score<true>, dim3(grid), dim3(kThreads), 0, s, ev0, ev1, 0, c, a);
+  else
+    hipExtLaunchKernelGGL(k_combine_score<false>, dim3(grid), dim3(kThreads), 0, s, ev0, ev1, 0, c, a);
   return hipGetLastError();
 }
 
