@@ -372,10 +372,12 @@ __global__ __launch_bounds__(kThreads) void k_fetch(char* pool, int64_t slot_byt
   fetch_blocks(f, pool, slot_bytes, n_slots, blockIdx.x);
 }
 
-// K split of the wavefronts of a tile: a function of K alone, so every launch
-// over an expert reduces in the same order. Each wavefront keeps a K range of
-// at least 256.
-inline int k_split(int K) { return K >= 1024 ? 4 : (K >= 512 ? 2 : 1); }
+// K split of the wavefronts of a tile: a function of the GEMM and its K
+// alone, so every launch over an expert reduces in the same order. Gate/up
+// (K = H) keeps a K range of at least 256 per wavefront; down (K = I) splits
+// only from 2048 on, so a tile streams longer weight rows.
+inline int k_split_up(int K) { return K >= 1024 ? 4 : (K >= 512 ? 2 : 1); }
+inline int k_split_down(int K) { return K >= 4096 ? 4 : (K >= 2048 ? 2 : 1); }
 
 int part_grid(const FfnLaunch& a, int nf);
 
@@ -414,7 +416,7 @@ hipError_t launch_mix_ks(const FfnLaunch& d, const FfnLaunch& u, hipEvent_t ev0,
 template <class TR, int KSD>
 hipError_t launch_mix_d(const FfnLaunch& d, const FfnLaunch& u, hipEvent_t ev0, hipEvent_t ev1,
                         hipStream_t s) {
-  switch (k_split(u.H)) {
+  switch (k_split_up(u.H)) {
     case 4: return launch_mix_ks<TR, KSD, 4>(d, u, ev0, ev1, s);
     case 2: return launch_mix_ks<TR, KSD, 2>(d, u, ev0, ev1, s);
     default: return launch_mix_ks<TR, KSD, 1>(d, u, ev0, ev1, s);
@@ -424,7 +426,7 @@ hipError_t launch_mix_d(const FfnLaunch& d, const FfnLaunch& u, hipEvent_t ev0, 
 template <class TR>
 hipError_t launch_mix_t(const FfnLaunch& d, const FfnLaunch& u, hipEvent_t ev0, hipEvent_t ev1,
                         hipStream_t s) {
-  switch (k_split(d.I)) {
+  switch (k_split_down(d.I)) {
     case 4: return launch_mix_d<TR, 4>(d, u, ev0, ev1, s);
     case 2: return launch_mix_d<TR, 2>(d, u, ev0, ev1, s);
     default: return launch_mix_d<TR, 1>(d, u, ev0, ev1, s);
@@ -433,7 +435,7 @@ hipError_t launch_mix_t(const FfnLaunch& d, const FfnLaunch& u, hipEvent_t ev0, 
 
 template <class TR, bool UP>
 hipError_t launch_ffn_t(const FfnLaunch& a, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
-  switch (k_split(UP ? a.H : a.I)) {
+  switch (UP ? k_split_up(a.H) : k_split_down(a.I)) {
     case 4: return launch_ffn_ks<TR, UP, 4>(a, ev0, ev1, s);
     case 2: return launch_ffn_ks<TR, UP, 2>(a, ev0, ev1, s);
     default: return launch_ffn_ks<TR, UP, 1>(a, ev0, ev1, s);

@@ -44,8 +44,8 @@ struct CacheView {
   int n_slots;
 };
 
-// One routing call, written by the permute stage into a pinned ring at
-// seq % kStatsRing (fields, system-scope fence, then seq).
+// One routing call, written by the permute stage into a device ring at
+// seq % kStatsRing; the host copies records out at its synchronisation points.
 struct RouteStats {
   int32_t layer;
   int32_t n_active;
@@ -61,17 +61,17 @@ struct RouteStats {
   int32_t seq;
 };
 
-// Staged misses of the last routing call, for host-issued copies (written by
-// the permute stage when asked; seq last, after a system-scope fence).
+// Staged misses and the record of the last routing call, for host-issued
+// copies: written by the permute stage into coherent pinned host memory when
+// asked (fields, system-scope fence, then seq).
 struct StagedList {
-  int32_t n;
+  RouteStats rec;
   int32_t exp[kMaxExperts];
   int32_t slot[kMaxExperts];
   int32_t seq;
 };
 
-// Written by the retention kernel into coherent pinned host memory, one per
-// layer (seq last, after a system-scope fence).
+// Written by the retention kernel into device memory, one per layer.
 struct RetainOut {
   uint32_t retained[kMaxExperts / 32];  // bit e: expert e stays cached
   int32_t bad_conf;    // a confidence outside [0, 1] was seen: nothing changed
@@ -141,7 +141,7 @@ struct PermuteOut {
   int32_t* inv_perm;
   WorkItem* items;
   int32_t* item_counts;   // [2] hit items, miss items
-  RouteStats* ring;       // pinned
+  RouteStats* ring;       // device ring of routing records
   StagedList* staged;     // pinned, or null
   int layer, E, seq;
   CacheView cv;
@@ -187,7 +187,7 @@ struct ScoreArgs {
   int T, k, E, C, layer, seq;
   CacheView cv;
   uint64_t* score_out;
-  RetainOut* out;
+  RetainOut* out;         // device, one per layer
 };
 
 // K5 arguments: y[t] = sum_j gate[t][j] * O[inv_perm[t*k + j]], fp32, rounded

@@ -49,7 +49,7 @@ using oled::WorkItem;
 thread_local std::string g_create_error;
 
 constexpr int kFetchBlocks = 64;    // workgroups of a launch that copy misses (multiple of 8)
-constexpr int kMissGridCap = 1024;  // GEMM workgroups of a miss launch (they loop over tiles)
+constexpr int kMissGridCap = 256;   // GEMM workgroups of a miss launch (they loop over tiles)
 
 enum class Stage { kIdle, kRouted, kHitsQueued, kApplied };
 
@@ -98,10 +98,14 @@ struct Ctx {
   int32_t* d_last_counts = nullptr;  // [L][4]
   int32_t* d_free = nullptr;       // [n_slots]
   uint64_t* d_host_addr = nullptr; // [L][E]
-  // coherent pinned host memory written by kernels
-  RouteStats* h_ring = nullptr;    // [kStatsRing]
+  // records written by kernels: device memory, copied out at synchronisation
+  // points into pinned mirrors; the staged list for host-issued copies is
+  // published straight into coherent pinned memory
+  RouteStats* d_ring = nullptr;    // [kStatsRing]
+  RetainOut* d_ret = nullptr;      // [L]
+  RouteStats* h_ring = nullptr;    // [kStatsRing] pinned mirror
+  RetainOut* h_ret = nullptr;      // [L] pinned mirror
   StagedList* h_staged = nullptr;
-  RetainOut* h_ret = nullptr;      // [L]
   // streams and events
   hipStream_t own_copy = nullptr;
   hipEvent_t ev_up = nullptr, ev_down = nullptr, ev_order = nullptr;
@@ -111,6 +115,7 @@ struct Ctx {
   std::vector<RouteStats> recs;    // consumed records kept for the profile accounting
   oled_stats acc{};                // accumulated since the last oled_collect_stats
   int bad_route_layer = -1;        // a bad block seen in a record, not yet reported
+  int reported_bad_route = 0;      // routing call whose bad block apply_misses reported
   // retention results
   int seq = 0;
   std::vector<int> ret_seq;        // [L] sequence number of the last retention (0: none)
@@ -238,20 +243,32 @@ oled_status wait_event_spin(Ctx* c, hipEvent_t ev, const char* what) {
   }
 }
 
-// Consumes routing records in order: all that are already published, and
-// every record up to `until`, waiting for those.
-oled_status drain_records(Ctx* c, int until) {
-  while (c->next_stat <= c->route_n) {
-    const RouteStats& r = c->h_ring[c->next_stat % oled::kStatsRing];
-    const volatile int32_t* ps = &r.seq;
-    if (*ps != c->next_stat) {
-      if (c->next_stat > until) return OLED_OK;
-      const oled_status st = wait_published(c, &r.seq, c->next_stat, c->cur_stream, "routing record");
-      if (st != OLED_OK) return st;
-    }
-    std::atomic_thread_fence(std::memory_order_acquire);
-    RouteStats v = r;
-    v.seq = c->next_stat;
+// Copies the routing records up to `until` and every layer's retention
+// result out of device memory (one synchronisation of the compute stream,
+// skipped when there is nothing new to read) and consumes the records in
+// order.
+oled_status drain_records(Ctx* c, int until, bool retentions = true) {
+  if (until > c->route_n) until = c->route_n;
+  bool pending_ret = false;
+  for (int l = 0; retentions && l < c->L; ++l) pending_ret |= c->ret_seq[l] != 0 && !c->ret_seen[l];
+  if ((c->next_stat > until && !pending_ret) || !c->have_stream) return OLED_OK;
+  hipStream_t s = c->cur_stream;
+  const int first = c->next_stat;
+  const int n = until >= first ? until - first + 1 : 0;
+  int idx = first % oled::kStatsRing;
+  int left = n;
+  while (left > 0) {
+    const int len = std::min(left, oled::kStatsRing - idx);
+    HIP_TRY(c, hipMemcpyAsync(c->h_ring + idx, c->d_ring + idx, sizeof(RouteStats) * len,
+                              hipMemcpyDeviceToHost, s));
+    left -= len;
+    idx = 0;
+  }
+  HIP_TRY(c, hipMemcpyAsync(c->h_ret, c->d_ret, sizeof(RetainOut) * c->L, hipMemcpyDeviceToHost, s));
+  HIP_TRY(c, hipStreamSynchronize(s));
+  for (int q = first; q <= until; ++q) {
+    const RouteStats& v = c->h_ring[q % oled::kStatsRing];
+    if (v.seq != q) return fail(c, OLED_ERR_HIP, "routing record %d missing (found %d)", q, v.seq);
     c->acc.layer_iters += 1;
     c->acc.n_active += v.n_active;
     c->acc.n_hits += v.n_hits;
@@ -260,28 +277,14 @@ oled_status drain_records(Ctx* c, int until) {
     c->acc.h2d_bytes += static_cast<int64_t>(v.n_staged) * c->eb;
     if (v.bad) {
       c->acc.n_bad_blocks += 1;
-      c->bad_route_layer = v.layer;
+      if (v.seq != c->reported_bad_route) c->bad_route_layer = v.layer;
     }
     if (c->profile_ops) c->recs.push_back(v);
-    ++c->next_stat;
   }
-  return OLED_OK;
-}
-
-const RouteStats* find_record(const Ctx* c, int seq) {
-  for (auto it = c->recs.rbegin(); it != c->recs.rend(); ++it)
-    if (it->seq == seq) return &*it;
-  return nullptr;
-}
-
-// Reads the retention results that have been published (every retention
-// enqueued before a published routing record, or before a synchronisation).
-void read_retentions(Ctx* c) {
+  if (n > 0) c->next_stat = until + 1;
+  // retentions: every one enqueued before the last consumed routing has run
   for (int l = 0; l < c->L; ++l) {
-    if (c->ret_seq[l] == 0 || c->ret_seen[l]) continue;
-    const volatile int32_t* ps = &c->h_ret[l].seq;
-    if (*ps != c->ret_seq[l]) continue;
-    std::atomic_thread_fence(std::memory_order_acquire);
+    if (c->ret_seq[l] == 0 || c->ret_seen[l] || c->h_ret[l].seq != c->ret_seq[l]) continue;
     c->ret_seen[l] = 1;
     if (c->h_ret[l].bad_conf) {
       c->rejected[l] = 1;
@@ -290,6 +293,13 @@ void read_retentions(Ctx* c) {
       c->rejected[l] = 0;
     }
   }
+  return OLED_OK;
+}
+
+const RouteStats* find_record(const Ctx* c, int seq) {
+  for (auto it = c->recs.rbegin(); it != c->recs.rend(); ++it)
+    if (it->seq == seq) return &*it;
+  return nullptr;
 }
 
 void free_ctx(Ctx* c) {
@@ -314,6 +324,8 @@ void free_ctx(Ctx* c) {
   if (c->h_ring) (void)hipHostFree(c->h_ring);
   if (c->h_staged) (void)hipHostFree(c->h_staged);
   if (c->h_ret) (void)hipHostFree(c->h_ret);
+  if (c->d_ring) (void)hipFree(c->d_ring);
+  if (c->d_ret) (void)hipFree(c->d_ret);
   delete c;
 }
 
@@ -613,10 +625,14 @@ oled_status oled_create(const oled_config* cfg, void** ctx_out) {
       return oom("host block table");
   }
   if (hipHostMalloc(reinterpret_cast<void**>(&c->h_ring), sizeof(RouteStats) * oled::kStatsRing,
-                    hipHostMallocCoherent) ||
+                    hipHostMallocDefault) ||
       hipHostMalloc(reinterpret_cast<void**>(&c->h_staged), sizeof(StagedList), hipHostMallocCoherent) ||
-      hipHostMalloc(reinterpret_cast<void**>(&c->h_ret), sizeof(RetainOut) * c->L, hipHostMallocCoherent))
+      hipHostMalloc(reinterpret_cast<void**>(&c->h_ret), sizeof(RetainOut) * c->L, hipHostMallocDefault))
     return oom("pinned records");
+  if (dev_alloc(&c->d_ring, oled::kStatsRing) || dev_alloc(&c->d_ret, c->L) ||
+      hipMemset(c->d_ring, 0, sizeof(RouteStats) * oled::kStatsRing) != hipSuccess ||
+      hipMemset(c->d_ret, 0, sizeof(RetainOut) * c->L) != hipSuccess)
+    return oom("record rings");
   std::memset(c->h_ring, 0, sizeof(RouteStats) * oled::kStatsRing);
   std::memset(c->h_staged, 0, sizeof(StagedList));
   std::memset(c->h_ret, 0, sizeof(RetainOut) * c->L);
@@ -664,6 +680,7 @@ oled_status oled_reset_cache(void* ctx) {
   std::fill(c->rejected.begin(), c->rejected.end(), 0);
   c->rejected_layer = -1;
   c->bad_route_layer = -1;
+  c->reported_bad_route = 0;
   return OLED_OK;
 }
 
@@ -687,7 +704,7 @@ oled_status route_block(void* ctx, int32_t layer, const float* logits_dev, int32
   }
   // consume what has been published; this call's ring entry must be free
   const int n = c->route_n + 1;
-  st = drain_records(c, n - oled::kStatsRing);
+  st = drain_records(c, n - oled::kStatsRing, false);
   if (st != OLED_OK) return st;
 
   PermuteOut o;
@@ -697,7 +714,7 @@ oled_status route_block(void* ctx, int32_t layer, const float* logits_dev, int32
   o.inv_perm = c->d_inv;
   o.items = c->d_items;
   o.item_counts = c->d_item_counts;
-  o.ring = c->h_ring;
+  o.ring = c->d_ring;
   o.staged = c->copy_mode == OLED_COPY_SDMA ? c->h_staged : nullptr;
   o.layer = layer;
   o.E = c->E;
@@ -796,11 +813,9 @@ oled_status moe_forward_cached(void* ctx, int32_t layer, const void* x_dev, void
 oled_status apply_misses_sdma(Ctx* c, int layer, hipStream_t cs, const RouteStats& r,
                               int64_t* bytes_out) {
   hipStream_t s = c->cur_stream;
-  oled_status st = wait_published(c, &c->h_staged->seq, c->cur_route, s, "staged misses");
-  if (st != OLED_OK) return st;
-  const int n = c->h_staged->n;
-  if (n != r.n_staged || n < 0 || n > c->E)
-    return fail(c, OLED_ERR_HIP, "staged list disagrees with the routing record");
+  oled_status st = OLED_OK;
+  const int n = c->h_staged->rec.n_staged;
+  if (n < 0 || n > c->E) return fail(c, OLED_ERR_HIP, "staged list out of range");
   int64_t bytes = 0;
   if (n > 0) {
     OpEvents ev = op_begin(c, OLED_OP_H2D);
@@ -877,21 +892,28 @@ oled_status apply_misses(void* ctx, int32_t layer, void* copy_stream, oled_miss_
   const bool shader = c->copy_mode == OLED_COPY_SHADER;
   const bool bf16 = c->dtype == OLED_BF16;
   RouteStats r{};
-  if (!shader || out) {  // the layer's routing record is needed
+  if (!shader) {  // copy engine: staged list and record, published by the routing kernel
+    st = wait_published(c, &c->h_staged->seq, c->cur_route, s, "staged misses");
+    if (st != OLED_OK) {
+      c->stage = Stage::kIdle;
+      return st;
+    }
+    r = c->h_staged->rec;
+  } else if (out) {  // a report synchronises the compute stream
     st = drain_records(c, c->cur_route);
     if (st != OLED_OK) {
       c->stage = Stage::kIdle;
       return st;
     }
     r = c->h_ring[c->cur_route % oled::kStatsRing];
-    read_retentions(c);  // every retention enqueued before this routing has run
-    if (r.bad) {
-      if (c->bad_route_layer == layer) c->bad_route_layer = -1;  // reported here
-      c->stage = Stage::kIdle;
-      return fail(c, OLED_ERR_INVALID_ARG,
-                  "bad block at layer %d (non-finite router logit): nothing staged, cache "
-                  "unchanged", layer);
-    }
+  }
+  if ((out || !shader) && r.bad) {
+    c->reported_bad_route = c->cur_route;
+    if (c->bad_route_layer == layer) c->bad_route_layer = -1;  // reported here
+    c->stage = Stage::kIdle;
+    return fail(c, OLED_ERR_INVALID_ARG,
+                "bad block at layer %d (non-finite router logit): nothing staged, cache "
+                "unchanged", layer);
   }
   int64_t bytes = 0;
   if (shader) {
@@ -999,7 +1021,7 @@ oled_status score_and_retain(void* ctx, int32_t layer, const float* conf_dev, vo
   a.seq = seq;
   a.cv = view(c);
   a.score_out = c->d_score + static_cast<size_t>(layer) * c->E;
-  a.out = &c->h_ret[layer];
+  a.out = c->d_ret + layer;
   const int64_t score_bytes = static_cast<int64_t>(c->cur_T) * c->K * 12 +
                               static_cast<int64_t>(c->cur_T) * 4 + static_cast<int64_t>(c->E) * 16;
   if (c->fwd_y) {  // the forward ran: the combine shares the launch
@@ -1036,7 +1058,6 @@ oled_status oled_read_layer_state(void* ctx, int32_t layer, oled_layer_state* ou
   HIP_TRY(c, hipDeviceSynchronize());
   oled_status st = drain_records(c, c->route_n);
   if (st != OLED_OK) return st;
-  read_retentions(c);
   const int T = (c->last_routed_layer == layer) ? c->last_routed_T : 0;
   const size_t R = static_cast<size_t>(T) * c->K;
   out->tokens = T;

@@ -10,101 +10,118 @@
 namespace oled {
 namespace {
 
-// Orderable 64-bit key: (logit as an order-preserving uint32, ~expert id).
-// The larger key is the larger logit, and on equal logits the lower id.
-__device__ __forceinline__ uint64_t route_key(float v, int e) {
+// Order-preserving 32-bit key of a logit (-0.0 ranks equal to +0.0).
+__device__ __forceinline__ uint32_t ord_key(float v) {
   uint32_t b = __float_as_uint(v);
-  if ((b << 1) == 0u) b = 0u;  // -0.0 ranks equal to +0.0
-  const uint32_t ord = (b & 0x80000000u) ? ~b : (b | 0x80000000u);
-  return (static_cast<uint64_t>(ord) << 32) | (0xFFFFFFFFu - static_cast<uint32_t>(e));
+  if ((b << 1) == 0u) b = 0u;
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
 }
 
-__device__ __forceinline__ float key_value(uint64_t key) {
-  const uint32_t ord = static_cast<uint32_t>(key >> 32);
-  return __uint_as_float((ord & 0x80000000u) ? (ord & 0x7FFFFFFFu) : ~ord);
+__device__ __forceinline__ float ord_value(uint32_t o) {
+  return __uint_as_float((o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o);
 }
 
-__device__ __forceinline__ uint64_t bcast_u64(uint64_t v, int lane) {
-  const uint32_t lo = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(v)), lane);
-  const uint32_t hi = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(v >> 32)), lane);
-  return (static_cast<uint64_t>(hi) << 32) | lo;
+// Maximum over the 64 lanes of a wavefront of values >= 0 (DPP row shifts
+// and row broadcasts as in an inclusive scan; lane 63 ends with the maximum).
+__device__ __forceinline__ uint32_t wave_max(uint32_t v) {
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x111, 0xf, 0xf, true)));
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x112, 0xf, 0xf, true)));
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x114, 0xf, 0xf, true)));
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x118, 0xf, 0xf, true)));
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x142, 0xa, 0xf, false)));
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x143, 0xc, 0xf, false)));
+  return static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v), 63));
 }
 
-// Routes one token with one wavefront; lane l holds logits l, l+64, ... (EPL
-// per lane). Each key's rank is the number of keys above it (all E keys are
-// broadcast lane by lane); the keys of rank j < k fill slot j, so the slots
-// are ordered by (logit desc, id asc). Slot j's expert and logit pass through
-// LDS (s_e, s_v: this wavefront's k entries); lane j < k takes
-// e_j = exp(l_j - l_0) in fp64, every lane sums e_0 + ... + e_{k-1} in slot
-// order (through s_x), and lane j returns g_j = fl32(e_j / s) and its expert
-// (else -1). `bad` collects non-finite logits.
+__device__ __forceinline__ double readlane_f64(double x, int lane) {
+  const uint64_t b = __double_as_longlong(x);
+  const uint32_t lo = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(b)), lane);
+  const uint32_t hi = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(b >> 32)), lane);
+  return __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(hi) << 32) | lo));
+}
+
+// Routes one token with one wavefront; lane l owns experts l, l+64, ... (EPL
+// per lane) of the logit row (global memory or LDS). Slot j takes the largest
+// remaining key in the order (logit desc, id asc): a wavefront maximum of the
+// ordered keys, then the lowest expert id holding it (ballots in expert
+// order), which leaves the candidates. Keys of valid experts are >= 1, so a
+// taken or absent expert (key 0) is never chosen again. Lane j < k keeps slot
+// j's expert and logit, takes e_j = exp(l_j - l_0) in fp64; every lane sums
+// e_0 + ... + e_{k-1} in slot order, and lane j returns g_j = fl32(e_j / s)
+// and its expert (else -1). *bad is set if a logit is non-finite.
 template <int EPL>
-__device__ __forceinline__ int route_token(const float* __restrict__ row, int E, int k,
-                                           int32_t* s_e, float* s_v, double* s_x,
+__device__ __forceinline__ int route_token(const float* row, int E, int k,
                                            float* __restrict__ gate_out, int* bad) {
   const int lane = threadIdx.x & 63;
-  uint64_t key[EPL];
-  int rank[EPL];
+  uint32_t ok[EPL];
   int nonfinite = 0;
 #pragma unroll
   for (int q = 0; q < EPL; ++q) {
     const int e = lane + 64 * q;
-    key[q] = 0;
-    rank[q] = 0;
+    ok[q] = 0u;
     if (e < E) {
       const float v = row[e];
       nonfinite |= !__builtin_isfinite(v);
-      key[q] = route_key(v, e);
+      ok[q] = max(ord_key(v), 1u);
     }
   }
   *bad |= __any(nonfinite);
+  int my_e = -1;
+  uint32_t my_key = 0u, key0 = 0u;
+  for (int j = 0; j < k; ++j) {
+    uint32_t lm = ok[0];
 #pragma unroll
-  for (int qs = 0; qs < EPL; ++qs) {
-    if (64 * qs >= E) break;
-#pragma unroll 8
-    for (int src = 0; src < 64; ++src) {
-      const uint64_t other = bcast_u64(key[qs], src);
+    for (int q = 1; q < EPL; ++q) lm = max(lm, ok[q]);
+    const uint32_t m = wave_max(lm);
+    int id = -1;
 #pragma unroll
-      for (int q = 0; q < EPL; ++q) rank[q] += other > key[q] ? 1 : 0;
+    for (int q = 0; q < EPL; ++q) {
+      const uint64_t b = __ballot(ok[q] == m);
+      if (id < 0 && b != 0ull) id = 64 * q + __builtin_ctzll(b);
     }
-  }
 #pragma unroll
-  for (int q = 0; q < EPL; ++q) {
-    if (key[q] != 0 && rank[q] < k) {
-      s_e[rank[q]] = static_cast<int32_t>(0xFFFFFFFFu - static_cast<uint32_t>(key[q]));
-      s_v[rank[q]] = key_value(key[q]);
+    for (int q = 0; q < EPL; ++q)
+      if (lane + 64 * q == id) ok[q] = 0u;
+    if (lane == j) {
+      my_e = id;
+      my_key = m;
     }
+    if (j == 0) key0 = m;
   }
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-  const float v0 = s_v[0];
-  const int my_e = lane < k ? s_e[lane] : -1;
-  const double ex = lane < k ? exp(static_cast<double>(s_v[lane]) - static_cast<double>(v0)) : 0.0;
-  if (lane < k) s_x[lane] = ex;
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+  const double v0 = static_cast<double>(ord_value(key0));
+  const double ex = lane < k ? exp(static_cast<double>(ord_value(my_key)) - v0) : 0.0;
   double s = 0.0;
-  for (int j = 0; j < k; ++j) s += s_x[j];
+  for (int j = 0; j < k; ++j) s += readlane_f64(ex, j);
   *gate_out = static_cast<float>(ex / s);
-  __builtin_amdgcn_wave_barrier();  // s_* are reused by this wavefront's next token
-  return my_e;
+  return lane < k ? my_e : -1;
 }
+
+// Inclusive prefix sum over the 64 lanes of a wavefront: shifts by 1, 2, 4
+// and 8 within each row of 16 lanes, then the row totals carried to the rows
+// above (DPP row_shr and row_bcast; lanes without a source add zero).
+__device__ __forceinline__ int wave_incl_scan(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, true);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, true);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, true);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, true);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xa, 0xf, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xc, 0xf, false);
+  return v;
+}
+
+__device__ __forceinline__ int wave_total(int incl) { return __builtin_amdgcn_readlane(incl, 63); }
 
 template <int EPL>
 __global__ __launch_bounds__(256) void k_route_topk(const float* __restrict__ logits, int T, int E,
                                                     int k, int32_t* __restrict__ topk_idx,
                                                     float* __restrict__ gates,
                                                     int32_t* __restrict__ bad_flag) {
-  __shared__ int32_t s_e[4][kMaxTopK];
-  __shared__ float s_v[4][kMaxTopK];
-  __shared__ double s_x[4][kMaxTopK];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nwaves = gridDim.x * 4;
   int bad = 0;
   for (int t = blockIdx.x * 4 + wave; t < T; t += nwaves) {
     float g;
-    const int e = route_token<EPL>(logits + static_cast<size_t>(t) * E, E, k, s_e[wave], s_v[wave],
-                                   s_x[wave], &g, &bad);
+    const int e = route_token<EPL>(logits + static_cast<size_t>(t) * E, E, k, &g, &bad);
     if (lane < k) {
       topk_idx[static_cast<size_t>(t) * k + lane] = e;
       gates[static_cast<size_t>(t) * k + lane] = g;
@@ -131,7 +148,8 @@ constexpr int kFusedMaxRoutes = 1024;       // fused routing path: T * k routes 
 // that chose e. Finally one wavefront publishes the routing record (fields,
 // system-scope fence, seq).
 __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, int bad,
-                                             const PermuteOut& o) {
+                                             const PermuteOut& o, const int32_t* s_free,
+                                             const int32_t* s_ftop) {
   __shared__ int32_t s_cnt[kMaxExperts];
   __shared__ int32_t s_off[kMaxExperts + 1];
   __shared__ int32_t s_item_base[kMaxExperts];
@@ -153,7 +171,7 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
   for (int r = tid; r < R; r += nthr) atomicAdd(&s_cnt[idx[r]], 1);
   __syncthreads();
 
-  if (tid < 64) {  // wave 0: scans over experts, 4 per lane
+  if (tid < 64) {  // wave 0: scans over experts, 4 per lane (DPP scans)
     const int lane = tid;
     int c[4], nh[4], nm[4];
     bool hit[4], miss[4];
@@ -179,31 +197,20 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
       hrows += hit[q] ? c[q] : 0;
       mrows += miss[q] ? c[q] : 0;
     }
-    int ic = sc, ih = sh, im = sm, ix = sx;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const int tc = __shfl_up(ic, off), th = __shfl_up(ih, off), tm = __shfl_up(im, off),
-                tx = __shfl_up(ix, off);
-      if (lane >= off) {
-        ic += tc;
-        ih += th;
-        im += tm;
-        ix += tx;
-      }
-    }
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-      n_act += __shfl_xor(n_act, off);
-      n_hit += __shfl_xor(n_hit, off);
-      n_res += __shfl_xor(n_res, off);
-      hrows += __shfl_xor(hrows, off);
-      mrows += __shfl_xor(mrows, off);
-    }
-    const int tot_hit = __shfl(ih, 63);
-    const int n_miss = __shfl(ix, 63);
+    const int ic = wave_incl_scan(sc), ih = wave_incl_scan(sh), im = wave_incl_scan(sm),
+              ix = wave_incl_scan(sx);
+    n_act = wave_total(wave_incl_scan(n_act));
+    n_hit = wave_total(wave_incl_scan(n_hit));
+    n_res = wave_total(wave_incl_scan(n_res));
+    hrows = wave_total(wave_incl_scan(hrows));
+    mrows = wave_total(wave_incl_scan(mrows));
+    const int tot_hit = wave_total(ih);
+    const int n_miss = wave_total(ix);
+    const int tot_routes = wave_total(ic);
+    const int tot_miss_items = wave_total(im);
     // staging: every miss takes a free slot, unless the block is bad
     CacheHdr* hdr = o.cv.hdr;
-    const int free_top = hdr->free_top;
+    const int free_top = *s_ftop;
     const bool stage = !bad && free_top >= 0 && free_top <= o.cv.n_slots && n_miss <= free_top;
     int xc = ic - sc, xh = ih - sh, xm = im - sm, xx = ix - sx;
 #pragma unroll
@@ -213,7 +220,7 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
         s_off[e] = xc;
         s_item_base[e] = (nh[q] > 0) ? xh : tot_hit + xm;
         if (stage && miss[q]) {
-          const int slot = o.cv.free_list[free_top - 1 - xx];
+          const int slot = s_free[xx];
           o.cv.slot_of[static_cast<size_t>(layer) * E + e] = slot;
           hdr->staged_exp[xx] = e;
           hdr->staged_slot[xx] = slot;
@@ -244,13 +251,11 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
       s_stat[5] = mrows;
       s_stat[6] = stage ? n_miss : 0;
       s_stat[7] = stage ? 0 : 1;
+      s_off[E] = tot_routes;
+      s_stat[8] = tot_hit;
+      s_stat[9] = tot_miss_items;
     }
     if (lane < kMaxExperts / 32) o.cv.res_before[layer].bits[lane] = s_res[lane];
-    if (lane == 63) {
-      s_off[E] = ic;
-      s_stat[8] = ih;
-      s_stat[9] = im;
-    }
   }
   __syncthreads();
 
@@ -303,47 +308,67 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
     __syncthreads();
   }
 
+  // the routing record: device ring (read by the host at its synchronisation
+  // points), and for host-issued copies the staged list in pinned memory
   if (tid < 64) {
     const int n_staged = s_stat[6];
+    RouteStats rs;
+    rs.layer = layer;
+    rs.n_active = s_stat[0];
+    rs.n_hits = s_stat[1];
+    rs.n_misses = s_stat[2];
+    rs.n_resident = s_stat[3];
+    rs.hit_rows = s_stat[4];
+    rs.miss_rows = s_stat[5];
+    rs.n_staged = n_staged;
+    rs.bad = bad ? 1 : s_stat[7];
+    rs.n_hit_items = s_stat[8];
+    rs.n_miss_items = s_stat[9];
+    rs.seq = o.seq;
+    if (tid == 0) {
+      o.item_counts[0] = s_stat[8];
+      o.item_counts[1] = s_stat[9];
+      o.ring[o.seq % kStatsRing] = rs;
+    }
     if (o.staged) {
       for (int j = tid; j < n_staged; j += 64) {
         o.staged->exp[j] = s_sexp[j];
         o.staged->slot[j] = s_sslot[j];
       }
-    }
-    RouteStats* rs = o.ring + (o.seq % kStatsRing);
-    if (tid == 0) {
-      o.item_counts[0] = s_stat[8];
-      o.item_counts[1] = s_stat[9];
-      rs->layer = layer;
-      rs->n_active = s_stat[0];
-      rs->n_hits = s_stat[1];
-      rs->n_misses = s_stat[2];
-      rs->n_resident = s_stat[3];
-      rs->hit_rows = s_stat[4];
-      rs->miss_rows = s_stat[5];
-      rs->n_staged = n_staged;
-      rs->bad = bad ? 1 : s_stat[7];
-      rs->n_hit_items = s_stat[8];
-      rs->n_miss_items = s_stat[9];
-      if (o.staged) o.staged->n = n_staged;
-    }
-    __threadfence_system();
-    if (tid == 0) {
-      *reinterpret_cast<volatile int32_t*>(&rs->seq) = o.seq;
-      if (o.staged) *reinterpret_cast<volatile int32_t*>(&o.staged->seq) = o.seq;
+      if (tid == 0) o.staged->rec = rs;
+      __threadfence_system();
+      if (tid == 0) *reinterpret_cast<volatile int32_t*>(&o.staged->seq) = o.seq;
     }
   }
+}
+
+// One wavefront loads the free-slot list's top (free_top and up to E entries
+// below it) into LDS ahead of the staging.
+__device__ __forceinline__ void prefetch_free(const CacheView& cv, int E, int32_t* s_free,
+                                              int32_t* s_ftop) {
+  const int lane = threadIdx.x & 63;
+  const int ft = cv.hdr->free_top;
+  if (ft >= 0 && ft <= cv.n_slots) {
+#pragma unroll
+    for (int q = 0; q < kMaxExperts / 64; ++q) {
+      const int j = lane + 64 * q;
+      if (j < E && j < ft) s_free[j] = cv.free_list[ft - 1 - j];
+    }
+  }
+  if (lane == 0) *s_ftop = ft;
 }
 
 __global__ __launch_bounds__(kPermThreads) void k_permute(const int32_t* __restrict__ topk_idx,
                                                           int T, int k,
                                                           int32_t* __restrict__ bad_flag,
                                                           PermuteOut o) {
+  __shared__ int32_t s_free[kMaxExperts];
+  __shared__ int32_t s_ftop;
   const int bad = *bad_flag;
+  if ((threadIdx.x >> 6) == 1) prefetch_free(o.cv, o.E, s_free, &s_ftop);
   __syncthreads();
   if (threadIdx.x == 0) *bad_flag = 0;
-  permute_body(topk_idx, T, k, bad, o);
+  permute_body(topk_idx, T, k, bad, o, s_free, &s_ftop);
 }
 
 // Small blocks (T*k <= 1024): routing on many CUs, one token per wavefront,
@@ -355,18 +380,16 @@ __global__ __launch_bounds__(256) void k_route_fused(const float* __restrict__ l
                                                      int k, int32_t* __restrict__ topk_idx,
                                                      float* __restrict__ gates,
                                                      int32_t* __restrict__ sync, PermuteOut o) {
-  __shared__ int32_t s_e[4][kMaxTopK];
-  __shared__ float s_v[4][kMaxTopK];
-  __shared__ double s_x[4][kMaxTopK];
   __shared__ int32_t s_idx[kFusedMaxRoutes];
+  __shared__ int32_t s_free[kMaxExperts];
+  __shared__ int32_t s_ftop;
   __shared__ int32_t s_last;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int E = o.E;
   int bad = 0;
   for (int t = blockIdx.x * 4 + wave; t < T; t += gridDim.x * 4) {
     float g;
-    const int e = route_token<EPL>(logits + static_cast<size_t>(t) * E, E, k, s_e[wave], s_v[wave],
-                                   s_x[wave], &g, &bad);
+    const int e = route_token<EPL>(logits + static_cast<size_t>(t) * E, E, k, &g, &bad);
     if (lane < k) {
       topk_idx[static_cast<size_t>(t) * k + lane] = e;
       gates[static_cast<size_t>(t) * k + lane] = g;
@@ -379,15 +402,19 @@ __global__ __launch_bounds__(256) void k_route_fused(const float* __restrict__ l
   __syncthreads();
   if (!s_last) return;
   __threadfence();   // see every other workgroup's routes
-  for (int r = threadIdx.x; r < T * k; r += blockDim.x) s_idx[r] = __hip_atomic_load(
-      &topk_idx[r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (wave == 3) {
+    prefetch_free(o.cv, E, s_free, &s_ftop);
+  } else {
+    for (int r = threadIdx.x; r < T * k; r += 192) s_idx[r] = __hip_atomic_load(
+        &topk_idx[r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
   const int any_bad = __hip_atomic_load(&sync[1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   __syncthreads();
   if (threadIdx.x == 0) {  // re-arm for the next launch (stream order)
     sync[0] = 0;
     sync[1] = 0;
   }
-  permute_body(s_idx, T, k, any_bad, o);
+  permute_body(s_idx, T, k, any_bad, o, s_free, &s_ftop);
 }
 
 }  // namespace

@@ -148,10 +148,8 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
     if (fault) hdr->fault |= fault;
     out->bad_conf = s_bad;
     out->n_retained = kept;
+    out->seq = a.seq;
   }
-  // publish: fields, system-scope fence, then seq
-  __threadfence_system();
-  if (lane == 0) *reinterpret_cast<volatile int32_t*>(&out->seq) = a.seq;
 }
 
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
