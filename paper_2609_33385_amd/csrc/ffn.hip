@@ -37,6 +37,8 @@
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace oled {
@@ -367,6 +369,314 @@ __global__ __launch_bounds__(kThreads) void k_ffn_mix(FfnLaunch d, FfnLaunch u, 
   gemm_tiles<TR, true, KSU>(u, b - nfetch - gd, static_cast<int>(gridDim.x) - nfetch - gd, s_buf);
 }
 
+// ---------------------------------------------------------------------------
+// Dense tiles for experts with many routed rows (bf16). A workgroup computes
+// up to 256 rows of one expert against 256 weight rows: gate/up 128 features
+// (each with its W1 and W3 row), down 256 features. Wavefront w owns 64 of
+// the weight rows and multiplies them by all of the tile's token rows with
+// v_mfma_f32_32x32x16_bf16 (the 16x16x32 form runs at less than half its
+// rate on this part), accumulators in registers.
+//  * Weights are private to a wavefront: it loads them from the packed
+//    fragments straight into registers, two stages of 64 of K ahead.
+//  * Token rows are shared by the four wavefronts: they are copied from
+//    memory into a 4-stage LDS ring (32 KiB per stage of 64 of K, three
+//    stages in flight) by LDS DMA (buffer loads with an LDS destination,
+//    lane l's 16 bytes at lane slot l), 8 rows of 128 bytes per instruction:
+//    whole 128-byte lines per 8 lanes run at the full L2-to-LDS rate, where
+//    16-byte pieces of 16 rows per instruction run at a third of it.
+// Every output sums its K range in ascending order in one accumulator. Tiles
+// are ordered feature tile major, so the row tiles of one expert that share
+// weights run next to each other on one XCD (its L2).
+constexpr int kDenseRows = 256;   // token rows per dense item
+constexpr int kDenseRing = 4;     // token stages in LDS
+constexpr int kDenseGroup = 4;    // items per tile group
+
+// Word 3 of a raw buffer resource (32-bit data format) on this part.
+constexpr int kBufferFlags = 0x00020000;
+
+// s_waitcnt immediate: wait until at most N vector-memory operations are
+// outstanding (other counters left at their maximum).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// Workgroup barrier without a memory fence: __syncthreads() would also wait
+// for every outstanding load of the wavefront, draining the ring. Each
+// wavefront has already waited for its own loads of the stage it needs; LDS
+// is coherent inside the CU. The empty asm statements keep the compiler from
+// moving memory accesses across the barrier.
+__device__ __forceinline__ void ring_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+typedef float floatx16_t __attribute__((ext_vector_type(16)));
+
+// One 32x32 output tile over 16 of K: v_mfma_f32_32x32x16_bf16. A: lane l
+// holds row l%32, k 8*(l/32)..+7; B: lane l holds column l%32, the same k;
+// D: lane l, register r -> row 8*(r/4) + 4*(l/32) + r%4, column l%32.
+__device__ __forceinline__ void mma32(floatx16_t& acc, const u32x4_t& a, const u32x4_t& b) {
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                               __builtin_bit_cast(bf16x8_t, b), acc, 0, 0, 0);
+}
+
+// Reads of the token ring are inline assembly, with explicit waits: the
+// compiler cannot tell which stage a read touches, so for its own LDS reads it
+// would wait for every LDS DMA in flight (vmcnt(0)) and drain the ring.
+__device__ __forceinline__ u32x4_t lds_read16(uint32_t addr) {
+  u32x4_t v;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr));
+  return v;
+}
+
+// Wait until at most N LDS operations are outstanding; the operands are tied
+// through the wait so that nothing reads them before it.
+template <int N, int NT>
+__device__ __forceinline__ void wait_lgkm(u32x4_t (&b)[NT]) {
+  static_assert(NT == 1 || NT == 2 || NT == 4 || NT == 8, "token tiles");
+  if constexpr (NT == 1) asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(b[0]) : "n"(N));
+  if constexpr (NT == 2) asm volatile("s_waitcnt lgkmcnt(%2)" : "+v"(b[0]), "+v"(b[1]) : "n"(N));
+  if constexpr (NT == 4)
+    asm volatile("s_waitcnt lgkmcnt(%4)" : "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]) : "n"(N));
+  if constexpr (NT == 8)
+    asm volatile("s_waitcnt lgkmcnt(%8)"
+                 : "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]), "+v"(b[4]), "+v"(b[5]),
+                   "+v"(b[6]), "+v"(b[7])
+                 : "n"(N));
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p));
+}
+
+// Token stage layout: instruction j of a stage holds rows 8j..8j+7, row r's
+// 16-byte chunk c (8 of K) at lane 8 (r%8) + (c ^ tok_swz(r)). The rotation
+// makes the operand reads of 8 or 16 consecutive rows hit distinct banks.
+__device__ __forceinline__ int tok_swz(int r) { return (r ^ (r >> 3)) & 7; }
+
+// One tile: NT token tiles of 32 rows (item rows <= 32 NT).
+template <bool UP, int NT>
+__device__ __forceinline__ void dense_tile(const FfnLaunch& a, const WorkItem& it, int f0,
+                                           const uint16_t* W, u32x4_t (*ring)[32][64]) {
+  constexpr int FRAG = 512;               // packed fragment: 16 rows x 32 of K
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int H = a.H, I = a.I;
+  const int K = UP ? H : I;
+  const int NS = K / 64;                  // stages
+  const int S32 = K / 32;                 // packed fragments per 16 weight rows
+  const uint16_t* src = static_cast<const uint16_t*>(a.src);
+
+  // token rows: NT DMA instructions per wavefront per stage, through a
+  // buffer resource over the source (reads past src_bytes return zeros).
+  // The per-lane byte offsets stay in registers for the whole tile; a stage
+  // adds 128 bytes through the scalar offset.
+  int toff[NT];
+#pragma unroll
+  for (int i = 0; i < NT; ++i) {
+    const int r = 8 * (wave * NT + i) + (lane >> 3);
+    const int rr = min(r, it.rows - 1);   // rows past the item read its last
+    const int pos = it.row_begin + rr;
+    const int c = (lane & 7) ^ tok_swz(r);
+    toff[i] = (UP ? (a.perm[pos] / a.k) * H : pos * I) * 2 + 16 * c;
+  }
+  const __amdgpu_buffer_rsrc_t trs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(src), 0, static_cast<int>(a.src_bytes), kBufferFlags);
+  auto issue_tok = [&](int s) {
+    u32x4_t (*stage)[64] = ring[s % kDenseRing];
+#pragma unroll
+    for (int i = 0; i < NT; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          trs, (__attribute__((address_space(3))) void*)(stage[wave * NT + i]), 16,
+          toff[i], 128 * s, 0, 0);
+  };
+
+  // weights: two 32-row A tiles per wavefront (gate and up of 32 features,
+  // or 64 down features). Lane l holds row l%32 (16-row fragment (l/16)%2)
+  // and the 8 of K at fragment lane l%16 + 16 (2 q + l/32) for the half q of
+  // a 32 step.
+  const uint16_t* wp[2];
+  size_t wstep;
+  {
+    const int m16 = (lane & 15) + 16 * (lane >> 5);
+    const int q0 = f0 / 16;
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      if (UP) {
+        const int q = q0 + 2 * wave + ((lane >> 4) & 1);
+        wp[t] = W + ((static_cast<size_t>(q) * S32) * 2 + t) * FRAG + 8 * m16;
+      } else {
+        const int q = q0 + 4 * wave + 2 * t + ((lane >> 4) & 1);
+        wp[t] = W + static_cast<size_t>(2) * I * H + static_cast<size_t>(q) * S32 * FRAG + 8 * m16;
+      }
+    }
+    wstep = (UP ? 2 : 1) * FRAG;
+  }
+  auto load_w = [&](int s, u32x4_t (&w)[2][4]) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int h = 0; h < 4; ++h)
+        w[t][h] = ldg16(wp[t] + (2 * s + (h >> 1)) * wstep + 256 * (h & 1));
+  };
+
+  floatx16_t acc[2][NT];
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int n = 0; n < NT; ++n)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[t][n][r] = 0.f;
+
+  // B operand position of token tile n for this lane (chunk c added later)
+  uint32_t brow_off[NT];
+  int bsw[NT];
+#pragma unroll
+  for (int n = 0; n < NT; ++n) {
+    const int r = 32 * n + (lane & 31);
+    brow_off[n] = static_cast<uint32_t>((r >> 3) * 1024 + 128 * (lane & 7));
+    bsw[n] = tok_swz(r);
+  }
+  const uint32_t ring_base = lds_addr(&ring[0][0][0]);
+
+  // Issue order: DMA(0) W(0) DMA(1) W(1) DMA(2); stage s: wait, barrier,
+  // DMA(s+3), multiply, W(s+2) (NS even, at least 4). Operations issued after
+  // DMA(s) before stage s reads it: at least 16 + 2 NT while s + 2 < NS, at
+  // least 16 at NS - 2.
+  u32x4_t wr[2][2][4];
+  issue_tok(0);
+  asm volatile("" ::: "memory");
+  load_w(0, wr[0]);
+  asm volatile("" ::: "memory");
+  issue_tok(1);
+  asm volatile("" ::: "memory");
+  load_w(1, wr[1]);
+  asm volatile("" ::: "memory");
+  issue_tok(2);
+
+  // DMA: issue DMA(s+3); WL: load W(s+2); VM: the wait before reading stage s
+  auto stage_body = [&](auto dma, auto wl, auto vm, int s, u32x4_t (&w)[2][4]) {
+    wait_vmcnt<decltype(vm)::value>();
+    ring_barrier();  // stage s landed for every wavefront; stage s - 1 is free
+    if constexpr (decltype(dma)::value) issue_tok(s + 3);
+    asm volatile("" ::: "memory");
+    const uint32_t sbase = ring_base + static_cast<uint32_t>(s % kDenseRing) * (32 * 64 * 16);
+    // half h's operands are read while half h - 1 multiplies
+    auto read_half = [&](int h, u32x4_t (&b)[NT]) {
+      const int c = 2 * h + (lane >> 5);
+#pragma unroll
+      for (int n = 0; n < NT; ++n) b[n] = lds_read16(sbase + brow_off[n] + 16 * (c ^ bsw[n]));
+    };
+    u32x4_t bq[2][NT];
+    read_half(0, bq[0]);
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      if (h < 3) {
+        read_half(h + 1, bq[(h + 1) & 1]);
+        wait_lgkm<NT>(bq[h & 1]);
+      } else {
+        wait_lgkm<0>(bq[h & 1]);
+      }
+#pragma unroll
+      for (int n = 0; n < NT; ++n)
+#pragma unroll
+        for (int t = 0; t < 2; ++t) mma32(acc[t][n], w[t][h], bq[h & 1][n]);
+    }
+    asm volatile("" ::: "memory");
+    if constexpr (decltype(wl)::value) load_w(s + 2, w);
+  };
+  using T_ = std::true_type;
+  using F_ = std::false_type;
+  using VS = std::integral_constant<int, 16 + 2 * NT>;
+  // steady state: every stage issues DMA(s+3) and W(s+2) (the loads stay
+  // unconditional, so the compiler's own waits for W count exactly)
+  int s = 0;
+  for (; s + 4 < NS; s += 2) {
+    stage_body(T_{}, T_{}, VS{}, s, wr[0]);
+    stage_body(T_{}, T_{}, VS{}, s + 1, wr[1]);
+  }
+  // NS - 4 .. NS - 1
+  stage_body(T_{}, T_{}, VS{}, s, wr[0]);
+  stage_body(F_{}, T_{}, VS{}, s + 1, wr[1]);
+  stage_body(F_{}, F_{}, std::integral_constant<int, 16>{}, s + 2, wr[0]);
+  stage_body(F_{}, F_{}, std::integral_constant<int, 0>{}, s + 3, wr[1]);
+  // epilogue: lane l holds token row 32 n + l%32 and, for register r, weight
+  // row 8 (r/4) + 4 (l/32) + r%4 of each A tile
+  const int col = lane & 31, hi = lane >> 5;
+#pragma unroll
+  for (int n = 0; n < NT; ++n) {
+    const int row = 32 * n + col;
+    if (row >= it.rows) continue;
+    const size_t pos = static_cast<size_t>(it.row_begin + row);
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4) {
+      if (UP) {
+        const int f = f0 + 32 * wave + 8 * r4 + 4 * hi;
+        float hv[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          hv[r] = TrBF16::silu(acc[0][n][4 * r4 + r]) * acc[1][n][4 * r4 + r];
+        uint2 packed;
+        packed.x = f32_to_bf16_rne(hv[0]) | (static_cast<uint32_t>(f32_to_bf16_rne(hv[1])) << 16);
+        packed.y = f32_to_bf16_rne(hv[2]) | (static_cast<uint32_t>(f32_to_bf16_rne(hv[3])) << 16);
+        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.hout) + pos * I + f) = packed;
+      } else {
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          const int f = f0 + 64 * wave + 32 * t + 8 * r4 + 4 * hi;
+          const floatx16_t& v = acc[t][n];
+          *reinterpret_cast<float4*>(a.oout + pos * H + f) =
+              make_float4(v[4 * r4], v[4 * r4 + 1], v[4 * r4 + 2], v[4 * r4 + 3]);
+        }
+      }
+    }
+  }
+}
+
+// Dense launch: one tile per workgroup. Items [0, c0) hold 256 rows each
+// and [c0, c0 + c1) fewer ((c0, c1) = item_counts on the device); full tiles
+// come first in dispatch order and the short ones last, so the hardware's
+// in-order dispatch balances the CUs. Within each class the tiles are spread
+// over the XCDs in contiguous ranges.
+template <bool UP>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void k_ffn_dense(FfnLaunch a) {
+  __shared__ u32x4_t s_ring[kDenseRing][32][64];
+  constexpr int DF = UP ? 128 : 256;
+  const int n_full = a.item_counts[0], n_short = a.item_counts[1];
+  const int nf = (UP ? a.I : a.H) / DF;
+  const int t = blockIdx.x;
+  int v, n, first;
+  if (t < n_full * nf) {
+    v = xcd_order(t, n_full * nf);
+    n = n_full;
+    first = 0;
+  } else {
+    const int u = t - n_full * nf;
+    if (u >= n_short * nf) return;
+    v = xcd_order(u, n_short * nf);
+    n = n_short;
+    first = n_full;
+  }
+  // groups of kDenseGroup items, feature tile major inside a group: the
+  // tiles running at once on an XCD share a few token row blocks and a few
+  // weight slices through its L2
+  const int gsz = kDenseGroup * nf;
+  const int g = v / gsz, rem = v - g * gsz;
+  const int gi = min(kDenseGroup, n - g * kDenseGroup);
+  const int ft = rem / gi;
+  const WorkItem it = a.items[a.item_base + first + g * kDenseGroup + (rem - ft * gi)];
+  const int slot = a.slot_of[it.expert];
+  if (slot < 0 || slot >= a.n_slots || it.rows <= 0 || it.rows > kDenseRows) return;
+  const uint16_t* W = reinterpret_cast<const uint16_t*>(static_cast<const char*>(a.pool) +
+                                                        static_cast<int64_t>(slot) * a.slot_bytes);
+  if (it.rows > 128) dense_tile<UP, 8>(a, it, ft * DF, W, s_ring);
+  else if (it.rows > 64) dense_tile<UP, 4>(a, it, ft * DF, W, s_ring);
+  else if (it.rows > 32) dense_tile<UP, 2>(a, it, ft * DF, W, s_ring);
+  else dense_tile<UP, 1>(a, it, ft * DF, W, s_ring);
+}
+
 __global__ __launch_bounds__(kThreads) void k_fetch(char* pool, int64_t slot_bytes, int n_slots,
                                                     FetchArgs f) {
   fetch_blocks(f, pool, slot_bytes, n_slots, blockIdx.x);
@@ -453,6 +763,21 @@ hipError_t launch_ffn_down(bool bf16, const FfnLaunch& a, hipEvent_t ev0, hipEve
                            hipStream_t s) {
   return bf16 ? launch_ffn_t<TrBF16, false>(a, ev0, ev1, s)
               : launch_ffn_t<TrF32, false>(a, ev0, ev1, s);
+}
+
+hipError_t launch_ffn_dense(bool up, const FfnLaunch& a, hipEvent_t ev0, hipEvent_t ev1,
+                            hipStream_t s) {
+  if (a.H % 256 || a.I % 256 || a.src_bytes <= 0 || a.src_bytes > INT32_MAX) return hipErrorInvalidValue;
+  const int64_t grid = static_cast<int64_t>(a.max_items) * (up ? a.I / 128 : a.H / 256);
+  if (grid <= 0) return hipSuccess;
+  if (grid > INT32_MAX) return hipErrorInvalidValue;
+  if (up)
+    hipExtLaunchKernelGGL(k_ffn_dense<true>, dim3(static_cast<unsigned>(grid)), dim3(kThreads), 0, s,
+                          ev0, ev1, 0, a);
+  else
+    hipExtLaunchKernelGGL(k_ffn_dense<false>, dim3(static_cast<unsigned>(grid)), dim3(kThreads), 0,
+                          s, ev0, ev1, 0, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_ffn_mix(bool bf16, const FfnLaunch& d, const FfnLaunch& u, hipEvent_t ev0,

@@ -123,6 +123,7 @@ struct FfnLaunch {
   void* hout;             // up: h [T*k][I]
   float* oout;            // down: O [T*k][H]
   FetchArgs fetch;
+  int64_t src_bytes;      // dense launches: bytes of src (below 2^31)
 };
 
 // Every launcher takes optional (ev0, ev1): if non-null they record the
@@ -172,6 +173,14 @@ hipError_t launch_ffn_down(bool bf16, const FfnLaunch& a, hipEvent_t ev0, hipEve
 // (d.fetch), and the misses' gate/up GEMM (u), in one launch.
 hipError_t launch_ffn_mix(bool bf16, const FfnLaunch& d, const FfnLaunch& u, hipEvent_t ev0,
                           hipEvent_t ev1, hipStream_t s);
+
+// Dense tiles (bf16, H a multiple of 256) for experts with at least
+// kDenseMinRows routed rows: work items of up to 128 rows; up: 128 features
+// x 128 rows per workgroup, down: 256 x 128. The launch's item list holds
+// only such experts.
+constexpr int kDenseMinRows = 128;
+hipError_t launch_ffn_dense(bool up, const FfnLaunch& a, hipEvent_t ev0, hipEvent_t ev1,
+                            hipStream_t s);
 
 // Transfer of the staged misses alone (no GEMM tiles).
 hipError_t launch_fetch(const void* pool, int64_t slot_bytes, int n_slots, const FetchArgs& f,
