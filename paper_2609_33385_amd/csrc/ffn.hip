@@ -387,7 +387,6 @@ __global__ __launch_bounds__(kThreads) void k_ffn_mix(FfnLaunch d, FfnLaunch u, 
 // Every output sums its K range in ascending order in one accumulator. Tiles
 // are ordered feature tile major, so the row tiles of one expert that share
 // weights run next to each other on one XCD (its L2).
-constexpr int kDenseRows = 256;   // token rows per dense item
 constexpr int kDenseRing = 4;     // token stages in LDS
 constexpr int kDenseGroup = 4;    // items per tile group
 
@@ -540,10 +539,11 @@ __device__ __forceinline__ void dense_tile(const FfnLaunch& a, const WorkItem& i
   }
   const uint32_t ring_base = lds_addr(&ring[0][0][0]);
 
-  // Issue order: DMA(0) W(0) DMA(1) W(1) DMA(2); stage s: wait, barrier,
-  // DMA(s+3), multiply, W(s+2) (NS even, at least 4). Operations issued after
-  // DMA(s) before stage s reads it: at least 16 + 2 NT while s + 2 < NS, at
-  // least 16 at NS - 2.
+  // Issue order: DMA(0) W(0) DMA(1) W(1) DMA(2), then barrier B(0). Stage s
+  // multiplies halves 0..2, passes barrier B(s+1) (stage s+1 landed for
+  // every wavefront, stage s-1 free), issues DMA(s+3) and the reads of stage
+  // s+1's first half, multiplies half 3, then loads W(s+2). Operations issued
+  // after DMA(s+1) when B(s+1) waits for it: at least 8 + NT.
   u32x4_t wr[2][2][4];
   issue_tok(0);
   asm volatile("" ::: "memory");
@@ -555,52 +555,59 @@ __device__ __forceinline__ void dense_tile(const FfnLaunch& a, const WorkItem& i
   asm volatile("" ::: "memory");
   issue_tok(2);
 
-  // DMA: issue DMA(s+3); WL: load W(s+2); VM: the wait before reading stage s
-  auto stage_body = [&](auto dma, auto wl, auto vm, int s, u32x4_t (&w)[2][4]) {
-    wait_vmcnt<decltype(vm)::value>();
-    ring_barrier();  // stage s landed for every wavefront; stage s - 1 is free
-    if constexpr (decltype(dma)::value) issue_tok(s + 3);
-    asm volatile("" ::: "memory");
+  auto read_half = [&](int s, int h, u32x4_t (&b)[NT]) {
     const uint32_t sbase = ring_base + static_cast<uint32_t>(s % kDenseRing) * (32 * 64 * 16);
-    // half h's operands are read while half h - 1 multiplies
-    auto read_half = [&](int h, u32x4_t (&b)[NT]) {
-      const int c = 2 * h + (lane >> 5);
+    const int c = 2 * h + (lane >> 5);
 #pragma unroll
-      for (int n = 0; n < NT; ++n) b[n] = lds_read16(sbase + brow_off[n] + 16 * (c ^ bsw[n]));
-    };
-    u32x4_t bq[2][NT];
-    read_half(0, bq[0]);
+    for (int n = 0; n < NT; ++n) b[n] = lds_read16(sbase + brow_off[n] + 16 * (c ^ bsw[n]));
+  };
+  u32x4_t bq[2][NT];
+  wait_vmcnt<16 + 2 * NT>();
+  ring_barrier();
+  read_half(0, 0, bq[0]);
+
+  // NX: a next stage exists; DMA: issue DMA(s+3); WL: load W(s+2)
+  auto stage_body = [&](auto nx, auto dma, auto wl, int s, u32x4_t (&w)[2][4]) {
 #pragma unroll
-    for (int h = 0; h < 4; ++h) {
-      if (h < 3) {
-        read_half(h + 1, bq[(h + 1) & 1]);
-        wait_lgkm<NT>(bq[h & 1]);
-      } else {
-        wait_lgkm<0>(bq[h & 1]);
-      }
+    for (int h = 0; h < 3; ++h) {
+      read_half(s, h + 1, bq[(h + 1) & 1]);
+      wait_lgkm<NT>(bq[h & 1]);
 #pragma unroll
       for (int n = 0; n < NT; ++n)
 #pragma unroll
         for (int t = 0; t < 2; ++t) mma32(acc[t][n], w[t][h], bq[h & 1][n]);
     }
+    if constexpr (decltype(nx)::value) {
+      wait_vmcnt<8 + NT>();
+      ring_barrier();  // B(s+1)
+      if constexpr (decltype(dma)::value) issue_tok(s + 3);
+      read_half(s + 1, 0, bq[0]);
+      wait_lgkm<NT>(bq[1]);
+    } else {
+      wait_lgkm<0>(bq[1]);
+    }
+#pragma unroll
+    for (int n = 0; n < NT; ++n)
+#pragma unroll
+      for (int t = 0; t < 2; ++t) mma32(acc[t][n], w[t][3], bq[1][n]);
     asm volatile("" ::: "memory");
     if constexpr (decltype(wl)::value) load_w(s + 2, w);
   };
   using T_ = std::true_type;
   using F_ = std::false_type;
-  using VS = std::integral_constant<int, 16 + 2 * NT>;
   // steady state: every stage issues DMA(s+3) and W(s+2) (the loads stay
   // unconditional, so the compiler's own waits for W count exactly)
   int s = 0;
   for (; s + 4 < NS; s += 2) {
-    stage_body(T_{}, T_{}, VS{}, s, wr[0]);
-    stage_body(T_{}, T_{}, VS{}, s + 1, wr[1]);
+    stage_body(T_{}, T_{}, T_{}, s, wr[0]);
+    stage_body(T_{}, T_{}, T_{}, s + 1, wr[1]);
   }
   // NS - 4 .. NS - 1
-  stage_body(T_{}, T_{}, VS{}, s, wr[0]);
-  stage_body(F_{}, T_{}, VS{}, s + 1, wr[1]);
-  stage_body(F_{}, F_{}, std::integral_constant<int, 16>{}, s + 2, wr[0]);
-  stage_body(F_{}, F_{}, std::integral_constant<int, 0>{}, s + 3, wr[1]);
+  stage_body(T_{}, T_{}, T_{}, s, wr[0]);
+  stage_body(T_{}, F_{}, T_{}, s + 1, wr[1]);
+  stage_body(T_{}, F_{}, F_{}, s + 2, wr[0]);
+  stage_body(F_{}, F_{}, F_{}, s + 3, wr[1]);
+
   // epilogue: lane l holds token row 32 n + l%32 and, for register r, weight
   // row 8 (r/4) + 4 (l/32) + r%4 of each A tile
   const int col = lane & 31, hi = lane >> 5;

@@ -58,6 +58,11 @@ struct RouteStats {
   int32_t bad;         // non-finite logit, or no free slot: nothing staged
   int32_t n_hit_items;
   int32_t n_miss_items;
+  int32_t n_dense;     // experts with dense items (at least kDenseMinRows rows)
+  int32_t n_dense_hits;
+  int32_t dense_rows;
+  int32_t dense_hit_rows;
+  int32_t n_dense_items;
   int32_t seq;
 };
 
@@ -142,6 +147,9 @@ struct PermuteOut {
   int32_t* inv_perm;
   WorkItem* items;
   int32_t* item_counts;   // [2] hit items, miss items
+  WorkItem* dense_items;  // experts with at least dense_min rows (0: none)
+  int32_t* dense_counts;  // [2] items of kDenseRows rows, shorter items
+  int dense_min;
   RouteStats* ring;       // device ring of routing records
   StagedList* staged;     // pinned, or null
   int layer, E, seq;
@@ -174,11 +182,14 @@ hipError_t launch_ffn_down(bool bf16, const FfnLaunch& a, hipEvent_t ev0, hipEve
 hipError_t launch_ffn_mix(bool bf16, const FfnLaunch& d, const FfnLaunch& u, hipEvent_t ev0,
                           hipEvent_t ev1, hipStream_t s);
 
-// Dense tiles (bf16, H a multiple of 256) for experts with at least
-// kDenseMinRows routed rows: work items of up to 128 rows; up: 128 features
-// x 128 rows per workgroup, down: 256 x 128. The launch's item list holds
-// only such experts.
+// Dense tiles (bf16; H and I multiples of 256; src below 2 GiB) for experts
+// with at least kDenseMinRows routed rows, hits and misses alike, once all
+// their weights are in their slots. Items of kDenseRows rows first
+// (item_counts[0] of them), then one shorter item per expert
+// (item_counts[1]); up: 128 features x 256 rows per workgroup, down: 256 x
+// 256. Those experts have no items in the streaming lists.
 constexpr int kDenseMinRows = 128;
+constexpr int kDenseRows = 256;
 hipError_t launch_ffn_dense(bool up, const FfnLaunch& a, hipEvent_t ev0, hipEvent_t ev1,
                             hipStream_t s);
 

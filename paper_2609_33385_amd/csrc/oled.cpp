@@ -56,7 +56,8 @@ enum class Stage { kIdle, kRouted, kHitsQueued, kApplied };
 struct OpRec {
   int kind, layer;
   int route_seq;          // routing record that completes the accounting (0: complete)
-  int part;               // 0 gate/up, 1 down, 2 hit down + miss gate/up, -1 other
+  int part;               // 0 gate/up, 1 down, 2 hit down + miss gate/up, 3 dense gate/up,
+                          // 4 dense down, -1 other
   bool hits;              // hit-expert launch (else miss launch)
   int64_t bytes, flops, h2d;
   hipEvent_t a, b;
@@ -72,6 +73,8 @@ struct Ctx {
   int n_slots = 0;
   int cap = 0;       // min(C, E)
   int max_items = 0;
+  bool dense_ok = false;  // shapes the dense-tile GEMM takes (bf16, H and I multiples of 256)
+  int max_dense = 0;
   const char* host_pool = nullptr;
   int64_t P = 0;
   std::vector<int64_t> host_block_of;
@@ -87,6 +90,8 @@ struct Ctx {
   int32_t* d_item_counts = nullptr;
   int32_t* d_sync = nullptr;       // completion counter + bad-logit flag of the fused routing
   WorkItem* d_items = nullptr;
+  WorkItem* d_dense_items = nullptr;
+  int32_t* d_dense_counts = nullptr;
   void* d_h = nullptr;
   float* d_O = nullptr;
   uint64_t* d_score = nullptr;     // [L][E]
@@ -125,6 +130,7 @@ struct Ctx {
   // the layer in flight
   Stage stage = Stage::kIdle;
   int cur_layer = -1, cur_T = 0, cur_route = 0;
+  bool cur_dense = false;          // the layer in flight has dense items
   hipStream_t cur_stream = nullptr;
   bool have_stream = false;
   const void* fwd_x = nullptr;
@@ -316,7 +322,8 @@ void free_ctx(Ctx* c) {
   if (c->ev_order) (void)hipEventDestroy(c->ev_order);
   if (c->own_copy) (void)hipStreamDestroy(c->own_copy);
   void* dev[] = {c->d_pool, c->d_topk, c->d_gates, c->d_counts, c->d_offsets, c->d_perm,
-                 c->d_inv, c->d_flag, c->d_item_counts, c->d_sync, c->d_items, c->d_h, c->d_O,
+                 c->d_inv, c->d_flag, c->d_item_counts, c->d_sync, c->d_items, c->d_dense_items,
+                 c->d_dense_counts, c->d_h, c->d_O,
                  c->d_score, c->d_hdr, c->d_slot_of, c->d_res, c->d_res_before,
                  c->d_last_counts, c->d_free, c->d_host_addr};
   for (void* p : dev)
@@ -418,6 +425,15 @@ int64_t down_bytes(const Ctx* c, int64_t n_exp, int64_t rows) {
 int64_t up_flops(const Ctx* c, int64_t rows) { return rows * 4 * static_cast<int64_t>(c->H) * c->I; }
 int64_t down_flops(const Ctx* c, int64_t rows) { return rows * 2 * static_cast<int64_t>(c->H) * c->I; }
 
+// Experts and rows of the streaming launches (the dense experts excluded).
+struct Part {
+  int64_t n, rows;
+};
+Part streamed(const RouteStats& r, bool hits) {
+  if (hits) return {r.n_hits - r.n_dense_hits, r.hit_rows - r.dense_hit_rows};
+  return {r.n_misses - (r.n_dense - r.n_dense_hits), r.miss_rows - (r.dense_rows - r.dense_hit_rows)};
+}
+
 // Completes the byte / flop accounting of a launch from its routing record.
 void complete_op(const Ctx* c, OpRec& op, const RouteStats& r) {
   if (op.kind == OLED_OP_H2D) {  // transfer-only launch (no GEMM tiles)
@@ -427,13 +443,22 @@ void complete_op(const Ctx* c, OpRec& op, const RouteStats& r) {
     return;
   }
   if (op.part == 2) {
-    op.bytes = down_bytes(c, r.n_hits, r.hit_rows) + up_bytes(c, r.n_misses, r.miss_rows);
-    op.flops = down_flops(c, r.hit_rows) + up_flops(c, r.miss_rows);
+    const Part h = streamed(r, true), m = streamed(r, false);
+    op.bytes = down_bytes(c, h.n, h.rows) + up_bytes(c, m.n, m.rows);
+    op.flops = down_flops(c, h.rows) + up_flops(c, m.rows);
     op.h2d = static_cast<int64_t>(r.n_staged) * (c->eb - c->e13);
     return;
   }
-  const int64_t n = op.hits ? r.n_hits : r.n_misses;
-  const int64_t rows = op.hits ? r.hit_rows : r.miss_rows;
+  if (op.part == 3 || op.part == 4) {  // dense tiles
+    const bool up = op.part == 3;
+    op.bytes = up ? up_bytes(c, r.n_dense, r.dense_rows) : down_bytes(c, r.n_dense, r.dense_rows);
+    op.flops = up ? up_flops(c, r.dense_rows) : down_flops(c, r.dense_rows);
+    op.h2d = 0;
+    return;
+  }
+  const Part pr = streamed(r, op.hits);
+  const int64_t n = pr.n;
+  const int64_t rows = pr.rows;
   if (op.part == 0) {
     op.bytes = up_bytes(c, n, rows);
     op.flops = up_flops(c, rows);
@@ -585,6 +610,10 @@ oled_status oled_create(const oled_config* cfg, void** ctx_out) {
   const int staging = routes < c->E ? static_cast<int>(routes) : c->E;
   c->n_slots = c->L * c->cap + staging;
   c->max_items = static_cast<int>(routes / oled::kItemRows) + c->E + 1;
+  c->dense_ok = c->dtype == OLED_BF16 && c->H % 256 == 0 && c->I % 256 == 0 &&
+                routes >= oled::kDenseMinRows && routes * c->I * 2 <= INT32_MAX &&
+                static_cast<int64_t>(c->Tmax) * c->H * 2 <= INT32_MAX;
+  c->max_dense = c->dense_ok ? static_cast<int>(routes / oled::kDenseRows) + c->E + 1 : 0;
   c->host_pool = static_cast<const char*>(cfg->host_pool);
   c->P = cfg->host_pool_blocks;
   c->host_block_of.assign(cfg->host_block_of, cfg->host_block_of + nb);
@@ -603,6 +632,8 @@ oled_status oled_create(const oled_config* cfg, void** ctx_out) {
       dev_alloc(&c->d_perm, routes) || dev_alloc(&c->d_inv, routes) || dev_alloc(&c->d_flag, 1) ||
       dev_alloc(&c->d_item_counts, 2) || dev_alloc(&c->d_sync, 2) ||
       dev_alloc(&c->d_items, c->max_items) ||
+      (c->dense_ok && (dev_alloc(&c->d_dense_items, c->max_dense) ||
+                       dev_alloc(&c->d_dense_counts, 2))) ||
       dev_alloc(reinterpret_cast<char**>(&c->d_h), routes * c->I * c->esz) ||
       dev_alloc(&c->d_O, routes * c->H) ||
       dev_alloc(&c->d_score, static_cast<size_t>(c->L) * c->E))
@@ -714,6 +745,11 @@ oled_status route_block(void* ctx, int32_t layer, const float* logits_dev, int32
   o.inv_perm = c->d_inv;
   o.items = c->d_items;
   o.item_counts = c->d_item_counts;
+  // experts with many rows go to the dense-tile GEMM
+  o.dense_min = c->dense_ok && static_cast<int64_t>(T) * c->K >= oled::kDenseMinRows
+                    ? oled::kDenseMinRows : 0;
+  o.dense_items = c->d_dense_items;
+  o.dense_counts = c->d_dense_counts;
   o.ring = c->d_ring;
   o.staged = c->copy_mode == OLED_COPY_SDMA ? c->h_staged : nullptr;
   o.layer = layer;
@@ -743,6 +779,7 @@ oled_status route_block(void* ctx, int32_t layer, const float* logits_dev, int32
   c->stage = Stage::kRouted;
   c->cur_layer = layer;
   c->cur_T = T;
+  c->cur_dense = o.dense_min > 0;
   c->cur_stream = s;
   c->have_stream = true;
   c->fwd_x = nullptr;
@@ -806,6 +843,34 @@ oled_status moe_forward_cached(void* ctx, int32_t layer, const void* x_dev, void
   return OLED_OK;
 }
 
+// The dense experts (at least kDenseMinRows routes; hits and misses alike,
+// every weight already in its slot): gate/up tiles, then down tiles. Their
+// item counts are on the device.
+oled_status launch_dense(Ctx* c, int layer, hipStream_t s) {
+  const int64_t routes = static_cast<int64_t>(c->cur_T) * c->K;
+  const int max_items = static_cast<int>(
+      routes / oled::kDenseRows + std::min<int64_t>(c->E, routes / oled::kDenseMinRows));
+  FfnLaunch a = ffn_args(c, layer, 0, max_items, 0);
+  a.items = c->d_dense_items;
+  a.item_counts = c->d_dense_counts;
+  a.src = c->fwd_x;
+  a.src_bytes = static_cast<int64_t>(c->cur_T) * c->H * 2;
+  for (int part = 3; part <= 4; ++part) {
+    const bool up = part == 3;
+    if (!up) {
+      a.src = c->d_h;
+      a.src_bytes = routes * c->I * 2;
+    }
+    OpEvents ev = op_begin(c, up ? OLED_OP_FFN_UP : OLED_OP_FFN_DOWN);
+    HIP_TRY(c, oled::launch_ffn_dense(up, a, ev.a, ev.b, s));
+    OpRec o = rec(up ? OLED_OP_FFN_UP : OLED_OP_FFN_DOWN, layer, -1);
+    o.route_seq = c->cur_route;
+    o.part = part;
+    op_end(c, ev, o);
+  }
+  return OLED_OK;
+}
+
 // Copy-engine transfer: the staged misses (from the routing kernel's list)
 // are copied with hipMemcpyAsync on the copy stream, gate/up parts of all
 // first, then the down parts; if the hits were queued, the misses' GEMMs are
@@ -850,8 +915,18 @@ oled_status apply_misses_sdma(Ctx* c, int layer, hipStream_t cs, const RouteStat
     c->copies_outstanding = true;
   }
   *bytes_out = bytes;
-  if (c->stage != Stage::kHitsQueued || r.n_miss_items <= 0) return OLED_OK;
+  if (c->stage != Stage::kHitsQueued) return OLED_OK;
+  if (r.n_miss_items <= 0) {
+    if (!c->cur_dense) return OLED_OK;
+    if (n > 0) {  // misses with dense items only
+      st = wait_event_spin(c, c->ev_down, "weight copies");
+      if (st != OLED_OK) return st;
+      c->copies_outstanding = false;
+    }
+    return launch_dense(c, layer, s);
+  }
   const bool bf16 = c->dtype == OLED_BF16;
+  const Part mp = streamed(r, false);
   FfnLaunch a = ffn_args(c, layer, 1, r.n_miss_items, 0);
   a.item_base = r.n_hit_items;
   a.n_items_host = r.n_miss_items;
@@ -861,8 +936,7 @@ oled_status apply_misses_sdma(Ctx* c, int layer, hipStream_t cs, const RouteStat
   {
     OpEvents ev = op_begin(c, OLED_OP_FFN_UP);
     HIP_TRY(c, oled::launch_ffn_up(bf16, a, ev.a, ev.b, s));
-    op_end(c, ev, rec(OLED_OP_FFN_UP, layer, up_bytes(c, r.n_misses, r.miss_rows),
-                      up_flops(c, r.miss_rows)));
+    op_end(c, ev, rec(OLED_OP_FFN_UP, layer, up_bytes(c, mp.n, mp.rows), up_flops(c, mp.rows)));
   }
   a.src = c->d_h;
   st = wait_event_spin(c, c->ev_down, "down weight copies");
@@ -871,10 +945,10 @@ oled_status apply_misses_sdma(Ctx* c, int layer, hipStream_t cs, const RouteStat
   {
     OpEvents ev = op_begin(c, OLED_OP_FFN_DOWN);
     HIP_TRY(c, oled::launch_ffn_down(bf16, a, ev.a, ev.b, s));
-    op_end(c, ev, rec(OLED_OP_FFN_DOWN, layer, down_bytes(c, r.n_misses, r.miss_rows),
-                      down_flops(c, r.miss_rows)));
+    op_end(c, ev, rec(OLED_OP_FFN_DOWN, layer, down_bytes(c, mp.n, mp.rows),
+                      down_flops(c, mp.rows)));
   }
-  return OLED_OK;
+  return c->cur_dense ? launch_dense(c, layer, s) : OLED_OK;
 }
 
 oled_status apply_misses(void* ctx, int32_t layer, void* copy_stream, oled_miss_report* out) {
@@ -952,6 +1026,10 @@ oled_status apply_misses(void* ctx, int32_t layer, void* copy_stream, oled_miss_
         o.route_seq = c->cur_route;
         o.part = 1;
         op_end(c, ev, o);
+      }
+      if (c->cur_dense) {
+        st = launch_dense(c, layer, s);
+        if (st != OLED_OK) return st;
       }
     } else {
       // control path: transfer the whole blocks of the staged misses

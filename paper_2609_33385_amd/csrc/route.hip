@@ -154,7 +154,9 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
   __shared__ int32_t s_off[kMaxExperts + 1];
   __shared__ int32_t s_item_base[kMaxExperts];
   __shared__ int32_t s_run[kMaxExperts];
-  __shared__ int32_t s_stat[12];
+  __shared__ int32_t s_stat[16];
+  __shared__ int32_t s_dfull[kMaxExperts];   // first full dense item of the expert, or -1
+  __shared__ int32_t s_dshort[kMaxExperts];  // its short dense item, or -1
   __shared__ int32_t s_sexp[kMaxExperts];
   __shared__ int32_t s_sslot[kMaxExperts];
   __shared__ uint32_t s_res[kMaxExperts / 32];
@@ -174,9 +176,10 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
   if (tid < 64) {  // wave 0: scans over experts, 4 per lane (DPP scans)
     const int lane = tid;
     int c[4], nh[4], nm[4];
-    bool hit[4], miss[4];
-    int sc = 0, sh = 0, sm = 0, sx = 0;
+    bool hit[4], miss[4], dn[4];
+    int sc = 0, sh = 0, sm = 0, sx = 0, sdf = 0, sds = 0;
     int n_act = 0, n_hit = 0, n_res = 0, hrows = 0, mrows = 0;
+    int n_dense = 0, n_dhit = 0, drows = 0, dhrows = 0;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int e = 4 * lane + q;
@@ -185,8 +188,15 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
       const bool res = e < E && ((s_res[e >> 5] >> (e & 31)) & 1u);
       hit[q] = res && c[q] > 0;
       miss[q] = !res && c[q] > 0;
-      nh[q] = hit[q] ? ni : 0;
-      nm[q] = miss[q] ? ni : 0;
+      dn[q] = o.dense_min > 0 && c[q] >= o.dense_min;
+      nh[q] = hit[q] && !dn[q] ? ni : 0;
+      nm[q] = miss[q] && !dn[q] ? ni : 0;
+      sdf += dn[q] ? c[q] / kDenseRows : 0;
+      sds += dn[q] && c[q] % kDenseRows ? 1 : 0;
+      n_dense += dn[q] ? 1 : 0;
+      n_dhit += dn[q] && hit[q] ? 1 : 0;
+      drows += dn[q] ? c[q] : 0;
+      dhrows += dn[q] && hit[q] ? c[q] : 0;
       sc += c[q];
       sh += nh[q];
       sm += nm[q];
@@ -208,17 +218,31 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
     const int n_miss = wave_total(ix);
     const int tot_routes = wave_total(ic);
     const int tot_miss_items = wave_total(im);
+    int idf = 0, ids = 0, tot_full = 0, tot_short = 0;
+    if (o.dense_min > 0) {
+      idf = wave_incl_scan(sdf);
+      ids = wave_incl_scan(sds);
+      tot_full = wave_total(idf);
+      tot_short = wave_total(ids);
+      n_dense = wave_total(wave_incl_scan(n_dense));
+      n_dhit = wave_total(wave_incl_scan(n_dhit));
+      drows = wave_total(wave_incl_scan(drows));
+      dhrows = wave_total(wave_incl_scan(dhrows));
+    }
     // staging: every miss takes a free slot, unless the block is bad
     CacheHdr* hdr = o.cv.hdr;
     const int free_top = *s_ftop;
     const bool stage = !bad && free_top >= 0 && free_top <= o.cv.n_slots && n_miss <= free_top;
-    int xc = ic - sc, xh = ih - sh, xm = im - sm, xx = ix - sx;
+    int xc = ic - sc, xh = ih - sh, xm = im - sm, xx = ix - sx, xdf = idf - sdf,
+        xds = tot_full + ids - sds;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int e = 4 * lane + q;
       if (e < E) {
         s_off[e] = xc;
         s_item_base[e] = (nh[q] > 0) ? xh : tot_hit + xm;
+        s_dfull[e] = dn[q] ? xdf : -1;
+        s_dshort[e] = dn[q] && c[q] % kDenseRows ? xds : -1;
         if (stage && miss[q]) {
           const int slot = s_free[xx];
           o.cv.slot_of[static_cast<size_t>(layer) * E + e] = slot;
@@ -232,6 +256,8 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
       xh += nh[q];
       xm += nm[q];
       xx += miss[q] ? 1 : 0;
+      xdf += dn[q] ? c[q] / kDenseRows : 0;
+      xds += dn[q] && c[q] % kDenseRows ? 1 : 0;
     }
     if (lane == 0) {
       hdr->free_top = stage ? free_top - n_miss : free_top;
@@ -254,6 +280,12 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
       s_off[E] = tot_routes;
       s_stat[8] = tot_hit;
       s_stat[9] = tot_miss_items;
+      s_stat[10] = n_dense;
+      s_stat[11] = n_dhit;
+      s_stat[12] = drows;
+      s_stat[13] = dhrows;
+      s_stat[14] = tot_full;
+      s_stat[15] = tot_short;
     }
     if (lane < kMaxExperts / 32) o.cv.res_before[layer].bits[lane] = s_res[lane];
   }
@@ -264,6 +296,14 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
     o.counts[e] = c;
     o.offsets[e] = s_off[e];
     s_run[e] = s_off[e];
+    if (s_dfull[e] >= 0) {  // dense: full items, then the expert's short item
+      const int full = c / kDenseRows;
+      for (int m = 0; m < full; ++m)
+        o.dense_items[s_dfull[e] + m] = WorkItem{e, s_off[e] + m * kDenseRows, kDenseRows, 0};
+      if (s_dshort[e] >= 0)
+        o.dense_items[s_dshort[e]] = WorkItem{e, s_off[e] + full * kDenseRows, c - full * kDenseRows, 0};
+      continue;
+    }
     const int base = s_item_base[e];
     for (int m = 0; m * kItemRows < c; ++m) {
       WorkItem it;
@@ -324,10 +364,20 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
     rs.bad = bad ? 1 : s_stat[7];
     rs.n_hit_items = s_stat[8];
     rs.n_miss_items = s_stat[9];
+    const bool dense = o.dense_min > 0;
+    rs.n_dense = dense ? s_stat[10] : 0;
+    rs.n_dense_hits = dense ? s_stat[11] : 0;
+    rs.dense_rows = dense ? s_stat[12] : 0;
+    rs.dense_hit_rows = dense ? s_stat[13] : 0;
+    rs.n_dense_items = dense ? s_stat[14] + s_stat[15] : 0;
     rs.seq = o.seq;
     if (tid == 0) {
       o.item_counts[0] = s_stat[8];
       o.item_counts[1] = s_stat[9];
+      if (dense) {
+        o.dense_counts[0] = s_stat[14];
+        o.dense_counts[1] = s_stat[15];
+      }
       o.ring[o.seq % kStatsRing] = rs;
     }
     if (o.staged) {

@@ -203,6 +203,40 @@ def test_cfg45_chain(wid):
     _chain(w, 0, layers, w.n_iters, 8, out_at={(0, 0), (2, w.n_iters - 1)}, out_tokens=rows)
 
 
+DENSE = W.WORKLOADS[1].replace(wid=300, name="dense", dtype="bf16", batch=4, block=256,
+                               n_experts=16, top_k=4, hidden=512, inter=256, n_layers=2,
+                               n_iters=3, capacity=6)
+
+
+@pytest.mark.parametrize("copy_mode", ["shader", "sdma"])
+def test_dense_tiles(copy_mode):
+    """Experts with 128+ routed rows run as dense tiles: this block has experts
+    with two 256-row items, one plus a shorter item, exactly 256 rows, a short
+    item only, and fewer than 128 rows (streaming), as hits and as misses."""
+    _chain(DENSE, 1, range(2), 3, 32, copy_mode=copy_mode)
+
+
+def test_dense_tiles_cross_residency_bitwise():
+    """The dense / streaming split depends on the routed rows only, so outputs
+    stay identical across cache states and transfers."""
+    w = DENSE
+    pool = HN.fill_pool(w, 1, 32)
+    outs = {}
+    for C, mode in ((w.n_experts, "shader"), (w.capacity, "shader"), (0, "shader"),
+                    (w.capacity, "sdma")):
+        ctx = HN.make_context(w, pool, capacity=C, n_layers=2, copy_mode=mode)
+        got = []
+        run_schedule_gpu(ctx, w, 1, range(2), 3, True,
+                         lambda i, li, st, y, rep: got.append(y.copy()))
+        ctx.close()
+        outs[(C, mode)] = got
+    pool.free()
+    base = outs[(w.n_experts, "shader")]
+    for key, got in outs.items():
+        for y0, y1 in zip(base, got):
+            assert np.array_equal(y0, y1), f"{key}: outputs differ from full residency"
+
+
 def test_cross_residency_bitwise():
     """Outputs do not depend on the cache state or the transfer (lossless):
     C = E, 40% and 0 with the shader transfer, 40% with the copy engine."""
