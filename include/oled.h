@@ -178,8 +178,10 @@ typedef enum {
   OLED_OP_FFN_DOWN = 3,      /* grouped down GEMM */
   OLED_OP_COMBINE = 4,       /* combine + priority/retention launch after a forward */
   OLED_OP_SCORE_RETAIN = 5,
-  OLED_OP_H2D = 6            /* copy-engine copies of one apply_misses, or a
+  OLED_OP_H2D = 6,           /* copy-engine copies of one apply_misses, or a
                                 transfer-only launch */
+  OLED_OP_FFN_DENSE_UP = 7,  /* dense-tile gate/up GEMM (experts with 128+ routed rows) */
+  OLED_OP_FFN_DENSE_DOWN = 8 /* dense-tile down GEMM */
 } oled_op_kind;
 
 /* Creates a context: allocates the slot pool (L*min(C,E) + min(E, Tmax*k)

@@ -861,9 +861,10 @@ oled_status launch_dense(Ctx* c, int layer, hipStream_t s) {
       a.src = c->d_h;
       a.src_bytes = routes * c->I * 2;
     }
-    OpEvents ev = op_begin(c, up ? OLED_OP_FFN_UP : OLED_OP_FFN_DOWN);
+    const int kind = up ? OLED_OP_FFN_DENSE_UP : OLED_OP_FFN_DENSE_DOWN;
+    OpEvents ev = op_begin(c, kind);
     HIP_TRY(c, oled::launch_ffn_dense(up, a, ev.a, ev.b, s));
-    OpRec o = rec(up ? OLED_OP_FFN_UP : OLED_OP_FFN_DOWN, layer, -1);
+    OpRec o = rec(kind, layer, -1);
     o.route_seq = c->cur_route;
     o.part = part;
     op_end(c, ev, o);

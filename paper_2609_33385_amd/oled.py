@@ -35,7 +35,7 @@ COPY_MODES = {"shader": OLED_COPY_SHADER, "sdma": OLED_COPY_SDMA}
 PROFILE_ALL = 0x7F
 
 OP_NAMES = {0: "route_topk", 1: "permute", 2: "ffn_up", 3: "ffn_down", 4: "combine",
-            5: "score_retain", 6: "h2d"}
+            5: "score_retain", 6: "h2d", 7: "ffn_dense_up", 8: "ffn_dense_down"}
 OP_KIND = {v: k for k, v in OP_NAMES.items()}
 
 
