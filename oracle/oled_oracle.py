@@ -19,6 +19,11 @@ float64 from the exact input bits:
   O8 retain     R^{i+1} = Top_C(R^i u G^i, p) (the retention rule, Sec. 4.2),
                 with G = M (every miss is transferred to the GPU)
   O9            R^{i+1} feeds the same layer at iteration i+1 (Sec. 4.1)
+  O10 adapt     layer-adaptive cache sizing (Sec. 4.3): smoothed activation
+                ratio a_l and cache utilisation u_l per layer, layer weight
+                w_l = a_l * u_l and capacity C_l = C_total * w_l / sum_j w_j,
+                recomputed every few iterations and enforced by evicting the
+                lowest-priority residents of layers left over capacity
 
 Readings where the paper is silent (each is restated in the design notes):
   * gate function: softmax over the k selected logits (equal to a full softmax
@@ -35,6 +40,24 @@ Readings where the paper is silent (each is restated in the design notes):
     S = 0 are kept while capacity remains (eviction only when over capacity);
   * utilisation = hits / C (fraction of cache capacity serving activated
     experts, Sec. 3.2 and Sec. 5.1).
+Readings of the layer-adaptive sizing (O10), where the paper gives the
+formulas but not the smoothing, the rounding or the enforcement:
+  * smoothing: an exponential moving average with weight 1/2 on the newest
+    observation, per layer, in float64: x <- obs / 2 + x / 2, starting at the
+    first observation; a_obs = |A_l| / E, u_obs = hits_l / C_l (skipped while
+    the layer has capacity 0);
+  * the update runs after every `period` completed iterations of the whole
+    layer stack (period 5 in the paper), counted from the empty cache;
+  * integer capacities: proportional shares q_l = C_avail * w_l / W (W the sum
+    of w over the layers still open, in layer order), layers whose share
+    exceeds E are set to E and the rest re-shared, then the largest-remainder
+    method: floor(q_l) each, and the leftover units one each to the open
+    layers below E in order of (q_l - floor(q_l) desc, layer asc). If every
+    w_l is 0 the capacities stay as they are;
+  * enforcement: a layer holding more experts than its new capacity evicts at
+    once its residents of lowest priority, ranked by (numerator of its last
+    priority desc, id asc); a layer whose capacity grew fills it at its next
+    retentions. So at no time do the layers hold more than C_total experts.
 """
 from __future__ import annotations
 
@@ -224,21 +247,133 @@ def layer_step(logits, conf, resident, top_k: int, capacity: int):
 
 
 def run_schedule(logits_fn, conf_fn, n_layers: int, n_iters: int, n_experts: int,
-                 top_k: int, capacity: int, resident0=None):
+                 top_k: int, capacity: int, resident0=None, adapt_period: int = 0):
     """O9. Replays the cache state of every layer over iterations 0..n_iters-1.
 
     logits_fn(l, i) -> float32 [T][E]; conf_fn(l, i) -> float32 [T].
     The cache starts empty (R^0 = {} per layer) unless resident0 is given.
-    Returns steps[i][l] (the layer_step dicts).
+    Every layer starts with capacity min(C, E). With adapt_period > 0 the
+    capacities are re-sized (O10) after every adapt_period-th iteration.
+    Returns steps[i][l] (the layer_step dicts, each with the `capacity` in
+    effect). After an update, the last layer's dict of that iteration also
+    holds `capacities_after` and `residents_after_update` (every layer's new
+    capacity and resident mask).
     """
     res = [np.zeros(n_experts, dtype=bool) if resident0 is None
            else np.asarray(resident0[l], dtype=bool) for l in range(n_layers)]
+    cap = [min(capacity, n_experts)] * n_layers
+    stats = AdaptStats(n_layers)
     steps = []
     for i in range(n_iters):
         row = []
         for l in range(n_layers):
-            st = layer_step(logits_fn(l, i), conf_fn(l, i), res[l], top_k, capacity)
+            st = layer_step(logits_fn(l, i), conf_fn(l, i), res[l], top_k, cap[l])
+            st["capacity"] = cap[l]
             res[l] = st["resident_after"]
+            if adapt_period > 0:
+                stats.observe(l, st["n_active"], st["n_hits"], cap[l], n_experts)
             row.append(st)
+        if adapt_period > 0 and (i + 1) % adapt_period == 0:
+            cap = adapt_capacities(stats, n_layers * min(capacity, n_experts), n_experts, cap)
+            res = [adapt_shrink(res[l], row[l]["S"], cap[l]) for l in range(n_layers)]
+            row[-1]["capacities_after"] = list(cap)
+            row[-1]["residents_after_update"] = [r.copy() for r in res]
         steps.append(row)
     return steps
+
+
+# ------------------------------------------------- O10 layer-adaptive sizing
+class AdaptStats:
+    """Smoothed per-layer statistics of Sec. 4.3: activation ratio a_l and
+    expert-cache utilisation u_l, exponential moving averages with weight 1/2
+    on the newest observation (float64)."""
+
+    def __init__(self, n_layers: int):
+        self.a = [0.0] * n_layers
+        self.u = [0.0] * n_layers
+        self.has_a = [False] * n_layers
+        self.has_u = [False] * n_layers
+
+    def observe(self, layer: int, n_active: int, n_hits: int, capacity: int, n_experts: int):
+        a_obs = float(n_active) / float(n_experts)
+        self.a[layer] = 0.5 * a_obs + 0.5 * self.a[layer] if self.has_a[layer] else a_obs
+        self.has_a[layer] = True
+        if capacity > 0:
+            u_obs = float(n_hits) / float(capacity)
+            self.u[layer] = 0.5 * u_obs + 0.5 * self.u[layer] if self.has_u[layer] else u_obs
+            self.has_u[layer] = True
+
+    def weights(self):
+        """w_l = a_l * u_l (0 for a layer without a utilisation observation)."""
+        return [self.a[l] * self.u[l] if (self.has_a[l] and self.has_u[l]) else 0.0
+                for l in range(len(self.a))]
+
+
+def adapt_capacities(stats: AdaptStats, c_total: int, n_experts: int, cap_old):
+    """O10. C_l = C_total * w_l / sum_j w_j with w_l = a_l * u_l (Sec. 4.3), in
+    integers: no layer above E (its share is re-spread over the others), then
+    the largest remainder. Returns the new capacities (the old ones if every
+    w_l is 0)."""
+    w = stats.weights()
+    L = len(w)
+    total = 0.0
+    for l in range(L):
+        total += w[l]
+    if total == 0.0:
+        return list(cap_old)
+    cap = [0] * L
+    open_ = [True] * L
+    avail = c_total
+    q = [0.0] * L
+    while True:
+        W = 0.0
+        for l in range(L):
+            if open_[l]:
+                W += w[l]
+        if W == 0.0:
+            for l in range(L):
+                if open_[l]:
+                    q[l] = 0.0
+            break
+        for l in range(L):
+            if open_[l]:
+                q[l] = (float(avail) * w[l]) / W
+        over = [l for l in range(L) if open_[l] and q[l] > n_experts]
+        if not over:
+            break
+        for l in over:
+            cap[l] = n_experts
+            open_[l] = False
+            avail -= n_experts
+    frac = [0.0] * L
+    given = 0
+    for l in range(L):
+        if open_[l]:
+            cap[l] = int(math.floor(q[l]))
+            frac[l] = q[l] - math.floor(q[l])
+            given += cap[l]
+    left = avail - given
+    order = sorted((l for l in range(L) if open_[l] and cap[l] < n_experts),
+                   key=lambda l: (-frac[l], l))
+    for l in order[:max(0, left)]:
+        cap[l] += 1
+    if left < 0:   # rounded shares summing above C_avail: take back from the smallest remainders
+        back = sorted((l for l in range(L) if open_[l] and cap[l] > 0), key=lambda l: (frac[l], -l))
+        for l in back[:-left]:
+            cap[l] -= 1
+    return cap
+
+
+def adapt_shrink(resident: np.ndarray, S: np.ndarray, capacity: int) -> np.ndarray:
+    """O10 enforcement: a layer over its new capacity keeps its `capacity`
+    residents of highest priority, by (S desc, id asc), S the numerators of its
+    last priority update; the rest are evicted."""
+    resident = np.asarray(resident, dtype=bool)
+    held = [e for e in range(len(resident)) if resident[e]]
+    if len(held) <= capacity:
+        return resident.copy()
+    held.sort(key=lambda e: (-int(S[e]), e))
+    keep = np.zeros(len(resident), dtype=bool)
+    for e in held[:max(0, capacity)]:
+        keep[e] = True
+    return keep

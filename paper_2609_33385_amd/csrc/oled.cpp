@@ -611,7 +611,7 @@ oled_status oled_create(const oled_config* cfg, void** ctx_out) {
   c->n_slots = c->L * c->cap + staging;
   c->max_items = static_cast<int>(routes / oled::kItemRows) + c->E + 1;
   c->dense_ok = c->dtype == OLED_BF16 && c->H % 256 == 0 && c->I % 256 == 0 &&
-                routes >= oled::kDenseMinRows && routes * c->I * 2 <= INT32_MAX &&
+                c->Tmax >= oled::kDenseMinRows && routes * c->I * 2 <= INT32_MAX &&
                 static_cast<int64_t>(c->Tmax) * c->H * 2 <= INT32_MAX;
   c->max_dense = c->dense_ok ? static_cast<int>(routes / oled::kDenseRows) + c->E + 1 : 0;
   c->host_pool = static_cast<const char*>(cfg->host_pool);
@@ -745,9 +745,9 @@ oled_status route_block(void* ctx, int32_t layer, const float* logits_dev, int32
   o.inv_perm = c->d_inv;
   o.items = c->d_items;
   o.item_counts = c->d_item_counts;
-  // experts with many rows go to the dense-tile GEMM
-  o.dense_min = c->dense_ok && static_cast<int64_t>(T) * c->K >= oled::kDenseMinRows
-                    ? oled::kDenseMinRows : 0;
+  // experts with many rows go to the dense-tile GEMM; a token picks an expert
+  // at most once, so no expert of a block of fewer tokens can have that many
+  o.dense_min = c->dense_ok && T >= oled::kDenseMinRows ? oled::kDenseMinRows : 0;
   o.dense_items = c->d_dense_items;
   o.dense_counts = c->d_dense_counts;
   o.ring = c->d_ring;
