@@ -140,6 +140,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--capacity", type=int, default=None, help="experts cached per layer")
+    ap.add_argument("--adapt-period", type=int, default=0,
+                    help="layer-adaptive cache sizing every N iterations (0: fixed capacity "
+                         "per layer, the headline configuration)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibration", action="store_true",
                     help="between warm-up and timed steps, run a plain streaming kernel of known traffic (torch "
@@ -153,7 +156,8 @@ def main():
                          "to this JSON file, for matching them with profiler records")
     ap.add_argument("--profile-ops", default="ffn_up",
                     help="operations timed with HIP events during the timed steps: any of "
-                         "ffn_up,ffn_down,h2d,combine,route_topk,permute,score_retain ('' for none)")
+                         "ffn_up,ffn_down,h2d,combine,route_topk,permute,score_retain,"
+                         "layer_adapt ('' for none)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: the expert-offloading layer path has no multi-GPU "
@@ -180,7 +184,7 @@ def main():
     prof = oled.profile_mask(*[o for o in args.profile_ops.split(",") if o])
     ctx = oled.Context(w.hidden, w.inter, E, w.top_k, L, w.capacity, T, w.dtype, pool.ptr,
                        pool.n_blocks, W.host_block_of(w, pool.n_blocks), profile_ops=prof,
-                       copy_mode=args.copy_mode)
+                       copy_mode=args.copy_mode, adapt_period=args.adapt_period)
     log(f"setup {time.time() - t0:.1f}s: pool {pool.n_blocks} x {w.expert_bytes >> 20} MiB pinned")
 
     h = ctx.ctx
@@ -238,6 +242,7 @@ def main():
     # weights (a launch that also transfers misses runs as long as its PCIe reads)
     up, down = agg("ffn_up", transfer=False), agg("ffn_down", transfer=False)
     up_x, down_x, h2d = agg("ffn_up", transfer=True), agg("ffn_down", transfer=True), agg("h2d")
+    adapt = agg("layer_adapt")
     up_gbs = (up["bytes"] / 1e9) / (up["ms"] / 1e3) if up["ms"] > 0 else 0.0
     ffn_ms = up["ms"] + down["ms"]
     ffn_tflops = ((up["flops"] + down["flops"]) / 1e12) / (ffn_ms / 1e3) if ffn_ms > 0 else 0.0
@@ -284,6 +289,8 @@ def main():
             "ffn_mfma_util": round(ffn_tflops / MFMA_BF16_PEAK_TFLOPS, 5) if down["n"] else None,
             "ffn_ms_per_step": round(ffn_ms / args.steps, 4) if down["n"] else None,
             "copy_mode": args.copy_mode,
+            "adapt_period": args.adapt_period,
+            "layer_adapt_us": round(adapt["ms"] / adapt["n"] * 1e3, 2) if adapt["n"] else None,
             "h2d_GBps": h2d_rate,
             "transfer_launches": up_x["n"] + down_x["n"] + h2d["n"],
             "profiled_ops": args.profile_ops,

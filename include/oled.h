@@ -85,7 +85,8 @@ typedef enum { OLED_COPY_SHADER = 0, OLED_COPY_SDMA = 1 } oled_copy_mode;
  * Shape and resources of one MoE layer stack.
  *  hidden H, inter I: multiples of 128. n_experts E in [1, 256]. top_k k in
  *  [1, min(E, 16)]. n_layers L >= 1. capacity C >= 0 experts per layer (C = 0:
- *  every active expert misses; C >= E: full residency). max_tokens Tmax in
+ *  every active expert misses; C >= E: full residency); with adapt_period > 0
+ *  the layers share C_total = L * min(C, E) and each holds at most E. max_tokens Tmax in
  *  [1, 65535] (bounds the integer priority sums, see score_and_retain).
  *  dtype: activations, weights and outputs; accumulation is fp32.
  *
@@ -113,7 +114,10 @@ typedef struct {
   int64_t host_pool_blocks;
   const int64_t* host_block_of;
   int32_t copy_mode;        /* oled_copy_mode */
-  int32_t reserved;
+  int32_t adapt_period;     /* 0: every layer keeps capacity min(C, E). > 0: layer-adaptive
+                               cache sizing (Sec. 4.3) after every adapt_period-th completed
+                               iteration of the layer stack (the paper uses 5); see
+                               score_and_retain. Needs n_layers <= 1024. */
 } oled_config;
 
 /* Result of apply_misses for the layer (Sec. 4.2). Counts are experts. */
@@ -158,6 +162,8 @@ typedef struct {
   int32_t* slot_of;           /* [E] committed cache slot per expert, -1 if absent */
   int32_t tokens;
   int32_t n_active, n_hits, n_misses;
+  int32_t capacity;           /* the layer's cache capacity now (min(C, E) unless adaptive) */
+  int32_t reserved;
 } oled_layer_state;
 
 /* One timed operation (see oled_config.profile_ops). */
@@ -181,14 +187,16 @@ typedef enum {
   OLED_OP_H2D = 6,           /* copy-engine copies of one apply_misses, or a
                                 transfer-only launch */
   OLED_OP_FFN_DENSE_UP = 7,  /* dense-tile gate/up GEMM (experts with 128+ routed rows) */
-  OLED_OP_FFN_DENSE_DOWN = 8 /* dense-tile down GEMM */
+  OLED_OP_FFN_DENSE_DOWN = 8, /* dense-tile down GEMM */
+  OLED_OP_LAYER_ADAPT = 9     /* layer-adaptive re-sizing of the capacities */
 } oled_op_kind;
 
 /* Creates a context: allocates the slot pool (L*min(C,E) + min(E, Tmax*k)
  * expert slots), the device cache state, routing scratch, pinned records, a
  * copy stream and events on cfg->device. The cache starts empty (R = {} for
- * every layer).
- * Errors: INVALID_ARG (bad field, host pool not pinned), UNSUPPORTED (shape),
+ * every layer) with capacity min(C, E) per layer.
+ * Errors: INVALID_ARG (bad field, host pool not pinned, adapt_period < 0),
+ * UNSUPPORTED (shape, or adapt_period > 0 with n_layers > 1024),
  * OUT_OF_MEMORY, HIP. On error *ctx_out is NULL. */
 oled_status oled_create(const oled_config* cfg, void** ctx_out);
 
@@ -199,7 +207,8 @@ void oled_destroy(void* ctx);
  * the last oled_create failure of the calling thread. */
 const char* oled_last_error(const void* ctx);
 
-/* Empties every layer's cache (R := {}), as at creation. Synchronises. Also
+/* Empties every layer's cache (R := {}) and restores capacity min(C, E), the
+ * smoothed statistics and the iteration count, as at creation. Synchronises. Also
  * the way out after OLED_ERR_HIP, which leaves the context refusing
  * route_block (OLED_ERR_STATE) until it is reset. */
 oled_status oled_reset_cache(void* ctx);
@@ -283,12 +292,28 @@ oled_status apply_misses(void* ctx, int32_t layer, void* copy_stream, oled_miss_
  *  is detected on the device: the layer keeps its previous R, its transferred
  *  misses are dropped, and the rejection is reported by the next report of
  *  apply_misses (rejected_layer) and by oled_read_layer_state.
+ *
+ *  Layer-adaptive sizing (oled_config.adapt_period > 0; Sec. 4.3, the layer
+ *  weight w_l = a_l * u_l and the capacity C_l = C_total * w_l / sum_j w_j).
+ *  C is then the layer's current capacity C_l. Each committed retention also
+ *  folds the layer's routing into its smoothed statistics (float64,
+ *  x <- obs/2 + x/2 from the first observation): activation ratio |A| / E and
+ *  utilisation hits / C_l (skipped while C_l = 0). After the retention of
+ *  layer L-1 that completes every adapt_period-th iteration (counted from
+ *  creation or oled_reset_cache), the same stream gets one more launch that
+ *  re-sizes all layers: proportional shares of C_total, none above E (the
+ *  excess re-shared), rounded by the largest remainder (ties to the lower
+ *  layer); if every w_l is 0 nothing changes. A layer now holding more than
+ *  its new C_l evicts its residents of lowest priority at once (its last
+ *  numerators S desc, id asc), so the layers never hold more than C_total
+ *  experts; a layer that grew fills its room at its next retentions.
  */
 oled_status score_and_retain(void* ctx, int32_t layer, const float* conf_dev, void* stream);
 
 /* Inspection (synchronises; see oled_layer_state). With no layer in flight it
  * also checks slot conservation over the whole device cache state (every
- * slot free or held by exactly one resident expert, |R| <= C per layer) and
+ * slot free or held by exactly one resident expert, |R| <= C_l per layer,
+ * capacities within [0, E] summing to at most C_total) and
  * returns HIP if it does not hold. Returns INVALID_ARG (with the arrays
  * filled) if the layer's last retention was rejected, or once after a bad
  * block of the layer that no report has named. */

@@ -34,6 +34,13 @@ struct CacheHdr {
   int32_t staged_slot[kMaxExperts];
 };
 
+// Smoothed statistics of a layer for the layer-adaptive sizing: activation
+// ratio a and cache utilisation u (float64 moving averages).
+struct LayerStat {
+  double a, u;
+  int32_t has_a, has_u;
+};
+
 struct CacheView {
   CacheHdr* hdr;
   int32_t* slot_of;        // [L][E] slot of a resident or staged expert, else -1
@@ -41,8 +48,13 @@ struct CacheView {
   ExpertMask* res_before;  // [L] R when the layer was last routed
   int32_t* last_counts;    // [L][4] n_active, n_hits, n_misses, |R| of the last routing
   int32_t* free_list;      // [n_slots]
+  int32_t* cap;            // [L] capacity of each layer now
+  LayerStat* stat;         // [L] smoothed statistics (updated only when adapt != 0)
+  int adapt;
   int n_slots;
 };
+
+constexpr int kMaxAdaptLayers = 1024;
 
 // One routing call, written by the permute stage into a device ring at
 // seq % kStatsRing; the host copies records out at its synchronisation points.
@@ -204,7 +216,7 @@ struct ScoreArgs {
   const float* conf;
   const int32_t* topk_idx;
   const int32_t* counts;
-  int T, k, E, C, layer, seq;
+  int T, k, E, layer, seq;     // the capacity is cv.cap[layer]
   CacheView cv;
   uint64_t* score_out;
   RetainOut* out;         // device, one per layer
@@ -221,6 +233,16 @@ struct CombineArgs {
 };
 
 hipError_t launch_score_retain(const ScoreArgs& a, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s);
+
+// Layer-adaptive re-sizing of every layer's capacity from the smoothed
+// statistics, and the eviction of the lowest-priority residents of layers
+// left over their new capacity (L <= kMaxAdaptLayers).
+struct AdaptArgs {
+  CacheView cv;
+  const uint64_t* score;  // [L][E] numerators of each layer's last priority update
+  int L, E, c_total;
+};
+hipError_t launch_layer_adapt(const AdaptArgs& a, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s);
 
 // K5 and K6 in one launch (the layer's last).
 hipError_t launch_combine_score(bool bf16, const CombineArgs& c, const ScoreArgs& a,

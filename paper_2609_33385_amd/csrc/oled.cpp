@@ -40,6 +40,7 @@ using oled::CacheView;
 using oled::ExpertMask;
 using oled::FetchArgs;
 using oled::FfnLaunch;
+using oled::LayerStat;
 using oled::PermuteOut;
 using oled::RetainOut;
 using oled::RouteStats;
@@ -67,6 +68,8 @@ struct Ctx {
   // shape
   int H = 0, I = 0, E = 0, K = 0, L = 0, C = 0, Tmax = 0, dtype = 0, esz = 0, device = 0;
   int copy_mode = OLED_COPY_SHADER;
+  int adapt_period = 0;    // layer-adaptive sizing after every adapt_period-th iteration (0: off)
+  int64_t iters_done = 0;  // iterations of the whole stack completed since the last reset
   uint32_t profile_ops = 0;
   int64_t eb = 0;    // bytes of one expert block
   int64_t e13 = 0;   // bytes of its gate/up part
@@ -102,6 +105,8 @@ struct Ctx {
   ExpertMask* d_res_before = nullptr;
   int32_t* d_last_counts = nullptr;  // [L][4]
   int32_t* d_free = nullptr;       // [n_slots]
+  int32_t* d_cap = nullptr;        // [L] capacity of each layer
+  LayerStat* d_stat = nullptr;     // [L] smoothed statistics of the adaptive sizing
   uint64_t* d_host_addr = nullptr; // [L][E]
   // records written by kernels: device memory, copied out at synchronisation
   // points into pinned mirrors; the staged list for host-issued copies is
@@ -325,7 +330,7 @@ void free_ctx(Ctx* c) {
                  c->d_inv, c->d_flag, c->d_item_counts, c->d_sync, c->d_items, c->d_dense_items,
                  c->d_dense_counts, c->d_h, c->d_O,
                  c->d_score, c->d_hdr, c->d_slot_of, c->d_res, c->d_res_before,
-                 c->d_last_counts, c->d_free, c->d_host_addr};
+                 c->d_last_counts, c->d_free, c->d_host_addr, c->d_cap, c->d_stat};
   for (void* p : dev)
     if (p) (void)hipFree(p);
   if (c->h_ring) (void)hipHostFree(c->h_ring);
@@ -358,7 +363,11 @@ oled_status init_cache_state(Ctx* c) {
   HIP_TRY(c, hipMemset(c->d_res_before, 0, sizeof(ExpertMask) * c->L));
   HIP_TRY(c, hipMemset(c->d_last_counts, 0, sizeof(int32_t) * 4 * c->L));
   HIP_TRY(c, hipMemset(c->d_score, 0, sizeof(uint64_t) * c->L * c->E));
+  std::vector<int32_t> caps(c->L, c->cap);
+  HIP_TRY(c, hipMemcpy(c->d_cap, caps.data(), sizeof(int32_t) * c->L, hipMemcpyHostToDevice));
+  HIP_TRY(c, hipMemset(c->d_stat, 0, sizeof(LayerStat) * c->L));
   HIP_TRY(c, hipDeviceSynchronize());
+  c->iters_done = 0;
   return OLED_OK;
 }
 
@@ -370,6 +379,9 @@ CacheView view(const Ctx* c) {
   v.res_before = c->d_res_before;
   v.last_counts = c->d_last_counts;
   v.free_list = c->d_free;
+  v.cap = c->d_cap;
+  v.stat = c->d_stat;
+  v.adapt = c->adapt_period > 0;
   v.n_slots = c->n_slots;
   return v;
 }
@@ -506,7 +518,9 @@ oled_status check_slots(Ctx* c) {
   CacheHdr hdr;
   std::vector<int32_t> slots(static_cast<size_t>(c->L) * c->E), free_list(c->n_slots);
   std::vector<ExpertMask> res(c->L);
+  std::vector<int32_t> caps(c->L);
   HIP_TRY(c, hipMemcpy(&hdr, c->d_hdr, sizeof(hdr), hipMemcpyDeviceToHost));
+  HIP_TRY(c, hipMemcpy(caps.data(), c->d_cap, sizeof(int32_t) * c->L, hipMemcpyDeviceToHost));
   HIP_TRY(c, hipMemcpy(slots.data(), c->d_slot_of, sizeof(int32_t) * slots.size(),
                        hipMemcpyDeviceToHost));
   HIP_TRY(c, hipMemcpy(free_list.data(), c->d_free, sizeof(int32_t) * c->n_slots,
@@ -515,6 +529,14 @@ oled_status check_slots(Ctx* c) {
   if (hdr.fault) return fail(c, OLED_ERR_HIP, "device cache state fault %d", hdr.fault);
   if (hdr.free_top < 0 || hdr.free_top > c->n_slots)
     return fail(c, OLED_ERR_HIP, "free list top %d outside [0,%d]", hdr.free_top, c->n_slots);
+  int64_t cap_sum = 0;
+  for (int l = 0; l < c->L; ++l) {
+    if (caps[l] < 0 || caps[l] > c->E)
+      return fail(c, OLED_ERR_HIP, "layer %d capacity %d outside [0,%d]", l, caps[l], c->E);
+    cap_sum += caps[l];
+  }
+  if (cap_sum > static_cast<int64_t>(c->L) * c->cap)
+    return fail(c, OLED_ERR_HIP, "capacities sum to %lld > C_total", static_cast<long long>(cap_sum));
   std::vector<int> owner(c->n_slots, 0);
   for (int i = 0; i < hdr.free_top; ++i) {
     const int s = free_list[i];
@@ -532,7 +554,8 @@ oled_status check_slots(Ctx* c) {
       if (s < 0) continue;
       if (s >= c->n_slots || owner[s]++) return fail(c, OLED_ERR_HIP, "slot %d held twice", s);
     }
-    if (n_res > c->cap) return fail(c, OLED_ERR_HIP, "layer %d holds %d > C experts", l, n_res);
+    if (n_res > caps[l])
+      return fail(c, OLED_ERR_HIP, "layer %d holds %d > C_l = %d experts", l, n_res, caps[l]);
   }
   for (int s = 0; s < c->n_slots; ++s)
     if (!owner[s]) return fail(c, OLED_ERR_HIP, "slot %d lost", s);
@@ -557,6 +580,9 @@ oled_status oled_create(const oled_config* cfg, void** ctx_out) {
     return bad(OLED_ERR_INVALID_ARG, "dtype must be OLED_F32 or OLED_BF16");
   if (cfg->copy_mode != OLED_COPY_SHADER && cfg->copy_mode != OLED_COPY_SDMA)
     return bad(OLED_ERR_INVALID_ARG, "copy_mode must be OLED_COPY_SHADER or OLED_COPY_SDMA");
+  if (cfg->adapt_period < 0) return bad(OLED_ERR_INVALID_ARG, "adapt_period < 0");
+  if (cfg->adapt_period > 0 && cfg->n_layers > oled::kMaxAdaptLayers)
+    return bad(OLED_ERR_UNSUPPORTED, "adapt_period > 0 needs n_layers <= 1024");
   if (cfg->top_k > cfg->n_experts) return bad(OLED_ERR_INVALID_ARG, "top_k > n_experts");
   if (cfg->hidden % 128 || cfg->inter % 128)
     return bad(OLED_ERR_UNSUPPORTED, "hidden and inter must be multiples of 128");
@@ -600,6 +626,7 @@ oled_status oled_create(const oled_config* cfg, void** ctx_out) {
   c->Tmax = cfg->max_tokens;
   c->dtype = cfg->dtype;
   c->copy_mode = cfg->copy_mode;
+  c->adapt_period = cfg->adapt_period;
   c->esz = cfg->dtype == OLED_F32 ? 4 : 2;
   c->device = cfg->device;
   c->profile_ops = static_cast<uint32_t>(cfg->profile_ops);
@@ -640,7 +667,8 @@ oled_status oled_create(const oled_config* cfg, void** ctx_out) {
     return oom("routing scratch");
   if (dev_alloc(&c->d_hdr, 1) || dev_alloc(&c->d_slot_of, nb) || dev_alloc(&c->d_res, c->L) ||
       dev_alloc(&c->d_res_before, c->L) || dev_alloc(&c->d_last_counts, 4 * c->L) ||
-      dev_alloc(&c->d_free, c->n_slots) || dev_alloc(&c->d_host_addr, nb))
+      dev_alloc(&c->d_free, c->n_slots) || dev_alloc(&c->d_host_addr, nb) ||
+      dev_alloc(&c->d_cap, c->L) || dev_alloc(&c->d_stat, c->L))
     return oom("cache state");
   if (hipMemset(c->d_flag, 0, sizeof(int32_t)) != hipSuccess ||
       hipMemset(c->d_item_counts, 0, 2 * sizeof(int32_t)) != hipSuccess ||
@@ -1095,7 +1123,6 @@ oled_status score_and_retain(void* ctx, int32_t layer, const float* conf_dev, vo
   a.T = c->cur_T;
   a.k = c->K;
   a.E = c->E;
-  a.C = c->C;
   a.layer = layer;
   a.seq = seq;
   a.cv = view(c);
@@ -1126,6 +1153,18 @@ oled_status score_and_retain(void* ctx, int32_t layer, const float* conf_dev, vo
   c->ret_seen[layer] = 0;
   c->stage = Stage::kIdle;
   c->cur_layer = -1;
+  if (c->adapt_period > 0 && layer == c->L - 1 && ++c->iters_done % c->adapt_period == 0) {
+    oled::AdaptArgs ad;
+    ad.cv = view(c);
+    ad.score = c->d_score;
+    ad.L = c->L;
+    ad.E = c->E;
+    ad.c_total = c->L * c->cap;
+    OpEvents ev = op_begin(c, OLED_OP_LAYER_ADAPT);
+    HIP_TRY(c, oled::launch_layer_adapt(ad, ev.a, ev.b, s));
+    op_end(c, ev, rec(OLED_OP_LAYER_ADAPT, layer,
+                      static_cast<int64_t>(c->L) * (c->E * 8 + 64)));
+  }
   return OLED_OK;
 }
 
@@ -1168,6 +1207,10 @@ oled_status oled_read_layer_state(void* ctx, int32_t layer, oled_layer_state* ou
   out->n_active = lc[0];
   out->n_hits = lc[1];
   out->n_misses = lc[2];
+  int32_t cap_now = 0;
+  HIP_TRY(c, hipMemcpy(&cap_now, c->d_cap + layer, sizeof(int32_t), hipMemcpyDeviceToHost));
+  out->capacity = cap_now;
+  out->reserved = 0;
   if (c->stage == Stage::kIdle) {
     st = check_slots(c);
     if (st != OLED_OK) return st;

@@ -25,13 +25,32 @@ __device__ __forceinline__ bool ranks_above(unsigned long long sa, bool ra, int 
   return sa > sb || (sa == sb && (ra > rb || (ra == rb && a < b)));
 }
 
+// Folds the layer's last routing into its smoothed statistics (Sec. 4.3):
+// activation ratio |A| / E and utilisation hits / C, moving averages with
+// weight 1/2 on the newest value (float64; halving is exact, so a fused
+// multiply-add rounds the same as the separate operations).
+__device__ __forceinline__ void observe_layer(const CacheView& cv, int layer, int E, int C) {
+  const int32_t* lc = cv.last_counts + 4 * layer;
+  LayerStat st = cv.stat[layer];
+  const double a_obs = static_cast<double>(lc[0]) / static_cast<double>(E);
+  st.a = st.has_a ? 0.5 * a_obs + 0.5 * st.a : a_obs;
+  st.has_a = 1;
+  if (C > 0) {
+    const double u_obs = static_cast<double>(lc[1]) / static_cast<double>(C);
+    st.u = st.has_u ? 0.5 * u_obs + 0.5 * st.u : u_obs;
+    st.has_u = 1;
+  }
+  cv.stat[layer] = st;
+}
+
 __device__ __forceinline__ void score_body(const ScoreArgs& a) {
   const float* __restrict__ gates = a.gates;
   const float* __restrict__ conf = a.conf;
   const int32_t* __restrict__ topk_idx = a.topk_idx;
   const int32_t* __restrict__ counts = a.counts;
-  const int T = a.T, k = a.k, E = a.E, C = a.C, layer = a.layer;
+  const int T = a.T, k = a.k, E = a.E, layer = a.layer;
   const CacheView& cv = a.cv;
+  const int C = cv.cap[layer];
   uint64_t* __restrict__ score_out = a.score_out;
   RetainOut* __restrict__ out = a.out;
   __shared__ unsigned long long s_S[kMaxExperts];
@@ -149,6 +168,7 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
     out->bad_conf = s_bad;
     out->n_retained = kept;
     out->seq = a.seq;
+    if (cv.adapt && commit) observe_layer(cv, layer, E, C);
   }
 }
 
@@ -199,7 +219,167 @@ __global__ __launch_bounds__(kThreads) void k_combine_score(CombineArgs c, Score
   combine_body<BF16>(c, (b - 1) / hx, (b - 1) % hx);
 }
 
+// Layer-adaptive sizing (Sec. 4.3): w_l = a_l * u_l, C_l = C_total * w_l /
+// sum_j w_j in integers, then the eviction of the lowest-priority residents of
+// every layer left over its new capacity. One workgroup; the shares are
+// computed by one thread in layer order, so every sum has a fixed order.
+//  * shares: q_l = (C_avail * w_l) / W over the open layers (W their sum in
+//    layer order); layers with q_l > E are closed at E and the rest re-shared;
+//  * integers: floor(q_l); the units left go one each to the open layers below
+//    E by (q_l - floor(q_l) desc, layer asc); should the rounded shares
+//    overshoot, the layers with the smallest remainders (ties: higher layer)
+//    give one back;
+//  * eviction: a layer with more residents than C_l keeps those of highest
+//    (S desc, id asc); released slots go back to the free list in expert order.
+// If every w_l is 0 nothing changes.
+__global__ __launch_bounds__(kThreads) void k_layer_adapt(AdaptArgs a) {
+#pragma clang fp contract(off)
+  __shared__ double s_w[kMaxAdaptLayers];
+  __shared__ double s_q[kMaxAdaptLayers];   // share, then its fractional part
+  __shared__ int32_t s_cap[kMaxAdaptLayers];
+  __shared__ uint8_t s_open[kMaxAdaptLayers];
+  __shared__ int32_t s_left, s_skip;
+  __shared__ int32_t s_rank[kMaxExperts];
+  const CacheView& cv = a.cv;
+  const int L = a.L, E = a.E, tid = threadIdx.x;
+  for (int l = tid; l < L; l += kThreads) {
+    const LayerStat st = cv.stat[l];
+    s_w[l] = (st.has_a && st.has_u) ? st.a * st.u : 0.0;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    double total = 0.0;
+    for (int l = 0; l < L; ++l) total += s_w[l];
+    s_skip = total == 0.0;
+    if (!s_skip) {
+      int avail = a.c_total;
+      for (int l = 0; l < L; ++l) {
+        s_open[l] = 1;
+        s_cap[l] = 0;
+      }
+      for (;;) {
+        double W = 0.0;
+        for (int l = 0; l < L; ++l)
+          if (s_open[l]) W += s_w[l];
+        if (W == 0.0) {
+          for (int l = 0; l < L; ++l)
+            if (s_open[l]) s_q[l] = 0.0;
+          break;
+        }
+        int n_over = 0;
+        for (int l = 0; l < L; ++l)
+          if (s_open[l]) {
+            const double num = static_cast<double>(avail) * s_w[l];
+            s_q[l] = num / W;
+            n_over += s_q[l] > static_cast<double>(E);
+          }
+        if (n_over == 0) break;
+        for (int l = 0; l < L; ++l)
+          if (s_open[l] && s_q[l] > static_cast<double>(E)) {
+            s_cap[l] = E;
+            s_open[l] = 0;
+            avail -= E;
+          }
+      }
+      int given = 0;
+      for (int l = 0; l < L; ++l)
+        if (s_open[l]) {
+          const double f = floor(s_q[l]);
+          s_cap[l] = static_cast<int>(f);
+          s_q[l] = s_q[l] - f;
+          given += s_cap[l];
+        }
+      s_left = avail - given;
+    }
+  }
+  __syncthreads();
+  if (s_skip) return;
+  const int left = s_left;
+  for (int l = tid; l < L; l += kThreads) {
+    if (!s_open[l]) continue;
+    const double fl = s_q[l];
+    if (left > 0 && s_cap[l] < E) {
+      int rank = 0;
+      for (int j = 0; j < L; ++j)
+        if (s_open[j] && s_cap[j] < E && (s_q[j] > fl || (s_q[j] == fl && j < l))) ++rank;
+      if (rank < left) ++s_cap[l];
+    } else if (left < 0 && s_cap[l] > 0) {
+      int rank = 0;
+      for (int j = 0; j < L; ++j)
+        if (s_open[j] && s_cap[j] > 0 && (s_q[j] < fl || (s_q[j] == fl && j > l))) ++rank;
+      if (rank < -left) --s_cap[l];
+    }
+  }
+  __syncthreads();
+  for (int l = tid; l < L; l += kThreads) cv.cap[l] = s_cap[l];
+
+  // eviction, layer by layer
+  CacheHdr* hdr = cv.hdr;
+  for (int l = 0; l < L; ++l) {
+    const ExpertMask held = cv.res[l];
+    int n_held = 0;
+#pragma unroll
+    for (int w = 0; w < kMaxExperts / 32; ++w) n_held += __popc(held.bits[w]);
+    const int cap = s_cap[l];
+    if (n_held <= cap) continue;   // uniform across the workgroup
+    const uint64_t* S = a.score + static_cast<size_t>(l) * E;
+    for (int e = tid; e < E; e += kThreads) {
+      int rank = 0;
+      if (held.test(e)) {
+        const uint64_t se = S[e];
+        for (int f = 0; f < E; ++f)
+          if (held.test(f) && (S[f] > se || (S[f] == se && f < e))) ++rank;
+      }
+      s_rank[e] = rank;
+    }
+    __syncthreads();
+    if (tid < 64) {
+      const int lane = tid;
+      int32_t* slot_row = cv.slot_of + static_cast<size_t>(l) * E;
+      int top = hdr->free_top;
+      int fault = 0;
+      uint32_t word[kMaxExperts / 32];
+#pragma unroll
+      for (int q = 0; q < kMaxExperts / 64; ++q) {
+        const int e = lane + 64 * q;
+        const bool h = e < E && held.test(e);
+        const bool drop = h && s_rank[e] >= cap;
+        const int sl = drop ? slot_row[e] : -1;
+        const bool release = drop && sl >= 0;
+        const uint64_t rel = __ballot(release);
+        const int pos = top + __popcll(rel & ((1ull << lane) - 1ull));
+        if (release) {
+          if (pos < cv.n_slots) cv.free_list[pos] = sl;
+          else fault = 2;
+        }
+        if (drop) slot_row[e] = -1;
+        top += __popcll(rel);
+        const uint64_t keep = __ballot(h && !drop);
+        word[2 * q] = static_cast<uint32_t>(keep);
+        word[2 * q + 1] = static_cast<uint32_t>(keep >> 32);
+      }
+      fault = __ballot(fault) ? 2 : 0;
+      uint32_t my_word = 0u;
+#pragma unroll
+      for (int w = 0; w < kMaxExperts / 32; ++w)
+        if (lane == w) my_word = word[w];
+      if (lane < kMaxExperts / 32) cv.res[l].bits[lane] = my_word;
+      if (lane == 0) {
+        hdr->free_top = top > cv.n_slots ? cv.n_slots : top;
+        if (fault) hdr->fault |= fault;
+      }
+    }
+    __syncthreads();
+  }
+}
+
 }  // namespace
+
+hipError_t launch_layer_adapt(const AdaptArgs& a, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
+  if (a.L <= 0 || a.L > kMaxAdaptLayers) return hipErrorInvalidValue;
+  hipExtLaunchKernelGGL(k_layer_adapt, dim3(1), dim3(kThreads), 0, s, ev0, ev1, 0, a);
+  return hipGetLastError();
+}
 
 hipError_t launch_score_retain(const ScoreArgs& a, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
   hipExtLaunchKernelGGL(k_score_retain, dim3(1), dim3(kThreads), 0, s, ev0, ev1, 0, a);

@@ -55,6 +55,7 @@ class Workload:
     sigma_it: float = 0.3 # std of the logit step between adjacent iterations
     zipf_s: float = 0.0   # >0: per-layer Zipf(s) popularity bias on logits
     conf_kind: str = "unmask"   # "beta22" | "uniform" | "unmask"
+    sigma_s_layers: tuple = ()  # non-empty: sigma_s of layer l is sigma_s_layers[l % len]
 
     @property
     def tokens(self) -> int:
@@ -129,14 +130,16 @@ def _layer_bias(w: Workload, seed: int, layer: int) -> np.ndarray:
 def logits_block(w: Workload, seed: int, layer: int, blk: int) -> np.ndarray:
     """Router logits of one layer for every iteration of one block: float32 [N][T][E].
 
-    Iteration 0 is sigma_s * z[seq] + n + bias; each later iteration adds an
+    Iteration 0 is sigma_s * z[seq] + n + bias (sigma_s per layer if
+    sigma_s_layers is set: layers that route with different spread); each later iteration adds an
     independent N(0, sigma_it^2) step (a random walk, so adjacent iterations
     route mostly to the same experts).
     """
     T, E, N = w.tokens, w.n_experts, w.n_iters
     z = _rng(w, seed, _TID_PREF, layer).standard_normal((w.batch, E))
     n = _rng(w, seed, _TID_NOISE, layer, blk).standard_normal((T, E))
-    base = w.sigma_s * np.repeat(z, w.block, axis=0) + n + _layer_bias(w, seed, layer)
+    sig = w.sigma_s_layers[layer % len(w.sigma_s_layers)] if w.sigma_s_layers else w.sigma_s
+    base = sig * np.repeat(z, w.block, axis=0) + n + _layer_bias(w, seed, layer)
     steps = _rng(w, seed, _TID_STEP, layer, blk).standard_normal((N, T, E))
     steps[0] = 0.0
     walk = np.cumsum(w.sigma_it * steps, axis=0)

@@ -166,3 +166,16 @@ def test_pack_expert_errors():
                                 a.ctypes.data) == oled.OLED_ERR_INVALID_ARG
     assert lib.oled_pack_expert(oled.OLED_BF16, 128, 128, None, a.ctypes.data,
                                 a.ctypes.data) == oled.OLED_ERR_INVALID_ARG
+
+
+def test_create_rejects_bad_adapt_period():
+    lib = oled.load()
+    h = ctypes.c_void_p()
+    cfg, _hbo = _cfg(host_pool=1, host_pool_blocks=1)
+    cfg.adapt_period = -1
+    assert lib.oled_create(ctypes.byref(cfg), ctypes.byref(h)) == oled.OLED_ERR_INVALID_ARG
+    assert b"adapt_period" in lib.oled_last_error(None)
+    cfg, _hbo = _cfg(host_pool=1, host_pool_blocks=1, n_layers=1025)
+    cfg.adapt_period = 5
+    assert lib.oled_create(ctypes.byref(cfg), ctypes.byref(h)) == oled.OLED_ERR_UNSUPPORTED
+    assert h.value is None
