@@ -146,7 +146,8 @@ struct FfnLaunch {
 // Every launcher takes optional (ev0, ev1): if non-null they record the
 // kernel's start and end on the dispatch itself (no extra stream packets).
 
-// K1: top-k + fp64 gates, one wavefront per token.
+// K1: top-k + fp64 gates: one wavefront per token, or for large blocks one
+// token per lane.
 hipError_t launch_route_topk(const float* logits, int T, int E, int k, int32_t* topk_idx,
                              float* gates, int32_t* bad_flag, hipEvent_t ev0, hipEvent_t ev1,
                              hipStream_t s);
@@ -169,9 +170,19 @@ struct PermuteOut {
 };
 
 // K2: histogram, offsets, stable permutation, hit-first work list, and the
-// staging of the misses into free slots (device cache state).
+// staging of the misses into free slots (device cache state); one workgroup.
 hipError_t launch_permute(const int32_t* topk_idx, int T, int k, int32_t* bad_flag,
                           const PermuteOut& o, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s);
+
+// K2 over many workgroups for large blocks (permute_chunked true): a counting
+// launch over chunks of 512 tokens whose last workgroup plans the layer, then
+// a ranking launch. chunk_base: [permute_chunks(T)][E] ints of scratch;
+// counter: one device int, zero before the first launch (left zero).
+bool permute_chunked(int T);
+int permute_chunks(int T);
+hipError_t launch_permute_chunked(const int32_t* topk_idx, int T, int k, int32_t* bad_flag,
+                                  int32_t* chunk_base, int32_t* counter, const PermuteOut& o,
+                                  hipEvent_t ev0, hipEvent_t ev1, hipStream_t s);
 
 // K1+K2 as one launch for blocks with T*k <= 1024 (route_fused true): the
 // last workgroup to finish routing permutes. sync: 2 device ints, zero
@@ -220,7 +231,13 @@ struct ScoreArgs {
   CacheView cv;
   uint64_t* score_out;
   RetainOut* out;         // device, one per layer
+  int parts;              // scoring workgroups: score_parts(T, k)
+  unsigned long long* acc;  // [E] zero between launches (several parts only)
+  int32_t* acc_sync;        // [2] completion counter, bad flag; zero between launches
 };
+
+// Workgroups that score a block of T tokens (one up to 8192 routes).
+int score_parts(int T, int k);
 
 // K5 arguments: y[t] = sum_j gate[t][j] * O[inv_perm[t*k + j]], fp32, rounded
 // once to dtype.

@@ -92,6 +92,10 @@ struct Ctx {
   int32_t* d_flag = nullptr;
   int32_t* d_item_counts = nullptr;
   int32_t* d_sync = nullptr;       // completion counter + bad-logit flag of the fused routing
+  int32_t* d_chunk = nullptr;      // [Tmax/512 chunks][E] per-chunk counts / bases (large blocks)
+  int32_t* d_pcount = nullptr;     // completion counter of the chunked permutation
+  unsigned long long* d_sacc = nullptr;  // [E] priority numerators of a many-part scoring
+  int32_t* d_ssync = nullptr;      // [2] its completion counter and bad-confidence flag
   WorkItem* d_items = nullptr;
   WorkItem* d_dense_items = nullptr;
   int32_t* d_dense_counts = nullptr;
@@ -330,7 +334,8 @@ void free_ctx(Ctx* c) {
                  c->d_inv, c->d_flag, c->d_item_counts, c->d_sync, c->d_items, c->d_dense_items,
                  c->d_dense_counts, c->d_h, c->d_O,
                  c->d_score, c->d_hdr, c->d_slot_of, c->d_res, c->d_res_before,
-                 c->d_last_counts, c->d_free, c->d_host_addr, c->d_cap, c->d_stat};
+                 c->d_last_counts, c->d_free, c->d_host_addr, c->d_cap, c->d_stat,
+                 c->d_chunk, c->d_pcount, c->d_sacc, c->d_ssync};
   for (void* p : dev)
     if (p) (void)hipFree(p);
   if (c->h_ring) (void)hipHostFree(c->h_ring);
@@ -366,6 +371,12 @@ oled_status init_cache_state(Ctx* c) {
   std::vector<int32_t> caps(c->L, c->cap);
   HIP_TRY(c, hipMemcpy(c->d_cap, caps.data(), sizeof(int32_t) * c->L, hipMemcpyHostToDevice));
   HIP_TRY(c, hipMemset(c->d_stat, 0, sizeof(LayerStat) * c->L));
+  // counters and accumulators that kernels leave at zero
+  HIP_TRY(c, hipMemset(c->d_flag, 0, sizeof(int32_t)));
+  HIP_TRY(c, hipMemset(c->d_sync, 0, 2 * sizeof(int32_t)));
+  HIP_TRY(c, hipMemset(c->d_pcount, 0, sizeof(int32_t)));
+  HIP_TRY(c, hipMemset(c->d_sacc, 0, sizeof(unsigned long long) * c->E));
+  HIP_TRY(c, hipMemset(c->d_ssync, 0, 2 * sizeof(int32_t)));
   HIP_TRY(c, hipDeviceSynchronize());
   c->iters_done = 0;
   return OLED_OK;
@@ -658,6 +669,8 @@ oled_status oled_create(const oled_config* cfg, void** ctx_out) {
       dev_alloc(&c->d_counts, c->E) || dev_alloc(&c->d_offsets, c->E + 1) ||
       dev_alloc(&c->d_perm, routes) || dev_alloc(&c->d_inv, routes) || dev_alloc(&c->d_flag, 1) ||
       dev_alloc(&c->d_item_counts, 2) || dev_alloc(&c->d_sync, 2) ||
+      dev_alloc(&c->d_chunk, static_cast<size_t>(oled::permute_chunks(c->Tmax)) * c->E) ||
+      dev_alloc(&c->d_pcount, 1) || dev_alloc(&c->d_sacc, c->E) || dev_alloc(&c->d_ssync, 2) ||
       dev_alloc(&c->d_items, c->max_items) ||
       (c->dense_ok && (dev_alloc(&c->d_dense_items, c->max_dense) ||
                        dev_alloc(&c->d_dense_counts, 2))) ||
@@ -672,7 +685,10 @@ oled_status oled_create(const oled_config* cfg, void** ctx_out) {
     return oom("cache state");
   if (hipMemset(c->d_flag, 0, sizeof(int32_t)) != hipSuccess ||
       hipMemset(c->d_item_counts, 0, 2 * sizeof(int32_t)) != hipSuccess ||
-      hipMemset(c->d_sync, 0, 2 * sizeof(int32_t)) != hipSuccess)
+      hipMemset(c->d_sync, 0, 2 * sizeof(int32_t)) != hipSuccess ||
+      hipMemset(c->d_pcount, 0, sizeof(int32_t)) != hipSuccess ||
+      hipMemset(c->d_sacc, 0, sizeof(unsigned long long) * c->E) != hipSuccess ||
+      hipMemset(c->d_ssync, 0, 2 * sizeof(int32_t)) != hipSuccess)
     return oom("scratch init");
   {
     std::vector<uint64_t> addr(nb);
@@ -799,7 +815,11 @@ oled_status route_block(void* ctx, int32_t layer, const float* logits_dev, int32
       op_end(c, ev, rec(OLED_OP_ROUTE_TOPK, layer, route_bytes));
     }
     OpEvents ev = op_begin(c, OLED_OP_PERMUTE);
-    HIP_TRY(c, oled::launch_permute(c->d_topk, T, c->K, c->d_flag, o, ev.a, ev.b, s));
+    if (oled::permute_chunked(T))
+      HIP_TRY(c, oled::launch_permute_chunked(c->d_topk, T, c->K, c->d_flag, c->d_chunk,
+                                              c->d_pcount, o, ev.a, ev.b, s));
+    else
+      HIP_TRY(c, oled::launch_permute(c->d_topk, T, c->K, c->d_flag, o, ev.a, ev.b, s));
     op_end(c, ev, rec(OLED_OP_PERMUTE, layer, perm_bytes));
   }
   c->route_n = n;
@@ -1128,6 +1148,9 @@ oled_status score_and_retain(void* ctx, int32_t layer, const float* conf_dev, vo
   a.cv = view(c);
   a.score_out = c->d_score + static_cast<size_t>(layer) * c->E;
   a.out = c->d_ret + layer;
+  a.parts = oled::score_parts(c->cur_T, c->K);
+  a.acc = c->d_sacc;
+  a.acc_sync = c->d_ssync;
   const int64_t score_bytes = static_cast<int64_t>(c->cur_T) * c->K * 12 +
                               static_cast<int64_t>(c->cur_T) * 4 + static_cast<int64_t>(c->E) * 16;
   if (c->fwd_y) {  // the forward ran: the combine shares the launch

@@ -130,11 +130,142 @@ __global__ __launch_bounds__(256) void k_route_topk(const float* __restrict__ lo
   if (bad && lane == 0) atomicOr(bad_flag, 1);
 }
 
+// Large blocks: one token per lane. A wavefront takes 64 tokens; their
+// logits pass through LDS 32 experts at a time (coalesced row loads, one
+// padded row per token), the next 32 already in flight while the current ones
+// are ranked. Each lane keeps its token's KM best (key, expert) sorted by (key
+// desc, id asc): experts arrive in ascending id and enter only above strictly
+// smaller keys, so equal logits keep the lower id first. The first k of them
+// are the token's routes; gates as in route_token (fp64 exp of l_j - l_0, sum
+// in slot order, one rounding to fp32).
+constexpr int kLaneChunk = 32;
+constexpr int kLaneRow = kLaneChunk + 1;   // padded LDS row (floats): conflict-free lane reads
+
+template <int KM>
+__global__ __launch_bounds__(256) void k_route_lanes(const float* __restrict__ logits, int T, int E,
+                                                     int k, int32_t* __restrict__ topk_idx,
+                                                     float* __restrict__ gates,
+                                                     int32_t* __restrict__ bad_flag) {
+  __shared__ float s_buf[4][64 * kLaneRow];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int t0 = (blockIdx.x * 4 + wave) * 64;
+  float* buf = s_buf[wave];
+  // lane l loads column l % 32 of rows l / 32 + 2 i, i < 32, of a chunk
+  const int lc = lane & 31, lr = lane >> 5;
+  float v[32];
+  auto load = [&](int e0) {
+    const int e = e0 + lc;
+#pragma unroll
+    for (int i = 0; i < 32; ++i) {
+      const int t = t0 + lr + 2 * i;
+      v[i] = (t < T && e < E) ? logits[static_cast<size_t>(t) * E + e] : 0.f;
+    }
+  };
+  uint32_t key[KM];
+  int id[KM];
+#pragma unroll
+  for (int j = 0; j < KM; ++j) {
+    key[j] = 0u;
+    id[j] = -1;
+  }
+  int nonfinite = 0;
+  load(0);
+  for (int e0 = 0; e0 < E; e0 += kLaneChunk) {
+    __syncthreads();   // the previous chunk's reads are done
+#pragma unroll
+    for (int i = 0; i < 32; ++i) buf[(lr + 2 * i) * kLaneRow + lc] = v[i];
+    if (e0 + kLaneChunk < E) load(e0 + kLaneChunk);
+    __syncthreads();
+    const int ne = min(kLaneChunk, E - e0);
+    for (int j = 0; j < ne; ++j) {
+      const float x = buf[lane * kLaneRow + j];
+      nonfinite |= !__builtin_isfinite(x);
+      const uint32_t xk = max(ord_key(x), 1u);
+      const int xe = e0 + j;
+#pragma unroll
+      for (int q = KM - 1; q > 0; --q) {
+        const bool above_prev = xk > key[q - 1];
+        const bool above = xk > key[q];
+        key[q] = above_prev ? key[q - 1] : (above ? xk : key[q]);
+        id[q] = above_prev ? id[q - 1] : (above ? xe : id[q]);
+      }
+      if (xk > key[0]) {
+        key[0] = xk;
+        id[0] = xe;
+      }
+    }
+  }
+  const int t = t0 + lane;
+  if (t < T) {
+    const double v0 = static_cast<double>(ord_value(key[0]));
+    double ex[KM];
+    double sum = 0.0;
+#pragma unroll
+    for (int j = 0; j < KM; ++j) {
+      ex[j] = j < k ? exp(static_cast<double>(ord_value(key[j])) - v0) : 0.0;
+      if (j < k) sum += ex[j];
+    }
+#pragma unroll
+    for (int j = 0; j < KM; ++j)
+      if (j < k) {
+        topk_idx[static_cast<size_t>(t) * k + j] = id[j];
+        gates[static_cast<size_t>(t) * k + j] = static_cast<float>(ex[j] / sum);
+      }
+  }
+  if (__any(t < T && nonfinite) && lane == 0) atomicOr(bad_flag, 1);
+}
+
 constexpr int kPermThreads = 1024;
 constexpr int kChunkWords = 16;               // bitmask words per expert per chunk
 constexpr int kChunkTokens = kChunkWords * 32;
 
 constexpr int kFusedMaxRoutes = 1024;       // fused routing path: T * k routes kept in LDS
+constexpr int kLaneTokensMin = 1024;        // blocks of more tokens route one token per lane
+constexpr int kChunkedMinTokens = 1024;     // and permute over many workgroups
+
+// Stable positions of the routes of tokens [t0, t1) (at most kChunkTokens):
+// a per-expert bitmask of the chunk's tokens that chose the expert (LDS
+// atomics), a running popcount prefix per 32-token word from the expert's
+// base s_run[e], and each route's position = that prefix + the tokens of its
+// word below it (positions outside [0, n_routes) are dropped). Advances s_run
+// past the chunk. Every thread of the workgroup takes part.
+__device__ __forceinline__ void rank_chunk(const int32_t* idx, int t0, int t1, int k, int E,
+                                           int n_routes,
+                                           uint32_t* s_mask, int32_t* s_pre, int32_t* s_run,
+                                           int32_t* __restrict__ perm,
+                                           int32_t* __restrict__ inv_perm) {
+  const int tid = threadIdx.x, nthr = blockDim.x;
+  for (int i = tid; i < E * kChunkWords; i += nthr) s_mask[i] = 0u;
+  __syncthreads();
+  for (int r = t0 * k + tid; r < t1 * k; r += nthr) {
+    const int e = idx[r];
+    const int lt = r / k - t0;
+    atomicOr(&s_mask[e * kChunkWords + (lt >> 5)], 1u << (lt & 31));
+  }
+  __syncthreads();
+  for (int e = tid; e < E; e += nthr) {
+    int run = s_run[e];
+#pragma unroll
+    for (int w = 0; w < kChunkWords; ++w) {
+      s_pre[e * kChunkWords + w] = run;
+      run += __popc(s_mask[e * kChunkWords + w]);
+    }
+    s_run[e] = run;
+  }
+  __syncthreads();
+  for (int r = t0 * k + tid; r < t1 * k; r += nthr) {
+    const int e = idx[r];
+    const int lt = r / k - t0;
+    const int w = lt >> 5;
+    const uint32_t below = s_mask[e * kChunkWords + w] & ((1u << (lt & 31)) - 1u);
+    const int pos = s_pre[e * kChunkWords + w] + __popc(below);
+    if (pos >= 0 && pos < n_routes) {
+      perm[pos] = r;
+      inv_perm[r] = pos;
+    }
+  }
+  __syncthreads();
+}
 
 // Histogram, offsets, work list and stable permutation of the T*k routes in
 // `idx` (global or LDS), by one workgroup, plus the staging of the layer's
@@ -149,7 +280,9 @@ constexpr int kFusedMaxRoutes = 1024;       // fused routing path: T * k routes 
 // system-scope fence, seq).
 __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, int bad,
                                              const PermuteOut& o, const int32_t* s_free,
-                                             const int32_t* s_ftop) {
+                                             const int32_t* s_ftop,
+                                             int32_t* __restrict__ chunk_base = nullptr,
+                                             int n_chunks = 0) {
   __shared__ int32_t s_cnt[kMaxExperts];
   __shared__ int32_t s_off[kMaxExperts + 1];
   __shared__ int32_t s_item_base[kMaxExperts];
@@ -170,7 +303,17 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
   for (int e = tid; e < kMaxExperts; e += nthr) s_cnt[e] = 0;
   if (tid < kMaxExperts / 32) s_res[tid] = o.cv.res[layer].bits[tid];
   __syncthreads();
-  for (int r = tid; r < R; r += nthr) atomicAdd(&s_cnt[idx[r]], 1);
+  if (chunk_base) {   // counts per chunk in chunk_base [n_chunks][E], from other workgroups
+    for (int e = tid; e < E; e += nthr) {
+      int c = 0;
+      for (int ch = 0; ch < n_chunks; ++ch)
+        c += __hip_atomic_load(chunk_base + static_cast<size_t>(ch) * E + e, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+      s_cnt[e] = c;
+    }
+  } else {
+    for (int r = tid; r < R; r += nthr) atomicAdd(&s_cnt[idx[r]], 1);
+  }
   __syncthreads();
 
   if (tid < 64) {  // wave 0: scans over experts, 4 per lane (DPP scans)
@@ -316,37 +459,22 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
   }
   if (tid == 0) o.offsets[E] = s_off[E];
 
-  for (int t0 = 0; t0 < T; t0 += kChunkTokens) {
-    const int t1 = min(T, t0 + kChunkTokens);
-    for (int i = tid; i < E * kChunkWords; i += nthr) s_mask[i] = 0u;
-    __syncthreads();
-    for (int r = t0 * k + tid; r < t1 * k; r += nthr) {
-      const int e = idx[r];
-      const int lt = r / k - t0;
-      atomicOr(&s_mask[e * kChunkWords + (lt >> 5)], 1u << (lt & 31));
-    }
-    __syncthreads();
+  if (chunk_base) {   // per-chunk bases for the ranking launch: exclusive scan over chunks
     for (int e = tid; e < E; e += nthr) {
-      int run = s_run[e];
-#pragma unroll
-      for (int w = 0; w < kChunkWords; ++w) {
-        s_pre[e * kChunkWords + w] = run;
-        run += __popc(s_mask[e * kChunkWords + w]);
+      int run = s_off[e];
+      for (int ch = 0; ch < n_chunks; ++ch) {
+        int32_t* p = chunk_base + static_cast<size_t>(ch) * E + e;
+        const int c = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        *p = run;
+        run += c;
       }
-      s_run[e] = run;
     }
-    __syncthreads();
-    for (int r = t0 * k + tid; r < t1 * k; r += nthr) {
-      const int e = idx[r];
-      const int lt = r / k - t0;
-      const int w = lt >> 5;
-      const uint32_t below = s_mask[e * kChunkWords + w] & ((1u << (lt & 31)) - 1u);
-      const int pos = s_pre[e * kChunkWords + w] + __popc(below);
-      o.perm[pos] = r;
-      o.inv_perm[r] = pos;
-    }
-    __syncthreads();
+  } else {
+    for (int t0 = 0; t0 < T; t0 += kChunkTokens)
+      rank_chunk(idx, t0, min(T, t0 + kChunkTokens), k, E, T * k, s_mask, s_pre, s_run, o.perm,
+                 o.inv_perm);
   }
+  __syncthreads();
 
   // the routing record: device ring (read by the host at its synchronisation
   // points), and for host-issued copies the staged list in pinned memory
@@ -421,6 +549,63 @@ __global__ __launch_bounds__(kPermThreads) void k_permute(const int32_t* __restr
   permute_body(topk_idx, T, k, bad, o, s_free, &s_ftop);
 }
 
+// Large blocks, first launch: workgroup c counts the routes of tokens
+// [512 c, 512 c + 512) per expert into chunk_base[c][E]; the last workgroup to
+// finish (a fenced counter; nobody waits) plans the layer as permute_body does
+// (totals, offsets, work lists, staging, records) and turns the counts into
+// each chunk's first position per expert.
+__global__ __launch_bounds__(kPermThreads) void k_perm_hist(const int32_t* __restrict__ topk_idx,
+                                                            int T, int k,
+                                                            int32_t* __restrict__ bad_flag,
+                                                            int32_t* __restrict__ chunk_base,
+                                                            int32_t* __restrict__ counter,
+                                                            PermuteOut o) {
+  __shared__ int32_t s_h[kMaxExperts];
+  __shared__ int32_t s_free[kMaxExperts];
+  __shared__ int32_t s_ftop;
+  __shared__ int32_t s_last;
+  const int E = o.E, tid = threadIdx.x, nthr = blockDim.x;
+  const int ch = blockIdx.x, n_chunks = gridDim.x;
+  for (int e = tid; e < kMaxExperts; e += nthr) s_h[e] = 0;
+  __syncthreads();
+  const int t0 = ch * kChunkTokens, t1 = min(T, t0 + kChunkTokens);
+  for (int r = t0 * k + tid; r < t1 * k; r += nthr) atomicAdd(&s_h[topk_idx[r]], 1);
+  __syncthreads();
+  for (int e = tid; e < E; e += nthr) chunk_base[static_cast<size_t>(ch) * E + e] = s_h[e];
+  __threadfence();   // this chunk's counts are visible device-wide
+  __syncthreads();
+  if (tid == 0) s_last = atomicAdd(counter, 1) == n_chunks - 1;
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();   // see every other chunk's counts
+  const int bad = __hip_atomic_load(bad_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if ((tid >> 6) == 1) prefetch_free(o.cv, E, s_free, &s_ftop);
+  __syncthreads();
+  if (tid == 0) {   // re-arm for the next launch (stream order)
+    *bad_flag = 0;
+    *counter = 0;
+  }
+  permute_body(topk_idx, T, k, bad, o, s_free, &s_ftop, chunk_base, n_chunks);
+}
+
+// Large blocks, second launch: workgroup c ranks the routes of its chunk from
+// the chunk's first positions per expert.
+__global__ __launch_bounds__(kPermThreads) void k_perm_rank(const int32_t* __restrict__ topk_idx,
+                                                            int T, int k, int E,
+                                                            const int32_t* __restrict__ chunk_base,
+                                                            int32_t* __restrict__ perm,
+                                                            int32_t* __restrict__ inv_perm) {
+  __shared__ uint32_t s_mask[kMaxExperts * kChunkWords];
+  __shared__ int32_t s_pre[kMaxExperts * kChunkWords];
+  __shared__ int32_t s_run[kMaxExperts];
+  const int ch = blockIdx.x;
+  for (int e = threadIdx.x; e < E; e += blockDim.x)
+    s_run[e] = chunk_base[static_cast<size_t>(ch) * E + e];
+  const int t0 = ch * kChunkTokens;
+  rank_chunk(topk_idx, t0, min(T, t0 + kChunkTokens), k, E, T * k, s_mask, s_pre, s_run, perm,
+             inv_perm);
+}
+
 // Small blocks (T*k <= 1024): routing on many CUs, one token per wavefront,
 // then the last workgroup to finish (a fenced counter; no workgroup ever
 // waits for another) permutes all routes. Workgroups hold 256 threads and
@@ -471,9 +656,29 @@ __global__ __launch_bounds__(256) void k_route_fused(const float* __restrict__ l
 
 bool route_fused(int T, int k) { return T * k <= kFusedMaxRoutes; }
 
+bool route_lanes(int T) { return T > kLaneTokensMin; }
+bool permute_chunked(int T) { return T > kChunkedMinTokens; }
+int permute_chunks(int T) { return (T + kChunkTokens - 1) / kChunkTokens; }
+
 hipError_t launch_route_topk(const float* logits, int T, int E, int k, int32_t* topk_idx,
                              float* gates, int32_t* bad_flag, hipEvent_t ev0, hipEvent_t ev1,
                              hipStream_t s) {
+  if (route_lanes(T)) {
+    const int blocks = (T + 255) / 256;
+    if (k <= 2)
+      hipExtLaunchKernelGGL(k_route_lanes<2>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits, T,
+                            E, k, topk_idx, gates, bad_flag);
+    else if (k <= 4)
+      hipExtLaunchKernelGGL(k_route_lanes<4>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits, T,
+                            E, k, topk_idx, gates, bad_flag);
+    else if (k <= 8)
+      hipExtLaunchKernelGGL(k_route_lanes<8>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits, T,
+                            E, k, topk_idx, gates, bad_flag);
+    else
+      hipExtLaunchKernelGGL(k_route_lanes<16>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits,
+                            T, E, k, topk_idx, gates, bad_flag);
+    return hipGetLastError();
+  }
   const int blocks = (T + 3) / 4 < 4096 ? (T + 3) / 4 : 4096;
   if (E <= 64)
     hipExtLaunchKernelGGL(k_route_topk<1>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits, T,
@@ -491,6 +696,19 @@ hipError_t launch_permute(const int32_t* topk_idx, int T, int k, int32_t* bad_fl
                           const PermuteOut& o, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
   hipExtLaunchKernelGGL(k_permute, dim3(1), dim3(kPermThreads), 0, s, ev0, ev1, 0, topk_idx, T, k,
                         bad_flag, o);
+  return hipGetLastError();
+}
+
+hipError_t launch_permute_chunked(const int32_t* topk_idx, int T, int k, int32_t* bad_flag,
+                                  int32_t* chunk_base, int32_t* counter, const PermuteOut& o,
+                                  hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
+  const int n = permute_chunks(T);
+  hipExtLaunchKernelGGL(k_perm_hist, dim3(n), dim3(kPermThreads), 0, s, ev0, nullptr, 0, topk_idx,
+                        T, k, bad_flag, chunk_base, counter, o);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipExtLaunchKernelGGL(k_perm_rank, dim3(n), dim3(kPermThreads), 0, s, nullptr, ev1, 0, topk_idx,
+                        T, k, o.E, chunk_base, o.perm, o.inv_perm);
   return hipGetLastError();
 }
 

@@ -19,6 +19,8 @@ namespace oled {
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kScoreRoutes = 8192;         // routes per scoring workgroup of a large block
+constexpr int kScoreRoutesSingle = 8192;   // up to this many routes one workgroup scores
 
 __device__ __forceinline__ bool ranks_above(unsigned long long sa, bool ra, int a,
                                             unsigned long long sb, bool rb, int b) {
@@ -43,40 +45,19 @@ __device__ __forceinline__ void observe_layer(const CacheView& cv, int layer, in
   cv.stat[layer] = st;
 }
 
-__device__ __forceinline__ void score_body(const ScoreArgs& a) {
+// Segment sums of routes [r0, r1) into s_S (zeroed by the caller): each
+// route's term floor(g * c * 2^48) is added to its expert's segment with an
+// integer LDS atomic. The routes are read in token order, so the expert id,
+// gate and confidence loads of a route are independent. Sets *s_bad for a
+// confidence outside [0, 1].
+__device__ __forceinline__ void score_sums(const ScoreArgs& a, int r0, int r1,
+                                           unsigned long long* s_S, int32_t* s_bad) {
   const float* __restrict__ gates = a.gates;
   const float* __restrict__ conf = a.conf;
   const int32_t* __restrict__ topk_idx = a.topk_idx;
-  const int32_t* __restrict__ counts = a.counts;
-  const int T = a.T, k = a.k, E = a.E, layer = a.layer;
-  const CacheView& cv = a.cv;
-  const int C = cv.cap[layer];
-  uint64_t* __restrict__ score_out = a.score_out;
-  RetainOut* __restrict__ out = a.out;
-  __shared__ unsigned long long s_S[kMaxExperts];
-  __shared__ uint32_t s_rc[kMaxExperts];  // bit 1: previously resident, bit 0: candidate
-  __shared__ int32_t s_rank[kMaxExperts];
-  __shared__ uint32_t s_res[kMaxExperts / 32];
-  __shared__ int32_t s_bad;
-  const int tid = threadIdx.x;
-  if (tid < kMaxExperts / 32) s_res[tid] = cv.res[layer].bits[tid];
-  if (tid == 0) s_bad = 0;
-  __syncthreads();
-  for (int e = tid; e < kMaxExperts; e += kThreads) {
-    s_S[e] = 0ull;
-    s_rank[e] = 0;
-    const bool r = e < E && ((s_res[e >> 5] >> (e & 31)) & 1u);
-    const bool c = e < E && (r || counts[e] > 0);
-    s_rc[e] = (r ? 2u : 0u) | (c ? 1u : 0u);
-  }
-  __syncthreads();
-
-  // Segment sums per expert: each route's term is added to its expert's
-  // segment with an integer LDS atomic. The routes are read in token order,
-  // so the expert id, gate and confidence loads of a route are independent.
+  const int k = a.k;
   int bad = 0;
-  const int R = T * k;
-  for (int r = tid; r < R; r += kThreads) {
+  for (int r = r0 + static_cast<int>(threadIdx.x); r < r1; r += kThreads) {
     const int e = topk_idx[r];
     const float g = gates[r];
     const float c = conf[r / k];
@@ -87,8 +68,33 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
     const double prod = static_cast<double>(g) * static_cast<double>(c);
     atomicAdd(&s_S[e], static_cast<unsigned long long>(floor(prod * 0x1p48)));
   }
-  if (bad) atomicOr(&s_bad, 1);
+  if (bad) atomicOr(s_bad, 1);
+}
+
+// Ranking, retention and commit of one layer from its numerators in s_S (and
+// *s_bad), by one workgroup.
+__device__ __forceinline__ void score_commit(const ScoreArgs& a, unsigned long long* s_S,
+                                             int32_t* p_bad) {
+  const int32_t* __restrict__ counts = a.counts;
+  const int E = a.E, layer = a.layer;
+  const CacheView& cv = a.cv;
+  const int C = cv.cap[layer];
+  uint64_t* __restrict__ score_out = a.score_out;
+  RetainOut* __restrict__ out = a.out;
+  __shared__ uint32_t s_rc[kMaxExperts];  // bit 1: previously resident, bit 0: candidate
+  __shared__ int32_t s_rank[kMaxExperts];
+  __shared__ uint32_t s_res[kMaxExperts / 32];
+  const int tid = threadIdx.x;
+  if (tid < kMaxExperts / 32) s_res[tid] = cv.res[layer].bits[tid];
   __syncthreads();
+  for (int e = tid; e < kMaxExperts; e += kThreads) {
+    s_rank[e] = 0;
+    const bool r = e < E && ((s_res[e >> 5] >> (e & 31)) & 1u);
+    const bool c = e < E && (r || counts[e] > 0);
+    s_rc[e] = (r ? 2u : 0u) | (c ? 1u : 0u);
+  }
+  __syncthreads();
+  const int s_bad = *p_bad;
 
   // Top-C over candidates R u A by (S desc, previously resident first, id
   // asc): rank[e] = number of candidates above e. Thread pairs (e, quarter of
@@ -204,19 +210,69 @@ __device__ __forceinline__ void combine_body(const CombineArgs& c, int t, int hb
   }
 }
 
-__global__ __launch_bounds__(kThreads) void k_score_retain(ScoreArgs a) { score_body(a); }
+// Priority numerators and retention of one layer by the first a.parts
+// workgroups of a launch. One part: that workgroup sums every route and
+// commits. Several parts (large blocks): part p sums routes [p*n, (p+1)*n)
+// (n = kScoreRoutes) into LDS, adds its nonzero numerators to the device
+// accumulators with integer atomics (any order, same bits), and the last part
+// to finish (a fenced counter; nobody waits) reads the totals, re-arms the
+// accumulators and commits.
+__device__ __forceinline__ void score_part(const ScoreArgs& a, int part) {
+  __shared__ unsigned long long s_S[kMaxExperts];
+  __shared__ int32_t s_bad;
+  __shared__ int32_t s_last;
+  const int tid = threadIdx.x, E = a.E;
+  const int R = a.T * a.k;
+  for (int e = tid; e < kMaxExperts; e += kThreads) s_S[e] = 0ull;
+  if (tid == 0) s_bad = 0;
+  __syncthreads();
+  if (a.parts <= 1) {
+    score_sums(a, 0, R, s_S, &s_bad);
+    __syncthreads();
+    score_commit(a, s_S, &s_bad);
+    return;
+  }
+  const int r0 = part * kScoreRoutes;
+  score_sums(a, r0, min(R, r0 + kScoreRoutes), s_S, &s_bad);
+  __syncthreads();
+  for (int e = tid; e < E; e += kThreads)
+    if (s_S[e]) atomicAdd(&a.acc[e], s_S[e]);
+  if (tid == 0 && s_bad) atomicOr(&a.acc_sync[1], 1);
+  __threadfence();   // this part's sums are visible device-wide
+  __syncthreads();
+  if (tid == 0) s_last = atomicAdd(&a.acc_sync[0], 1) == a.parts - 1;
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();   // see every other part's sums
+  for (int e = tid; e < E; e += kThreads) {
+    s_S[e] = __hip_atomic_load(&a.acc[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    a.acc[e] = 0ull;   // re-arm for the next launch (stream order)
+  }
+  if (tid == 0) {
+    s_bad = __hip_atomic_load(&a.acc_sync[1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    a.acc_sync[0] = 0;
+    a.acc_sync[1] = 0;
+  }
+  __syncthreads();
+  score_commit(a, s_S, &s_bad);
+}
 
-// The layer's last launch: workgroup 0 scores and commits the retention,
-// workgroups 1.. combine (the two parts touch disjoint data).
+__global__ __launch_bounds__(kThreads) void k_score_retain(ScoreArgs a) {
+  score_part(a, blockIdx.x);
+}
+
+// The layer's last launch: workgroups [0, a.parts) score and commit the
+// retention, the rest combine (the two parts touch disjoint data).
 template <bool BF16>
 __global__ __launch_bounds__(kThreads) void k_combine_score(CombineArgs c, ScoreArgs a) {
   const int b = blockIdx.x;
-  if (b == 0) {
-    score_body(a);
+  const int np = a.parts < 1 ? 1 : a.parts;
+  if (b < np) {
+    score_part(a, b);
     return;
   }
   const int hx = (c.H + 1023) / 1024;
-  combine_body<BF16>(c, (b - 1) / hx, (b - 1) % hx);
+  combine_body<BF16>(c, (b - np) / hx, (b - np) % hx);
 }
 
 // Layer-adaptive sizing (Sec. 4.3): w_l = a_l * u_l, C_l = C_total * w_l /
@@ -381,14 +437,21 @@ hipError_t launch_layer_adapt(const AdaptArgs& a, hipEvent_t ev0, hipEvent_t ev1
   return hipGetLastError();
 }
 
+int score_parts(int T, int k) {
+  const int64_t R = static_cast<int64_t>(T) * k;
+  return R <= kScoreRoutesSingle ? 1 : static_cast<int>((R + kScoreRoutes - 1) / kScoreRoutes);
+}
+
 hipError_t launch_score_retain(const ScoreArgs& a, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
-  hipExtLaunchKernelGGL(k_score_retain, dim3(1), dim3(kThreads), 0, s, ev0, ev1, 0, a);
+  if (a.parts != score_parts(a.T, a.k)) return hipErrorInvalidValue;
+  hipExtLaunchKernelGGL(k_score_retain, dim3(a.parts), dim3(kThreads), 0, s, ev0, ev1, 0, a);
   return hipGetLastError();
 }
 
 hipError_t launch_combine_score(bool bf16, const CombineArgs& c, const ScoreArgs& a,
                                 hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
-  const int grid = 1 + c.T * ((c.H + 1023) / 1024);
+  if (a.parts != score_parts(a.T, a.k)) return hipErrorInvalidValue;
+  const int grid = a.parts + c.T * ((c.H + 1023) / 1024);
   if (bf16)
     hipExtLaunchKernelGGL(k_combine_score<true>, dim3(grid), dim3(kThreads), 0, s, ev0, ev1, 0, c, a);
   else

@@ -1,0 +1,82 @@
+"""GPU parity at large blocks, where routing takes one token per lane, the
+permutation runs over many workgroups (counting launch + ranking launch) and
+the priority numerators are summed by several workgroups: the largest block
+(65535 tokens), ragged chunk tails, top-k below the kernel's list length,
+expert counts that are not a multiple of the 32-expert LDS chunk, and fp32.
+Control path bit for bit against the oracle at every layer-iteration; layer
+outputs on sampled token rows."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import oled_oracle as O
+from paper_2609_33385_amd import harness as HN
+from paper_2609_33385_amd import oled
+from paper_2609_33385_amd import workload as W
+
+from gpu_common import (OracleWeights, compare_control, oracle_schedule, rel_l2, run_schedule_gpu,
+                        tol)
+
+pytestmark = pytest.mark.gpu
+
+BASE = W.WORKLOADS[2].replace(n_experts=128, top_k=8, hidden=256, inter=256, n_layers=2, n_iters=3,
+                              capacity=51)
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    oled.load()
+
+
+def _run(w, seed, forward=False, out_rows=16):
+    layers = list(range(w.n_layers))
+    _say(f"[large] {w.name} T={w.tokens} E={w.n_experts} k={w.top_k} {w.dtype} C={w.capacity} "
+         f"forward={forward}")
+    ref = oracle_schedule(w, seed, layers, w.n_iters, w.capacity)
+    pool = HN.fill_pool(w, seed, 8)
+    ctx = HN.make_context(w, pool)
+    ow = OracleWeights(w, seed, 8, len(layers))
+    rows = np.random.default_rng(seed).choice(w.tokens, min(out_rows, w.tokens), replace=False)
+    worst = [0.0]
+
+    def check(i, li, st, y, rep):
+        o = ref[i][li]
+        compare_control(st, o, w.tokens, f"{w.name} l={li} i={i}")
+        if y is not None:
+            x = O.decode(W.activations(w, seed, layers[li], 0, i))
+            y_ref = O.moe_output(x, o["idx"], o["gates"], ow.fn(li), tokens=rows)
+            err = rel_l2(O.decode(y)[rows], y_ref)
+            worst[0] = max(worst[0], err)
+            assert err <= tol(w), f"l={li} i={i}: rel L2 {err:.3e}"
+
+    try:
+        run_schedule_gpu(ctx, w, seed, layers, w.n_iters, forward, check)
+    finally:
+        ctx.close()
+        pool.free()
+    _say(f"[large] ok, worst rel L2 {worst[0]:.3e}")
+
+
+def test_largest_block_control_path():
+    _run(BASE.replace(wid=320, name="t65535", batch=255, block=257), 0)
+
+
+@pytest.mark.parametrize("E,k,batch,block", [(128, 8, 17, 241), (64, 6, 9, 130), (200, 3, 5, 411),
+                                              (40, 1, 3, 700)])
+def test_ragged_blocks_forward(E, k, batch, block):
+    w = BASE.replace(wid=321, name=f"e{E}k{k}t{batch * block}", n_experts=E, top_k=k, batch=batch,
+                     block=block, capacity=int(0.4 * E))
+    _run(w, 1, forward=True)
+
+
+def test_large_block_f32():
+    w = BASE.replace(wid=322, name="f32-t3000", dtype="f32", batch=12, block=250, capacity=40)
+    _run(w, 2, forward=True)
