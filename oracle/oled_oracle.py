@@ -19,6 +19,9 @@ float64 from the exact input bits:
   O8 retain     R^{i+1} = Top_C(R^i u G^i, p) (the retention rule, Sec. 4.2),
                 with G = M (every miss is transferred to the GPU)
   O9            R^{i+1} feeds the same layer at iteration i+1 (Sec. 4.1)
+  O11 policies  the comparison retention policies of Sec. 5.1 / 5.3 (LRU,
+                LFU) in place of the priority, the clairvoyant ideal cache
+                bound, and the effective transfer ratio (Sec. 5.3)
   O10 adapt     layer-adaptive cache sizing (Sec. 4.3): smoothed activation
                 ratio a_l and cache utilisation u_l per layer, layer weight
                 w_l = a_l * u_l and capacity C_l = C_total * w_l / sum_j w_j,
@@ -40,6 +43,19 @@ Readings where the paper is silent (each is restated in the design notes):
     S = 0 are kept while capacity remains (eviction only when over capacity);
   * utilisation = hits / C (fraction of cache capacity serving activated
     experts, Sec. 3.2 and Sec. 5.1).
+Readings of the comparison policies (O11), which the paper names but does not
+define:
+  * every policy keeps Top_C of the same candidates R u M and differs only in
+    the primary key, with the same tie-breaks (previously resident first, id
+    asc): LRU ranks by the layer iteration in which the expert was last
+    activated (iterations of the layer counted from 1 since the empty cache);
+    LFU by the number of routes (tokens) sent to it in the layer since the
+    empty cache, evicted or not;
+  * ideal cache bound: with perfect knowledge of A, the most activated experts
+    a cache of C can hold before the layer runs, min(C, |A|) hits;
+  * effective transfer ratio: of the experts transferred at a layer's
+    iteration i, the share retained and activated again at its iteration
+    i + 1, summed over iterations that have a next one.
 Readings of the layer-adaptive sizing (O10), where the paper gives the
 formulas but not the smoothing, the rounding or the enforcement:
   * smoothing: an exponential moving average with weight 1/2 on the newest
@@ -55,9 +71,10 @@ formulas but not the smoothing, the rounding or the enforcement:
     layers below E in order of (q_l - floor(q_l) desc, layer asc). If every
     w_l is 0 the capacities stay as they are;
   * enforcement: a layer holding more experts than its new capacity evicts at
-    once its residents of lowest priority, ranked by (numerator of its last
-    priority desc, id asc); a layer whose capacity grew fills it at its next
-    retentions. So at no time do the layers hold more than C_total experts.
+    once its residents of lowest priority, ranked by (its last retention key
+    desc, id asc), the key being the priority numerator S under the paper's
+    policy; a layer whose capacity grew fills it at its next retentions. So at
+    no time do the layers hold more than C_total experts.
 """
 from __future__ import annotations
 
@@ -225,29 +242,40 @@ def retain(S: np.ndarray, resident: np.ndarray, miss: np.ndarray, capacity: int)
 
 
 # --------------------------------------------------- O1..O9, one layer-step
-def layer_step(logits, conf, resident, top_k: int, capacity: int):
+def layer_step(logits, conf, resident, top_k: int, capacity: int, policy: str = "priority",
+               history=None):
     """Control path of one layer-iteration (O1-O3, O6-O8): no expert outputs.
 
-    Returns a dict with idx, gates, counts, offsets, perm, inv_perm, active,
-    hit, miss, n_hits, n_misses, util, S, p and the new resident mask.
+    policy "priority" (the paper's) ranks the candidates by S; "lru" / "lfu"
+    (O11) by the layer's history, which `history` (a PolicyHistory) carries
+    from one iteration to the next. Returns a dict with idx, gates, counts,
+    offsets, perm, inv_perm, active, hit, miss, n_hits, n_misses, util, S, p,
+    the retention key and the new resident mask.
     """
     E = logits.shape[1]
     idx, gates = route(logits, top_k)
     counts, offsets, perm, inv_perm = permute(idx, E)
     active, hit, miss = classify(counts, resident)
     S, p = score(idx, gates, conf, E)
-    new_res = retain(S, resident, miss, capacity)
+    if policy == "priority":
+        key = S
+    else:
+        history.observe(counts)
+        key = history.key(policy)
+    new_res = retain(key, resident, miss, capacity)
     n_hits = int(hit.sum())
     return dict(idx=idx, gates=gates, counts=counts, offsets=offsets, perm=perm,
                 inv_perm=inv_perm, active=active, hit=hit, miss=miss,
                 n_active=int(active.sum()), n_hits=n_hits, n_misses=int(miss.sum()),
                 util=(n_hits / capacity if capacity > 0 else 0.0),
-                S=S, p=p, resident_before=np.asarray(resident, dtype=bool).copy(),
+                S=S, p=p, key=np.asarray(key, dtype=np.uint64),
+                resident_before=np.asarray(resident, dtype=bool).copy(),
                 resident_after=new_res)
 
 
 def run_schedule(logits_fn, conf_fn, n_layers: int, n_iters: int, n_experts: int,
-                 top_k: int, capacity: int, resident0=None, adapt_period: int = 0):
+                 top_k: int, capacity: int, resident0=None, adapt_period: int = 0,
+                 policy: str = "priority"):
     """O9. Replays the cache state of every layer over iterations 0..n_iters-1.
 
     logits_fn(l, i) -> float32 [T][E]; conf_fn(l, i) -> float32 [T].
@@ -257,29 +285,78 @@ def run_schedule(logits_fn, conf_fn, n_layers: int, n_iters: int, n_experts: int
     Returns steps[i][l] (the layer_step dicts, each with the `capacity` in
     effect). After an update, the last layer's dict of that iteration also
     holds `capacities_after` and `residents_after_update` (every layer's new
-    capacity and resident mask).
+    capacity and resident mask). `policy` selects the retention key (O11).
+    Each dict also holds `prev_transferred` (experts the layer transferred at
+    its previous iteration) and `reused_transfers` (those of them retained and
+    activated now), the terms of the effective transfer ratio.
     """
+    if policy not in POLICIES:
+        raise ValueError(f"unknown policy {policy}")
     res = [np.zeros(n_experts, dtype=bool) if resident0 is None
            else np.asarray(resident0[l], dtype=bool) for l in range(n_layers)]
     cap = [min(capacity, n_experts)] * n_layers
     stats = AdaptStats(n_layers)
+    hist = [PolicyHistory(n_experts) for _ in range(n_layers)]
+    prev_miss = [np.zeros(n_experts, dtype=bool) for _ in range(n_layers)]
     steps = []
     for i in range(n_iters):
         row = []
         for l in range(n_layers):
-            st = layer_step(logits_fn(l, i), conf_fn(l, i), res[l], top_k, cap[l])
+            st = layer_step(logits_fn(l, i), conf_fn(l, i), res[l], top_k, cap[l], policy, hist[l])
             st["capacity"] = cap[l]
+            st["prev_transferred"] = int(prev_miss[l].sum())
+            st["reused_transfers"] = int((st["active"] & st["resident_before"] & prev_miss[l]).sum())
+            prev_miss[l] = st["miss"].copy()
             res[l] = st["resident_after"]
             if adapt_period > 0:
                 stats.observe(l, st["n_active"], st["n_hits"], cap[l], n_experts)
             row.append(st)
         if adapt_period > 0 and (i + 1) % adapt_period == 0:
             cap = adapt_capacities(stats, n_layers * min(capacity, n_experts), n_experts, cap)
-            res = [adapt_shrink(res[l], row[l]["S"], cap[l]) for l in range(n_layers)]
+            res = [adapt_shrink(res[l], row[l]["key"], cap[l]) for l in range(n_layers)]
             row[-1]["capacities_after"] = list(cap)
             row[-1]["residents_after_update"] = [r.copy() for r in res]
         steps.append(row)
     return steps
+
+
+# ------------------------------------------- O11 comparison retention policies
+POLICIES = ("priority", "lru", "lfu")
+
+
+class PolicyHistory:
+    """History of one layer for LRU and LFU retention: the layer iteration in
+    which each expert was last activated (iterations counted from 1; 0 never)
+    and the routes sent to it so far."""
+
+    def __init__(self, n_experts: int):
+        self.iters = 0
+        self.last_use = [0] * n_experts
+        self.freq = [0] * n_experts
+
+    def observe(self, counts):
+        self.iters += 1
+        for e, c in enumerate(counts):
+            if c > 0:
+                self.last_use[e] = self.iters
+                self.freq[e] += int(c)
+
+    def key(self, policy: str):
+        return self.last_use if policy == "lru" else self.freq
+
+
+def ideal_hits(n_active: int, capacity: int) -> int:
+    """Clairvoyant ideal cache bound of one layer-iteration: knowing A, a cache
+    of C experts holds min(C, |A|) of them when the layer runs."""
+    return min(capacity, n_active)
+
+
+def effective_transfer_ratio(steps) -> float:
+    """Share of transferred experts retained and activated again at the next
+    iteration of their layer (over transfers that have a next iteration)."""
+    moved = sum(st["prev_transferred"] for row in steps for st in row)
+    reused = sum(st["reused_transfers"] for row in steps for st in row)
+    return reused / moved if moved else 0.0
 
 
 # ------------------------------------------------- O10 layer-adaptive sizing
@@ -366,8 +443,9 @@ def adapt_capacities(stats: AdaptStats, c_total: int, n_experts: int, cap_old):
 
 def adapt_shrink(resident: np.ndarray, S: np.ndarray, capacity: int) -> np.ndarray:
     """O10 enforcement: a layer over its new capacity keeps its `capacity`
-    residents of highest priority, by (S desc, id asc), S the numerators of its
-    last priority update; the rest are evicted."""
+    residents of highest priority, by (S desc, id asc), S the keys of its last
+    retention (the priority numerators under the paper's policy); the rest are
+    evicted."""
     resident = np.asarray(resident, dtype=bool)
     held = [e for e in range(len(resident)) if resident[e]]
     if len(held) <= capacity:
