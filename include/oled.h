@@ -80,6 +80,13 @@ typedef enum { OLED_F32 = 0, OLED_BF16 = 1 } oled_dtype;
 /* How the misses reach their staging slots (see above). */
 typedef enum { OLED_COPY_SHADER = 0, OLED_COPY_SDMA = 1 } oled_copy_mode;
 
+/* Retention key of score_and_retain. OLED_POLICY_PRIORITY is the paper's
+ * confidence-gate priority (Sec. 4.3); LRU and LFU are the comparison
+ * policies of its evaluation (Sec. 5.1, Sec. 5.3), ranking the same
+ * candidates by the layer iteration of each expert's last activation, or by
+ * the routes sent to it so far, with the same tie-breaks. */
+typedef enum { OLED_POLICY_PRIORITY = 0, OLED_POLICY_LRU = 1, OLED_POLICY_LFU = 2 } oled_policy;
+
 
 /*
  * Shape and resources of one MoE layer stack.
@@ -118,6 +125,8 @@ typedef struct {
                                cache sizing (Sec. 4.3) after every adapt_period-th completed
                                iteration of the layer stack (the paper uses 5); see
                                score_and_retain. Needs n_layers <= 1024. */
+  int32_t policy;           /* oled_policy */
+  int32_t reserved;
 } oled_config;
 
 /* Result of apply_misses for the layer (Sec. 4.2). Counts are experts. */
@@ -141,6 +150,10 @@ typedef struct {
   int64_t n_transferred;  /* misses given a staging slot and transferred */
   int64_t h2d_bytes;      /* their bytes */
   int64_t n_bad_blocks;   /* blocks with a non-finite logit (nothing staged) */
+  int64_t n_prev_transferred;  /* experts each routed layer transferred at its previous
+                                  iteration (the effective transfer ratio's denominator) */
+  int64_t n_transfers_reused;  /* of those, retained and activated again (its numerator,
+                                  Sec. 5.3) */
 } oled_stats;
 
 /*
@@ -164,6 +177,11 @@ typedef struct {
   int32_t n_active, n_hits, n_misses;
   int32_t capacity;           /* the layer's cache capacity now (min(C, E) unless adaptive) */
   int32_t reserved;
+  uint64_t* retain_key;       /* [E] key of the last retention of `layer` (score_q under
+                                 OLED_POLICY_PRIORITY; last activation / routes under LRU / LFU) */
+  int32_t prev_transferred;   /* the last routing of `layer`: experts it transferred at its
+                                 previous iteration, */
+  int32_t reused_transfers;   /* and those of them retained and activated now */
 } oled_layer_state;
 
 /* One timed operation (see oled_config.profile_ops). */
@@ -280,6 +298,8 @@ oled_status apply_misses(void* ctx, int32_t layer, void* copy_stream, oled_miss_
 
 /*
  * score_and_retain: priorities of Sec. 4.3 and the retention rule of Sec. 4.2.
+ *  (With oled_config.policy LRU or LFU the candidates are ranked by that key
+ *  instead of S; S is still computed and reported.)
  *  conf_dev: float [T] token confidence in [0, 1]. For each expert,
  *  S[e] = sum over its routes of floor(fp64(gate) * fp64(conf[t]) * 2^48)
  *  (exact; p_e = S[e] / sum S). Residents that no token routed to score 0.

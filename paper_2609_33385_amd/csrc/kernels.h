@@ -46,13 +46,21 @@ struct CacheView {
   int32_t* slot_of;        // [L][E] slot of a resident or staged expert, else -1
   ExpertMask* res;         // [L] committed resident set R
   ExpertMask* res_before;  // [L] R when the layer was last routed
-  int32_t* last_counts;    // [L][4] n_active, n_hits, n_misses, |R| of the last routing
+  int32_t* last_counts;    // [L][kCountsPerLayer] n_active, n_hits, n_misses, |R|, experts
+                           // transferred at the previous iteration, of them reused now
   int32_t* free_list;      // [n_slots]
   int32_t* cap;            // [L] capacity of each layer now
   LayerStat* stat;         // [L] smoothed statistics (updated only when adapt != 0)
   int adapt;
   int n_slots;
+  int policy;              // retention key: 0 priority, 1 LRU, 2 LFU
+  int32_t* iters;          // [L] iterations of each layer (LRU / LFU history)
+  int32_t* last_use;       // [L][E] layer iteration of the last activation (0: never)
+  uint64_t* freq;          // [L][E] routes so far
+  ExpertMask* prev_miss;   // [L] misses transferred at the layer's previous iteration
 };
+
+constexpr int kCountsPerLayer = 8;
 
 constexpr int kMaxAdaptLayers = 1024;
 
@@ -75,6 +83,8 @@ struct RouteStats {
   int32_t dense_rows;
   int32_t dense_hit_rows;
   int32_t n_dense_items;
+  int32_t prev_xfer;   // experts transferred at the layer's previous iteration
+  int32_t reused_xfer; // of them retained and activated now
   int32_t seq;
 };
 
@@ -231,6 +241,7 @@ struct ScoreArgs {
   CacheView cv;
   uint64_t* score_out;
   RetainOut* out;         // device, one per layer
+  uint64_t* key_out;      // [E] retention key of each expert (S under the priority policy)
   int parts;              // scoring workgroups: score_parts(T, k)
   unsigned long long* acc;  // [E] zero between launches (several parts only)
   int32_t* acc_sync;        // [2] completion counter, bad flag; zero between launches
@@ -256,7 +267,7 @@ hipError_t launch_score_retain(const ScoreArgs& a, hipEvent_t ev0, hipEvent_t ev
 // left over their new capacity (L <= kMaxAdaptLayers).
 struct AdaptArgs {
   CacheView cv;
-  const uint64_t* score;  // [L][E] numerators of each layer's last priority update
+  const uint64_t* score;  // [L][E] keys of each layer's last retention
   int L, E, c_total;
 };
 hipError_t launch_layer_adapt(const AdaptArgs& a, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s);

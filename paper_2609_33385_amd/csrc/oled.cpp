@@ -69,6 +69,7 @@ struct Ctx {
   int H = 0, I = 0, E = 0, K = 0, L = 0, C = 0, Tmax = 0, dtype = 0, esz = 0, device = 0;
   int copy_mode = OLED_COPY_SHADER;
   int adapt_period = 0;    // layer-adaptive sizing after every adapt_period-th iteration (0: off)
+  int policy = OLED_POLICY_PRIORITY;
   int64_t iters_done = 0;  // iterations of the whole stack completed since the last reset
   uint32_t profile_ops = 0;
   int64_t eb = 0;    // bytes of one expert block
@@ -107,7 +108,12 @@ struct Ctx {
   int32_t* d_slot_of = nullptr;    // [L][E]
   ExpertMask* d_res = nullptr;     // [L]
   ExpertMask* d_res_before = nullptr;
-  int32_t* d_last_counts = nullptr;  // [L][4]
+  int32_t* d_last_counts = nullptr;  // [L][kCountsPerLayer]
+  int32_t* d_iters = nullptr;      // [L] iterations of each layer (LRU / LFU history)
+  int32_t* d_last_use = nullptr;   // [L][E]
+  uint64_t* d_freq = nullptr;      // [L][E]
+  ExpertMask* d_prev_miss = nullptr;  // [L]
+  uint64_t* d_key = nullptr;       // [L][E] keys of each layer's last retention
   int32_t* d_free = nullptr;       // [n_slots]
   int32_t* d_cap = nullptr;        // [L] capacity of each layer
   LayerStat* d_stat = nullptr;     // [L] smoothed statistics of the adaptive sizing
@@ -290,6 +296,8 @@ oled_status drain_records(Ctx* c, int until, bool retentions = true) {
     c->acc.n_misses += v.n_misses;
     c->acc.n_transferred += v.n_staged;
     c->acc.h2d_bytes += static_cast<int64_t>(v.n_staged) * c->eb;
+    c->acc.n_prev_transferred += v.prev_xfer;
+    c->acc.n_transfers_reused += v.reused_xfer;
     if (v.bad) {
       c->acc.n_bad_blocks += 1;
       if (v.seq != c->reported_bad_route) c->bad_route_layer = v.layer;
@@ -335,7 +343,8 @@ void free_ctx(Ctx* c) {
                  c->d_dense_counts, c->d_h, c->d_O,
                  c->d_score, c->d_hdr, c->d_slot_of, c->d_res, c->d_res_before,
                  c->d_last_counts, c->d_free, c->d_host_addr, c->d_cap, c->d_stat,
-                 c->d_chunk, c->d_pcount, c->d_sacc, c->d_ssync};
+                 c->d_chunk, c->d_pcount, c->d_sacc, c->d_ssync, c->d_iters, c->d_last_use,
+                 c->d_freq, c->d_prev_miss, c->d_key};
   for (void* p : dev)
     if (p) (void)hipFree(p);
   if (c->h_ring) (void)hipHostFree(c->h_ring);
@@ -366,7 +375,12 @@ oled_status init_cache_state(Ctx* c) {
                        hipMemcpyHostToDevice));
   HIP_TRY(c, hipMemset(c->d_res, 0, sizeof(ExpertMask) * c->L));
   HIP_TRY(c, hipMemset(c->d_res_before, 0, sizeof(ExpertMask) * c->L));
-  HIP_TRY(c, hipMemset(c->d_last_counts, 0, sizeof(int32_t) * 4 * c->L));
+  HIP_TRY(c, hipMemset(c->d_last_counts, 0, sizeof(int32_t) * oled::kCountsPerLayer * c->L));
+  HIP_TRY(c, hipMemset(c->d_iters, 0, sizeof(int32_t) * c->L));
+  HIP_TRY(c, hipMemset(c->d_last_use, 0, sizeof(int32_t) * c->L * c->E));
+  HIP_TRY(c, hipMemset(c->d_freq, 0, sizeof(uint64_t) * c->L * c->E));
+  HIP_TRY(c, hipMemset(c->d_prev_miss, 0, sizeof(ExpertMask) * c->L));
+  HIP_TRY(c, hipMemset(c->d_key, 0, sizeof(uint64_t) * c->L * c->E));
   HIP_TRY(c, hipMemset(c->d_score, 0, sizeof(uint64_t) * c->L * c->E));
   std::vector<int32_t> caps(c->L, c->cap);
   HIP_TRY(c, hipMemcpy(c->d_cap, caps.data(), sizeof(int32_t) * c->L, hipMemcpyHostToDevice));
@@ -393,6 +407,11 @@ CacheView view(const Ctx* c) {
   v.cap = c->d_cap;
   v.stat = c->d_stat;
   v.adapt = c->adapt_period > 0;
+  v.policy = c->policy;
+  v.iters = c->d_iters;
+  v.last_use = c->d_last_use;
+  v.freq = c->d_freq;
+  v.prev_miss = c->d_prev_miss;
   v.n_slots = c->n_slots;
   return v;
 }
@@ -592,6 +611,9 @@ oled_status oled_create(const oled_config* cfg, void** ctx_out) {
   if (cfg->copy_mode != OLED_COPY_SHADER && cfg->copy_mode != OLED_COPY_SDMA)
     return bad(OLED_ERR_INVALID_ARG, "copy_mode must be OLED_COPY_SHADER or OLED_COPY_SDMA");
   if (cfg->adapt_period < 0) return bad(OLED_ERR_INVALID_ARG, "adapt_period < 0");
+  if (cfg->policy != OLED_POLICY_PRIORITY && cfg->policy != OLED_POLICY_LRU &&
+      cfg->policy != OLED_POLICY_LFU)
+    return bad(OLED_ERR_INVALID_ARG, "policy must be OLED_POLICY_PRIORITY, _LRU or _LFU");
   if (cfg->adapt_period > 0 && cfg->n_layers > oled::kMaxAdaptLayers)
     return bad(OLED_ERR_UNSUPPORTED, "adapt_period > 0 needs n_layers <= 1024");
   if (cfg->top_k > cfg->n_experts) return bad(OLED_ERR_INVALID_ARG, "top_k > n_experts");
@@ -638,6 +660,7 @@ oled_status oled_create(const oled_config* cfg, void** ctx_out) {
   c->dtype = cfg->dtype;
   c->copy_mode = cfg->copy_mode;
   c->adapt_period = cfg->adapt_period;
+  c->policy = cfg->policy;
   c->esz = cfg->dtype == OLED_F32 ? 4 : 2;
   c->device = cfg->device;
   c->profile_ops = static_cast<uint32_t>(cfg->profile_ops);
@@ -679,7 +702,10 @@ oled_status oled_create(const oled_config* cfg, void** ctx_out) {
       dev_alloc(&c->d_score, static_cast<size_t>(c->L) * c->E))
     return oom("routing scratch");
   if (dev_alloc(&c->d_hdr, 1) || dev_alloc(&c->d_slot_of, nb) || dev_alloc(&c->d_res, c->L) ||
-      dev_alloc(&c->d_res_before, c->L) || dev_alloc(&c->d_last_counts, 4 * c->L) ||
+      dev_alloc(&c->d_res_before, c->L) ||
+      dev_alloc(&c->d_last_counts, oled::kCountsPerLayer * c->L) ||
+      dev_alloc(&c->d_iters, c->L) || dev_alloc(&c->d_last_use, nb) || dev_alloc(&c->d_freq, nb) ||
+      dev_alloc(&c->d_prev_miss, c->L) || dev_alloc(&c->d_key, nb) ||
       dev_alloc(&c->d_free, c->n_slots) || dev_alloc(&c->d_host_addr, nb) ||
       dev_alloc(&c->d_cap, c->L) || dev_alloc(&c->d_stat, c->L))
     return oom("cache state");
@@ -1148,6 +1174,7 @@ oled_status score_and_retain(void* ctx, int32_t layer, const float* conf_dev, vo
   a.cv = view(c);
   a.score_out = c->d_score + static_cast<size_t>(layer) * c->E;
   a.out = c->d_ret + layer;
+  a.key_out = c->d_key + static_cast<size_t>(layer) * c->E;
   a.parts = oled::score_parts(c->cur_T, c->K);
   a.acc = c->d_sacc;
   a.acc_sync = c->d_ssync;
@@ -1179,7 +1206,7 @@ oled_status score_and_retain(void* ctx, int32_t layer, const float* conf_dev, vo
   if (c->adapt_period > 0 && layer == c->L - 1 && ++c->iters_done % c->adapt_period == 0) {
     oled::AdaptArgs ad;
     ad.cv = view(c);
-    ad.score = c->d_score;
+    ad.score = c->d_key;
     ad.L = c->L;
     ad.E = c->E;
     ad.c_total = c->L * c->cap;
@@ -1215,11 +1242,12 @@ oled_status oled_read_layer_state(void* ctx, int32_t layer, oled_layer_state* ou
     HIP_TRY(c, hipMemcpy(out->score_q, c->d_score + static_cast<size_t>(layer) * c->E, c->E * 8,
                          hipMemcpyDeviceToHost));
   ExpertMask before, after;
-  int32_t lc[4];
+  int32_t lc[oled::kCountsPerLayer];
   std::vector<int32_t> slots(c->E);
   HIP_TRY(c, hipMemcpy(&before, c->d_res_before + layer, sizeof(ExpertMask), hipMemcpyDeviceToHost));
   HIP_TRY(c, hipMemcpy(&after, c->d_res + layer, sizeof(ExpertMask), hipMemcpyDeviceToHost));
-  HIP_TRY(c, hipMemcpy(lc, c->d_last_counts + 4 * layer, sizeof(lc), hipMemcpyDeviceToHost));
+  HIP_TRY(c, hipMemcpy(lc, c->d_last_counts + oled::kCountsPerLayer * layer, sizeof(lc),
+                       hipMemcpyDeviceToHost));
   HIP_TRY(c, hipMemcpy(slots.data(), c->d_slot_of + static_cast<size_t>(layer) * c->E,
                        sizeof(int32_t) * c->E, hipMemcpyDeviceToHost));
   for (int e = 0; e < c->E; ++e) {
@@ -1234,6 +1262,11 @@ oled_status oled_read_layer_state(void* ctx, int32_t layer, oled_layer_state* ou
   HIP_TRY(c, hipMemcpy(&cap_now, c->d_cap + layer, sizeof(int32_t), hipMemcpyDeviceToHost));
   out->capacity = cap_now;
   out->reserved = 0;
+  out->prev_transferred = lc[4];
+  out->reused_transfers = lc[5];
+  if (out->retain_key)
+    HIP_TRY(c, hipMemcpy(out->retain_key, c->d_key + static_cast<size_t>(layer) * c->E, c->E * 8,
+                         hipMemcpyDeviceToHost));
   if (c->stage == Stage::kIdle) {
     st = check_slots(c);
     if (st != OLED_OK) return st;

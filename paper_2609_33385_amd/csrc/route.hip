@@ -287,7 +287,7 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
   __shared__ int32_t s_off[kMaxExperts + 1];
   __shared__ int32_t s_item_base[kMaxExperts];
   __shared__ int32_t s_run[kMaxExperts];
-  __shared__ int32_t s_stat[16];
+  __shared__ int32_t s_stat[18];
   __shared__ int32_t s_dfull[kMaxExperts];   // first full dense item of the expert, or -1
   __shared__ int32_t s_dshort[kMaxExperts];  // its short dense item, or -1
   __shared__ int32_t s_sexp[kMaxExperts];
@@ -321,7 +321,8 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
     int c[4], nh[4], nm[4];
     bool hit[4], miss[4], dn[4];
     int sc = 0, sh = 0, sm = 0, sx = 0, sdf = 0, sds = 0;
-    int n_act = 0, n_hit = 0, n_res = 0, hrows = 0, mrows = 0;
+    int n_act = 0, n_hit = 0, n_res = 0, hrows = 0, mrows = 0, n_px = 0, n_rx = 0;
+    const ExpertMask pmask = o.cv.prev_miss[layer];   // transferred at the previous iteration
     int n_dense = 0, n_dhit = 0, drows = 0, dhrows = 0;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -347,6 +348,9 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
       n_act += c[q] > 0 ? 1 : 0;
       n_hit += hit[q] ? 1 : 0;
       n_res += res ? 1 : 0;
+      const bool pm = e < E && pmask.test(e);
+      n_px += pm ? 1 : 0;
+      n_rx += pm && hit[q] ? 1 : 0;   // retained (resident now) and activated again
       hrows += hit[q] ? c[q] : 0;
       mrows += miss[q] ? c[q] : 0;
     }
@@ -355,6 +359,8 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
     n_act = wave_total(wave_incl_scan(n_act));
     n_hit = wave_total(wave_incl_scan(n_hit));
     n_res = wave_total(wave_incl_scan(n_res));
+    n_px = wave_total(wave_incl_scan(n_px));
+    n_rx = wave_total(wave_incl_scan(n_rx));
     hrows = wave_total(wave_incl_scan(hrows));
     mrows = wave_total(wave_incl_scan(mrows));
     const int tot_hit = wave_total(ih);
@@ -402,16 +408,34 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
       xdf += dn[q] ? c[q] / kDenseRows : 0;
       xds += dn[q] && c[q] % kDenseRows ? 1 : 0;
     }
+    // this iteration's transferred misses, for the next one: expert e = 4 lane + q
+    // is bit 4 (lane % 8) + q of word lane / 8
+    uint64_t mb[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) mb[q] = __ballot(stage && miss[q]);
+    if (lane < kMaxExperts / 32) {
+      uint32_t word = 0u;
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          word |= static_cast<uint32_t>((mb[q] >> (8 * lane + j)) & 1ull) << (4 * j + q);
+      o.cv.prev_miss[layer].bits[lane] = word;
+    }
     if (lane == 0) {
       hdr->free_top = stage ? free_top - n_miss : free_top;
       hdr->staged_n = stage ? n_miss : 0;
       hdr->route_bad = stage ? 0 : 1;
       if (!bad && !stage) hdr->fault |= 1;
-      int32_t* lc = o.cv.last_counts + 4 * layer;
+      int32_t* lc = o.cv.last_counts + kCountsPerLayer * layer;
       lc[0] = n_act;
       lc[1] = n_hit;
       lc[2] = n_miss;
       lc[3] = n_res;
+      lc[4] = n_px;
+      lc[5] = n_rx;
+      s_stat[16] = n_px;
+      s_stat[17] = n_rx;
       s_stat[0] = n_act;
       s_stat[1] = n_hit;
       s_stat[2] = n_miss;
@@ -498,6 +522,8 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
     rs.dense_rows = dense ? s_stat[12] : 0;
     rs.dense_hit_rows = dense ? s_stat[13] : 0;
     rs.n_dense_items = dense ? s_stat[14] + s_stat[15] : 0;
+    rs.prev_xfer = s_stat[16];
+    rs.reused_xfer = s_stat[17];
     rs.seq = o.seq;
     if (tid == 0) {
       o.item_counts[0] = s_stat[8];

@@ -32,7 +32,7 @@ __device__ __forceinline__ bool ranks_above(unsigned long long sa, bool ra, int 
 // weight 1/2 on the newest value (float64; halving is exact, so a fused
 // multiply-add rounds the same as the separate operations).
 __device__ __forceinline__ void observe_layer(const CacheView& cv, int layer, int E, int C) {
-  const int32_t* lc = cv.last_counts + 4 * layer;
+  const int32_t* lc = cv.last_counts + kCountsPerLayer * layer;
   LayerStat st = cv.stat[layer];
   const double a_obs = static_cast<double>(lc[0]) / static_cast<double>(E);
   st.a = st.has_a ? 0.5 * a_obs + 0.5 * st.a : a_obs;
@@ -93,22 +93,48 @@ __device__ __forceinline__ void score_commit(const ScoreArgs& a, unsigned long l
     const bool c = e < E && (r || counts[e] > 0);
     s_rc[e] = (r ? 2u : 0u) | (c ? 1u : 0u);
   }
-  __syncthreads();
   const int s_bad = *p_bad;
+  CacheHdr* hdr = cv.hdr;
+  const bool commit = !s_bad && !hdr->route_bad;
 
-  // Top-C over candidates R u A by (S desc, previously resident first, id
+  // The retention key: S under the paper's priority; under LRU / LFU the
+  // layer's history, advanced by this iteration's routing when it commits
+  // (the iteration of the last activation, or the routes so far).
+  __shared__ unsigned long long s_K[kMaxExperts];
+  const int it_now = cv.iters[layer] + 1;
+  for (int e = tid; e < E; e += kThreads) {
+    if (cv.policy == 0) {
+      s_K[e] = s_S[e];
+      continue;
+    }
+    int32_t* lu = cv.last_use + static_cast<size_t>(layer) * E + e;
+    uint64_t* fr = cv.freq + static_cast<size_t>(layer) * E + e;
+    int32_t u = *lu;
+    uint64_t f = *fr;
+    if (commit && counts[e] > 0) {
+      u = it_now;
+      f += static_cast<uint64_t>(counts[e]);
+      *lu = u;
+      *fr = f;
+    }
+    s_K[e] = cv.policy == 1 ? static_cast<unsigned long long>(u) : f;
+  }
+  __syncthreads();
+  if (tid == 0 && commit && cv.policy != 0) cv.iters[layer] = it_now;
+
+  // Top-C over candidates R u A by (key desc, previously resident first, id
   // asc): rank[e] = number of candidates above e. Thread pairs (e, quarter of
   // the candidates) count with broadcast LDS reads; LDS atomics sum the parts.
   const int fq = (E + 3) >> 2;
   for (int idx = tid; idx < 4 * E; idx += kThreads) {
     const int e = idx % E, part = idx / E;
-    const unsigned long long se = s_S[e];
+    const unsigned long long se = s_K[e];
     const bool re = s_rc[e] & 2u;
     int cnt = 0;
     const int f1 = min(E, (part + 1) * fq);
     for (int f = part * fq; f < f1; ++f) {
       const uint32_t rcf = s_rc[f];
-      cnt += ((rcf & 1u) && ranks_above(s_S[f], rcf & 2u, f, se, re, e)) ? 1 : 0;
+      cnt += ((rcf & 1u) && ranks_above(s_K[f], rcf & 2u, f, se, re, e)) ? 1 : 0;
     }
     atomicAdd(&s_rank[e], cnt);
   }
@@ -120,8 +146,6 @@ __device__ __forceinline__ void score_commit(const ScoreArgs& a, unsigned long l
   // slot no longer held returns to the free list, in expert order.
   const int lane = tid;
   constexpr int Q = kMaxExperts / 64;
-  CacheHdr* hdr = cv.hdr;
-  const bool commit = !s_bad && !hdr->route_bad;
   int32_t* slot_row = cv.slot_of + static_cast<size_t>(layer) * E;
   int top = hdr->free_top;
   int fault = 0;
@@ -139,7 +163,10 @@ __device__ __forceinline__ void score_commit(const ScoreArgs& a, unsigned long l
       fault |= 4;
       keep = false;
     }
-    if (e < E) score_out[e] = s_S[e];
+    if (e < E) {
+      score_out[e] = s_S[e];
+      a.key_out[e] = s_K[e];
+    }
     const bool release = sl >= 0 && !keep;
     const uint64_t rel = __ballot(release);
     const int pos = top + __popcll(rel & ((1ull << lane) - 1ull));

@@ -28,14 +28,14 @@ def fill_pool(w: W.Workload, seed: int, n_blocks: int) -> oled.PinnedPool:
 def make_context(w: W.Workload, pool: oled.PinnedPool, capacity: int | None = None,
                  n_layers: int | None = None, max_tokens: int | None = None,
                  profile_ops: int = 0, copy_mode: str = "shader",
-                 adapt_period: int = 0) -> oled.Context:
+                 adapt_period: int = 0, policy: str = "priority") -> oled.Context:
     L = n_layers if n_layers is not None else w.n_layers
     return oled.Context(w.hidden, w.inter, w.n_experts, w.top_k, L,
                         w.capacity if capacity is None else capacity,
                         max_tokens if max_tokens is not None else w.tokens, w.dtype,
                         pool.ptr, pool.n_blocks,
                         W.host_block_of(w.replace(n_layers=L), pool.n_blocks), profile_ops=profile_ops,
-                        copy_mode=copy_mode, adapt_period=adapt_period)
+                        copy_mode=copy_mode, adapt_period=adapt_period, policy=policy)
 
 
 def torch_dtype(w: W.Workload):

@@ -32,6 +32,7 @@ OLED_BF16 = 1
 OLED_COPY_SHADER = 0
 OLED_COPY_SDMA = 1
 COPY_MODES = {"shader": OLED_COPY_SHADER, "sdma": OLED_COPY_SDMA}
+POLICIES = {"priority": 0, "lru": 1, "lfu": 2}
 PROFILE_ALL = 0x3FF
 
 OP_NAMES = {0: "route_topk", 1: "permute", 2: "ffn_up", 3: "ffn_down", 4: "combine",
@@ -61,7 +62,8 @@ class OledConfig(ctypes.Structure):
                 ("device", ctypes.c_int32), ("profile_ops", ctypes.c_int32),
                 ("host_pool", ctypes.c_void_p), ("host_pool_blocks", ctypes.c_int64),
                 ("host_block_of", ctypes.POINTER(ctypes.c_int64)),
-                ("copy_mode", ctypes.c_int32), ("adapt_period", ctypes.c_int32)]
+                ("copy_mode", ctypes.c_int32), ("adapt_period", ctypes.c_int32),
+                ("policy", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class MissReport(ctypes.Structure):
@@ -75,7 +77,8 @@ class Stats(ctypes.Structure):
     _fields_ = [("layer_iters", ctypes.c_int64), ("n_active", ctypes.c_int64),
                 ("n_hits", ctypes.c_int64), ("n_misses", ctypes.c_int64),
                 ("n_transferred", ctypes.c_int64), ("h2d_bytes", ctypes.c_int64),
-                ("n_bad_blocks", ctypes.c_int64)]
+                ("n_bad_blocks", ctypes.c_int64), ("n_prev_transferred", ctypes.c_int64),
+                ("n_transfers_reused", ctypes.c_int64)]
 
     def as_dict(self) -> dict:
         return {name: getattr(self, name) for name, _ in self._fields_}
@@ -89,7 +92,9 @@ class LayerState(ctypes.Structure):
                 ("resident_after", ctypes.c_void_p), ("slot_of", ctypes.c_void_p),
                 ("tokens", ctypes.c_int32), ("n_active", ctypes.c_int32),
                 ("n_hits", ctypes.c_int32), ("n_misses", ctypes.c_int32),
-                ("capacity", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("capacity", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("retain_key", ctypes.c_void_p), ("prev_transferred", ctypes.c_int32),
+                ("reused_transfers", ctypes.c_int32)]
 
 
 class OpTime(ctypes.Structure):
@@ -282,13 +287,13 @@ class Context:
     def __init__(self, hidden, inter, n_experts, top_k, n_layers, capacity, max_tokens,
                  dtype: str, host_pool: int, host_pool_blocks: int, host_block_of,
                  device: int = 0, profile_ops: int = 0, copy_mode: str = "shader",
-                 adapt_period: int = 0):
+                 adapt_period: int = 0, policy: str = "priority"):
         self._hbo = np.ascontiguousarray(host_block_of, dtype=np.int64)
         cfg = OledConfig(hidden, inter, n_experts, top_k, n_layers, capacity, max_tokens,
                          OLED_F32 if dtype == "f32" else OLED_BF16, device,
                          profile_ops, host_pool, host_pool_blocks,
                          self._hbo.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
-                         COPY_MODES[copy_mode], adapt_period)
+                         COPY_MODES[copy_mode], adapt_period, POLICIES[policy], 0)
         self.E, self.k, self.L, self.C, self.Tmax = n_experts, top_k, n_layers, capacity, max_tokens
         self.ctx = oled_create(cfg)
 
@@ -329,7 +334,9 @@ class Context:
                    perm=np.zeros(R, np.int32), inv_perm=np.zeros(R, np.int32),
                    score_q=np.zeros(E, np.uint64), resident_before=np.zeros(E, np.uint8),
                    resident_after=np.zeros(E, np.uint8), slot_of=np.zeros(E, np.int32))
-        st = LayerState(*[a.ctypes.data for a in out.values()], 0, 0, 0, 0, 0, 0)
+        rkey = np.zeros(E, np.uint64)
+        st = LayerState(*[a.ctypes.data for a in out.values()], 0, 0, 0, 0, 0, 0,
+                        rkey.ctypes.data, 0, 0)
         status = oled_read_layer_state(self.ctx, layer, st)
         if status not in (OLED_OK, OLED_ERR_INVALID_ARG):
             _check(self.ctx, status)
@@ -339,7 +346,9 @@ class Context:
         out["topk_idx"] = out["topk_idx"].reshape(Tn, k)
         out["gates"] = out["gates"].reshape(Tn, k)
         out.update(tokens=Tn, n_active=st.n_active, n_hits=st.n_hits, n_misses=st.n_misses,
-                   capacity=st.capacity, rejected=(status == OLED_ERR_INVALID_ARG))
+                   capacity=st.capacity, retain_key=rkey, prev_transferred=st.prev_transferred,
+                   reused_transfers=st.reused_transfers,
+                   rejected=(status == OLED_ERR_INVALID_ARG))
         out["resident_before"] = out["resident_before"].astype(bool)
         out["resident_after"] = out["resident_after"].astype(bool)
         return out

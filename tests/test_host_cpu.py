@@ -51,7 +51,7 @@ def _cfg(**kw):
                         base["n_layers"], base["capacity"], base["max_tokens"], base["dtype"],
                         base["device"], base["profile_ops"], base["host_pool"] or 0,
                         base["host_pool_blocks"],
-                        hbo.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), 0, 0)
+                        hbo.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), 0, 0, 0, 0)
     return c, hbo
 
 
@@ -179,3 +179,12 @@ def test_create_rejects_bad_adapt_period():
     cfg.adapt_period = 5
     assert lib.oled_create(ctypes.byref(cfg), ctypes.byref(h)) == oled.OLED_ERR_UNSUPPORTED
     assert h.value is None
+
+
+def test_create_rejects_bad_policy():
+    lib = oled.load()
+    h = ctypes.c_void_p()
+    cfg, _hbo = _cfg(host_pool=1, host_pool_blocks=1)
+    cfg.policy = 3
+    assert lib.oled_create(ctypes.byref(cfg), ctypes.byref(h)) == oled.OLED_ERR_INVALID_ARG
+    assert b"policy" in lib.oled_last_error(None)
