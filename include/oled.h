@@ -154,6 +154,8 @@ typedef struct {
                                   iteration (the effective transfer ratio's denominator) */
   int64_t n_transfers_reused;  /* of those, retained and activated again (its numerator,
                                   Sec. 5.3) */
+  int64_t n_ideal_hits;   /* sum of min(C_l, |A|): hits of the clairvoyant ideal cache
+                             bound (Sec. 5.1) */
 } oled_stats;
 
 /*

@@ -85,6 +85,7 @@ struct RouteStats {
   int32_t n_dense_items;
   int32_t prev_xfer;   // experts transferred at the layer's previous iteration
   int32_t reused_xfer; // of them retained and activated now
+  int32_t ideal_hits;  // the clairvoyant bound min(C_l, |A|)
   int32_t seq;
 };
 

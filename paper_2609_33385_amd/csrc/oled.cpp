@@ -298,6 +298,7 @@ oled_status drain_records(Ctx* c, int until, bool retentions = true) {
     c->acc.h2d_bytes += static_cast<int64_t>(v.n_staged) * c->eb;
     c->acc.n_prev_transferred += v.prev_xfer;
     c->acc.n_transfers_reused += v.reused_xfer;
+    c->acc.n_ideal_hits += v.ideal_hits;
     if (v.bad) {
       c->acc.n_bad_blocks += 1;
       if (v.seq != c->reported_bad_route) c->bad_route_layer = v.layer;

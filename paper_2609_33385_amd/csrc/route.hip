@@ -524,6 +524,7 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
     rs.n_dense_items = dense ? s_stat[14] + s_stat[15] : 0;
     rs.prev_xfer = s_stat[16];
     rs.reused_xfer = s_stat[17];
+    rs.ideal_hits = min(o.cv.cap[layer], s_stat[0]);
     rs.seq = o.seq;
     if (tid == 0) {
       o.item_counts[0] = s_stat[8];

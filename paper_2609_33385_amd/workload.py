@@ -56,6 +56,7 @@ class Workload:
     zipf_s: float = 0.0   # >0: per-layer Zipf(s) popularity bias on logits
     conf_kind: str = "unmask"   # "beta22" | "uniform" | "unmask"
     sigma_s_layers: tuple = ()  # non-empty: sigma_s of layer l is sigma_s_layers[l % len]
+    conf_informed: bool = False # steps of token t scaled by 2 (1 - its previous confidence)
 
     @property
     def tokens(self) -> int:
@@ -131,9 +132,12 @@ def logits_block(w: Workload, seed: int, layer: int, blk: int) -> np.ndarray:
     """Router logits of one layer for every iteration of one block: float32 [N][T][E].
 
     Iteration 0 is sigma_s * z[seq] + n + bias (sigma_s per layer if
-    sigma_s_layers is set: layers that route with different spread); each later iteration adds an
-    independent N(0, sigma_it^2) step (a random walk, so adjacent iterations
-    route mostly to the same experts).
+    sigma_s_layers is set: layers that route with different spread); each later
+    iteration adds an independent N(0, sigma_it^2) step (a random walk, so
+    adjacent iterations route mostly to the same experts). With conf_informed
+    the step of token t at iteration i is scaled by 2 (1 - c_t^{i-1}), so the
+    routes of confident tokens persist, as the paper observes of real
+    denoising (Sec. 4.3).
     """
     T, E, N = w.tokens, w.n_experts, w.n_iters
     z = _rng(w, seed, _TID_PREF, layer).standard_normal((w.batch, E))
@@ -142,6 +146,10 @@ def logits_block(w: Workload, seed: int, layer: int, blk: int) -> np.ndarray:
     base = sig * np.repeat(z, w.block, axis=0) + n + _layer_bias(w, seed, layer)
     steps = _rng(w, seed, _TID_STEP, layer, blk).standard_normal((N, T, E))
     steps[0] = 0.0
+    if w.conf_informed:   # confident tokens move less: their routes persist (Sec. 4.3)
+        for i in range(1, N):
+            c = confidence(w, seed, blk, i - 1).astype(np.float64)
+            steps[i] *= 2.0 * (1.0 - c)[:, None]
     walk = np.cumsum(w.sigma_it * steps, axis=0)
     return (base[None] + walk).astype(np.float32)
 

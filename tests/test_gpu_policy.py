@@ -72,6 +72,8 @@ def _chain(w, seed, C, policy, period=0, forward=False, outs=None):
     flat = [o for row in ref for o in row]
     assert stats["n_prev_transferred"] == sum(o["prev_transferred"] for o in flat)
     assert stats["n_transfers_reused"] == sum(o["reused_transfers"] for o in flat)
+    if period == 0:
+        assert stats["n_ideal_hits"] == sum(O.ideal_hits(o["n_active"], C) for o in flat)
     _say(f"[policy] ok: hits {sum(o['n_hits'] for o in flat)}, effective transfer ratio "
          f"{O.effective_transfer_ratio(ref):.3f}")
 
