@@ -22,6 +22,10 @@ float64 from the exact input bits:
   O11 policies  the comparison retention policies of Sec. 5.1 / 5.3 (LRU,
                 LFU) in place of the priority, the clairvoyant ideal cache
                 bound, and the effective transfer ratio (Sec. 5.3)
+  O12 coop      cooperative compensation (Sec. 4.4): the hardware-aware
+                split rho, and the two-stage load- and reuse-aware dispatch of
+                the misses into transfers G and CPU executions M \ G; only G
+                joins the retention candidates
   O10 adapt     layer-adaptive cache sizing (Sec. 4.3): smoothed activation
                 ratio a_l and cache utilisation u_l per layer, layer weight
                 w_l = a_l * u_l and capacity C_l = C_total * w_l / sum_j w_j,
@@ -56,6 +60,23 @@ define:
   * effective transfer ratio: of the experts transferred at a layer's
     iteration i, the share retained and activated again at its iteration
     i + 1, summed over iterations that have a next one.
+Readings of the cooperative compensation (O12), where the paper names the
+objective J(G) = T_comp - lambda * sum_{e in G} p_e and a two-stage heuristic
+but not the cost model or the bounds:
+  * T_comp(G) = max(T_H2D * |G|, tau_CPU * sum_{e in M \ G} n_e): the transfer
+    path and the CPU path run in parallel (n_e = routed tokens of e); the GPU
+    compute of transferred experts is left out;
+  * rho = nbar tau_CPU / (nbar tau_CPU + T_H2D); stage 1 transfers the
+    round_half_up(rho |M|) misses of highest priority (S desc, id asc);
+  * stage 2: at most |M| swaps of one transferred and one CPU expert, each the
+    best swap by J (first in (transferred id, CPU id) order among equals),
+    taken only if it lowers J strictly; swaps keep |G| at the hardware-aware
+    split;
+  * sum_{e in G} p_e = (sum_{e in G} S_e) / (sum_e S_e) (0 if no mass), and
+    every term in float64 in the order written; lambda is an input (time per
+    unit of priority mass);
+  * only G joins the retention candidates R u G; CPU-executed experts leave
+    no trace in the cache.
 Readings of the layer-adaptive sizing (O10), where the paper gives the
 formulas but not the smoothing, the rounding or the enforcement:
   * smoothing: an exponential moving average with weight 1/2 on the newest
@@ -357,6 +378,111 @@ def effective_transfer_ratio(steps) -> float:
     moved = sum(st["prev_transferred"] for row in steps for st in row)
     reused = sum(st["reused_transfers"] for row in steps for st in row)
     return reused / moved if moved else 0.0
+
+
+# ------------------------------------------- O12 cooperative compensation
+def coop_rho(t_h2d: float, tau_cpu: float, nbar: float) -> float:
+    """Hardware-aware baseline share of misses to transfer (Sec. 4.4):
+    rho = nbar tau_CPU / (nbar tau_CPU + T_H2D)."""
+    cpu = nbar * tau_cpu
+    den = cpu + t_h2d
+    return cpu / den if den > 0.0 else 1.0
+
+
+def coop_objective(G, misses, n_tok, S, S_total, t_h2d, tau_cpu, lam) -> float:
+    """J(G) = T_comp(G) - lambda * sum_{e in G} p_e (Sec. 4.4), with
+    T_comp = max(T_H2D |G|, tau_CPU * tokens left to the CPU)."""
+    cpu_tokens = 0
+    for e in misses:
+        if e not in G:
+            cpu_tokens += int(n_tok[e])
+    t_comp = max(t_h2d * float(len(G)), tau_cpu * float(cpu_tokens))
+    mass = 0
+    for e in G:
+        mass += int(S[e])
+    share = float(mass) / float(S_total) if S_total > 0 else 0.0
+    return t_comp - lam * share
+
+
+def coop_dispatch(miss, n_tok, S, t_h2d: float, tau_cpu: float, nbar: float, lam: float):
+    """O12. Which misses to transfer (Sec. 4.4). miss: bool [E]; n_tok: routed
+    tokens per expert; S: priority numerators of every expert of the layer.
+    Stage 1 takes the round_half_up(rho |M|) misses of highest priority;
+    stage 2 makes bounded swaps that lower J. Returns the transfer mask G."""
+    E = len(miss)
+    misses = [e for e in range(E) if miss[e]]
+    S_total = 0
+    for e in range(E):
+        S_total += int(S[e])
+    rho = coop_rho(t_h2d, tau_cpu, nbar)
+    n_g = int(math.floor(rho * float(len(misses)) + 0.5))
+    by_priority = sorted(misses, key=lambda e: (-int(S[e]), e))
+    G = set(by_priority[:n_g])
+    J = coop_objective(G, misses, n_tok, S, S_total, t_h2d, tau_cpu, lam)
+    for _ in range(len(misses)):
+        best = None
+        for g in sorted(G):
+            for c in misses:
+                if c in G:
+                    continue
+                Gs = (G - {g}) | {c}
+                j = coop_objective(Gs, misses, n_tok, S, S_total, t_h2d, tau_cpu, lam)
+                if best is None or j < best[0]:
+                    best = (j, Gs)
+        if best is None or not best[0] < J:
+            break
+        J, G = best
+    out = np.zeros(E, dtype=bool)
+    for e in G:
+        out[e] = True
+    return out
+
+
+def coop_layer_step(logits, conf, resident, top_k: int, capacity: int, t_h2d: float,
+                    tau_cpu: float, nbar: float, lam: float):
+    """O1-O3, O6, O12, O8 for one layer-iteration with cooperative
+    compensation: the misses are split into transfers G and CPU executions;
+    the retention keeps Top_C of R u G. Returns the layer_step dict plus
+    `transfer` (G) and `cpu` (M \ G) masks."""
+    E = logits.shape[1]
+    idx, gates = route(logits, top_k)
+    counts, offsets, perm, inv_perm = permute(idx, E)
+    active, hit, miss = classify(counts, resident)
+    S, p = score(idx, gates, conf, E)
+    G = coop_dispatch(miss, counts, S, t_h2d, tau_cpu, nbar, lam)
+    new_res = retain(S, resident, G, capacity)
+    n_hits = int(hit.sum())
+    return dict(idx=idx, gates=gates, counts=counts, offsets=offsets, perm=perm,
+                inv_perm=inv_perm, active=active, hit=hit, miss=miss,
+                n_active=int(active.sum()), n_hits=n_hits, n_misses=int(miss.sum()),
+                util=(n_hits / capacity if capacity > 0 else 0.0), S=S, p=p,
+                key=np.asarray(S, dtype=np.uint64),
+                resident_before=np.asarray(resident, dtype=bool).copy(), resident_after=new_res,
+                transfer=G, cpu=miss & ~G)
+
+
+def run_coop_schedule(logits_fn, conf_fn, n_layers: int, n_iters: int, n_experts: int,
+                      top_k: int, capacity: int, t_h2d: float, tau_cpu: float, nbar: float,
+                      lam: float):
+    """O9 with cooperative compensation (O12): steps[i][l]. Each dict also
+    holds prev_transferred / reused_transfers over the transferred experts."""
+    res = [np.zeros(n_experts, dtype=bool) for _ in range(n_layers)]
+    prev = [np.zeros(n_experts, dtype=bool) for _ in range(n_layers)]
+    cap = min(capacity, n_experts)
+    steps = []
+    for i in range(n_iters):
+        row = []
+        for l in range(n_layers):
+            st = coop_layer_step(logits_fn(l, i), conf_fn(l, i), res[l], top_k, cap, t_h2d,
+                                 tau_cpu, nbar, lam)
+            st["capacity"] = cap
+            st["prev_transferred"] = int(prev[l].sum())
+            st["reused_transfers"] = int((st["active"] & st["resident_before"] & prev[l]).sum())
+            prev[l] = st["transfer"].copy()
+            res[l] = st["resident_after"]
+            row.append(st)
+        steps.append(row)
+    return steps
 
 
 # ------------------------------------------------- O10 layer-adaptive sizing
