@@ -126,7 +126,16 @@ typedef struct {
                                iteration of the layer stack (the paper uses 5); see
                                score_and_retain. Needs n_layers <= 1024. */
   int32_t policy;           /* oled_policy */
+  int32_t coop;             /* 1: cooperative compensation (Sec. 4.4): misses are split
+                               between transfer and CPU execution by apply_misses_coop.
+                               Needs OLED_COPY_SHADER. */
+  int32_t coop_threads;     /* host threads of the CPU expert execution (>= 1 with coop) */
   int32_t reserved;
+  double coop_t_h2d_us;     /* T_H2D: transfer time of one expert (profiled, microseconds) */
+  double coop_tau_cpu_us;   /* tau_CPU: CPU time of one expert for one token (microseconds) */
+  double coop_nbar;         /* nbar: average routed tokens per missed expert (profiled) */
+  double coop_lambda_us;    /* lambda: weight of the transferred priority mass in J, in
+                               microseconds per unit of priority (p summed over G) */
 } oled_config;
 
 /* Result of apply_misses for the layer (Sec. 4.2). Counts are experts. */
@@ -137,7 +146,7 @@ typedef struct {
   int32_t n_resident;     /* |R| before execution */
   int32_t rejected_layer; /* a layer whose last retention was rejected for an
                              invalid confidence since the previous report, else -1 */
-  int32_t reserved;
+  int32_t n_cpu;          /* misses executed on the CPU (apply_misses_coop), else 0 */
   int64_t h2d_bytes;      /* bytes transferred host->device for the misses */
 } oled_miss_report;
 
@@ -156,6 +165,7 @@ typedef struct {
                                   Sec. 5.3) */
   int64_t n_ideal_hits;   /* sum of min(C_l, |A|): hits of the clairvoyant ideal cache
                              bound (Sec. 5.1) */
+  int64_t n_cpu_executed; /* misses executed on the CPU (apply_misses_coop) */
 } oled_stats;
 
 /*
@@ -331,6 +341,59 @@ oled_status apply_misses(void* ctx, int32_t layer, void* copy_stream, oled_miss_
  *  experts; a layer that grew fills its room at its next retentions.
  */
 oled_status score_and_retain(void* ctx, int32_t layer, const float* conf_dev, void* stream);
+
+/*
+ * apply_misses_coop: cooperative compensation of the routed layer's misses
+ *  (Sec. 4.4), in place of apply_misses on a context created with coop = 1.
+ *  Waits for route_block's result and copies the layer's routing, conf_dev
+ *  (float [T], the same confidence score_and_retain gets) and, after
+ *  moe_forward_cached, x to pinned host memory. Then:
+ *   - priorities S_e as in score_and_retain (exact integers);
+ *   - the hardware-aware split rho = nbar tau / (nbar tau + T_H2D) and the
+ *     two-stage dispatch of oled_coop_dispatch: the transfer set G;
+ *   - the staging slots of the CPU experts M \ G return to the free list
+ *     (one launch); G is transferred as in OLED_COPY_SHADER and computed on
+ *     the GPU with the hits (the launches moe_forward_cached deferred);
+ *   - the CPU experts run on coop_threads host threads from the pinned pool
+ *     (oled_cpu_ffn's kernels); their output rows are copied into the
+ *     layer's per-route outputs before the combine. The call returns once
+ *     they are copied in (stream order).
+ *  score_and_retain then keeps Top_C of R u G: CPU-executed experts never
+ *  enter the cache. out (may be NULL) reports the layer's counts; its
+ *  h2d_bytes are G's.
+ *  Errors: STATE (not in flight, or not a coop context), INVALID_ARG (NULL
+ *  conf, or a bad block as in apply_misses), HIP.
+ */
+oled_status apply_misses_coop(void* ctx, int32_t layer, const float* conf_dev,
+                              oled_miss_report* out);
+
+/*
+ * oled_coop_dispatch: the dispatch of Sec. 4.4 on host arrays (the same code
+ *  apply_misses_coop runs). miss [E] (nonzero: a miss), n_tok [E] routed
+ *  tokens, score [E] priority numerators of every expert of the layer.
+ *  rho = nbar tau / (nbar tau + T_H2D) (1 if that is 0/0); stage 1 marks the
+ *  round_half_up(rho |M|) misses of highest (score desc, id asc); stage 2
+ *  makes at most |M| swaps of a transferred and a CPU expert, each the best
+ *  by J(G) = max(T_H2D |G|, tau * CPU tokens) - lambda * (sum_G S / sum S)
+ *  (first in (transferred id, CPU id) order among equals) and only if it
+ *  lowers J. float64, in that order of operations. transfer_out [E]: 1 for G.
+ *  Errors: INVALID_ARG (NULL pointers, E outside [1, 256], negative times).
+ */
+oled_status oled_coop_dispatch(int32_t n_experts, const uint8_t* miss, const int32_t* n_tok,
+                               const uint64_t* score, double t_h2d_us, double tau_cpu_us,
+                               double nbar, double lambda_us, uint8_t* transfer_out);
+
+/*
+ * oled_cpu_ffn: one expert's SwiGLU on the host CPU (the kernels of the
+ *  cooperative compensation). block: packed expert block (oled_pack_expert
+ *  layout, dtype); x: [n][H] token rows in dtype; out: [n][H] fp32.
+ *  Accumulates in fp32; silu(W1 x) * (W3 x) is rounded to dtype as the GPU
+ *  stores it. threads >= 1 host threads. Needs AVX2 and FMA.
+ *  Errors: INVALID_ARG (NULL pointers, n < 0, threads < 1, bad dtype),
+ *  UNSUPPORTED (shape, or the CPU lacks AVX2/FMA).
+ */
+oled_status oled_cpu_ffn(int32_t dtype, int32_t hidden, int32_t inter, const void* block,
+                         const void* x, int32_t n, float* out, int32_t threads);
 
 /* Inspection (synchronises; see oled_layer_state). With no layer in flight it
  * also checks slot conservation over the whole device cache state (every

@@ -24,7 +24,7 @@ HIPCC = os.path.join(ROCM, "bin", "hipcc")
 ARCH = "gfx950"
 
 HIP_SOURCES = ["route.hip", "ffn.hip", "score.hip"]
-HOST_SOURCES = ["oled.cpp"]
+HOST_SOURCES = ["oled.cpp", "cpu_ffn.cpp"]
 
 HIP_FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
              # keep hand-written and compiler-generated fp32 code off packed-fp32 ops
@@ -32,6 +32,10 @@ HIP_FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
              f"-I{INCLUDE}", f"-I{CSRC}"]
 HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-D__HIP_PLATFORM_AMD__",
               f"-I{ROCM}/include", f"-I{INCLUDE}", f"-I{CSRC}"]
+# per-file host flags: the runtime takes float64 decisions that must round
+# exactly as written (no contraction); the CPU expert kernels are vectorised
+# (their AVX2/FMA functions are selected at run time)
+FILE_FLAGS = {"oled.cpp": ["-ffp-contract=off"], "cpu_ffn.cpp": ["-O3", "-ffp-contract=fast"]}
 
 
 def _run(cmd):
@@ -47,7 +51,7 @@ def _compile(src: str) -> str:
     if src.endswith(".hip"):
         _run([HIPCC, *HIP_FLAGS, "-c", path, "-o", obj])
     else:
-        _run(["g++", *HOST_FLAGS, "-c", path, "-o", obj])
+        _run(["g++", *HOST_FLAGS, *FILE_FLAGS.get(src, []), "-c", path, "-o", obj])
     return obj
 
 
@@ -60,7 +64,7 @@ def build(verbose: bool = False) -> str:
     with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
         objs = list(ex.map(_compile, srcs))
     tmp = LIB + ".tmp"
-    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp])
+    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-lpthread", "-o", tmp])
     os.replace(tmp, LIB)
     if verbose:
         print("built", LIB)

@@ -1,0 +1,293 @@
+// Host CPU execution of missed experts (OLED-MoE Sec. 4.4): the SwiGLU
+// expert FFN on a few token rows, read straight from the packed expert block
+// in the pinned host pool, so a CPU-executed miss moves no weights over PCIe.
+//
+// The packed block holds fragments of 16 weight rows x SPAN columns (SPAN =
+// 32 for bf16, 16 for fp32) with element l*V + i (V = SPAN/4) at row 16q +
+// l%16, column SPAN*s + V*(l/16) + i. A 16-row feature block is therefore a
+// run of fragments over s; every lane's V contiguous weights meet V
+// contiguous inputs: each weight row accumulates, for a few tokens at a
+// time, V-wide vector multiply-adds in registers over its pieces, summed
+// across the vector at the end. fp32 accumulation; the intermediate
+// silu(W1 x) * (W3 x) is rounded to the layer dtype as the GPU kernels store
+// it.
+#include "cpu_ffn.h"
+
+#include <immintrin.h>
+
+#include <atomic>
+#include <cmath>
+#include <cstring>
+
+namespace oled {
+
+ThreadPool::ThreadPool(int n_threads) : n_(n_threads < 1 ? 1 : n_threads) {
+  for (int t = 1; t < n_; ++t) workers_.emplace_back(&ThreadPool::worker, this, t);
+}
+
+ThreadPool::~ThreadPool() {
+  {
+    std::lock_guard<std::mutex> lk(m_);
+    stop_ = true;
+  }
+  wake_.notify_all();
+  for (auto& w : workers_) w.join();
+}
+
+void ThreadPool::worker(int tid) {
+  uint64_t seen = 0;
+  for (;;) {
+    const std::function<void(int)>* fn;
+    {
+      std::unique_lock<std::mutex> lk(m_);
+      wake_.wait(lk, [&] { return stop_ || gen_ != seen; });
+      if (stop_) return;
+      seen = gen_;
+      fn = fn_;
+    }
+    (*fn)(tid);
+    {
+      std::lock_guard<std::mutex> lk(m_);
+      if (--pending_ == 0) done_.notify_one();
+    }
+  }
+}
+
+void ThreadPool::run(const std::function<void(int)>& fn) {
+  if (n_ == 1) {
+    fn(0);
+    return;
+  }
+  {
+    std::lock_guard<std::mutex> lk(m_);
+    fn_ = &fn;
+    pending_ = n_ - 1;
+    ++gen_;
+  }
+  wake_.notify_all();
+  fn(0);
+  std::unique_lock<std::mutex> lk(m_);
+  done_.wait(lk, [&] { return pending_ == 0; });
+  fn_ = nullptr;
+}
+
+bool cpu_ffn_supported() {
+  return __builtin_cpu_supports("avx2") && __builtin_cpu_supports("fma");
+}
+
+namespace {
+
+inline float bf16_to_f32(uint16_t b) {
+  const uint32_t u = static_cast<uint32_t>(b) << 16;
+  float f;
+  std::memcpy(&f, &u, 4);
+  return f;
+}
+
+inline float round_bf16(float f) {
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  u = (u + 0x7FFFu + ((u >> 16) & 1u)) & 0xFFFF0000u;
+  float r;
+  std::memcpy(&r, &u, 4);
+  return r;
+}
+
+// Dot products of one weight row r of a 16-row block with NT token rows:
+// out1[t] (and out3[t] for the second matrix of a gate/up step) = sum over
+// the fragments s of the row's SPAN columns times the token's. The row's
+// V-element pieces sit at lanes r + 16 g, g < 4, of each fragment; every piece
+// meets V contiguous inputs in one vector multiply-add per token.
+__attribute__((target("avx2,fma"))) inline __m256 load_w8(const uint16_t* p) {
+  const __m256i w = _mm256_cvtepu16_epi32(_mm_loadu_si128(reinterpret_cast<const __m128i*>(p)));
+  return _mm256_castsi256_ps(_mm256_slli_epi32(w, 16));
+}
+
+__attribute__((target("avx2,fma"))) inline float hsum8(__m256 v) {
+  const __m128 s = _mm_add_ps(_mm256_castps256_ps128(v), _mm256_extractf128_ps(v, 1));
+  const __m128 t = _mm_add_ps(s, _mm_movehl_ps(s, s));
+  return _mm_cvtss_f32(_mm_add_ss(t, _mm_shuffle_ps(t, t, 1)));
+}
+
+__attribute__((target("avx2,fma"))) inline float hsum4(__m128 s) {
+  const __m128 t = _mm_add_ps(s, _mm_movehl_ps(s, s));
+  return _mm_cvtss_f32(_mm_add_ss(t, _mm_shuffle_ps(t, t, 1)));
+}
+
+template <int NT, int NM>
+__attribute__((target("avx2,fma"))) void row_bf16(const uint16_t* blk, size_t first, size_t step,
+                                                  int steps, const float* xs, int K, int nt, int r,
+                                                  float* out1, float* out3) {
+  __m256 a1[NT], a3[NT];
+  for (int t = 0; t < NT; ++t) a1[t] = a3[t] = _mm256_setzero_ps();
+  for (int s = 0; s < steps; ++s) {
+    const uint16_t* f = blk + first + static_cast<size_t>(s) * step;
+    for (int g = 0; g < 4; ++g) {
+      const int l = r + 16 * g;
+      const __m256 w1 = load_w8(f + l * 8);
+      const __m256 w3 = NM == 2 ? load_w8(f + 512 + l * 8) : _mm256_setzero_ps();
+      const float* xc = xs + 32 * s + 8 * g;
+#pragma GCC unroll 12
+      for (int t = 0; t < NT; ++t) {
+        if (t < nt) {
+          const __m256 x8 = _mm256_loadu_ps(xc + static_cast<size_t>(t) * K);
+          a1[t] = _mm256_fmadd_ps(w1, x8, a1[t]);
+          if (NM == 2) a3[t] = _mm256_fmadd_ps(w3, x8, a3[t]);
+        }
+      }
+    }
+  }
+  for (int t = 0; t < nt; ++t) {
+    out1[t] = hsum8(a1[t]);
+    if (NM == 2) out3[t] = hsum8(a3[t]);
+  }
+}
+
+template <int NT, int NM>
+__attribute__((target("avx2,fma"))) void row_f32(const float* blk, size_t first, size_t step,
+                                                 int steps, const float* xs, int K, int nt, int r,
+                                                 float* out1, float* out3) {
+  __m128 a1[NT], a3[NT];
+  for (int t = 0; t < NT; ++t) a1[t] = a3[t] = _mm_setzero_ps();
+  for (int s = 0; s < steps; ++s) {
+    const float* f = blk + first + static_cast<size_t>(s) * step;
+    for (int g = 0; g < 4; ++g) {
+      const int l = r + 16 * g;
+      const __m128 w1 = _mm_loadu_ps(f + l * 4);
+      const __m128 w3 = NM == 2 ? _mm_loadu_ps(f + 256 + l * 4) : _mm_setzero_ps();
+      const float* xc = xs + 16 * s + 4 * g;
+#pragma GCC unroll 12
+      for (int t = 0; t < NT; ++t) {
+        if (t < nt) {
+          const __m128 x4 = _mm_loadu_ps(xc + static_cast<size_t>(t) * K);
+          a1[t] = _mm_fmadd_ps(w1, x4, a1[t]);
+          if (NM == 2) a3[t] = _mm_fmadd_ps(w3, x4, a3[t]);
+        }
+      }
+    }
+  }
+  for (int t = 0; t < nt; ++t) {
+    out1[t] = hsum4(a1[t]);
+    if (NM == 2) out3[t] = hsum4(a3[t]);
+  }
+}
+
+// All 16 rows of a block for n tokens, NT tokens at a time (accumulators in
+// registers: 6 per matrix for gate/up, 12 for down).
+template <bool BF16, int NM>
+void block_rows(const void* blk, size_t first, size_t step, int steps, const float* xs, int K,
+                int n, float* out1, float* out3) {
+  constexpr int NT = NM == 2 ? 6 : 12;
+  for (int t0 = 0; t0 < n; t0 += NT) {
+    const int nt = n - t0 < NT ? n - t0 : NT;
+    const float* x = xs + static_cast<size_t>(t0) * K;
+    for (int r = 0; r < 16; ++r) {
+      float* o1 = out1 + static_cast<size_t>(r) * n + t0;
+      float* o3 = NM == 2 ? out3 + static_cast<size_t>(r) * n + t0 : nullptr;
+      if (BF16)
+        row_bf16<NT, NM>(static_cast<const uint16_t*>(blk), first, step, steps, x, K, nt, r, o1, o3);
+      else
+        row_f32<NT, NM>(static_cast<const float*>(blk), first, step, steps, x, K, nt, r, o1, o3);
+    }
+  }
+}
+
+template <bool BF16>
+void run_t(ThreadPool& pool, int H, int I, const void* x, const CpuExpertJob* jobs, int n_jobs,
+           std::vector<float>& scratch) {
+  constexpr int V = BF16 ? 8 : 4;
+  constexpr int SPAN = 4 * V;
+  constexpr int FRAG = 16 * SPAN;
+  // scratch: per job xs [n][H] and h [n][I]
+  std::vector<size_t> xs_off(n_jobs), h_off(n_jobs);
+  size_t total = 0;
+  int max_n = 0;
+  for (int j = 0; j < n_jobs; ++j) {
+    xs_off[j] = total;
+    total += static_cast<size_t>(jobs[j].n) * H;
+    h_off[j] = total;
+    total += static_cast<size_t>(jobs[j].n) * I;
+    if (jobs[j].n > max_n) max_n = jobs[j].n;
+  }
+  if (scratch.size() < total) scratch.resize(total);
+  float* sc = scratch.data();
+  const int nth = pool.size();
+  std::vector<std::vector<float>> part(nth);   // per thread: [16][n] of each matrix
+  for (auto& a : part) a.resize(static_cast<size_t>(max_n) * 16 * 2);
+
+  // phase 0: token rows to fp32
+  std::atomic<int> next{0};
+  std::vector<int> row_job, row_idx;
+  for (int j = 0; j < n_jobs; ++j)
+    for (int t = 0; t < jobs[j].n; ++t) {
+      row_job.push_back(j);
+      row_idx.push_back(t);
+    }
+  const int rows_total = static_cast<int>(row_job.size());
+  pool.run([&](int) {
+    for (int i = next.fetch_add(1); i < rows_total; i = next.fetch_add(1)) {
+      const CpuExpertJob& jb = jobs[row_job[i]];
+      const int t = row_idx[i];
+      float* dst = sc + xs_off[row_job[i]] + static_cast<size_t>(t) * H;
+      const size_t src = static_cast<size_t>(jb.tokens[t]) * H;
+      if (BF16) {
+        const uint16_t* xr = static_cast<const uint16_t*>(x) + src;
+        for (int h = 0; h < H; ++h) dst[h] = bf16_to_f32(xr[h]);
+      } else {
+        std::memcpy(dst, static_cast<const float*>(x) + src, sizeof(float) * H);
+      }
+    }
+  });
+
+  // phase 1: gate/up blocks of 16 features, h = silu(W1 x) * (W3 x)
+  const int nq = I / 16, S = H / SPAN;
+  next = 0;
+  pool.run([&](int tid) {
+    float* pa = part[tid].data();
+    for (int i = next.fetch_add(1); i < n_jobs * nq; i = next.fetch_add(1)) {
+      const int j = i / nq, q = i % nq;
+      const CpuExpertJob& jb = jobs[j];
+      float* pb = pa + static_cast<size_t>(jb.n) * 16;
+      block_rows<BF16, 2>(jb.block, static_cast<size_t>(q) * S * 2 * FRAG, 2 * FRAG, S,
+                          sc + xs_off[j], H, jb.n, pa, pb);
+      for (int r = 0; r < 16; ++r)
+        for (int t = 0; t < jb.n; ++t) {
+          const float a = pa[static_cast<size_t>(r) * jb.n + t];
+          const float b = pb[static_cast<size_t>(r) * jb.n + t];
+          float hv = a / (1.f + std::exp(-a)) * b;
+          if (BF16) hv = round_bf16(hv);
+          sc[h_off[j] + static_cast<size_t>(t) * I + 16 * q + r] = hv;
+        }
+    }
+  });
+
+  // phase 2: down blocks of 16 output features
+  const int np = H / 16, S2 = I / SPAN;
+  const size_t down0 = static_cast<size_t>(2) * I * H;
+  next = 0;
+  pool.run([&](int tid) {
+    float* pa = part[tid].data();
+    for (int i = next.fetch_add(1); i < n_jobs * np; i = next.fetch_add(1)) {
+      const int j = i / np, p = i % np;
+      const CpuExpertJob& jb = jobs[j];
+      block_rows<BF16, 1>(jb.block, down0 + static_cast<size_t>(p) * S2 * FRAG, FRAG, S2,
+                          sc + h_off[j], I, jb.n, pa, nullptr);
+      for (int r = 0; r < 16; ++r)
+        for (int t = 0; t < jb.n; ++t)
+          jb.out[static_cast<size_t>(t) * H + 16 * p + r] = pa[static_cast<size_t>(r) * jb.n + t];
+    }
+  });
+}
+
+}  // namespace
+
+void cpu_ffn_run(ThreadPool& pool, bool bf16, int H, int I, const void* x,
+                 const CpuExpertJob* jobs, int n_jobs, std::vector<float>& scratch) {
+  if (n_jobs <= 0) return;
+  if (bf16)
+    run_t<true>(pool, H, I, x, jobs, n_jobs, scratch);
+  else
+    run_t<false>(pool, H, I, x, jobs, n_jobs, scratch);
+}
+
+}  // namespace oled

@@ -58,6 +58,8 @@ struct CacheView {
   int32_t* last_use;       // [L][E] layer iteration of the last activation (0: never)
   uint64_t* freq;          // [L][E] routes so far
   ExpertMask* prev_miss;   // [L] misses transferred at the layer's previous iteration
+  ExpertMask* cpu_exec;    // [L] misses of the layer in flight executed on the CPU (not
+                           // retention candidates); cleared by the retention
 };
 
 constexpr int kCountsPerLayer = 8;
@@ -272,6 +274,13 @@ struct AdaptArgs {
   int L, E, c_total;
 };
 hipError_t launch_layer_adapt(const AdaptArgs& a, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s);
+
+// Cooperative compensation: the staged misses in `cpu` run on the host CPU.
+// Their staging slots return to the free list, they leave the staged list
+// (so only the transferred ones are copied) and the previous-transfer mask,
+// and the retention of the layer skips them as candidates.
+hipError_t launch_coop_unstage(const CacheView& cv, int layer, int E, const ExpertMask& cpu,
+                               hipStream_t s);
 
 // K5 and K6 in one launch (the layer's last).
 hipError_t launch_combine_score(bool bf16, const CombineArgs& c, const ScoreArgs& a,

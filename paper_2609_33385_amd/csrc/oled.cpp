@@ -25,12 +25,15 @@
 
 #include <algorithm>
 #include <atomic>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <memory>
 #include <string>
 #include <vector>
 
+#include "cpu_ffn.h"
 #include "kernels.h"
 
 namespace {
@@ -157,6 +160,22 @@ struct Ctx {
   // profiling
   std::vector<OpRec> ops;
   std::vector<hipEvent_t> ev_free;
+  // cooperative compensation (coop contexts)
+  bool coop = false;
+  double coop_t = 0.0, coop_tau = 0.0, coop_nbar = 0.0, coop_lambda = 0.0;
+  std::unique_ptr<oled::ThreadPool> pool;
+  std::vector<float> cpu_scratch;
+  ExpertMask* d_cpu = nullptr;     // [L] CPU-executed misses of the layer in flight
+  int32_t* h_ctopk = nullptr;      // pinned copies of the layer's routing, confidence, x
+  float* h_cgates = nullptr;
+  float* h_cconf = nullptr;
+  char* h_cx = nullptr;
+  float* h_cout[2] = {nullptr, nullptr};  // CPU expert outputs, alternating per layer
+  hipEvent_t ev_cout[2] = {nullptr, nullptr};
+  bool cout_used[2] = {false, false};
+  int cout_buf = 0;
+  hipEvent_t ev_coop = nullptr;
+  bool deferred = false;           // moe_forward_cached left the hit launches to apply_misses_coop
 };
 
 oled_status fail(Ctx* c, oled_status st, const char* fmt, ...) {
@@ -338,6 +357,16 @@ void free_ctx(Ctx* c) {
   if (c->ev_up) (void)hipEventDestroy(c->ev_up);
   if (c->ev_down) (void)hipEventDestroy(c->ev_down);
   if (c->ev_order) (void)hipEventDestroy(c->ev_order);
+  if (c->ev_coop) (void)hipEventDestroy(c->ev_coop);
+  for (int b = 0; b < 2; ++b) {
+    if (c->ev_cout[b]) (void)hipEventDestroy(c->ev_cout[b]);
+    if (c->h_cout[b]) (void)hipHostFree(c->h_cout[b]);
+  }
+  void* pinned[] = {c->h_ctopk, c->h_cgates, c->h_cconf, c->h_cx};
+  for (void* p : pinned)
+    if (p) (void)hipHostFree(p);
+  if (c->d_cpu) (void)hipFree(c->d_cpu);
+  c->pool.reset();
   if (c->own_copy) (void)hipStreamDestroy(c->own_copy);
   void* dev[] = {c->d_pool, c->d_topk, c->d_gates, c->d_counts, c->d_offsets, c->d_perm,
                  c->d_inv, c->d_flag, c->d_item_counts, c->d_sync, c->d_items, c->d_dense_items,
@@ -382,6 +411,7 @@ oled_status init_cache_state(Ctx* c) {
   HIP_TRY(c, hipMemset(c->d_freq, 0, sizeof(uint64_t) * c->L * c->E));
   HIP_TRY(c, hipMemset(c->d_prev_miss, 0, sizeof(ExpertMask) * c->L));
   HIP_TRY(c, hipMemset(c->d_key, 0, sizeof(uint64_t) * c->L * c->E));
+  if (c->d_cpu) HIP_TRY(c, hipMemset(c->d_cpu, 0, sizeof(ExpertMask) * c->L));
   HIP_TRY(c, hipMemset(c->d_score, 0, sizeof(uint64_t) * c->L * c->E));
   std::vector<int32_t> caps(c->L, c->cap);
   HIP_TRY(c, hipMemcpy(c->d_cap, caps.data(), sizeof(int32_t) * c->L, hipMemcpyHostToDevice));
@@ -413,6 +443,7 @@ CacheView view(const Ctx* c) {
   v.last_use = c->d_last_use;
   v.freq = c->d_freq;
   v.prev_miss = c->d_prev_miss;
+  v.cpu_exec = c->d_cpu;
   v.n_slots = c->n_slots;
   return v;
 }
@@ -489,7 +520,7 @@ void complete_op(const Ctx* c, OpRec& op, const RouteStats& r) {
     const Part h = streamed(r, true), m = streamed(r, false);
     op.bytes = down_bytes(c, h.n, h.rows) + up_bytes(c, m.n, m.rows);
     op.flops = down_flops(c, h.rows) + up_flops(c, m.rows);
-    op.h2d = static_cast<int64_t>(r.n_staged) * (c->eb - c->e13);
+    if (op.h2d < 0) op.h2d = static_cast<int64_t>(r.n_staged) * (c->eb - c->e13);
     return;
   }
   if (op.part == 3 || op.part == 4) {  // dense tiles
@@ -593,293 +624,15 @@ oled_status check_slots(Ctx* c) {
   return OLED_OK;
 }
 
-}  // namespace
 
-extern "C" {
-
-oled_status oled_create(const oled_config* cfg, void** ctx_out) {
-  if (ctx_out) *ctx_out = nullptr;
-  auto bad = [](oled_status st, const char* m) {
-    g_create_error = m;
-    return st;
-  };
-  if (!cfg || !ctx_out) return bad(OLED_ERR_INVALID_ARG, "NULL config or output pointer");
-  if (cfg->hidden <= 0 || cfg->inter <= 0 || cfg->n_experts <= 0 || cfg->top_k <= 0 ||
-      cfg->n_layers <= 0 || cfg->capacity < 0 || cfg->max_tokens <= 0)
-    return bad(OLED_ERR_INVALID_ARG, "non-positive shape field");
-  if (cfg->dtype != OLED_F32 && cfg->dtype != OLED_BF16)
-    return bad(OLED_ERR_INVALID_ARG, "dtype must be OLED_F32 or OLED_BF16");
-  if (cfg->copy_mode != OLED_COPY_SHADER && cfg->copy_mode != OLED_COPY_SDMA)
-    return bad(OLED_ERR_INVALID_ARG, "copy_mode must be OLED_COPY_SHADER or OLED_COPY_SDMA");
-  if (cfg->adapt_period < 0) return bad(OLED_ERR_INVALID_ARG, "adapt_period < 0");
-  if (cfg->policy != OLED_POLICY_PRIORITY && cfg->policy != OLED_POLICY_LRU &&
-      cfg->policy != OLED_POLICY_LFU)
-    return bad(OLED_ERR_INVALID_ARG, "policy must be OLED_POLICY_PRIORITY, _LRU or _LFU");
-  if (cfg->adapt_period > 0 && cfg->n_layers > oled::kMaxAdaptLayers)
-    return bad(OLED_ERR_UNSUPPORTED, "adapt_period > 0 needs n_layers <= 1024");
-  if (cfg->top_k > cfg->n_experts) return bad(OLED_ERR_INVALID_ARG, "top_k > n_experts");
-  if (cfg->hidden % 128 || cfg->inter % 128)
-    return bad(OLED_ERR_UNSUPPORTED, "hidden and inter must be multiples of 128");
-  if (cfg->n_experts > oled::kMaxExperts) return bad(OLED_ERR_UNSUPPORTED, "n_experts > 256");
-  if (cfg->top_k > oled::kMaxTopK) return bad(OLED_ERR_UNSUPPORTED, "top_k > 16");
-  if (cfg->max_tokens > 65535) return bad(OLED_ERR_UNSUPPORTED, "max_tokens > 65535");
-  if (!cfg->host_pool || cfg->host_pool_blocks <= 0 || !cfg->host_block_of)
-    return bad(OLED_ERR_INVALID_ARG, "host pool, block count and block table are required");
-  const int64_t nb = static_cast<int64_t>(cfg->n_layers) * cfg->n_experts;
-  for (int64_t i = 0; i < nb; ++i)
-    if (cfg->host_block_of[i] < 0 || cfg->host_block_of[i] >= cfg->host_pool_blocks)
-      return bad(OLED_ERR_INVALID_ARG, "host_block_of entry outside [0, host_pool_blocks)");
-
-  int ndev = 0;
-  if (hipGetDeviceCount(&ndev) != hipSuccess || ndev <= 0)
-    return bad(OLED_ERR_HIP, "no HIP device");
-  if (cfg->device < 0 || cfg->device >= ndev) return bad(OLED_ERR_INVALID_ARG, "bad device ordinal");
-  if (hipSetDevice(cfg->device) != hipSuccess) return bad(OLED_ERR_HIP, "hipSetDevice failed");
-
-  hipPointerAttribute_t attr;
-  std::memset(&attr, 0, sizeof(attr));
-  if (hipPointerGetAttributes(&attr, cfg->host_pool) != hipSuccess || attr.type != hipMemoryTypeHost) {
-    (void)hipGetLastError();
-    return bad(OLED_ERR_INVALID_ARG, "host_pool is not pinned host memory");
-  }
-  // the address kernels use to read the pool (same allocation, device view)
-  void* dev_view = nullptr;
-  if (hipHostGetDevicePointer(&dev_view, const_cast<void*>(cfg->host_pool), 0) != hipSuccess ||
-      !dev_view) {
-    (void)hipGetLastError();
-    return bad(OLED_ERR_INVALID_ARG, "host_pool is not mapped for device access");
-  }
-
-  Ctx* c = new Ctx();
-  c->H = cfg->hidden;
-  c->I = cfg->inter;
-  c->E = cfg->n_experts;
-  c->K = cfg->top_k;
-  c->L = cfg->n_layers;
-  c->C = cfg->capacity;
-  c->Tmax = cfg->max_tokens;
-  c->dtype = cfg->dtype;
-  c->copy_mode = cfg->copy_mode;
-  c->adapt_period = cfg->adapt_period;
-  c->policy = cfg->policy;
-  c->esz = cfg->dtype == OLED_F32 ? 4 : 2;
-  c->device = cfg->device;
-  c->profile_ops = static_cast<uint32_t>(cfg->profile_ops);
-  c->eb = static_cast<int64_t>(3) * c->H * c->I * c->esz;
-  c->e13 = static_cast<int64_t>(2) * c->H * c->I * c->esz;
-  c->cap = c->C < c->E ? c->C : c->E;
-  const int64_t routes = static_cast<int64_t>(c->Tmax) * c->K;
-  const int staging = routes < c->E ? static_cast<int>(routes) : c->E;
-  c->n_slots = c->L * c->cap + staging;
-  c->max_items = static_cast<int>(routes / oled::kItemRows) + c->E + 1;
-  c->dense_ok = c->dtype == OLED_BF16 && c->H % 256 == 0 && c->I % 256 == 0 &&
-                c->Tmax >= oled::kDenseMinRows && routes * c->I * 2 <= INT32_MAX &&
-                static_cast<int64_t>(c->Tmax) * c->H * 2 <= INT32_MAX;
-  c->max_dense = c->dense_ok ? static_cast<int>(routes / oled::kDenseRows) + c->E + 1 : 0;
-  c->host_pool = static_cast<const char*>(cfg->host_pool);
-  c->P = cfg->host_pool_blocks;
-  c->host_block_of.assign(cfg->host_block_of, cfg->host_block_of + nb);
-
-  auto oom = [&](const char* what) {
-    (void)hipGetLastError();
-    g_create_error = std::string("device allocation failed: ") + what;
-    free_ctx(c);
-    return OLED_ERR_OUT_OF_MEMORY;
-  };
-  if (hipMalloc(reinterpret_cast<void**>(&c->d_pool), static_cast<size_t>(c->n_slots) * c->eb) !=
-      hipSuccess)
-    return oom("slot pool");
-  if (dev_alloc(&c->d_topk, routes) || dev_alloc(&c->d_gates, routes) ||
-      dev_alloc(&c->d_counts, c->E) || dev_alloc(&c->d_offsets, c->E + 1) ||
-      dev_alloc(&c->d_perm, routes) || dev_alloc(&c->d_inv, routes) || dev_alloc(&c->d_flag, 1) ||
-      dev_alloc(&c->d_item_counts, 2) || dev_alloc(&c->d_sync, 2) ||
-      dev_alloc(&c->d_chunk, static_cast<size_t>(oled::permute_chunks(c->Tmax)) * c->E) ||
-      dev_alloc(&c->d_pcount, 1) || dev_alloc(&c->d_sacc, c->E) || dev_alloc(&c->d_ssync, 2) ||
-      dev_alloc(&c->d_items, c->max_items) ||
-      (c->dense_ok && (dev_alloc(&c->d_dense_items, c->max_dense) ||
-                       dev_alloc(&c->d_dense_counts, 2))) ||
-      dev_alloc(reinterpret_cast<char**>(&c->d_h), routes * c->I * c->esz) ||
-      dev_alloc(&c->d_O, routes * c->H) ||
-      dev_alloc(&c->d_score, static_cast<size_t>(c->L) * c->E))
-    return oom("routing scratch");
-  if (dev_alloc(&c->d_hdr, 1) || dev_alloc(&c->d_slot_of, nb) || dev_alloc(&c->d_res, c->L) ||
-      dev_alloc(&c->d_res_before, c->L) ||
-      dev_alloc(&c->d_last_counts, oled::kCountsPerLayer * c->L) ||
-      dev_alloc(&c->d_iters, c->L) || dev_alloc(&c->d_last_use, nb) || dev_alloc(&c->d_freq, nb) ||
-      dev_alloc(&c->d_prev_miss, c->L) || dev_alloc(&c->d_key, nb) ||
-      dev_alloc(&c->d_free, c->n_slots) || dev_alloc(&c->d_host_addr, nb) ||
-      dev_alloc(&c->d_cap, c->L) || dev_alloc(&c->d_stat, c->L))
-    return oom("cache state");
-  if (hipMemset(c->d_flag, 0, sizeof(int32_t)) != hipSuccess ||
-      hipMemset(c->d_item_counts, 0, 2 * sizeof(int32_t)) != hipSuccess ||
-      hipMemset(c->d_sync, 0, 2 * sizeof(int32_t)) != hipSuccess ||
-      hipMemset(c->d_pcount, 0, sizeof(int32_t)) != hipSuccess ||
-      hipMemset(c->d_sacc, 0, sizeof(unsigned long long) * c->E) != hipSuccess ||
-      hipMemset(c->d_ssync, 0, 2 * sizeof(int32_t)) != hipSuccess)
-    return oom("scratch init");
-  {
-    std::vector<uint64_t> addr(nb);
-    for (int64_t i = 0; i < nb; ++i)
-      addr[i] = reinterpret_cast<uint64_t>(dev_view) +
-                static_cast<uint64_t>(c->host_block_of[i]) * static_cast<uint64_t>(c->eb);
-    if (hipMemcpy(c->d_host_addr, addr.data(), sizeof(uint64_t) * nb, hipMemcpyHostToDevice) !=
-        hipSuccess)
-      return oom("host block table");
-  }
-  if (hipHostMalloc(reinterpret_cast<void**>(&c->h_ring), sizeof(RouteStats) * oled::kStatsRing,
-                    hipHostMallocDefault) ||
-      hipHostMalloc(reinterpret_cast<void**>(&c->h_staged), sizeof(StagedList), hipHostMallocCoherent) ||
-      hipHostMalloc(reinterpret_cast<void**>(&c->h_ret), sizeof(RetainOut) * c->L, hipHostMallocDefault))
-    return oom("pinned records");
-  if (dev_alloc(&c->d_ring, oled::kStatsRing) || dev_alloc(&c->d_ret, c->L) ||
-      hipMemset(c->d_ring, 0, sizeof(RouteStats) * oled::kStatsRing) != hipSuccess ||
-      hipMemset(c->d_ret, 0, sizeof(RetainOut) * c->L) != hipSuccess)
-    return oom("record rings");
-  std::memset(c->h_ring, 0, sizeof(RouteStats) * oled::kStatsRing);
-  std::memset(c->h_staged, 0, sizeof(StagedList));
-  std::memset(c->h_ret, 0, sizeof(RetainOut) * c->L);
-  if (hipStreamCreateWithFlags(&c->own_copy, hipStreamNonBlocking) != hipSuccess ||
-      hipEventCreateWithFlags(&c->ev_up, hipEventDisableTiming) != hipSuccess ||
-      hipEventCreateWithFlags(&c->ev_down, hipEventDisableTiming) != hipSuccess ||
-      hipEventCreateWithFlags(&c->ev_order, hipEventDisableTiming) != hipSuccess) {
-    g_create_error = "stream/event creation failed";
-    free_ctx(c);
-    return OLED_ERR_HIP;
-  }
-  c->ret_seq.assign(c->L, 0);
-  c->ret_seen.assign(c->L, 0);
-  c->rejected.assign(c->L, 0);
-  if (init_cache_state(c) != OLED_OK) {
-    g_create_error = c->err;
-    free_ctx(c);
-    return OLED_ERR_HIP;
-  }
-  g_create_error.clear();
-  *ctx_out = c;
-  return OLED_OK;
-}
-
-void oled_destroy(void* ctx) { free_ctx(static_cast<Ctx*>(ctx)); }
-
-const char* oled_last_error(const void* ctx) {
-  if (!ctx) return g_create_error.c_str();
-  return static_cast<const Ctx*>(ctx)->err.c_str();
-}
-
-oled_status oled_reset_cache(void* ctx) {
-  Ctx* c = static_cast<Ctx*>(ctx);
-  if (!c) return OLED_ERR_INVALID_ARG;
-  if (c->stage != Stage::kIdle) return fail(c, OLED_ERR_STATE, "reset while a layer is in flight");
-  HIP_TRY(c, hipSetDevice(c->device));
-  HIP_TRY(c, hipDeviceSynchronize());
-  oled_status st = drain_records(c, c->route_n);
-  if (st != OLED_OK) return st;
-  st = init_cache_state(c);
-  if (st != OLED_OK) return st;
-  c->broken = false;
-  std::fill(c->ret_seq.begin(), c->ret_seq.end(), 0);
-  std::fill(c->ret_seen.begin(), c->ret_seen.end(), 0);
-  std::fill(c->rejected.begin(), c->rejected.end(), 0);
-  c->rejected_layer = -1;
-  c->bad_route_layer = -1;
-  c->reported_bad_route = 0;
-  return OLED_OK;
-}
-
-oled_status route_block(void* ctx, int32_t layer, const float* logits_dev, int32_t T, void* stream) {
-  Ctx* c = static_cast<Ctx*>(ctx);
-  if (!c) return OLED_ERR_INVALID_ARG;
-  oled_status st = check_layer(c, layer);
-  if (st != OLED_OK) return st;
-  if (c->broken)
-    return fail(c, OLED_ERR_STATE, "an earlier HIP failure left the cache state unknown: "
-                                   "call oled_reset_cache");
-  if (c->stage != Stage::kIdle)
-    return fail(c, OLED_ERR_STATE, "route_block while layer %d is in flight", c->cur_layer);
-  if (!logits_dev) return fail(c, OLED_ERR_INVALID_ARG, "NULL logits");
-  if (T < 1 || T > c->Tmax) return fail(c, OLED_ERR_INVALID_ARG, "T=%d outside [1,%d]", T, c->Tmax);
-  HIP_TRY(c, hipSetDevice(c->device));
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  if (c->have_stream && s != c->cur_stream) {  // order the new stream after the old one
-    HIP_TRY(c, hipEventRecord(c->ev_order, c->cur_stream));
-    HIP_TRY(c, hipStreamWaitEvent(s, c->ev_order, 0));
-  }
-  // consume what has been published; this call's ring entry must be free
-  const int n = c->route_n + 1;
-  st = drain_records(c, n - oled::kStatsRing, false);
-  if (st != OLED_OK) return st;
-
-  PermuteOut o;
-  o.counts = c->d_counts;
-  o.offsets = c->d_offsets;
-  o.perm = c->d_perm;
-  o.inv_perm = c->d_inv;
-  o.items = c->d_items;
-  o.item_counts = c->d_item_counts;
-  // experts with many rows go to the dense-tile GEMM; a token picks an expert
-  // at most once, so no expert of a block of fewer tokens can have that many
-  o.dense_min = c->dense_ok && T >= oled::kDenseMinRows ? oled::kDenseMinRows : 0;
-  o.dense_items = c->d_dense_items;
-  o.dense_counts = c->d_dense_counts;
-  o.ring = c->d_ring;
-  o.staged = c->copy_mode == OLED_COPY_SDMA ? c->h_staged : nullptr;
-  o.layer = layer;
-  o.E = c->E;
-  o.seq = n;
-  o.cv = view(c);
-  const int64_t route_bytes = static_cast<int64_t>(T) * c->E * 4 + static_cast<int64_t>(T) * c->K * 8;
-  const int64_t perm_bytes = static_cast<int64_t>(T) * c->K * 12 + static_cast<int64_t>(c->E) * 8;
-  if (oled::route_fused(T, c->K)) {
-    OpEvents ev = op_begin(c, OLED_OP_ROUTE_TOPK);
-    HIP_TRY(c, oled::launch_route_fused(logits_dev, T, c->K, c->d_topk, c->d_gates, c->d_sync, o,
-                                        ev.a, ev.b, s));
-    op_end(c, ev, rec(OLED_OP_ROUTE_TOPK, layer, route_bytes + perm_bytes));
-  } else {
-    {
-      OpEvents ev = op_begin(c, OLED_OP_ROUTE_TOPK);
-      HIP_TRY(c, oled::launch_route_topk(logits_dev, T, c->E, c->K, c->d_topk, c->d_gates,
-                                         c->d_flag, ev.a, ev.b, s));
-      op_end(c, ev, rec(OLED_OP_ROUTE_TOPK, layer, route_bytes));
-    }
-    OpEvents ev = op_begin(c, OLED_OP_PERMUTE);
-    if (oled::permute_chunked(T))
-      HIP_TRY(c, oled::launch_permute_chunked(c->d_topk, T, c->K, c->d_flag, c->d_chunk,
-                                              c->d_pcount, o, ev.a, ev.b, s));
-    else
-      HIP_TRY(c, oled::launch_permute(c->d_topk, T, c->K, c->d_flag, o, ev.a, ev.b, s));
-    op_end(c, ev, rec(OLED_OP_PERMUTE, layer, perm_bytes));
-  }
-  c->route_n = n;
-  c->cur_route = n;
-  c->stage = Stage::kRouted;
-  c->cur_layer = layer;
-  c->cur_T = T;
-  c->cur_dense = o.dense_min > 0;
-  c->cur_stream = s;
-  c->have_stream = true;
-  c->fwd_x = nullptr;
-  c->fwd_y = nullptr;
-  c->last_routed_layer = layer;
-  c->last_routed_T = T;
-  return OLED_OK;
-}
-
-oled_status moe_forward_cached(void* ctx, int32_t layer, const void* x_dev, void* y_dev, void* stream) {
-  Ctx* c = static_cast<Ctx*>(ctx);
-  if (!c) return OLED_ERR_INVALID_ARG;
-  oled_status st = check_layer(c, layer);
-  if (st != OLED_OK) return st;
-  if (c->stage != Stage::kRouted)
-    return fail(c, OLED_ERR_STATE, "moe_forward_cached must follow route_block");
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  st = check_in_flight(c, layer, s, "moe_forward_cached");
-  if (st != OLED_OK) return st;
-  if (!x_dev || !y_dev) return fail(c, OLED_ERR_INVALID_ARG, "NULL x or y");
-  HIP_TRY(c, hipSetDevice(c->device));
-  // hits: the active residents, at most min(C, E) experts; their item count
-  // stays on the device. With the shader transfer the first workgroups of the
-  // launch copy the staged misses' gate/up weights, and the hits' down GEMM
-  // is enqueued by apply_misses (sharing a launch with the misses' gate/up).
+// The hits' GEMMs: the active residents, at most min(C, E) experts; their
+// item count stays on the device. With the shader transfer the first
+// workgroups of the gate/up launch copy the staged misses' gate/up weights
+// (h2d: their bytes, or -1 to take them from the routing record), and the
+// hits' down GEMM is enqueued later (sharing a launch with the misses'
+// gate/up); with the copy engine it follows at once.
+oled_status launch_hits(Ctx* c, int layer, hipStream_t s, int64_t h2d) {
+  const void* x_dev = c->fwd_x;
   const int64_t routes = static_cast<int64_t>(c->cur_T) * c->K;
   const int max_hit_items =
       c->cap > 0 ? static_cast<int>(std::min<int64_t>(c->cap, routes) + routes / oled::kItemRows) : 0;
@@ -899,7 +652,7 @@ oled_status moe_forward_cached(void* ctx, int32_t layer, const void* x_dev, void
     r.route_seq = c->cur_route;
     r.part = 0;
     r.hits = true;
-    r.h2d = shader ? -1 : 0;
+    r.h2d = shader ? (h2d >= 0 ? h2d * c->e13 / c->eb : -1) : 0;
     op_end(c, ev, r);
   }
   if (!shader) {
@@ -912,11 +665,9 @@ oled_status moe_forward_cached(void* ctx, int32_t layer, const void* x_dev, void
     r.hits = true;
     op_end(c, ev, r);
   }
-  c->fwd_x = x_dev;
-  c->fwd_y = y_dev;
-  c->stage = Stage::kHitsQueued;
   return OLED_OK;
 }
+
 
 // The dense experts (at least kDenseMinRows routes; hits and misses alike,
 // every weight already in its slot): gate/up tiles, then down tiles. Their
@@ -1027,11 +778,462 @@ oled_status apply_misses_sdma(Ctx* c, int layer, hipStream_t cs, const RouteStat
   return c->cur_dense ? launch_dense(c, layer, s) : OLED_OK;
 }
 
+// Cooperative compensation, Sec. 4.4: the objective J(G) = T_comp(G) -
+// lambda * sum_{e in G} p_e with T_comp = max(T_H2D |G|, tau_CPU * tokens left
+// to the CPU) and sum_G p = (sum_G S) / (sum S). float64, no contraction.
+double coop_objective(const std::vector<int>& misses, const std::vector<uint8_t>& in_g, int n_g,
+                      const int32_t* n_tok, const uint64_t* S, uint64_t S_total, double t_h2d,
+                      double tau, double lam) {
+  int64_t cpu_tokens = 0;
+  uint64_t mass = 0;
+  for (int e : misses) {
+    if (in_g[e]) mass += S[e];
+    else cpu_tokens += n_tok[e];
+  }
+  const double t_gpu = t_h2d * static_cast<double>(n_g);
+  const double t_cpu = tau * static_cast<double>(cpu_tokens);
+  const double t_comp = t_gpu >= t_cpu ? t_gpu : t_cpu;
+  const double share = S_total > 0 ? static_cast<double>(mass) / static_cast<double>(S_total) : 0.0;
+  return t_comp - lam * share;
+}
+
+// The two-stage dispatch: rho = nbar tau / (nbar tau + T_H2D); stage 1 takes
+// the round_half_up(rho |M|) misses of highest (S desc, id asc); stage 2 makes
+// at most |M| swaps, each the best by J (the first in (transferred id, CPU id)
+// order among equals) and only if it lowers J.
+void coop_dispatch(int E, const uint8_t* miss, const int32_t* n_tok, const uint64_t* S,
+                   double t_h2d, double tau, double nbar, double lam, uint8_t* transfer) {
+  std::vector<int> misses;
+  uint64_t S_total = 0;
+  for (int e = 0; e < E; ++e) {
+    if (miss[e]) misses.push_back(e);
+    S_total += S[e];
+  }
+  const double cpu = nbar * tau;
+  const double den = cpu + t_h2d;
+  const double rho = den > 0.0 ? cpu / den : 1.0;
+  const int m = static_cast<int>(misses.size());
+  const int n_g = static_cast<int>(std::floor(rho * static_cast<double>(m) + 0.5));
+  std::vector<int> order = misses;
+  std::sort(order.begin(), order.end(), [&](int a, int b) { return S[a] != S[b] ? S[a] > S[b] : a < b; });
+  std::vector<uint8_t> in_g(E, 0);
+  for (int i = 0; i < n_g && i < m; ++i) in_g[order[i]] = 1;
+  double J = coop_objective(misses, in_g, n_g, n_tok, S, S_total, t_h2d, tau, lam);
+  for (int round = 0; round < m; ++round) {
+    bool found = false;
+    double best = 0.0;
+    int bg = -1, bc = -1;
+    for (int g : misses) {
+      if (!in_g[g]) continue;
+      for (int c2 : misses) {
+        if (in_g[c2]) continue;
+        in_g[g] = 0;
+        in_g[c2] = 1;
+        const double j = coop_objective(misses, in_g, n_g, n_tok, S, S_total, t_h2d, tau, lam);
+        in_g[g] = 1;
+        in_g[c2] = 0;
+        if (!found || j < best) {
+          found = true;
+          best = j;
+          bg = g;
+          bc = c2;
+        }
+      }
+    }
+    if (!found || !(best < J)) break;
+    in_g[bg] = 0;
+    in_g[bc] = 1;
+    J = best;
+  }
+  for (int e = 0; e < E; ++e) transfer[e] = in_g[e];
+}
+
+// Shader transfer, after the hits' gate/up launch: one launch with the hits'
+// down GEMM, the transfer of the misses' down weights and the misses' gate/up
+// GEMM (their gate/up weights landed with the previous launch); then the
+// misses' down GEMM and the dense experts. Miss items are bounded by the
+// staging capacity; their count is on the device. h2d: bytes of the staged
+// misses, or -1 to take them from the routing record.
+oled_status launch_shader_rest(Ctx* c, int layer, hipStream_t s, int64_t h2d) {
+  const bool bf16 = c->dtype == OLED_BF16;
+  const int64_t routes = static_cast<int64_t>(c->cur_T) * c->K;
+  const int max_hit_items =
+      c->cap > 0 ? static_cast<int>(std::min<int64_t>(c->cap, routes) + routes / oled::kItemRows)
+                 : 0;
+  const int max_miss_items =
+      static_cast<int>(std::min<int64_t>(c->E, routes) + routes / oled::kItemRows);
+  FfnLaunch d = ffn_args(c, layer, 0, max_hit_items, 0);
+  d.src = c->d_h;
+  d.fetch.nblk = kFetchBlocks;
+  d.fetch.off = c->e13;
+  d.fetch.len = c->eb - c->e13;
+  FfnLaunch u = ffn_args(c, layer, 1, max_miss_items, kMissGridCap);
+  u.src = c->fwd_x;
+  {
+    OpEvents ev = op_begin(c, OLED_OP_FFN_DOWN);
+    HIP_TRY(c, oled::launch_ffn_mix(bf16, d, u, ev.a, ev.b, s));
+    OpRec o = rec(OLED_OP_FFN_DOWN, layer, -1);
+    o.route_seq = c->cur_route;
+    o.part = 2;
+    o.h2d = h2d >= 0 ? h2d - h2d * c->e13 / c->eb : -1;
+    op_end(c, ev, o);
+  }
+  FfnLaunch a = ffn_args(c, layer, 1, max_miss_items, kMissGridCap);
+  a.src = c->d_h;
+  {
+    OpEvents ev = op_begin(c, OLED_OP_FFN_DOWN);
+    HIP_TRY(c, oled::launch_ffn_down(bf16, a, ev.a, ev.b, s));
+    OpRec o = rec(OLED_OP_FFN_DOWN, layer, -1);
+    o.route_seq = c->cur_route;
+    o.part = 1;
+    op_end(c, ev, o);
+  }
+  return c->cur_dense ? launch_dense(c, layer, s) : OLED_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+oled_status oled_create(const oled_config* cfg, void** ctx_out) {
+  if (ctx_out) *ctx_out = nullptr;
+  auto bad = [](oled_status st, const char* m) {
+    g_create_error = m;
+    return st;
+  };
+  if (!cfg || !ctx_out) return bad(OLED_ERR_INVALID_ARG, "NULL config or output pointer");
+  if (cfg->hidden <= 0 || cfg->inter <= 0 || cfg->n_experts <= 0 || cfg->top_k <= 0 ||
+      cfg->n_layers <= 0 || cfg->capacity < 0 || cfg->max_tokens <= 0)
+    return bad(OLED_ERR_INVALID_ARG, "non-positive shape field");
+  if (cfg->dtype != OLED_F32 && cfg->dtype != OLED_BF16)
+    return bad(OLED_ERR_INVALID_ARG, "dtype must be OLED_F32 or OLED_BF16");
+  if (cfg->copy_mode != OLED_COPY_SHADER && cfg->copy_mode != OLED_COPY_SDMA)
+    return bad(OLED_ERR_INVALID_ARG, "copy_mode must be OLED_COPY_SHADER or OLED_COPY_SDMA");
+  if (cfg->adapt_period < 0) return bad(OLED_ERR_INVALID_ARG, "adapt_period < 0");
+  if (cfg->coop != 0 && cfg->coop != 1) return bad(OLED_ERR_INVALID_ARG, "coop must be 0 or 1");
+  if (cfg->coop) {
+    if (cfg->copy_mode != OLED_COPY_SHADER)
+      return bad(OLED_ERR_UNSUPPORTED, "coop needs OLED_COPY_SHADER");
+    if (cfg->coop_threads < 1) return bad(OLED_ERR_INVALID_ARG, "coop_threads < 1");
+    if (!(cfg->coop_t_h2d_us >= 0.0) || !(cfg->coop_tau_cpu_us >= 0.0) ||
+        !(cfg->coop_nbar >= 0.0) || !(cfg->coop_lambda_us >= 0.0) ||
+        !std::isfinite(cfg->coop_t_h2d_us) || !std::isfinite(cfg->coop_tau_cpu_us) ||
+        !std::isfinite(cfg->coop_nbar) || !std::isfinite(cfg->coop_lambda_us))
+      return bad(OLED_ERR_INVALID_ARG, "coop times and weights must be finite and >= 0");
+    if (!oled::cpu_ffn_supported())
+      return bad(OLED_ERR_UNSUPPORTED, "coop needs a CPU with AVX2 and FMA");
+  }
+  if (cfg->policy != OLED_POLICY_PRIORITY && cfg->policy != OLED_POLICY_LRU &&
+      cfg->policy != OLED_POLICY_LFU)
+    return bad(OLED_ERR_INVALID_ARG, "policy must be OLED_POLICY_PRIORITY, _LRU or _LFU");
+  if (cfg->adapt_period > 0 && cfg->n_layers > oled::kMaxAdaptLayers)
+    return bad(OLED_ERR_UNSUPPORTED, "adapt_period > 0 needs n_layers <= 1024");
+  if (cfg->top_k > cfg->n_experts) return bad(OLED_ERR_INVALID_ARG, "top_k > n_experts");
+  if (cfg->hidden % 128 || cfg->inter % 128)
+    return bad(OLED_ERR_UNSUPPORTED, "hidden and inter must be multiples of 128");
+  if (cfg->n_experts > oled::kMaxExperts) return bad(OLED_ERR_UNSUPPORTED, "n_experts > 256");
+  if (cfg->top_k > oled::kMaxTopK) return bad(OLED_ERR_UNSUPPORTED, "top_k > 16");
+  if (cfg->max_tokens > 65535) return bad(OLED_ERR_UNSUPPORTED, "max_tokens > 65535");
+  if (!cfg->host_pool || cfg->host_pool_blocks <= 0 || !cfg->host_block_of)
+    return bad(OLED_ERR_INVALID_ARG, "host pool, block count and block table are required");
+  const int64_t nb = static_cast<int64_t>(cfg->n_layers) * cfg->n_experts;
+  for (int64_t i = 0; i < nb; ++i)
+    if (cfg->host_block_of[i] < 0 || cfg->host_block_of[i] >= cfg->host_pool_blocks)
+      return bad(OLED_ERR_INVALID_ARG, "host_block_of entry outside [0, host_pool_blocks)");
+
+  int ndev = 0;
+  if (hipGetDeviceCount(&ndev) != hipSuccess || ndev <= 0)
+    return bad(OLED_ERR_HIP, "no HIP device");
+  if (cfg->device < 0 || cfg->device >= ndev) return bad(OLED_ERR_INVALID_ARG, "bad device ordinal");
+  if (hipSetDevice(cfg->device) != hipSuccess) return bad(OLED_ERR_HIP, "hipSetDevice failed");
+
+  hipPointerAttribute_t attr;
+  std::memset(&attr, 0, sizeof(attr));
+  if (hipPointerGetAttributes(&attr, cfg->host_pool) != hipSuccess || attr.type != hipMemoryTypeHost) {
+    (void)hipGetLastError();
+    return bad(OLED_ERR_INVALID_ARG, "host_pool is not pinned host memory");
+  }
+  // the address kernels use to read the pool (same allocation, device view)
+  void* dev_view = nullptr;
+  if (hipHostGetDevicePointer(&dev_view, const_cast<void*>(cfg->host_pool), 0) != hipSuccess ||
+      !dev_view) {
+    (void)hipGetLastError();
+    return bad(OLED_ERR_INVALID_ARG, "host_pool is not mapped for device access");
+  }
+
+  Ctx* c = new Ctx();
+  c->H = cfg->hidden;
+  c->I = cfg->inter;
+  c->E = cfg->n_experts;
+  c->K = cfg->top_k;
+  c->L = cfg->n_layers;
+  c->C = cfg->capacity;
+  c->Tmax = cfg->max_tokens;
+  c->dtype = cfg->dtype;
+  c->copy_mode = cfg->copy_mode;
+  c->adapt_period = cfg->adapt_period;
+  c->policy = cfg->policy;
+  c->coop = cfg->coop != 0;
+  c->coop_t = cfg->coop_t_h2d_us;
+  c->coop_tau = cfg->coop_tau_cpu_us;
+  c->coop_nbar = cfg->coop_nbar;
+  c->coop_lambda = cfg->coop_lambda_us;
+  c->esz = cfg->dtype == OLED_F32 ? 4 : 2;
+  c->device = cfg->device;
+  c->profile_ops = static_cast<uint32_t>(cfg->profile_ops);
+  c->eb = static_cast<int64_t>(3) * c->H * c->I * c->esz;
+  c->e13 = static_cast<int64_t>(2) * c->H * c->I * c->esz;
+  c->cap = c->C < c->E ? c->C : c->E;
+  const int64_t routes = static_cast<int64_t>(c->Tmax) * c->K;
+  const int staging = routes < c->E ? static_cast<int>(routes) : c->E;
+  c->n_slots = c->L * c->cap + staging;
+  c->max_items = static_cast<int>(routes / oled::kItemRows) + c->E + 1;
+  c->dense_ok = c->dtype == OLED_BF16 && c->H % 256 == 0 && c->I % 256 == 0 &&
+                c->Tmax >= oled::kDenseMinRows && routes * c->I * 2 <= INT32_MAX &&
+                static_cast<int64_t>(c->Tmax) * c->H * 2 <= INT32_MAX;
+  c->max_dense = c->dense_ok ? static_cast<int>(routes / oled::kDenseRows) + c->E + 1 : 0;
+  c->host_pool = static_cast<const char*>(cfg->host_pool);
+  c->P = cfg->host_pool_blocks;
+  c->host_block_of.assign(cfg->host_block_of, cfg->host_block_of + nb);
+
+  auto oom = [&](const char* what) {
+    (void)hipGetLastError();
+    g_create_error = std::string("device allocation failed: ") + what;
+    free_ctx(c);
+    return OLED_ERR_OUT_OF_MEMORY;
+  };
+  if (hipMalloc(reinterpret_cast<void**>(&c->d_pool), static_cast<size_t>(c->n_slots) * c->eb) !=
+      hipSuccess)
+    return oom("slot pool");
+  if (dev_alloc(&c->d_topk, routes) || dev_alloc(&c->d_gates, routes) ||
+      dev_alloc(&c->d_counts, c->E) || dev_alloc(&c->d_offsets, c->E + 1) ||
+      dev_alloc(&c->d_perm, routes) || dev_alloc(&c->d_inv, routes) || dev_alloc(&c->d_flag, 1) ||
+      dev_alloc(&c->d_item_counts, 2) || dev_alloc(&c->d_sync, 2) ||
+      dev_alloc(&c->d_chunk, static_cast<size_t>(oled::permute_chunks(c->Tmax)) * c->E) ||
+      dev_alloc(&c->d_pcount, 1) || dev_alloc(&c->d_sacc, c->E) || dev_alloc(&c->d_ssync, 2) ||
+      dev_alloc(&c->d_items, c->max_items) ||
+      (c->dense_ok && (dev_alloc(&c->d_dense_items, c->max_dense) ||
+                       dev_alloc(&c->d_dense_counts, 2))) ||
+      dev_alloc(reinterpret_cast<char**>(&c->d_h), routes * c->I * c->esz) ||
+      dev_alloc(&c->d_O, routes * c->H) ||
+      dev_alloc(&c->d_score, static_cast<size_t>(c->L) * c->E))
+    return oom("routing scratch");
+  if (dev_alloc(&c->d_hdr, 1) || dev_alloc(&c->d_slot_of, nb) || dev_alloc(&c->d_res, c->L) ||
+      dev_alloc(&c->d_res_before, c->L) ||
+      dev_alloc(&c->d_last_counts, oled::kCountsPerLayer * c->L) ||
+      dev_alloc(&c->d_iters, c->L) || dev_alloc(&c->d_last_use, nb) || dev_alloc(&c->d_freq, nb) ||
+      dev_alloc(&c->d_prev_miss, c->L) || dev_alloc(&c->d_key, nb) ||
+      dev_alloc(&c->d_free, c->n_slots) || dev_alloc(&c->d_host_addr, nb) ||
+      dev_alloc(&c->d_cap, c->L) || dev_alloc(&c->d_stat, c->L))
+    return oom("cache state");
+  if (hipMemset(c->d_flag, 0, sizeof(int32_t)) != hipSuccess ||
+      hipMemset(c->d_item_counts, 0, 2 * sizeof(int32_t)) != hipSuccess ||
+      hipMemset(c->d_sync, 0, 2 * sizeof(int32_t)) != hipSuccess ||
+      hipMemset(c->d_pcount, 0, sizeof(int32_t)) != hipSuccess ||
+      hipMemset(c->d_sacc, 0, sizeof(unsigned long long) * c->E) != hipSuccess ||
+      hipMemset(c->d_ssync, 0, 2 * sizeof(int32_t)) != hipSuccess)
+    return oom("scratch init");
+  {
+    std::vector<uint64_t> addr(nb);
+    for (int64_t i = 0; i < nb; ++i)
+      addr[i] = reinterpret_cast<uint64_t>(dev_view) +
+                static_cast<uint64_t>(c->host_block_of[i]) * static_cast<uint64_t>(c->eb);
+    if (hipMemcpy(c->d_host_addr, addr.data(), sizeof(uint64_t) * nb, hipMemcpyHostToDevice) !=
+        hipSuccess)
+      return oom("host block table");
+  }
+  if (hipHostMalloc(reinterpret_cast<void**>(&c->h_ring), sizeof(RouteStats) * oled::kStatsRing,
+                    hipHostMallocDefault) ||
+      hipHostMalloc(reinterpret_cast<void**>(&c->h_staged), sizeof(StagedList), hipHostMallocCoherent) ||
+      hipHostMalloc(reinterpret_cast<void**>(&c->h_ret), sizeof(RetainOut) * c->L, hipHostMallocDefault))
+    return oom("pinned records");
+  if (dev_alloc(&c->d_ring, oled::kStatsRing) || dev_alloc(&c->d_ret, c->L) ||
+      hipMemset(c->d_ring, 0, sizeof(RouteStats) * oled::kStatsRing) != hipSuccess ||
+      hipMemset(c->d_ret, 0, sizeof(RetainOut) * c->L) != hipSuccess)
+    return oom("record rings");
+  std::memset(c->h_ring, 0, sizeof(RouteStats) * oled::kStatsRing);
+  std::memset(c->h_staged, 0, sizeof(StagedList));
+  std::memset(c->h_ret, 0, sizeof(RetainOut) * c->L);
+  if (hipStreamCreateWithFlags(&c->own_copy, hipStreamNonBlocking) != hipSuccess ||
+      hipEventCreateWithFlags(&c->ev_up, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&c->ev_down, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&c->ev_order, hipEventDisableTiming) != hipSuccess) {
+    g_create_error = "stream/event creation failed";
+    free_ctx(c);
+    return OLED_ERR_HIP;
+  }
+  if (c->coop) {
+    const size_t rmax = static_cast<size_t>(routes);
+    if (dev_alloc(&c->d_cpu, c->L) ||
+        hipHostMalloc(reinterpret_cast<void**>(&c->h_ctopk), rmax * 4, hipHostMallocDefault) ||
+        hipHostMalloc(reinterpret_cast<void**>(&c->h_cgates), rmax * 4, hipHostMallocDefault) ||
+        hipHostMalloc(reinterpret_cast<void**>(&c->h_cconf), static_cast<size_t>(c->Tmax) * 4,
+                      hipHostMallocDefault) ||
+        hipHostMalloc(reinterpret_cast<void**>(&c->h_cx),
+                      static_cast<size_t>(c->Tmax) * c->H * c->esz, hipHostMallocDefault) ||
+        hipHostMalloc(reinterpret_cast<void**>(&c->h_cout[0]), rmax * c->H * 4,
+                      hipHostMallocDefault) ||
+        hipHostMalloc(reinterpret_cast<void**>(&c->h_cout[1]), rmax * c->H * 4,
+                      hipHostMallocDefault))
+      return oom("cooperative compensation buffers");
+    if (hipEventCreateWithFlags(&c->ev_coop, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&c->ev_cout[0], hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&c->ev_cout[1], hipEventDisableTiming) != hipSuccess) {
+      g_create_error = "coop event creation failed";
+      free_ctx(c);
+      return OLED_ERR_HIP;
+    }
+    c->pool.reset(new oled::ThreadPool(cfg->coop_threads));
+  }
+  c->ret_seq.assign(c->L, 0);
+  c->ret_seen.assign(c->L, 0);
+  c->rejected.assign(c->L, 0);
+  if (init_cache_state(c) != OLED_OK) {
+    g_create_error = c->err;
+    free_ctx(c);
+    return OLED_ERR_HIP;
+  }
+  g_create_error.clear();
+  *ctx_out = c;
+  return OLED_OK;
+}
+
+void oled_destroy(void* ctx) { free_ctx(static_cast<Ctx*>(ctx)); }
+
+const char* oled_last_error(const void* ctx) {
+  if (!ctx) return g_create_error.c_str();
+  return static_cast<const Ctx*>(ctx)->err.c_str();
+}
+
+oled_status oled_reset_cache(void* ctx) {
+  Ctx* c = static_cast<Ctx*>(ctx);
+  if (!c) return OLED_ERR_INVALID_ARG;
+  if (c->stage != Stage::kIdle) return fail(c, OLED_ERR_STATE, "reset while a layer is in flight");
+  HIP_TRY(c, hipSetDevice(c->device));
+  HIP_TRY(c, hipDeviceSynchronize());
+  oled_status st = drain_records(c, c->route_n);
+  if (st != OLED_OK) return st;
+  st = init_cache_state(c);
+  if (st != OLED_OK) return st;
+  c->broken = false;
+  std::fill(c->ret_seq.begin(), c->ret_seq.end(), 0);
+  std::fill(c->ret_seen.begin(), c->ret_seen.end(), 0);
+  std::fill(c->rejected.begin(), c->rejected.end(), 0);
+  c->rejected_layer = -1;
+  c->bad_route_layer = -1;
+  c->reported_bad_route = 0;
+  return OLED_OK;
+}
+
+oled_status route_block(void* ctx, int32_t layer, const float* logits_dev, int32_t T, void* stream) {
+  Ctx* c = static_cast<Ctx*>(ctx);
+  if (!c) return OLED_ERR_INVALID_ARG;
+  oled_status st = check_layer(c, layer);
+  if (st != OLED_OK) return st;
+  if (c->broken)
+    return fail(c, OLED_ERR_STATE, "an earlier HIP failure left the cache state unknown: "
+                                   "call oled_reset_cache");
+  if (c->stage != Stage::kIdle)
+    return fail(c, OLED_ERR_STATE, "route_block while layer %d is in flight", c->cur_layer);
+  if (!logits_dev) return fail(c, OLED_ERR_INVALID_ARG, "NULL logits");
+  if (T < 1 || T > c->Tmax) return fail(c, OLED_ERR_INVALID_ARG, "T=%d outside [1,%d]", T, c->Tmax);
+  HIP_TRY(c, hipSetDevice(c->device));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (c->have_stream && s != c->cur_stream) {  // order the new stream after the old one
+    HIP_TRY(c, hipEventRecord(c->ev_order, c->cur_stream));
+    HIP_TRY(c, hipStreamWaitEvent(s, c->ev_order, 0));
+  }
+  // consume what has been published; this call's ring entry must be free
+  const int n = c->route_n + 1;
+  st = drain_records(c, n - oled::kStatsRing, false);
+  if (st != OLED_OK) return st;
+
+  PermuteOut o;
+  o.counts = c->d_counts;
+  o.offsets = c->d_offsets;
+  o.perm = c->d_perm;
+  o.inv_perm = c->d_inv;
+  o.items = c->d_items;
+  o.item_counts = c->d_item_counts;
+  // experts with many rows go to the dense-tile GEMM; a token picks an expert
+  // at most once, so no expert of a block of fewer tokens can have that many
+  o.dense_min = c->dense_ok && T >= oled::kDenseMinRows ? oled::kDenseMinRows : 0;
+  o.dense_items = c->d_dense_items;
+  o.dense_counts = c->d_dense_counts;
+  o.ring = c->d_ring;
+  o.staged = (c->copy_mode == OLED_COPY_SDMA || c->coop) ? c->h_staged : nullptr;
+  o.layer = layer;
+  o.E = c->E;
+  o.seq = n;
+  o.cv = view(c);
+  const int64_t route_bytes = static_cast<int64_t>(T) * c->E * 4 + static_cast<int64_t>(T) * c->K * 8;
+  const int64_t perm_bytes = static_cast<int64_t>(T) * c->K * 12 + static_cast<int64_t>(c->E) * 8;
+  if (oled::route_fused(T, c->K)) {
+    OpEvents ev = op_begin(c, OLED_OP_ROUTE_TOPK);
+    HIP_TRY(c, oled::launch_route_fused(logits_dev, T, c->K, c->d_topk, c->d_gates, c->d_sync, o,
+                                        ev.a, ev.b, s));
+    op_end(c, ev, rec(OLED_OP_ROUTE_TOPK, layer, route_bytes + perm_bytes));
+  } else {
+    {
+      OpEvents ev = op_begin(c, OLED_OP_ROUTE_TOPK);
+      HIP_TRY(c, oled::launch_route_topk(logits_dev, T, c->E, c->K, c->d_topk, c->d_gates,
+                                         c->d_flag, ev.a, ev.b, s));
+      op_end(c, ev, rec(OLED_OP_ROUTE_TOPK, layer, route_bytes));
+    }
+    OpEvents ev = op_begin(c, OLED_OP_PERMUTE);
+    if (oled::permute_chunked(T))
+      HIP_TRY(c, oled::launch_permute_chunked(c->d_topk, T, c->K, c->d_flag, c->d_chunk,
+                                              c->d_pcount, o, ev.a, ev.b, s));
+    else
+      HIP_TRY(c, oled::launch_permute(c->d_topk, T, c->K, c->d_flag, o, ev.a, ev.b, s));
+    op_end(c, ev, rec(OLED_OP_PERMUTE, layer, perm_bytes));
+  }
+  c->route_n = n;
+  c->cur_route = n;
+  c->stage = Stage::kRouted;
+  c->cur_layer = layer;
+  c->cur_T = T;
+  c->cur_dense = o.dense_min > 0;
+  c->cur_stream = s;
+  c->have_stream = true;
+  c->fwd_x = nullptr;
+  c->fwd_y = nullptr;
+  c->last_routed_layer = layer;
+  c->last_routed_T = T;
+  return OLED_OK;
+}
+
+oled_status moe_forward_cached(void* ctx, int32_t layer, const void* x_dev, void* y_dev, void* stream) {
+  Ctx* c = static_cast<Ctx*>(ctx);
+  if (!c) return OLED_ERR_INVALID_ARG;
+  oled_status st = check_layer(c, layer);
+  if (st != OLED_OK) return st;
+  if (c->stage != Stage::kRouted)
+    return fail(c, OLED_ERR_STATE, "moe_forward_cached must follow route_block");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  st = check_in_flight(c, layer, s, "moe_forward_cached");
+  if (st != OLED_OK) return st;
+  if (!x_dev || !y_dev) return fail(c, OLED_ERR_INVALID_ARG, "NULL x or y");
+  HIP_TRY(c, hipSetDevice(c->device));
+  c->fwd_x = x_dev;
+  c->fwd_y = y_dev;
+  c->stage = Stage::kHitsQueued;
+  if (c->coop) {  // the launches wait for the dispatch in apply_misses_coop
+    c->deferred = true;
+    return OLED_OK;
+  }
+  st = launch_hits(c, layer, s, -1);
+  if (st != OLED_OK) c->stage = Stage::kRouted;
+  return st;
+}
+
+
 oled_status apply_misses(void* ctx, int32_t layer, void* copy_stream, oled_miss_report* out) {
   Ctx* c = static_cast<Ctx*>(ctx);
   if (!c) return OLED_ERR_INVALID_ARG;
   oled_status st = check_layer(c, layer);
   if (st != OLED_OK) return st;
+  if (c->coop) return fail(c, OLED_ERR_STATE, "a coop context compensates with apply_misses_coop");
   if (c->stage != Stage::kRouted && c->stage != Stage::kHitsQueued)
     return fail(c, OLED_ERR_STATE, "apply_misses must follow route_block or moe_forward_cached");
   if (layer != c->cur_layer)
@@ -1068,45 +1270,8 @@ oled_status apply_misses(void* ctx, int32_t layer, void* copy_stream, oled_miss_
   int64_t bytes = 0;
   if (shader) {
     if (c->stage == Stage::kHitsQueued) {
-      // one launch: the hits' down GEMM + the transfer of the misses' down
-      // weights + the misses' gate/up GEMM (their gate/up weights landed in
-      // the previous launch); then the misses' down GEMM. Miss items are
-      // bounded by the staging capacity; their count is on the device.
-      const int64_t routes = static_cast<int64_t>(c->cur_T) * c->K;
-      const int max_hit_items =
-          c->cap > 0 ? static_cast<int>(std::min<int64_t>(c->cap, routes) + routes / oled::kItemRows)
-                     : 0;
-      const int max_miss_items =
-          static_cast<int>(std::min<int64_t>(c->E, routes) + routes / oled::kItemRows);
-      FfnLaunch d = ffn_args(c, layer, 0, max_hit_items, 0);
-      d.src = c->d_h;
-      d.fetch.nblk = kFetchBlocks;
-      d.fetch.off = c->e13;
-      d.fetch.len = c->eb - c->e13;
-      FfnLaunch u = ffn_args(c, layer, 1, max_miss_items, kMissGridCap);
-      u.src = c->fwd_x;
-      {
-        OpEvents ev = op_begin(c, OLED_OP_FFN_DOWN);
-        HIP_TRY(c, oled::launch_ffn_mix(bf16, d, u, ev.a, ev.b, s));
-        OpRec o = rec(OLED_OP_FFN_DOWN, layer, -1);
-        o.route_seq = c->cur_route;
-        o.part = 2;
-        op_end(c, ev, o);
-      }
-      FfnLaunch a = ffn_args(c, layer, 1, max_miss_items, kMissGridCap);
-      a.src = c->d_h;
-      {
-        OpEvents ev = op_begin(c, OLED_OP_FFN_DOWN);
-        HIP_TRY(c, oled::launch_ffn_down(bf16, a, ev.a, ev.b, s));
-        OpRec o = rec(OLED_OP_FFN_DOWN, layer, -1);
-        o.route_seq = c->cur_route;
-        o.part = 1;
-        op_end(c, ev, o);
-      }
-      if (c->cur_dense) {
-        st = launch_dense(c, layer, s);
-        if (st != OLED_OK) return st;
-      }
+      st = launch_shader_rest(c, layer, s, -1);
+      if (st != OLED_OK) return st;
     } else {
       // control path: transfer the whole blocks of the staged misses
       FetchArgs f;
@@ -1137,11 +1302,187 @@ oled_status apply_misses(void* ctx, int32_t layer, void* copy_stream, oled_miss_
     out->n_misses = r.n_misses;
     out->n_resident = r.n_resident;
     out->rejected_layer = c->rejected_layer;
-    out->reserved = 0;
+    out->n_cpu = 0;
     out->h2d_bytes = bytes;
     c->rejected_layer = -1;
   }
   c->stage = Stage::kApplied;
+  return OLED_OK;
+}
+
+oled_status apply_misses_coop(void* ctx, int32_t layer, const float* conf_dev,
+                              oled_miss_report* out) {
+  Ctx* c = static_cast<Ctx*>(ctx);
+  if (!c) return OLED_ERR_INVALID_ARG;
+  oled_status st = check_layer(c, layer);
+  if (st != OLED_OK) return st;
+  if (!c->coop) return fail(c, OLED_ERR_STATE, "apply_misses_coop needs a context with coop = 1");
+  if (c->stage != Stage::kRouted && c->stage != Stage::kHitsQueued)
+    return fail(c, OLED_ERR_STATE, "apply_misses_coop must follow route_block or moe_forward_cached");
+  if (layer != c->cur_layer)
+    return fail(c, OLED_ERR_STATE, "apply_misses_coop: layer %d is not the layer in flight (%d)",
+                layer, c->cur_layer);
+  if (!conf_dev) return fail(c, OLED_ERR_INVALID_ARG, "NULL confidence");
+  HIP_TRY(c, hipSetDevice(c->device));
+  hipStream_t s = c->cur_stream;
+  st = wait_published(c, &c->h_staged->seq, c->cur_route, s, "staged misses");
+  if (st != OLED_OK) {
+    c->stage = Stage::kIdle;
+    return st;
+  }
+  const RouteStats r = c->h_staged->rec;
+  if (r.bad) {
+    c->reported_bad_route = c->cur_route;
+    if (c->bad_route_layer == layer) c->bad_route_layer = -1;
+    c->stage = Stage::kIdle;
+    return fail(c, OLED_ERR_INVALID_ARG,
+                "bad block at layer %d (non-finite router logit): nothing staged, cache "
+                "unchanged", layer);
+  }
+  const int n = r.n_staged, E = c->E, T = c->cur_T, k = c->K;
+  if (n < 0 || n > E) return fail(c, OLED_ERR_HIP, "staged list out of range");
+  const bool fwd = c->stage == Stage::kHitsQueued;
+  std::vector<uint8_t> cpu(E, 0);
+  std::vector<int32_t> cnt(E, 0);
+  int n_cpu = 0;
+  if (n > 0) {
+    // the layer's routing, confidence and inputs to the host
+    const size_t R = static_cast<size_t>(T) * k;
+    HIP_TRY(c, hipMemcpyAsync(c->h_ctopk, c->d_topk, R * 4, hipMemcpyDeviceToHost, s));
+    HIP_TRY(c, hipMemcpyAsync(c->h_cgates, c->d_gates, R * 4, hipMemcpyDeviceToHost, s));
+    HIP_TRY(c, hipMemcpyAsync(c->h_cconf, conf_dev, static_cast<size_t>(T) * 4,
+                              hipMemcpyDeviceToHost, s));
+    if (fwd)
+      HIP_TRY(c, hipMemcpyAsync(c->h_cx, c->fwd_x, static_cast<size_t>(T) * c->H * c->esz,
+                                hipMemcpyDeviceToHost, s));
+    HIP_TRY(c, hipEventRecord(c->ev_coop, s));
+    st = wait_event_spin(c, c->ev_coop, "routing copy");
+    if (st != OLED_OK) return st;
+    // routes per expert and priority numerators, as the retention computes them
+    std::vector<uint64_t> S(E, 0);
+    for (size_t q = 0; q < R; ++q) {
+      const int e = c->h_ctopk[q];
+      if (e < 0 || e >= E) return fail(c, OLED_ERR_HIP, "routing copy out of range");
+      ++cnt[e];
+      const float cf = c->h_cconf[q / k];
+      if (cf >= 0.f && cf <= 1.f)
+        S[e] += static_cast<uint64_t>(
+            std::floor(static_cast<double>(c->h_cgates[q]) * static_cast<double>(cf) * 0x1p48));
+    }
+    std::vector<uint8_t> miss(E, 0), transfer(E, 0);
+    for (int j = 0; j < n; ++j) {
+      const int e = c->h_staged->exp[j];
+      if (e < 0 || e >= E) return fail(c, OLED_ERR_HIP, "staged list out of range");
+      miss[e] = 1;
+    }
+    coop_dispatch(E, miss.data(), cnt.data(), S.data(), c->coop_t, c->coop_tau, c->coop_nbar,
+                  c->coop_lambda, transfer.data());
+    for (int e = 0; e < E; ++e) {
+      cpu[e] = miss[e] && !transfer[e];
+      n_cpu += cpu[e];
+    }
+  }
+  ExpertMask cm;
+  std::memset(&cm, 0, sizeof(cm));
+  for (int e = 0; e < E; ++e)
+    if (cpu[e]) cm.bits[e >> 5] |= 1u << (e & 31);
+  if (n_cpu > 0) HIP_TRY(c, oled::launch_coop_unstage(view(c), layer, E, cm, s));
+  const int64_t g_bytes = static_cast<int64_t>(n - n_cpu) * c->eb;
+  if (fwd) {  // the hits, and the transferred misses through the shader transfer
+    st = launch_hits(c, layer, s, g_bytes);
+    if (st == OLED_OK) st = launch_shader_rest(c, layer, s, g_bytes);
+    if (st != OLED_OK) return st;
+    c->deferred = false;
+  } else if (n - n_cpu > 0) {  // control path: whole blocks of the transferred misses
+    FetchArgs f;
+    f.host_addr = c->d_host_addr + static_cast<size_t>(layer) * E;
+    f.hdr = c->d_hdr;
+    f.off = 0;
+    f.len = c->eb;
+    f.nblk = kFetchBlocks;
+    f.E = E;
+    OpEvents ev = op_begin(c, OLED_OP_H2D);
+    HIP_TRY(c, oled::launch_fetch(c->d_pool, c->eb, c->n_slots, f, ev.a, ev.b, s));
+    OpRec o = rec(OLED_OP_H2D, layer, g_bytes);
+    o.h2d = g_bytes;
+    op_end(c, ev, o);
+  }
+  if (fwd && n_cpu > 0) {
+    // the CPU experts' rows, in the expert-sorted route order (offsets of the
+    // stable permutation: an expert's routes in token order)
+    std::vector<int32_t> off(E + 1, 0);
+    for (int e = 0; e < E; ++e) off[e + 1] = off[e] + cnt[e];
+    std::vector<std::vector<int32_t>> toks(E);
+    const size_t R = static_cast<size_t>(T) * k;
+    for (size_t q = 0; q < R; ++q)
+      if (cpu[c->h_ctopk[q]]) toks[c->h_ctopk[q]].push_back(static_cast<int32_t>(q / k));
+    const int b = c->cout_buf;
+    if (c->cout_used[b]) {  // its previous rows have been copied out
+      st = wait_event_spin(c, c->ev_cout[b], "CPU output copy");
+      if (st != OLED_OK) return st;
+    }
+    float* hout = c->h_cout[b];
+    std::vector<oled::CpuExpertJob> jobs;
+    for (int e = 0; e < E; ++e) {
+      if (!cpu[e]) continue;
+      const int64_t blk = c->host_block_of[static_cast<size_t>(layer) * E + e];
+      jobs.push_back({c->host_pool + blk * c->eb, toks[e].data(), cnt[e],
+                      hout + static_cast<size_t>(off[e]) * c->H});
+    }
+    oled::cpu_ffn_run(*c->pool, c->dtype == OLED_BF16, c->H, c->I, c->h_cx, jobs.data(),
+                      static_cast<int>(jobs.size()), c->cpu_scratch);
+    for (int e = 0; e < E; ++e) {
+      if (!cpu[e]) continue;
+      const size_t o0 = static_cast<size_t>(off[e]) * c->H;
+      HIP_TRY(c, hipMemcpyAsync(c->d_O + o0, hout + o0, static_cast<size_t>(cnt[e]) * c->H * 4,
+                                hipMemcpyHostToDevice, s));
+    }
+    HIP_TRY(c, hipEventRecord(c->ev_cout[b], s));
+    c->cout_used[b] = true;
+    c->cout_buf = b ^ 1;
+  }
+  c->acc.n_cpu_executed += n_cpu;
+  c->acc.n_transferred -= n_cpu;
+  c->acc.h2d_bytes -= static_cast<int64_t>(n_cpu) * c->eb;
+  if (out) {
+    out->n_active = r.n_active;
+    out->n_hits = r.n_hits;
+    out->n_misses = r.n_misses;
+    out->n_resident = r.n_resident;
+    out->rejected_layer = c->rejected_layer;
+    out->n_cpu = n_cpu;
+    out->h2d_bytes = g_bytes;
+    c->rejected_layer = -1;
+  }
+  c->stage = Stage::kApplied;
+  return OLED_OK;
+}
+
+oled_status oled_coop_dispatch(int32_t n_experts, const uint8_t* miss, const int32_t* n_tok,
+                               const uint64_t* score, double t_h2d_us, double tau_cpu_us,
+                               double nbar, double lambda_us, uint8_t* transfer_out) {
+  if (!miss || !n_tok || !score || !transfer_out) return OLED_ERR_INVALID_ARG;
+  if (n_experts < 1 || n_experts > oled::kMaxExperts) return OLED_ERR_INVALID_ARG;
+  if (!(t_h2d_us >= 0.0) || !(tau_cpu_us >= 0.0) || !(nbar >= 0.0) || !(lambda_us >= 0.0))
+    return OLED_ERR_INVALID_ARG;
+  coop_dispatch(n_experts, miss, n_tok, score, t_h2d_us, tau_cpu_us, nbar, lambda_us,
+                transfer_out);
+  return OLED_OK;
+}
+
+oled_status oled_cpu_ffn(int32_t dtype, int32_t hidden, int32_t inter, const void* block,
+                         const void* x, int32_t n, float* out, int32_t threads) {
+  if (!block || !x || !out || n < 0 || threads < 1) return OLED_ERR_INVALID_ARG;
+  if (dtype != OLED_F32 && dtype != OLED_BF16) return OLED_ERR_INVALID_ARG;
+  if (hidden <= 0 || inter <= 0 || hidden % 128 || inter % 128) return OLED_ERR_UNSUPPORTED;
+  if (!oled::cpu_ffn_supported()) return OLED_ERR_UNSUPPORTED;
+  if (n == 0) return OLED_OK;
+  std::vector<int32_t> rows(n);
+  for (int i = 0; i < n; ++i) rows[i] = i;
+  oled::CpuExpertJob job{block, rows.data(), n, out};
+  oled::ThreadPool pool(threads);
+  std::vector<float> scratch;
+  oled::cpu_ffn_run(pool, dtype == OLED_BF16, hidden, inter, x, &job, 1, scratch);
   return OLED_OK;
 }
 

@@ -84,15 +84,21 @@ __device__ __forceinline__ void score_commit(const ScoreArgs& a, unsigned long l
   __shared__ uint32_t s_rc[kMaxExperts];  // bit 1: previously resident, bit 0: candidate
   __shared__ int32_t s_rank[kMaxExperts];
   __shared__ uint32_t s_res[kMaxExperts / 32];
+  __shared__ uint32_t s_cpu[kMaxExperts / 32];   // CPU-executed misses: no candidates
   const int tid = threadIdx.x;
-  if (tid < kMaxExperts / 32) s_res[tid] = cv.res[layer].bits[tid];
+  if (tid < kMaxExperts / 32) {
+    s_res[tid] = cv.res[layer].bits[tid];
+    s_cpu[tid] = cv.cpu_exec ? cv.cpu_exec[layer].bits[tid] : 0u;
+  }
   __syncthreads();
   for (int e = tid; e < kMaxExperts; e += kThreads) {
     s_rank[e] = 0;
     const bool r = e < E && ((s_res[e >> 5] >> (e & 31)) & 1u);
-    const bool c = e < E && (r || counts[e] > 0);
+    const bool cpu = e < E && ((s_cpu[e >> 5] >> (e & 31)) & 1u);
+    const bool c = e < E && (r || (counts[e] > 0 && !cpu));
     s_rc[e] = (r ? 2u : 0u) | (c ? 1u : 0u);
   }
+  // (s_rc and s_rank are next read after the barrier that follows the keys)
   const int s_bad = *p_bad;
   CacheHdr* hdr = cv.hdr;
   const bool commit = !s_bad && !hdr->route_bad;
@@ -192,6 +198,7 @@ __device__ __forceinline__ void score_commit(const ScoreArgs& a, unsigned long l
   if (lane < kMaxExperts / 32) {
     cv.res[layer].bits[lane] = my_word;
     out->retained[lane] = my_word;
+    if (cv.cpu_exec) cv.cpu_exec[layer].bits[lane] = 0u;
   }
   if (lane == 0) {
     hdr->free_top = top;
@@ -456,7 +463,43 @@ __global__ __launch_bounds__(kThreads) void k_layer_adapt(AdaptArgs a) {
   }
 }
 
+// See launch_coop_unstage. One thread walks the staged list in order.
+__global__ __launch_bounds__(64) void k_coop_unstage(CacheView cv, int layer, int E,
+                                                     ExpertMask cpu) {
+  if (threadIdx.x != 0) return;
+  CacheHdr* hdr = cv.hdr;
+  int32_t* slot_row = cv.slot_of + static_cast<size_t>(layer) * E;
+  int top = hdr->free_top;
+  const int n = min(hdr->staged_n, kMaxExperts);
+  int m = 0;
+  for (int j = 0; j < n; ++j) {
+    const int e = hdr->staged_exp[j], sl = hdr->staged_slot[j];
+    if (e >= 0 && e < E && cpu.test(e)) {
+      if (sl >= 0 && sl < cv.n_slots && top < cv.n_slots) cv.free_list[top++] = sl;
+      else hdr->fault |= 2;
+      slot_row[e] = -1;
+    } else {
+      hdr->staged_exp[m] = e;
+      hdr->staged_slot[m] = sl;
+      ++m;
+    }
+  }
+  hdr->staged_n = m;
+  hdr->free_top = top;
+  for (int w = 0; w < kMaxExperts / 32; ++w) {
+    cv.prev_miss[layer].bits[w] &= ~cpu.bits[w];
+    cv.cpu_exec[layer].bits[w] = cpu.bits[w];
+  }
+}
+
 }  // namespace
+
+hipError_t launch_coop_unstage(const CacheView& cv, int layer, int E, const ExpertMask& cpu,
+                               hipStream_t s) {
+  if (!cv.cpu_exec) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_coop_unstage, dim3(1), dim3(64), 0, s, cv, layer, E, cpu);
+  return hipGetLastError();
+}
 
 hipError_t launch_layer_adapt(const AdaptArgs& a, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
   if (a.L <= 0 || a.L > kMaxAdaptLayers) return hipErrorInvalidValue;

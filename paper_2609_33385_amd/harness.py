@@ -28,14 +28,15 @@ def fill_pool(w: W.Workload, seed: int, n_blocks: int) -> oled.PinnedPool:
 def make_context(w: W.Workload, pool: oled.PinnedPool, capacity: int | None = None,
                  n_layers: int | None = None, max_tokens: int | None = None,
                  profile_ops: int = 0, copy_mode: str = "shader",
-                 adapt_period: int = 0, policy: str = "priority") -> oled.Context:
+                 adapt_period: int = 0, policy: str = "priority",
+                 coop: dict | None = None) -> oled.Context:
     L = n_layers if n_layers is not None else w.n_layers
     return oled.Context(w.hidden, w.inter, w.n_experts, w.top_k, L,
                         w.capacity if capacity is None else capacity,
                         max_tokens if max_tokens is not None else w.tokens, w.dtype,
                         pool.ptr, pool.n_blocks,
                         W.host_block_of(w.replace(n_layers=L), pool.n_blocks), profile_ops=profile_ops,
-                        copy_mode=copy_mode, adapt_period=adapt_period, policy=policy)
+                        copy_mode=copy_mode, adapt_period=adapt_period, policy=policy, coop=coop)
 
 
 def torch_dtype(w: W.Workload):
@@ -68,6 +69,9 @@ def layer_step(ctx: oled.Context, layer: int, logits: torch.Tensor, conf: torch.
     ctx.route_block(layer, logits, T, s)
     if x is not None:
         ctx.moe_forward_cached(layer, x, y, s)
-    rep = ctx.apply_misses(layer, report=report)
+    if getattr(ctx, "coop", False):
+        rep = ctx.apply_misses_coop(layer, conf, report=report)
+    else:
+        rep = ctx.apply_misses(layer, report=report)
     ctx.score_and_retain(layer, conf, s)
     return rep

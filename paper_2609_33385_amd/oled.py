@@ -49,9 +49,10 @@ def profile_mask(*names) -> int:
     return m
 
 EXPORTED = ["oled_create", "oled_destroy", "oled_last_error", "oled_reset_cache", "route_block",
-            "apply_misses", "moe_forward_cached", "score_and_retain", "oled_read_layer_state",
-            "oled_collect_stats", "oled_profile_collect", "oled_pack_expert", "oled_host_alloc",
-            "oled_host_free"]
+            "apply_misses", "apply_misses_coop", "moe_forward_cached", "score_and_retain",
+            "oled_read_layer_state", "oled_collect_stats", "oled_profile_collect",
+            "oled_pack_expert", "oled_host_alloc", "oled_host_free", "oled_coop_dispatch",
+            "oled_cpu_ffn"]
 
 
 class OledConfig(ctypes.Structure):
@@ -63,13 +64,16 @@ class OledConfig(ctypes.Structure):
                 ("host_pool", ctypes.c_void_p), ("host_pool_blocks", ctypes.c_int64),
                 ("host_block_of", ctypes.POINTER(ctypes.c_int64)),
                 ("copy_mode", ctypes.c_int32), ("adapt_period", ctypes.c_int32),
-                ("policy", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("policy", ctypes.c_int32), ("coop", ctypes.c_int32),
+                ("coop_threads", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("coop_t_h2d_us", ctypes.c_double), ("coop_tau_cpu_us", ctypes.c_double),
+                ("coop_nbar", ctypes.c_double), ("coop_lambda_us", ctypes.c_double)]
 
 
 class MissReport(ctypes.Structure):
     _fields_ = [("n_active", ctypes.c_int32), ("n_hits", ctypes.c_int32),
                 ("n_misses", ctypes.c_int32), ("n_resident", ctypes.c_int32),
-                ("rejected_layer", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("rejected_layer", ctypes.c_int32), ("n_cpu", ctypes.c_int32),
                 ("h2d_bytes", ctypes.c_int64)]
 
 
@@ -78,7 +82,8 @@ class Stats(ctypes.Structure):
                 ("n_hits", ctypes.c_int64), ("n_misses", ctypes.c_int64),
                 ("n_transferred", ctypes.c_int64), ("h2d_bytes", ctypes.c_int64),
                 ("n_bad_blocks", ctypes.c_int64), ("n_prev_transferred", ctypes.c_int64),
-                ("n_transfers_reused", ctypes.c_int64), ("n_ideal_hits", ctypes.c_int64)]
+                ("n_transfers_reused", ctypes.c_int64), ("n_ideal_hits", ctypes.c_int64),
+                ("n_cpu_executed", ctypes.c_int64)]
 
     def as_dict(self) -> dict:
         return {name: getattr(self, name) for name, _ in self._fields_}
@@ -128,6 +133,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "oled_reset_cache": (i32, [vp]),
         "route_block": (i32, [vp, i32, vp, i32, vp]),
         "apply_misses": (i32, [vp, i32, vp, ctypes.POINTER(MissReport)]),
+        "apply_misses_coop": (i32, [vp, i32, vp, ctypes.POINTER(MissReport)]),
+        "oled_coop_dispatch": (i32, [i32, vp, vp, vp, ctypes.c_double, ctypes.c_double,
+                                     ctypes.c_double, ctypes.c_double, vp]),
+        "oled_cpu_ffn": (i32, [i32, i32, i32, vp, vp, i32, vp, i32]),
         "moe_forward_cached": (i32, [vp, i32, vp, vp, vp]),
         "score_and_retain": (i32, [vp, i32, vp, vp]),
         "oled_read_layer_state": (i32, [vp, i32, ctypes.POINTER(LayerState)]),
@@ -200,6 +209,41 @@ def route_block(ctx, layer: int, logits, T: int, stream=None) -> int:
 def apply_misses(ctx, layer: int, copy_stream=None, report: MissReport | None = None) -> int:
     return load().apply_misses(ctx, layer, _stream(copy_stream),
                                ctypes.byref(report) if report is not None else None)
+
+
+def apply_misses_coop(ctx, layer: int, conf, report: MissReport | None = None) -> int:
+    return load().apply_misses_coop(ctx, layer, _ptr(conf),
+                                    ctypes.byref(report) if report is not None else None)
+
+
+def oled_coop_dispatch(miss: np.ndarray, n_tok: np.ndarray, score: np.ndarray, t_h2d_us: float,
+                       tau_cpu_us: float, nbar: float, lambda_us: float) -> np.ndarray:
+    """The library's dispatch of the misses (transfer mask, bool [E])."""
+    miss = np.ascontiguousarray(miss, dtype=np.uint8)
+    n_tok = np.ascontiguousarray(n_tok, dtype=np.int32)
+    score = np.ascontiguousarray(score, dtype=np.uint64)
+    out = np.zeros(miss.size, np.uint8)
+    st = load().oled_coop_dispatch(miss.size, miss.ctypes.data, n_tok.ctypes.data,
+                                   score.ctypes.data, t_h2d_us, tau_cpu_us, nbar, lambda_us,
+                                   out.ctypes.data)
+    if st != OLED_OK:
+        raise OledError(st, "oled_coop_dispatch")
+    return out.astype(bool)
+
+
+def oled_cpu_ffn(dtype: str, hidden: int, inter: int, block: np.ndarray, x: np.ndarray,
+                 threads: int = 1) -> np.ndarray:
+    """One packed expert's SwiGLU on the host CPU: x [n][H] (float32, or bf16
+    bits) -> float32 [n][H]."""
+    block = np.ascontiguousarray(block)
+    x = np.ascontiguousarray(x)
+    n = x.shape[0]
+    out = np.zeros((n, hidden), np.float32)
+    st = load().oled_cpu_ffn(OLED_F32 if dtype == "f32" else OLED_BF16, hidden, inter,
+                             block.ctypes.data, x.ctypes.data, n, out.ctypes.data, threads)
+    if st != OLED_OK:
+        raise OledError(st, "oled_cpu_ffn")
+    return out
 
 
 def moe_forward_cached(ctx, layer: int, x, y, stream=None) -> int:
@@ -287,13 +331,21 @@ class Context:
     def __init__(self, hidden, inter, n_experts, top_k, n_layers, capacity, max_tokens,
                  dtype: str, host_pool: int, host_pool_blocks: int, host_block_of,
                  device: int = 0, profile_ops: int = 0, copy_mode: str = "shader",
-                 adapt_period: int = 0, policy: str = "priority"):
+                 adapt_period: int = 0, policy: str = "priority", coop: dict | None = None):
+        """coop: None, or dict(threads, t_h2d_us, tau_cpu_us, nbar, lambda_us) for the
+        cooperative compensation (apply_misses_coop)."""
         self._hbo = np.ascontiguousarray(host_block_of, dtype=np.int64)
         cfg = OledConfig(hidden, inter, n_experts, top_k, n_layers, capacity, max_tokens,
                          OLED_F32 if dtype == "f32" else OLED_BF16, device,
                          profile_ops, host_pool, host_pool_blocks,
                          self._hbo.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
-                         COPY_MODES[copy_mode], adapt_period, POLICIES[policy], 0)
+                         COPY_MODES[copy_mode], adapt_period, POLICIES[policy],
+                         1 if coop else 0, int(coop["threads"]) if coop else 0, 0,
+                         float(coop["t_h2d_us"]) if coop else 0.0,
+                         float(coop["tau_cpu_us"]) if coop else 0.0,
+                         float(coop["nbar"]) if coop else 0.0,
+                         float(coop["lambda_us"]) if coop else 0.0)
+        self.coop = bool(coop)
         self.E, self.k, self.L, self.C, self.Tmax = n_experts, top_k, n_layers, capacity, max_tokens
         self.ctx = oled_create(cfg)
 
@@ -318,6 +370,11 @@ class Context:
         """With report=False nothing waits for the device (shader transfer)."""
         rep = MissReport() if report else None
         _check(self.ctx, apply_misses(self.ctx, layer, copy_stream, rep))
+        return rep
+
+    def apply_misses_coop(self, layer, conf, report: bool = True) -> MissReport | None:
+        rep = MissReport() if report else None
+        _check(self.ctx, apply_misses_coop(self.ctx, layer, conf, rep))
         return rep
 
     def moe_forward_cached(self, layer, x, y, stream=None):

@@ -1,0 +1,96 @@
+"""GPU parity of the cooperative compensation (Sec. 4.4) against the oracle:
+the misses of every layer-iteration are split between transfer and CPU
+execution exactly as the oracle's two-stage dispatch splits them, only the
+transferred ones become retention candidates (resident sets bit for bit),
+and the layer outputs, with the CPU experts' rows computed on the host,
+match the oracle within the dtype's bound."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import oled_oracle as O
+from paper_2609_33385_amd import harness as HN
+from paper_2609_33385_amd import oled
+from paper_2609_33385_amd import workload as W
+
+from gpu_common import OracleWeights, compare_control, rel_l2, run_schedule_gpu, tol
+
+pytestmark = pytest.mark.gpu
+
+COOP = dict(threads=4, t_h2d_us=100.0, tau_cpu_us=10.0, nbar=10.0, lambda_us=50.0)
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    oled.load()
+
+
+def _coop_chain(w, seed, C, coop, forward=True, n_blocks=16, out_at=None):
+    L = w.n_layers
+    _say(f"[coop] {w.name} L={L} iters={w.n_iters} C={C} {coop} forward={forward}")
+    ref = O.run_coop_schedule(lambda li, i: W.logits(w, seed, li, 0, i),
+                              lambda li, i: W.confidence(w, seed, 0, i), L, w.n_iters,
+                              w.n_experts, w.top_k, C, coop["t_h2d_us"], coop["tau_cpu_us"],
+                              coop["nbar"], coop["lambda_us"])
+    n_cpu_ref = sum(int(st["cpu"].sum()) for row in ref for st in row)
+    assert n_cpu_ref > 0, "the test should send some misses to the CPU"
+    pool = HN.fill_pool(w, seed, n_blocks)
+    ctx = HN.make_context(w, pool, capacity=C, coop=coop)
+    ow = OracleWeights(w, seed, n_blocks, L)
+    worst = [0.0]
+
+    def check(i, li, st, y, rep):
+        o = ref[i][li]
+        where = f"{w.name} l={li} i={i}"
+        compare_control(st, o, w.tokens, where)
+        assert rep.n_cpu == int(o["cpu"].sum()), where
+        assert rep.h2d_bytes == int(o["transfer"].sum()) * w.expert_bytes, where
+        assert (st["prev_transferred"], st["reused_transfers"]) == (
+            o["prev_transferred"], o["reused_transfers"]), where
+        if y is not None and (out_at is None or (li, i) in out_at):
+            x = O.decode(W.activations(w, seed, li, 0, i))
+            y_ref = O.moe_output(x, o["idx"], o["gates"], ow.fn(li))
+            err = rel_l2(O.decode(y), y_ref)
+            worst[0] = max(worst[0], err)
+            assert err <= tol(w), f"{where}: rel L2 {err:.3e}"
+
+    try:
+        ctx.collect_stats()
+        run_schedule_gpu(ctx, w, seed, list(range(L)), w.n_iters, forward, check)
+        stats = ctx.collect_stats()
+    finally:
+        ctx.close()
+        pool.free()
+    assert stats["n_cpu_executed"] == n_cpu_ref
+    flat = [st for row in ref for st in row]
+    assert stats["n_transferred"] == sum(int(st["transfer"].sum()) for st in flat)
+    _say(f"[coop] ok: {n_cpu_ref} CPU-executed misses, worst rel L2 {worst[0]:.3e}")
+
+
+def test_coop_bf16_stack():
+    w = W.WORKLOADS[2].replace(wid=350, name="coop-stack", n_layers=4, n_iters=6)
+    _coop_chain(w, 0, 12, COOP)
+
+
+def test_coop_tiny_f32():
+    w = W.WORKLOADS[1].replace(wid=351, name="coop-tiny", n_iters=6)
+    _coop_chain(w, 1, 2, dict(COOP, threads=2, t_h2d_us=30.0))
+
+
+def test_coop_control_path_only():
+    w = W.WORKLOADS[2].replace(wid=352, name="coop-control", n_layers=3, n_iters=5)
+    _coop_chain(w, 2, 8, dict(COOP, lambda_us=0.0), forward=False)
+
+
+def test_coop_large_block():
+    w = W.WORKLOADS[3].replace(wid=353, name="coop-b8", n_layers=2, n_iters=4, hidden=1024,
+                               inter=512)
+    _coop_chain(w, 3, 20, dict(COOP, threads=8, t_h2d_us=60.0), out_at={(0, 1), (1, 3)})

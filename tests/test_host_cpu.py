@@ -51,7 +51,8 @@ def _cfg(**kw):
                         base["n_layers"], base["capacity"], base["max_tokens"], base["dtype"],
                         base["device"], base["profile_ops"], base["host_pool"] or 0,
                         base["host_pool_blocks"],
-                        hbo.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), 0, 0, 0, 0)
+                        hbo.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), 0, 0, 0, 0, 0, 0,
+                        0.0, 0.0, 0.0, 0.0)
     return c, hbo
 
 
