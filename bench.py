@@ -94,6 +94,52 @@ def measured_traffic():
     return rec.get("traffic_bytes_per_launch")
 
 
+def profile_coop(w, pool, logits, xs, conf, args):
+    """Split constants of the cooperative compensation, profiled on this
+    machine: T_H2D (one expert block host->device), tau_CPU (CPU expert time
+    per routed token at nbar tokens) and nbar (routed tokens per missed
+    expert, from a run of the warm-up steps without CPU execution)."""
+    import torch
+    from paper_2609_33385_amd import oled
+    from paper_2609_33385_amd import workload as W
+    L, T = w.n_layers, w.tokens
+    ctx = oled.Context(w.hidden, w.inter, w.n_experts, w.top_k, L, w.capacity, T, w.dtype,
+                       pool.ptr, pool.n_blocks, W.host_block_of(w, pool.n_blocks))
+    y = torch.empty((T, w.hidden), dtype=torch.bfloat16, device="cuda")
+    s = torch.cuda.current_stream()
+    for g in range(args.warmup):
+        for l in range(L):
+            ctx.route_block(l, logits[g, l].data_ptr(), T, s)
+            ctx.moe_forward_cached(l, xs[g, l].data_ptr(), y.data_ptr(), s)
+            ctx.apply_misses(l, report=False)
+            ctx.score_and_retain(l, conf[g].data_ptr(), s)
+    st = ctx.collect_stats()
+    ctx.close()
+    nbar = st["n_miss_rows"] / max(1, st["n_misses"])
+    # T_H2D: copy of one expert block from the pinned pool
+    host = torch.from_numpy(pool.view(np.uint8)[: w.expert_bytes])
+    dev = torch.empty(w.expert_bytes, dtype=torch.uint8, device="cuda")
+    dev.copy_(host, non_blocking=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(20):
+        dev.copy_(host, non_blocking=True)
+    torch.cuda.synchronize()
+    t_h2d = (time.perf_counter() - t0) / 20 * 1e6
+    # tau_CPU: the CPU expert kernels on nbar tokens
+    n = max(1, int(round(nbar)))
+    block = pool.block(0, np.uint16)
+    x = W.activations(w.replace(batch=1, block=n), args.seed, 0, 0, 0)
+    oled.oled_cpu_ffn(w.dtype, w.hidden, w.inter, block, x, args.coop_threads)
+    t0 = time.perf_counter()
+    for _ in range(5):
+        oled.oled_cpu_ffn(w.dtype, w.hidden, w.inter, block, x, args.coop_threads)
+    tau = (time.perf_counter() - t0) / 5 * 1e6 / n
+    lam = t_h2d if args.coop_lambda is None else args.coop_lambda
+    return dict(threads=args.coop_threads, t_h2d_us=round(t_h2d, 2), tau_cpu_us=round(tau, 2),
+                nbar=round(nbar, 3), lambda_us=round(lam, 2))
+
+
 def cpu_baseline(w, seed: int):
     """The oracle on host cores: every layer of block 0, iterations 1-4, with the FFN."""
     from threadpoolctl import threadpool_info
@@ -140,9 +186,18 @@ def main():
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--capacity", type=int, default=None, help="experts cached per layer")
+    ap.add_argument("--workload", type=int, default=2, choices=[2, 3],
+                    help="2: the 40%% stack with 32 tokens per iteration (the headline); 3: the "
+                         "same stack with batch 8 x block 32 = 256 tokens per iteration")
     ap.add_argument("--adapt-period", type=int, default=0,
                     help="layer-adaptive cache sizing every N iterations (0: fixed capacity "
                          "per layer, the headline configuration)")
+    ap.add_argument("--coop", action="store_true",
+                    help="cooperative compensation (CPU execution of part of the misses); its "
+                         "split constants are profiled here before the timed steps")
+    ap.add_argument("--coop-threads", type=int, default=8)
+    ap.add_argument("--coop-lambda", type=float, default=None,
+                    help="lambda in microseconds per unit of priority (default: T_H2D)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibration", action="store_true",
                     help="between warm-up and timed steps, run a plain streaming kernel of known traffic (torch "
@@ -168,7 +223,7 @@ def main():
     from paper_2609_33385_amd import oled
     from paper_2609_33385_amd import workload as W
 
-    w = W.WORKLOADS[2]
+    w = W.WORKLOADS[args.workload]
     if args.capacity is not None:
         w = w.replace(capacity=args.capacity)
     L, T, E = w.n_layers, w.tokens, w.n_experts
@@ -182,9 +237,13 @@ def main():
     logits, xs, conf = make_inputs(w, args.seed, n_total)
     y = torch.empty((T, w.hidden), dtype=torch.bfloat16, device="cuda")
     prof = oled.profile_mask(*[o for o in args.profile_ops.split(",") if o])
+    coop = None
+    if args.coop:
+        coop = profile_coop(w, pool, logits, xs, conf, args)
+        log(f"coop split constants: {coop}")
     ctx = oled.Context(w.hidden, w.inter, E, w.top_k, L, w.capacity, T, w.dtype, pool.ptr,
                        pool.n_blocks, W.host_block_of(w, pool.n_blocks), profile_ops=prof,
-                       copy_mode=args.copy_mode, adapt_period=args.adapt_period)
+                       copy_mode=args.copy_mode, adapt_period=args.adapt_period, coop=coop)
     log(f"setup {time.time() - t0:.1f}s: pool {pool.n_blocks} x {w.expert_bytes >> 20} MiB pinned")
 
     h = ctx.ctx
@@ -201,7 +260,10 @@ def main():
                 raise oled.OledError(1, oled.last_error(h))
             if lib.moe_forward_cached(h, l, x_p[g][l], y_p, sp):
                 raise oled.OledError(1, oled.last_error(h))
-            if lib.apply_misses(h, l, None, None):
+            if coop:
+                if lib.apply_misses_coop(h, l, c_p[g], None):
+                    raise oled.OledError(1, oled.last_error(h))
+            elif lib.apply_misses(h, l, None, None):
                 raise oled.OledError(1, oled.last_error(h))
             if lib.score_and_retain(h, l, c_p[g], sp):
                 raise oled.OledError(1, oled.last_error(h))
@@ -227,7 +289,8 @@ def main():
     ops = ctx.profile_collect()
     st = ctx.collect_stats()
     stats = {"hits": st["n_hits"], "misses": st["n_misses"], "active": st["n_active"],
-             "h2d_bytes": st["h2d_bytes"], "layer_iters": st["layer_iters"]}
+             "h2d_bytes": st["h2d_bytes"], "layer_iters": st["layer_iters"],
+             "cpu": st["n_cpu_executed"]}
 
     def agg(name, transfer=None):
         """Launches of one kind; transfer True/False: only those that did / did
@@ -270,9 +333,14 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded router logits, activations, confidence; random-init bf16 experts)",
-        "config": {"workload": "LLaDA-MoE-like layer stack, bf16: hidden 2048, 64 experts, top-8, "
-                               "expert intermediate 1024, 16 MoE layers, batch 1 x block 32 tokens, "
-                               "8 denoising iterations per block, expert cache 26/64 (40%) per layer",
+        "config": {"workload": (f"LLaDA-MoE-like layer stack, bf16: hidden {w.hidden}, {E} experts, "
+                                f"top-{w.top_k}, expert intermediate {w.inter}, {L} MoE layers, "
+                                f"batch {w.batch} x block {w.block} tokens, {w.n_iters} denoising "
+                                f"iterations per block, expert cache {w.capacity}/{E} "
+                                f"({round(100 * w.capacity / E)}%) per layer"
+                                + (", cooperative CPU compensation" if coop else "")
+                                + (f", layer-adaptive sizing every {args.adapt_period} iterations"
+                                   if args.adapt_period else "")),
                    "hidden": w.hidden, "n_experts": E, "top_k": w.top_k, "inter": w.inter,
                    "n_layers": L, "tokens_per_iteration": T, "iterations_per_block": w.n_iters,
                    "capacity": w.capacity},
@@ -299,6 +367,8 @@ def main():
             "active_per_layer_iter": round(stats["active"] / li, 3),
             "cache_util": round(stats["hits"] / li / max(1, w.capacity), 4),
             "h2d_MiB_per_step": round(stats["h2d_bytes"] / args.steps / 2 ** 20, 2),
+            "coop": coop,
+            "cpu_executed_per_layer_iter": round(stats["cpu"] / li, 3) if coop else None,
         },
     }
     ctx.close()

@@ -166,6 +166,7 @@ typedef struct {
   int64_t n_ideal_hits;   /* sum of min(C_l, |A|): hits of the clairvoyant ideal cache
                              bound (Sec. 5.1) */
   int64_t n_cpu_executed; /* misses executed on the CPU (apply_misses_coop) */
+  int64_t n_miss_rows;    /* routed tokens of the misses (sum over misses of their routes) */
 } oled_stats;
 
 /*
@@ -345,19 +346,22 @@ oled_status score_and_retain(void* ctx, int32_t layer, const float* conf_dev, vo
 /*
  * apply_misses_coop: cooperative compensation of the routed layer's misses
  *  (Sec. 4.4), in place of apply_misses on a context created with coop = 1.
- *  Waits for route_block's result and copies the layer's routing, conf_dev
- *  (float [T], the same confidence score_and_retain gets) and, after
- *  moe_forward_cached, x to pinned host memory. Then:
+ *  On such a context moe_forward_cached launches the hits' gate/up GEMM
+ *  without copying any miss, and copies x to pinned host memory on the
+ *  context's copy stream; the routing kernel publishes the layer's routes
+ *  with its staged misses. apply_misses_coop waits for them; if there are
+ *  misses it copies conf_dev (float [T], the same confidence
+ *  score_and_retain gets) to the host and computes:
  *   - priorities S_e as in score_and_retain (exact integers);
  *   - the hardware-aware split rho = nbar tau / (nbar tau + T_H2D) and the
  *     two-stage dispatch of oled_coop_dispatch: the transfer set G;
- *   - the staging slots of the CPU experts M \ G return to the free list
- *     (one launch); G is transferred as in OLED_COPY_SHADER and computed on
- *     the GPU with the hits (the launches moe_forward_cached deferred);
+ *   - the staging slots of the CPU experts M minus G return to the free list
+ *     (one launch); the hits' down GEMM copies G's whole blocks in its first
+ *     workgroups, then G's GEMMs run on the GPU;
  *   - the CPU experts run on coop_threads host threads from the pinned pool
  *     (oled_cpu_ffn's kernels); their output rows are copied into the
- *     layer's per-route outputs before the combine. The call returns once
- *     they are copied in (stream order).
+ *     layer's per-route outputs before the combine (stream order). The call
+ *     returns once those copies are enqueued.
  *  score_and_retain then keeps Top_C of R u G: CPU-executed experts never
  *  enter the cache. out (may be NULL) reports the layer's counts; its
  *  h2d_bytes are G's.

@@ -24,7 +24,7 @@ float64 from the exact input bits:
                 bound, and the effective transfer ratio (Sec. 5.3)
   O12 coop      cooperative compensation (Sec. 4.4): the hardware-aware
                 split rho, and the two-stage load- and reuse-aware dispatch of
-                the misses into transfers G and CPU executions M \ G; only G
+                the misses into transfers G and CPU executions M - G; only G
                 joins the retention candidates
   O10 adapt     layer-adaptive cache sizing (Sec. 4.3): smoothed activation
                 ratio a_l and cache utilisation u_l per layer, layer weight
@@ -63,7 +63,7 @@ define:
 Readings of the cooperative compensation (O12), where the paper names the
 objective J(G) = T_comp - lambda * sum_{e in G} p_e and a two-stage heuristic
 but not the cost model or the bounds:
-  * T_comp(G) = max(T_H2D * |G|, tau_CPU * sum_{e in M \ G} n_e): the transfer
+  * T_comp(G) = max(T_H2D * |G|, tau_CPU * sum_{e in M - G} n_e): the transfer
     path and the CPU path run in parallel (n_e = routed tokens of e); the GPU
     compute of transferred experts is left out;
   * rho = nbar tau_CPU / (nbar tau_CPU + T_H2D); stage 1 transfers the
@@ -443,7 +443,7 @@ def coop_layer_step(logits, conf, resident, top_k: int, capacity: int, t_h2d: fl
     """O1-O3, O6, O12, O8 for one layer-iteration with cooperative
     compensation: the misses are split into transfers G and CPU executions;
     the retention keeps Top_C of R u G. Returns the layer_step dict plus
-    `transfer` (G) and `cpu` (M \ G) masks."""
+    `transfer` (G) and `cpu` (M - G) masks."""
     E = logits.shape[1]
     idx, gates = route(logits, top_k)
     counts, offsets, perm, inv_perm = permute(idx, E)

@@ -29,6 +29,7 @@ ThreadPool::~ThreadPool() {
   {
     std::lock_guard<std::mutex> lk(m_);
     stop_ = true;
+    gen_.fetch_add(1, std::memory_order_release);
   }
   wake_.notify_all();
   for (auto& w : workers_) w.join();
@@ -37,19 +38,20 @@ ThreadPool::~ThreadPool() {
 void ThreadPool::worker(int tid) {
   uint64_t seen = 0;
   for (;;) {
-    const std::function<void(int)>* fn;
-    {
+    // poll for a new job, then sleep until one is posted
+    for (int spin = 0; spin < (1 << 16) && gen_.load(std::memory_order_acquire) == seen; ++spin)
+      _mm_pause();
+    if (gen_.load(std::memory_order_acquire) == seen) {
       std::unique_lock<std::mutex> lk(m_);
-      wake_.wait(lk, [&] { return stop_ || gen_ != seen; });
-      if (stop_) return;
-      seen = gen_;
-      fn = fn_;
+      wake_.wait(lk, [&] { return stop_ || gen_.load(std::memory_order_acquire) != seen; });
     }
-    (*fn)(tid);
     {
       std::lock_guard<std::mutex> lk(m_);
-      if (--pending_ == 0) done_.notify_one();
+      if (stop_) return;
     }
+    seen = gen_.load(std::memory_order_acquire);
+    (*fn_)(tid);
+    pending_.fetch_sub(1, std::memory_order_acq_rel);
   }
 }
 
@@ -58,16 +60,15 @@ void ThreadPool::run(const std::function<void(int)>& fn) {
     fn(0);
     return;
   }
+  fn_ = &fn;
+  pending_.store(n_ - 1, std::memory_order_relaxed);
   {
     std::lock_guard<std::mutex> lk(m_);
-    fn_ = &fn;
-    pending_ = n_ - 1;
-    ++gen_;
+    gen_.fetch_add(1, std::memory_order_release);
   }
   wake_.notify_all();
   fn(0);
-  std::unique_lock<std::mutex> lk(m_);
-  done_.wait(lk, [&] { return pending_ == 0; });
+  while (pending_.load(std::memory_order_acquire) != 0) _mm_pause();
   fn_ = nullptr;
 }
 

@@ -3,6 +3,7 @@
 // transferred). Internal to the library.
 #pragma once
 
+#include <atomic>
 #include <condition_variable>
 #include <cstdint>
 #include <functional>
@@ -13,7 +14,9 @@
 namespace oled {
 
 // Fixed set of worker threads; run(fn) calls fn(tid) once on every thread
-// (the caller is tid 0) and returns when all calls have returned.
+// (the caller is tid 0) and returns when all calls have returned. Between
+// jobs a worker polls for the next one for a short while before it sleeps,
+// so back-to-back jobs (the phases of a layer) start without a wake-up.
 class ThreadPool {
  public:
   explicit ThreadPool(int n_threads);
@@ -28,10 +31,10 @@ class ThreadPool {
   int n_;
   std::vector<std::thread> workers_;
   std::mutex m_;
-  std::condition_variable wake_, done_;
+  std::condition_variable wake_;
   const std::function<void(int)>* fn_ = nullptr;
-  uint64_t gen_ = 0;
-  int pending_ = 0;
+  std::atomic<uint64_t> gen_{0};
+  std::atomic<int> pending_{0};
   bool stop_ = false;
 };
 

@@ -178,6 +178,9 @@ struct PermuteOut {
   int dense_min;
   RouteStats* ring;       // device ring of routing records
   StagedList* staged;     // pinned, or null
+  const float* gates;     // the layer's gates (read when routes are published)
+  int32_t* pub_topk;      // pinned [T*k]: with `staged`, the routes are published too
+  float* pub_gates;       //   (cooperative compensation), or null
   int layer, E, seq;
   CacheView cv;
 };

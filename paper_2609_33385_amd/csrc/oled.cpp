@@ -174,8 +174,8 @@ struct Ctx {
   hipEvent_t ev_cout[2] = {nullptr, nullptr};
   bool cout_used[2] = {false, false};
   int cout_buf = 0;
-  hipEvent_t ev_coop = nullptr;
-  bool deferred = false;           // moe_forward_cached left the hit launches to apply_misses_coop
+  hipEvent_t ev_coop = nullptr;    // the confidence copy
+  hipEvent_t ev_x = nullptr;       // the copy of x to the host
 };
 
 oled_status fail(Ctx* c, oled_status st, const char* fmt, ...) {
@@ -318,6 +318,7 @@ oled_status drain_records(Ctx* c, int until, bool retentions = true) {
     c->acc.n_prev_transferred += v.prev_xfer;
     c->acc.n_transfers_reused += v.reused_xfer;
     c->acc.n_ideal_hits += v.ideal_hits;
+    c->acc.n_miss_rows += v.miss_rows;
     if (v.bad) {
       c->acc.n_bad_blocks += 1;
       if (v.seq != c->reported_bad_route) c->bad_route_layer = v.layer;
@@ -358,6 +359,7 @@ void free_ctx(Ctx* c) {
   if (c->ev_down) (void)hipEventDestroy(c->ev_down);
   if (c->ev_order) (void)hipEventDestroy(c->ev_order);
   if (c->ev_coop) (void)hipEventDestroy(c->ev_coop);
+  if (c->ev_x) (void)hipEventDestroy(c->ev_x);
   for (int b = 0; b < 2; ++b) {
     if (c->ev_cout[b]) (void)hipEventDestroy(c->ev_cout[b]);
     if (c->h_cout[b]) (void)hipHostFree(c->h_cout[b]);
@@ -628,9 +630,9 @@ oled_status check_slots(Ctx* c) {
 // The hits' GEMMs: the active residents, at most min(C, E) experts; their
 // item count stays on the device. With the shader transfer the first
 // workgroups of the gate/up launch copy the staged misses' gate/up weights
-// (h2d: their bytes, or -1 to take them from the routing record), and the
-// hits' down GEMM is enqueued later (sharing a launch with the misses'
-// gate/up); with the copy engine it follows at once.
+// (h2d: their bytes, or -1 to take them from the routing record; 0: the
+// launch copies nothing), and the hits' down GEMM is enqueued later (sharing
+// a launch with the misses' gate/up); with the copy engine it follows at once.
 oled_status launch_hits(Ctx* c, int layer, hipStream_t s, int64_t h2d) {
   const void* x_dev = c->fwd_x;
   const int64_t routes = static_cast<int64_t>(c->cur_T) * c->K;
@@ -640,7 +642,7 @@ oled_status launch_hits(Ctx* c, int layer, hipStream_t s, int64_t h2d) {
   const bool bf16 = c->dtype == OLED_BF16;
   FfnLaunch a = ffn_args(c, layer, 0, max_hit_items, 0);
   a.src = x_dev;
-  if (shader) {
+  if (shader && h2d != 0) {
     a.fetch.nblk = kFetchBlocks;
     a.fetch.off = 0;
     a.fetch.len = c->e13;
@@ -846,6 +848,51 @@ void coop_dispatch(int E, const uint8_t* miss, const int32_t* n_tok, const uint6
     J = best;
   }
   for (int e = 0; e < E; ++e) transfer[e] = in_g[e];
+}
+
+// Cooperative compensation, after the hits' gate/up launch (which copied no
+// misses): the hits' down GEMM whose first workgroups copy the whole blocks
+// of the transferred misses, then the transferred misses' gate/up and down
+// GEMMs, then the dense experts. h2d: bytes of the transferred misses.
+oled_status launch_coop_rest(Ctx* c, int layer, hipStream_t s, int64_t h2d) {
+  const bool bf16 = c->dtype == OLED_BF16;
+  const int64_t routes = static_cast<int64_t>(c->cur_T) * c->K;
+  const int max_hit_items =
+      c->cap > 0 ? static_cast<int>(std::min<int64_t>(c->cap, routes) + routes / oled::kItemRows)
+                 : 0;
+  const int max_miss_items =
+      static_cast<int>(std::min<int64_t>(c->E, routes) + routes / oled::kItemRows);
+  FfnLaunch d = ffn_args(c, layer, 0, max_hit_items, 0);
+  d.src = c->d_h;
+  if (h2d > 0) {
+    d.fetch.nblk = kFetchBlocks;
+    d.fetch.off = 0;
+    d.fetch.len = c->eb;
+  }
+  {
+    OpEvents ev = op_begin(c, OLED_OP_FFN_DOWN);
+    HIP_TRY(c, oled::launch_ffn_down(bf16, d, ev.a, ev.b, s));
+    OpRec o = rec(OLED_OP_FFN_DOWN, layer, -1);
+    o.route_seq = c->cur_route;
+    o.part = 1;
+    o.hits = true;
+    o.h2d = h2d;
+    op_end(c, ev, o);
+  }
+  for (int part = 0; part <= 1; ++part) {
+    FfnLaunch a = ffn_args(c, layer, 1, max_miss_items, kMissGridCap);
+    a.src = part == 0 ? c->fwd_x : c->d_h;
+    const int kind = part == 0 ? OLED_OP_FFN_UP : OLED_OP_FFN_DOWN;
+    OpEvents ev = op_begin(c, kind);
+    HIP_TRY(c, part == 0 ? oled::launch_ffn_up(bf16, a, ev.a, ev.b, s)
+                         : oled::launch_ffn_down(bf16, a, ev.a, ev.b, s));
+    OpRec o = rec(kind, layer, -1);
+    o.route_seq = c->cur_route;
+    o.part = part;
+    o.h2d = 0;
+    op_end(c, ev, o);
+  }
+  return c->cur_dense ? launch_dense(c, layer, s) : OLED_OK;
 }
 
 // Shader transfer, after the hits' gate/up launch: one launch with the hits'
@@ -1077,6 +1124,7 @@ oled_status oled_create(const oled_config* cfg, void** ctx_out) {
                       hipHostMallocDefault))
       return oom("cooperative compensation buffers");
     if (hipEventCreateWithFlags(&c->ev_coop, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&c->ev_x, hipEventDisableTiming) != hipSuccess ||
         hipEventCreateWithFlags(&c->ev_cout[0], hipEventDisableTiming) != hipSuccess ||
         hipEventCreateWithFlags(&c->ev_cout[1], hipEventDisableTiming) != hipSuccess) {
       g_create_error = "coop event creation failed";
@@ -1162,6 +1210,9 @@ oled_status route_block(void* ctx, int32_t layer, const float* logits_dev, int32
   o.dense_counts = c->d_dense_counts;
   o.ring = c->d_ring;
   o.staged = (c->copy_mode == OLED_COPY_SDMA || c->coop) ? c->h_staged : nullptr;
+  o.gates = c->d_gates;
+  o.pub_topk = c->coop ? c->h_ctopk : nullptr;
+  o.pub_gates = c->coop ? c->h_cgates : nullptr;
   o.layer = layer;
   o.E = c->E;
   o.seq = n;
@@ -1218,9 +1269,16 @@ oled_status moe_forward_cached(void* ctx, int32_t layer, const void* x_dev, void
   c->fwd_x = x_dev;
   c->fwd_y = y_dev;
   c->stage = Stage::kHitsQueued;
-  if (c->coop) {  // the launches wait for the dispatch in apply_misses_coop
-    c->deferred = true;
-    return OLED_OK;
+  if (c->coop) {
+    // x to the host for CPU-executed experts (copy stream; x is an input);
+    // the hits' gate/up GEMM at once, without copying misses: which misses
+    // are transferred is decided in apply_misses_coop
+    HIP_TRY(c, hipMemcpyAsync(c->h_cx, x_dev, static_cast<size_t>(c->cur_T) * c->H * c->esz,
+                              hipMemcpyDeviceToHost, c->own_copy));
+    HIP_TRY(c, hipEventRecord(c->ev_x, c->own_copy));
+    st = launch_hits(c, layer, s, 0);
+    if (st != OLED_OK) c->stage = Stage::kRouted;
+    return st;
   }
   st = launch_hits(c, layer, s, -1);
   if (st != OLED_OK) c->stage = Stage::kRouted;
@@ -1346,23 +1404,18 @@ oled_status apply_misses_coop(void* ctx, int32_t layer, const float* conf_dev,
   std::vector<int32_t> cnt(E, 0);
   int n_cpu = 0;
   if (n > 0) {
-    // the layer's routing, confidence and inputs to the host
-    const size_t R = static_cast<size_t>(T) * k;
-    HIP_TRY(c, hipMemcpyAsync(c->h_ctopk, c->d_topk, R * 4, hipMemcpyDeviceToHost, s));
-    HIP_TRY(c, hipMemcpyAsync(c->h_cgates, c->d_gates, R * 4, hipMemcpyDeviceToHost, s));
+    // the routes came with the staged list; the confidence over the copy stream
     HIP_TRY(c, hipMemcpyAsync(c->h_cconf, conf_dev, static_cast<size_t>(T) * 4,
-                              hipMemcpyDeviceToHost, s));
-    if (fwd)
-      HIP_TRY(c, hipMemcpyAsync(c->h_cx, c->fwd_x, static_cast<size_t>(T) * c->H * c->esz,
-                                hipMemcpyDeviceToHost, s));
-    HIP_TRY(c, hipEventRecord(c->ev_coop, s));
-    st = wait_event_spin(c, c->ev_coop, "routing copy");
+                              hipMemcpyDeviceToHost, c->own_copy));
+    HIP_TRY(c, hipEventRecord(c->ev_coop, c->own_copy));
+    st = wait_event_spin(c, c->ev_coop, "confidence copy");
     if (st != OLED_OK) return st;
     // routes per expert and priority numerators, as the retention computes them
+    const size_t R = static_cast<size_t>(T) * k;
     std::vector<uint64_t> S(E, 0);
     for (size_t q = 0; q < R; ++q) {
       const int e = c->h_ctopk[q];
-      if (e < 0 || e >= E) return fail(c, OLED_ERR_HIP, "routing copy out of range");
+      if (e < 0 || e >= E) return fail(c, OLED_ERR_HIP, "published routes out of range");
       ++cnt[e];
       const float cf = c->h_cconf[q / k];
       if (cf >= 0.f && cf <= 1.f)
@@ -1388,11 +1441,9 @@ oled_status apply_misses_coop(void* ctx, int32_t layer, const float* conf_dev,
     if (cpu[e]) cm.bits[e >> 5] |= 1u << (e & 31);
   if (n_cpu > 0) HIP_TRY(c, oled::launch_coop_unstage(view(c), layer, E, cm, s));
   const int64_t g_bytes = static_cast<int64_t>(n - n_cpu) * c->eb;
-  if (fwd) {  // the hits, and the transferred misses through the shader transfer
-    st = launch_hits(c, layer, s, g_bytes);
-    if (st == OLED_OK) st = launch_shader_rest(c, layer, s, g_bytes);
+  if (fwd) {
+    st = n == 0 ? launch_shader_rest(c, layer, s, 0) : launch_coop_rest(c, layer, s, g_bytes);
     if (st != OLED_OK) return st;
-    c->deferred = false;
   } else if (n - n_cpu > 0) {  // control path: whole blocks of the transferred misses
     FetchArgs f;
     f.host_addr = c->d_host_addr + static_cast<size_t>(layer) * E;
@@ -1421,6 +1472,8 @@ oled_status apply_misses_coop(void* ctx, int32_t layer, const float* conf_dev,
       st = wait_event_spin(c, c->ev_cout[b], "CPU output copy");
       if (st != OLED_OK) return st;
     }
+    st = wait_event_spin(c, c->ev_x, "copy of x");
+    if (st != OLED_OK) return st;
     float* hout = c->h_cout[b];
     std::vector<oled::CpuExpertJob> jobs;
     for (int e = 0; e < E; ++e) {

@@ -540,6 +540,12 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
         o.staged->exp[j] = s_sexp[j];
         o.staged->slot[j] = s_sslot[j];
       }
+      if (o.pub_topk && n_staged > 0) {   // the routes, for the host's dispatch of the misses
+        for (int r = tid; r < T * k; r += 64) {
+          o.pub_topk[r] = idx[r];
+          o.pub_gates[r] = __hip_atomic_load(o.gates + r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+      }
       if (tid == 0) o.staged->rec = rs;
       __threadfence_system();
       if (tid == 0) *reinterpret_cast<volatile int32_t*>(&o.staged->seq) = o.seq;

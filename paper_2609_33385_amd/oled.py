@@ -83,7 +83,7 @@ class Stats(ctypes.Structure):
                 ("n_transferred", ctypes.c_int64), ("h2d_bytes", ctypes.c_int64),
                 ("n_bad_blocks", ctypes.c_int64), ("n_prev_transferred", ctypes.c_int64),
                 ("n_transfers_reused", ctypes.c_int64), ("n_ideal_hits", ctypes.c_int64),
-                ("n_cpu_executed", ctypes.c_int64)]
+                ("n_cpu_executed", ctypes.c_int64), ("n_miss_rows", ctypes.c_int64)]
 
     def as_dict(self) -> dict:
         return {name: getattr(self, name) for name, _ in self._fields_}
