@@ -331,3 +331,43 @@ def test_bad_block_without_report():
     finally:
         ctx.close()
         pool.free()
+
+
+def test_block_boundaries():
+    """Blocks follow each other without resetting the caches (semi-autoregressive
+    decoding, Sec. 2.1): two blocks of the 40% stack back to back, the second
+    starting from the first block's resident sets; every layer-iteration
+    against the oracle, outputs at the block boundary."""
+    w = W.WORKLOADS[2]
+    layers, N = [0, 7, 15], w.n_iters
+    _say(f"[blocks] {w.name} layers={layers} blocks=2 iters={N}")
+    ref = O.run_schedule(lambda li, g: W.logits(w, 0, layers[li], g // N, g % N),
+                         lambda li, g: W.confidence(w, 0, g // N, g % N),
+                         len(layers), 2 * N, w.n_experts, w.top_k, w.capacity)
+    pool = HN.fill_pool(w, 0, 32)
+    ctx = HN.make_context(w, pool, n_layers=len(layers))
+    ow = OracleWeights(w, 0, 32, len(layers))
+    dt = HN.torch_dtype(w)
+    try:
+        for g in range(2 * N):
+            b, i = divmod(g, N)
+            conf = torch.from_numpy(W.confidence(w, 0, b, i)).cuda()
+            for li, l in enumerate(layers):
+                lg = torch.from_numpy(W.logits(w, 0, l, b, i)).cuda()
+                x = HN.to_device(W.activations(w, 0, l, b, i))
+                y = torch.empty((w.tokens, w.hidden), dtype=dt, device="cuda")
+                rep = HN.layer_step(ctx, li, lg, conf, x, y)
+                st = ctx.read_layer_state(li, w.tokens)
+                where = f"block {b} iter {i} layer {l}"
+                compare_control(st, ref[g][li], w.tokens, where)
+                check_report(rep, ref[g][li], w.expert_bytes, where)
+                if g in (N - 1, N):
+                    o = ref[g][li]
+                    y_ref = O.moe_output(O.decode(W.activations(w, 0, l, b, i)), o["idx"],
+                                         o["gates"], ow.fn(li))
+                    err = rel_l2(O.decode(HN.from_device(y)), y_ref)
+                    assert err <= tol(w), f"{where}: rel L2 {err:.3e}"
+        _say("[blocks] ok")
+    finally:
+        ctx.close()
+        pool.free()
