@@ -195,6 +195,8 @@ typedef struct {
   int32_t prev_transferred;   /* the last routing of `layer`: experts it transferred at its
                                  previous iteration, */
   int32_t reused_transfers;   /* and those of them retained and activated now */
+  float* logits;              /* [T*E] fp32 logits of the gate GEMM, filled if the last routing
+                                 of `layer` was route_block_gate (else untouched) */
 } oled_layer_state;
 
 /* One timed operation (see oled_config.profile_ops). */
@@ -219,7 +221,8 @@ typedef enum {
                                 transfer-only launch */
   OLED_OP_FFN_DENSE_UP = 7,  /* dense-tile gate/up GEMM (experts with 128+ routed rows) */
   OLED_OP_FFN_DENSE_DOWN = 8, /* dense-tile down GEMM */
-  OLED_OP_LAYER_ADAPT = 9     /* layer-adaptive re-sizing of the capacities */
+  OLED_OP_LAYER_ADAPT = 9,    /* layer-adaptive re-sizing of the capacities */
+  OLED_OP_ROUTE_GEMM = 10     /* the gate GEMM of route_block_gate */
 } oled_op_kind;
 
 /* Creates a context: allocates the slot pool (L*min(C,E) + min(E, Tmax*k)
@@ -262,6 +265,19 @@ oled_status oled_reset_cache(void* ctx);
  */
 oled_status route_block(void* ctx, int32_t layer, const float* logits_dev, int32_t T,
                         void* stream);
+
+/*
+ * route_block_gate: route_block with the gate in front (Sec. 2.1, 4.1: the
+ *  MoE gate scores every token against every expert). x_dev: [T][H] dtype,
+ *  the layer's input; w_gate_dev: [E][H] dtype, the gate weights (row e
+ *  scores expert e). logits[t][e] = sum_h x[t][h] * w_gate[e][h], products
+ *  exact, accumulated in fp32 in a fixed order (one MFMA tile per 16 tokens
+ *  x 16 experts), into the context's logits buffer; then everything
+ *  route_block does, on those logits. oled_read_layer_state returns them.
+ *  Errors: as route_block (NULL x or w_gate: INVALID_ARG).
+ */
+oled_status route_block_gate(void* ctx, int32_t layer, const void* x_dev, const void* w_gate_dev,
+                             int32_t T, void* stream);
 
 /*
  * moe_forward_cached: the cached experts of the routed layer (Sec. 4.1).

@@ -22,6 +22,8 @@ float64 from the exact input bits:
   O11 policies  the comparison retention policies of Sec. 5.1 / 5.3 (LRU,
                 LFU) in place of the priority, the clairvoyant ideal cache
                 bound, and the effective transfer ratio (Sec. 5.3)
+  O13 gate      the gate's logits in front of O1 (Sec. 2.1): x W_gate^T in
+                float64, and the bound on an fp32 accumulation of them
   O12 coop      cooperative compensation (Sec. 4.4): the hardware-aware
                 split rho, and the two-stage load- and reuse-aware dispatch of
                 the misses into transfers G and CPU executions M - G; only G
@@ -483,6 +485,23 @@ def run_coop_schedule(logits_fn, conf_fn, n_layers: int, n_iters: int, n_experts
             row.append(st)
         steps.append(row)
     return steps
+
+
+# --------------------------------------------------------------- O13 gate
+def router_logits(x: np.ndarray, w_gate: np.ndarray) -> np.ndarray:
+    """O13. The gate's logits: logits[t][e] = sum_h x[t][h] * w_gate[e][h] in
+    float64 (x [T][H], w_gate [E][H])."""
+    return np.asarray(x, dtype=np.float64) @ np.asarray(w_gate, dtype=np.float64).T
+
+
+def fp32_sum_bound(x: np.ndarray, w_gate: np.ndarray) -> np.ndarray:
+    """Bound on |fl32 accumulation - exact| of each logit when the H products
+    are exact and summed in float32 in any order: gamma_H * sum_h |x_h w_h|,
+    gamma_n = n u / (1 - n u), u = 2^-24."""
+    H = np.asarray(x).shape[1]
+    u = 2.0 ** -24
+    gamma = H * u / (1.0 - H * u)
+    return gamma * (np.abs(np.asarray(x, np.float64)) @ np.abs(np.asarray(w_gate, np.float64)).T)
 
 
 # ------------------------------------------------- O10 layer-adaptive sizing

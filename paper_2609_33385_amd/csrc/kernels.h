@@ -159,6 +159,11 @@ struct FfnLaunch {
 // Every launcher takes optional (ev0, ev1): if non-null they record the
 // kernel's start and end on the dispatch itself (no extra stream packets).
 
+// The gate GEMM in front of K1: logits [T][E] fp32 = x [T][H] . wg [E][H]^T
+// (bf16 or fp32 inputs, fp32 accumulation in a fixed order).
+hipError_t launch_router_logits(bool bf16, const void* x, const void* wg, int T, int E, int H,
+                                float* logits, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s);
+
 // K1: top-k + fp64 gates: one wavefront per token, or for large blocks one
 // token per lane.
 hipError_t launch_route_topk(const float* logits, int T, int E, int k, int32_t* topk_idx,

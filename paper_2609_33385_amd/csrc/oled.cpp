@@ -97,6 +97,8 @@ struct Ctx {
   int32_t* d_item_counts = nullptr;
   int32_t* d_sync = nullptr;       // completion counter + bad-logit flag of the fused routing
   int32_t* d_chunk = nullptr;      // [Tmax/512 chunks][E] per-chunk counts / bases (large blocks)
+  float* d_logits = nullptr;       // [Tmax][E] logits of route_block_gate's gate GEMM
+  int logits_layer = -1;           // the layer they belong to (-1: none)
   int32_t* d_pcount = nullptr;     // completion counter of the chunked permutation
   unsigned long long* d_sacc = nullptr;  // [E] priority numerators of a many-part scoring
   int32_t* d_ssync = nullptr;      // [2] its completion counter and bad-confidence flag
@@ -376,6 +378,7 @@ void free_ctx(Ctx* c) {
                  c->d_score, c->d_hdr, c->d_slot_of, c->d_res, c->d_res_before,
                  c->d_last_counts, c->d_free, c->d_host_addr, c->d_cap, c->d_stat,
                  c->d_chunk, c->d_pcount, c->d_sacc, c->d_ssync, c->d_iters, c->d_last_use,
+                 c->d_logits,
                  c->d_freq, c->d_prev_miss, c->d_key};
   for (void* p : dev)
     if (p) (void)hipFree(p);
@@ -1058,6 +1061,7 @@ oled_status oled_create(const oled_config* cfg, void** ctx_out) {
       dev_alloc(&c->d_item_counts, 2) || dev_alloc(&c->d_sync, 2) ||
       dev_alloc(&c->d_chunk, static_cast<size_t>(oled::permute_chunks(c->Tmax)) * c->E) ||
       dev_alloc(&c->d_pcount, 1) || dev_alloc(&c->d_sacc, c->E) || dev_alloc(&c->d_ssync, 2) ||
+      dev_alloc(&c->d_logits, static_cast<size_t>(c->Tmax) * c->E) ||
       dev_alloc(&c->d_items, c->max_items) ||
       (c->dense_ok && (dev_alloc(&c->d_dense_items, c->max_dense) ||
                        dev_alloc(&c->d_dense_counts, 2))) ||
@@ -1173,27 +1177,35 @@ oled_status oled_reset_cache(void* ctx) {
   return OLED_OK;
 }
 
-oled_status route_block(void* ctx, int32_t layer, const float* logits_dev, int32_t T, void* stream) {
-  Ctx* c = static_cast<Ctx*>(ctx);
-  if (!c) return OLED_ERR_INVALID_ARG;
+}  // extern "C"
+
+namespace {
+
+// Checks shared by route_block and route_block_gate, and the ordering of a
+// new stream after the previous one.
+oled_status route_begin(Ctx* c, int32_t layer, int32_t T, hipStream_t s, const char* call) {
   oled_status st = check_layer(c, layer);
   if (st != OLED_OK) return st;
   if (c->broken)
     return fail(c, OLED_ERR_STATE, "an earlier HIP failure left the cache state unknown: "
                                    "call oled_reset_cache");
   if (c->stage != Stage::kIdle)
-    return fail(c, OLED_ERR_STATE, "route_block while layer %d is in flight", c->cur_layer);
-  if (!logits_dev) return fail(c, OLED_ERR_INVALID_ARG, "NULL logits");
+    return fail(c, OLED_ERR_STATE, "%s while layer %d is in flight", call, c->cur_layer);
   if (T < 1 || T > c->Tmax) return fail(c, OLED_ERR_INVALID_ARG, "T=%d outside [1,%d]", T, c->Tmax);
   HIP_TRY(c, hipSetDevice(c->device));
-  hipStream_t s = static_cast<hipStream_t>(stream);
   if (c->have_stream && s != c->cur_stream) {  // order the new stream after the old one
     HIP_TRY(c, hipEventRecord(c->ev_order, c->cur_stream));
     HIP_TRY(c, hipStreamWaitEvent(s, c->ev_order, 0));
+    c->cur_stream = s;
   }
+  return OLED_OK;
+}
+
+// Routing, permutation and staging of the layer from logits on the device.
+oled_status route_impl(Ctx* c, int32_t layer, const float* logits_dev, int32_t T, hipStream_t s) {
   // consume what has been published; this call's ring entry must be free
   const int n = c->route_n + 1;
-  st = drain_records(c, n - oled::kStatsRing, false);
+  oled_status st = drain_records(c, n - oled::kStatsRing, false);
   if (st != OLED_OK) return st;
 
   PermuteOut o;
@@ -1252,6 +1264,42 @@ oled_status route_block(void* ctx, int32_t layer, const float* logits_dev, int32
   c->last_routed_layer = layer;
   c->last_routed_T = T;
   return OLED_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+oled_status route_block(void* ctx, int32_t layer, const float* logits_dev, int32_t T, void* stream) {
+  Ctx* c = static_cast<Ctx*>(ctx);
+  if (!c) return OLED_ERR_INVALID_ARG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (!logits_dev && layer >= 0 && layer < c->L && c->stage == Stage::kIdle)
+    return fail(c, OLED_ERR_INVALID_ARG, "NULL logits");
+  oled_status st = route_begin(c, layer, T, s, "route_block");
+  if (st != OLED_OK) return st;
+  return route_impl(c, layer, logits_dev, T, s);
+}
+
+oled_status route_block_gate(void* ctx, int32_t layer, const void* x_dev, const void* w_gate_dev,
+                             int32_t T, void* stream) {
+  Ctx* c = static_cast<Ctx*>(ctx);
+  if (!c) return OLED_ERR_INVALID_ARG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((!x_dev || !w_gate_dev) && layer >= 0 && layer < c->L && c->stage == Stage::kIdle)
+    return fail(c, OLED_ERR_INVALID_ARG, "NULL x or gate weights");
+  oled_status st = route_begin(c, layer, T, s, "route_block_gate");
+  if (st != OLED_OK) return st;
+  OpEvents ev = op_begin(c, OLED_OP_ROUTE_GEMM);
+  HIP_TRY(c, oled::launch_router_logits(c->dtype == OLED_BF16, x_dev, w_gate_dev, T, c->E, c->H,
+                                        c->d_logits, ev.a, ev.b, s));
+  op_end(c, ev, rec(OLED_OP_ROUTE_GEMM, layer,
+                    static_cast<int64_t>(T) * c->H * c->esz +
+                        static_cast<int64_t>(c->E) * c->H * c->esz +
+                        static_cast<int64_t>(T) * c->E * 4,
+                    static_cast<int64_t>(2) * T * c->E * c->H));
+  c->logits_layer = layer;
+  return route_impl(c, layer, c->d_logits, T, s);
 }
 
 oled_status moe_forward_cached(void* ctx, int32_t layer, const void* x_dev, void* y_dev, void* stream) {
@@ -1659,6 +1707,9 @@ oled_status oled_read_layer_state(void* ctx, int32_t layer, oled_layer_state* ou
   out->reserved = 0;
   out->prev_transferred = lc[4];
   out->reused_transfers = lc[5];
+  if (out->logits && T > 0 && c->logits_layer == layer)
+    HIP_TRY(c, hipMemcpy(out->logits, c->d_logits, static_cast<size_t>(T) * c->E * 4,
+                         hipMemcpyDeviceToHost));
   if (out->retain_key)
     HIP_TRY(c, hipMemcpy(out->retain_key, c->d_key + static_cast<size_t>(layer) * c->E, c->E * 8,
                          hipMemcpyDeviceToHost));

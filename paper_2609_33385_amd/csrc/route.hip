@@ -685,7 +685,77 @@ __global__ __launch_bounds__(256) void k_route_fused(const float* __restrict__ l
   permute_body(s_idx, T, k, any_bad, o, s_free, &s_ftop);
 }
 
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float floatx4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+// The gate: logits[t][e] = sum_h x[t][h] * wg[e][h], accumulated in fp32 in
+// a fixed order. One 16 x 16 tile (16 tokens x 16 experts) per wavefront
+// over the whole hidden dimension: A = token rows, B = gate rows, both read
+// 16 bytes per lane per step straight from memory (row-major), D lane (c, g)
+// register i -> token 4g + i, expert c. Tokens and experts past the end read
+// the last row; their results are not stored.
+template <bool BF16>
+__global__ __launch_bounds__(256) void k_router_logits(const void* __restrict__ x,
+                                                       const void* __restrict__ wg, int T, int E,
+                                                       int H, float* __restrict__ logits) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int tiles_e = (E + 15) >> 4;
+  const int tile = blockIdx.x * 4 + wave;
+  const int tt = tile / tiles_e, te = tile - tt * tiles_e;
+  if (tt * 16 >= T) return;
+  const int c = lane & 15, g = lane >> 4;
+  const size_t t = static_cast<size_t>(min(tt * 16 + c, T - 1));
+  const size_t e = static_cast<size_t>(min(te * 16 + c, E - 1));
+  floatx4_t acc = {0.f, 0.f, 0.f, 0.f};
+  if constexpr (BF16) {
+    const uint16_t* xa = static_cast<const uint16_t*>(x) + t * H + 8 * g;
+    const uint16_t* wb = static_cast<const uint16_t*>(wg) + e * H + 8 * g;
+#pragma unroll 4
+    for (int k = 0; k < H; k += 32) {
+      const u32x4_t a = *reinterpret_cast<const u32x4_t*>(xa + k);
+      const u32x4_t b = *reinterpret_cast<const u32x4_t*>(wb + k);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                    __builtin_bit_cast(bf16x8_t, b), acc, 0, 0, 0);
+    }
+  } else {
+    // fp32: lane group g holds k 4g..4g+3 of a 16-wide step; MFMA q takes element q
+    const float* xa = static_cast<const float*>(x) + t * H + 4 * g;
+    const float* wb = static_cast<const float*>(wg) + e * H + 4 * g;
+#pragma unroll 2
+    for (int k = 0; k < H; k += 16) {
+      const floatx4_t a = *reinterpret_cast<const floatx4_t*>(xa + k);
+      const floatx4_t b = *reinterpret_cast<const floatx4_t*>(wb + k);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[q], b[q], acc, 0, 0, 0);
+    }
+  }
+  const int ec = te * 16 + c;
+  if (ec < E) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int tr = tt * 16 + 4 * g + i;
+      if (tr < T) logits[static_cast<size_t>(tr) * E + ec] = acc[i];
+    }
+  }
+}
+
 }  // namespace
+
+hipError_t launch_router_logits(bool bf16, const void* x, const void* wg, int T, int E, int H,
+                                float* logits, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
+  if (T <= 0 || E <= 0 || H <= 0 || H % 32) return hipErrorInvalidValue;
+  const int64_t tiles = static_cast<int64_t>((T + 15) / 16) * ((E + 15) / 16);
+  const int64_t blocks = (tiles + 3) / 4;
+  if (blocks > INT32_MAX) return hipErrorInvalidValue;
+  if (bf16)
+    hipExtLaunchKernelGGL(k_router_logits<true>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
+                          s, ev0, ev1, 0, x, wg, T, E, H, logits);
+  else
+    hipExtLaunchKernelGGL(k_router_logits<false>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
+                          s, ev0, ev1, 0, x, wg, T, E, H, logits);
+  return hipGetLastError();
+}
 
 bool route_fused(int T, int k) { return T * k <= kFusedMaxRoutes; }
 

@@ -33,11 +33,11 @@ OLED_COPY_SHADER = 0
 OLED_COPY_SDMA = 1
 COPY_MODES = {"shader": OLED_COPY_SHADER, "sdma": OLED_COPY_SDMA}
 POLICIES = {"priority": 0, "lru": 1, "lfu": 2}
-PROFILE_ALL = 0x3FF
+PROFILE_ALL = 0x7FF
 
 OP_NAMES = {0: "route_topk", 1: "permute", 2: "ffn_up", 3: "ffn_down", 4: "combine",
             5: "score_retain", 6: "h2d", 7: "ffn_dense_up", 8: "ffn_dense_down",
-            9: "layer_adapt"}
+            9: "layer_adapt", 10: "route_gemm"}
 OP_KIND = {v: k for k, v in OP_NAMES.items()}
 
 
@@ -49,6 +49,7 @@ def profile_mask(*names) -> int:
     return m
 
 EXPORTED = ["oled_create", "oled_destroy", "oled_last_error", "oled_reset_cache", "route_block",
+            "route_block_gate",
             "apply_misses", "apply_misses_coop", "moe_forward_cached", "score_and_retain",
             "oled_read_layer_state", "oled_collect_stats", "oled_profile_collect",
             "oled_pack_expert", "oled_host_alloc", "oled_host_free", "oled_coop_dispatch",
@@ -99,7 +100,7 @@ class LayerState(ctypes.Structure):
                 ("n_hits", ctypes.c_int32), ("n_misses", ctypes.c_int32),
                 ("capacity", ctypes.c_int32), ("reserved", ctypes.c_int32),
                 ("retain_key", ctypes.c_void_p), ("prev_transferred", ctypes.c_int32),
-                ("reused_transfers", ctypes.c_int32)]
+                ("reused_transfers", ctypes.c_int32), ("logits", ctypes.c_void_p)]
 
 
 class OpTime(ctypes.Structure):
@@ -132,6 +133,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "oled_last_error": (ctypes.c_char_p, [vp]),
         "oled_reset_cache": (i32, [vp]),
         "route_block": (i32, [vp, i32, vp, i32, vp]),
+        "route_block_gate": (i32, [vp, i32, vp, vp, i32, vp]),
         "apply_misses": (i32, [vp, i32, vp, ctypes.POINTER(MissReport)]),
         "apply_misses_coop": (i32, [vp, i32, vp, ctypes.POINTER(MissReport)]),
         "oled_coop_dispatch": (i32, [i32, vp, vp, vp, ctypes.c_double, ctypes.c_double,
@@ -204,6 +206,10 @@ def oled_reset_cache(ctx) -> None:
 
 def route_block(ctx, layer: int, logits, T: int, stream=None) -> int:
     return load().route_block(ctx, layer, _ptr(logits), T, _stream(stream))
+
+
+def route_block_gate(ctx, layer: int, x, w_gate, T: int, stream=None) -> int:
+    return load().route_block_gate(ctx, layer, _ptr(x), _ptr(w_gate), T, _stream(stream))
 
 
 def apply_misses(ctx, layer: int, copy_stream=None, report: MissReport | None = None) -> int:
@@ -366,6 +372,9 @@ class Context:
     def route_block(self, layer, logits, T, stream=None):
         _check(self.ctx, route_block(self.ctx, layer, logits, T, stream))
 
+    def route_block_gate(self, layer, x, w_gate, T, stream=None):
+        _check(self.ctx, route_block_gate(self.ctx, layer, x, w_gate, T, stream))
+
     def apply_misses(self, layer, copy_stream=None, report: bool = True) -> MissReport | None:
         """With report=False nothing waits for the device (shader transfer)."""
         rep = MissReport() if report else None
@@ -392,8 +401,9 @@ class Context:
                    score_q=np.zeros(E, np.uint64), resident_before=np.zeros(E, np.uint8),
                    resident_after=np.zeros(E, np.uint8), slot_of=np.zeros(E, np.int32))
         rkey = np.zeros(E, np.uint64)
+        lgt = np.full(R * E // k, np.nan, np.float32)
         st = LayerState(*[a.ctypes.data for a in out.values()], 0, 0, 0, 0, 0, 0,
-                        rkey.ctypes.data, 0, 0)
+                        rkey.ctypes.data, 0, 0, lgt.ctypes.data)
         status = oled_read_layer_state(self.ctx, layer, st)
         if status not in (OLED_OK, OLED_ERR_INVALID_ARG):
             _check(self.ctx, status)
@@ -404,6 +414,7 @@ class Context:
         out["gates"] = out["gates"].reshape(Tn, k)
         out.update(tokens=Tn, n_active=st.n_active, n_hits=st.n_hits, n_misses=st.n_misses,
                    capacity=st.capacity, retain_key=rkey, prev_transferred=st.prev_transferred,
+                   logits=lgt[: Tn * E].reshape(Tn, E),
                    reused_transfers=st.reused_transfers,
                    rejected=(status == OLED_ERR_INVALID_ARG))
         out["resident_before"] = out["resident_before"].astype(bool)

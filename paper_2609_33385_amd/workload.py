@@ -33,6 +33,7 @@ _TID_ZIPF = 4     # per-layer popularity rank permutation
 _TID_CONF = 5     # confidence draws
 _TID_X = 6        # activations
 _TID_W = 7        # expert weight blocks
+_TID_GATE = 8     # gate weights
 
 
 @dataclasses.dataclass(frozen=True)
@@ -200,6 +201,15 @@ def expert_block(w: Workload, seed: int, b: int) -> np.ndarray:
     """
     r = _rng(w, seed, _TID_W, 0, b)
     v = 0.02 * r.standard_normal(w.expert_elems)
+    return _emit(w, v)
+
+
+def gate_weights(w: Workload, seed: int, layer: int) -> np.ndarray:
+    """Gate weights of a layer [E][H] in the workload dtype encoding, entries
+    ~ N(0, (150 / sqrt(H))^2), so that logits of N(0, 0.02^2) activations have
+    a standard deviation of about 3."""
+    r = _rng(w, seed, _TID_GATE, layer)
+    v = (150.0 / math.sqrt(w.hidden)) * r.standard_normal((w.n_experts, w.hidden))
     return _emit(w, v)
 
 
