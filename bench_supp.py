@@ -17,6 +17,13 @@
   524280 routes; per-launch device times (HIP events) and HBM fractions of
   the algorithmic bytes against 8 TB/s.
 
+--gate: the gate GEMM of route_block_gate (logits = x W_gate^T, fp32
+  accumulation) on the 40% stack's shape (32 tokens, hidden 2048, 64 experts),
+  its batch-8 form (256 tokens), the E=128 stack (1024 tokens, hidden 4096)
+  and the prefill-like block (16384 tokens, hidden 4096, 128 experts):
+  device time per launch (HIP events), TFLOP/s and the HBM fraction of its
+  algorithmic bytes (x, W_gate, logits).
+
 Each mode prints one JSON line. Inputs are seeded and synthetic.
 """
 from __future__ import annotations
@@ -184,10 +191,52 @@ def route(args):
     print(json.dumps(out), flush=True)
 
 
+def gate(args):
+    import torch
+    from paper_2609_33385_amd import harness as HN
+    from paper_2609_33385_amd import oled
+    from paper_2609_33385_amd import workload as W
+    out = {"mode": "gate", "shapes": []}
+    for name, w in (("40% stack", W.WORKLOADS[2].replace(n_layers=1)),
+                    ("batch 8", W.WORKLOADS[3].replace(n_layers=1)),
+                    ("E=128 stack", W.WORKLOADS[4].replace(n_layers=1)),
+                    ("prefill", W.WORKLOADS[5].replace(wid=400, batch=256, block=64, n_layers=1,
+                                                      capacity=128))):
+        T, E, H = w.tokens, w.n_experts, w.hidden
+        pool = oled.PinnedPool(2, w.expert_bytes)
+        ctx = HN.make_context(w, pool, capacity=0, profile_ops=oled.profile_mask("route_gemm"))
+        x = HN.to_device(W.activations(w, args.seed, 0, 0, 0))
+        g = HN.to_device(W.gate_weights(w, args.seed, 0))
+        conf = torch.ones(T, device="cuda")
+        s = torch.cuda.current_stream()
+        ops = []
+        for it in range(args.iters + 1):
+            ctx.route_block_gate(0, x, g, T, s)
+            ctx.apply_misses(0, report=False)
+            ctx.score_and_retain(0, conf, s)
+            torch.cuda.synchronize()
+            got = ctx.profile_collect()
+            if it > 0:
+                ops += [o for o in got if o[0] == "route_gemm"]
+        ctx.close()
+        pool.free()
+        ms = sum(o[2] for o in ops) / len(ops)
+        by, fl = ops[0][3], ops[0][4]
+        out["shapes"].append({"shape": name, "tokens": T, "hidden": H, "experts": E,
+                              "avg_us": round(ms * 1e3, 2),
+                              "TFLOPs": round(fl / 1e12 / (ms / 1e3), 2),
+                              "GBps": round(by / 1e9 / (ms / 1e3), 1),
+                              "hbm_frac": round(by / 1e9 / (ms / 1e3) / HBM_PEAK_GBS, 4),
+                              "mfma_frac": round(fl / 1e12 / (ms / 1e3) / MFMA_BF16_PEAK_TFLOPS, 4),
+                              "launches": len(ops)})
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gemm", action="store_true")
     ap.add_argument("--route", action="store_true")
+    ap.add_argument("--gate", action="store_true")
     ap.add_argument("--iters", type=int, default=3)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--check-rows", type=int, default=8)
@@ -200,6 +249,8 @@ def main():
         gemm(args)
     if args.route:
         route(args)
+    if args.gate:
+        gate(args)
 
 
 if __name__ == "__main__":

@@ -221,6 +221,7 @@ constexpr int kChunkTokens = kChunkWords * 32;
 
 constexpr int kFusedMaxRoutes = 1024;       // fused routing path: T * k routes kept in LDS
 constexpr int kLaneTokensMin = 1024;        // blocks of more tokens route one token per lane
+constexpr int kGateFullGrid = 256;          // gate GEMM workgroups that fill the compute units
 constexpr int kChunkedMinTokens = 1024;     // and permute over many workgroups
 
 // Stable positions of the routes of tokens [t0, t1) (at most kChunkTokens):
@@ -689,71 +690,195 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
-// The gate: logits[t][e] = sum_h x[t][h] * wg[e][h], accumulated in fp32 in
-// a fixed order. One 16 x 16 tile (16 tokens x 16 experts) per wavefront
-// over the whole hidden dimension: A = token rows, B = gate rows, both read
-// 16 bytes per lane per step straight from memory (row-major), D lane (c, g)
-// register i -> token 4g + i, expert c. Tokens and experts past the end read
-// the last row; their results are not stored.
-template <bool BF16>
-__global__ __launch_bounds__(256) void k_router_logits(const void* __restrict__ x,
-                                                       const void* __restrict__ wg, int T, int E,
-                                                       int H, float* __restrict__ logits) {
+// Bijection on [0, total): workgroup b (XCD b % 8) -> contiguous tile range
+// per XCD, so the tiles of one token range share an L2.
+__device__ __forceinline__ int xcd_tile(int b, int total) {
+  const int x = b & 7, local = b >> 3;
+  const int q = total >> 3, r = total & 7;
+  return x * q + (x < r ? x : r) + local;
+}
+
+// The gate: logits[t][e] = sum_h x[t][h] * wg[e][h] in fp32. A workgroup
+// owns a tile of 16*TA tokens x 16*NB experts; its KS wavefronts split the
+// hidden dimension into KS contiguous ranges, each accumulating every 16 x 16
+// fragment of the tile over its range (A = token rows, B = gate rows, both
+// read straight from memory; the next step's operands in flight while the
+// current one multiplies, or the loads of G steps issued together). The partial tiles meet in LDS and are summed in
+// wavefront order, so the result does not depend on timing. A step covers 64
+// hidden elements in bf16 (lane group g holds elements 16g..16g+15, 32
+// contiguous bytes of its row: two MFMAs of 8) or 32 in fp32 (elements
+// 8g..8g+7: eight 16x16x4 MFMAs); the hidden size is a multiple of 128, so
+// the steps tile it exactly. D lane (c, g) register
+// i -> token 4g + i, expert c. Tokens and experts past the end read the last
+// row; their results are not stored. Tiles are numbered token-major and laid
+// out over the XCDs in contiguous ranges.
+template <bool BF16, int TA, int NB, int KS, int G>
+__global__ __launch_bounds__(64 * KS) void k_router_logits(const void* __restrict__ x,
+                                                          const void* __restrict__ wg, int T,
+                                                          int E, int H,
+                                                          float* __restrict__ logits) {
+  constexpr int NF = TA * NB;
+  constexpr int kStep = BF16 ? 64 : 32;          // hidden elements per step
+  constexpr int kEsz = BF16 ? 2 : 4;
+  __shared__ floatx4_t s_part[KS][NF][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int tiles_e = (E + 15) >> 4;
-  const int tile = blockIdx.x * 4 + wave;
-  const int tt = tile / tiles_e, te = tile - tt * tiles_e;
-  if (tt * 16 >= T) return;
   const int c = lane & 15, g = lane >> 4;
-  const size_t t = static_cast<size_t>(min(tt * 16 + c, T - 1));
-  const size_t e = static_cast<size_t>(min(te * 16 + c, E - 1));
-  floatx4_t acc = {0.f, 0.f, 0.f, 0.f};
-  if constexpr (BF16) {
-    const uint16_t* xa = static_cast<const uint16_t*>(x) + t * H + 8 * g;
-    const uint16_t* wb = static_cast<const uint16_t*>(wg) + e * H + 8 * g;
-#pragma unroll 4
-    for (int k = 0; k < H; k += 32) {
-      const u32x4_t a = *reinterpret_cast<const u32x4_t*>(xa + k);
-      const u32x4_t b = *reinterpret_cast<const u32x4_t*>(wb + k);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
-                                                    __builtin_bit_cast(bf16x8_t, b), acc, 0, 0, 0);
+  const int tiles_e = (E + 16 * NB - 1) / (16 * NB);
+  const int tile = xcd_tile(blockIdx.x, gridDim.x);
+  const int tt = tile / tiles_e, te = tile - tt * tiles_e;
+  const int t0 = tt * 16 * TA, e0 = te * 16 * NB;
+  const int n_steps = H / kStep;
+  const int s0 = wave * n_steps / KS, s1 = (wave + 1) * n_steps / KS;
+  const char* pa[TA];
+  const char* pb[NB];
+#pragma unroll
+  for (int a = 0; a < TA; ++a)
+    pa[a] = static_cast<const char*>(x) +
+            (static_cast<size_t>(min(t0 + 16 * a + c, T - 1)) * H) * kEsz + 32 * g;
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+    pb[b] = static_cast<const char*>(wg) +
+            (static_cast<size_t>(min(e0 + 16 * b + c, E - 1)) * H) * kEsz + 32 * g;
+  floatx4_t acc[TA][NB];
+#pragma unroll
+  for (int a = 0; a < TA; ++a)
+#pragma unroll
+    for (int b = 0; b < NB; ++b) acc[a][b] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+
+  auto mma = [&](const u32x4_t (&va)[TA][2], const u32x4_t (&vb)[NB][2]) {
+#pragma unroll
+    for (int a = 0; a < TA; ++a)
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        if constexpr (BF16) {
+#pragma unroll
+          for (int v = 0; v < 2; ++v)
+            acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8_t, va[a][v]), __builtin_bit_cast(bf16x8_t, vb[b][v]),
+                acc[a][b], 0, 0, 0);
+        } else {
+#pragma unroll
+          for (int v = 0; v < 2; ++v) {
+            const floatx4_t fa = __builtin_bit_cast(floatx4_t, va[a][v]);
+            const floatx4_t fb = __builtin_bit_cast(floatx4_t, vb[b][v]);
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[q], fb[q], acc[a][b], 0, 0, 0);
+          }
+        }
+      }
+  };
+  const int n = s1 - s0;
+  auto offset = [&](int j) { return static_cast<size_t>(s0 + j) * kStep * kEsz; };
+  auto load_a = [&](int j, u32x4_t (&va)[TA][2]) {
+    const size_t off = offset(j);
+#pragma unroll
+    for (int a = 0; a < TA; ++a) {
+      va[a][0] = *reinterpret_cast<const u32x4_t*>(pa[a] + off);
+      va[a][1] = *reinterpret_cast<const u32x4_t*>(pa[a] + off + 16);
+    }
+  };
+  auto load_b = [&](int j, u32x4_t (&vb)[NB][2]) {
+    const size_t off = offset(j);
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      vb[b][0] = *reinterpret_cast<const u32x4_t*>(pb[b] + off);
+      vb[b][1] = *reinterpret_cast<const u32x4_t*>(pb[b] + off + 16);
+    }
+  };
+  auto load = [&](int j, u32x4_t (&va)[TA][2], u32x4_t (&vb)[NB][2]) {
+    load_a(j, va);
+    load_b(j, vb);
+  };
+
+  if constexpr (G > 1) {
+    // short ranges: the loads of G steps at once, then their products
+    for (int j0 = 0; j0 < n; j0 += G) {
+      u32x4_t va[G][TA][2], vb[G][NB][2];
+#pragma unroll
+      for (int j = 0; j < G; ++j)
+        if (j0 + j < n) load(j0 + j, va[j], vb[j]);
+#pragma unroll
+      for (int j = 0; j < G; ++j)
+        if (j0 + j < n) mma(va[j], vb[j]);
     }
   } else {
-    // fp32: lane group g holds k 4g..4g+3 of a 16-wide step; MFMA q takes element q
-    const float* xa = static_cast<const float*>(x) + t * H + 4 * g;
-    const float* wb = static_cast<const float*>(wg) + e * H + 4 * g;
-#pragma unroll 2
-    for (int k = 0; k < H; k += 16) {
-      const floatx4_t a = *reinterpret_cast<const floatx4_t*>(xa + k);
-      const floatx4_t b = *reinterpret_cast<const floatx4_t*>(wb + k);
+    u32x4_t ca[TA][2], cb[NB][2], na[TA][2], nb[NB][2];
+    if (n > 0) load(0, ca, cb);
+    int j = 0;
+    for (; j + 1 < n; j += 2) {
+      load(j + 1, na, nb);
+      mma(ca, cb);
+      if (j + 2 < n) load(j + 2, ca, cb);
+      mma(na, nb);
+    }
+    if (j < n) mma(ca, cb);
+  }
 #pragma unroll
-      for (int q = 0; q < 4; ++q) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[q], b[q], acc, 0, 0, 0);
+  for (int a = 0; a < TA; ++a)
+#pragma unroll
+    for (int b = 0; b < NB; ++b) s_part[wave][a * NB + b][lane] = acc[a][b];
+  __syncthreads();
+  for (int f = wave; f < NF; f += KS) {   // fragment f is summed by wavefront f mod KS
+    floatx4_t sum = s_part[0][f][lane];
+#pragma unroll
+    for (int w = 1; w < KS; ++w) sum += s_part[w][f][lane];
+    const int a = f / NB, b = f - a * NB;
+    const int ec = e0 + 16 * b + c;
+    if (ec < E) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int tr = t0 + 16 * a + 4 * g + i;
+        if (tr < T) logits[static_cast<size_t>(tr) * E + ec] = sum[i];
+      }
     }
   }
-  const int ec = te * 16 + c;
-  if (ec < E) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int tr = tt * 16 + 4 * g + i;
-      if (tr < T) logits[static_cast<size_t>(tr) * E + ec] = acc[i];
-    }
-  }
+}
+
+template <bool BF16, int TA, int NB, int KS, int G>
+void launch_logits_cfg(const void* x, const void* wg, int T, int E, int H, float* logits,
+                       hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
+  const int64_t blocks =
+      static_cast<int64_t>((T + 16 * TA - 1) / (16 * TA)) * ((E + 16 * NB - 1) / (16 * NB));
+  hipExtLaunchKernelGGL(k_router_logits<BF16, TA, NB, KS, G>, dim3(static_cast<unsigned>(blocks)),
+                        dim3(64 * KS), 0, s, ev0, ev1, 0, x, wg, T, E, H, logits);
+}
+
+// Tile shape of the gate GEMM: the largest tile that still gives every
+// compute unit a workgroup (64 tokens x all of up to 128 experts reads x
+// once; 32 x 64 and 16 x 32 for mid-sized blocks). The re-reads of the gate
+// rows by every tile, not HBM, bound the larger blocks: the operands come
+// through L2 at about 8 TB/s for every tile shape measured, so the tile that
+// reads the fewest bytes wins. Small blocks take 16 x 16 tiles whose 4
+// wavefronts issue the loads of 4 steps at once.
+template <bool BF16>
+void launch_logits(const void* x, const void* wg, int T, int E, int H, float* logits,
+                   hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
+  auto wgs = [&](int ta, int nb) {
+    return static_cast<int64_t>((T + 16 * ta - 1) / (16 * ta)) * ((E + 16 * nb - 1) / (16 * nb));
+  };
+  if (E <= 64 && wgs(4, 4) >= kGateFullGrid)
+    launch_logits_cfg<BF16, 4, 4, 4, 1>(x, wg, T, E, H, logits, ev0, ev1, s);
+  else if (E > 64 && wgs(4, 8) >= kGateFullGrid)
+    launch_logits_cfg<BF16, 4, 8, 4, 1>(x, wg, T, E, H, logits, ev0, ev1, s);
+  else if (wgs(2, 4) >= kGateFullGrid)
+    launch_logits_cfg<BF16, 2, 4, 8, 1>(x, wg, T, E, H, logits, ev0, ev1, s);
+  else if (wgs(1, 2) >= kGateFullGrid)
+    launch_logits_cfg<BF16, 1, 2, 16, 2>(x, wg, T, E, H, logits, ev0, ev1, s);
+  else
+    launch_logits_cfg<BF16, 1, 1, 4, 4>(x, wg, T, E, H, logits, ev0, ev1, s);
 }
 
 }  // namespace
 
 hipError_t launch_router_logits(bool bf16, const void* x, const void* wg, int T, int E, int H,
                                 float* logits, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
-  if (T <= 0 || E <= 0 || H <= 0 || H % 32) return hipErrorInvalidValue;
-  const int64_t tiles = static_cast<int64_t>((T + 15) / 16) * ((E + 15) / 16);
-  const int64_t blocks = (tiles + 3) / 4;
-  if (blocks > INT32_MAX) return hipErrorInvalidValue;
+  if (T <= 0 || E <= 0 || H <= 0 || H % 64) return hipErrorInvalidValue;
+  if (static_cast<int64_t>((T + 15) / 16) * ((E + 15) / 16) > INT32_MAX) return hipErrorInvalidValue;
   if (bf16)
-    hipExtLaunchKernelGGL(k_router_logits<true>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
-                          s, ev0, ev1, 0, x, wg, T, E, H, logits);
+    launch_logits<true>(x, wg, T, E, H, logits, ev0, ev1, s);
   else
-    hipExtLaunchKernelGGL(k_router_logits<false>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
-                          s, ev0, ev1, 0, x, wg, T, E, H, logits);
+    launch_logits<false>(x, wg, T, E, H, logits, ev0, ev1, s);
   return hipGetLastError();
 }
 

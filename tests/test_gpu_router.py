@@ -85,3 +85,41 @@ def test_gate_routing(dtype, batch, block, E, k, H, C):
     finally:
         ctx.close()
         pool.free()
+
+
+# blocks large enough for the wide tiles of the gate GEMM (64 tokens x 128 or
+# 64 experts per workgroup), with ragged token and expert tails, in both dtypes
+TILE_CASES = [
+    ("bf16", 40, 410, 128, 256),
+    ("bf16", 3, 5481, 48, 256),
+    ("f32", 40, 410, 128, 128),
+]
+
+
+@pytest.mark.parametrize("dtype,batch,block,E,H", TILE_CASES)
+def test_gate_logits_wide_tiles(dtype, batch, block, E, H):
+    w = W.WORKLOADS[2].replace(wid=361, name=f"gate-wide-{dtype}-E{E}-H{H}", dtype=dtype,
+                               batch=batch, block=block, n_experts=E, top_k=4, hidden=H,
+                               inter=128, n_layers=1, n_iters=1, capacity=E // 2)
+    T = w.tokens
+    _say(f"[gate wide] {w.name} T={T}")
+    pool = HN.fill_pool(w, 0, 4)
+    ctx = HN.make_context(w, pool)
+    s = torch.cuda.current_stream()
+    try:
+        xh = W.activations(w, 1, 0, 0, 0)
+        gh = W.gate_weights(w, 1, 0)
+        x, g = HN.to_device(xh), HN.to_device(gh)
+        conf = torch.from_numpy(W.confidence(w, 1, 0, 0)).cuda()
+        ctx.route_block_gate(0, x, g, T, s)
+        ctx.apply_misses(0, report=False)
+        ctx.score_and_retain(0, conf, s)
+        lg = ctx.read_layer_state(0, T)["logits"]
+        ref = O.router_logits(O.decode(xh), O.decode(gh))
+        bound = O.fp32_sum_bound(O.decode(xh), O.decode(gh))
+        err = np.abs(lg.astype(np.float64) - ref)
+        assert np.all(err <= bound), f"logit error {err.max():.3e} above the bound"
+        _say(f"[gate wide] ok, max error {err.max():.3e}")
+    finally:
+        ctx.close()
+        pool.free()
