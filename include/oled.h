@@ -271,9 +271,11 @@ oled_status route_block(void* ctx, int32_t layer, const float* logits_dev, int32
  *  MoE gate scores every token against every expert). x_dev: [T][H] dtype,
  *  the layer's input; w_gate_dev: [E][H] dtype, the gate weights (row e
  *  scores expert e). logits[t][e] = sum_h x[t][h] * w_gate[e][h], products
- *  exact, accumulated in fp32 in a fixed order (one MFMA tile per 16 tokens
- *  x 16 experts), into the context's logits buffer; then everything
- *  route_block does, on those logits. oled_read_layer_state returns them.
+ *  exact, accumulated in fp32 in an order fixed by (T, E, H): each tile of
+ *  tokens x experts splits the hidden dimension over its wavefronts and sums
+ *  their partial tiles in wavefront order, so repeated calls give identical
+ *  logits. They go to the context's logits buffer, then everything
+ *  route_block does runs on them; oled_read_layer_state returns them.
  *  Errors: as route_block (NULL x or w_gate: INVALID_ARG).
  */
 oled_status route_block_gate(void* ctx, int32_t layer, const void* x_dev, const void* w_gate_dev,
