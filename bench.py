@@ -15,7 +15,10 @@ and resident in HBM; the expert weights live in a pinned host pool (all
 
 Prints one JSON line with the layer-token throughput, the roofline of the
 dominant kernel (grouped gate/up GEMM, timed with HIP events on its stream
-during the timed steps) and the CPU oracle timed on a bounded sample.
+during the timed steps) and the CPU oracle timed on a bounded sample. After
+the timed steps, a short pass on a second context times every operation
+(detail.phase_pass: per-phase device times, their rates against HBM, and the
+overlap of miss transfers with compute); it is not part of the timed region.
 """
 from __future__ import annotations
 
@@ -140,6 +143,103 @@ def profile_coop(w, pool, logits, xs, conf, args):
                 nbar=round(nbar, 3), lambda_us=round(lam, 2))
 
 
+PHASES = ("route_topk", "permute", "ffn_up", "ffn_down", "ffn_dense_up", "ffn_dense_down",
+          "h2d", "combine", "score_retain", "layer_adapt")
+
+
+def pinned_h2d_gbps(pool, w):
+    """Host-to-device rate of plain copies of one expert block from the pinned
+    pool (hipMemcpyAsync, 20 copies)."""
+    import torch
+    host = torch.from_numpy(pool.view(np.uint8)[: w.expert_bytes])
+    dev = torch.empty(w.expert_bytes, dtype=torch.uint8, device="cuda")
+    dev.copy_(host, non_blocking=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(20):
+        dev.copy_(host, non_blocking=True)
+    torch.cuda.synchronize()
+    return 20 * w.expert_bytes / (time.perf_counter() - t0) / 1e9
+
+
+def phase_pass(w, pool, step_fn, make_ctx, args):
+    """Per-phase device times, outside the timed steps: a second context with
+    every operation timed (HIP events around each launch), the same warm-up,
+    then args.phase_steps steps over the timed steps' inputs.
+
+    Per phase: launches, microseconds per layer-iteration, and the rate of its
+    algorithmic bytes against HBM. Overlap efficiency over the layer-iterations
+    that transferred misses: sum of max(t_copy, t_compute) / sum of t_layer,
+    with t_layer the device time of the layer's launches, t_copy its
+    transferred bytes at the pinned host-to-device rate of plain copies, and
+    t_compute the mean t_layer of the layer-iterations without transfers
+    (same shapes, all work on cached experts); 1.0 means the copy hides all
+    compute or the compute hides all of the copy. Shader transfer only: with
+    copy-engine copies the layer's span is not the sum of its launches."""
+    import torch
+    from paper_2609_33385_amd import oled
+    ctx = make_ctx(oled.PROFILE_ALL)
+    try:
+        for g in range(args.warmup):
+            step_fn(ctx, g)
+        torch.cuda.synchronize()
+        ctx.profile_collect()
+        t0 = time.perf_counter()
+        for g in range(args.warmup, args.warmup + args.phase_steps):
+            step_fn(ctx, g)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        ops = ctx.profile_collect()
+    finally:
+        ctx.close()
+    groups = []
+    for o in ops:                        # a layer-iteration starts with its routing
+        if o[0] in ("route_topk", "route_gemm") or not groups:
+            groups.append([])
+        groups[-1].append(o)
+    n_li = max(1, len(groups))
+    phases = {}
+    for name in PHASES:
+        sel = [o for o in ops if o[0] == name]
+        if not sel:
+            continue
+        ms = sum(o[2] for o in sel)
+        by = sum(o[3] for o in sel)
+        gbs = (by / 1e9) / (ms / 1e3) if ms > 0 else None
+        phases[name] = {"launches": len(sel), "us_per_layer_iter": round(ms * 1e3 / n_li, 2),
+                        "avg_us": round(ms * 1e3 / len(sel), 2),
+                        "GBps": round(gbs, 1) if gbs else None,
+                        "hbm_frac": round(gbs / HBM_PEAK_GBS, 4) if gbs else None}
+        calm_sel = [o for o in sel if o[5] == 0]
+        if name != "h2d" and 0 < len(calm_sel) < len(sel):
+            # launches that also carried miss weights run as long as the PCIe reads
+            cms = sum(o[2] for o in calm_sel)
+            cgb = (sum(o[3] for o in calm_sel) / 1e9) / (cms / 1e3) if cms > 0 else None
+            phases[name]["without_transfer"] = {
+                "launches": len(calm_sel), "avg_us": round(cms * 1e3 / len(calm_sel), 2),
+                "GBps": round(cgb, 1) if cgb else None,
+                "hbm_frac": round(cgb / HBM_PEAK_GBS, 4) if cgb else None}
+    link = pinned_h2d_gbps(pool, w)
+    # launches on the compute stream (copy-engine copies run beside them)
+    t_layer = [sum(o[2] for o in gr if o[0] != "h2d") for gr in groups]
+    xfer = [sum(max(0, o[5]) for o in gr) for gr in groups]
+    calm = [t for t, b in zip(t_layer, xfer) if b == 0]
+    t_comp = float(np.mean(calm)) if calm else None
+    miss = [(t, b) for t, b in zip(t_layer, xfer) if b > 0]
+    overlap = None
+    if miss and t_comp is not None and args.copy_mode == "shader":
+        # every launch of a layer is on the compute stream, one after another,
+        # so their durations add up to the layer's device time
+        overlap = round(sum(max(b / (link * 1e6), t_comp) for t, b in miss)
+                        / sum(t for t, b in miss), 4)
+    return {"steps": args.phase_steps, "layer_iters": len(groups), "phases": phases,
+            "device_busy_frac": round(sum(t_layer) / 1e3 / wall, 4) if wall > 0 else None,
+            "layer_us_without_transfer": round(t_comp * 1e3, 2) if t_comp else None,
+            "layer_us_with_transfer": round(float(np.mean([t for t, b in miss])) * 1e3, 2)
+            if miss else None,
+            "pinned_h2d_GBps": round(link, 2), "overlap_efficiency": overlap}
+
+
 def cpu_baseline(w, seed: int):
     """The oracle on host cores: every layer of block 0, iterations 1-4, with the FFN."""
     from threadpoolctl import threadpool_info
@@ -199,6 +299,9 @@ def main():
     ap.add_argument("--coop-lambda", type=float, default=None,
                     help="lambda in microseconds per unit of priority (default: T_H2D)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--phase-steps", type=int, default=8,
+                    help="after the timed steps, this many steps on a second context with every "
+                         "operation timed: per-phase times and overlap efficiency (0: skip)")
     ap.add_argument("--calibration", action="store_true",
                     help="between warm-up and timed steps, run a plain streaming kernel of known traffic (torch "
                          "negation over 256 MiB fp32: 256 MiB read, 256 MiB written) to scale "
@@ -233,7 +336,7 @@ def main():
     t0 = time.time()
     pool = oled.PinnedPool(L * E, w.expert_bytes)
     fill_pool_device(pool, w, args.seed)
-    n_total = args.warmup + args.steps
+    n_total = args.warmup + max(args.steps, args.phase_steps)
     logits, xs, conf = make_inputs(w, args.seed, n_total)
     y = torch.empty((T, w.hidden), dtype=torch.bfloat16, device="cuda")
     prof = oled.profile_mask(*[o for o in args.profile_ops.split(",") if o])
@@ -241,12 +344,14 @@ def main():
     if args.coop:
         coop = profile_coop(w, pool, logits, xs, conf, args)
         log(f"coop split constants: {coop}")
-    ctx = oled.Context(w.hidden, w.inter, E, w.top_k, L, w.capacity, T, w.dtype, pool.ptr,
-                       pool.n_blocks, W.host_block_of(w, pool.n_blocks), profile_ops=prof,
-                       copy_mode=args.copy_mode, adapt_period=args.adapt_period, coop=coop)
+    def make_ctx(profile_ops):
+        return oled.Context(w.hidden, w.inter, E, w.top_k, L, w.capacity, T, w.dtype, pool.ptr,
+                            pool.n_blocks, W.host_block_of(w, pool.n_blocks),
+                            profile_ops=profile_ops, copy_mode=args.copy_mode,
+                            adapt_period=args.adapt_period, coop=coop)
+    ctx = make_ctx(prof)
     log(f"setup {time.time() - t0:.1f}s: pool {pool.n_blocks} x {w.expert_bytes >> 20} MiB pinned")
 
-    h = ctx.ctx
     s = torch.cuda.current_stream()
     sp = s.cuda_stream
     lg_p = [[logits[g, l].data_ptr() for l in range(L)] for g in range(n_total)]
@@ -254,7 +359,8 @@ def main():
     c_p = [conf[g].data_ptr() for g in range(n_total)]
     y_p = y.data_ptr()
 
-    def step(g):
+    def step_on(c, g):
+        h = c.ctx
         for l in range(L):
             if lib.route_block(h, l, lg_p[g][l], T, sp):
                 raise oled.OledError(1, oled.last_error(h))
@@ -267,6 +373,9 @@ def main():
                 raise oled.OledError(1, oled.last_error(h))
             if lib.score_and_retain(h, l, c_p[g], sp):
                 raise oled.OledError(1, oled.last_error(h))
+
+    def step(g):
+        step_on(ctx, g)
 
     for g in range(args.warmup):
         step(g)
@@ -372,6 +481,8 @@ def main():
         },
     }
     ctx.close()
+    if args.phase_steps > 0:
+        out["detail"]["phase_pass"] = phase_pass(w, pool, step_on, make_ctx, args)
     pool.free()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.seed)
