@@ -1,10 +1,12 @@
 """Summarises rocprofv3 runs of bench.py into the text summaries kept with the
 benchmark: per-kernel timings, and HBM traffic of the grouped gate/up GEMM.
 
-Input runs (CSV output, `-o run`), each with bench.py's --launch-log:
-  trace  rocprofv3 --kernel-trace --stats   -- python3 bench.py
-  fetch  rocprofv3 --pmc FETCH_SIZE         -- python3 bench.py --calibration --no-cpu-baseline
-  write  rocprofv3 --pmc WRITE_SIZE         -- python3 bench.py --calibration --no-cpu-baseline
+Input runs (CSV output, `-o run`), each with bench.py's --launch-log and
+--phase-steps 0 (no per-phase pass after the timed steps, so that the last
+gate/up dispatches are the timed ones):
+  trace  rocprofv3 --kernel-trace --stats   -- python3 bench.py --phase-steps 0
+  fetch  rocprofv3 --pmc FETCH_SIZE         -- python3 bench.py --phase-steps 0 --calibration --no-cpu-baseline
+  write  rocprofv3 --pmc WRITE_SIZE         -- python3 bench.py --phase-steps 0 --calibration --no-cpu-baseline
 
 `--calibration` runs torch's negation over 64 Mi fp32 (256 MiB read, 256 MiB
 written) between the warm-up and the timed steps. Its counter readings give
@@ -165,7 +167,7 @@ def main():
     args = ap.parse_args()
 
     trace_cmd = ("rocprofv3 --kernel-trace --stats --output-format csv -d <dir> -o run "
-                 "-- python3 bench.py --launch-log <dir>/launches.json")
+                 "-- python3 bench.py --phase-steps 0 --launch-log <dir>/launches.json")
     tb = last_json_line(args.trace_bench)
     with open(os.path.join(args.out, "k_ffn_up_llada40_kernel_stats.md"), "w") as f:
         f.write(summarise_trace(args.trace, tb, last_json_line(args.plain_bench),
@@ -181,7 +183,8 @@ def main():
     with open(FFN_SOURCE, "rb") as f:
         sha = hashlib.sha256(f.read()).hexdigest()
     pmc_cmd = ("timeout -s KILL 150 rocprofv3 --pmc {c} --output-format csv -d <dir> -o run "
-               "-- python3 bench.py --calibration --no-cpu-baseline --launch-log <dir>/launches.json")
+               "-- python3 bench.py --phase-steps 0 --calibration --no-cpu-baseline "
+               "--launch-log <dir>/launches.json")
     rec = {
         "kernel": "k_ffn UP=true (grouped gate/up SwiGLU GEMM)",
         "workload": "bf16 H2048 E64 k8 I1024, 16 layers, 32 tokens/iteration, cache 26/64",
