@@ -8,12 +8,14 @@
 // while enough wavefronts are in flight to cover HBM latency.
 //
 // Tile = one work item (up to 64 expert-sorted routes of one expert) x
-// 16 * 4 / KS output features. The 4 wavefronts of a workgroup form 4 / KS
-// feature groups of 16 and split K in KS contiguous parts (KS = 4, 2 or 1 by
-// the size of K); each streams its 16 (gate/up: 2 x 16) weight rows from HBM
-// straight into registers (A operand, M = features) and the token rows of its
-// K part from L2 (B operand, N = 16 tokens per MFMA tile); the KS partial
-// tiles are summed in LDS in a fixed order (deterministic). Expert weights are
+// 32 * 4 / KS output features. The 4 wavefronts of a workgroup form 4 / KS
+// feature groups of 2 x 16 and split K in KS contiguous parts (KS = 4, 2 or 1
+// by the size of K); each streams its 2 x 16 (gate/up: 2 x 2 x 16) weight rows
+// from HBM straight into registers (A operand, M = features) and the token
+// rows of its K part from L2 (B operand, N = 16 tokens per MFMA tile), each
+// token load feeding both runs of 16 features (half the L2 reads of the token
+// rows of one run per wavefront); the KS partial tiles are summed in LDS in a
+// fixed order (deterministic). Expert weights are
 // stored packed (see oled_pack_expert): the A fragment of one MFMA step is
 // 1 KiB of contiguous memory in lane order, so each wavefront streams one
 // contiguous range of its expert's block.
@@ -83,7 +85,8 @@ struct TrF32 {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = 4;
-constexpr int kFeat = 16;                  // output features per tile
+constexpr int kFeat = 16;                  // output features per 16-row weight fragment
+constexpr int kFG = 2;                     // runs of 16 features per wavefront (share token loads)
 constexpr int kMaxNT = kItemRows / 16;     // token tiles per item
 
 __device__ __forceinline__ u32x4_t ldg16(const void* p) {
@@ -102,37 +105,45 @@ __device__ __forceinline__ int xcd_order(int t, int total) {
   return x * q + (x < r ? x : r) + local;
 }
 
-// Streams one K range of a tile: NT token tiles, groups of U MFMA steps with
-// the next group's loads in flight while the current group multiplies (U is
-// smaller for more token tiles to keep registers, and so occupancy, in check).
-template <class TR, bool UP, int NT>
-__device__ __forceinline__ void stream_k(const typename TR::T* a1, const typename TR::T* a3,
+// Streams one K range of a tile: F groups of 16 weight rows (gate and up rows
+// for gate/up) against NT token tiles; every token load feeds all F groups.
+// Groups of U MFMA steps, the next group's loads in flight while the current
+// group multiplies (U shrinks as the loads per step grow, to keep registers,
+// and so occupancy, in check).
+template <class TR, bool UP, int NT, int F>
+__device__ __forceinline__ void stream_k(const typename TR::T* const* a1,
+                                         const typename TR::T* const* a3,
                                          const typename TR::T* const* b, int steps,
-                                         floatx4_t* acc1, floatx4_t* acc3) {
+                                         floatx4_t (*acc1)[NT], floatx4_t (*acc3)[NT]) {
   constexpr int SPAN = TR::SPAN;
-  constexpr int U = NT == 1 ? 4 : 2;
+  constexpr int VEC = F * (UP ? 2 : 1) + NT;        // 16-byte loads per lane per step
+  constexpr int U = VEC <= 3 ? 4 : (VEC <= 6 ? 2 : 1);
   const int groups = steps / U;
-  u32x4_t ra1[2][U], ra3[2][U], rb[2][U][NT];
+  u32x4_t ra1[2][U][F], ra3[2][U][F], rb[2][U][NT];
   constexpr int ASTEP = (UP ? 2 : 1) * 16 * SPAN;  // packed weights per MFMA step
   auto load = [&](int buf, int g0) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int kk = (g0 * U + u) * SPAN;
-      ra1[buf][u] = ldw16(a1 + (g0 * U + u) * ASTEP);
-      if (UP) ra3[buf][u] = ldw16(a3 + (g0 * U + u) * ASTEP);
+#pragma unroll
+      for (int j = 0; j < F; ++j) {
+        ra1[buf][u][j] = ldw16(a1[j] + (g0 * U + u) * ASTEP);
+        if (UP) ra3[buf][u][j] = ldw16(a3[j] + (g0 * U + u) * ASTEP);
+      }
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) rb[buf][u][nt] = ldg16(b[nt] + kk);
     }
   };
   auto mult = [&](int buf) {
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
+    for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        TR::mma(acc1[nt], ra1[buf][u], rb[buf][u][nt]);
-        if (UP) TR::mma(acc3[nt], ra3[buf][u], rb[buf][u][nt]);
-      }
-    }
+      for (int j = 0; j < F; ++j)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          TR::mma(acc1[j][nt], ra1[buf][u][j], rb[buf][u][nt]);
+          if (UP) TR::mma(acc3[j][nt], ra3[buf][u][j], rb[buf][u][nt]);
+        }
   };
   if (groups > 0) load(0, 0);
   int gi = 0;
@@ -146,14 +157,20 @@ __device__ __forceinline__ void stream_k(const typename TR::T* a1, const typenam
   // remaining steps (K range not a multiple of U steps)
   for (int st = groups * U; st < steps; ++st) {
     const int kk = st * SPAN;
-    const u32x4_t x1 = ldw16(a1 + st * ASTEP);
-    u32x4_t x3;
-    if (UP) x3 = ldw16(a3 + st * ASTEP);
+    u32x4_t x1[F], x3[F];
+#pragma unroll
+    for (int j = 0; j < F; ++j) {
+      x1[j] = ldw16(a1[j] + st * ASTEP);
+      if (UP) x3[j] = ldw16(a3[j] + st * ASTEP);
+    }
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const u32x4_t bv = ldg16(b[nt] + kk);
-      TR::mma(acc1[nt], x1, bv);
-      if (UP) TR::mma(acc3[nt], x3, bv);
+#pragma unroll
+      for (int j = 0; j < F; ++j) {
+        TR::mma(acc1[j][nt], x1[j], bv);
+        if (UP) TR::mma(acc3[j][nt], x3[j], bv);
+      }
     }
   }
 }
@@ -188,10 +205,12 @@ __device__ __forceinline__ void store_tile(const WorkItem& it, int nt, int f0, c
   }
 }
 
-// One tile of 16 * (4 / KS) output features. Wavefront w takes feature group
-// w / KS and K part w % KS; with KS > 1 the KS partial tiles of a feature
-// group are summed in LDS in a fixed order and the parts share the epilogue.
-template <class TR, bool UP, int KS, int NT>
+// One tile of 16 * F * (4 / KS) output features. Wavefront w takes feature
+// group w / KS (F runs of 16 features) and K part w % KS; with KS > 1 the KS
+// partial tiles of each run of 16 features are summed in LDS in a fixed order
+// and the parts share the epilogue. Which workgroup computes a feature does not
+// change its arithmetic: the K split is a function of the GEMM alone.
+template <class TR, bool UP, int KS, int NT, int F>
 __device__ __forceinline__ void run_tile(const WorkItem& it, int tile_f0, const typename TR::T* W,
                                          const typename TR::T* __restrict__ src,
                                          const int32_t* __restrict__ perm, int k, int H, int I,
@@ -203,7 +222,7 @@ __device__ __forceinline__ void run_tile(const WorkItem& it, int tile_f0, const 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lr = lane & 15, g = lane >> 4;
   const int fg = wave / KS, kp = wave % KS;
-  const int f0 = tile_f0 + kFeat * fg;
+  const int f0 = tile_f0 + kFeat * F * fg;
   const int Kdim = UP ? H : I;
   const int kw = Kdim / KS;
   const int kbeg = kp * kw;
@@ -212,15 +231,20 @@ __device__ __forceinline__ void run_tile(const WorkItem& it, int tile_f0, const 
   // packed expert block: one 16-row x SPAN-k fragment per MFMA step, stored in
   // the order the lanes consume it, so a wavefront load reads 1 KiB contiguously
   constexpr int FRAG = 16 * TR::SPAN;
-  const T* a1;
-  const T* a3;
-  if (UP) {
-    a1 = W + (static_cast<size_t>(f0 / 16) * (H / TR::SPAN) + kbeg / TR::SPAN) * 2 * FRAG + lane * EPV;
-    a3 = a1 + FRAG;
-  } else {
-    a1 = W + static_cast<size_t>(2) * I * H +
-         (static_cast<size_t>(f0 / 16) * (I / TR::SPAN) + kbeg / TR::SPAN) * FRAG + lane * EPV;
-    a3 = a1;
+  const T* a1[F];
+  const T* a3[F];
+#pragma unroll
+  for (int j = 0; j < F; ++j) {
+    const int fj = f0 + kFeat * j;
+    if (UP) {
+      a1[j] = W + (static_cast<size_t>(fj / 16) * (H / TR::SPAN) + kbeg / TR::SPAN) * 2 * FRAG +
+              lane * EPV;
+      a3[j] = a1[j] + FRAG;
+    } else {
+      a1[j] = W + static_cast<size_t>(2) * I * H +
+              (static_cast<size_t>(fj / 16) * (I / TR::SPAN) + kbeg / TR::SPAN) * FRAG + lane * EPV;
+      a3[j] = a1[j];
+    }
   }
   // token rows past the item's end read its last row; their results are dropped
   const T* b[NT];
@@ -231,35 +255,43 @@ __device__ __forceinline__ void run_tile(const WorkItem& it, int tile_f0, const 
     b[nt] = (UP ? src + static_cast<size_t>(perm[pos] / k) * H : src + static_cast<size_t>(pos) * I) +
             kbeg + EPV * g;
   }
-  floatx4_t acc1[NT], acc3[NT];
+  floatx4_t acc1[F][NT], acc3[F][NT];
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    acc1[nt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
-    acc3[nt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
-  }
-  stream_k<TR, UP, NT>(a1, a3, b, kw / TR::SPAN, acc1, acc3);
+  for (int j = 0; j < F; ++j)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      acc1[j][nt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+      acc3[j][nt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+    }
+  stream_k<TR, UP, NT, F>(a1, a3, b, kw / TR::SPAN, acc1, acc3);
 
   if constexpr (KS == 1) {
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) store_tile<TR, UP>(it, nt, f0, acc1[nt], acc3[nt], H, I, hout, oout);
+    for (int j = 0; j < F; ++j)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+        store_tile<TR, UP>(it, nt, f0 + kFeat * j, acc1[j][nt], acc3[j][nt], H, I, hout, oout);
   } else {
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      s_red[wave][nt][lane] = acc1[nt];
-      if (UP) s_red[wave][kMaxNT + nt][lane] = acc3[nt];
-    }
-    __syncthreads();
-    for (int nt = kp; nt < NT; nt += KS) {
-      floatx4_t s1 = s_red[fg * KS][nt][lane];
-      floatx4_t s3 = UP ? s_red[fg * KS][kMaxNT + nt][lane] : floatx4_t{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < F; ++j) {
 #pragma unroll
-      for (int j = 1; j < KS; ++j) {
-        s1 += s_red[fg * KS + j][nt][lane];
-        if (UP) s3 += s_red[fg * KS + j][kMaxNT + nt][lane];
+      for (int nt = 0; nt < NT; ++nt) {
+        s_red[wave][nt][lane] = acc1[j][nt];
+        if (UP) s_red[wave][kMaxNT + nt][lane] = acc3[j][nt];
       }
-      store_tile<TR, UP>(it, nt, f0, s1, s3, H, I, hout, oout);
+      __syncthreads();
+      for (int nt = kp; nt < NT; nt += KS) {
+        floatx4_t s1 = s_red[fg * KS][nt][lane];
+        floatx4_t s3 = UP ? s_red[fg * KS][kMaxNT + nt][lane] : floatx4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int q = 1; q < KS; ++q) {
+          s1 += s_red[fg * KS + q][nt][lane];
+          if (UP) s3 += s_red[fg * KS + q][kMaxNT + nt][lane];
+        }
+        store_tile<TR, UP>(it, nt, f0 + kFeat * j, s1, s3, H, I, hout, oout);
+      }
+      __syncthreads();  // s_red is reused by the next run of features / tile
     }
-    __syncthreads();  // s_red is reused by the next tile
   }
 }
 
@@ -304,7 +336,7 @@ template <class TR, bool UP, int KS>
 __device__ __forceinline__ void gemm_tiles(const FfnLaunch& a, int t0, int stride,
                                            floatx4_t (*s_red)[(UP ? 2 : 1) * kMaxNT][64]) {
   using T = typename TR::T;
-  constexpr int FEAT = kFeat * (kWaves / KS);  // output features per tile
+  constexpr int FEAT = kFeat * kFG * (kWaves / KS);  // output features per tile
   int base, n_items;
   if (a.n_items_host >= 0) {
     base = a.item_base;
@@ -328,10 +360,10 @@ __device__ __forceinline__ void gemm_tiles(const FfnLaunch& a, int t0, int strid
     const T* W = reinterpret_cast<const T*>(static_cast<const char*>(a.pool) +
                                             static_cast<int64_t>(slot) * a.slot_bytes);
     switch ((it.rows + 15) >> 4) {
-      case 1: run_tile<TR, UP, KS, 1>(it, f0, W, src, a.perm, a.k, a.H, a.I, hout, a.oout, s_red); break;
-      case 2: run_tile<TR, UP, KS, 2>(it, f0, W, src, a.perm, a.k, a.H, a.I, hout, a.oout, s_red); break;
-      case 3: run_tile<TR, UP, KS, 3>(it, f0, W, src, a.perm, a.k, a.H, a.I, hout, a.oout, s_red); break;
-      default: run_tile<TR, UP, KS, 4>(it, f0, W, src, a.perm, a.k, a.H, a.I, hout, a.oout, s_red); break;
+      case 1: run_tile<TR, UP, KS, 1, kFG>(it, f0, W, src, a.perm, a.k, a.H, a.I, hout, a.oout, s_red); break;
+      case 2: run_tile<TR, UP, KS, 2, kFG>(it, f0, W, src, a.perm, a.k, a.H, a.I, hout, a.oout, s_red); break;
+      case 3: run_tile<TR, UP, KS, 3, kFG>(it, f0, W, src, a.perm, a.k, a.H, a.I, hout, a.oout, s_red); break;
+      default: run_tile<TR, UP, KS, 4, kFG>(it, f0, W, src, a.perm, a.k, a.H, a.I, hout, a.oout, s_red); break;
     }
   }
 }
@@ -702,7 +734,7 @@ template <class TR, bool UP, int KS>
 hipError_t launch_ffn_ks(const FfnLaunch& a, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
   if (a.fetch.nblk % 8) return hipErrorInvalidValue;
   const int64_t grid = static_cast<int64_t>(a.fetch.nblk) +
-                       part_grid(a, (UP ? a.I : a.H) / (kFeat * (kWaves / KS)));
+                       part_grid(a, (UP ? a.I : a.H) / (kFeat * kFG * (kWaves / KS)));
   if (grid <= 0) return hipSuccess;
   hipExtLaunchKernelGGL(k_ffn<TR, UP, KS>, dim3(static_cast<unsigned>(grid)), dim3(kThreads), 0, s,
                         ev0, ev1, 0, a);
@@ -721,8 +753,8 @@ template <class TR, int KSD, int KSU>
 hipError_t launch_mix_ks(const FfnLaunch& d, const FfnLaunch& u, hipEvent_t ev0, hipEvent_t ev1,
                          hipStream_t s) {
   if (d.fetch.nblk % 8) return hipErrorInvalidValue;
-  const int gd = part_grid(d, d.H / (kFeat * (kWaves / KSD)));
-  const int gu = part_grid(u, u.I / (kFeat * (kWaves / KSU)));
+  const int gd = part_grid(d, d.H / (kFeat * kFG * (kWaves / KSD)));
+  const int gu = part_grid(u, u.I / (kFeat * kFG * (kWaves / KSU)));
   const int64_t grid = static_cast<int64_t>(d.fetch.nblk) + gd + gu;
   if (grid <= 0) return hipSuccess;
   hipExtLaunchKernelGGL(k_ffn_mix<TR, KSD, KSU>, dim3(static_cast<unsigned>(grid)), dim3(kThreads),
