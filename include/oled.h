@@ -410,7 +410,10 @@ oled_status oled_coop_dispatch(int32_t n_experts, const uint8_t* miss, const int
  *  cooperative compensation). block: packed expert block (oled_pack_expert
  *  layout, dtype); x: [n][H] token rows in dtype; out: [n][H] fp32.
  *  Accumulates in fp32; silu(W1 x) * (W3 x) is rounded to dtype as the GPU
- *  stores it. threads >= 1 host threads. Needs AVX2 and FMA.
+ *  stores it. threads >= 1 host threads: the first call with a given count
+ *  starts them, later calls reuse them (calls from several threads take
+ *  turns). Needs AVX2 and FMA; bf16 uses AVX-512 BF16 dot products where the
+ *  CPU has them (environment OLED_CPU_FFN_AVX2=1 forces the AVX2 kernels).
  *  Errors: INVALID_ARG (NULL pointers, n < 0, threads < 1, bad dtype),
  *  UNSUPPORTED (shape, or the CPU lacks AVX2/FMA).
  */

@@ -29,7 +29,9 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <map>
 #include <memory>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -1581,9 +1583,14 @@ oled_status oled_cpu_ffn(int32_t dtype, int32_t hidden, int32_t inter, const voi
   std::vector<int32_t> rows(n);
   for (int i = 0; i < n; ++i) rows[i] = i;
   oled::CpuExpertJob job{block, rows.data(), n, out};
-  oled::ThreadPool pool(threads);
+  // thread pools live until the process ends, one per thread count
+  static std::mutex mu;
+  static std::map<int, std::unique_ptr<oled::ThreadPool>> pools;
+  std::lock_guard<std::mutex> lk(mu);
+  std::unique_ptr<oled::ThreadPool>& pool = pools[threads];
+  if (!pool) pool.reset(new oled::ThreadPool(threads));
   std::vector<float> scratch;
-  oled::cpu_ffn_run(pool, dtype == OLED_BF16, hidden, inter, x, &job, 1, scratch);
+  oled::cpu_ffn_run(*pool, dtype == OLED_BF16, hidden, inter, x, &job, 1, scratch);
   return OLED_OK;
 }
 

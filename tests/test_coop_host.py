@@ -18,10 +18,17 @@ def _rel(a, b):
     return float(np.linalg.norm(a - b) / np.linalg.norm(b))
 
 
+@pytest.mark.parametrize("isa", ["auto", "avx2"])
 @pytest.mark.parametrize("dtype,H,I,n,threads", [("bf16", 256, 512, 1, 1), ("bf16", 512, 256, 13, 4),
-                                                 ("bf16", 2048, 1024, 3, 8), ("f32", 256, 128, 7, 3),
-                                                 ("f32", 128, 384, 20, 1)])
-def test_cpu_ffn_matches_oracle(dtype, H, I, n, threads):
+                                                 ("bf16", 2048, 1024, 3, 8), ("bf16", 256, 256, 29, 3),
+                                                 ("f32", 256, 128, 7, 3), ("f32", 128, 384, 20, 1)])
+def test_cpu_ffn_matches_oracle(dtype, H, I, n, threads, isa, monkeypatch):
+    """Both bf16 kernels: AVX-512 BF16 dot products where the CPU has them
+    ("auto"), and the AVX2 kernels (forced)."""
+    if isa == "avx2":
+        monkeypatch.setenv("OLED_CPU_FFN_AVX2", "1")
+    else:
+        monkeypatch.delenv("OLED_CPU_FFN_AVX2", raising=False)
     w = W.WORKLOADS[1].replace(wid=340, dtype=dtype, hidden=H, inter=I)
     raw = W.expert_block(w, 0, 3)
     w13, w2 = W.split_expert(w, raw)
