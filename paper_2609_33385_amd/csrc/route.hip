@@ -281,7 +281,8 @@ __device__ __forceinline__ void rank_chunk(const int32_t* idx, int t0, int t1, i
 // system-scope fence, seq).
 __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, int bad,
                                              const PermuteOut& o, const int32_t* s_free,
-                                             const int32_t* s_ftop,
+                                             const int32_t* s_ftop, const uint32_t* s_res,
+                                             const uint32_t* s_pm,
                                              int32_t* __restrict__ chunk_base = nullptr,
                                              int n_chunks = 0) {
   __shared__ int32_t s_cnt[kMaxExperts];
@@ -293,7 +294,6 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
   __shared__ int32_t s_dshort[kMaxExperts];  // its short dense item, or -1
   __shared__ int32_t s_sexp[kMaxExperts];
   __shared__ int32_t s_sslot[kMaxExperts];
-  __shared__ uint32_t s_res[kMaxExperts / 32];
   __shared__ uint32_t s_mask[kMaxExperts * kChunkWords];
   __shared__ int32_t s_pre[kMaxExperts * kChunkWords];
 
@@ -302,7 +302,6 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
   const int E = o.E, layer = o.layer;
   const int R = T * k;
   for (int e = tid; e < kMaxExperts; e += nthr) s_cnt[e] = 0;
-  if (tid < kMaxExperts / 32) s_res[tid] = o.cv.res[layer].bits[tid];
   __syncthreads();
   if (chunk_base) {   // counts per chunk in chunk_base [n_chunks][E], from other workgroups
     for (int e = tid; e < E; e += nthr) {
@@ -323,7 +322,6 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
     bool hit[4], miss[4], dn[4];
     int sc = 0, sh = 0, sm = 0, sx = 0, sdf = 0, sds = 0;
     int n_act = 0, n_hit = 0, n_res = 0, hrows = 0, mrows = 0, n_px = 0, n_rx = 0;
-    const ExpertMask pmask = o.cv.prev_miss[layer];   // transferred at the previous iteration
     int n_dense = 0, n_dhit = 0, drows = 0, dhrows = 0;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -349,7 +347,7 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
       n_act += c[q] > 0 ? 1 : 0;
       n_hit += hit[q] ? 1 : 0;
       n_res += res ? 1 : 0;
-      const bool pm = e < E && pmask.test(e);
+      const bool pm = e < E && ((s_pm[e >> 5] >> (e & 31)) & 1u);   // transferred last time
       n_px += pm ? 1 : 0;
       n_rx += pm && hit[q] ? 1 : 0;   // retained (resident now) and activated again
       hrows += hit[q] ? c[q] : 0;
@@ -556,9 +554,15 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
 
 // One wavefront loads the free-slot list's top (free_top and up to E entries
 // below it) into LDS ahead of the staging.
-__device__ __forceinline__ void prefetch_free(const CacheView& cv, int E, int32_t* s_free,
-                                              int32_t* s_ftop) {
+// One wavefront reads the cache state the planning step needs into LDS: the
+// layer's resident set and the experts transferred at its previous iteration
+// (words), and the top of the free-slot list.
+__device__ __forceinline__ void prefetch_state(const CacheView& cv, int E, int layer,
+                                               int32_t* s_free, int32_t* s_ftop, uint32_t* s_res,
+                                               uint32_t* s_pm) {
   const int lane = threadIdx.x & 63;
+  if (lane < kMaxExperts / 32) s_res[lane] = cv.res[layer].bits[lane];
+  else if (lane < kMaxExperts / 16) s_pm[lane - kMaxExperts / 32] = cv.prev_miss[layer].bits[lane - kMaxExperts / 32];
   const int ft = cv.hdr->free_top;
   if (ft >= 0 && ft <= cv.n_slots) {
 #pragma unroll
@@ -576,11 +580,12 @@ __global__ __launch_bounds__(kPermThreads) void k_permute(const int32_t* __restr
                                                           PermuteOut o) {
   __shared__ int32_t s_free[kMaxExperts];
   __shared__ int32_t s_ftop;
+  __shared__ uint32_t s_res[kMaxExperts / 32], s_pm[kMaxExperts / 32];
   const int bad = *bad_flag;
-  if ((threadIdx.x >> 6) == 1) prefetch_free(o.cv, o.E, s_free, &s_ftop);
+  if ((threadIdx.x >> 6) == 1) prefetch_state(o.cv, o.E, o.layer, s_free, &s_ftop, s_res, s_pm);
   __syncthreads();
   if (threadIdx.x == 0) *bad_flag = 0;
-  permute_body(topk_idx, T, k, bad, o, s_free, &s_ftop);
+  permute_body(topk_idx, T, k, bad, o, s_free, &s_ftop, s_res, s_pm);
 }
 
 // Large blocks, first launch: workgroup c counts the routes of tokens
@@ -598,9 +603,12 @@ __global__ __launch_bounds__(kPermThreads) void k_perm_hist(const int32_t* __res
   __shared__ int32_t s_free[kMaxExperts];
   __shared__ int32_t s_ftop;
   __shared__ int32_t s_last;
+  __shared__ uint32_t s_res[kMaxExperts / 32], s_pm[kMaxExperts / 32];
   const int E = o.E, tid = threadIdx.x, nthr = blockDim.x;
   const int ch = blockIdx.x, n_chunks = gridDim.x;
   for (int e = tid; e < kMaxExperts; e += nthr) s_h[e] = 0;
+  // the cache state the last workgroup plans with, read while chunks count
+  if ((tid >> 6) == 1) prefetch_state(o.cv, E, o.layer, s_free, &s_ftop, s_res, s_pm);
   __syncthreads();
   const int t0 = ch * kChunkTokens, t1 = min(T, t0 + kChunkTokens);
   for (int r = t0 * k + tid; r < t1 * k; r += nthr) atomicAdd(&s_h[topk_idx[r]], 1);
@@ -613,13 +621,11 @@ __global__ __launch_bounds__(kPermThreads) void k_perm_hist(const int32_t* __res
   if (!s_last) return;
   __threadfence();   // see every other chunk's counts
   const int bad = __hip_atomic_load(bad_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  if ((tid >> 6) == 1) prefetch_free(o.cv, E, s_free, &s_ftop);
-  __syncthreads();
   if (tid == 0) {   // re-arm for the next launch (stream order)
     *bad_flag = 0;
     *counter = 0;
   }
-  permute_body(topk_idx, T, k, bad, o, s_free, &s_ftop, chunk_base, n_chunks);
+  permute_body(topk_idx, T, k, bad, o, s_free, &s_ftop, s_res, s_pm, chunk_base, n_chunks);
 }
 
 // Large blocks, second launch: workgroup c ranks the routes of its chunk from
@@ -653,8 +659,12 @@ __global__ __launch_bounds__(256) void k_route_fused(const float* __restrict__ l
   __shared__ int32_t s_free[kMaxExperts];
   __shared__ int32_t s_ftop;
   __shared__ int32_t s_last;
+  __shared__ uint32_t s_res[kMaxExperts / 32], s_pm[kMaxExperts / 32];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int E = o.E;
+  // the cache state the last workgroup plans with, read while the tokens are
+  // routed (no kernel of this launch changes it before the planning step)
+  if (wave == 3) prefetch_state(o.cv, E, o.layer, s_free, &s_ftop, s_res, s_pm);
   int bad = 0;
   for (int t = blockIdx.x * 4 + wave; t < T; t += gridDim.x * 4) {
     float g;
@@ -671,19 +681,15 @@ __global__ __launch_bounds__(256) void k_route_fused(const float* __restrict__ l
   __syncthreads();
   if (!s_last) return;
   __threadfence();   // see every other workgroup's routes
-  if (wave == 3) {
-    prefetch_free(o.cv, E, s_free, &s_ftop);
-  } else {
-    for (int r = threadIdx.x; r < T * k; r += 192) s_idx[r] = __hip_atomic_load(
-        &topk_idx[r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
+  for (int r = threadIdx.x; r < T * k; r += 256) s_idx[r] = __hip_atomic_load(
+      &topk_idx[r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   const int any_bad = __hip_atomic_load(&sync[1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   __syncthreads();
   if (threadIdx.x == 0) {  // re-arm for the next launch (stream order)
     sync[0] = 0;
     sync[1] = 0;
   }
-  permute_body(s_idx, T, k, any_bad, o, s_free, &s_ftop);
+  permute_body(s_idx, T, k, any_bad, o, s_free, &s_ftop, s_res, s_pm);
 }
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
