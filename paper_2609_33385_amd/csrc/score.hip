@@ -71,26 +71,51 @@ __device__ __forceinline__ void score_sums(const ScoreArgs& a, int r0, int r1,
   if (bad) atomicOr(s_bad, 1);
 }
 
+// The cache state a commit reads, loaded into LDS by the committing workgroup
+// (before it sums the routes, when it is the only part), so that its global
+// reads overlap the sums instead of following one another. Nothing else in
+// the launch writes it.
+struct ScoreState {
+  uint32_t res[kMaxExperts / 32];
+  uint32_t cpu[kMaxExperts / 32];   // CPU-executed misses: no candidates
+  int32_t cnt[kMaxExperts];         // routes per expert
+  int32_t slot[kMaxExperts];        // the layer's slot table
+  int32_t cap, iters, free_top, route_bad;
+};
+
+__device__ __forceinline__ void score_prefetch(const ScoreArgs& a, ScoreState& st) {
+  const CacheView& cv = a.cv;
+  const int tid = threadIdx.x, E = a.E, layer = a.layer;
+  for (int e = tid; e < E; e += kThreads) {
+    st.cnt[e] = a.counts[e];
+    st.slot[e] = cv.slot_of[static_cast<size_t>(layer) * E + e];
+  }
+  if (tid < kMaxExperts / 32) {
+    st.res[tid] = cv.res[layer].bits[tid];
+    st.cpu[tid] = cv.cpu_exec ? cv.cpu_exec[layer].bits[tid] : 0u;
+  } else if (tid == kMaxExperts / 32) {
+    st.cap = cv.cap[layer];
+    st.iters = cv.iters[layer];
+    st.free_top = cv.hdr->free_top;
+    st.route_bad = cv.hdr->route_bad;
+  }
+}
+
 // Ranking, retention and commit of one layer from its numerators in s_S (and
-// *s_bad), by one workgroup.
+// *s_bad) and the prefetched state st, by one workgroup.
 __device__ __forceinline__ void score_commit(const ScoreArgs& a, unsigned long long* s_S,
-                                             int32_t* p_bad) {
-  const int32_t* __restrict__ counts = a.counts;
+                                             int32_t* p_bad, const ScoreState& st) {
+  const int32_t* __restrict__ counts = st.cnt;
   const int E = a.E, layer = a.layer;
   const CacheView& cv = a.cv;
-  const int C = cv.cap[layer];
+  const int C = st.cap;
   uint64_t* __restrict__ score_out = a.score_out;
   RetainOut* __restrict__ out = a.out;
   __shared__ uint32_t s_rc[kMaxExperts];  // bit 1: previously resident, bit 0: candidate
   __shared__ int32_t s_rank[kMaxExperts];
-  __shared__ uint32_t s_res[kMaxExperts / 32];
-  __shared__ uint32_t s_cpu[kMaxExperts / 32];   // CPU-executed misses: no candidates
+  const uint32_t* s_res = st.res;
+  const uint32_t* s_cpu = st.cpu;
   const int tid = threadIdx.x;
-  if (tid < kMaxExperts / 32) {
-    s_res[tid] = cv.res[layer].bits[tid];
-    s_cpu[tid] = cv.cpu_exec ? cv.cpu_exec[layer].bits[tid] : 0u;
-  }
-  __syncthreads();
   for (int e = tid; e < kMaxExperts; e += kThreads) {
     s_rank[e] = 0;
     const bool r = e < E && ((s_res[e >> 5] >> (e & 31)) & 1u);
@@ -101,13 +126,13 @@ __device__ __forceinline__ void score_commit(const ScoreArgs& a, unsigned long l
   // (s_rc and s_rank are next read after the barrier that follows the keys)
   const int s_bad = *p_bad;
   CacheHdr* hdr = cv.hdr;
-  const bool commit = !s_bad && !hdr->route_bad;
+  const bool commit = !s_bad && !st.route_bad;
 
   // The retention key: S under the paper's priority; under LRU / LFU the
   // layer's history, advanced by this iteration's routing when it commits
   // (the iteration of the last activation, or the routes so far).
   __shared__ unsigned long long s_K[kMaxExperts];
-  const int it_now = cv.iters[layer] + 1;
+  const int it_now = st.iters + 1;
   for (int e = tid; e < E; e += kThreads) {
     if (cv.policy == 0) {
       s_K[e] = s_S[e];
@@ -153,7 +178,7 @@ __device__ __forceinline__ void score_commit(const ScoreArgs& a, unsigned long l
   const int lane = tid;
   constexpr int Q = kMaxExperts / 64;
   int32_t* slot_row = cv.slot_of + static_cast<size_t>(layer) * E;
-  int top = hdr->free_top;
+  int top = st.free_top;
   int fault = 0;
   uint32_t word[kMaxExperts / 32];
 #pragma unroll
@@ -164,7 +189,7 @@ __device__ __forceinline__ void score_commit(const ScoreArgs& a, unsigned long l
     const int e = lane + 64 * q;
     const bool was = e < E && (s_rc[e] & 2u);
     bool keep = commit ? (e < E && (s_rc[e] & 1u) && s_rank[e] < C) : was;
-    const int sl = e < E ? slot_row[e] : -1;
+    const int sl = e < E ? st.slot[e] : -1;
     if (keep && sl < 0) {
       fault |= 4;
       keep = false;
@@ -255,15 +280,17 @@ __device__ __forceinline__ void score_part(const ScoreArgs& a, int part) {
   __shared__ unsigned long long s_S[kMaxExperts];
   __shared__ int32_t s_bad;
   __shared__ int32_t s_last;
+  __shared__ ScoreState st;
   const int tid = threadIdx.x, E = a.E;
   const int R = a.T * a.k;
   for (int e = tid; e < kMaxExperts; e += kThreads) s_S[e] = 0ull;
   if (tid == 0) s_bad = 0;
+  if (a.parts <= 1) score_prefetch(a, st);
   __syncthreads();
   if (a.parts <= 1) {
     score_sums(a, 0, R, s_S, &s_bad);
     __syncthreads();
-    score_commit(a, s_S, &s_bad);
+    score_commit(a, s_S, &s_bad, st);
     return;
   }
   const int r0 = part * kScoreRoutes;
@@ -287,8 +314,9 @@ __device__ __forceinline__ void score_part(const ScoreArgs& a, int part) {
     a.acc_sync[0] = 0;
     a.acc_sync[1] = 0;
   }
+  score_prefetch(a, st);
   __syncthreads();
-  score_commit(a, s_S, &s_bad);
+  score_commit(a, s_S, &s_bad, st);
 }
 
 __global__ __launch_bounds__(kThreads) void k_score_retain(ScoreArgs a) {
