@@ -286,9 +286,15 @@ def main():
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--capacity", type=int, default=None, help="experts cached per layer")
-    ap.add_argument("--workload", type=int, default=2, choices=[2, 3],
+    ap.add_argument("--workload", type=int, default=2, choices=[2, 3, 4, 5],
                     help="2: the 40%% stack with 32 tokens per iteration (the headline); 3: the "
-                         "same stack with batch 8 x block 32 = 256 tokens per iteration")
+                         "same stack with batch 8 x block 32 = 256 tokens per iteration; 4: the "
+                         "E=128 stack (hidden 4096, 48 layers, 1024 tokens, Zipf popularity, "
+                         "40%%); 5: its stress form (20%%, iteration noise 1.5). 4 and 5 alias "
+                         "their experts onto --pool-blocks host blocks and take minutes per "
+                         "few steps: pass small --warmup/--steps")
+    ap.add_argument("--pool-blocks", type=int, default=None,
+                    help="distinct pinned host blocks (default: every expert, up to 16 GiB)")
     ap.add_argument("--adapt-period", type=int, default=0,
                     help="layer-adaptive cache sizing every N iterations (0: fixed capacity "
                          "per layer, the headline configuration)")
@@ -334,7 +340,8 @@ def main():
     lib = oled.load()
 
     t0 = time.time()
-    pool = oled.PinnedPool(L * E, w.expert_bytes)
+    n_blocks = args.pool_blocks or min(L * E, (16 << 30) // w.expert_bytes)
+    pool = oled.PinnedPool(n_blocks, w.expert_bytes)
     fill_pool_device(pool, w, args.seed)
     n_total = args.warmup + max(args.steps, args.phase_steps)
     logits, xs, conf = make_inputs(w, args.seed, n_total)
@@ -447,12 +454,16 @@ def main():
                                 f"batch {w.batch} x block {w.block} tokens, {w.n_iters} denoising "
                                 f"iterations per block, expert cache {w.capacity}/{E} "
                                 f"({round(100 * w.capacity / E)}%) per layer"
+                                + (f", router logits with Zipf({w.zipf_s}) expert popularity"
+                                   if w.zipf_s else "")
+                                + (f", iteration noise N(0, {w.sigma_it})"
+                                   if w.sigma_it != 0.3 else "")
                                 + (", cooperative CPU compensation" if coop else "")
                                 + (f", layer-adaptive sizing every {args.adapt_period} iterations"
                                    if args.adapt_period else "")),
                    "hidden": w.hidden, "n_experts": E, "top_k": w.top_k, "inter": w.inter,
                    "n_layers": L, "tokens_per_iteration": T, "iterations_per_block": w.n_iters,
-                   "capacity": w.capacity},
+                   "capacity": w.capacity, "host_pool_blocks": n_blocks},
         "roofline": {"kernel": "grouped gate/up SwiGLU GEMM (k_ffn up), launches that moved no "
                                "miss weights", "bound": "hbm",
                      "achieved": round(up_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -484,7 +495,8 @@ def main():
     if args.phase_steps > 0:
         out["detail"]["phase_pass"] = phase_pass(w, pool, step_on, make_ctx, args)
     pool.free()
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.workload <= 3:
+        # (the E=128 stacks' float64 oracle takes minutes per layer-iteration)
         out["cpu_baseline"] = cpu_baseline(w, args.seed)
     print(json.dumps(out), flush=True)
 

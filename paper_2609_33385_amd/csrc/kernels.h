@@ -231,8 +231,11 @@ hipError_t launch_ffn_mix(bool bf16, const FfnLaunch& d, const FfnLaunch& u, hip
 // their weights are in their slots. Items of kDenseRows rows first
 // (item_counts[0] of them), then one shorter item per expert
 // (item_counts[1]); up: 128 features x 256 rows per workgroup, down: 256 x
-// 256. Those experts have no items in the streaming lists.
-constexpr int kDenseMinRows = 128;
+// 256. Those experts have no items in the streaming lists. The threshold is
+// one row above a streaming work item: an expert the streaming kernels would
+// split into two items (each reading all of its weights) runs as one dense
+// item instead.
+constexpr int kDenseMinRows = kItemRows + 1;
 constexpr int kDenseRows = 256;
 hipError_t launch_ffn_dense(bool up, const FfnLaunch& a, hipEvent_t ev0, hipEvent_t ev1,
                             hipStream_t s);
