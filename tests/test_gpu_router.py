@@ -123,3 +123,43 @@ def test_gate_logits_wide_tiles(dtype, batch, block, E, H):
     finally:
         ctx.close()
         pool.free()
+
+
+def test_gate_error_paths():
+    """route_block_gate's argument and state checks, and a non-finite token
+    row: its logits are non-finite, so the block is refused like a bad block
+    of logits and the cache state does not change."""
+    w = W.WORKLOADS[2].replace(wid=362, name="gate-errors", n_layers=2, n_iters=2, hidden=256,
+                               inter=128, capacity=26)
+    T, H = w.tokens, w.hidden
+    pool = HN.fill_pool(w, 0, 4)
+    ctx = HN.make_context(w, pool)
+    s = torch.cuda.current_stream()
+    try:
+        xh = W.activations(w, 0, 0, 0, 0)
+        x, g = HN.to_device(xh), HN.to_device(W.gate_weights(w, 0, 0))
+        conf = torch.from_numpy(W.confidence(w, 0, 0, 0)).cuda()
+        assert oled.route_block_gate(ctx.ctx, 0, None, g, T, s) == oled.OLED_ERR_INVALID_ARG
+        assert oled.route_block_gate(ctx.ctx, 0, x, None, T, s) == oled.OLED_ERR_INVALID_ARG
+        assert oled.route_block_gate(ctx.ctx, 0, x, g, 0, s) == oled.OLED_ERR_INVALID_ARG
+        assert oled.route_block_gate(ctx.ctx, 0, x, g, T + 1, s) == oled.OLED_ERR_INVALID_ARG
+        assert oled.route_block_gate(ctx.ctx, 2, x, g, T, s) == oled.OLED_ERR_INVALID_ARG
+        # a good layer fills the cache
+        ctx.route_block_gate(0, x, g, T, s)
+        # in flight: a second routing of any layer is out of order
+        assert oled.route_block_gate(ctx.ctx, 1, x, g, T, s) == oled.OLED_ERR_STATE
+        ctx.apply_misses(0, report=False)
+        ctx.score_and_retain(0, conf, s)
+        before = ctx.read_layer_state(0, T)["resident_after"].copy()
+        assert before.any()
+        # a NaN in one token row
+        bad = x.clone()
+        bad[5, 7] = float("nan")
+        ctx.route_block_gate(0, bad, g, T, s)
+        rep = oled.MissReport()
+        assert oled.apply_misses(ctx.ctx, 0, None, rep) == oled.OLED_ERR_INVALID_ARG
+        assert np.array_equal(ctx.read_layer_state(0, T)["resident_after"], before)
+        _say("[gate errors] ok")
+    finally:
+        ctx.close()
+        pool.free()
