@@ -355,7 +355,7 @@ __device__ __forceinline__ void gemm_tiles(const FfnLaunch& a, int t0, int strid
     const int ii = v / nf;
     const int f0 = (v - ii * nf) * FEAT;
     const WorkItem it = a.items[base + ii];
-    const int slot = a.slot_of[it.expert];
+    const int slot = it.pad >= 0 ? it.pad : a.slot_of[it.expert];
     if (slot < 0 || slot >= a.n_slots) continue;  // no weights on the device (bad block)
     const T* W = reinterpret_cast<const T*>(static_cast<const char*>(a.pool) +
                                             static_cast<int64_t>(slot) * a.slot_bytes);
@@ -706,7 +706,7 @@ void k_ffn_dense(FfnLaunch a) {
   const int gi = min(kDenseGroup, n - g * kDenseGroup);
   const int ft = rem / gi;
   const WorkItem it = a.items[a.item_base + first + g * kDenseGroup + (rem - ft * gi)];
-  const int slot = a.slot_of[it.expert];
+  const int slot = it.pad >= 0 ? it.pad : a.slot_of[it.expert];
   if (slot < 0 || slot >= a.n_slots || it.rows <= 0 || it.rows > kDenseRows) return;
   const uint16_t* W = reinterpret_cast<const uint16_t*>(static_cast<const char*>(a.pool) +
                                                         static_cast<int64_t>(slot) * a.slot_bytes);

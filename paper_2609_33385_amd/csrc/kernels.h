@@ -116,7 +116,7 @@ struct WorkItem {
   int32_t expert;
   int32_t row_begin;
   int32_t rows;
-  int32_t pad;
+  int32_t pad;   // a hit's cache slot (fixed until the layer's retention), -1 for a miss
 };
 
 // Host-to-device transfer of the staged misses done by workgroups of a GEMM

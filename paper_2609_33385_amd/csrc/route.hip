@@ -282,7 +282,7 @@ __device__ __forceinline__ void rank_chunk(const int32_t* idx, int t0, int t1, i
 __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, int bad,
                                              const PermuteOut& o, const int32_t* s_free,
                                              const int32_t* s_ftop, const uint32_t* s_res,
-                                             const uint32_t* s_pm,
+                                             const uint32_t* s_pm, const int32_t* s_slot,
                                              int32_t* __restrict__ chunk_base = nullptr,
                                              int n_chunks = 0) {
   __shared__ int32_t s_cnt[kMaxExperts];
@@ -462,12 +462,15 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
     o.counts[e] = c;
     o.offsets[e] = s_off[e];
     s_run[e] = s_off[e];
+    // a hit's slot cannot change before the layer's retention: the GEMMs take
+    // it from the item; a miss's slot is looked up when its GEMM runs
+    const int hslot = ((s_res[e >> 5] >> (e & 31)) & 1u) ? s_slot[e] : -1;
     if (s_dfull[e] >= 0) {  // dense: full items, then the expert's short item
       const int full = c / kDenseRows;
       for (int m = 0; m < full; ++m)
-        o.dense_items[s_dfull[e] + m] = WorkItem{e, s_off[e] + m * kDenseRows, kDenseRows, 0};
+        o.dense_items[s_dfull[e] + m] = WorkItem{e, s_off[e] + m * kDenseRows, kDenseRows, hslot};
       if (s_dshort[e] >= 0)
-        o.dense_items[s_dshort[e]] = WorkItem{e, s_off[e] + full * kDenseRows, c - full * kDenseRows, 0};
+        o.dense_items[s_dshort[e]] = WorkItem{e, s_off[e] + full * kDenseRows, c - full * kDenseRows, hslot};
       continue;
     }
     const int base = s_item_base[e];
@@ -476,7 +479,7 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
       it.expert = e;
       it.row_begin = s_off[e] + m * kItemRows;
       it.rows = min(kItemRows, c - m * kItemRows);
-      it.pad = 0;
+      it.pad = hslot;
       o.items[base + m] = it;
     }
   }
@@ -559,8 +562,13 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
 // (words), and the top of the free-slot list.
 __device__ __forceinline__ void prefetch_state(const CacheView& cv, int E, int layer,
                                                int32_t* s_free, int32_t* s_ftop, uint32_t* s_res,
-                                               uint32_t* s_pm) {
+                                               uint32_t* s_pm, int32_t* s_slot) {
   const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int q = 0; q < kMaxExperts / 64; ++q) {
+    const int e = lane + 64 * q;
+    if (e < E) s_slot[e] = cv.slot_of[static_cast<size_t>(layer) * E + e];
+  }
   if (lane < kMaxExperts / 32) s_res[lane] = cv.res[layer].bits[lane];
   else if (lane < kMaxExperts / 16) s_pm[lane - kMaxExperts / 32] = cv.prev_miss[layer].bits[lane - kMaxExperts / 32];
   const int ft = cv.hdr->free_top;
@@ -581,11 +589,12 @@ __global__ __launch_bounds__(kPermThreads) void k_permute(const int32_t* __restr
   __shared__ int32_t s_free[kMaxExperts];
   __shared__ int32_t s_ftop;
   __shared__ uint32_t s_res[kMaxExperts / 32], s_pm[kMaxExperts / 32];
+  __shared__ int32_t s_slot[kMaxExperts];
   const int bad = *bad_flag;
-  if ((threadIdx.x >> 6) == 1) prefetch_state(o.cv, o.E, o.layer, s_free, &s_ftop, s_res, s_pm);
+  if ((threadIdx.x >> 6) == 1) prefetch_state(o.cv, o.E, o.layer, s_free, &s_ftop, s_res, s_pm, s_slot);
   __syncthreads();
   if (threadIdx.x == 0) *bad_flag = 0;
-  permute_body(topk_idx, T, k, bad, o, s_free, &s_ftop, s_res, s_pm);
+  permute_body(topk_idx, T, k, bad, o, s_free, &s_ftop, s_res, s_pm, s_slot);
 }
 
 // Large blocks, first launch: workgroup c counts the routes of tokens
@@ -604,11 +613,12 @@ __global__ __launch_bounds__(kPermThreads) void k_perm_hist(const int32_t* __res
   __shared__ int32_t s_ftop;
   __shared__ int32_t s_last;
   __shared__ uint32_t s_res[kMaxExperts / 32], s_pm[kMaxExperts / 32];
+  __shared__ int32_t s_slot[kMaxExperts];
   const int E = o.E, tid = threadIdx.x, nthr = blockDim.x;
   const int ch = blockIdx.x, n_chunks = gridDim.x;
   for (int e = tid; e < kMaxExperts; e += nthr) s_h[e] = 0;
   // the cache state the last workgroup plans with, read while chunks count
-  if ((tid >> 6) == 1) prefetch_state(o.cv, E, o.layer, s_free, &s_ftop, s_res, s_pm);
+  if ((tid >> 6) == 1) prefetch_state(o.cv, E, o.layer, s_free, &s_ftop, s_res, s_pm, s_slot);
   __syncthreads();
   const int t0 = ch * kChunkTokens, t1 = min(T, t0 + kChunkTokens);
   for (int r = t0 * k + tid; r < t1 * k; r += nthr) atomicAdd(&s_h[topk_idx[r]], 1);
@@ -625,7 +635,7 @@ __global__ __launch_bounds__(kPermThreads) void k_perm_hist(const int32_t* __res
     *bad_flag = 0;
     *counter = 0;
   }
-  permute_body(topk_idx, T, k, bad, o, s_free, &s_ftop, s_res, s_pm, chunk_base, n_chunks);
+  permute_body(topk_idx, T, k, bad, o, s_free, &s_ftop, s_res, s_pm, s_slot, chunk_base, n_chunks);
 }
 
 // Large blocks, second launch: workgroup c ranks the routes of its chunk from
@@ -660,11 +670,12 @@ __global__ __launch_bounds__(256) void k_route_fused(const float* __restrict__ l
   __shared__ int32_t s_ftop;
   __shared__ int32_t s_last;
   __shared__ uint32_t s_res[kMaxExperts / 32], s_pm[kMaxExperts / 32];
+  __shared__ int32_t s_slot[kMaxExperts];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int E = o.E;
   // the cache state the last workgroup plans with, read while the tokens are
   // routed (no kernel of this launch changes it before the planning step)
-  if (wave == 3) prefetch_state(o.cv, E, o.layer, s_free, &s_ftop, s_res, s_pm);
+  if (wave == 3) prefetch_state(o.cv, E, o.layer, s_free, &s_ftop, s_res, s_pm, s_slot);
   int bad = 0;
   for (int t = blockIdx.x * 4 + wave; t < T; t += gridDim.x * 4) {
     float g;
@@ -689,7 +700,7 @@ __global__ __launch_bounds__(256) void k_route_fused(const float* __restrict__ l
     sync[0] = 0;
     sync[1] = 0;
   }
-  permute_body(s_idx, T, k, any_bad, o, s_free, &s_ftop, s_res, s_pm);
+  permute_body(s_idx, T, k, any_bad, o, s_free, &s_ftop, s_res, s_pm, s_slot);
 }
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
