@@ -555,8 +555,6 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
   }
 }
 
-// One wavefront loads the free-slot list's top (free_top and up to E entries
-// below it) into LDS ahead of the staging.
 // One wavefront reads the cache state the planning step needs into LDS: the
 // layer's resident set and the experts transferred at its previous iteration
 // (words), and the top of the free-slot list.
