@@ -1,7 +1,8 @@
 // K1 top-k routing and K2 histogram / prefix-sum / stable permutation for one
 // denoising block (OLED-MoE Sec. 4.1: the gate yields routed expert ids and
 // gate scores for every token of the block; Sec. 4.2: the active set A, the
-// misses M = A \ R, each given a staging slot in the device cache state).
+// misses M = A \ R, each given a staging slot in the device cache state), and
+// the gate GEMM that can precede them (logits = x W_gate^T, Sec. 2.1).
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
