@@ -851,6 +851,166 @@ __global__ __launch_bounds__(64 * KS) void k_router_logits(const void* __restric
   }
 }
 
+// The wide tiles (64 tokens x 16*NB experts, 4 wavefronts splitting the
+// hidden dimension) with the gate rows staged through LDS: each step a
+// wavefront loads its 16*NB rows' next 128 bytes as whole lines (8 rows of
+// 128 bytes per instruction; chunk q of row r kept at q ^ (r mod 8), so the
+// fragment reads of 8 consecutive rows hit distinct banks), then reads its B
+// fragments from LDS. Token rows come straight from memory as in
+// k_router_logits. Each wavefront stages only its own range (double-buffered;
+// LDS operations of one wavefront complete in order), and the buffer is
+// reused for the partial tiles once every wavefront is done.
+template <bool BF16, int NB>
+__global__ __launch_bounds__(256) void k_router_logits_staged(const void* __restrict__ x,
+                                                             const void* __restrict__ wg,
+                                                             int T, int E, int H,
+                                                             float* __restrict__ logits) {
+  constexpr int TA = 4, KS = 4, NF = TA * NB;
+  constexpr int kStep = BF16 ? 64 : 32;          // hidden elements per 128-byte step
+  constexpr int kEsz = BF16 ? 2 : 4;
+  constexpr int kRows = 16 * NB;                 // gate rows of the tile
+  constexpr int kStage = kRows * 8;              // 16-byte chunks per stage
+  constexpr int kPart = KS * NF * 64;            // 16-byte slots of the partial tiles
+  constexpr int kLds = kPart > KS * 2 * kStage ? kPart : KS * 2 * kStage;
+  __shared__ u32x4_t s_lds[kLds];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int c = lane & 15, g = lane >> 4;
+  const int tiles_e = (E + kRows - 1) / kRows;
+  const int tile = xcd_tile(blockIdx.x, gridDim.x);
+  const int tt = tile / tiles_e, te = tile - tt * tiles_e;
+  const int t0 = tt * 16 * TA, e0 = te * kRows;
+  const int n_steps = H / kStep;
+  const int s0 = wave * n_steps / KS, s1 = (wave + 1) * n_steps / KS;
+  const int n = s1 - s0;
+  const char* pa[TA];
+#pragma unroll
+  for (int a = 0; a < TA; ++a)
+    pa[a] = static_cast<const char*>(x) +
+            (static_cast<size_t>(min(t0 + 16 * a + c, T - 1)) * H) * kEsz + 32 * g;
+  // staging: instruction i loads rows 8i + lane / 8, chunk lane % 8
+  const char* ps[2 * NB];
+  int slot_w[2 * NB];
+#pragma unroll
+  for (int i = 0; i < 2 * NB; ++i) {
+    const int r = 8 * i + (lane >> 3), q = lane & 7;
+    ps[i] = static_cast<const char*>(wg) +
+            (static_cast<size_t>(min(e0 + r, E - 1)) * H) * kEsz + 16 * q;
+    slot_w[i] = r * 8 + (q ^ (r & 7));
+  }
+  int slot_r[NB][2];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    const int r = 16 * b + c;
+    slot_r[b][0] = r * 8 + ((2 * g) ^ (r & 7));
+    slot_r[b][1] = r * 8 + ((2 * g + 1) ^ (r & 7));
+  }
+  u32x4_t* stage = s_lds + wave * 2 * kStage;
+  floatx4_t acc[TA][NB];
+#pragma unroll
+  for (int a = 0; a < TA; ++a)
+#pragma unroll
+    for (int b = 0; b < NB; ++b) acc[a][b] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+
+  auto off = [&](int j) { return static_cast<size_t>(s0 + j) * kStep * kEsz; };
+  auto load_a = [&](int j, u32x4_t (&va)[TA][2]) {
+#pragma unroll
+    for (int a = 0; a < TA; ++a) {
+      va[a][0] = *reinterpret_cast<const u32x4_t*>(pa[a] + off(j));
+      va[a][1] = *reinterpret_cast<const u32x4_t*>(pa[a] + off(j) + 16);
+    }
+  };
+  auto load_s = [&](int j, u32x4_t (&vs)[2 * NB]) {
+#pragma unroll
+    for (int i = 0; i < 2 * NB; ++i) vs[i] = *reinterpret_cast<const u32x4_t*>(ps[i] + off(j));
+  };
+  auto put_s = [&](int buf, const u32x4_t (&vs)[2 * NB]) {
+#pragma unroll
+    for (int i = 0; i < 2 * NB; ++i) stage[buf * kStage + slot_w[i]] = vs[i];
+  };
+  auto mma = [&](int buf, const u32x4_t (&va)[TA][2]) {
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const u32x4_t vb0 = stage[buf * kStage + slot_r[b][0]];
+      const u32x4_t vb1 = stage[buf * kStage + slot_r[b][1]];
+#pragma unroll
+      for (int a = 0; a < TA; ++a) {
+        if constexpr (BF16) {
+          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, va[a][0]),
+                                                              __builtin_bit_cast(bf16x8_t, vb0),
+                                                              acc[a][b], 0, 0, 0);
+          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, va[a][1]),
+                                                              __builtin_bit_cast(bf16x8_t, vb1),
+                                                              acc[a][b], 0, 0, 0);
+        } else {
+          const floatx4_t fa0 = __builtin_bit_cast(floatx4_t, va[a][0]);
+          const floatx4_t fa1 = __builtin_bit_cast(floatx4_t, va[a][1]);
+          const floatx4_t fb0 = __builtin_bit_cast(floatx4_t, vb0);
+          const floatx4_t fb1 = __builtin_bit_cast(floatx4_t, vb1);
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa0[q], fb0[q], acc[a][b], 0, 0, 0);
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa1[q], fb1[q], acc[a][b], 0, 0, 0);
+        }
+      }
+    }
+  };
+
+  if (n > 0) {
+    u32x4_t ca[TA][2], na[TA][2], vs[2 * NB];
+    load_s(0, vs);
+    load_a(0, ca);
+    put_s(0, vs);
+    for (int j = 0; j < n; ++j) {
+      const bool more = j + 1 < n;
+      if (more) {
+        load_s(j + 1, vs);
+        load_a(j + 1, na);
+      }
+      mma(j & 1, ca);
+      if (more) {
+        put_s((j + 1) & 1, vs);
+#pragma unroll
+        for (int a = 0; a < TA; ++a) {
+          ca[a][0] = na[a][0];
+          ca[a][1] = na[a][1];
+        }
+      }
+    }
+  }
+  __syncthreads();   // every wavefront is done with its stages: the LDS holds partials now
+  floatx4_t (*s_part)[NF][64] = reinterpret_cast<floatx4_t (*)[NF][64]>(s_lds);
+#pragma unroll
+  for (int a = 0; a < TA; ++a)
+#pragma unroll
+    for (int b = 0; b < NB; ++b) s_part[wave][a * NB + b][lane] = acc[a][b];
+  __syncthreads();
+  for (int f = wave; f < NF; f += KS) {   // fragment f is summed by wavefront f mod KS
+    floatx4_t sum = s_part[0][f][lane];
+#pragma unroll
+    for (int w = 1; w < KS; ++w) sum += s_part[w][f][lane];
+    const int a = f / NB, b = f - a * NB;
+    const int ec = e0 + 16 * b + c;
+    if (ec < E) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int tr = t0 + 16 * a + 4 * g + i;
+        if (tr < T) logits[static_cast<size_t>(tr) * E + ec] = sum[i];
+      }
+    }
+  }
+}
+
+template <bool BF16, int NB>
+void launch_logits_staged(const void* x, const void* wg, int T, int E, int H, float* logits,
+                          hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
+  const int64_t blocks =
+      static_cast<int64_t>((T + 63) / 64) * ((E + 16 * NB - 1) / (16 * NB));
+  hipExtLaunchKernelGGL(k_router_logits_staged<BF16, NB>, dim3(static_cast<unsigned>(blocks)),
+                        dim3(256), 0, s, ev0, ev1, 0, x, wg, T, E, H, logits);
+}
+
 template <bool BF16, int TA, int NB, int KS, int G>
 void launch_logits_cfg(const void* x, const void* wg, int T, int E, int H, float* logits,
                        hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
@@ -862,13 +1022,13 @@ void launch_logits_cfg(const void* x, const void* wg, int T, int E, int H, float
 
 // Tile shape of the gate GEMM: the largest tile that still gives every
 // compute unit a workgroup (64 tokens x all of up to 128 experts reads x
-// once; 32 x 64 and 16 x 32 for mid-sized blocks). The re-reads of the gate
-// rows by every tile, not HBM, bound the larger blocks: with each wavefront
-// load spread over 16 rows (64 bytes of each), the operands come in at about
-// 8 TB/s for every tile shape measured (a coalesced read of L2-resident data
-// runs at about 25 TB/s), so the tile that reads the fewest bytes wins. Small
-// blocks take 16 x 16 tiles whose 4 wavefronts issue the loads of 4 steps at
-// once.
+// once, its gate rows staged through LDS; 32 x 64 and 16 x 32 for mid-sized
+// blocks). The re-reads of the gate rows by every tile, not HBM, bound the
+// larger blocks: with each wavefront load spread over 16 rows (64 bytes of
+// each), the operands come in at about 8 TB/s for every tile shape measured
+// (a coalesced read of L2-resident data runs at about 25 TB/s), so the tile
+// that reads the fewest bytes wins. Small blocks take 16 x 16 tiles whose 4
+// wavefronts issue the loads of 4 steps at once.
 template <bool BF16>
 void launch_logits(const void* x, const void* wg, int T, int E, int H, float* logits,
                    hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
@@ -876,9 +1036,9 @@ void launch_logits(const void* x, const void* wg, int T, int E, int H, float* lo
     return static_cast<int64_t>((T + 16 * ta - 1) / (16 * ta)) * ((E + 16 * nb - 1) / (16 * nb));
   };
   if (E <= 64 && wgs(4, 4) >= kGateFullGrid)
-    launch_logits_cfg<BF16, 4, 4, 4, 1>(x, wg, T, E, H, logits, ev0, ev1, s);
+    launch_logits_staged<BF16, 4>(x, wg, T, E, H, logits, ev0, ev1, s);
   else if (E > 64 && wgs(4, 8) >= kGateFullGrid)
-    launch_logits_cfg<BF16, 4, 8, 4, 1>(x, wg, T, E, H, logits, ev0, ev1, s);
+    launch_logits_staged<BF16, 8>(x, wg, T, E, H, logits, ev0, ev1, s);
   else if (wgs(2, 4) >= kGateFullGrid)
     launch_logits_cfg<BF16, 2, 4, 8, 1>(x, wg, T, E, H, logits, ev0, ev1, s);
   else if (wgs(1, 2) >= kGateFullGrid)
