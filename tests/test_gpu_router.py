@@ -93,6 +93,7 @@ TILE_CASES = [
     ("bf16", 40, 410, 128, 256),
     ("bf16", 3, 5481, 48, 256),
     ("f32", 40, 410, 128, 128),
+    ("bf16", 40, 410, 64, 128),   # two of the four hidden-dimension parts are empty
 ]
 
 
