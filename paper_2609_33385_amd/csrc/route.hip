@@ -134,19 +134,55 @@ __global__ __launch_bounds__(256) void k_route_topk(const float* __restrict__ lo
 // Large blocks: one token per lane. A wavefront takes 64 tokens; their
 // logits pass through LDS 32 experts at a time (coalesced row loads, one
 // padded row per token), the next 32 already in flight while the current ones
-// are ranked. Each lane keeps its token's KM best (key, expert) sorted by (key
-// desc, id asc): experts arrive in ascending id and enter only above strictly
-// smaller keys, so equal logits keep the lower id first. The first k of them
-// are the token's routes; gates as in route_token (fp64 exp of l_j - l_0, sum
-// in slot order, one rounding to fp32).
+// are ranked. Each lane ranks its token's experts by a packed 32-bit key: the
+// top 24 bits of the order-preserving logit key, then 255 - id, so that one
+// max / min pair per list position inserts (a bubble network over KP >= k + 1
+// positions). Where the k + 1 best packed keys differ in their top 24 bits,
+// their order is the exact (logit desc, id asc) order and the first k are the
+// routes; where two of them share those bits the whole wavefront ranks that
+// token again from memory with full keys (wave_topk_ids). Gates as in route_token (fp64 exp of
+// l_j - l_0, sum in slot order, one rounding to fp32), from the logits re-read
+// by expert id.
 constexpr int kLaneChunk = 32;
 constexpr int kLaneRow = kLaneChunk + 1;   // padded LDS row (floats): conflict-free lane reads
 
+// The whole wavefront ranks one row with full keys (E <= 256): k rounds of a
+// wavefront maximum, the lowest id holding it taken by ballot, as in
+// route_token; the lane that owns the token keeps the ids.
 template <int KM>
+__device__ __forceinline__ void wave_topk_ids(const float* row, int E, int k, bool mine,
+                                              int32_t (&ids)[KM]) {
+  const int lane = threadIdx.x & 63;
+  uint32_t ok[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = lane + 64 * q;
+    ok[q] = e < E ? max(ord_key(row[e]), 1u) : 0u;
+  }
+#pragma unroll
+  for (int j = 0; j < KM; ++j) {
+    if (j < k) {
+      const uint32_t m = wave_max(max(max(ok[0], ok[1]), max(ok[2], ok[3])));
+      int id = -1;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const uint64_t bq = __ballot(ok[q] == m);
+        if (id < 0 && bq != 0ull) id = 64 * q + __builtin_ctzll(bq);
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (lane + 64 * q == id) ok[q] = 0u;
+      if (mine) ids[j] = id;
+    }
+  }
+}
+
+template <int KP, int KM>
 __global__ __launch_bounds__(256) void k_route_lanes(const float* __restrict__ logits, int T, int E,
                                                      int k, int32_t* __restrict__ topk_idx,
                                                      float* __restrict__ gates,
                                                      int32_t* __restrict__ bad_flag) {
+  static_assert(KP > KM, "the packed list holds the k-th and the (k+1)-th key");
   __shared__ float s_buf[4][64 * kLaneRow];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int t0 = (blockIdx.x * 4 + wave) * 64;
@@ -162,13 +198,9 @@ __global__ __launch_bounds__(256) void k_route_lanes(const float* __restrict__ l
       v[i] = (t < T && e < E) ? logits[static_cast<size_t>(t) * E + e] : 0.f;
     }
   };
-  uint32_t key[KM];
-  int id[KM];
+  uint32_t key[KP];
 #pragma unroll
-  for (int j = 0; j < KM; ++j) {
-    key[j] = 0u;
-    id[j] = -1;
-  }
+  for (int j = 0; j < KP; ++j) key[j] = 0u;
   int nonfinite = 0;
   load(0);
   for (int e0 = 0; e0 < E; e0 += kLaneChunk) {
@@ -181,29 +213,39 @@ __global__ __launch_bounds__(256) void k_route_lanes(const float* __restrict__ l
     for (int j = 0; j < ne; ++j) {
       const float x = buf[lane * kLaneRow + j];
       nonfinite |= !__builtin_isfinite(x);
-      const uint32_t xk = max(ord_key(x), 1u);
-      const int xe = e0 + j;
+      uint32_t c = (max(ord_key(x), 1u) & 0xFFFFFF00u) | static_cast<uint32_t>(255 - (e0 + j));
 #pragma unroll
-      for (int q = KM - 1; q > 0; --q) {
-        const bool above_prev = xk > key[q - 1];
-        const bool above = xk > key[q];
-        key[q] = above_prev ? key[q - 1] : (above ? xk : key[q]);
-        id[q] = above_prev ? id[q - 1] : (above ? xe : id[q]);
-      }
-      if (xk > key[0]) {
-        key[0] = xk;
-        id[0] = xe;
+      for (int q = 0; q < KP; ++q) {
+        const uint32_t hi = max(key[q], c);
+        c = min(key[q], c);
+        key[q] = hi;
       }
     }
   }
   const int t = t0 + lane;
+  bool amb = false;
   if (t < T) {
-    const double v0 = static_cast<double>(ord_value(key[0]));
+#pragma unroll
+    for (int j = 0; j + 1 < KP; ++j)
+      if (j < k) amb |= (key[j] >> 8) == (key[j + 1] >> 8);
+  }
+  int32_t id[KM];
+#pragma unroll
+  for (int j = 0; j < KM; ++j) id[j] = 255 - static_cast<int>(key[j] & 0xFFu);
+  for (uint64_t todo = __ballot(amb); todo != 0ull; todo &= todo - 1) {
+    const int owner = __builtin_ctzll(todo);
+    wave_topk_ids<KM>(logits + static_cast<size_t>(t0 + owner) * E, E, k, lane == owner, id);
+  }
+  if (t < T) {
+    const float* row = logits + static_cast<size_t>(t) * E;
+    double lv[KM];
+#pragma unroll
+    for (int j = 0; j < KM; ++j) lv[j] = j < k ? static_cast<double>(row[id[j]]) : 0.0;
     double ex[KM];
     double sum = 0.0;
 #pragma unroll
     for (int j = 0; j < KM; ++j) {
-      ex[j] = j < k ? exp(static_cast<double>(ord_value(key[j])) - v0) : 0.0;
+      ex[j] = j < k ? exp(lv[j] - lv[0]) : 0.0;
       if (j < k) sum += ex[j];
     }
 #pragma unroll
@@ -1072,17 +1114,17 @@ hipError_t launch_route_topk(const float* logits, int T, int E, int k, int32_t* 
   if (route_lanes(T)) {
     const int blocks = (T + 255) / 256;
     if (k <= 2)
-      hipExtLaunchKernelGGL(k_route_lanes<2>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits, T,
-                            E, k, topk_idx, gates, bad_flag);
-    else if (k <= 4)
-      hipExtLaunchKernelGGL(k_route_lanes<4>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits, T,
-                            E, k, topk_idx, gates, bad_flag);
-    else if (k <= 8)
-      hipExtLaunchKernelGGL(k_route_lanes<8>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits, T,
-                            E, k, topk_idx, gates, bad_flag);
-    else
-      hipExtLaunchKernelGGL(k_route_lanes<16>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits,
+      hipExtLaunchKernelGGL(k_route_lanes<3, 2>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits,
                             T, E, k, topk_idx, gates, bad_flag);
+    else if (k <= 4)
+      hipExtLaunchKernelGGL(k_route_lanes<5, 4>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits,
+                            T, E, k, topk_idx, gates, bad_flag);
+    else if (k <= 8)
+      hipExtLaunchKernelGGL(k_route_lanes<9, 8>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits,
+                            T, E, k, topk_idx, gates, bad_flag);
+    else
+      hipExtLaunchKernelGGL(k_route_lanes<17, 16>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0,
+                            logits, T, E, k, topk_idx, gates, bad_flag);
     return hipGetLastError();
   }
   const int blocks = (T + 3) / 4 < 4096 ? (T + 3) / 4 : 4096;

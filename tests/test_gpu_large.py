@@ -80,3 +80,39 @@ def test_ragged_blocks_forward(E, k, batch, block):
 def test_large_block_f32():
     w = BASE.replace(wid=322, name="f32-t3000", dtype="f32", batch=12, block=250, capacity=40)
     _run(w, 2, forward=True)
+
+
+@pytest.mark.parametrize("E,k", [(128, 8), (64, 4), (200, 2), (33, 16)])
+def test_lane_routing_ties(E, k):
+    """Large-block routing on logits full of exact ties (values on a 0.5 grid,
+    signed zeros) and near ties (one ulp apart, so their packed keys agree in
+    their top 24 bits): those tokens take the exact re-ranking; every route and
+    gate bit for bit against the oracle."""
+    T = 2100
+    w = BASE.replace(wid=323, name=f"lane-ties-e{E}k{k}", n_experts=E, top_k=k, batch=7, block=300,
+                     n_layers=1, n_iters=1, capacity=E // 3)
+    assert w.tokens == T
+    rng = np.random.default_rng(50 + E + k)
+    lg = (np.round(rng.standard_normal((T, E)) * 2) / 2).astype(np.float32)
+    nudge = rng.uniform(0, 1, (T, E)) < 0.25
+    lg = np.where(nudge, np.nextafter(lg, np.float32(np.inf)), lg).astype(np.float32)
+    zero = (lg == 0) & (rng.uniform(0, 1, (T, E)) < 0.5)
+    lg[zero] = np.float32(-0.0)
+    _say(f"[lane ties] E={E} k={k} T={T}")
+    pool = HN.fill_pool(w, 0, 4)
+    ctx = HN.make_context(w, pool)
+    s = torch.cuda.current_stream()
+    try:
+        conf = torch.from_numpy(W.confidence(w, 0, 0, 0)).cuda()
+        ctx.route_block(0, torch.from_numpy(lg).cuda(), T, s)
+        ctx.apply_misses(0, report=False)
+        ctx.score_and_retain(0, conf, s)
+        st = ctx.read_layer_state(0, T)
+        idx_ref, g_ref = O.route(lg, k)
+        bad = np.nonzero(np.any(st["topk_idx"] != idx_ref, axis=1))[0]
+        assert bad.size == 0, f"tokens {bad[:5]} routed differently"
+        assert np.array_equal(st["gates"].view(np.uint32), g_ref.view(np.uint32))
+        _say("[lane ties] ok")
+    finally:
+        ctx.close()
+        pool.free()
