@@ -346,12 +346,27 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
   const int R = T * k;
   for (int e = tid; e < kMaxExperts; e += nthr) s_cnt[e] = 0;
   __syncthreads();
-  if (chunk_base) {   // counts per chunk in chunk_base [n_chunks][E], from other workgroups
-    for (int e = tid; e < E; e += nthr) {
+  // Chunked: counts per chunk in chunk_base [n_chunks][E], from other
+  // workgroups. G threads per expert each take a contiguous run of chunks
+  // (short chains of dependent loads); their partial sums stay in s_pre
+  // (g * E + e), which the chunked path does not otherwise use, for the
+  // per-chunk bases at the end.
+  const int G = chunk_base ? max(1, min(nthr / E, n_chunks)) : 1;
+  const int per = chunk_base ? (n_chunks + G - 1) / G : 0;
+  if (chunk_base) {
+    for (int i = tid; i < G * E; i += nthr) {
+      const int g = i / E, e = i - g * E;
+      const int c1 = min(n_chunks, (g + 1) * per);
       int c = 0;
-      for (int ch = 0; ch < n_chunks; ++ch)
+      for (int ch = g * per; ch < c1; ++ch)
         c += __hip_atomic_load(chunk_base + static_cast<size_t>(ch) * E + e, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
+      s_pre[i] = c;
+    }
+    __syncthreads();
+    for (int e = tid; e < E; e += nthr) {
+      int c = 0;
+      for (int g = 0; g < G; ++g) c += s_pre[g * E + e];
       s_cnt[e] = c;
     }
   } else {
@@ -529,9 +544,12 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
   if (tid == 0) o.offsets[E] = s_off[E];
 
   if (chunk_base) {   // per-chunk bases for the ranking launch: exclusive scan over chunks
-    for (int e = tid; e < E; e += nthr) {
+    for (int i = tid; i < G * E; i += nthr) {
+      const int g = i / E, e = i - g * E;
       int run = s_off[e];
-      for (int ch = 0; ch < n_chunks; ++ch) {
+      for (int h = 0; h < g; ++h) run += s_pre[h * E + e];
+      const int c1 = min(n_chunks, (g + 1) * per);
+      for (int ch = g * per; ch < c1; ++ch) {
         int32_t* p = chunk_base + static_cast<size_t>(ch) * E + e;
         const int c = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         *p = run;
