@@ -358,6 +358,7 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
       const int g = i / E, e = i - g * E;
       const int c1 = min(n_chunks, (g + 1) * per);
       int c = 0;
+#pragma unroll 4
       for (int ch = g * per; ch < c1; ++ch)
         c += __hip_atomic_load(chunk_base + static_cast<size_t>(ch) * E + e, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
@@ -549,11 +550,18 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
       int run = s_off[e];
       for (int h = 0; h < g; ++h) run += s_pre[h * E + e];
       const int c1 = min(n_chunks, (g + 1) * per);
-      for (int ch = g * per; ch < c1; ++ch) {
-        int32_t* p = chunk_base + static_cast<size_t>(ch) * E + e;
-        const int c = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        *p = run;
-        run += c;
+      for (int ch = g * per; ch < c1; ch += 4) {   // 4 counts read, then 4 bases written
+        int c[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          c[u] = ch + u < c1 ? __hip_atomic_load(chunk_base + static_cast<size_t>(ch + u) * E + e,
+                                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                             : 0;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          if (ch + u < c1) chunk_base[static_cast<size_t>(ch + u) * E + e] = run;
+          run += c[u];
+        }
       }
     }
   } else {
@@ -680,7 +688,14 @@ __global__ __launch_bounds__(kPermThreads) void k_perm_hist(const int32_t* __res
   if ((tid >> 6) == 1) prefetch_state(o.cv, E, o.layer, s_free, &s_ftop, s_res, s_pm, s_slot);
   __syncthreads();
   const int t0 = ch * kChunkTokens, t1 = min(T, t0 + kChunkTokens);
-  for (int r = t0 * k + tid; r < t1 * k; r += nthr) atomicAdd(&s_h[topk_idx[r]], 1);
+  for (int r = t0 * k + tid; r < t1 * k; r += 4 * nthr) {   // 4 loads in flight per thread
+    int e[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) e[u] = r + u * nthr < t1 * k ? topk_idx[r + u * nthr] : -1;
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (e[u] >= 0) atomicAdd(&s_h[e[u]], 1);
+  }
   __syncthreads();
   for (int e = tid; e < E; e += nthr) chunk_base[static_cast<size_t>(ch) * E + e] = s_h[e];
   __threadfence();   // this chunk's counts are visible device-wide

@@ -56,17 +56,33 @@ __device__ __forceinline__ void score_sums(const ScoreArgs& a, int r0, int r1,
   const float* __restrict__ conf = a.conf;
   const int32_t* __restrict__ topk_idx = a.topk_idx;
   const int k = a.k;
+  // kSumBatch routes per thread are loaded before any of them is added, so
+  // their loads are in flight together (integer adds: any order, same bits)
+  constexpr int kSumBatch = 8;
   int bad = 0;
-  for (int r = r0 + static_cast<int>(threadIdx.x); r < r1; r += kThreads) {
-    const int e = topk_idx[r];
-    const float g = gates[r];
-    const float c = conf[r / k];
-    if (!(c >= 0.f && c <= 1.f)) {
-      bad = 1;
-      continue;
+  for (int r = r0 + static_cast<int>(threadIdx.x); r < r1; r += kThreads * kSumBatch) {
+    int e[kSumBatch];
+    float g[kSumBatch], c[kSumBatch];
+#pragma unroll
+    for (int u = 0; u < kSumBatch; ++u) {
+      const int ru = r + u * kThreads;
+      e[u] = -1;
+      if (ru < r1) {
+        e[u] = topk_idx[ru];
+        g[u] = gates[ru];
+        c[u] = conf[ru / k];
+      }
     }
-    const double prod = static_cast<double>(g) * static_cast<double>(c);
-    atomicAdd(&s_S[e], static_cast<unsigned long long>(floor(prod * 0x1p48)));
+#pragma unroll
+    for (int u = 0; u < kSumBatch; ++u) {
+      if (e[u] < 0) continue;
+      if (!(c[u] >= 0.f && c[u] <= 1.f)) {
+        bad = 1;
+        continue;
+      }
+      const double prod = static_cast<double>(g[u]) * static_cast<double>(c[u]);
+      atomicAdd(&s_S[e[u]], static_cast<unsigned long long>(floor(prod * 0x1p48)));
+    }
   }
   if (bad) atomicOr(s_bad, 1);
 }
