@@ -265,16 +265,29 @@ __device__ __forceinline__ void combine_body(const CombineArgs& c, int t, int hb
   const int h = (hb * 256 + static_cast<int>(threadIdx.x)) * 4;
   if (h >= c.H) return;
   const int k = c.k, H = c.H;
+  // every route's gate and row position, then every row, are loaded before
+  // the sum, so the loads of all k routes are in flight together
+  float gj[kMaxTopK];
+  int pos[kMaxTopK];
+#pragma unroll
+  for (int j = 0; j < kMaxTopK; ++j)
+    if (j < k) {
+      gj[j] = c.gates[static_cast<size_t>(t) * k + j];
+      pos[j] = c.inv_perm[static_cast<size_t>(t) * k + j];
+    }
+  float4 o[kMaxTopK];
+#pragma unroll
+  for (int j = 0; j < kMaxTopK; ++j)
+    if (j < k) o[j] = *reinterpret_cast<const float4*>(c.O + static_cast<size_t>(pos[j]) * H + h);
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int j = 0; j < k; ++j) {
-    const float gj = c.gates[static_cast<size_t>(t) * k + j];
-    const int pos = c.inv_perm[static_cast<size_t>(t) * k + j];
-    const float4 o = *reinterpret_cast<const float4*>(c.O + static_cast<size_t>(pos) * H + h);
-    acc.x = fmaf(gj, o.x, acc.x);
-    acc.y = fmaf(gj, o.y, acc.y);
-    acc.z = fmaf(gj, o.z, acc.z);
-    acc.w = fmaf(gj, o.w, acc.w);
-  }
+#pragma unroll
+  for (int j = 0; j < kMaxTopK; ++j)
+    if (j < k) {
+      acc.x = fmaf(gj[j], o[j].x, acc.x);
+      acc.y = fmaf(gj[j], o[j].y, acc.y);
+      acc.z = fmaf(gj[j], o[j].z, acc.z);
+      acc.w = fmaf(gj[j], o[j].w, acc.w);
+    }
   if (BF16) {
     uint2 packed;
     packed.x = f32_to_bf16_rne(acc.x) | (static_cast<uint32_t>(f32_to_bf16_rne(acc.y)) << 16);
