@@ -324,8 +324,8 @@ def main():
                          "layer_adapt ('' for none)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU: the expert-offloading layer path has no multi-GPU "
-              "mode in this build (run with --gpus 1)", file=sys.stderr)
+        print("bench.py measures one GPU: the expert-offloading layer path runs on a single "
+              "GPU and has no multi-GPU mode (run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
 
     import torch
