@@ -197,6 +197,10 @@ typedef struct {
   int32_t reused_transfers;   /* and those of them retained and activated now */
   float* logits;              /* [T*E] fp32 logits of the gate GEMM, filled if the last routing
                                  of `layer` was route_block_gate (else untouched) */
+  uint8_t* retained;          /* [E] the set the last score_and_retain of `layer` kept
+                                 (Top_C of the retention rule, Sec. 4.2), before any eviction
+                                 by a layer-adaptive re-sizing that followed it (Sec. 4.3);
+                                 equals resident_after unless such a re-sizing shrank the layer */
 } oled_layer_state;
 
 /* One timed operation (see oled_config.profile_ops). */

@@ -1169,6 +1169,7 @@ oled_status oled_reset_cache(void* ctx) {
   if (st != OLED_OK) return st;
   st = init_cache_state(c);
   if (st != OLED_OK) return st;
+  HIP_TRY(c, hipMemset(c->d_ret, 0, sizeof(RetainOut) * c->L));
   c->broken = false;
   std::fill(c->ret_seq.begin(), c->ret_seq.end(), 0);
   std::fill(c->ret_seen.begin(), c->ret_seen.end(), 0);
@@ -1720,6 +1721,11 @@ oled_status oled_read_layer_state(void* ctx, int32_t layer, oled_layer_state* ou
   if (out->retain_key)
     HIP_TRY(c, hipMemcpy(out->retain_key, c->d_key + static_cast<size_t>(layer) * c->E, c->E * 8,
                          hipMemcpyDeviceToHost));
+  if (out->retained) {
+    RetainOut ro;
+    HIP_TRY(c, hipMemcpy(&ro, c->d_ret + layer, sizeof(RetainOut), hipMemcpyDeviceToHost));
+    for (int e = 0; e < c->E; ++e) out->retained[e] = (ro.retained[e >> 5] >> (e & 31)) & 1u;
+  }
   if (c->stage == Stage::kIdle) {
     st = check_slots(c);
     if (st != OLED_OK) return st;

@@ -14,14 +14,27 @@ from . import oled
 from . import workload as W
 
 
-def fill_pool(w: W.Workload, seed: int, n_blocks: int) -> oled.PinnedPool:
-    """Pinned host pool of n_blocks expert blocks drawn by workload.expert_block,
-    packed into the library's expert-block layout."""
+def fill_pool(w: W.Workload, seed: int, n_blocks: int, raw: dict | None = None,
+              threads: int = 16) -> oled.PinnedPool:
+    """Pinned host pool of n_blocks expert blocks drawn by workload.expert_block
+    (or taken from `raw`, {block: drawn block}), packed into the library's
+    expert-block layout on a thread pool (the draws and the packing call
+    release the GIL)."""
+    import concurrent.futures
     pool = oled.PinnedPool(n_blocks, w.expert_bytes)
     dt = np.float32 if w.dtype == "f32" else np.uint16
-    for b in range(n_blocks):
-        w13, w2 = W.split_expert(w, W.expert_block(w, seed, b))
+
+    def one(b):
+        flat = raw[b] if raw is not None else W.expert_block(w, seed, b)
+        w13, w2 = W.split_expert(w, flat)
         oled.oled_pack_expert(w.dtype, w.hidden, w.inter, w13, w2, pool.block(b, dt))
+
+    try:
+        with concurrent.futures.ThreadPoolExecutor(max(1, min(threads, n_blocks))) as ex:
+            list(ex.map(one, range(n_blocks)))
+    except BaseException:
+        pool.free()
+        raise
     return pool
 
 

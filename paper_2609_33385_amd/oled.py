@@ -100,7 +100,8 @@ class LayerState(ctypes.Structure):
                 ("n_hits", ctypes.c_int32), ("n_misses", ctypes.c_int32),
                 ("capacity", ctypes.c_int32), ("reserved", ctypes.c_int32),
                 ("retain_key", ctypes.c_void_p), ("prev_transferred", ctypes.c_int32),
-                ("reused_transfers", ctypes.c_int32), ("logits", ctypes.c_void_p)]
+                ("reused_transfers", ctypes.c_int32), ("logits", ctypes.c_void_p),
+                ("retained", ctypes.c_void_p)]
 
 
 class OpTime(ctypes.Structure):
@@ -402,8 +403,9 @@ class Context:
                    resident_after=np.zeros(E, np.uint8), slot_of=np.zeros(E, np.int32))
         rkey = np.zeros(E, np.uint64)
         lgt = np.full(R * E // k, np.nan, np.float32)
+        kept = np.zeros(E, np.uint8)
         st = LayerState(*[a.ctypes.data for a in out.values()], 0, 0, 0, 0, 0, 0,
-                        rkey.ctypes.data, 0, 0, lgt.ctypes.data)
+                        rkey.ctypes.data, 0, 0, lgt.ctypes.data, kept.ctypes.data)
         status = oled_read_layer_state(self.ctx, layer, st)
         if status not in (OLED_OK, OLED_ERR_INVALID_ARG):
             _check(self.ctx, status)
@@ -415,7 +417,7 @@ class Context:
         out.update(tokens=Tn, n_active=st.n_active, n_hits=st.n_hits, n_misses=st.n_misses,
                    capacity=st.capacity, retain_key=rkey, prev_transferred=st.prev_transferred,
                    logits=lgt[: Tn * E].reshape(Tn, E),
-                   reused_transfers=st.reused_transfers,
+                   reused_transfers=st.reused_transfers, retained=kept.astype(bool),
                    rejected=(status == OLED_ERR_INVALID_ARG))
         out["resident_before"] = out["resident_before"].astype(bool)
         out["resident_after"] = out["resident_after"].astype(bool)

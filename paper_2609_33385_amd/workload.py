@@ -204,6 +204,16 @@ def expert_block(w: Workload, seed: int, b: int) -> np.ndarray:
     return _emit(w, v)
 
 
+def expert_blocks(w: Workload, seed: int, blocks, threads: int = 16) -> dict:
+    """{b: expert_block(w, seed, b)} for the given block ids, drawn on a thread
+    pool (the draws and conversions release the GIL). Same bits as drawing
+    them one by one."""
+    import concurrent.futures
+    ids = [int(b) for b in blocks]
+    with concurrent.futures.ThreadPoolExecutor(max(1, threads)) as ex:
+        return dict(zip(ids, ex.map(lambda b: expert_block(w, seed, b), ids)))
+
+
 def gate_weights(w: Workload, seed: int, layer: int) -> np.ndarray:
     """Gate weights of a layer [E][H] in the workload dtype encoding, entries
     ~ N(0, (150 / sqrt(H))^2), so that logits of N(0, 0.02^2) activations have

@@ -44,7 +44,7 @@ def _oracle(w, seed, layers, n_iters, C, period):
                           len(layers), n_iters, w.n_experts, w.top_k, C, adapt_period=period)
 
 
-def _adaptive_chain(w, seed, period, C, n_blocks=32, forward=False, copy_mode="shader",
+def _adaptive_chain(w, seed, period, C, n_blocks=None, forward=False, copy_mode="shader",
                     out_at=()):
     layers = list(range(w.n_layers))
     L = len(layers)
@@ -54,21 +54,24 @@ def _adaptive_chain(w, seed, period, C, n_blocks=32, forward=False, copy_mode="s
     moved = any(r[-1].get("capacities_after", [min(C, w.n_experts)] * L) != [min(C, w.n_experts)] * L
                 for r in ref)
     assert moved, "the test workload should move capacity between layers"
-    pool = HN.fill_pool(w, seed, n_blocks)
+    if n_blocks is None:     # distinct weights within a layer, shifted per layer
+        n_blocks = w.n_experts + 1
+    raw = W.expert_blocks(w, seed, range(n_blocks))
+    pool = HN.fill_pool(w, seed, n_blocks, raw=raw)
     ctx = HN.make_context(w, pool, capacity=C, copy_mode=copy_mode, adapt_period=period)
-    ow = OracleWeights(w, seed, n_blocks, L)
+    ow = OracleWeights(w, seed, n_blocks, L, raw=raw)
     worst = [0.0]
 
     def check(i, li, st, y, rep):
         o = ref[i][li]
         where = f"{w.name} l={li} i={i}"
         resized = li == L - 1 and "capacities_after" in o
-        if resized:
-            # the re-sizing ran right after this retention, so the state read
-            # shows its result: compare the retention's own result through the
-            # oracle's, then every layer's state after the re-sizing
-            st = dict(st, resident_after=o["resident_after"])
-        compare_control(st, o, w.tokens, where)
+        # the re-sizing ran right after this retention: the retention's own
+        # result is compared directly, the layer's state with the oracle's
+        # state after the re-sizing, then every other layer's state
+        compare_control(st, o, w.tokens, where, W.logits(w, seed, layers[li], 0, i),
+                        W.confidence(w, seed, 0, i), o["capacity"],
+                        state_after=o["residents_after_update"][li] if resized else None)
         if resized:
             for lj in range(L):
                 sj = ctx.read_layer_state(lj, w.tokens)

@@ -33,7 +33,7 @@ def _gpu():
     oled.load()
 
 
-def _coop_chain(w, seed, C, coop, forward=True, n_blocks=16, out_at=None):
+def _coop_chain(w, seed, C, coop, forward=True, n_blocks=None, out_at=None):
     L = w.n_layers
     _say(f"[coop] {w.name} L={L} iters={w.n_iters} C={C} {coop} forward={forward}")
     ref = O.run_coop_schedule(lambda li, i: W.logits(w, seed, li, 0, i),
@@ -42,15 +42,19 @@ def _coop_chain(w, seed, C, coop, forward=True, n_blocks=16, out_at=None):
                               coop["nbar"], coop["lambda_us"])
     n_cpu_ref = sum(int(st["cpu"].sum()) for row in ref for st in row)
     assert n_cpu_ref > 0, "the test should send some misses to the CPU"
-    pool = HN.fill_pool(w, seed, n_blocks)
+    if n_blocks is None:     # distinct weights within a layer, shifted per layer
+        n_blocks = w.n_experts + 1
+    raw = W.expert_blocks(w, seed, range(n_blocks))
+    pool = HN.fill_pool(w, seed, n_blocks, raw=raw)
     ctx = HN.make_context(w, pool, capacity=C, coop=coop)
-    ow = OracleWeights(w, seed, n_blocks, L)
+    ow = OracleWeights(w, seed, n_blocks, L, raw=raw)
     worst = [0.0]
 
     def check(i, li, st, y, rep):
         o = ref[i][li]
         where = f"{w.name} l={li} i={i}"
-        compare_control(st, o, w.tokens, where)
+        compare_control(st, o, w.tokens, where, W.logits(w, seed, li, 0, i),
+                        W.confidence(w, seed, 0, i), C, policy="coop")
         assert rep.n_cpu == int(o["cpu"].sum()), where
         assert rep.h2d_bytes == int(o["transfer"].sum()) * w.expert_bytes, where
         assert (st["prev_transferred"], st["reused_transfers"]) == (

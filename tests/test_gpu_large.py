@@ -16,7 +16,7 @@ from paper_2609_33385_amd import harness as HN
 from paper_2609_33385_amd import oled
 from paper_2609_33385_amd import workload as W
 
-from gpu_common import (OracleWeights, compare_control, oracle_schedule, rel_l2, run_schedule_gpu,
+from gpu_common import (LockstepOracle, OracleWeights, compare_control, rel_l2, run_schedule_gpu,
                         tol)
 
 pytestmark = pytest.mark.gpu
@@ -40,16 +40,21 @@ def _run(w, seed, forward=False, out_rows=16):
     layers = list(range(w.n_layers))
     _say(f"[large] {w.name} T={w.tokens} E={w.n_experts} k={w.top_k} {w.dtype} C={w.capacity} "
          f"forward={forward}")
-    ref = oracle_schedule(w, seed, layers, w.n_iters, w.capacity)
-    pool = HN.fill_pool(w, seed, 8)
+    # one host block per (layer, expert) where the weights are small enough,
+    # else E + 1 (distinct within a layer, shifted per layer)
+    P = len(layers) * w.n_experts if w.expert_bytes * len(layers) * w.n_experts <= (1 << 30) \
+        else w.n_experts + 1
+    lock = LockstepOracle(len(layers), w.n_experts, w.top_k, w.capacity)
+    raw = W.expert_blocks(w, seed, range(P))
+    pool = HN.fill_pool(w, seed, P, raw=raw)
     ctx = HN.make_context(w, pool)
-    ow = OracleWeights(w, seed, 8, len(layers))
+    ow = OracleWeights(w, seed, P, len(layers), raw=raw)
     rows = np.random.default_rng(seed).choice(w.tokens, min(out_rows, w.tokens), replace=False)
     worst = [0.0]
 
     def check(i, li, st, y, rep):
-        o = ref[i][li]
-        compare_control(st, o, w.tokens, f"{w.name} l={li} i={i}")
+        o = lock.step(li, W.logits(w, seed, layers[li], 0, i), W.confidence(w, seed, 0, i), st,
+                      f"{w.name} l={li} i={i}")
         if y is not None:
             x = O.decode(W.activations(w, seed, layers[li], 0, i))
             y_ref = O.moe_output(x, o["idx"], o["gates"], ow.fn(li), tokens=rows)
@@ -111,7 +116,9 @@ def test_lane_routing_ties(E, k):
         idx_ref, g_ref = O.route(lg, k)
         bad = np.nonzero(np.any(st["topk_idx"] != idx_ref, axis=1))[0]
         assert bad.size == 0, f"tokens {bad[:5]} routed differently"
-        assert np.array_equal(st["gates"].view(np.uint32), g_ref.view(np.uint32))
+        o = O.layer_step(lg, W.confidence(w, 0, 0, 0), np.zeros(E, bool), k, w.capacity)
+        compare_control(st, o, T, f"lane ties E={E} k={k}", lg, W.confidence(w, 0, 0, 0),
+                        w.capacity)
         _say("[lane ties] ok")
     finally:
         ctx.close()

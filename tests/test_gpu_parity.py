@@ -18,8 +18,8 @@ from paper_2609_33385_amd import harness as HN
 from paper_2609_33385_amd import oled
 from paper_2609_33385_amd import workload as W
 
-from gpu_common import (OracleWeights, check_report, compare_control, oracle_schedule, rel_l2,
-                        run_schedule_gpu, tol)
+from gpu_common import (LockstepOracle, OracleWeights, check_report, compare_control,
+                        oracle_schedule, rel_l2, run_schedule_gpu, tol)
 
 pytestmark = pytest.mark.gpu
 
@@ -37,27 +37,33 @@ def _gpu():
 
 def _chain(w, seed, layers, n_iters, n_blocks, out_at=None, out_tokens=None, capacity=None,
            forward=True, copy_mode="shader", report=True):
-    """Runs a schedule on both sides and compares every layer-iteration.
+    """Runs a schedule on both sides and compares every layer-iteration, the
+    oracle advancing in lockstep with the GPU.
 
+    n_blocks: host pool blocks; expert (l, e) of the chain reads block
+    (l*E + e) mod n_blocks, so n_blocks >= len(layers)*E gives every tested
+    expert weights of its own, and E + 1 gives distinct weights within a
+    layer that shift from layer to layer.
     out_at: set of (layer index, iteration) whose outputs are checked (None: all).
     out_tokens: token rows checked there (None: all).
     """
     C = w.capacity if capacity is None else capacity
     _say(f"[chain] {w.name} layers={list(layers)} iters={n_iters} C={C} P={n_blocks} "
          f"copy={copy_mode} report={report}")
-    pool = HN.fill_pool(w, seed, n_blocks)
+    raw = W.expert_blocks(w, seed, range(n_blocks))
+    pool = HN.fill_pool(w, seed, n_blocks, raw=raw)
     ctx = HN.make_context(w, pool, capacity=C, n_layers=len(layers), copy_mode=copy_mode)
-    ref = oracle_schedule(w, seed, layers, n_iters, C)
-    ow = OracleWeights(w, seed, n_blocks, len(layers))
+    lock = LockstepOracle(len(layers), w.n_experts, w.top_k, C)
+    ow = OracleWeights(w, seed, n_blocks, len(layers), raw=raw)
     worst = [0.0]
 
     def check(i, li, st, y, rep):
         where = f"{w.name} l={layers[li]} i={i}"
-        compare_control(st, ref[i][li], w.tokens, where)
-        check_report(rep, ref[i][li], w.expert_bytes, where)
+        o = lock.step(li, W.logits(w, seed, layers[li], 0, i), W.confidence(w, seed, 0, i),
+                      st, where)
+        check_report(rep, o, w.expert_bytes, where)
         if y is None or (out_at is not None and (li, i) not in out_at):
             return
-        o = ref[i][li]
         x = O.decode(W.activations(w, seed, layers[li], 0, i))
         rows = np.arange(w.tokens) if out_tokens is None else np.asarray(out_tokens)
         y_ref = O.moe_output(x, o["idx"], o["gates"], ow.fn(li), tokens=rows)
@@ -70,7 +76,8 @@ def _chain(w, seed, layers, n_iters, n_blocks, out_at=None, out_tokens=None, cap
     finally:
         ctx.close()
         pool.free()
-    _say(f"[chain] {w.name} ok, worst rel L2 {worst[0]:.3e}")
+    _say(f"[chain] {w.name} ok, worst rel L2 {worst[0]:.3e}, accepted gate roundings "
+         f"{lock.flips}")
 
 
 @pytest.mark.parametrize("copy_mode", ["shader", "sdma"])
@@ -104,9 +111,9 @@ def test_small_shapes(E, k, T, C, dt, H, I):
     w = W.WORKLOADS[1].replace(wid=100 + E, name=f"small-E{E}-k{k}-T{T}", dtype=dt, batch=1,
                                block=T, n_experts=E, top_k=k, hidden=H, inter=I, n_layers=2,
                                n_iters=3, capacity=C)
-    _chain(w, 1, range(2), 3, min(2 * E, 24))
+    _chain(w, 1, range(2), 3, 2 * E)
     if E in (5, 64):
-        _chain(w, 1, range(2), 3, min(2 * E, 24), copy_mode="sdma")
+        _chain(w, 1, range(2), 3, 2 * E, copy_mode="sdma")
 
 
 def test_ties_and_signed_zero():
@@ -125,7 +132,7 @@ def test_ties_and_signed_zero():
         HN.layer_step(ctx, 0, torch.from_numpy(lg).cuda(), torch.from_numpy(conf).cuda())
         st = ctx.read_layer_state(0, T)
         ref = O.layer_step(lg, conf, np.zeros(E, bool), k, 4)
-        compare_control(st, ref, T, "ties")
+        compare_control(st, ref, T, "ties", lg, conf, 4)
     finally:
         ctx.close()
         pool.free()
@@ -133,10 +140,22 @@ def test_ties_and_signed_zero():
 
 @pytest.mark.parametrize("copy_mode", ["shader", "sdma"])
 def test_cfg2_chain(copy_mode):
+    """All 16 layers; E + 1 host blocks: distinct weights within every layer,
+    shifted from layer to layer."""
     w = W.WORKLOADS[2]
     L, N = w.n_layers, w.n_iters
     out_at = {(l, i) for l in (0, L // 2, L - 1) for i in (0, 1, N - 1)}
-    _chain(w, 0, range(L), N, 64, out_at=out_at, copy_mode=copy_mode)
+    _chain(w, 0, range(L), N, w.n_experts + 1, out_at=out_at, copy_mode=copy_mode)
+
+
+def test_cfg2_chain_unaliased():
+    """Four layers, one host block per (layer, expert): no two tested experts
+    share weights, so a slot, address or work-item mistake that reads another
+    expert's weights changes the output."""
+    w = W.WORKLOADS[2]
+    layers, N = [0, 5, 10, 15], w.n_iters
+    out_at = {(li, i) for li in range(4) for i in (1, N - 1)}
+    _chain(w, 0, layers, N, len(layers) * w.n_experts, out_at=out_at)
 
 
 def test_cfg2_no_sync_until_the_end():
@@ -146,10 +165,12 @@ def test_cfg2_no_sync_until_the_end():
     w = W.WORKLOADS[2]
     layers, N, T = [0, 5, 11, 15], w.n_iters, w.tokens
     _say(f"[async] {w.name} layers={layers} iters={N}")
-    pool = HN.fill_pool(w, 0, 64)
+    P = len(layers) * w.n_experts
+    raw = W.expert_blocks(w, 0, range(P))
+    pool = HN.fill_pool(w, 0, P, raw=raw)
     ctx = HN.make_context(w, pool, n_layers=len(layers))
     ref = oracle_schedule(w, 0, layers, N, w.capacity)
-    ow = OracleWeights(w, 0, 64, len(layers))
+    ow = OracleWeights(w, 0, P, len(layers), raw=raw)
     s = torch.cuda.current_stream()
     dt = HN.torch_dtype(w)
     try:
@@ -192,15 +213,18 @@ def test_cfg2_no_sync_until_the_end():
 def test_cfg3_chain():
     w = W.WORKLOADS[3]
     L, N = w.n_layers, w.n_iters
-    _chain(w, 0, range(L), N, 64, out_at={(0, 0), (L - 1, N - 1)})
+    _chain(w, 0, range(L), N, w.n_experts + 1, out_at={(0, 0), (L - 1, N - 1)})
 
 
 @pytest.mark.parametrize("wid", [4, 5])
 def test_cfg45_chain(wid):
+    """The E=128 stacks on three sampled layers, one host block per (layer,
+    expert) (384 blocks of 36 MiB): no two tested experts share weights."""
     w = W.WORKLOADS[wid]
     layers = [0, w.n_layers // 2, w.n_layers - 1]
     rows = np.random.default_rng(wid).choice(w.tokens, 16, replace=False)
-    _chain(w, 0, layers, w.n_iters, 8, out_at={(0, 0), (2, w.n_iters - 1)}, out_tokens=rows)
+    _chain(w, 0, layers, w.n_iters, len(layers) * w.n_experts,
+           out_at={(0, 0), (1, 1), (2, w.n_iters - 1)}, out_tokens=rows)
 
 
 DENSE = W.WORKLOADS[1].replace(wid=300, name="dense", dtype="bf16", batch=4, block=256,
@@ -341,28 +365,28 @@ def test_block_boundaries():
     w = W.WORKLOADS[2]
     layers, N = [0, 7, 15], w.n_iters
     _say(f"[blocks] {w.name} layers={layers} blocks=2 iters={N}")
-    ref = O.run_schedule(lambda li, g: W.logits(w, 0, layers[li], g // N, g % N),
-                         lambda li, g: W.confidence(w, 0, g // N, g % N),
-                         len(layers), 2 * N, w.n_experts, w.top_k, w.capacity)
-    pool = HN.fill_pool(w, 0, 32)
+    P = len(layers) * w.n_experts
+    raw = W.expert_blocks(w, 0, range(P))
+    pool = HN.fill_pool(w, 0, P, raw=raw)
     ctx = HN.make_context(w, pool, n_layers=len(layers))
-    ow = OracleWeights(w, 0, 32, len(layers))
+    lock = LockstepOracle(len(layers), w.n_experts, w.top_k, w.capacity)
+    ow = OracleWeights(w, 0, P, len(layers), raw=raw)
     dt = HN.torch_dtype(w)
     try:
         for g in range(2 * N):
             b, i = divmod(g, N)
             conf = torch.from_numpy(W.confidence(w, 0, b, i)).cuda()
             for li, l in enumerate(layers):
-                lg = torch.from_numpy(W.logits(w, 0, l, b, i)).cuda()
+                lg_h = W.logits(w, 0, l, b, i)
+                lg = torch.from_numpy(lg_h).cuda()
                 x = HN.to_device(W.activations(w, 0, l, b, i))
                 y = torch.empty((w.tokens, w.hidden), dtype=dt, device="cuda")
                 rep = HN.layer_step(ctx, li, lg, conf, x, y)
                 st = ctx.read_layer_state(li, w.tokens)
                 where = f"block {b} iter {i} layer {l}"
-                compare_control(st, ref[g][li], w.tokens, where)
-                check_report(rep, ref[g][li], w.expert_bytes, where)
+                o = lock.step(li, lg_h, W.confidence(w, 0, b, i), st, where)
+                check_report(rep, o, w.expert_bytes, where)
                 if g in (N - 1, N):
-                    o = ref[g][li]
                     y_ref = O.moe_output(O.decode(W.activations(w, 0, l, b, i)), o["idx"],
                                          o["gates"], ow.fn(li))
                     err = rel_l2(O.decode(HN.from_device(y)), y_ref)

@@ -43,19 +43,21 @@ def _chain(w, seed, C, policy, period=0, forward=False, outs=None):
     L = w.n_layers
     _say(f"[policy] {w.name} policy={policy} C={C} period={period} forward={forward}")
     ref = _oracle(w, seed, C, policy, period)
-    pool = HN.fill_pool(w, seed, 16)
+    pool = HN.fill_pool(w, seed, w.n_experts + 1)
     ctx = HN.make_context(w, pool, capacity=C, policy=policy, adapt_period=period)
 
     def check(i, li, st, y, rep):
         o = ref[i][li]
         where = f"{policy} l={li} i={i}"
-        if li == L - 1 and "capacities_after" in o:
-            st = dict(st, resident_after=o["resident_after"])
+        resized = li == L - 1 and "capacities_after" in o
+        if resized:
             for lj in range(L):
                 sj = ctx.read_layer_state(lj, w.tokens)
                 np.testing.assert_array_equal(sj["resident_after"], o["residents_after_update"][lj],
                                               err_msg=f"{where} layer {lj} after re-sizing")
-        compare_control(st, o, w.tokens, where)
+        compare_control(st, o, w.tokens, where, W.logits(w, seed, li, 0, i),
+                        W.confidence(w, seed, 0, i), o["capacity"], policy=policy,
+                        state_after=o["residents_after_update"][li] if resized else None)
         np.testing.assert_array_equal(st["retain_key"], o["key"], err_msg=where + " key")
         assert (st["prev_transferred"], st["reused_transfers"]) == (
             o["prev_transferred"], o["reused_transfers"]), where

@@ -70,7 +70,8 @@ def test_gate_routing(dtype, batch, block, E, k, H, C):
                 err = np.abs(lg.astype(np.float64) - ref)
                 assert np.all(err <= bound), f"logit error {err.max():.3e} above the bound"
                 o = O.layer_step(lg.copy(), conf_h, res[l], k, C)
-                compare_control(st, o, T, f"{w.name} l={l} i={i}")
+                o["lockstep"] = True
+                o = compare_control(st, o, T, f"{w.name} l={l} i={i}", lg.copy(), conf_h, C)
                 res[l] = o["resident_after"]
                 # where rounding cannot reorder them, the exact top-k set
                 srt = np.sort(ref, axis=1)[:, ::-1]
