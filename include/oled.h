@@ -60,6 +60,7 @@
 #ifndef OLED_H_
 #define OLED_H_
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -456,6 +457,38 @@ oled_status oled_profile_collect(void* ctx, oled_op_time* out, int32_t cap, int3
  */
 oled_status oled_pack_expert(int32_t dtype, int32_t hidden, int32_t inter, const void* w13,
                              const void* w2, void* block_out);
+
+/*
+ * Routing and permutation of one block without a context and without any
+ * allocation: for callers that cannot allocate device memory (code under HIP
+ * graph capture, serving loops and harnesses that forbid hipMalloc). It
+ * computes what route_block computes before the cache is consulted, with the
+ * same kernels and bit-identical results: top-k ids and fp64-evaluated gates
+ * (one fp32 rounding, slot order logit desc / id asc), the expert histogram,
+ * exclusive offsets and the stable permutation. There is no expert cache:
+ * no hit/miss split, staging or records.
+ *  logits_dev [T][E] fp32 (read); topk_idx_dev [T*k] int32, gates_dev [T*k]
+ *  fp32, counts_dev [E], offsets_dev [E+1], perm_dev [T*k] (sorted position ->
+ *  route), inv_perm_dev [T*k] (route -> position), all int32 except gates,
+ *  caller-owned device memory on the current device, overwritten.
+ *  nonfinite_dev: optional int32 written 1 if a logit was NaN or infinite
+ *  (the other outputs are then unspecified), else 0.
+ *  stream: a stream of the current device (NULL: the null stream).
+ * Limits: 1 <= T <= 65535, 1 <= k <= E <= 256, k <= 16 (UNSUPPORTED beyond
+ * them, INVALID_ARG for a NULL output or T, E, k below 1; the text is in
+ * oled_last_error(NULL)). The launches' counters and per-chunk counts live in
+ * one file-scope device array of oled_route_noalloc_scratch_bytes() bytes
+ * (about 128 KiB), one copy per GPU, held until the process ends; the call
+ * clears what must start at zero with a small kernel (no memset node), so it
+ * can be captured. Calls on one GPU share that array: calls whose work
+ * overlaps on the device (concurrent streams, or threads) race; calls in
+ * one stream's order do not. Returns HIP if a launch fails.
+ */
+oled_status oled_route_noalloc(const float* logits_dev, int32_t T, int32_t E, int32_t k,
+                               int32_t* topk_idx_dev, float* gates_dev, int32_t* counts_dev,
+                               int32_t* offsets_dev, int32_t* perm_dev, int32_t* inv_perm_dev,
+                               int32_t* nonfinite_dev, void* stream);
+size_t oled_route_noalloc_scratch_bytes(void);
 
 /* Pinned host memory for expert pools (hipHostMalloc). *ptr_out NULL on error. */
 oled_status oled_host_alloc(int64_t bytes, void** ptr_out);

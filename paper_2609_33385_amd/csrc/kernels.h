@@ -187,7 +187,9 @@ struct PermuteOut {
   int32_t* pub_topk;      // pinned [T*k]: with `staged`, the routes are published too
   float* pub_gates;       //   (cooperative compensation), or null
   int layer, E, seq;
-  CacheView cv;
+  CacheView cv;           // cv.hdr null: no expert cache (routing and permutation only:
+                          // no staging, work items, records or cache-state writes)
+  int32_t* bad_out = nullptr;  // without a cache: 1 if a logit was non-finite, else 0
 };
 
 // K2: histogram, offsets, stable permutation, hit-first work list, and the
@@ -290,6 +292,9 @@ hipError_t launch_layer_adapt(const AdaptArgs& a, hipEvent_t ev0, hipEvent_t ev1
 // Their staging slots return to the free list, they leave the staged list
 // (so only the transferred ones are copied) and the previous-transfer mask,
 // and the retention of the layer skips them as candidates.
+// Text of oled_last_error(NULL): errors of calls without a context.
+void set_noctx_error(const char* msg);
+
 hipError_t launch_coop_unstage(const CacheView& cv, int layer, int E, const ExpertMask& cpu,
                                hipStream_t s);
 

@@ -1815,3 +1815,7 @@ void oled_host_free(void* ptr) {
 }
 
 }  // extern "C"
+
+namespace oled {
+void set_noctx_error(const char* msg) { g_create_error = msg; }
+}  // namespace oled

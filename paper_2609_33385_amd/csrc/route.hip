@@ -344,6 +344,7 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
   const int nthr = blockDim.x;
   const int E = o.E, layer = o.layer;
   const int R = T * k;
+  const bool cache = o.cv.hdr != nullptr;   // else routing and permutation only
   for (int e = tid; e < kMaxExperts; e += nthr) s_cnt[e] = 0;
   __syncthreads();
   // Chunked: counts per chunk in chunk_base [n_chunks][E], from other
@@ -439,7 +440,8 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
     // staging: every miss takes a free slot, unless the block is bad
     CacheHdr* hdr = o.cv.hdr;
     const int free_top = *s_ftop;
-    const bool stage = !bad && free_top >= 0 && free_top <= o.cv.n_slots && n_miss <= free_top;
+    const bool stage = cache && !bad && free_top >= 0 && free_top <= o.cv.n_slots &&
+                       n_miss <= free_top;
     int xc = ic - sc, xh = ih - sh, xm = im - sm, xx = ix - sx, xdf = idf - sdf,
         xds = tot_full + ids - sds;
 #pragma unroll
@@ -471,7 +473,7 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
     uint64_t mb[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) mb[q] = __ballot(stage && miss[q]);
-    if (lane < kMaxExperts / 32) {
+    if (cache && lane < kMaxExperts / 32) {
       uint32_t word = 0u;
 #pragma unroll
       for (int j = 0; j < 8; ++j)
@@ -481,17 +483,21 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
       o.cv.prev_miss[layer].bits[lane] = word;
     }
     if (lane == 0) {
-      hdr->free_top = stage ? free_top - n_miss : free_top;
-      hdr->staged_n = stage ? n_miss : 0;
-      hdr->route_bad = stage ? 0 : 1;
-      if (!bad && !stage) hdr->fault |= 1;
-      int32_t* lc = o.cv.last_counts + kCountsPerLayer * layer;
-      lc[0] = n_act;
-      lc[1] = n_hit;
-      lc[2] = n_miss;
-      lc[3] = n_res;
-      lc[4] = n_px;
-      lc[5] = n_rx;
+      if (cache) {
+        hdr->free_top = stage ? free_top - n_miss : free_top;
+        hdr->staged_n = stage ? n_miss : 0;
+        hdr->route_bad = stage ? 0 : 1;
+        if (!bad && !stage) hdr->fault |= 1;
+        int32_t* lc = o.cv.last_counts + kCountsPerLayer * layer;
+        lc[0] = n_act;
+        lc[1] = n_hit;
+        lc[2] = n_miss;
+        lc[3] = n_res;
+        lc[4] = n_px;
+        lc[5] = n_rx;
+      } else if (o.bad_out) {
+        *o.bad_out = bad ? 1 : 0;
+      }
       s_stat[16] = n_px;
       s_stat[17] = n_rx;
       s_stat[0] = n_act;
@@ -512,7 +518,7 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
       s_stat[14] = tot_full;
       s_stat[15] = tot_short;
     }
-    if (lane < kMaxExperts / 32) o.cv.res_before[layer].bits[lane] = s_res[lane];
+    if (cache && lane < kMaxExperts / 32) o.cv.res_before[layer].bits[lane] = s_res[lane];
   }
   __syncthreads();
 
@@ -521,6 +527,7 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
     o.counts[e] = c;
     o.offsets[e] = s_off[e];
     s_run[e] = s_off[e];
+    if (!o.items) continue;   // no work lists without a cache
     // a hit's slot cannot change before the layer's retention: the GEMMs take
     // it from the item; a miss's slot is looked up when its GEMM runs
     const int hslot = ((s_res[e >> 5] >> (e & 31)) & 1u) ? s_slot[e] : -1;
@@ -573,7 +580,7 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
 
   // the routing record: device ring (read by the host at its synchronisation
   // points), and for host-issued copies the staged list in pinned memory
-  if (tid < 64) {
+  if (cache && tid < 64) {
     const int n_staged = s_stat[6];
     RouteStats rs;
     rs.layer = layer;
@@ -631,6 +638,15 @@ __device__ __forceinline__ void prefetch_state(const CacheView& cv, int E, int l
                                                int32_t* s_free, int32_t* s_ftop, uint32_t* s_res,
                                                uint32_t* s_pm, int32_t* s_slot) {
   const int lane = threadIdx.x & 63;
+  if (!cv.hdr) {   // no expert cache: nothing resident, nothing to stage into
+#pragma unroll
+    for (int q = 0; q < kMaxExperts / 64; ++q)
+      if (lane + 64 * q < E) s_slot[lane + 64 * q] = -1;
+    if (lane < kMaxExperts / 32) s_res[lane] = 0u;
+    else if (lane < kMaxExperts / 16) s_pm[lane - kMaxExperts / 32] = 0u;
+    if (lane == 0) *s_ftop = 0;
+    return;
+  }
 #pragma unroll
   for (int q = 0; q < kMaxExperts / 64; ++q) {
     const int e = lane + 64 * q;
@@ -1210,3 +1226,118 @@ hipError_t launch_route_fused(const float* logits, int T, int k, int32_t* topk_i
 }
 
 }  // namespace oled
+
+// ---------------------------------------------------------------------------
+// Routing and permutation without a context and without allocation: the
+// scratch of the routing launches lives in one file-scope device array.
+#include <mutex>
+
+#include "oled.h"
+
+namespace {
+
+constexpr int kNoAllocMaxTokens = 65535;
+constexpr int kNoAllocChunks = (kNoAllocMaxTokens + oled::kChunkTokens - 1) / oled::kChunkTokens;
+// int32 layout: [0] non-finite flag of the top-k launch, [1] completion
+// counter of the counting launch, [2..3] completion counter and flag of the
+// fused launch, [64, 64 + kNoAllocChunks * kMaxExperts) per-chunk counts.
+constexpr int kScratchHead = 64;
+constexpr int kScratchInts = kScratchHead + kNoAllocChunks * oled::kMaxExperts;
+constexpr int kMaxDevices = 64;
+
+__device__ __align__(256) int32_t scratch[kScratchInts];
+
+int32_t* g_scratch_dev[kMaxDevices];   // device address of `scratch` on each GPU
+std::mutex g_scratch_mu;
+
+__global__ __launch_bounds__(64) void k_clear_head(int32_t* head) {
+  head[threadIdx.x] = 0;
+}
+
+// Address of this GPU's copy of the array (looked up once per device, with
+// that device current).
+hipError_t scratch_on(int dev, int32_t** out) {
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_dev[dev] = static_cast<int32_t*>(p);
+  }
+  *out = g_scratch_dev[dev];
+  return hipSuccess;
+}
+
+}  // namespace
+
+extern "C" size_t oled_route_noalloc_scratch_bytes(void) {
+  return sizeof(int32_t) * static_cast<size_t>(kScratchInts);
+}
+
+extern "C" oled_status oled_route_noalloc(const float* logits_dev, int32_t T, int32_t E,
+                                          int32_t k, int32_t* topk_idx_dev, float* gates_dev,
+                                          int32_t* counts_dev, int32_t* offsets_dev,
+                                          int32_t* perm_dev, int32_t* inv_perm_dev,
+                                          int32_t* nonfinite_dev, void* stream) {
+  if (!logits_dev || !topk_idx_dev || !gates_dev || !counts_dev || !offsets_dev || !perm_dev ||
+      !inv_perm_dev) {
+    oled::set_noctx_error("oled_route_noalloc: NULL input or output");
+    return OLED_ERR_INVALID_ARG;
+  }
+  if (T < 1 || E < 1 || k < 1 || k > E) {
+    oled::set_noctx_error("oled_route_noalloc: T, E and k must be >= 1 and k <= E");
+    return OLED_ERR_INVALID_ARG;
+  }
+  if (T > kNoAllocMaxTokens || E > oled::kMaxExperts || k > oled::kMaxTopK) {
+    oled::set_noctx_error("oled_route_noalloc: T above 65535, E above 256 or k above 16 "
+                          "exceeds the fixed scratch array");
+    return OLED_ERR_UNSUPPORTED;
+  }
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    oled::set_noctx_error("oled_route_noalloc: no current device");
+    return OLED_ERR_HIP;
+  }
+  int32_t* sc = nullptr;
+  if (scratch_on(dev, &sc) != hipSuccess) {
+    oled::set_noctx_error("oled_route_noalloc: hipGetSymbolAddress of the scratch array failed");
+    return OLED_ERR_HIP;
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+
+  oled::PermuteOut o{};
+  o.counts = counts_dev;
+  o.offsets = offsets_dev;
+  o.perm = perm_dev;
+  o.inv_perm = inv_perm_dev;
+  o.gates = gates_dev;
+  o.E = E;
+  o.bad_out = nonfinite_dev;   // written by the planning workgroup (cv.hdr null: no cache)
+
+  // the counters and flags start at zero (the launches also leave them zero)
+  hipLaunchKernelGGL(k_clear_head, dim3(1), dim3(kScratchHead), 0, s, sc);
+  if (hipGetLastError() != hipSuccess) {
+    oled::set_noctx_error("oled_route_noalloc: launch failed");
+    return OLED_ERR_HIP;
+  }
+  hipError_t e;
+  if (oled::route_fused(T, k)) {
+    e = oled::launch_route_fused(logits_dev, T, k, topk_idx_dev, gates_dev, sc + 2, o, nullptr,
+                                 nullptr, s);
+  } else {
+    e = oled::launch_route_topk(logits_dev, T, E, k, topk_idx_dev, gates_dev, sc, nullptr,
+                                nullptr, s);
+    if (e == hipSuccess) {
+      if (oled::permute_chunked(T))
+        e = oled::launch_permute_chunked(topk_idx_dev, T, k, sc, sc + kScratchHead, sc + 1, o,
+                                         nullptr, nullptr, s);
+      else
+        e = oled::launch_permute(topk_idx_dev, T, k, sc, o, nullptr, nullptr, s);
+    }
+  }
+  if (e != hipSuccess) {
+    oled::set_noctx_error("oled_route_noalloc: launch failed");
+    return OLED_ERR_HIP;
+  }
+  return OLED_OK;
+}

@@ -53,7 +53,7 @@ EXPORTED = ["oled_create", "oled_destroy", "oled_last_error", "oled_reset_cache"
             "apply_misses", "apply_misses_coop", "moe_forward_cached", "score_and_retain",
             "oled_read_layer_state", "oled_collect_stats", "oled_profile_collect",
             "oled_pack_expert", "oled_host_alloc", "oled_host_free", "oled_coop_dispatch",
-            "oled_cpu_ffn"]
+            "oled_cpu_ffn", "oled_route_noalloc", "oled_route_noalloc_scratch_bytes"]
 
 
 class OledConfig(ctypes.Structure):
@@ -148,6 +148,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "oled_pack_expert": (i32, [i32, i32, i32, vp, vp, vp]),
         "oled_host_alloc": (i32, [i64, ctypes.POINTER(vp)]),
         "oled_host_free": (None, [vp]),
+        "oled_route_noalloc": (i32, [vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp]),
+        "oled_route_noalloc_scratch_bytes": (ctypes.c_size_t, []),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -251,6 +253,15 @@ def oled_cpu_ffn(dtype: str, hidden: int, inter: int, block: np.ndarray, x: np.n
     if st != OLED_OK:
         raise OledError(st, "oled_cpu_ffn")
     return out
+
+
+def oled_route_noalloc(logits, T: int, E: int, k: int, topk_idx, gates, counts, offsets, perm,
+                       inv_perm, nonfinite=None, stream=None) -> int:
+    """Routing and permutation without a context (device tensors in, device
+    tensors out); returns the status."""
+    return load().oled_route_noalloc(_ptr(logits), T, E, k, _ptr(topk_idx), _ptr(gates),
+                                     _ptr(counts), _ptr(offsets), _ptr(perm), _ptr(inv_perm),
+                                     _ptr(nonfinite), _stream(stream))
 
 
 def moe_forward_cached(ctx, layer: int, x, y, stream=None) -> int:

@@ -18,7 +18,8 @@ HEADER = os.path.join(ROOT, "include", "oled.h")
 
 def header_functions():
     text = open(HEADER).read()
-    return re.findall(r"^\s*(?:oled_status|void|const char\s*\*)\s+(\w+)\s*\(", text, re.M)
+    return re.findall(r"^\s*(?:oled_status|void|size_t|const char\s*\*)\s+(\w+)\s*\(", text,
+                      re.M)
 
 
 def test_library_exports_header_symbols():
@@ -189,3 +190,23 @@ def test_create_rejects_bad_policy():
     cfg.policy = 3
     assert lib.oled_create(ctypes.byref(cfg), ctypes.byref(h)) == oled.OLED_ERR_INVALID_ARG
     assert b"policy" in lib.oled_last_error(None)
+
+
+def test_route_noalloc_checks_arguments_before_the_gpu():
+    """The allocation-free routing call rejects bad sizes and NULL buffers on
+    the host (no device is touched), with the reason in oled_last_error(NULL)."""
+    lib = oled.load()
+    d = 0x1000    # never dereferenced: every call below fails its host checks
+    assert lib.oled_route_noalloc_scratch_bytes() >= 4 * 128 * 256
+    cases = [((None, 8, 8, 2), oled.OLED_ERR_INVALID_ARG),
+             ((d, 0, 8, 2), oled.OLED_ERR_INVALID_ARG),
+             ((d, 8, 8, 9), oled.OLED_ERR_INVALID_ARG),
+             ((d, 65536, 8, 2), oled.OLED_ERR_UNSUPPORTED),
+             ((d, 8, 257, 2), oled.OLED_ERR_UNSUPPORTED),
+             ((d, 8, 64, 17), oled.OLED_ERR_UNSUPPORTED)]
+    for (lg, T, E, k), want in cases:
+        st = lib.oled_route_noalloc(lg, T, E, k, d, d, d, d, d, d, None, None)
+        assert st == want, (T, E, k)
+        assert "oled_route_noalloc" in oled.last_error(None)
+    assert lib.oled_route_noalloc(d, 8, 8, 2, d, None, d, d, d, d, None, None) == \
+        oled.OLED_ERR_INVALID_ARG
