@@ -204,17 +204,22 @@ def expert_ffn(x: np.ndarray, w13: np.ndarray, w2: np.ndarray) -> np.ndarray:
 
 
 def moe_output(x: np.ndarray, idx: np.ndarray, gates: np.ndarray, expert_weights,
-               tokens=None) -> np.ndarray:
+               tokens=None, experts=None) -> np.ndarray:
     """O5. y[t] = sum_j gate[t][j] * FFN_{idx[t][j]}(x[t]) in float64.
 
     x float64 [T][H]; expert_weights(e) -> (w13, w2) float64. `tokens`
-    restricts the evaluation to a subset of token rows (returned in that order).
+    restricts the evaluation to a subset of token rows (returned in that order);
+    `experts` restricts the sum to the routes of those experts (the partial sum
+    a cost sample of the full output evaluates).
     """
     T = x.shape[0]
     rows = np.arange(T) if tokens is None else np.asarray(tokens)
     y = np.zeros((rows.size, x.shape[1]), dtype=np.float64)
     sub = idx[rows]
-    for e in np.unique(sub):
+    todo = np.unique(sub)
+    if experts is not None:
+        todo = np.intersect1d(todo, np.asarray(experts))
+    for e in todo:
         w13, w2 = expert_weights(int(e))
         for j in range(idx.shape[1]):
             sel = np.nonzero(sub[:, j] == e)[0]

@@ -386,6 +386,28 @@ def test_moe_token_subset():
     assert np.allclose(ys, y[sub], rtol=1e-13, atol=1e-15)
 
 
+def test_moe_expert_subsets_partition_the_output():
+    """Partial sums over disjoint expert sets add up to the full output, and
+    one expert's partial sum is its gate-weighted FFN on its own tokens."""
+    rng = np.random.default_rng(13)
+    T, E, H, I, k = 11, 6, 4, 3, 3
+    lg = rng.standard_normal((T, E)).astype(np.float32)
+    x = rng.standard_normal((T, H))
+    Ws = [(rng.standard_normal((2 * I, H)), rng.standard_normal((H, I))) for _ in range(E)]
+    idx, g = O.route(lg, k)
+    y = O.moe_output(x, idx, g, lambda e: Ws[e])
+    parts = [O.moe_output(x, idx, g, lambda e: Ws[e], experts=s) for s in ([0, 3], [1, 5], [2, 4])]
+    assert np.allclose(sum(parts), y, rtol=1e-12, atol=1e-14)
+    e = int(idx[0, 0])
+    ye = O.moe_output(x, idx, g, lambda q: Ws[q], experts=[e])
+    for t in range(T):
+        want = np.zeros(H)
+        for j in range(k):
+            if idx[t, j] == e:
+                want += float(g[t, j]) * O.expert_ffn(x[t:t + 1], *Ws[e])[0]
+        assert np.allclose(ye[t], want, rtol=1e-12, atol=1e-14)
+
+
 def test_bf16_decode():
     bits = np.array([0x3F80, 0xBF80, 0x0000, 0x8000, 0x4049, 0x7F7F], np.uint16)
     v = oracle.bf16_bits_to_f64(bits)
