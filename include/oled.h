@@ -243,14 +243,29 @@ oled_status oled_create(const oled_config* cfg, void** ctx_out);
 void oled_destroy(void* ctx);
 
 /* Text of the last error of ctx (never NULL; empty if none). With ctx NULL,
- * the last oled_create failure of the calling thread. */
+ * the last failure of a call without a context (oled_create,
+ * oled_route_noalloc) on the calling thread. */
 const char* oled_last_error(const void* ctx);
 
 /* Empties every layer's cache (R := {}) and restores capacity min(C, E), the
  * smoothed statistics and the iteration count, as at creation. Synchronises. Also
- * the way out after OLED_ERR_HIP, which leaves the context refusing
+ * the way out after an OLED_ERR_HIP that left the device state unknown (a
+ * failed launch, a wait past its deadline), which leaves the context refusing
  * route_block (OLED_ERR_STATE) until it is reset. */
 oled_status oled_reset_cache(void* ctx);
+
+/*
+ * Failure injection, for tests of the host's error paths (no device work
+ * fails; every kernel runs normally). Resets the enqueue count.
+ *  copy_fail_at > 0: the copy_fail_at-th miss copy that apply_misses enqueues
+ *  from now on (OLED_COPY_SDMA) is not enqueued and fails as a failed
+ *  hipMemcpyAsync would, once; 0: off.
+ *  wait_deadline_ms > 0: how long the host waits for miss copies and for
+ *  route_block's published result before it gives up with OLED_ERR_HIP;
+ *  0: the default, 60000 ms.
+ *  Errors: INVALID_ARG (NULL ctx, a negative value).
+ */
+oled_status oled_set_fault_injection(void* ctx, int32_t copy_fail_at, int32_t wait_deadline_ms);
 
 /*
  * route_block: the gate of Sec. 4.1 for the T tokens of the block.
@@ -325,10 +340,16 @@ oled_status moe_forward_cached(void* ctx, int32_t layer, const void* x_dev, void
  *  Errors: STATE; INVALID_ARG if the record shows a non-finite logit (only
  *  seen when the record is read: with a report, or always with
  *  OLED_COPY_SDMA): nothing was staged, y is not written, the layer returns
- *  to idle with its cache unchanged; HIP if a launch or copy could not be
- *  enqueued (the context then needs oled_reset_cache). Retentions enqueued
- *  earlier that were rejected for an invalid confidence are named in
- *  out->rejected_layer (the call still returns OLED_OK for its own work).
+ *  to idle with its cache unchanged. HIP if a miss copy could not be
+ *  enqueued: the copies already enqueued are waited for, the staged misses
+ *  return their slots, the layer's resident set, slot table and last
+ *  retention keys stay as they were, y is not written and the layer returns
+ *  to idle (the context stays usable). HIP if a launch failed, or a copy or
+ *  the routing result did not complete within the wait deadline (60 s by
+ *  default): the device state is then unknown and the context needs
+ *  oled_reset_cache. Retentions enqueued earlier that were rejected for an
+ *  invalid confidence are named in out->rejected_layer (the call still
+ *  returns OLED_OK for its own work).
  */
 oled_status apply_misses(void* ctx, int32_t layer, void* copy_stream, oled_miss_report* out);
 

@@ -261,6 +261,8 @@ struct ScoreArgs {
   int parts;              // scoring workgroups: score_parts(T, k)
   unsigned long long* acc;  // [E] zero between launches (several parts only)
   int32_t* acc_sync;        // [2] completion counter, bad flag; zero between launches
+  int reject = 0;         // 1: commit nothing (R stays, staged misses return their slots);
+                          // with T = 0 no route or confidence is read
 };
 
 // Workgroups that score a block of T tokens (one up to 8192 routes).

@@ -25,6 +25,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <chrono>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -68,6 +69,8 @@ struct OpRec {
   int64_t bytes, flops, h2d;
   hipEvent_t a, b;
 };
+
+constexpr int64_t kDefaultWaitDeadlineMs = 60000;
 
 struct Ctx {
   // shape
@@ -160,6 +163,10 @@ struct Ctx {
   int last_routed_layer = -1, last_routed_T = 0;
   bool copies_outstanding = false;
   bool broken = false;             // a HIP failure left the device state unknown
+  // host waits give up after this long (oled_set_fault_injection may shorten it)
+  int64_t wait_deadline_ms = kDefaultWaitDeadlineMs;
+  int copy_fail_at = 0;            // injection: the n-th miss copy enqueue from now fails
+  int copy_count = 0;
   std::string err;
   // profiling
   std::vector<OpRec> ops;
@@ -250,16 +257,26 @@ OpRec rec(int kind, int layer, int64_t bytes, int64_t flops = 0) {
   return r;
 }
 
+bool past_deadline(const Ctx* c, std::chrono::steady_clock::time_point t0) {
+  return std::chrono::steady_clock::now() - t0 > std::chrono::milliseconds(c->wait_deadline_ms);
+}
+
 // Spins until a kernel has published `want` into *flag (coherent pinned
 // memory). Checks the stream now and then so a failed launch cannot hang.
 oled_status wait_published(Ctx* c, const int32_t* flag, int want, hipStream_t s, const char* what) {
   const volatile int32_t* p = flag;
+  const auto t0 = std::chrono::steady_clock::now();
   for (uint64_t spin = 1;; ++spin) {
     if (*p == want) {
       std::atomic_thread_fence(std::memory_order_acquire);
       return OLED_OK;
     }
     if ((spin & 255) == 0) {
+      if (past_deadline(c, t0)) {
+        c->broken = true;
+        return fail(c, OLED_ERR_HIP, "%s: not published within %lld ms", what,
+                    static_cast<long long>(c->wait_deadline_ms));
+      }
       const hipError_t e = hipStreamQuery(s);
       if (e == hipSuccess) {  // the stream is idle: the value must be visible now
         if (*p == want) {
@@ -279,10 +296,16 @@ oled_status wait_published(Ctx* c, const int32_t* flag, int want, hipStream_t s,
 // a few microseconds; a GPU-side stream wait on a copy-engine event has been
 // measured to add tens of microseconds on this path.
 oled_status wait_event_spin(Ctx* c, hipEvent_t ev, const char* what) {
-  for (;;) {
+  const auto t0 = std::chrono::steady_clock::now();
+  for (uint64_t spin = 1;; ++spin) {
     const hipError_t e = hipEventQuery(ev);
     if (e == hipSuccess) return OLED_OK;
     if (e != hipErrorNotReady) return hip_fail(c, e, what);
+    if ((spin & 63) == 0 && past_deadline(c, t0)) {   // copies still in flight: state unknown
+      c->broken = true;
+      return fail(c, OLED_ERR_HIP, "%s: not complete within %lld ms", what,
+                  static_cast<long long>(c->wait_deadline_ms));
+    }
     _mm_pause();
   }
 }
@@ -705,6 +728,50 @@ oled_status launch_dense(Ctx* c, int layer, hipStream_t s) {
   return OLED_OK;
 }
 
+// hipMemcpyAsync of a miss copy on the copy stream, or the injected failure
+// of the n-th enqueue (oled_set_fault_injection).
+hipError_t enqueue_miss_copy(Ctx* c, void* dst, const void* src, size_t n, hipStream_t cs) {
+  if (c->copy_fail_at > 0 && ++c->copy_count >= c->copy_fail_at) {
+    c->copy_fail_at = 0;
+    c->copy_count = 0;
+    return hipErrorInvalidValue;
+  }
+  return hipMemcpyAsync(dst, src, n, hipMemcpyHostToDevice, cs);
+}
+
+// After a miss copy could not be enqueued: waits for the copies already
+// enqueued, then a retention launch that commits nothing returns the staged
+// misses' slots to the free list and keeps the layer's resident set, slot
+// table and last retention keys, so the layer is left as its last retention
+// left it. Device work stays in stream order, so the context stays usable.
+oled_status rollback_layer(Ctx* c, int layer, hipStream_t s, hipStream_t cs) {
+  HIP_TRY(c, hipStreamSynchronize(cs));
+  c->copies_outstanding = false;
+  const int seq = ++c->seq;
+  oled::ScoreArgs a;
+  a.gates = c->d_gates;
+  a.conf = nullptr;
+  a.topk_idx = c->d_topk;
+  a.counts = c->d_counts;
+  a.T = 0;                  // no route or confidence is read
+  a.k = c->K;
+  a.E = c->E;
+  a.layer = layer;
+  a.seq = seq;
+  a.cv = view(c);
+  a.score_out = c->d_score + static_cast<size_t>(layer) * c->E;
+  a.out = c->d_ret + layer;
+  a.key_out = c->d_key + static_cast<size_t>(layer) * c->E;
+  a.parts = oled::score_parts(0, c->K);
+  a.acc = c->d_sacc;
+  a.acc_sync = c->d_ssync;
+  a.reject = 1;
+  HIP_TRY(c, oled::launch_score_retain(a, nullptr, nullptr, s));
+  c->ret_seq[layer] = seq;
+  c->ret_seen[layer] = 0;
+  return OLED_OK;
+}
+
 // Copy-engine transfer: the staged misses (from the routing kernel's list)
 // are copied with hipMemcpyAsync on the copy stream, gate/up parts of all
 // first, then the down parts; if the hits were queued, the misses' GEMMs are
@@ -730,18 +797,22 @@ oled_status apply_misses_sdma(Ctx* c, int layer, hipStream_t cs, const RouteStat
           break;
         }
         const int64_t blk = c->host_block_of[static_cast<size_t>(layer) * c->E + ex];
-        e = hipMemcpyAsync(c->d_pool + static_cast<int64_t>(sl) * c->eb + off,
-                           c->host_pool + blk * c->eb + off, len, hipMemcpyHostToDevice, cs);
+        e = enqueue_miss_copy(c, c->d_pool + static_cast<int64_t>(sl) * c->eb + off,
+                              c->host_pool + blk * c->eb + off, len, cs);
         bytes += len;
       }
       if (e == hipSuccess) e = hipEventRecord(part == 0 ? c->ev_up : c->ev_down, cs);
     }
     if (e == hipSuccess && ev.b) e = hipEventRecord(ev.b, cs);
     if (e != hipSuccess) {
-      (void)hipStreamSynchronize(cs);
       if (ev.a) c->ev_free.push_back(ev.a);
       if (ev.b) c->ev_free.push_back(ev.b);
-      return hip_fail(c, e, "enqueueing the miss copies");
+      st = rollback_layer(c, layer, s, cs);
+      if (st != OLED_OK) return st;
+      return fail(c, OLED_ERR_HIP,
+                  "layer %d: a miss copy could not be enqueued (%s); its misses were not "
+                  "installed, its cache is unchanged and its output was not computed",
+                  layer, hipGetErrorString(e));
     }
     OpRec o = rec(OLED_OP_H2D, layer, bytes);
     o.h2d = bytes;
@@ -1157,6 +1228,15 @@ void oled_destroy(void* ctx) { free_ctx(static_cast<Ctx*>(ctx)); }
 const char* oled_last_error(const void* ctx) {
   if (!ctx) return g_create_error.c_str();
   return static_cast<const Ctx*>(ctx)->err.c_str();
+}
+
+oled_status oled_set_fault_injection(void* ctx, int32_t copy_fail_at, int32_t wait_deadline_ms) {
+  Ctx* c = static_cast<Ctx*>(ctx);
+  if (!c || copy_fail_at < 0 || wait_deadline_ms < 0) return OLED_ERR_INVALID_ARG;
+  c->copy_fail_at = copy_fail_at;
+  c->copy_count = 0;
+  c->wait_deadline_ms = wait_deadline_ms > 0 ? wait_deadline_ms : kDefaultWaitDeadlineMs;
+  return OLED_OK;
 }
 
 oled_status oled_reset_cache(void* ctx) {

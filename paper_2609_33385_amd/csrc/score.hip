@@ -142,7 +142,7 @@ __device__ __forceinline__ void score_commit(const ScoreArgs& a, unsigned long l
   // (s_rc and s_rank are next read after the barrier that follows the keys)
   const int s_bad = *p_bad;
   CacheHdr* hdr = cv.hdr;
-  const bool commit = !s_bad && !st.route_bad;
+  const bool commit = !s_bad && !st.route_bad && !a.reject;
 
   // The retention key: S under the paper's priority; under LRU / LFU the
   // layer's history, advanced by this iteration's routing when it commits
@@ -210,7 +210,7 @@ __device__ __forceinline__ void score_commit(const ScoreArgs& a, unsigned long l
       fault |= 4;
       keep = false;
     }
-    if (e < E) {
+    if (e < E && !a.reject) {   // a rejected layer keeps its last retention's keys
       score_out[e] = s_S[e];
       a.key_out[e] = s_K[e];
     }

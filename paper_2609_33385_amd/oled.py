@@ -53,7 +53,8 @@ EXPORTED = ["oled_create", "oled_destroy", "oled_last_error", "oled_reset_cache"
             "apply_misses", "apply_misses_coop", "moe_forward_cached", "score_and_retain",
             "oled_read_layer_state", "oled_collect_stats", "oled_profile_collect",
             "oled_pack_expert", "oled_host_alloc", "oled_host_free", "oled_coop_dispatch",
-            "oled_cpu_ffn", "oled_route_noalloc", "oled_route_noalloc_scratch_bytes"]
+            "oled_cpu_ffn", "oled_route_noalloc", "oled_route_noalloc_scratch_bytes",
+            "oled_set_fault_injection"]
 
 
 class OledConfig(ctypes.Structure):
@@ -149,6 +150,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "oled_host_alloc": (i32, [i64, ctypes.POINTER(vp)]),
         "oled_host_free": (None, [vp]),
         "oled_route_noalloc": (i32, [vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp]),
+        "oled_set_fault_injection": (i32, [vp, i32, i32]),
         "oled_route_noalloc_scratch_bytes": (ctypes.c_size_t, []),
     }
     for name, (res, args) in sig.items():
@@ -380,6 +382,9 @@ class Context:
 
     def reset_cache(self):
         oled_reset_cache(self.ctx)
+
+    def set_fault_injection(self, copy_fail_at: int = 0, wait_deadline_ms: int = 0):
+        _check(self.ctx, load().oled_set_fault_injection(self.ctx, copy_fail_at, wait_deadline_ms))
 
     def route_block(self, layer, logits, T, stream=None):
         _check(self.ctx, route_block(self.ctx, layer, logits, T, stream))
