@@ -172,6 +172,51 @@ def route(args):
     ctx.close()
     pool.free()
 
+    # the same 1 GiB as one batch of 32 independent blocks: one top-k launch
+    # over every token, the counting and ranking launches over (chunk, block),
+    # and the priority numerators of every block (HIP events on the stream)
+    lg_all = torch.stack(logits)
+    del logits
+    conf_all = torch.rand((L, T), generator=g, device="cuda")
+    dev = dict(topk=torch.empty((L, T * k), dtype=torch.int32, device="cuda"),
+               gates=torch.empty((L, T * k), dtype=torch.float32, device="cuda"),
+               counts=torch.empty((L, E), dtype=torch.int32, device="cuda"),
+               offsets=torch.empty((L, E + 1), dtype=torch.int32, device="cuda"),
+               perm=torch.empty((L, T * k), dtype=torch.int32, device="cuda"),
+               inv=torch.empty((L, T * k), dtype=torch.int32, device="cuda"),
+               bad=torch.empty((L,), dtype=torch.int32, device="cuda"),
+               S=torch.empty((L, E), dtype=torch.int64, device="cuda"))
+    ws = torch.empty(oled.oled_route_batch_workspace(L, T, E), dtype=torch.uint8, device="cuda")
+    st = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    t_route, t_prio = [], []
+    for it in range(args.iters + 1):
+        ev[0].record(st)
+        rc = oled.oled_route_batch(lg_all, L, T, E, k, dev["topk"], dev["gates"], dev["counts"],
+                                   dev["offsets"], dev["perm"], dev["inv"], dev["bad"], ws, st)
+        ev[1].record(st)
+        rc |= oled.oled_priority_batch(dev["topk"], dev["gates"], conf_all, L, T, E, k, dev["S"],
+                                       None, st)
+        ev[2].record(st)
+        torch.cuda.synchronize()
+        if rc:
+            raise RuntimeError(oled.last_error(None))
+        if it > 0:
+            t_route.append(ev[0].elapsed_time(ev[1]))
+            t_prio.append(ev[1].elapsed_time(ev[2]))
+    assert int(dev["bad"].sum()) == 0
+
+    def rate(ms, nbytes):
+        gbs = nbytes / 1e9 / (ms / 1e3)
+        return {"avg_us": round(ms * 1e3, 2), "bytes": nbytes, "GBps": round(gbs, 1),
+                "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)}
+
+    route_bytes = L * (T * E * 4 + T * k * 8 + T * k * 12 + E * 8)
+    prio_bytes = L * (T * k * 8 + T * 4 + E * 8)
+    batched = {"blocks": L, "calls": args.iters,
+               "route_batch": rate(float(np.mean(t_route)), route_bytes),
+               "priority_batch": rate(float(np.mean(t_prio)), prio_bytes)}
+
     def agg(name):
         sel = [o for o in ops if o[0] == name]
         ms, by = sum(o[2] for o in sel), sum(o[3] for o in sel)
@@ -187,7 +232,7 @@ def route(args):
                       "logit_bytes_per_pass": L * T * E * 4},
            "route_topk": agg("route_topk"), "permute": agg("permute"),
            "score_retain": agg("score_retain"), "passes": args.iters,
-           "wall_ms_per_pass": round(float(np.mean(t_wall)) * 1e3, 3)}
+           "wall_ms_per_pass": round(float(np.mean(t_wall)) * 1e3, 3), "batched": batched}
     print(json.dumps(out), flush=True)
 
 

@@ -511,6 +511,52 @@ oled_status oled_route_noalloc(const float* logits_dev, int32_t T, int32_t E, in
                                int32_t* nonfinite_dev, void* stream);
 size_t oled_route_noalloc_scratch_bytes(void);
 
+/*
+ * The gate's routing (Sec. 4.1) and the expert histogram, offsets and stable
+ * permutation (the active set of Sec. 4.2) of B independent blocks of T
+ * tokens in one pass, without a context or an expert cache: for work over
+ * many blocks whose logits are all at hand (replaying recorded routing of
+ * many layers or requests, as policy studies do, Sec. 5.3). Block b's results
+ * are bit-identical to route_block on block b alone.
+ *  logits_dev [B][T][E] fp32; outputs, per block b at offset b*T*k (routes),
+ *  b*E (counts), b*(E+1) (offsets): topk_idx_dev [B][T*k] int32, gates_dev
+ *  [B][T*k] fp32, counts_dev [B][E], offsets_dev [B][E+1], perm_dev [B][T*k]
+ *  (position within the block -> route within the block), inv_perm_dev
+ *  [B][T*k]; nonfinite_dev: optional int32 [B], 1 where a block has a NaN or
+ *  infinite logit (its other outputs are then unspecified), else 0. All
+ *  caller-owned device memory, overwritten.
+ *  workspace_dev: caller-owned device memory of at least
+ *  oled_route_batch_workspace(B, T, E) bytes (counters and per-chunk counts;
+ *  the call clears what must start at zero); nothing is allocated.
+ * Limits: 1 <= T <= 65535, 1 <= k <= E <= 256, k <= 16, B*T*k < 2^31
+ * (UNSUPPORTED beyond them; INVALID_ARG for NULL pointers, sizes below 1 or a
+ * short workspace, with the text in oled_last_error(NULL)). Calls that share
+ * a workspace must not overlap on the device.
+ */
+oled_status oled_route_batch(const float* logits_dev, int32_t B, int32_t T, int32_t E, int32_t k,
+                             int32_t* topk_idx_dev, float* gates_dev, int32_t* counts_dev,
+                             int32_t* offsets_dev, int32_t* perm_dev, int32_t* inv_perm_dev,
+                             int32_t* nonfinite_dev, void* workspace_dev, size_t workspace_bytes,
+                             void* stream);
+size_t oled_route_batch_workspace(int32_t B, int32_t T, int32_t E);
+
+/*
+ * The reuse-priority numerators of the priority equation of Sec. 4.3
+ * (psi(c) = c) of B independent blocks in one pass, without retention:
+ * score_q[b][e] = sum over routes r of block b with topk_idx[b][r] = e of
+ * floor(gate[b][r] * conf[b][r / k] * 2^48), exact in uint64 (the values
+ * score_and_retain computes for one block).
+ *  topk_idx_dev, gates_dev [B][T*k] as oled_route_batch writes them; conf_dev
+ *  [B][T] fp32 in [0, 1]; score_q_dev [B][E] uint64, overwritten;
+ *  bad_conf_dev: optional int32 [B], 1 where a block has a confidence outside
+ *  [0, 1] (its numerators are then unspecified), else 0.
+ * Limits and errors as oled_route_batch (T <= 65535 keeps every sum below
+ * 2^64). Nothing is allocated.
+ */
+oled_status oled_priority_batch(const int32_t* topk_idx_dev, const float* gates_dev,
+                                const float* conf_dev, int32_t B, int32_t T, int32_t E, int32_t k,
+                                uint64_t* score_q_dev, int32_t* bad_conf_dev, void* stream);
+
 /* Pinned host memory for expert pools (hipHostMalloc). *ptr_out NULL on error. */
 oled_status oled_host_alloc(int64_t bytes, void** ptr_out);
 void oled_host_free(void* ptr);

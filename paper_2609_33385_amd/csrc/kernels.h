@@ -166,9 +166,11 @@ hipError_t launch_router_logits(bool bf16, const void* x, const void* wg, int T,
 
 // K1: top-k + fp64 gates: one wavefront per token, or for large blocks one
 // token per lane.
+// block_tokens > 0: the T tokens are blocks of that many, and a non-finite
+// logit of token t sets bad_flag[t / block_tokens] (else bad_flag[0]).
 hipError_t launch_route_topk(const float* logits, int T, int E, int k, int32_t* topk_idx,
                              float* gates, int32_t* bad_flag, hipEvent_t ev0, hipEvent_t ev1,
-                             hipStream_t s);
+                             hipStream_t s, int block_tokens = 0);
 
 // Outputs of the permute stage for one layer.
 struct PermuteOut {
@@ -206,6 +208,16 @@ int permute_chunks(int T);
 hipError_t launch_permute_chunked(const int32_t* topk_idx, int T, int k, int32_t* bad_flag,
                                   int32_t* chunk_base, int32_t* counter, const PermuteOut& o,
                                   hipEvent_t ev0, hipEvent_t ev1, hipStream_t s);
+
+// K2 over B independent blocks of T tokens without a cache (o.cv.hdr null):
+// a counting launch over (chunk, block), a planning launch of one workgroup
+// per block and a ranking launch over (chunk, block); o's outputs advance per
+// block (routes by T*k, counts by E, offsets by E+1, bad_out by 1).
+// bad_flag: [B] non-finite flags of the top-k launch; chunk_base:
+// [B][permute_chunks(T)][E] scratch.
+hipError_t launch_permute_batch(const int32_t* topk_idx, int B, int T, int k,
+                                const int32_t* bad_flag, int32_t* chunk_base, const PermuteOut& o,
+                                hipStream_t s);
 
 // K1+K2 as one launch for blocks with T*k <= 1024 (route_fused true): the
 // last workgroup to finish routing permutes. sync: 2 device ints, zero

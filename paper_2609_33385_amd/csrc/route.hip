@@ -18,6 +18,11 @@ __device__ __forceinline__ uint32_t ord_key(float v) {
   return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
 }
 
+// Median of three (the compiler emits one v_med3_u32 for this form).
+__device__ __forceinline__ uint32_t med3u(uint32_t a, uint32_t b, uint32_t c) {
+  return max(min(a, b), min(max(a, b), c));
+}
+
 __device__ __forceinline__ float ord_value(uint32_t o) {
   return __uint_as_float((o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o);
 }
@@ -112,23 +117,34 @@ __device__ __forceinline__ int wave_incl_scan(int v) {
 
 __device__ __forceinline__ int wave_total(int incl) { return __builtin_amdgcn_readlane(incl, 63); }
 
+// Inclusive prefix sum within each row of 16 lanes (the first four steps of
+// wave_incl_scan).
+__device__ __forceinline__ int row16_incl_scan(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, true);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, true);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, true);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, true);
+  return v;
+}
+
+// T tokens in blocks of Tb: a non-finite logit of token t sets bad_flag[t / Tb].
 template <int EPL>
 __global__ __launch_bounds__(256) void k_route_topk(const float* __restrict__ logits, int T, int E,
                                                     int k, int32_t* __restrict__ topk_idx,
                                                     float* __restrict__ gates,
-                                                    int32_t* __restrict__ bad_flag) {
+                                                    int32_t* __restrict__ bad_flag, int Tb) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nwaves = gridDim.x * 4;
-  int bad = 0;
   for (int t = blockIdx.x * 4 + wave; t < T; t += nwaves) {
     float g;
+    int bad = 0;
     const int e = route_token<EPL>(logits + static_cast<size_t>(t) * E, E, k, &g, &bad);
     if (lane < k) {
       topk_idx[static_cast<size_t>(t) * k + lane] = e;
       gates[static_cast<size_t>(t) * k + lane] = g;
     }
+    if (bad && lane == 0) atomicOr(&bad_flag[t / Tb], 1);
   }
-  if (bad && lane == 0) atomicOr(bad_flag, 1);
 }
 
 // Large blocks: one token per lane. A wavefront takes 64 tokens; their
@@ -145,6 +161,7 @@ __global__ __launch_bounds__(256) void k_route_topk(const float* __restrict__ lo
 // by expert id.
 constexpr int kLaneChunk = 32;
 constexpr int kLaneRow = kLaneChunk + 1;   // padded LDS row (floats): conflict-free lane reads
+constexpr int kLaneRowsPerLoad = 64 / kLaneChunk;
 
 // The whole wavefront ranks one row with full keys (E <= 256): k rounds of a
 // wavefront maximum, the lowest id holding it taken by ballot, as in
@@ -181,20 +198,21 @@ template <int KP, int KM>
 __global__ __launch_bounds__(256) void k_route_lanes(const float* __restrict__ logits, int T, int E,
                                                      int k, int32_t* __restrict__ topk_idx,
                                                      float* __restrict__ gates,
-                                                     int32_t* __restrict__ bad_flag) {
+                                                     int32_t* __restrict__ bad_flag, int Tb) {
   static_assert(KP > KM, "the packed list holds the k-th and the (k+1)-th key");
   __shared__ float s_buf[4][64 * kLaneRow];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int t0 = (blockIdx.x * 4 + wave) * 64;
   float* buf = s_buf[wave];
-  // lane l loads column l % 32 of rows l / 32 + 2 i, i < 32, of a chunk
-  const int lc = lane & 31, lr = lane >> 5;
-  float v[32];
+  // lane l loads column l % C of rows l / C + (64 / C) i, i < C, of a chunk
+  // of C = kLaneChunk experts
+  const int lc = lane % kLaneChunk, lr = lane / kLaneChunk;
+  float v[kLaneChunk];
   auto load = [&](int e0) {
     const int e = e0 + lc;
 #pragma unroll
-    for (int i = 0; i < 32; ++i) {
-      const int t = t0 + lr + 2 * i;
+    for (int i = 0; i < kLaneChunk; ++i) {
+      const int t = t0 + lr + kLaneRowsPerLoad * i;
       v[i] = (t < T && e < E) ? logits[static_cast<size_t>(t) * E + e] : 0.f;
     }
   };
@@ -203,23 +221,26 @@ __global__ __launch_bounds__(256) void k_route_lanes(const float* __restrict__ l
   for (int j = 0; j < KP; ++j) key[j] = 0u;
   int nonfinite = 0;
   load(0);
+  // Each wavefront stages its own rows: ordering its LDS writes and reads
+  // needs no workgroup barrier, only that the compiler keep them in program
+  // order (a wavefront's LDS operations complete in issue order).
   for (int e0 = 0; e0 < E; e0 += kLaneChunk) {
-    __syncthreads();   // the previous chunk's reads are done
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the previous chunk's reads are done
 #pragma unroll
-    for (int i = 0; i < 32; ++i) buf[(lr + 2 * i) * kLaneRow + lc] = v[i];
+    for (int i = 0; i < kLaneChunk; ++i) buf[(lr + kLaneRowsPerLoad * i) * kLaneRow + lc] = v[i];
     if (e0 + kLaneChunk < E) load(e0 + kLaneChunk);
-    __syncthreads();
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     const int ne = min(kLaneChunk, E - e0);
     for (int j = 0; j < ne; ++j) {
       const float x = buf[lane * kLaneRow + j];
       nonfinite |= !__builtin_isfinite(x);
-      uint32_t c = (max(ord_key(x), 1u) & 0xFFFFFF00u) | static_cast<uint32_t>(255 - (e0 + j));
+      const uint32_t c = (max(ord_key(x), 1u) & 0xFFFFFF00u) | static_cast<uint32_t>(255 - (e0 + j));
+      // insertion into the descending list: new[q] = max(old[q], min(old[q-1], c)),
+      // the median of (old[q-1], old[q], c) since old[q-1] >= old[q]: one
+      // v_med3_u32 per position, every position from the old list
 #pragma unroll
-      for (int q = 0; q < KP; ++q) {
-        const uint32_t hi = max(key[q], c);
-        c = min(key[q], c);
-        key[q] = hi;
-      }
+      for (int q = KP - 1; q >= 1; --q) key[q] = med3u(key[q - 1], key[q], c);
+      key[0] = max(key[0], c);
     }
   }
   const int t = t0 + lane;
@@ -255,11 +276,12 @@ __global__ __launch_bounds__(256) void k_route_lanes(const float* __restrict__ l
         gates[static_cast<size_t>(t) * k + j] = static_cast<float>(ex[j] / sum);
       }
   }
-  if (__any(t < T && nonfinite) && lane == 0) atomicOr(bad_flag, 1);
+  if (t < T && nonfinite) atomicOr(&bad_flag[t / Tb], 1);   // token t's block
 }
 
 constexpr int kPermThreads = 1024;
 constexpr int kChunkWords = 16;               // bitmask words per expert per chunk
+static_assert(kChunkWords == 16, "the ranking's per-expert prefix is a 16-lane row scan");
 constexpr int kChunkTokens = kChunkWords * 32;
 
 constexpr int kFusedMaxRoutes = 1024;       // fused routing path: T * k routes kept in LDS
@@ -287,14 +309,17 @@ __device__ __forceinline__ void rank_chunk(const int32_t* idx, int t0, int t1, i
     atomicOr(&s_mask[e * kChunkWords + (lt >> 5)], 1u << (lt & 31));
   }
   __syncthreads();
-  for (int e = tid; e < E; e += nthr) {
-    int run = s_run[e];
-#pragma unroll
-    for (int w = 0; w < kChunkWords; ++w) {
-      s_pre[e * kChunkWords + w] = run;
-      run += __popc(s_mask[e * kChunkWords + w]);
+  // word w of expert e is lane w of a 16-lane row: the popcount prefix over
+  // the expert's words is a row scan (whole wavefronts take part)
+  for (int i = tid; i < ((E * kChunkWords + 63) & ~63); i += nthr) {
+    const int e = i / kChunkWords;
+    const int c = e < E ? __popc(s_mask[i]) : 0;
+    const int incl = row16_incl_scan(c);
+    if (e < E) {
+      const int run = s_run[e];
+      s_pre[i] = run + incl - c;
+      if (i % kChunkWords == kChunkWords - 1) s_run[e] = run + incl;
     }
-    s_run[e] = run;
   }
   __syncthreads();
   for (int r = t0 * k + tid; r < t1 * k; r += nthr) {
@@ -685,12 +710,11 @@ __global__ __launch_bounds__(kPermThreads) void k_permute(const int32_t* __restr
 // finish (a fenced counter; nobody waits) plans the layer as permute_body does
 // (totals, offsets, work lists, staging, records) and turns the counts into
 // each chunk's first position per expert.
-__global__ __launch_bounds__(kPermThreads) void k_perm_hist(const int32_t* __restrict__ topk_idx,
-                                                            int T, int k,
-                                                            int32_t* __restrict__ bad_flag,
-                                                            int32_t* __restrict__ chunk_base,
-                                                            int32_t* __restrict__ counter,
-                                                            PermuteOut o) {
+__device__ __forceinline__ void perm_hist_body(const int32_t* __restrict__ topk_idx, int T, int k,
+                                               int32_t* __restrict__ bad_flag,
+                                               int32_t* __restrict__ chunk_base,
+                                               int32_t* __restrict__ counter, const PermuteOut& o,
+                                               int ch, int n_chunks) {
   __shared__ int32_t s_h[kMaxExperts];
   __shared__ int32_t s_free[kMaxExperts];
   __shared__ int32_t s_ftop;
@@ -698,7 +722,6 @@ __global__ __launch_bounds__(kPermThreads) void k_perm_hist(const int32_t* __res
   __shared__ uint32_t s_res[kMaxExperts / 32], s_pm[kMaxExperts / 32];
   __shared__ int32_t s_slot[kMaxExperts];
   const int E = o.E, tid = threadIdx.x, nthr = blockDim.x;
-  const int ch = blockIdx.x, n_chunks = gridDim.x;
   for (int e = tid; e < kMaxExperts; e += nthr) s_h[e] = 0;
   // the cache state the last workgroup plans with, read while chunks count
   if ((tid >> 6) == 1) prefetch_state(o.cv, E, o.layer, s_free, &s_ftop, s_res, s_pm, s_slot);
@@ -728,22 +751,99 @@ __global__ __launch_bounds__(kPermThreads) void k_perm_hist(const int32_t* __res
   permute_body(topk_idx, T, k, bad, o, s_free, &s_ftop, s_res, s_pm, s_slot, chunk_base, n_chunks);
 }
 
+__global__ __launch_bounds__(kPermThreads) void k_perm_hist(const int32_t* __restrict__ topk_idx,
+                                                            int T, int k,
+                                                            int32_t* __restrict__ bad_flag,
+                                                            int32_t* __restrict__ chunk_base,
+                                                            int32_t* __restrict__ counter,
+                                                            PermuteOut o) {
+  perm_hist_body(topk_idx, T, k, bad_flag, chunk_base, counter, o, blockIdx.x, gridDim.x);
+}
+
 // Large blocks, second launch: workgroup c ranks the routes of its chunk from
 // the chunk's first positions per expert.
-__global__ __launch_bounds__(kPermThreads) void k_perm_rank(const int32_t* __restrict__ topk_idx,
-                                                            int T, int k, int E,
-                                                            const int32_t* __restrict__ chunk_base,
-                                                            int32_t* __restrict__ perm,
-                                                            int32_t* __restrict__ inv_perm) {
+__device__ __forceinline__ void perm_rank_body(const int32_t* __restrict__ topk_idx, int T, int k,
+                                               int E, const int32_t* __restrict__ chunk_base,
+                                               int32_t* __restrict__ perm,
+                                               int32_t* __restrict__ inv_perm, int ch) {
   __shared__ uint32_t s_mask[kMaxExperts * kChunkWords];
   __shared__ int32_t s_pre[kMaxExperts * kChunkWords];
   __shared__ int32_t s_run[kMaxExperts];
-  const int ch = blockIdx.x;
   for (int e = threadIdx.x; e < E; e += blockDim.x)
     s_run[e] = chunk_base[static_cast<size_t>(ch) * E + e];
   const int t0 = ch * kChunkTokens;
   rank_chunk(topk_idx, t0, min(T, t0 + kChunkTokens), k, E, T * k, s_mask, s_pre, s_run, perm,
              inv_perm);
+}
+
+__global__ __launch_bounds__(kPermThreads) void k_perm_rank(const int32_t* __restrict__ topk_idx,
+                                                            int T, int k, int E,
+                                                            const int32_t* __restrict__ chunk_base,
+                                                            int32_t* __restrict__ perm,
+                                                            int32_t* __restrict__ inv_perm) {
+  perm_rank_body(topk_idx, T, k, E, chunk_base, perm, inv_perm, blockIdx.x);
+}
+
+// Many independent blocks of T tokens (no cache), in three launches with no
+// workgroup waiting on another. First: workgroup (c, b) counts chunk c of
+// block b per expert into chunk_base[b][c][*].
+__global__ __launch_bounds__(256) void k_perm_count_batch(const int32_t* __restrict__ topk_idx,
+                                                         int T, int k, int E,
+                                                         int32_t* __restrict__ chunk_base) {
+  __shared__ int32_t s_h[kMaxExperts];
+  const int b = blockIdx.y, ch = blockIdx.x, tid = threadIdx.x;
+  const int32_t* idx = topk_idx + static_cast<size_t>(b) * T * k;
+  for (int e = tid; e < kMaxExperts; e += 256) s_h[e] = 0;
+  __syncthreads();
+  const int t0 = ch * kChunkTokens, t1 = min(T, t0 + kChunkTokens);
+  for (int r = t0 * k + tid; r < t1 * k; r += 4 * 256) {   // 4 loads in flight per thread
+    int e[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) e[u] = r + u * 256 < t1 * k ? idx[r + u * 256] : -1;
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (e[u] >= 0) atomicAdd(&s_h[e[u]], 1);
+  }
+  __syncthreads();
+  int32_t* out = chunk_base + (static_cast<size_t>(b) * gridDim.x + ch) * E;
+  for (int e = tid; e < E; e += 256) out[e] = s_h[e];
+}
+
+// Second: one workgroup per block turns its per-chunk counts into the
+// block's counts, offsets and per-chunk first positions (the planning step of
+// permute_body, without a cache). Per block b: routes at b*T*k, counts at
+// b*E, offsets at b*(E+1), non-finite flag at b.
+__global__ __launch_bounds__(kPermThreads) void k_perm_plan_batch(
+    const int32_t* __restrict__ topk_idx, int T, int k, int n_chunks,
+    const int32_t* __restrict__ bad_flag, int32_t* __restrict__ chunk_base, PermuteOut o) {
+  __shared__ int32_t s_free[kMaxExperts];
+  __shared__ int32_t s_ftop;
+  __shared__ uint32_t s_res[kMaxExperts / 32], s_pm[kMaxExperts / 32];
+  __shared__ int32_t s_slot[kMaxExperts];
+  const int b = blockIdx.x, E = o.E;
+  const size_t R = static_cast<size_t>(T) * k;
+  PermuteOut ob = o;
+  ob.counts += static_cast<size_t>(b) * E;
+  ob.offsets += static_cast<size_t>(b) * (E + 1);
+  ob.perm += b * R;
+  ob.inv_perm += b * R;
+  if (ob.bad_out) ob.bad_out += b;
+  if ((threadIdx.x >> 6) == 1) prefetch_state(ob.cv, E, 0, s_free, &s_ftop, s_res, s_pm, s_slot);
+  __syncthreads();
+  permute_body(topk_idx + b * R, T, k, bad_flag[b], ob, s_free, &s_ftop, s_res, s_pm, s_slot,
+               chunk_base + static_cast<size_t>(b) * n_chunks * E, n_chunks);
+}
+
+// Third: workgroup (c, b) ranks chunk c of block b from its first positions.
+__global__ __launch_bounds__(kPermThreads) void k_perm_rank_batch(
+    const int32_t* __restrict__ topk_idx, int T, int k, int E,
+    const int32_t* __restrict__ chunk_base, int32_t* __restrict__ perm,
+    int32_t* __restrict__ inv_perm) {
+  const int b = blockIdx.y;
+  const size_t R = static_cast<size_t>(T) * k;
+  perm_rank_body(topk_idx + b * R, T, k, E,
+                 chunk_base + static_cast<size_t>(b) * gridDim.x * E, perm + b * R,
+                 inv_perm + b * R, blockIdx.x);
 }
 
 // Small blocks (T*k <= 1024): routing on many CUs, one token per wavefront,
@@ -1159,33 +1259,34 @@ int permute_chunks(int T) { return (T + kChunkTokens - 1) / kChunkTokens; }
 
 hipError_t launch_route_topk(const float* logits, int T, int E, int k, int32_t* topk_idx,
                              float* gates, int32_t* bad_flag, hipEvent_t ev0, hipEvent_t ev1,
-                             hipStream_t s) {
+                             hipStream_t s, int block_tokens) {
+  const int Tb = block_tokens > 0 ? block_tokens : T;
   if (route_lanes(T)) {
     const int blocks = (T + 255) / 256;
     if (k <= 2)
       hipExtLaunchKernelGGL(k_route_lanes<3, 2>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits,
-                            T, E, k, topk_idx, gates, bad_flag);
+                            T, E, k, topk_idx, gates, bad_flag, Tb);
     else if (k <= 4)
       hipExtLaunchKernelGGL(k_route_lanes<5, 4>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits,
-                            T, E, k, topk_idx, gates, bad_flag);
+                            T, E, k, topk_idx, gates, bad_flag, Tb);
     else if (k <= 8)
       hipExtLaunchKernelGGL(k_route_lanes<9, 8>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits,
-                            T, E, k, topk_idx, gates, bad_flag);
+                            T, E, k, topk_idx, gates, bad_flag, Tb);
     else
       hipExtLaunchKernelGGL(k_route_lanes<17, 16>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0,
-                            logits, T, E, k, topk_idx, gates, bad_flag);
+                            logits, T, E, k, topk_idx, gates, bad_flag, Tb);
     return hipGetLastError();
   }
   const int blocks = (T + 3) / 4 < 4096 ? (T + 3) / 4 : 4096;
   if (E <= 64)
     hipExtLaunchKernelGGL(k_route_topk<1>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits, T,
-                          E, k, topk_idx, gates, bad_flag);
+                          E, k, topk_idx, gates, bad_flag, Tb);
   else if (E <= 128)
     hipExtLaunchKernelGGL(k_route_topk<2>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits, T,
-                          E, k, topk_idx, gates, bad_flag);
+                          E, k, topk_idx, gates, bad_flag, Tb);
   else
     hipExtLaunchKernelGGL(k_route_topk<4>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits, T,
-                          E, k, topk_idx, gates, bad_flag);
+                          E, k, topk_idx, gates, bad_flag, Tb);
   return hipGetLastError();
 }
 
@@ -1206,6 +1307,23 @@ hipError_t launch_permute_chunked(const int32_t* topk_idx, int T, int k, int32_t
   if (e != hipSuccess) return e;
   hipExtLaunchKernelGGL(k_perm_rank, dim3(n), dim3(kPermThreads), 0, s, nullptr, ev1, 0, topk_idx,
                         T, k, o.E, chunk_base, o.perm, o.inv_perm);
+  return hipGetLastError();
+}
+
+hipError_t launch_permute_batch(const int32_t* topk_idx, int B, int T, int k,
+                                const int32_t* bad_flag, int32_t* chunk_base, const PermuteOut& o,
+                                hipStream_t s) {
+  const int n = permute_chunks(T);
+  hipLaunchKernelGGL(k_perm_count_batch, dim3(n, B), dim3(256), 0, s, topk_idx, T, k, o.E,
+                     chunk_base);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_perm_plan_batch, dim3(B), dim3(kPermThreads), 0, s, topk_idx, T, k, n,
+                     bad_flag, chunk_base, o);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_perm_rank_batch, dim3(n, B), dim3(kPermThreads), 0, s, topk_idx, T, k, o.E,
+                     chunk_base, o.perm, o.inv_perm);
   return hipGetLastError();
 }
 
@@ -1337,6 +1455,81 @@ extern "C" oled_status oled_route_noalloc(const float* logits_dev, int32_t T, in
   }
   if (e != hipSuccess) {
     oled::set_noctx_error("oled_route_noalloc: launch failed");
+    return OLED_ERR_HIP;
+  }
+  return OLED_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Routing and permutation of many independent blocks in one pass (no cache):
+// one top-k launch over every token of the batch, then the counting and
+// ranking launches over (chunk, block).
+namespace {
+
+__global__ __launch_bounds__(256) void k_clear_ints(int32_t* p, int n) {
+  const int i = blockIdx.x * 256 + static_cast<int>(threadIdx.x);
+  if (i < n) p[i] = 0;
+}
+
+size_t batch_head_ints(int32_t B) { return ((2 * static_cast<size_t>(B) + 63) / 64) * 64; }
+
+}  // namespace
+
+extern "C" size_t oled_route_batch_workspace(int32_t B, int32_t T, int32_t E) {
+  if (B < 1 || T < 1 || E < 1) return 0;
+  return sizeof(int32_t) * (batch_head_ints(B) + static_cast<size_t>(B) *
+                                                      oled::permute_chunks(T) * E);
+}
+
+extern "C" oled_status oled_route_batch(const float* logits_dev, int32_t B, int32_t T, int32_t E,
+                                        int32_t k, int32_t* topk_idx_dev, float* gates_dev,
+                                        int32_t* counts_dev, int32_t* offsets_dev,
+                                        int32_t* perm_dev, int32_t* inv_perm_dev,
+                                        int32_t* nonfinite_dev, void* workspace_dev,
+                                        size_t workspace_bytes, void* stream) {
+  if (!logits_dev || !topk_idx_dev || !gates_dev || !counts_dev || !offsets_dev || !perm_dev ||
+      !inv_perm_dev || !workspace_dev) {
+    oled::set_noctx_error("oled_route_batch: NULL input, output or workspace");
+    return OLED_ERR_INVALID_ARG;
+  }
+  if (B < 1 || T < 1 || E < 1 || k < 1 || k > E) {
+    oled::set_noctx_error("oled_route_batch: B, T, E and k must be >= 1 and k <= E");
+    return OLED_ERR_INVALID_ARG;
+  }
+  if (T > kNoAllocMaxTokens || E > oled::kMaxExperts || k > oled::kMaxTopK ||
+      static_cast<int64_t>(B) * T * k > INT32_MAX) {
+    oled::set_noctx_error("oled_route_batch: T above 65535, E above 256, k above 16 or "
+                          "B*T*k above 2^31-1");
+    return OLED_ERR_UNSUPPORTED;
+  }
+  if (workspace_bytes < oled_route_batch_workspace(B, T, E)) {
+    oled::set_noctx_error("oled_route_batch: workspace smaller than "
+                          "oled_route_batch_workspace(B, T, E)");
+    return OLED_ERR_INVALID_ARG;
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int32_t* ws = static_cast<int32_t*>(workspace_dev);
+  int32_t* bad = ws;                                  // [B] non-finite flags of the top-k launch
+  int32_t* chunk_base = ws + batch_head_ints(B);      // [B][chunks][E]
+  const int n_head = B;
+  hipLaunchKernelGGL(k_clear_ints, dim3((n_head + 255) / 256), dim3(256), 0, s, ws, n_head);
+  hipError_t e = hipGetLastError();
+  if (e == hipSuccess)
+    e = oled::launch_route_topk(logits_dev, B * T, E, k, topk_idx_dev, gates_dev, bad, nullptr,
+                                nullptr, s, T);
+  if (e == hipSuccess) {
+    oled::PermuteOut o{};
+    o.counts = counts_dev;
+    o.offsets = offsets_dev;
+    o.perm = perm_dev;
+    o.inv_perm = inv_perm_dev;
+    o.gates = gates_dev;
+    o.E = E;
+    o.bad_out = nonfinite_dev;
+    e = oled::launch_permute_batch(topk_idx_dev, B, T, k, bad, chunk_base, o, s);
+  }
+  if (e != hipSuccess) {
+    oled::set_noctx_error("oled_route_batch: launch failed");
     return OLED_ERR_HIP;
   }
   return OLED_OK;

@@ -587,3 +587,89 @@ hipError_t launch_combine_score(bool bf16, const CombineArgs& c, const ScoreArgs
 }
 
 }  // namespace oled
+
+// ---------------------------------------------------------------------------
+// Priority numerators of many independent blocks in one pass (no retention):
+// workgroup (p, b) sums routes [p n, (p + 1) n) of block b (n = kScoreRoutes)
+// into LDS and adds its nonzero numerators to S[b][*] with integer atomics
+// (any order, same bits); S and the flags are cleared by a first launch.
+#include "oled.h"
+
+namespace oled {
+namespace {
+
+__global__ __launch_bounds__(kThreads) void k_priority_clear(unsigned long long* S, int n,
+                                                             int32_t* bad, int B) {
+  const int i = blockIdx.x * kThreads + static_cast<int>(threadIdx.x);
+  if (i < n) S[i] = 0ull;
+  if (bad && i < B) bad[i] = 0;
+}
+
+__global__ __launch_bounds__(kThreads) void k_priority_batch(const int32_t* __restrict__ topk_idx,
+                                                             const float* __restrict__ gates,
+                                                             const float* __restrict__ conf,
+                                                             int T, int k, int E,
+                                                             unsigned long long* __restrict__ S,
+                                                             int32_t* __restrict__ bad) {
+  __shared__ unsigned long long s_S[kMaxExperts];
+  __shared__ int32_t s_bad;
+  const int tid = threadIdx.x, b = blockIdx.y;
+  const size_t R = static_cast<size_t>(T) * k;
+  for (int e = tid; e < kMaxExperts; e += kThreads) s_S[e] = 0ull;
+  if (tid == 0) s_bad = 0;
+  __syncthreads();
+  ScoreArgs a{};
+  a.gates = gates + b * R;
+  a.conf = conf + static_cast<size_t>(b) * T;
+  a.topk_idx = topk_idx + b * R;
+  a.k = k;
+  const int r0 = blockIdx.x * kScoreRoutes;
+  score_sums(a, r0, min(static_cast<int>(R), r0 + kScoreRoutes), s_S, &s_bad);
+  __syncthreads();
+  for (int e = tid; e < E; e += kThreads)
+    if (s_S[e]) atomicAdd(&S[static_cast<size_t>(b) * E + e], s_S[e]);
+  if (tid == 0 && s_bad && bad) atomicOr(&bad[b], 1);
+}
+
+}  // namespace
+}  // namespace oled
+
+extern "C" oled_status oled_priority_batch(const int32_t* topk_idx_dev, const float* gates_dev,
+                                           const float* conf_dev, int32_t B, int32_t T, int32_t E,
+                                           int32_t k, uint64_t* score_q_dev,
+                                           int32_t* bad_conf_dev, void* stream) {
+  if (!topk_idx_dev || !gates_dev || !conf_dev || !score_q_dev) {
+    oled::set_noctx_error("oled_priority_batch: NULL input or output");
+    return OLED_ERR_INVALID_ARG;
+  }
+  if (B < 1 || T < 1 || E < 1 || k < 1 || k > E) {
+    oled::set_noctx_error("oled_priority_batch: B, T, E and k must be >= 1 and k <= E");
+    return OLED_ERR_INVALID_ARG;
+  }
+  if (T > 65535 || E > oled::kMaxExperts || k > oled::kMaxTopK ||
+      static_cast<int64_t>(B) * T * k > INT32_MAX || static_cast<int64_t>(B) * E > INT32_MAX) {
+    oled::set_noctx_error("oled_priority_batch: T above 65535, E above 256, k above 16 or "
+                          "B*T*k above 2^31-1");
+    return OLED_ERR_UNSUPPORTED;
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int n = B * E;
+  const int clear = (n > B ? n : B);
+  hipLaunchKernelGGL(oled::k_priority_clear, dim3((clear + oled::kThreads - 1) / oled::kThreads),
+                     dim3(oled::kThreads), 0, s,
+                     reinterpret_cast<unsigned long long*>(score_q_dev), n, bad_conf_dev, B);
+  hipError_t e = hipGetLastError();
+  if (e == hipSuccess) {
+    const int parts = static_cast<int>((static_cast<int64_t>(T) * k + oled::kScoreRoutes - 1) /
+                                       oled::kScoreRoutes);
+    hipLaunchKernelGGL(oled::k_priority_batch, dim3(parts, B), dim3(oled::kThreads), 0, s,
+                       topk_idx_dev, gates_dev, conf_dev, T, k, E,
+                       reinterpret_cast<unsigned long long*>(score_q_dev), bad_conf_dev);
+    e = hipGetLastError();
+  }
+  if (e != hipSuccess) {
+    oled::set_noctx_error("oled_priority_batch: launch failed");
+    return OLED_ERR_HIP;
+  }
+  return OLED_OK;
+}

@@ -54,7 +54,8 @@ EXPORTED = ["oled_create", "oled_destroy", "oled_last_error", "oled_reset_cache"
             "oled_read_layer_state", "oled_collect_stats", "oled_profile_collect",
             "oled_pack_expert", "oled_host_alloc", "oled_host_free", "oled_coop_dispatch",
             "oled_cpu_ffn", "oled_route_noalloc", "oled_route_noalloc_scratch_bytes",
-            "oled_set_fault_injection"]
+            "oled_set_fault_injection", "oled_route_batch", "oled_route_batch_workspace",
+            "oled_priority_batch"]
 
 
 class OledConfig(ctypes.Structure):
@@ -151,6 +152,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "oled_host_free": (None, [vp]),
         "oled_route_noalloc": (i32, [vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp]),
         "oled_set_fault_injection": (i32, [vp, i32, i32]),
+        "oled_route_batch": (i32, [vp, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp,
+                                   ctypes.c_size_t, vp]),
+        "oled_route_batch_workspace": (ctypes.c_size_t, [i32, i32, i32]),
+        "oled_priority_batch": (i32, [vp, vp, vp, i32, i32, i32, i32, vp, vp, vp]),
         "oled_route_noalloc_scratch_bytes": (ctypes.c_size_t, []),
     }
     for name, (res, args) in sig.items():
@@ -264,6 +269,29 @@ def oled_route_noalloc(logits, T: int, E: int, k: int, topk_idx, gates, counts, 
     return load().oled_route_noalloc(_ptr(logits), T, E, k, _ptr(topk_idx), _ptr(gates),
                                      _ptr(counts), _ptr(offsets), _ptr(perm), _ptr(inv_perm),
                                      _ptr(nonfinite), _stream(stream))
+
+
+def oled_route_batch(logits, B: int, T: int, E: int, k: int, topk_idx, gates, counts, offsets,
+                     perm, inv_perm, nonfinite, workspace, stream=None) -> int:
+    """Routing and permutation of B independent blocks (device tensors);
+    workspace: a device tensor of at least oled_route_batch_workspace(B, T, E)
+    bytes. Returns the status."""
+    nbytes = workspace.numel() * workspace.element_size()
+    return load().oled_route_batch(_ptr(logits), B, T, E, k, _ptr(topk_idx), _ptr(gates),
+                                   _ptr(counts), _ptr(offsets), _ptr(perm), _ptr(inv_perm),
+                                   _ptr(nonfinite), _ptr(workspace), nbytes, _stream(stream))
+
+
+def oled_route_batch_workspace(B: int, T: int, E: int) -> int:
+    return load().oled_route_batch_workspace(B, T, E)
+
+
+def oled_priority_batch(topk_idx, gates, conf, B: int, T: int, E: int, k: int, score_q,
+                        bad_conf=None, stream=None) -> int:
+    """Priority numerators of B independent blocks (device tensors); returns
+    the status."""
+    return load().oled_priority_batch(_ptr(topk_idx), _ptr(gates), _ptr(conf), B, T, E, k,
+                                      _ptr(score_q), _ptr(bad_conf), _stream(stream))
 
 
 def moe_forward_cached(ctx, layer: int, x, y, stream=None) -> int:

@@ -156,7 +156,7 @@ hipError_t launch_router_logits(bool, const void*, const void*, int, int, int, f
   return hipSuccess;
 }
 hipError_t launch_route_topk(const float*, int, int, int, int32_t*, float*, int32_t*, hipEvent_t,
-                             hipEvent_t, hipStream_t) {
+                             hipEvent_t, hipStream_t, int) {
   return hipSuccess;
 }
 hipError_t launch_permute(const int32_t*, int T, int k, int32_t*, const PermuteOut& o, hipEvent_t,

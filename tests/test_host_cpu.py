@@ -210,3 +210,28 @@ def test_route_noalloc_checks_arguments_before_the_gpu():
         assert "oled_route_noalloc" in oled.last_error(None)
     assert lib.oled_route_noalloc(d, 8, 8, 2, d, None, d, d, d, d, None, None) == \
         oled.OLED_ERR_INVALID_ARG
+
+
+def test_batch_calls_check_arguments_before_the_gpu():
+    """The batched routing and priority calls reject bad sizes, NULL buffers
+    and a short workspace on the host."""
+    lib = oled.load()
+    d = 0x1000    # never dereferenced: every call below fails its host checks
+    ws = lib.oled_route_batch_workspace(4, 3000, 128)
+    assert ws >= 4 * 4 * 6 * 128
+    assert lib.oled_route_batch_workspace(0, 10, 10) == 0
+    rb = lib.oled_route_batch
+    assert rb(d, 4, 3000, 128, 8, d, d, d, d, d, d, None, d, ws - 4, None) == \
+        oled.OLED_ERR_INVALID_ARG
+    assert rb(d, 4, 3000, 128, 8, d, d, d, d, d, d, None, None, ws, None) == \
+        oled.OLED_ERR_INVALID_ARG
+    assert rb(d, 0, 3000, 128, 8, d, d, d, d, d, d, None, d, ws, None) == oled.OLED_ERR_INVALID_ARG
+    assert rb(d, 4, 65536, 128, 8, d, d, d, d, d, d, None, d, 1 << 40, None) == \
+        oled.OLED_ERR_UNSUPPORTED
+    assert rb(d, 5000, 65535, 128, 8, d, d, d, d, d, d, None, d, 1 << 40, None) == \
+        oled.OLED_ERR_UNSUPPORTED
+    pb = lib.oled_priority_batch
+    assert pb(d, d, None, 4, 30, 16, 2, d, None, None) == oled.OLED_ERR_INVALID_ARG
+    assert pb(d, d, d, 4, 30, 16, 17, d, None, None) == oled.OLED_ERR_INVALID_ARG
+    assert pb(d, d, d, 4, 65536, 16, 2, d, None, None) == oled.OLED_ERR_UNSUPPORTED
+    assert "oled_priority_batch" in oled.last_error(None)
