@@ -554,8 +554,8 @@ def run_workload(w, args, lib, oled, coop=None, headline=True):
     st = {k: sum(r[2][k] for r in runs) for k in runs[0][2]}
     if args.launch_log and headline:
         os.makedirs(os.path.dirname(os.path.abspath(args.launch_log)), exist_ok=True)
-        with open(args.launch_log, "w") as f:
-            json.dump({"ffn_up": [[o[3], o[5]] for o in runs[-1][1] if o[0] == "ffn_up"]}, f)
+        with open(args.launch_log, "w") as f:   # every timed profiled operation, in order
+            json.dump({"ops": [[o[0], o[1], o[2], o[3], o[4], o[5]] for o in runs[-1][1]]}, f)
     li = max(1, st["layer_iters"])
     ms_step = elapsed / steps * 1e3
     h2d_step = st["h2d_bytes"] / (steps * len(runs))
@@ -646,8 +646,9 @@ def main():
                     help="transfer of the misses: workgroups of the hit GEMM launches (shader) "
                          "or hipMemcpyAsync on a copy stream (sdma)")
     ap.add_argument("--launch-log", default=None,
-                    help="write the timed gate/up launches in order ([bytes, h2d bytes] each) "
-                         "to this JSON file, for matching them with profiler records")
+                    help="write the timed profiled operations in order ([op, layer, ms, bytes, "
+                         "flops, h2d bytes] each) to this JSON file, for matching them with "
+                         "profiler records")
     ap.add_argument("--profile-ops", default="ffn_up",
                     help="operations timed with HIP events during the timed steps: any of "
                          "ffn_up,ffn_down,h2d,combine,route_topk,permute,score_retain,"

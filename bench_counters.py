@@ -1,25 +1,30 @@
-"""Summarises rocprofv3 runs of bench.py into the text summaries kept with the
-benchmark: per-kernel timings, and HBM traffic of the grouped gate/up GEMM.
+"""Summarises rocprofv3 runs of bench.py into the text summaries kept under
+profiles/: the kernel trace of the timed steps against bench.py's own HIP
+events, HBM traffic of the grouped GEMM launches from hardware counters
+against their algorithmic bytes, and matrix-core busy cycles.
 
-Input runs (CSV output, `-o run`), each with bench.py's --launch-log and
---phase-steps 0 (no per-phase pass after the timed steps, so that the last
-gate/up dispatches are the timed ones):
-  trace  rocprofv3 --kernel-trace --stats   -- python3 bench.py --phase-steps 0
-  fetch  rocprofv3 --pmc FETCH_SIZE         -- python3 bench.py --phase-steps 0 --calibration --no-cpu-baseline
-  write  rocprofv3 --pmc WRITE_SIZE         -- python3 bench.py --phase-steps 0 --calibration --no-cpu-baseline
+Input runs (CSV output, `-o run`), each of the same bench.py command with
+--phase-steps 0 --full-steps 0 --no-secondary --no-cpu-baseline --calibration
+--launch-log <dir>/launches.json --profile-ops ffn_up,ffn_down,ffn_dense_up,ffn_dense_down
+and the workload's own flags:
+  trace  rocprofv3 --kernel-trace --stats
+  fetch  rocprofv3 --pmc FETCH_SIZE
+  write  rocprofv3 --pmc WRITE_SIZE
+  mfma   rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CYCLES GRBM_GUI_ACTIVE
 
 `--calibration` runs torch's negation over 64 Mi fp32 (256 MiB read, 256 MiB
-written) between the warm-up and the timed steps. Its counter readings give
+written) between the warm-up and the timed steps: its counter readings give
 the scale from counter KiB to bytes, and its position in dispatch order marks
-where the timed steps begin: the gate/up GEMM dispatches after it are the
-ones bench.py times.
-
-The gate/up GEMM is the k_ffn instance with UP = true (hit and miss launches
-use the same instance). The launch log lists the timed gate/up launches in
-dispatch order with the bytes each moved host-to-device; like bench.py's
-roofline, the summaries take the launches that moved none (a launch that
-transfers miss weights runs as long as its PCIe reads). Traffic per launch is
-the mean over those dispatches of scaled FETCH_SIZE + WRITE_SIZE.
+where the timed steps begin. The launch log lists the timed operations in
+order with their algorithmic bytes, flops and host-to-device bytes; the
+dispatches of each GEMM kernel after the calibration kernel are matched to
+them in order:
+  k_ffn<..., true, ...>   gate/up GEMM of the cached experts (+ the misses'
+                          gate/up copy)                       <- ffn_up
+  k_ffn_mix<...>          cached experts' down GEMM + the misses' down copy
+                          + the misses' gate/up GEMM          <- ffn_down, 1st of each layer
+  k_ffn<..., false, ...>  the misses' down GEMM               <- ffn_down, 2nd of each layer
+  k_ffn_dense<true/false> dense tiles                        <- ffn_dense_up / _down
 """
 from __future__ import annotations
 
@@ -33,17 +38,27 @@ import re
 ROOT = os.path.dirname(os.path.abspath(__file__))
 FFN_SOURCE = os.path.join(ROOT, "paper_2609_33385_amd", "csrc", "ffn.hip")
 CAL_BYTES = 64 * 2 ** 20 * 4     # bytes read, and bytes written, by the calibration kernel
+N_SIMD = 1024                    # 256 CUs x 4 SIMDs
+N_XCD = 8                        # GRBM_GUI_ACTIVE sums the busy cycles of the 8 XCDs
+CLASSES = ("up", "mix", "down", "dense_up", "dense_down")
 
 
-def is_up(name: str) -> bool:
-    return "k_ffn<" in name and ", true," in name
+def kclass(name: str):
+    if "k_ffn_mix<" in name:
+        return "mix"
+    if "k_ffn_dense<true>" in name:
+        return "dense_up"
+    if "k_ffn_dense<false>" in name:
+        return "dense_down"
+    if "k_ffn<" in name:
+        return "up" if ", true," in name else "down"
+    return None
 
 
 def short(name: str) -> str:
     m = re.search(r"oled::\(anonymous namespace\)::(k_\w+)(<[^>]*>)?", name)
     if m:
-        s = m.group(1) + (m.group(2) or "")
-        return s.replace("oled::(anonymous namespace)::", "")
+        return m.group(1) + (m.group(2) or "")
     if name.startswith("__amd_rocclr"):
         return name
     m = re.search(r"at::native::(?:\(anonymous namespace\)::)?(\w+)", name)
@@ -51,8 +66,7 @@ def short(name: str) -> str:
 
 
 def read_csv(d: str, kind: str):
-    path = os.path.join(d, f"run_{kind}.csv")
-    with open(path) as f:
+    with open(os.path.join(d, f"run_{kind}.csv")) as f:
         return list(csv.DictReader(f))
 
 
@@ -62,177 +76,163 @@ def last_json_line(path: str) -> dict:
     return json.loads(lines[-1])
 
 
-def load_log(path: str):
-    with open(path) as f:
-        return json.load(f)["ffn_up"]
+def ops_by_class(log_path: str):
+    """The timed operations of the launch log per kernel class, in order."""
+    with open(log_path) as f:
+        ops = json.load(f)["ops"]
+    down = [o for o in ops if o[0] == "ffn_down"]
+    return {"up": [o for o in ops if o[0] == "ffn_up"], "mix": down[0::2], "down": down[1::2],
+            "dense_up": [o for o in ops if o[0] == "ffn_dense_up"],
+            "dense_down": [o for o in ops if o[0] == "ffn_dense_down"]}
 
 
-def select(dispatches, log):
-    """The dispatches of the timed launches that moved no miss weights."""
-    if len(dispatches) != len(log):
-        raise SystemExit(f"{len(dispatches)} gate/up dispatches, launch log has {len(log)}")
-    return [d for d, (_, h2d) in zip(dispatches, log) if h2d <= 0]
-
-
-def summarise_trace(d: str, bench: dict, plain: dict, log, cmd: str) -> str:
-    stats = read_csv(d, "kernel_stats")
-    trace = read_csv(d, "kernel_trace")
-    up = sorted((r for r in trace if is_up(r["Kernel_Name"])), key=lambda r: int(r["Dispatch_Id"]))
-    timed = select(up[-len(log):], log)
-    n_timed = bench["roofline"]["launches"]
-    if len(timed) != n_timed:
-        raise SystemExit(f"{len(timed)} launches without transfer, bench.py timed {n_timed}")
-    dur = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in timed]
-    timed_avg = sum(dur) / len(dur)
-    up_stats = [r for r in stats if is_up(r["Name"])][0]
-    lines = [
-        "# Kernel timings: bench.py default run (block-MoE layer stack, 40% residency)",
-        "",
-        "Workload: bf16, hidden 2048, 64 experts, top-8, intermediate 1024, 16 layers, "
-        "32 tokens per iteration, cache 26/64 per layer; 8 warm-up + 64 timed steps.",
-        "",
-        "Command (from the repository root, `TMPDIR=/tmp`):",
-        "",
-        f"    {cmd}",
-        "",
-        f"bench.py line of this run: value {bench['value']} {bench['unit']}, "
-        f"{bench['ms_per_step']} ms/step; gate/up GEMM avg_launch_us "
-        f"{bench['roofline']['avg_launch_us']} over {n_timed} launches (HIP events).",
-        "",
-        f"`python3 bench.py` without the profiler, same machine and tree, just before: value "
-        f"{plain['value']} {plain['unit']}, {plain['ms_per_step']} ms/step, gate/up GEMM "
-        f"avg_launch_us {plain['roofline']['avg_launch_us']} over "
-        f"{plain['roofline']['launches']} launches, roofline frac {plain['roofline']['frac']}.",
-        "",
-        "Under the kernel tracer the HIP events attached to each GEMM dispatch also span the "
-        "tracer's own per-dispatch work, so the event figure of the profiled run is above the "
-        "trace; the unprofiled run's events are the figure bench.py reports.",
-        "",
-        "## Gate/up GEMM (k_ffn UP=true), trace vs. bench.py events",
-        "",
-        "| source | launches | avg us |",
-        "|---|---|---|",
-        f"| rocprofv3 stats, all dispatches | {up_stats['Calls']} | "
-        f"{float(up_stats['AverageNs']) / 1e3:.2f} |",
-        f"| rocprofv3 trace, timed dispatches that moved no miss weights | {len(timed)} | "
-        f"{timed_avg:.2f} |",
-        f"| bench.py HIP events, timed steps, profiled run | {n_timed} | "
-        f"{bench['roofline']['avg_launch_us']} |",
-        f"| bench.py HIP events, timed steps, unprofiled run | {plain['roofline']['launches']} | "
-        f"{plain['roofline']['avg_launch_us']} |",
-        "",
-        "## All kernels (rocprofv3 --stats)",
-        "",
-        "| kernel | calls | avg us | total ms | % |",
-        "|---|---|---|---|---|",
-    ]
-    for r in stats:
-        lines.append(f"| `{short(r['Name'])}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
-                     f"{float(r['TotalDurationNs']) / 1e6:.2f} | {float(r['Percentage']):.2f} |")
-    return "\n".join(lines) + "\n"
-
-
-def counter_rows(d: str, counter: str):
-    rows = [r for r in read_csv(d, "counter_collection") if r["Counter_Name"] == counter]
-    rows.sort(key=lambda r: int(r["Dispatch_Id"]))
-    return rows
-
-
-def split_timed(rows, bench: dict, log):
+def timed_dispatches(rows, key="Dispatch_Id"):
+    """Rows after the last calibration dispatch, per kernel class, in order."""
+    rows = sorted(rows, key=lambda r: int(r[key]))
     cal = [i for i, r in enumerate(rows) if "neg_kernel" in r["Kernel_Name"]]
     if not cal:
-        raise SystemExit("no calibration dispatch (torch neg) in the counter run")
-    cal_val = float(rows[cal[-1]]["Counter_Value"])
-    up = [float(r["Counter_Value"]) for r in rows[cal[-1] + 1:] if is_up(r["Kernel_Name"])]
-    up = select(up, log)
-    if len(up) != bench["roofline"]["launches"]:
-        raise SystemExit(f"{len(up)} gate/up dispatches without transfer after calibration, "
-                         f"bench.py timed {bench['roofline']['launches']}")
-    return cal_val, up
+        raise SystemExit("no calibration dispatch (torch neg) in the run")
+    out = {c: [] for c in CLASSES}
+    for r in rows[cal[-1] + 1:]:
+        c = kclass(r["Kernel_Name"])
+        if c:
+            out[c].append(r)
+    return rows[cal[-1]], out
+
+
+def counter_run(d: str, counter: str, ops):
+    rows = [r for r in read_csv(d, "counter_collection") if r["Counter_Name"] == counter]
+    cal, per = timed_dispatches(rows)
+    for c in CLASSES:
+        if len(per[c]) != len(ops[c]):
+            raise SystemExit(f"{counter}: {len(per[c])} {c} dispatches after calibration, "
+                             f"launch log has {len(ops[c])}")
+    return float(cal["Counter_Value"]), {c: [float(r["Counter_Value"]) for r in per[c]]
+                                         for c in CLASSES}
+
+
+def mean(v):
+    return sum(v) / len(v) if v else 0.0
 
 
 def main():
     ap = argparse.ArgumentParser()
-    ap.add_argument("--trace", required=True, help="rocprofv3 output dir of the kernel-trace run")
-    ap.add_argument("--trace-bench", required=True, help="bench.py output of the kernel-trace run")
-    ap.add_argument("--trace-log", required=True, help="its --launch-log file")
-    ap.add_argument("--fetch-log", required=True)
-    ap.add_argument("--write-log", required=True)
+    ap.add_argument("--name", required=True, help="workload tag of the summaries (e128_zipf40)")
+    ap.add_argument("--workload-text", required=True)
+    ap.add_argument("--command", required=True, help="the bench.py command line of the runs")
     ap.add_argument("--plain-bench", required=True, help="bench.py output without the profiler")
-    ap.add_argument("--fetch", required=True, help="rocprofv3 output dir of the FETCH_SIZE run")
-    ap.add_argument("--fetch-bench", required=True)
-    ap.add_argument("--write", required=True, help="rocprofv3 output dir of the WRITE_SIZE run")
-    ap.add_argument("--write-bench", required=True)
+    for run in ("trace", "fetch", "write", "mfma"):
+        ap.add_argument(f"--{run}", required=True, help=f"rocprofv3 output dir of the {run} run")
+        ap.add_argument(f"--{run}-bench", required=True)
+        ap.add_argument(f"--{run}-log", required=True)
     ap.add_argument("--out", default=os.path.join(ROOT, "profiles"))
     args = ap.parse_args()
+    plain = last_json_line(args.plain_bench)
 
-    trace_cmd = ("rocprofv3 --kernel-trace --stats --output-format csv -d <dir> -o run "
-                 "-- python3 bench.py --phase-steps 0 --launch-log <dir>/launches.json")
+    # ---- kernel trace against the events
     tb = last_json_line(args.trace_bench)
-    with open(os.path.join(args.out, "k_ffn_up_llada40_kernel_stats.md"), "w") as f:
-        f.write(summarise_trace(args.trace, tb, last_json_line(args.plain_bench),
-                                load_log(args.trace_log), trace_cmd))
+    ops_t = ops_by_class(args.trace_log)
+    trace = read_csv(args.trace, "kernel_trace")
+    _, per_t = timed_dispatches(trace)
+    if len(per_t["up"]) != len(ops_t["up"]):
+        raise SystemExit(f"trace: {len(per_t['up'])} gate/up dispatches, log {len(ops_t['up'])}")
+    dur = {c: [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in per_t[c]]
+           for c in CLASSES}
+    ev = {c: [o[2] * 1e3 for o in ops_t[c]] for c in CLASSES}
+    stats = read_csv(args.trace, "kernel_stats")
+    cmd_trace = f"rocprofv3 --kernel-trace --stats --output-format csv -d <dir> -o run -- {args.command}"
+    md = [f"# Kernel trace: bench.py on the {args.workload_text}", "",
+          "Command (repository root, `TMPDIR=/tmp`):", "", f"    {cmd_trace}", "",
+          f"bench.py line of this run: value {tb['value']} {tb['unit']}, {tb['ms_per_step']} "
+          f"ms per step. Without the profiler, same machine and tree: value {plain['value']} "
+          f"{plain['unit']}, {plain['ms_per_step']} ms per step; gate/up GEMM "
+          f"avg_launch_us {plain['roofline']['avg_launch_us']} over "
+          f"{plain['roofline']['launches']} launches (HIP events on the dispatches).", "",
+          "## Timed GEMM launches: trace against the HIP events of the same run", "",
+          "| kernel | launches | trace avg us | events avg us |", "|---|---|---|---|"]
+    for c in CLASSES:
+        if dur[c]:
+            md.append(f"| {c} | {len(dur[c])} | {mean(dur[c]):.2f} | {mean(ev[c]):.2f} |")
+    md += ["", "## All kernels of the run (rocprofv3 --stats)", "",
+           "| kernel | calls | avg us | total ms | % |", "|---|---|---|---|---|"]
+    for r in stats:
+        md.append(f"| `{short(r['Name'])}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                  f"{float(r['TotalDurationNs']) / 1e6:.2f} | {float(r['Percentage']):.2f} |")
+    with open(os.path.join(args.out, f"k_ffn_up_{args.name}_kernel_stats.md"), "w") as f:
+        f.write("\n".join(md) + "\n")
 
-    fb, wb = last_json_line(args.fetch_bench), last_json_line(args.write_bench)
-    cal_f, up_f = split_timed(counter_rows(args.fetch, "FETCH_SIZE"), fb, load_log(args.fetch_log))
-    cal_w, up_w = split_timed(counter_rows(args.write, "WRITE_SIZE"), wb, load_log(args.write_log))
-    sf, sw = CAL_BYTES / cal_f, CAL_BYTES / cal_w       # bytes per counter KiB
-    fetch_b = sum(up_f) / len(up_f) * sf
-    write_b = sum(up_w) / len(up_w) * sw
-    alg = fb["roofline"]["bytes_per_launch"]
+    # ---- HBM traffic per launch class
+    ops_f, ops_w = ops_by_class(args.fetch_log), ops_by_class(args.write_log)
+    cal_f, fetch = counter_run(args.fetch, "FETCH_SIZE", ops_f)
+    cal_w, write = counter_run(args.write, "WRITE_SIZE", ops_w)
+    sf, sw = CAL_BYTES / cal_f, CAL_BYTES / cal_w     # bytes per counter KiB
+    ops_m = ops_by_class(args.mfma_log)
+    mfma, gui = {}, {}
+    for cnt, dst in (("SQ_VALU_MFMA_BUSY_CYCLES", mfma), ("GRBM_GUI_ACTIVE", gui)):
+        rows = [r for r in read_csv(args.mfma, "counter_collection") if r["Counter_Name"] == cnt]
+        _, per = timed_dispatches(rows)
+        for c in CLASSES:
+            dst[c] = [float(r["Counter_Value"]) for r in per[c]]
     with open(FFN_SOURCE, "rb") as f:
         sha = hashlib.sha256(f.read()).hexdigest()
-    pmc_cmd = ("timeout -s KILL 150 rocprofv3 --pmc {c} --output-format csv -d <dir> -o run "
-               "-- python3 bench.py --phase-steps 0 --calibration --no-cpu-baseline "
-               "--launch-log <dir>/launches.json")
-    rec = {
-        "kernel": "k_ffn UP=true (grouped gate/up SwiGLU GEMM)",
-        "workload": "bf16 H2048 E64 k8 I1024, 16 layers, 32 tokens/iteration, cache 26/64",
-        "ffn_source_sha256": sha,
-        "traffic_bytes_per_launch": int(round(fetch_b + write_b)),
-        "fetch_bytes_per_launch": int(round(fetch_b)),
-        "write_bytes_per_launch": int(round(write_b)),
-        "algorithmic_bytes_per_launch": alg,
-        "launches": len(up_f),
-        "fetch_scale_bytes_per_kib": sf,
-        "write_scale_bytes_per_kib": sw,
-        "calibration": "torch neg over 64 Mi fp32: 256 MiB read + 256 MiB written",
-        "calibration_fetch_kib": cal_f,
-        "calibration_write_kib": cal_w,
-        "commands": [pmc_cmd.format(c="FETCH_SIZE"), pmc_cmd.format(c="WRITE_SIZE")],
-    }
-    with open(os.path.join(args.out, "k_ffn_up_llada40_traffic.json"), "w") as f:
+    rows_md, per_class = [], {}
+    for c in CLASSES:
+        if not ops_f[c]:
+            continue
+        alg = mean([o[3] for o in ops_f[c]])
+        h2d = mean([max(0, o[5]) for o in ops_f[c]])
+        fb, wb = mean(fetch[c]) * sf, mean(write[c]) * sw
+        flops = mean([o[4] for o in ops_t[c]])
+        busy = mean(mfma[c]) / (N_SIMD * mean(gui[c]) / N_XCD) if mean(gui[c]) else None
+        t_us = mean([o[2] for o in ops_t[c]]) * 1e3
+        flop_util = flops / (t_us * 1e-6) / 2.5e15 if t_us > 0 else None
+        per_class[c] = dict(launches=len(ops_f[c]), algorithmic_bytes=int(alg), h2d_bytes=int(h2d),
+                            fetch_bytes=int(fb), write_bytes=int(wb), mfma_busy=busy,
+                            flop_util=flop_util)
+        rows_md.append(f"| {c} | {len(ops_f[c])} | {alg / 1e6:.1f} | {h2d / 1e6:.1f} | "
+                       f"{fb / 1e6:.1f} | {wb / 1e6:.1f} | {(fb + wb) / max(1.0, alg + 2 * h2d):.3f} | "
+                       f"{busy:.4f} | {flop_util:.4f} |")
+    up = per_class["up"]
+    rec = {"kernel": "k_ffn UP=true (grouped gate/up SwiGLU GEMM, with the misses' gate/up copy)",
+           "workload": args.workload_text, "ffn_source_sha256": sha,
+           "traffic_bytes_per_launch": up["fetch_bytes"] + up["write_bytes"],
+           "fetch_bytes_per_launch": up["fetch_bytes"], "write_bytes_per_launch": up["write_bytes"],
+           "algorithmic_bytes_per_launch": up["algorithmic_bytes"],
+           "h2d_bytes_per_launch": up["h2d_bytes"], "launches": up["launches"],
+           "fetch_scale_bytes_per_kib": sf, "write_scale_bytes_per_kib": sw,
+           "calibration": "torch neg over 64 Mi fp32: 256 MiB read + 256 MiB written",
+           "per_class": per_class,
+           "commands": [f"timeout -s KILL 300 rocprofv3 --pmc {c} --output-format csv -d <dir> -o run "
+                        f"-- {args.command}" for c in ("FETCH_SIZE", "WRITE_SIZE",
+                                                      "SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CYCLES "
+                                                      "GRBM_GUI_ACTIVE")]}
+    with open(os.path.join(args.out, f"k_ffn_up_{args.name}_traffic.json"), "w") as f:
         json.dump(rec, f, indent=1)
         f.write("\n")
-    md = [
-        "# HBM traffic: gate/up GEMM (k_ffn UP=true), block-MoE layer stack at 40% residency",
-        "",
-        "Commands (from the repository root, `TMPDIR=/tmp`), one counter per run:",
-        "",
-        *[f"    {c}" for c in rec["commands"]],
-        "",
-        "Scale: the calibration kernel (torch neg over 64 Mi fp32, 256 MiB read and 256 MiB "
-        f"written) read FETCH_SIZE {cal_f:.0f} KiB and WRITE_SIZE {cal_w:.0f} KiB, so one "
-        f"counter KiB is {sf:.1f} B fetched and {sw:.1f} B written.",
-        "",
-        f"Over the {len(up_f)} timed gate/up launches that moved no miss weights (hit and miss "
-        "launches, dispatches after the calibration kernel):",
-        "",
-        "| per launch | bytes |",
-        "|---|---|",
-        f"| fetched (scaled FETCH_SIZE) | {fetch_b:.0f} |",
-        f"| written (scaled WRITE_SIZE) | {write_b:.0f} |",
-        f"| traffic | {fetch_b + write_b:.0f} |",
-        f"| algorithmic (weights + activations + outputs) | {alg} |",
-        f"| traffic / algorithmic | {(fetch_b + write_b) / alg:.3f} |",
-        "",
-        f"Kernel source sha256 `{sha}`; bench.py reports this traffic only while "
-        "ffn.hip is unchanged.",
-    ]
-    with open(os.path.join(args.out, "k_ffn_up_llada40_traffic.md"), "w") as f:
+    md = [f"# Grouped GEMM launches: counters on the {args.workload_text}", "",
+          "Commands (repository root, `TMPDIR=/tmp`), one counter set per run:", "",
+          *[f"    {c}" for c in rec["commands"]], "",
+          f"Scale: the calibration kernel (torch neg over 64 Mi fp32) read FETCH_SIZE {cal_f:.0f} "
+          f"KiB and WRITE_SIZE {cal_w:.0f} KiB for 256 MiB each way, so one counter KiB is "
+          f"{sf:.1f} B fetched and {sw:.1f} B written.", "",
+          "Per launch, averaged over the timed launches of each class (MB = 1e6 bytes). "
+          "Algorithmic bytes are the GEMM's own operands (weights, token rows, outputs); "
+          "launches that carry the misses' copy also read those bytes from pinned host memory "
+          "and write them into their slots, so the ratio's denominator adds twice the copied "
+          "bytes. MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES (summed over the 1024 SIMDs) / (1024 x "
+          "GRBM_GUI_ACTIVE / 8): the share of the launch's active cycles the matrix cores were "
+          "busy (GRBM_GUI_ACTIVE sums the 8 XCDs: divided by 8 it matches the launch's duration "
+          "at 2.4 GHz); it counts the MFMAs of padded tile rows too. Flop util = algorithmic "
+          "flops / event time of the trace run / 2.5 PFLOP/s.", "",
+          "| launch class | launches | algorithmic MB | copied host->device MB | fetched MB | "
+          "written MB | traffic / (algorithmic + 2 x copied) | MFMA busy | flop util |",
+          "|---|---|---|---|---|---|---|---|---|", *rows_md, "",
+          f"Kernel source sha256 `{sha}`; bench.py reports the gate/up traffic only while "
+          "ffn.hip is unchanged."]
+    with open(os.path.join(args.out, f"ffn_kernels_{args.name}_counters.md"), "w") as f:
         f.write("\n".join(md) + "\n")
-    print(json.dumps({k: rec[k] for k in ("traffic_bytes_per_launch", "algorithmic_bytes_per_launch",
-                                          "launches")}))
+    print(json.dumps({"traffic_bytes_per_launch": rec["traffic_bytes_per_launch"],
+                      "per_class": per_class}))
 
 
 if __name__ == "__main__":
