@@ -409,16 +409,29 @@ __global__ __launch_bounds__(kThreads) void k_ffn_mix(FfnLaunch d, FfnLaunch u, 
 // v_mfma_f32_32x32x16_bf16 (the 16x16x32 form runs at less than half its
 // rate on this part), accumulators in registers.
 //  * Weights are private to a wavefront: it loads them from the packed
-//    fragments straight into registers, two stages of 64 of K ahead.
+//    fragments straight into registers, about two stages of 64 of K ahead.
 //  * Token rows are shared by the four wavefronts: they are copied from
 //    memory into a 4-stage LDS ring (32 KiB per stage of 64 of K, three
 //    stages in flight) by LDS DMA (buffer loads with an LDS destination,
 //    lane l's 16 bytes at lane slot l), 8 rows of 128 bytes per instruction:
 //    whole 128-byte lines per 8 lanes run at the full L2-to-LDS rate, where
 //    16-byte pieces of 16 rows per instruction run at a third of it.
-// Every output sums its K range in ascending order in one accumulator. Tiles
-// are ordered feature tile major, so the row tiles of one expert that share
-// weights run next to each other on one XCD (its L2).
+//  * With one wavefront per SIMD, the matrix core idles whenever the
+//    wavefront stops issuing MFMAs (a run of other instructions, a wait), so
+//    the loop is software-pipelined by hand: each quarter of a stage (16 of
+//    K) is 8 groups of two MFMAs (token tile n against the two weight tiles)
+//    plus the LDS read of token tile n for the next quarter, with the weight
+//    loads and the ring's DMA spread over the groups; scheduling barriers
+//    keep the groups in order. Each MFMA pair waits only for its own token
+//    fragment.
+//  * Down multiplies token rows (A) by weight rows (B), so that lane l holds
+//    output feature l % 32: every store writes 128 contiguous bytes of an
+//    output row. (Gate/up keeps weights as A: a lane then holds four
+//    consecutive features of a row for its gate and up products.)
+// Every output sums its K range in ascending order in one accumulator (the
+// same products and order either way round). Tiles are ordered feature tile
+// major, so the row tiles of one expert that share weights run next to each
+// other on one XCD (its L2).
 constexpr int kDenseRing = 4;     // token stages in LDS
 constexpr int kDenseGroup = 4;    // items per tile group
 
@@ -462,22 +475,6 @@ __device__ __forceinline__ u32x4_t lds_read16(uint32_t addr) {
   return v;
 }
 
-// Wait until at most N LDS operations are outstanding; the operands are tied
-// through the wait so that nothing reads them before it.
-template <int N, int NT>
-__device__ __forceinline__ void wait_lgkm(u32x4_t (&b)[NT]) {
-  static_assert(NT == 1 || NT == 2 || NT == 4 || NT == 8, "token tiles");
-  if constexpr (NT == 1) asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(b[0]) : "n"(N));
-  if constexpr (NT == 2) asm volatile("s_waitcnt lgkmcnt(%2)" : "+v"(b[0]), "+v"(b[1]) : "n"(N));
-  if constexpr (NT == 4)
-    asm volatile("s_waitcnt lgkmcnt(%4)" : "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]) : "n"(N));
-  if constexpr (NT == 8)
-    asm volatile("s_waitcnt lgkmcnt(%8)"
-                 : "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]), "+v"(b[4]), "+v"(b[5]),
-                   "+v"(b[6]), "+v"(b[7])
-                 : "n"(N));
-}
-
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p));
 }
@@ -487,15 +484,59 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 // makes the operand reads of 8 or 16 consecutive rows hit distinct banks.
 __device__ __forceinline__ int tok_swz(int r) { return (r ^ (r >> 3)) & 7; }
 
+// Wait until at most N LDS operations are outstanding; the operand is tied
+// through the wait so that nothing reads it before.
+template <int N>
+__device__ __forceinline__ void wait_lgkm1(u32x4_t& b) {
+  asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(b) : "n"(N));
+}
+
+// Wait for token fragment n of the last quarter of a tile, when no reads of
+// a next quarter follow it (NT - 1 - n reads issued after it).
+template <int NT>
+__device__ __forceinline__ void wait_last(u32x4_t& b, int n) {
+  if constexpr (NT == 8) {
+    switch (n) {
+      case 0: wait_lgkm1<7>(b); break;
+      case 1: wait_lgkm1<6>(b); break;
+      case 2: wait_lgkm1<5>(b); break;
+      case 3: wait_lgkm1<4>(b); break;
+      case 4: wait_lgkm1<3>(b); break;
+      case 5: wait_lgkm1<2>(b); break;
+      case 6: wait_lgkm1<1>(b); break;
+      default: wait_lgkm1<0>(b); break;
+    }
+  } else {
+    wait_lgkm1<0>(b);
+  }
+}
+
+template <int V>
+using ic_t = std::integral_constant<int, V>;
+
 // One tile: NT token tiles of 32 rows (item rows <= 32 NT).
+//
+// Issue order. Stage s of 64 of K has quarters q0..q3; group n of quarter q
+// issues { MFMA pair of token tile n, LDS read n of the next quarter }, and
+// group 0 also two weight loads: in q0 W(s+1) quarter 3, in q1..q3 W(s+2)
+// quarter q-1 (each into registers freed by the quarter before). Barrier
+// B(s+1) sits between q2 and q3 (stage s+1 landed for every wavefront, stage
+// s-1's slot free); q3 also issues DMA instruction n of DMA(s+3) into that
+// slot, after its weight loads. The prologue issues the same sequence for
+// stages -3..-1: DMA(0); W(0) q0..q2, DMA(1); W(0) q3, W(1) q0..q2, DMA(2).
+// Vector-memory operations complete in issue order, so the wait before
+// B(s+1) may leave outstanding what was issued after DMA(s+1): all of stage
+// s-1 and q0..q2 of stage s, 14 + NT in steady state (10 two stages from the
+// end, where no DMA and only the last weight quarter remain).
 template <bool UP, int NT>
 __device__ __forceinline__ void dense_tile(const FfnLaunch& a, const WorkItem& it, int f0,
                                            const uint16_t* W, u32x4_t (*ring)[32][64]) {
   constexpr int FRAG = 512;               // packed fragment: 16 rows x 32 of K
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: scalar LDS bases
   const int H = a.H, I = a.I;
   const int K = UP ? H : I;
-  const int NS = K / 64;                  // stages
+  const int NS = K / 64;                  // stages (a multiple of 4)
   const int S32 = K / 32;                 // packed fragments per 16 weight rows
   const uint16_t* src = static_cast<const uint16_t*>(a.src);
 
@@ -514,19 +555,21 @@ __device__ __forceinline__ void dense_tile(const FfnLaunch& a, const WorkItem& i
   }
   const __amdgpu_buffer_rsrc_t trs = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(src), 0, static_cast<int>(a.src_bytes), kBufferFlags);
-  auto issue_tok = [&](int s) {
+  auto dma1 = [&](int s, int i) {
     u32x4_t (*stage)[64] = ring[s % kDenseRing];
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        trs, (__attribute__((address_space(3))) void*)(stage[wave * NT + i]), 16, toff[i],
+        128 * s, 0, 0);
+  };
+  auto dma_all = [&](int s) {
 #pragma unroll
-    for (int i = 0; i < NT; ++i)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          trs, (__attribute__((address_space(3))) void*)(stage[wave * NT + i]), 16,
-          toff[i], 128 * s, 0, 0);
+    for (int i = 0; i < NT; ++i) dma1(s, i);
   };
 
-  // weights: two 32-row A tiles per wavefront (gate and up of 32 features,
-  // or 64 down features). Lane l holds row l%32 (16-row fragment (l/16)%2)
-  // and the 8 of K at fragment lane l%16 + 16 (2 q + l/32) for the half q of
-  // a 32 step.
+  // weights: two 32-row tiles per wavefront (gate and up of 32 features, or
+  // 64 down features). Lane l holds row l%32 (16-row fragment (l/16)%2) and
+  // the 8 of K at fragment lane l%16 + 16 (2 q + l/32) for the half q of a
+  // 32 step.
   const uint16_t* wp[2];
   size_t wstep;
   {
@@ -544,12 +587,10 @@ __device__ __forceinline__ void dense_tile(const FfnLaunch& a, const WorkItem& i
     }
     wstep = (UP ? 2 : 1) * FRAG;
   }
-  auto load_w = [&](int s, u32x4_t (&w)[2][4]) {
+  // weight quarter h (16 of K) of stage s: one 16-byte load per weight tile
+  auto load_wq = [&](int s, int h, u32x4_t (&w)[2][4]) {
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int h = 0; h < 4; ++h)
-        w[t][h] = ldg16(wp[t] + (2 * s + (h >> 1)) * wstep + 256 * (h & 1));
+    for (int t = 0; t < 2; ++t) w[t][h] = ldg16(wp[t] + (2 * s + (h >> 1)) * wstep + 256 * (h & 1));
   };
 
   floatx16_t acc[2][NT];
@@ -560,7 +601,7 @@ __device__ __forceinline__ void dense_tile(const FfnLaunch& a, const WorkItem& i
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[t][n][r] = 0.f;
 
-  // B operand position of token tile n for this lane (chunk c added later)
+  // operand position of token tile n for this lane (chunk c added later)
   uint32_t brow_off[NT];
   int bsw[NT];
 #pragma unroll
@@ -570,87 +611,108 @@ __device__ __forceinline__ void dense_tile(const FfnLaunch& a, const WorkItem& i
     bsw[n] = tok_swz(r);
   }
   const uint32_t ring_base = lds_addr(&ring[0][0][0]);
-
-  // Issue order: DMA(0) W(0) DMA(1) W(1) DMA(2), then barrier B(0). Stage s
-  // multiplies halves 0..2, passes barrier B(s+1) (stage s+1 landed for
-  // every wavefront, stage s-1 free), issues DMA(s+3) and the reads of stage
-  // s+1's first half, multiplies half 3, then loads W(s+2). Operations issued
-  // after DMA(s+1) when B(s+1) waits for it: at least 8 + NT.
-  u32x4_t wr[2][2][4];
-  issue_tok(0);
-  asm volatile("" ::: "memory");
-  load_w(0, wr[0]);
-  asm volatile("" ::: "memory");
-  issue_tok(1);
-  asm volatile("" ::: "memory");
-  load_w(1, wr[1]);
-  asm volatile("" ::: "memory");
-  issue_tok(2);
-
-  auto read_half = [&](int s, int h, u32x4_t (&b)[NT]) {
+  auto read1 = [&](int s, int h, int n) {
     const uint32_t sbase = ring_base + static_cast<uint32_t>(s % kDenseRing) * (32 * 64 * 16);
     const int c = 2 * h + (lane >> 5);
-#pragma unroll
-    for (int n = 0; n < NT; ++n) b[n] = lds_read16(sbase + brow_off[n] + 16 * (c ^ bsw[n]));
+    return lds_read16(sbase + brow_off[n] + 16 * (c ^ bsw[n]));
   };
-  u32x4_t bq[2][NT];
-  wait_vmcnt<16 + 2 * NT>();
-  ring_barrier();
-  read_half(0, 0, bq[0]);
 
-  // NX: a next stage exists; DMA: issue DMA(s+3); WL: load W(s+2)
-  auto stage_body = [&](auto nx, auto dma, auto wl, int s, u32x4_t (&w)[2][4]) {
+  u32x4_t wr[2][2][4];   // weights of stages of even / odd index
+  dma_all(0);
+  asm volatile("" ::: "memory");
+  load_wq(0, 0, wr[0]);
+  load_wq(0, 1, wr[0]);
+  load_wq(0, 2, wr[0]);
+  asm volatile("" ::: "memory");
+  dma_all(1);
+  asm volatile("" ::: "memory");
+  load_wq(0, 3, wr[0]);
+  load_wq(1, 0, wr[1]);
+  load_wq(1, 1, wr[1]);
+  load_wq(1, 2, wr[1]);
+  asm volatile("" ::: "memory");
+  dma_all(2);
+  asm volatile("" ::: "memory");
+  wait_vmcnt<14 + 2 * NT>();   // DMA(0) landed
+  ring_barrier();              // B(0)
+  u32x4_t bq[2][NT];           // token fragments of the current / next quarter
 #pragma unroll
-    for (int h = 0; h < 3; ++h) {
-      read_half(s, h + 1, bq[(h + 1) & 1]);
-      wait_lgkm<NT>(bq[h & 1]);
+  for (int n = 0; n < NT; ++n) bq[0][n] = read1(0, 0, n);
+
+  // NX: a next stage exists; DMA: issue DMA(s+3); W1: load W(s+1) quarter 3;
+  // W2: load W(s+2); CNT: the wait before B(s+1)
+  auto stage_body = [&](auto nx, auto dma, auto w1, auto w2, auto cnt, int s,
+                        u32x4_t (&w)[2][4], u32x4_t (&wn)[2][4]) {
+    constexpr bool NX = decltype(nx)::value, DM = decltype(dma)::value;
+    constexpr bool W1 = decltype(w1)::value, W2 = decltype(w2)::value;
 #pragma unroll
-      for (int n = 0; n < NT; ++n)
+    for (int h = 0; h < 4; ++h) {
+      if (h == 3) {
+        if constexpr (NX) {
+          asm volatile("" ::: "memory");
+          wait_vmcnt<decltype(cnt)::value>();
+          ring_barrier();  // B(s+1)
+        }
+      }
+      u32x4_t (&cur)[NT] = bq[h & 1];
+      u32x4_t (&nxt)[NT] = bq[(h + 1) & 1];
+      const bool reads_next = h < 3 || NX;
 #pragma unroll
-        for (int t = 0; t < 2; ++t) mma32(acc[t][n], w[t][h], bq[h & 1][n]);
+      for (int n = 0; n < NT; ++n) {
+        // reads in flight after fragment n: the rest of this quarter and
+        // the next quarter's reads issued so far, NT - 1 in all
+        if (reads_next) wait_lgkm1<NT - 1>(cur[n]);
+        else wait_last<NT>(cur[n], n);
+        if (UP) {
+          mma32(acc[0][n], w[0][h], cur[n]);
+          mma32(acc[1][n], w[1][h], cur[n]);
+        } else {
+          mma32(acc[0][n], cur[n], w[0][h]);
+          mma32(acc[1][n], cur[n], w[1][h]);
+        }
+        if (h < 3) nxt[n] = read1(s, h + 1, n);
+        else if constexpr (NX) nxt[n] = read1(s + 1, 0, n);
+        if (n == 0) {
+          asm volatile("" ::: "memory");
+          if (h == 0) {
+            if constexpr (W1) load_wq(s + 1, 3, wn);
+          } else {
+            if constexpr (W2) load_wq(s + 2, h - 1, w);
+          }
+          asm volatile("" ::: "memory");
+        }
+        if (h == 3) {
+          if constexpr (DM) dma1(s + 3, n);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
-    if constexpr (decltype(nx)::value) {
-      wait_vmcnt<8 + NT>();
-      ring_barrier();  // B(s+1)
-      if constexpr (decltype(dma)::value) issue_tok(s + 3);
-      read_half(s + 1, 0, bq[0]);
-      wait_lgkm<NT>(bq[1]);
-    } else {
-      wait_lgkm<0>(bq[1]);
-    }
-#pragma unroll
-    for (int n = 0; n < NT; ++n)
-#pragma unroll
-      for (int t = 0; t < 2; ++t) mma32(acc[t][n], w[t][3], bq[1][n]);
-    asm volatile("" ::: "memory");
-    if constexpr (decltype(wl)::value) load_w(s + 2, w);
   };
   using T_ = std::true_type;
   using F_ = std::false_type;
-  // steady state: every stage issues DMA(s+3) and W(s+2) (the loads stay
-  // unconditional, so the compiler's own waits for W count exactly)
+  constexpr int STEADY = 14 + NT;
   int s = 0;
   for (; s + 4 < NS; s += 2) {
-    stage_body(T_{}, T_{}, T_{}, s, wr[0]);
-    stage_body(T_{}, T_{}, T_{}, s + 1, wr[1]);
+    stage_body(T_{}, T_{}, T_{}, T_{}, ic_t<STEADY>{}, s, wr[0], wr[1]);
+    stage_body(T_{}, T_{}, T_{}, T_{}, ic_t<STEADY>{}, s + 1, wr[1], wr[0]);
   }
-  // NS - 4 .. NS - 1
-  stage_body(T_{}, T_{}, T_{}, s, wr[0]);
-  stage_body(T_{}, F_{}, T_{}, s + 1, wr[1]);
-  stage_body(T_{}, F_{}, F_{}, s + 2, wr[0]);
-  stage_body(F_{}, F_{}, F_{}, s + 3, wr[1]);
+  // the last four stages (NS - 4 is even)
+  stage_body(T_{}, T_{}, T_{}, T_{}, ic_t<STEADY>{}, s, wr[0], wr[1]);
+  stage_body(T_{}, F_{}, T_{}, T_{}, ic_t<STEADY>{}, s + 1, wr[1], wr[0]);
+  stage_body(T_{}, F_{}, T_{}, F_{}, ic_t<10>{}, s + 2, wr[0], wr[1]);
+  stage_body(F_{}, F_{}, F_{}, F_{}, ic_t<0>{}, s + 3, wr[1], wr[0]);
 
-  // epilogue: lane l holds token row 32 n + l%32 and, for register r, weight
-  // row 8 (r/4) + 4 (l/32) + r%4 of each A tile
   const int col = lane & 31, hi = lane >> 5;
+  if constexpr (UP) {
+    // lane l holds token row 32 n + l%32 and, for register r, weight row
+    // 8 (r/4) + 4 (l/32) + r%4 of each weight tile
 #pragma unroll
-  for (int n = 0; n < NT; ++n) {
-    const int row = 32 * n + col;
-    if (row >= it.rows) continue;
-    const size_t pos = static_cast<size_t>(it.row_begin + row);
+    for (int n = 0; n < NT; ++n) {
+      const int row = 32 * n + col;
+      if (row >= it.rows) continue;
+      const size_t pos = static_cast<size_t>(it.row_begin + row);
 #pragma unroll
-    for (int r4 = 0; r4 < 4; ++r4) {
-      if (UP) {
+      for (int r4 = 0; r4 < 4; ++r4) {
         const int f = f0 + 32 * wave + 8 * r4 + 4 * hi;
         float hv[4];
 #pragma unroll
@@ -660,15 +722,21 @@ __device__ __forceinline__ void dense_tile(const FfnLaunch& a, const WorkItem& i
         packed.x = f32_to_bf16_rne(hv[0]) | (static_cast<uint32_t>(f32_to_bf16_rne(hv[1])) << 16);
         packed.y = f32_to_bf16_rne(hv[2]) | (static_cast<uint32_t>(f32_to_bf16_rne(hv[3])) << 16);
         *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.hout) + pos * I + f) = packed;
-      } else {
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
-          const int f = f0 + 64 * wave + 32 * t + 8 * r4 + 4 * hi;
-          const floatx16_t& v = acc[t][n];
-          *reinterpret_cast<float4*>(a.oout + pos * H + f) =
-              make_float4(v[4 * r4], v[4 * r4 + 1], v[4 * r4 + 2], v[4 * r4 + 3]);
-        }
       }
+    }
+  } else {
+    // lane l holds feature 32 t + l%32 of the wavefront's 64 and, for
+    // register r, token row 8 (r/4) + 4 (l/32) + r%4 of token tile n
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      float* o = a.oout + f0 + 64 * wave + 32 * t + col;
+#pragma unroll
+      for (int n = 0; n < NT; ++n)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = 32 * n + 8 * (r >> 2) + 4 * hi + (r & 3);
+          if (row < it.rows) o[static_cast<size_t>(it.row_begin + row) * H] = acc[t][n][r];
+        }
     }
   }
 }
