@@ -17,6 +17,12 @@
   524280 routes; per-launch device times (HIP events) and HBM fractions of
   the algorithmic bytes against 8 TB/s.
 
+--vendor: context for --gemm: the vendor library's batched bf16 GEMM
+  (torch.bmm, which calls hipBLASLt) on plain contiguous operands of the
+  same dimensions: 128 experts x 1024 rows against the gate/up weights
+  (4096 -> 3072) and the down weights (1536 -> 4096), bf16 output, event
+  timed. It does none of the routed gather, SwiGLU or expert-sorted rows.
+
 --gate: the gate GEMM of route_block_gate (logits = x W_gate^T, fp32
   accumulation) on the 40% stack's shape (32 tokens, hidden 2048, 64 experts),
   its batch-8 form (256 tokens), the E=128 stack (1024 tokens, hidden 4096)
@@ -277,11 +283,44 @@ def gate(args):
     print(json.dumps(out), flush=True)
 
 
+def vendor(args):
+    import torch
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(args.seed)
+    out = {"mode": "vendor",
+           "config": {"workload": "torch.bmm (hipBLASLt), bf16 in and out, contiguous operands: "
+                                  "128 batches of 1024 x K by K x N"}}
+    for name, (G, M, K, N) in (("gate_up", (128, 1024, 4096, 3072)),
+                               ("down", (128, 1024, 1536, 4096))):
+        a = torch.randn(G, M, K, generator=g, device="cuda").to(torch.bfloat16)
+        b = torch.randn(G, K, N, generator=g, device="cuda").to(torch.bfloat16).contiguous()
+        c = torch.empty(G, M, N, device="cuda", dtype=torch.bfloat16)
+        for _ in range(3):
+            torch.bmm(a, b, out=c)
+        torch.cuda.synchronize()
+        ms = []
+        for _ in range(args.iters * 3):
+            ev0.record()
+            torch.bmm(a, b, out=c)
+            ev1.record()
+            torch.cuda.synchronize()
+            ms.append(ev0.elapsed_time(ev1))
+        fl = 2.0 * G * M * K * N
+        avg = sum(ms) / len(ms)
+        out[name] = {"dims": [G, M, K, N], "launches": len(ms), "avg_ms": round(avg, 4),
+                     "tflops": round(fl / 1e12 / (avg / 1e3), 1),
+                     "mfma_frac": round(fl / 1e12 / (avg / 1e3) / MFMA_BF16_PEAK_TFLOPS, 4)}
+        del a, b, c
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gemm", action="store_true")
     ap.add_argument("--route", action="store_true")
     ap.add_argument("--gate", action="store_true")
+    ap.add_argument("--vendor", action="store_true")
     ap.add_argument("--iters", type=int, default=3)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--check-rows", type=int, default=8)
@@ -296,6 +335,8 @@ def main():
         route(args)
     if args.gate:
         gate(args)
+    if args.vendor:
+        vendor(args)
 
 
 if __name__ == "__main__":
