@@ -167,12 +167,16 @@ def main():
     cal_w, write = counter_run(args.write, "WRITE_SIZE", ops_w)
     sf, sw = CAL_BYTES / cal_f, CAL_BYTES / cal_w     # bytes per counter KiB
     ops_m = ops_by_class(args.mfma_log)
-    mfma, gui = {}, {}
+    mfma, gui, clk = {}, {}, {}
     for cnt, dst in (("SQ_VALU_MFMA_BUSY_CYCLES", mfma), ("GRBM_GUI_ACTIVE", gui)):
         rows = [r for r in read_csv(args.mfma, "counter_collection") if r["Counter_Name"] == cnt]
         _, per = timed_dispatches(rows)
         for c in CLASSES:
             dst[c] = [float(r["Counter_Value"]) for r in per[c]]
+            if cnt == "GRBM_GUI_ACTIVE":   # shader-clock cycles per XCD over the dispatch
+                clk[c] = [float(r["Counter_Value"]) / N_XCD /
+                          max(1, int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+                          for r in per[c]]
     with open(FFN_SOURCE, "rb") as f:
         sha = hashlib.sha256(f.read()).hexdigest()
     rows_md, per_class = [], {}
@@ -186,12 +190,13 @@ def main():
         busy = mean(mfma[c]) / (N_SIMD * mean(gui[c]) / N_XCD) if mean(gui[c]) else None
         t_us = mean([o[2] for o in ops_t[c]]) * 1e3
         flop_util = flops / (t_us * 1e-6) / 2.5e15 if t_us > 0 else None
+        ghz = mean(clk[c]) if clk[c] else None
         per_class[c] = dict(launches=len(ops_f[c]), algorithmic_bytes=int(alg), h2d_bytes=int(h2d),
                             fetch_bytes=int(fb), write_bytes=int(wb), mfma_busy=busy,
-                            flop_util=flop_util)
+                            flop_util=flop_util, clock_ghz=ghz)
         rows_md.append(f"| {c} | {len(ops_f[c])} | {alg / 1e6:.1f} | {h2d / 1e6:.1f} | "
                        f"{fb / 1e6:.1f} | {wb / 1e6:.1f} | {(fb + wb) / max(1.0, alg + 2 * h2d):.3f} | "
-                       f"{busy:.4f} | {flop_util:.4f} |")
+                       f"{ghz:.2f} | {busy:.4f} | {flop_util:.4f} |")
     up = per_class["up"]
     rec = {"kernel": "k_ffn UP=true (grouped gate/up SwiGLU GEMM, with the misses' gate/up copy)",
            "workload": args.workload_text, "ffn_source_sha256": sha,
@@ -220,13 +225,15 @@ def main():
           "launches that carry the misses' copy also read those bytes from pinned host memory "
           "and write them into their slots, so the ratio's denominator adds twice the copied "
           "bytes. MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES (summed over the 1024 SIMDs) / (1024 x "
-          "GRBM_GUI_ACTIVE / 8): the share of the launch's active cycles the matrix cores were "
-          "busy (GRBM_GUI_ACTIVE sums the 8 XCDs: divided by 8 it matches the launch's duration "
-          "at 2.4 GHz); it counts the MFMAs of padded tile rows too. Flop util = algorithmic "
-          "flops / event time of the trace run / 2.5 PFLOP/s.", "",
+          "GRBM_GUI_ACTIVE / 8): the share of the launch's shader-clock cycles the matrix "
+          "cores were busy (GRBM_GUI_ACTIVE counts shader-clock cycles summed over the 8 XCDs; "
+          "divided by 8 and by the dispatch's duration it gives the clock the launch ran at, "
+          "the clock column); it counts the MFMAs of padded tile rows too. Flop util = "
+          "algorithmic flops / event time of the trace run / 2.5 PFLOP/s.", "",
           "| launch class | launches | algorithmic MB | copied host->device MB | fetched MB | "
-          "written MB | traffic / (algorithmic + 2 x copied) | MFMA busy | flop util |",
-          "|---|---|---|---|---|---|---|---|---|", *rows_md, "",
+          "written MB | traffic / (algorithmic + 2 x copied) | clock (GHz) | MFMA busy | "
+          "flop util |",
+          "|---|---|---|---|---|---|---|---|---|---|", *rows_md, "",
           f"Kernel source sha256 `{sha}`; bench.py reports the gate/up traffic only while "
           "ffn.hip is unchanged."]
     with open(os.path.join(args.out, f"ffn_kernels_{args.name}_counters.md"), "w") as f:

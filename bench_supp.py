@@ -15,7 +15,8 @@
   over the fp32 router logits of 32 layers x 65535 tokens x 128 experts,
   then the histogram / scan / permutation and the retention of each layer's
   524280 routes; per-launch device times (HIP events) and HBM fractions of
-  the algorithmic bytes against 8 TB/s.
+  the algorithmic bytes against 8 TB/s; for context, the read rate of
+  torch.amax over each token's experts and of torch.sum on the same 1 GiB.
 
 --vendor: context for --gemm: the vendor library's batched bf16 GEMM
   (torch.bmm, which calls hipBLASLt) on plain contiguous operands of the
@@ -217,6 +218,27 @@ def route(args):
         return {"avg_us": round(ms * 1e3, 2), "bytes": nbytes, "GBps": round(gbs, 1),
                 "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)}
 
+    # context: the read rate plain library reductions get on the same 1 GiB
+    # (torch.amax over the experts of each token, the top-k's access pattern,
+    # and a sum over the whole tensor)
+    read_ref = {}
+    for name, fn in (("amax_per_token", lambda: lg_all.amax(dim=2)),
+                     ("sum_all", lambda: lg_all.sum())):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(args.iters + 2):
+            ev[0].record(st)
+            fn()
+            ev[1].record(st)
+            torch.cuda.synchronize()
+            ts.append(ev[0].elapsed_time(ev[1]))
+        ms = float(np.mean(ts))
+        gbs = L * T * E * 4 / 1e9 / (ms / 1e3)
+        read_ref[name] = {"avg_us": round(ms * 1e3, 2), "GBps": round(gbs, 1),
+                          "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)}
+
     route_bytes = L * (T * E * 4 + T * k * 8 + T * k * 12 + E * 8)
     prio_bytes = L * (T * k * 8 + T * 4 + E * 8)
     batched = {"blocks": L, "calls": args.iters,
@@ -238,7 +260,8 @@ def route(args):
                       "logit_bytes_per_pass": L * T * E * 4},
            "route_topk": agg("route_topk"), "permute": agg("permute"),
            "score_retain": agg("score_retain"), "passes": args.iters,
-           "wall_ms_per_pass": round(float(np.mean(t_wall)) * 1e3, 3), "batched": batched}
+           "wall_ms_per_pass": round(float(np.mean(t_wall)) * 1e3, 3), "batched": batched,
+           "torch_read_reference": read_ref}
     print(json.dumps(out), flush=True)
 
 
