@@ -41,6 +41,7 @@ CAL_BYTES = 64 * 2 ** 20 * 4     # bytes read, and bytes written, by the calibra
 N_SIMD = 1024                    # 256 CUs x 4 SIMDs
 N_XCD = 8                        # GRBM_GUI_ACTIVE sums the busy cycles of the 8 XCDs
 CLASSES = ("up", "mix", "down", "dense_up", "dense_down")
+MIN_CLOCK_NS = 200_000           # clock column only for dispatches of 200 us or more
 
 
 def kclass(name: str):
@@ -174,9 +175,10 @@ def main():
         for c in CLASSES:
             dst[c] = [float(r["Counter_Value"]) for r in per[c]]
             if cnt == "GRBM_GUI_ACTIVE":   # shader-clock cycles per XCD over the dispatch
-                clk[c] = [float(r["Counter_Value"]) / N_XCD /
-                          max(1, int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
-                          for r in per[c]]
+                durs = [max(1, int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) for r in per[c]]
+                # the counter's window exceeds short dispatches: clock only for long ones
+                clk[c] = ([float(r["Counter_Value"]) / N_XCD / d for r, d in zip(per[c], durs)]
+                          if durs and mean(durs) >= MIN_CLOCK_NS else [])
     with open(FFN_SOURCE, "rb") as f:
         sha = hashlib.sha256(f.read()).hexdigest()
     rows_md, per_class = [], {}
@@ -196,7 +198,7 @@ def main():
                             flop_util=flop_util, clock_ghz=ghz)
         rows_md.append(f"| {c} | {len(ops_f[c])} | {alg / 1e6:.1f} | {h2d / 1e6:.1f} | "
                        f"{fb / 1e6:.1f} | {wb / 1e6:.1f} | {(fb + wb) / max(1.0, alg + 2 * h2d):.3f} | "
-                       f"{ghz:.2f} | {busy:.4f} | {flop_util:.4f} |")
+                       f"{'—' if ghz is None else f'{ghz:.2f}'} | {busy:.4f} | {flop_util:.4f} |")
     up = per_class["up"]
     rec = {"kernel": "k_ffn UP=true (grouped gate/up SwiGLU GEMM, with the misses' gate/up copy)",
            "workload": args.workload_text, "ffn_source_sha256": sha,
@@ -228,7 +230,9 @@ def main():
           "GRBM_GUI_ACTIVE / 8): the share of the launch's shader-clock cycles the matrix "
           "cores were busy (GRBM_GUI_ACTIVE counts shader-clock cycles summed over the 8 XCDs; "
           "divided by 8 and by the dispatch's duration it gives the clock the launch ran at, "
-          "the clock column); it counts the MFMAs of padded tile rows too. Flop util = "
+          "the clock column, shown for classes whose dispatches last 200 us or more: the "
+          "counter's window exceeds shorter ones, which also makes their MFMA busy a lower "
+          "bound); it counts the MFMAs of padded tile rows too. Flop util = "
           "algorithmic flops / event time of the trace run / 2.5 PFLOP/s.", "",
           "| launch class | launches | algorithmic MB | copied host->device MB | fetched MB | "
           "written MB | traffic / (algorithmic + 2 x copied) | clock (GHz) | MFMA busy | "
