@@ -22,7 +22,8 @@
   (torch.bmm, which calls hipBLASLt) on plain contiguous operands of the
   same dimensions: 128 experts x 1024 rows against the gate/up weights
   (4096 -> 3072) and the down weights (1536 -> 4096), bf16 output, event
-  timed. It does none of the routed gather, SwiGLU or expert-sorted rows.
+  timed; then the down product right behind the gate/up product, as a layer
+  runs them. It does none of the routed gather, SwiGLU or expert-sorted rows.
 
 --gate: the gate GEMM of route_block_gate (logits = x W_gate^T, fp32
   accumulation) on the 40% stack's shape (32 tokens, hidden 2048, 64 experts),
@@ -311,6 +312,7 @@ def vendor(args):
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     g = torch.Generator(device="cuda")
     g.manual_seed(args.seed)
+    ops = {}
     out = {"mode": "vendor",
            "config": {"workload": "torch.bmm (hipBLASLt), bf16 in and out, contiguous operands: "
                                   "128 batches of 1024 x K by K x N"}}
@@ -334,7 +336,24 @@ def vendor(args):
         out[name] = {"dims": [G, M, K, N], "launches": len(ms), "avg_ms": round(avg, 4),
                      "tflops": round(fl / 1e12 / (avg / 1e3), 1),
                      "mfma_frac": round(fl / 1e12 / (avg / 1e3) / MFMA_BF16_PEAK_TFLOPS, 4)}
-        del a, b, c
+        ops[name] = (a, b, c, fl)
+    # the down product right behind the gate/up product, as the layer runs them
+    (ua, ub, uc, _), (da, db, dc, dfl) = ops["gate_up"], ops["down"]
+    ev2 = torch.cuda.Event(enable_timing=True)
+    ms = []
+    for i in range(args.iters * 3 + 2):
+        ev0.record()
+        torch.bmm(ua, ub, out=uc)
+        ev1.record()
+        torch.bmm(da, db, out=dc)
+        ev2.record()
+        torch.cuda.synchronize()
+        if i >= 2:
+            ms.append(ev1.elapsed_time(ev2))
+    avg = sum(ms) / len(ms)
+    out["down_after_gate_up"] = {"launches": len(ms), "avg_ms": round(avg, 4),
+                                 "mfma_frac": round(dfl / 1e12 / (avg / 1e3) /
+                                                    MFMA_BF16_PEAK_TFLOPS, 4)}
     print(json.dumps(out), flush=True)
 
 
