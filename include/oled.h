@@ -224,7 +224,7 @@ typedef enum {
   OLED_OP_SCORE_RETAIN = 5,
   OLED_OP_H2D = 6,           /* copy-engine copies of one apply_misses, or a
                                 transfer-only launch */
-  OLED_OP_FFN_DENSE_UP = 7,  /* dense-tile gate/up GEMM (experts with 128+ routed rows) */
+  OLED_OP_FFN_DENSE_UP = 7,  /* dense-tile gate/up GEMM (bf16 experts with 65+ routed rows) */
   OLED_OP_FFN_DENSE_DOWN = 8, /* dense-tile down GEMM */
   OLED_OP_LAYER_ADAPT = 9,    /* layer-adaptive re-sizing of the capacities */
   OLED_OP_ROUTE_GEMM = 10     /* the gate GEMM of route_block_gate */

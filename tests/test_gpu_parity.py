@@ -36,7 +36,7 @@ def _gpu():
 
 
 def _chain(w, seed, layers, n_iters, n_blocks, out_at=None, out_tokens=None, capacity=None,
-           forward=True, copy_mode="shader", report=True):
+           forward=True, copy_mode="shader", report=True, expect_dense=False):
     """Runs a schedule on both sides and compares every layer-iteration, the
     oracle advancing in lockstep with the GPU.
 
@@ -52,7 +52,9 @@ def _chain(w, seed, layers, n_iters, n_blocks, out_at=None, out_tokens=None, cap
          f"copy={copy_mode} report={report}")
     raw = W.expert_blocks(w, seed, range(n_blocks))
     pool = HN.fill_pool(w, seed, n_blocks, raw=raw)
-    ctx = HN.make_context(w, pool, capacity=C, n_layers=len(layers), copy_mode=copy_mode)
+    prof = oled.profile_mask("ffn_dense_up", "ffn_dense_down") if expect_dense else 0
+    ctx = HN.make_context(w, pool, capacity=C, n_layers=len(layers), copy_mode=copy_mode,
+                          profile_ops=prof)
     lock = LockstepOracle(len(layers), w.n_experts, w.top_k, C)
     ow = OracleWeights(w, seed, n_blocks, len(layers), raw=raw)
     worst = [0.0]
@@ -73,6 +75,10 @@ def _chain(w, seed, layers, n_iters, n_blocks, out_at=None, out_tokens=None, cap
 
     try:
         run_schedule_gpu(ctx, w, seed, layers, n_iters, forward, check, report=report)
+        if expect_dense:   # the dense-tile launches ran, with work
+            ops = ctx.profile_collect()
+            for name in ("ffn_dense_up", "ffn_dense_down"):
+                assert any(o[0] == name and o[4] > 0 for o in ops), f"{w.name}: no {name} launch"
     finally:
         ctx.close()
         pool.free()
@@ -237,7 +243,19 @@ def test_dense_tiles(copy_mode):
     """Experts with 128+ routed rows run as dense tiles: this block has experts
     with two 256-row items, one plus a shorter item, exactly 256 rows, a short
     item only, and fewer than 128 rows (streaming), as hits and as misses."""
-    _chain(DENSE, 1, range(2), 3, 32, copy_mode=copy_mode)
+    _chain(DENSE, 1, range(2), 3, 32, copy_mode=copy_mode, expect_dense=True)
+
+
+@pytest.mark.parametrize("H,I", [(256, 512), (768, 1280)])
+def test_dense_tiles_stage_counts(H, I):
+    """Dense tiles whose K loops have 4 stages (gate/up at hidden 256: only the
+    last four stages), 8, 12 (gate/up at hidden 768: one pass of the steady
+    loop) and 20 (down at intermediate 1280), each against the oracle on
+    sampled token rows, as hits and as misses."""
+    w = DENSE.replace(wid=310 + H // 256, name=f"dense-H{H}-I{I}", hidden=H, inter=I)
+    rows = np.random.default_rng(H + I).choice(w.tokens, 96, replace=False)
+    _chain(w, 2, range(2), 3, 2 * w.n_experts + 1, out_at={(0, 0), (1, 1), (0, 2)},
+           out_tokens=rows, expect_dense=True)
 
 
 def test_dense_tiles_cross_residency_bitwise():
