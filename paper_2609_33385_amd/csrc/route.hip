@@ -6,6 +6,8 @@
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace oled {
@@ -194,89 +196,212 @@ __device__ __forceinline__ void wave_topk_ids(const float* row, int E, int k, bo
   }
 }
 
-template <int KP, int KM>
+// Word 3 of a raw buffer resource (32-bit data format) on this part.
+constexpr int kRouteBufferFlags = 0x00020000;
+
+// s_waitcnt immediate: at most N vector-memory operations outstanding.
+template <int N>
+__device__ __forceinline__ void route_wait_vmcnt() {
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+typedef uint32_t u32x4r_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ u32x4r_t lds_read16r(uint32_t addr) {
+  u32x4r_t v;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr));
+  return v;
+}
+
+// DMA streaming (E % 32 == 0, the rows within a 32-bit byte offset): each
+// wavefront ranks several blocks of 64 tokens in turn, its logits copied into
+// LDS 32 experts (128 bytes per row) at a time by LDS DMA, two chunks in
+// flight across block boundaries; no staging registers. DMA instruction i of
+// a chunk moves rows 8 i .. 8 i + 7: lane l = 8 r + s loads the 16-byte slot
+// s ^ r of row 8 i + r into LDS slot l, so that token t's slot c sits at
+// 8 t + (c ^ (t % 8)) and the 8 lanes of each LDS access group read 8
+// distinct bank groups. A block's ids are written when its ranking ends; the
+// logits of its routes for the gates are loaded then and the gates computed
+// after the next block, so the wavefront does not wait for those loads.
+// Otherwise (register staging) one block per wavefront, one 4-byte load per
+// lane through registers and a padded LDS row.
+template <int KP, int KM, bool DMA>
 __global__ __launch_bounds__(256) void k_route_lanes(const float* __restrict__ logits, int T, int E,
                                                      int k, int32_t* __restrict__ topk_idx,
                                                      float* __restrict__ gates,
                                                      int32_t* __restrict__ bad_flag, int Tb) {
   static_assert(KP > KM, "the packed list holds the k-th and the (k+1)-th key");
-  __shared__ float s_buf[4][64 * kLaneRow];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int t0 = (blockIdx.x * 4 + wave) * 64;
-  float* buf = s_buf[wave];
-  // lane l loads column l % C of rows l / C + (64 / C) i, i < C, of a chunk
-  // of C = kLaneChunk experts
-  const int lc = lane % kLaneChunk, lr = lane / kLaneChunk;
-  float v[kLaneChunk];
-  auto load = [&](int e0) {
-    const int e = e0 + lc;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  uint32_t key[KP];
+  int nonfinite = 0;
+  auto reset = [&]() {
 #pragma unroll
-    for (int i = 0; i < kLaneChunk; ++i) {
-      const int t = t0 + lr + kLaneRowsPerLoad * i;
-      v[i] = (t < T && e < E) ? logits[static_cast<size_t>(t) * E + e] : 0.f;
+    for (int j = 0; j < KP; ++j) key[j] = 0u;
+    nonfinite = 0;
+  };
+  auto insert = [&](float x, int e) {
+    nonfinite |= !__builtin_isfinite(x);
+    const uint32_t c = (max(ord_key(x), 1u) & 0xFFFFFF00u) | static_cast<uint32_t>(255 - e);
+    // insertion into the descending list: new[q] = max(old[q], min(old[q-1], c)),
+    // the median of (old[q-1], old[q], c) since old[q-1] >= old[q]: one
+    // v_med3_u32 per position, every position from the old list
+#pragma unroll
+    for (int q = KP - 1; q >= 1; --q) key[q] = med3u(key[q - 1], key[q], c);
+    key[0] = max(key[0], c);
+  };
+  // ids of the block at t0 from the lanes' keys: where two of the k + 1 best
+  // share their top 24 bits, the whole wavefront ranks that token again from
+  // memory with full keys
+  auto block_ids = [&](int t0, int32_t (&id)[KM]) {
+    const int t = t0 + lane;
+    bool amb = false;
+    if (t < T) {
+#pragma unroll
+      for (int j = 0; j + 1 < KP; ++j)
+        if (j < k) amb |= (key[j] >> 8) == (key[j + 1] >> 8);
+    }
+#pragma unroll
+    for (int j = 0; j < KM; ++j) id[j] = 255 - static_cast<int>(key[j] & 0xFFu);
+    for (uint64_t todo = __ballot(amb); todo != 0ull; todo &= todo - 1) {
+      const int owner = __builtin_ctzll(todo);
+      wave_topk_ids<KM>(logits + static_cast<size_t>(t0 + owner) * E, E, k, lane == owner, id);
     }
   };
-  uint32_t key[KP];
-#pragma unroll
-  for (int j = 0; j < KP; ++j) key[j] = 0u;
-  int nonfinite = 0;
-  load(0);
-  // Each wavefront stages its own rows: ordering its LDS writes and reads
-  // needs no workgroup barrier, only that the compiler keep them in program
-  // order (a wavefront's LDS operations complete in issue order).
-  for (int e0 = 0; e0 < E; e0 += kLaneChunk) {
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the previous chunk's reads are done
-#pragma unroll
-    for (int i = 0; i < kLaneChunk; ++i) buf[(lr + kLaneRowsPerLoad * i) * kLaneRow + lc] = v[i];
-    if (e0 + kLaneChunk < E) load(e0 + kLaneChunk);
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    const int ne = min(kLaneChunk, E - e0);
-    for (int j = 0; j < ne; ++j) {
-      const float x = buf[lane * kLaneRow + j];
-      nonfinite |= !__builtin_isfinite(x);
-      const uint32_t c = (max(ord_key(x), 1u) & 0xFFFFFF00u) | static_cast<uint32_t>(255 - (e0 + j));
-      // insertion into the descending list: new[q] = max(old[q], min(old[q-1], c)),
-      // the median of (old[q-1], old[q], c) since old[q-1] >= old[q]: one
-      // v_med3_u32 per position, every position from the old list
-#pragma unroll
-      for (int q = KP - 1; q >= 1; --q) key[q] = med3u(key[q - 1], key[q], c);
-      key[0] = max(key[0], c);
-    }
-  }
-  const int t = t0 + lane;
-  bool amb = false;
-  if (t < T) {
-#pragma unroll
-    for (int j = 0; j + 1 < KP; ++j)
-      if (j < k) amb |= (key[j] >> 8) == (key[j + 1] >> 8);
-  }
-  int32_t id[KM];
-#pragma unroll
-  for (int j = 0; j < KM; ++j) id[j] = 255 - static_cast<int>(key[j] & 0xFFu);
-  for (uint64_t todo = __ballot(amb); todo != 0ull; todo &= todo - 1) {
-    const int owner = __builtin_ctzll(todo);
-    wave_topk_ids<KM>(logits + static_cast<size_t>(t0 + owner) * E, E, k, lane == owner, id);
-  }
-  if (t < T) {
-    const float* row = logits + static_cast<size_t>(t) * E;
-    double lv[KM];
-#pragma unroll
-    for (int j = 0; j < KM; ++j) lv[j] = j < k ? static_cast<double>(row[id[j]]) : 0.0;
+  // gates of token t from the logits of its routes: fp64 exp of l_j - l_0,
+  // summed in slot order, one rounding to fp32
+  auto write_gates = [&](const float (&lvf)[KM], int t) {
     double ex[KM];
     double sum = 0.0;
 #pragma unroll
     for (int j = 0; j < KM; ++j) {
-      ex[j] = j < k ? exp(lv[j] - lv[0]) : 0.0;
+      ex[j] = j < k ? exp(static_cast<double>(lvf[j]) - static_cast<double>(lvf[0])) : 0.0;
       if (j < k) sum += ex[j];
     }
 #pragma unroll
     for (int j = 0; j < KM; ++j)
-      if (j < k) {
-        topk_idx[static_cast<size_t>(t) * k + j] = id[j];
-        gates[static_cast<size_t>(t) * k + j] = static_cast<float>(ex[j] / sum);
+      if (j < k) gates[static_cast<size_t>(t) * k + j] = static_cast<float>(ex[j] / sum);
+  };
+  if constexpr (DMA) {
+    __shared__ u32x4r_t s_dma[4][2][64 * 8];   // [wavefront][buffer][token][slot]: 64 KiB
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(logits), 0, T * E * 4, kRouteBufferFlags);   // rows past T read 0
+    const int r8 = lane >> 3, s8 = lane & 7;
+    const int nch = E / 32;
+    const int stride = static_cast<int>(gridDim.x) * 4;   // blocks per grid step
+    const int blk0 = static_cast<int>(blockIdx.x) * 4 + wave;
+    const int nblk = (T + 63) >> 6;
+    const int my_n = blk0 < nblk ? (nblk - 1 - blk0) / stride + 1 : 0;
+    const int total = my_n * nch;   // chunks of this wavefront
+    auto dma = [&](int g) {
+      const int bi = g / nch, c = g - bi * nch;
+      const int voff = ((blk0 + bi * stride) * 64 + r8) * E * 4 + 16 * (s8 ^ r8);
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            rs, (__attribute__((address_space(3))) void*)(&s_dma[wave][g & 1][64 * i]), 16,
+            voff + i * 8 * E * 4, 128 * c, 0, 0);
+    };
+    if (total > 0) dma(0);
+    if (total > 1) dma(1);
+    const uint32_t rbase = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&s_dma[wave][0][0])) +
+                           16u * 8u * static_cast<uint32_t>(lane);
+    const int sw = lane & 7;
+    bool pend = false;   // a block whose gates are still to be written
+    int pt = 0;
+    float plv[KM];
+#pragma unroll
+    for (int j = 0; j < KM; ++j) plv[j] = 0.f;
+    for (int g = 0; g < total; ++g) {
+      const int bi = g / nch, c = g - bi * nch;
+      if (c == 0) reset();
+      // wait for DMA(g): issued after it are DMA(g + 1) and, in the first two
+      // chunks of every block but the first, the last block's gate loads
+      // (fewer allowed than that only waits longer)
+      const bool more = g + 1 < total, loads = c <= 1 && bi >= 1;
+      if (more && loads) route_wait_vmcnt<16>();
+      else if (more || loads) route_wait_vmcnt<8>();
+      else route_wait_vmcnt<0>();
+      asm volatile("" ::: "memory");
+      const uint32_t base = rbase + static_cast<uint32_t>(g & 1) * (64u * 8u * 16u);
+      u32x4r_t x[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) x[j] = lds_read16r(base + 16u * static_cast<uint32_t>(j ^ sw));
+      asm volatile("s_waitcnt lgkmcnt(0)"
+                   : "+v"(x[0]), "+v"(x[1]), "+v"(x[2]), "+v"(x[3]), "+v"(x[4]), "+v"(x[5]),
+                     "+v"(x[6]), "+v"(x[7])::"memory");
+      if (g + 2 < total) dma(g + 2);   // into the buffer just read
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) insert(__uint_as_float(x[j][q]), 32 * c + 4 * j + q);
+      if (c == nch - 1) {   // the block is ranked
+        const int t0 = (blk0 + bi * stride) * 64;
+        int32_t id[KM];
+        block_ids(t0, id);
+        const int t = t0 + lane;
+        if (t < T) {
+#pragma unroll
+          for (int j = 0; j < KM; ++j)
+            if (j < k) topk_idx[static_cast<size_t>(t) * k + j] = id[j];
+          if (nonfinite) atomicOr(&bad_flag[t / Tb], 1);   // token t's block
+        }
+        if (pend && pt < T) write_gates(plv, pt);   // the last block's logits have landed
+        if (t < T) {
+          const float* row = logits + static_cast<size_t>(t) * E;
+#pragma unroll
+          for (int j = 0; j < KM; ++j) plv[j] = j < k ? row[id[j]] : 0.f;
+        }
+        pend = true;
+        pt = t;
       }
+    }
+    if (pend && pt < T) write_gates(plv, pt);
+  } else {
+    __shared__ float s_buf[4][64 * kLaneRow];
+    float* buf = s_buf[wave];
+    const int t0 = (blockIdx.x * 4 + wave) * 64;
+    // lane l loads column l % C of rows l / C + (64 / C) i, i < C, of a chunk
+    // of C = kLaneChunk experts
+    const int lc = lane % kLaneChunk, lr = lane / kLaneChunk;
+    float v[kLaneChunk];
+    auto load = [&](int e0) {
+      const int e = e0 + lc;
+#pragma unroll
+      for (int i = 0; i < kLaneChunk; ++i) {
+        const int t = t0 + lr + kLaneRowsPerLoad * i;
+        v[i] = (t < T && e < E) ? logits[static_cast<size_t>(t) * E + e] : 0.f;
+      }
+    };
+    reset();
+    load(0);
+    // Each wavefront stages its own rows: ordering its LDS writes and reads
+    // needs no workgroup barrier, only that the compiler keep them in program
+    // order (a wavefront's LDS operations complete in issue order).
+    for (int e0 = 0; e0 < E; e0 += kLaneChunk) {
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the previous chunk's reads are done
+#pragma unroll
+      for (int i = 0; i < kLaneChunk; ++i) buf[(lr + kLaneRowsPerLoad * i) * kLaneRow + lc] = v[i];
+      if (e0 + kLaneChunk < E) load(e0 + kLaneChunk);
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      const int ne = min(kLaneChunk, E - e0);
+      for (int j = 0; j < ne; ++j) insert(buf[lane * kLaneRow + j], e0 + j);
+    }
+    int32_t id[KM];
+    block_ids(t0, id);
+    const int t = t0 + lane;
+    if (t < T) {
+      const float* row = logits + static_cast<size_t>(t) * E;
+      float lv[KM];
+#pragma unroll
+      for (int j = 0; j < KM; ++j) lv[j] = j < k ? row[id[j]] : 0.f;
+#pragma unroll
+      for (int j = 0; j < KM; ++j)
+        if (j < k) topk_idx[static_cast<size_t>(t) * k + j] = id[j];
+      write_gates(lv, t);
+      if (nonfinite) atomicOr(&bad_flag[t / Tb], 1);   // token t's block
+    }
   }
-  if (t < T && nonfinite) atomicOr(&bad_flag[t / Tb], 1);   // token t's block
 }
 
 constexpr int kPermThreads = 1024;
@@ -286,6 +411,7 @@ constexpr int kChunkTokens = kChunkWords * 32;
 
 constexpr int kFusedMaxRoutes = 1024;       // fused routing path: T * k routes kept in LDS
 constexpr int kLaneTokensMin = 1024;        // blocks of more tokens route one token per lane
+constexpr int kRouteStreamGrid = 512;       // DMA-streamed top-k: two workgroups per CU
 constexpr int kGateFullGrid = 256;          // gate GEMM workgroups that fill the compute units
 constexpr int kChunkedMinTokens = 1024;     // and permute over many workgroups
 
@@ -1263,18 +1389,26 @@ hipError_t launch_route_topk(const float* logits, int T, int E, int k, int32_t* 
   const int Tb = block_tokens > 0 ? block_tokens : T;
   if (route_lanes(T)) {
     const int blocks = (T + 255) / 256;
-    if (k <= 2)
-      hipExtLaunchKernelGGL(k_route_lanes<3, 2>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits,
-                            T, E, k, topk_idx, gates, bad_flag, Tb);
-    else if (k <= 4)
-      hipExtLaunchKernelGGL(k_route_lanes<5, 4>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits,
-                            T, E, k, topk_idx, gates, bad_flag, Tb);
-    else if (k <= 8)
-      hipExtLaunchKernelGGL(k_route_lanes<9, 8>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, logits,
-                            T, E, k, topk_idx, gates, bad_flag, Tb);
-    else
-      hipExtLaunchKernelGGL(k_route_lanes<17, 16>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0,
-                            logits, T, E, k, topk_idx, gates, bad_flag, Tb);
+    // DMA streaming: whole 32-expert chunks, byte offsets of every row the
+    // wavefronts touch within a 32-bit buffer offset; one grid of two
+    // workgroups per CU whose wavefronts take blocks of 64 tokens in turn
+    const bool dma = E % 32 == 0 && E <= 256 &&
+                     static_cast<int64_t>((T + 63) / 64) * 64 * E * 4 <= INT32_MAX;
+    const int grid = dma ? (blocks < kRouteStreamGrid ? blocks : kRouteStreamGrid) : blocks;
+    auto go = [&](auto kp, auto km) {
+      constexpr int KP = decltype(kp)::value, KM = decltype(km)::value;
+      if (dma)
+        hipExtLaunchKernelGGL(k_route_lanes<KP, KM, true>, dim3(grid), dim3(256), 0, s, ev0, ev1,
+                              0, logits, T, E, k, topk_idx, gates, bad_flag, Tb);
+      else
+        hipExtLaunchKernelGGL(k_route_lanes<KP, KM, false>, dim3(blocks), dim3(256), 0, s, ev0, ev1,
+                              0, logits, T, E, k, topk_idx, gates, bad_flag, Tb);
+    };
+    using std::integral_constant;
+    if (k <= 2) go(integral_constant<int, 3>{}, integral_constant<int, 2>{});
+    else if (k <= 4) go(integral_constant<int, 5>{}, integral_constant<int, 4>{});
+    else if (k <= 8) go(integral_constant<int, 9>{}, integral_constant<int, 8>{});
+    else go(integral_constant<int, 17>{}, integral_constant<int, 16>{});
     return hipGetLastError();
   }
   const int blocks = (T + 3) / 4 < 4096 ? (T + 3) / 4 : 4096;
