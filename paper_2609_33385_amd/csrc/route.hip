@@ -213,6 +213,24 @@ __device__ __forceinline__ u32x4r_t lds_read16r(uint32_t addr) {
   return v;
 }
 
+// 4-byte LDS accesses as inline assembly, ordered with explicit lgkmcnt
+// waits: the compiler's own LDS accesses would wait for every LDS DMA in
+// flight.
+__device__ __forceinline__ void lds_write4r(uint32_t addr, uint32_t v) {
+  asm volatile("ds_write_b32 %0, %1" ::"v"(addr), "v"(v) : "memory");
+}
+__device__ __forceinline__ uint32_t lds_read4r(uint32_t addr) {
+  uint32_t v;
+  asm volatile("ds_read_b32 %0, %1" : "=v"(v) : "v"(addr) : "memory");
+  return v;
+}
+template <int N>
+__device__ __forceinline__ void lds_wait_all(uint32_t (&v)[N]) {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+  for (int i = 0; i < N; ++i) asm volatile("" : "+v"(v[i]));
+}
+
 // DMA streaming (E % 32 == 0, the rows within a 32-bit byte offset): each
 // wavefront ranks several blocks of 64 tokens in turn, its logits copied into
 // LDS 32 experts (128 bytes per row) at a time by LDS DMA, two chunks in
@@ -309,19 +327,42 @@ __global__ __launch_bounds__(256) void k_route_lanes(const float* __restrict__ l
     const int sw = lane & 7;
     bool pend = false;   // a block whose gates are still to be written
     int pt = 0;
-    float plv[KM];
+    float gv[KM];        // its route logits: token (64 m + lane) / KM, slot lane % KM
+    uint32_t gon = 0u;   // bit m: gv[m] is a route's logit
 #pragma unroll
-    for (int j = 0; j < KM; ++j) plv[j] = 0.f;
+    for (int j = 0; j < KM; ++j) gv[j] = 0.f;
+    __shared__ uint32_t s_tbl[4][64 * KM];   // per wavefront: [token][slot] ids, then logits
+    const uint32_t tbl = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&s_tbl[wave][0]));
+    // gates of the pending block: its logits back to one token per lane
+    auto finish = [&]() {
+#pragma unroll
+      for (int m = 0; m < KM; ++m)
+        lds_write4r(tbl + 4u * (64 * m + lane), ((gon >> m) & 1u) ? __float_as_uint(gv[m]) : 0u);
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      uint32_t lvu[KM];
+#pragma unroll
+      for (int j = 0; j < KM; ++j) lvu[j] = lds_read4r(tbl + 4u * (KM * lane + j));
+      lds_wait_all(lvu);
+      float lvf[KM];
+#pragma unroll
+      for (int j = 0; j < KM; ++j) lvf[j] = __uint_as_float(lvu[j]);
+      if (pt < T) write_gates(lvf, pt);
+    };
     for (int g = 0; g < total; ++g) {
       const int bi = g / nch, c = g - bi * nch;
       if (c == 0) reset();
-      // wait for DMA(g): issued after it are DMA(g + 1) and, in the first two
-      // chunks of every block but the first, the last block's gate loads
-      // (fewer allowed than that only waits longer)
+      // wait for DMA(g): issued after it are DMA(g + 1) (8 loads) and, in the
+      // first two chunks of every block but the first, the last block's KM
+      // gate loads (issued by every lane, so exactly KM; with one chunk per
+      // block two blocks' loads, of which counting one only waits longer)
       const bool more = g + 1 < total, loads = c <= 1 && bi >= 1;
-      if (more && loads) route_wait_vmcnt<16>();
-      else if (more || loads) route_wait_vmcnt<8>();
-      else route_wait_vmcnt<0>();
+      if (more) {
+        if (loads) route_wait_vmcnt<8 + KM>();
+        else route_wait_vmcnt<8>();
+      } else {
+        if (loads) route_wait_vmcnt<KM>();
+        else route_wait_vmcnt<0>();
+      }
       asm volatile("" ::: "memory");
       const uint32_t base = rbase + static_cast<uint32_t>(g & 1) * (64u * 8u * 16u);
       u32x4r_t x[8];
@@ -346,17 +387,33 @@ __global__ __launch_bounds__(256) void k_route_lanes(const float* __restrict__ l
             if (j < k) topk_idx[static_cast<size_t>(t) * k + j] = id[j];
           if (nonfinite) atomicOr(&bad_flag[t / Tb], 1);   // token t's block
         }
-        if (pend && pt < T) write_gates(plv, pt);   // the last block's logits have landed
-        if (t < T) {
-          const float* row = logits + static_cast<size_t>(t) * E;
+        if (pend) finish();   // the last block's logits have landed
+        // this block's route logits for its gates, loaded with KM lanes per
+        // token (through the table) so that one load's lanes share a row
+        uint32_t idx[KM];
 #pragma unroll
-          for (int j = 0; j < KM; ++j) plv[j] = j < k ? row[id[j]] : 0.f;
+        for (int j = 0; j < KM; ++j) lds_write4r(tbl + 4u * (KM * lane + j), static_cast<uint32_t>(id[j]));
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+        for (int m = 0; m < KM; ++m) idx[m] = lds_read4r(tbl + 4u * (64 * m + lane));
+        lds_wait_all(idx);
+        // every lane loads (row t0, expert 0 when inactive); the values are
+        // first used after the next block, so nothing waits for them here
+        gon = 0u;
+#pragma unroll
+        for (int m = 0; m < KM; ++m) {
+          const int q = 64 * m + lane, jj = q % KM;
+          const bool on = t0 + q / KM < T && jj < k;
+          const int tok = on ? t0 + q / KM : t0;
+          gv[m] = logits[static_cast<size_t>(tok) * E + (on ? static_cast<int>(idx[m]) : 0)];
+          gon |= (on ? 1u : 0u) << m;
         }
+        asm volatile("" ::: "memory");
         pend = true;
         pt = t;
       }
     }
-    if (pend && pt < T) write_gates(plv, pt);
+    if (pend) finish();   // the last block
   } else {
     __shared__ float s_buf[4][64 * kLaneRow];
     float* buf = s_buf[wave];
