@@ -200,14 +200,14 @@ hipError_t launch_permute(const int32_t* topk_idx, int T, int k, int32_t* bad_fl
                           const PermuteOut& o, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s);
 
 // K2 over many workgroups for large blocks (permute_chunked true): a counting
-// launch over chunks of 512 tokens whose last workgroup plans the layer, then
-// a ranking launch. chunk_base: [permute_chunks(T)][E] ints of scratch;
-// counter: one device int, zero before the first launch (left zero).
+// launch over chunks of 512 tokens, a planning launch of one workgroup, then a
+// ranking launch over the chunks. chunk_base: [permute_chunks(T)][E] ints of
+// scratch.
 bool permute_chunked(int T);
 int permute_chunks(int T);
 hipError_t launch_permute_chunked(const int32_t* topk_idx, int T, int k, int32_t* bad_flag,
-                                  int32_t* chunk_base, int32_t* counter, const PermuteOut& o,
-                                  hipEvent_t ev0, hipEvent_t ev1, hipStream_t s);
+                                  int32_t* chunk_base, const PermuteOut& o, hipEvent_t ev0,
+                                  hipEvent_t ev1, hipStream_t s);
 
 // K2 over B independent blocks of T tokens without a cache (o.cv.hdr null):
 // a counting launch over (chunk, block), a planning launch of one workgroup

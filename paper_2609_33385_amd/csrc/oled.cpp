@@ -104,7 +104,6 @@ struct Ctx {
   int32_t* d_chunk = nullptr;      // [Tmax/512 chunks][E] per-chunk counts / bases (large blocks)
   float* d_logits = nullptr;       // [Tmax][E] logits of route_block_gate's gate GEMM
   int logits_layer = -1;           // the layer they belong to (-1: none)
-  int32_t* d_pcount = nullptr;     // completion counter of the chunked permutation
   unsigned long long* d_sacc = nullptr;  // [E] priority numerators of a many-part scoring
   int32_t* d_ssync = nullptr;      // [2] its completion counter and bad-confidence flag
   WorkItem* d_items = nullptr;
@@ -402,7 +401,7 @@ void free_ctx(Ctx* c) {
                  c->d_dense_counts, c->d_h, c->d_O,
                  c->d_score, c->d_hdr, c->d_slot_of, c->d_res, c->d_res_before,
                  c->d_last_counts, c->d_free, c->d_host_addr, c->d_cap, c->d_stat,
-                 c->d_chunk, c->d_pcount, c->d_sacc, c->d_ssync, c->d_iters, c->d_last_use,
+                 c->d_chunk, c->d_sacc, c->d_ssync, c->d_iters, c->d_last_use,
                  c->d_logits,
                  c->d_freq, c->d_prev_miss, c->d_key};
   for (void* p : dev)
@@ -449,7 +448,6 @@ oled_status init_cache_state(Ctx* c) {
   // counters and accumulators that kernels leave at zero
   HIP_TRY(c, hipMemset(c->d_flag, 0, sizeof(int32_t)));
   HIP_TRY(c, hipMemset(c->d_sync, 0, 2 * sizeof(int32_t)));
-  HIP_TRY(c, hipMemset(c->d_pcount, 0, sizeof(int32_t)));
   HIP_TRY(c, hipMemset(c->d_sacc, 0, sizeof(unsigned long long) * c->E));
   HIP_TRY(c, hipMemset(c->d_ssync, 0, 2 * sizeof(int32_t)));
   HIP_TRY(c, hipDeviceSynchronize());
@@ -1133,7 +1131,7 @@ oled_status oled_create(const oled_config* cfg, void** ctx_out) {
       dev_alloc(&c->d_perm, routes) || dev_alloc(&c->d_inv, routes) || dev_alloc(&c->d_flag, 1) ||
       dev_alloc(&c->d_item_counts, 2) || dev_alloc(&c->d_sync, 2) ||
       dev_alloc(&c->d_chunk, static_cast<size_t>(oled::permute_chunks(c->Tmax)) * c->E) ||
-      dev_alloc(&c->d_pcount, 1) || dev_alloc(&c->d_sacc, c->E) || dev_alloc(&c->d_ssync, 2) ||
+      dev_alloc(&c->d_sacc, c->E) || dev_alloc(&c->d_ssync, 2) ||
       dev_alloc(&c->d_logits, static_cast<size_t>(c->Tmax) * c->E) ||
       dev_alloc(&c->d_items, c->max_items) ||
       (c->dense_ok && (dev_alloc(&c->d_dense_items, c->max_dense) ||
@@ -1153,7 +1151,6 @@ oled_status oled_create(const oled_config* cfg, void** ctx_out) {
   if (hipMemset(c->d_flag, 0, sizeof(int32_t)) != hipSuccess ||
       hipMemset(c->d_item_counts, 0, 2 * sizeof(int32_t)) != hipSuccess ||
       hipMemset(c->d_sync, 0, 2 * sizeof(int32_t)) != hipSuccess ||
-      hipMemset(c->d_pcount, 0, sizeof(int32_t)) != hipSuccess ||
       hipMemset(c->d_sacc, 0, sizeof(unsigned long long) * c->E) != hipSuccess ||
       hipMemset(c->d_ssync, 0, 2 * sizeof(int32_t)) != hipSuccess)
     return oom("scratch init");
@@ -1328,8 +1325,8 @@ oled_status route_impl(Ctx* c, int32_t layer, const float* logits_dev, int32_t T
     }
     OpEvents ev = op_begin(c, OLED_OP_PERMUTE);
     if (oled::permute_chunked(T))
-      HIP_TRY(c, oled::launch_permute_chunked(c->d_topk, T, c->K, c->d_flag, c->d_chunk,
-                                              c->d_pcount, o, ev.a, ev.b, s));
+      HIP_TRY(c, oled::launch_permute_chunked(c->d_topk, T, c->K, c->d_flag, c->d_chunk, o, ev.a,
+                                              ev.b, s));
     else
       HIP_TRY(c, oled::launch_permute(c->d_topk, T, c->K, c->d_flag, o, ev.a, ev.b, s));
     op_end(c, ev, rec(OLED_OP_PERMUTE, layer, perm_bytes));

@@ -888,83 +888,165 @@ __global__ __launch_bounds__(kPermThreads) void k_permute(const int32_t* __restr
   permute_body(topk_idx, T, k, bad, o, s_free, &s_ftop, s_res, s_pm, s_slot);
 }
 
-// Large blocks, first launch: workgroup c counts the routes of tokens
-// [512 c, 512 c + 512) per expert into chunk_base[c][E]; the last workgroup to
-// finish (a fenced counter; nobody waits) plans the layer as permute_body does
-// (totals, offsets, work lists, staging, records) and turns the counts into
-// each chunk's first position per expert.
-__device__ __forceinline__ void perm_hist_body(const int32_t* __restrict__ topk_idx, int T, int k,
-                                               int32_t* __restrict__ bad_flag,
-                                               int32_t* __restrict__ chunk_base,
-                                               int32_t* __restrict__ counter, const PermuteOut& o,
-                                               int ch, int n_chunks) {
-  __shared__ int32_t s_h[kMaxExperts];
+// Large blocks: the routes of chunk c (tokens [512 c, 512 c + 512)) are
+// counted per expert by the counting launch below (k_perm_count_batch over a
+// single block), then one workgroup plans the layer from the per-chunk counts
+// as permute_body does (totals, offsets, work lists, staging, records) and
+// turns the counts into each chunk's first position per expert, then the
+// ranking launch. Three launches in stream order, so no workgroup waits on
+// another and no device-scope fence is needed between them (with the
+// planning done by the last counting workgroup, the fences that ordered the
+// counts cost more than the whole permutation).
+__global__ __launch_bounds__(kPermThreads) void k_perm_plan(const int32_t* __restrict__ topk_idx,
+                                                            int T, int k, int n_chunks,
+                                                            int32_t* __restrict__ bad_flag,
+                                                            int32_t* __restrict__ chunk_base,
+                                                            PermuteOut o) {
   __shared__ int32_t s_free[kMaxExperts];
   __shared__ int32_t s_ftop;
-  __shared__ int32_t s_last;
   __shared__ uint32_t s_res[kMaxExperts / 32], s_pm[kMaxExperts / 32];
   __shared__ int32_t s_slot[kMaxExperts];
-  const int E = o.E, tid = threadIdx.x, nthr = blockDim.x;
-  for (int e = tid; e < kMaxExperts; e += nthr) s_h[e] = 0;
-  // the cache state the last workgroup plans with, read while chunks count
-  if ((tid >> 6) == 1) prefetch_state(o.cv, E, o.layer, s_free, &s_ftop, s_res, s_pm, s_slot);
+  const int bad = *bad_flag;
+  if ((threadIdx.x >> 6) == 1) prefetch_state(o.cv, o.E, o.layer, s_free, &s_ftop, s_res, s_pm, s_slot);
   __syncthreads();
-  const int t0 = ch * kChunkTokens, t1 = min(T, t0 + kChunkTokens);
-  for (int r = t0 * k + tid; r < t1 * k; r += 4 * nthr) {   // 4 loads in flight per thread
-    int e[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) e[u] = r + u * nthr < t1 * k ? topk_idx[r + u * nthr] : -1;
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (e[u] >= 0) atomicAdd(&s_h[e[u]], 1);
-  }
-  __syncthreads();
-  for (int e = tid; e < E; e += nthr) chunk_base[static_cast<size_t>(ch) * E + e] = s_h[e];
-  __threadfence();   // this chunk's counts are visible device-wide
-  __syncthreads();
-  if (tid == 0) s_last = atomicAdd(counter, 1) == n_chunks - 1;
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();   // see every other chunk's counts
-  const int bad = __hip_atomic_load(bad_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  if (tid == 0) {   // re-arm for the next launch (stream order)
-    *bad_flag = 0;
-    *counter = 0;
-  }
+  if (threadIdx.x == 0) *bad_flag = 0;   // re-armed for the next top-k launch (stream order)
   permute_body(topk_idx, T, k, bad, o, s_free, &s_ftop, s_res, s_pm, s_slot, chunk_base, n_chunks);
 }
 
-__global__ __launch_bounds__(kPermThreads) void k_perm_hist(const int32_t* __restrict__ topk_idx,
-                                                            int T, int k,
-                                                            int32_t* __restrict__ bad_flag,
-                                                            int32_t* __restrict__ chunk_base,
-                                                            int32_t* __restrict__ counter,
-                                                            PermuteOut o) {
-  perm_hist_body(topk_idx, T, k, bad_flag, chunk_base, counter, o, blockIdx.x, gridDim.x);
-}
+// Large blocks, second launch: workgroup c ranks the routes of chunk c from
+// its first positions per expert (chunk_base[c][e]). Thread i takes token
+// i / 2 of the chunk and half (i % 2) of its routes, loaded once into
+// registers. The per-expert token bitmasks sit in rows of kMaskStride = 17
+// words (16 words of 32 tokens, one pad word): the lanes of a wavefront, one
+// 32-token word apart in token order and scattered over experts, then fall in
+// distinct LDS banks (with 16-word rows every expert row began in one of two
+// banks). Each route's rank among the chunk's routes to its expert also
+// places it in a counting sort of the chunk by expert in LDS, so perm is
+// written in contiguous runs per expert (positions s_run[e] + rank) by
+// consecutive lanes instead of one scattered store per lane. Stores go
+// through buffer resources of T*k entries: positions outside are dropped.
+constexpr int kMaskStride = kChunkWords + 1;
+constexpr int kMaskRows = kMaxExperts + 1;     // + a row that missing routes target
+constexpr int kRouteBits = 13;                 // chunk-local route index
+static_assert(kChunkTokens * kMaxTopK <= 1 << kRouteBits, "chunk-local routes fit 13 bits");
+static_assert(kPermThreads == 2 * kChunkTokens, "two threads per token of a chunk");
 
-// Large blocks, second launch: workgroup c ranks the routes of its chunk from
-// the chunk's first positions per expert.
+template <int KH>
 __device__ __forceinline__ void perm_rank_body(const int32_t* __restrict__ topk_idx, int T, int k,
                                                int E, const int32_t* __restrict__ chunk_base,
                                                int32_t* __restrict__ perm,
                                                int32_t* __restrict__ inv_perm, int ch) {
-  __shared__ uint32_t s_mask[kMaxExperts * kChunkWords];
-  __shared__ int32_t s_pre[kMaxExperts * kChunkWords];
+  static_assert(2 * KH <= kMaxTopK && 2 * KH >= 4, "routes per thread");
+  __shared__ uint32_t s_mask[kMaskRows * kMaskStride];
+  __shared__ int32_t s_pre[kMaskRows * kMaskStride];
   __shared__ int32_t s_run[kMaxExperts];
-  for (int e = threadIdx.x; e < E; e += blockDim.x)
-    s_run[e] = chunk_base[static_cast<size_t>(ch) * E + e];
-  const int t0 = ch * kChunkTokens;
-  rank_chunk(topk_idx, t0, min(T, t0 + kChunkTokens), k, E, T * k, s_mask, s_pre, s_run, perm,
-             inv_perm);
+  __shared__ int32_t s_first[kMaxExperts];
+  __shared__ int32_t s_sorted[kChunkTokens * kMaxTopK];
+  const int tid = threadIdx.x, lt = tid >> 1;
+  const int kh = (k + 1) >> 1, j0 = (tid & 1) * kh, nj = min(kh, k - j0);
+  const int t0 = ch * kChunkTokens, t = t0 + lt;
+  const bool tok = t < T;
+  const int nr = (min(T, t0 + kChunkTokens) - t0) * k;
+  const int rl = lt * k + j0;                  // chunk-local route of this thread's first slot
+  const size_t r0 = static_cast<size_t>(t0) * k;
+  // the common case, k = 8 on 16-byte aligned arrays: one 16-byte load and store per thread
+  const bool vec = KH == 4 && k == 8 &&
+                   ((reinterpret_cast<uintptr_t>(topk_idx) | reinterpret_cast<uintptr_t>(inv_perm)) &
+                    15) == 0;
+  int ev[KH];
+  if (vec) {
+    const int4 v = tok ? *reinterpret_cast<const int4*>(topk_idx + r0 + rl) : make_int4(-1, -1, -1, -1);
+    ev[0] = v.x;
+    ev[1] = v.y;
+    ev[2] = v.z;
+    ev[3] = v.w;
+  } else {
+#pragma unroll
+    for (int u = 0; u < KH; ++u) ev[u] = tok && u < nj ? topk_idx[r0 + rl + u] : -1;
+  }
+  const int run = tid < E ? chunk_base[static_cast<size_t>(ch) * E + tid] : 0;
+  const uint32_t bit = 1u << (lt & 31);
+  const int wofs = lt >> 5;
+  const int spare = kMaxExperts * kMaskStride;
+  int a[KH];
+#pragma unroll
+  for (int u = 0; u < KH; ++u) a[u] = ev[u] >= 0 && ev[u] < E ? ev[u] * kMaskStride + wofs : spare;
+
+  for (int i = tid; i < kMaskRows * kMaskStride; i += kPermThreads) s_mask[i] = 0u;
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < KH; ++u) atomicOr(&s_mask[a[u]], bit);
+  if (tid < E) s_run[tid] = run;
+  __syncthreads();
+  // word w of expert e is lane w of a 16-lane row: the chunk-local prefix of
+  // the expert's words, and its chunk total at the row's last lane
+  for (int i = tid; i < ((E * kChunkWords + 63) & ~63); i += kPermThreads) {
+    const int e = i / kChunkWords, w = i & (kChunkWords - 1);
+    const int cnt = e < E ? __popc(s_mask[e * kMaskStride + w]) : 0;
+    const int incl = row16_incl_scan(cnt);
+    if (e < E) {
+      s_pre[e * kMaskStride + w] = incl - cnt;
+      if (w == kChunkWords - 1) s_first[e] = incl;
+    }
+  }
+  __syncthreads();
+  if (tid < 64) {   // the experts' first chunk-local positions: one wavefront, 4 experts a lane
+    int c[4], sum = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = 4 * tid + q;
+      c[q] = e < E ? s_first[e] : 0;
+      sum += c[q];
+    }
+    int first = wave_incl_scan(sum) - sum;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = 4 * tid + q;
+      if (e < E) s_first[e] = first;
+      first += c[q];
+    }
+  }
+  __syncthreads();
+  const int n_routes = T * k;
+  int pv[KH];
+  uint32_t mv[KH];
+#pragma unroll
+  for (int u = 0; u < KH; ++u) {
+    pv[u] = s_pre[a[u]];
+    mv[u] = s_mask[a[u]];
+  }
+  const __amdgpu_buffer_rsrc_t rinv =
+      __builtin_amdgcn_make_buffer_rsrc(inv_perm, 0, n_routes * 4, kRouteBufferFlags);
+#pragma unroll
+  for (int u = 0; u < KH; ++u) {
+    const bool ok = a[u] != spare;
+    const int e = ok ? ev[u] : 0;
+    const int local = pv[u] + __popc(mv[u] & (bit - 1u));
+    pv[u] = s_run[e] + local;
+    if (ok) s_sorted[s_first[e] + local] = (e << kRouteBits) | (rl + u);
+    if (!vec && ok)
+      __builtin_amdgcn_raw_buffer_store_b32(pv[u], rinv, static_cast<int>(r0 + rl + u) * 4, 0, 0);
+  }
+  if (vec && tok)
+    *reinterpret_cast<int4*>(inv_perm + r0 + rl) = make_int4(pv[0], pv[1], pv[2], pv[3]);
+  __syncthreads();
+  const __amdgpu_buffer_rsrc_t rperm =
+      __builtin_amdgcn_make_buffer_rsrc(perm, 0, n_routes * 4, kRouteBufferFlags);
+  for (int p = tid; p < nr; p += kPermThreads) {
+    const int v = s_sorted[p];
+    const int e = (v >> kRouteBits) & (kMaxExperts - 1);
+    __builtin_amdgcn_raw_buffer_store_b32(static_cast<int>(r0) + (v & ((1 << kRouteBits) - 1)),
+                                          rperm, (s_run[e] + p - s_first[e]) * 4, 0, 0);
+  }
 }
 
+template <int KH>
 __global__ __launch_bounds__(kPermThreads) void k_perm_rank(const int32_t* __restrict__ topk_idx,
                                                             int T, int k, int E,
                                                             const int32_t* __restrict__ chunk_base,
                                                             int32_t* __restrict__ perm,
                                                             int32_t* __restrict__ inv_perm) {
-  perm_rank_body(topk_idx, T, k, E, chunk_base, perm, inv_perm, blockIdx.x);
+  perm_rank_body<KH>(topk_idx, T, k, E, chunk_base, perm, inv_perm, blockIdx.x);
 }
 
 // Many independent blocks of T tokens (no cache), in three launches with no
@@ -1018,15 +1100,16 @@ __global__ __launch_bounds__(kPermThreads) void k_perm_plan_batch(
 }
 
 // Third: workgroup (c, b) ranks chunk c of block b from its first positions.
+template <int KH>
 __global__ __launch_bounds__(kPermThreads) void k_perm_rank_batch(
     const int32_t* __restrict__ topk_idx, int T, int k, int E,
     const int32_t* __restrict__ chunk_base, int32_t* __restrict__ perm,
     int32_t* __restrict__ inv_perm) {
   const int b = blockIdx.y;
   const size_t R = static_cast<size_t>(T) * k;
-  perm_rank_body(topk_idx + b * R, T, k, E,
-                 chunk_base + static_cast<size_t>(b) * gridDim.x * E, perm + b * R,
-                 inv_perm + b * R, blockIdx.x);
+  perm_rank_body<KH>(topk_idx + b * R, T, k, E,
+                     chunk_base + static_cast<size_t>(b) * gridDim.x * E, perm + b * R,
+                     inv_perm + b * R, blockIdx.x);
 }
 
 // Small blocks (T*k <= 1024): routing on many CUs, one token per wavefront,
@@ -1448,18 +1531,23 @@ hipError_t launch_route_topk(const float* logits, int T, int E, int k, int32_t* 
     const int blocks = (T + 255) / 256;
     // DMA streaming: whole 32-expert chunks, byte offsets of every row the
     // wavefronts touch within a 32-bit buffer offset; one grid of two
-    // workgroups per CU whose wavefronts take blocks of 64 tokens in turn
-    const bool dma = E % 32 == 0 && E <= 256 &&
+    // workgroups per CU whose wavefronts take blocks of 64 tokens in turn.
+    // Up to k = 8 (the streamed form's gathers for k = 16 hold 179 VGPRs and
+    // take the compiler minutes; k = 16 stages through registers)
+    const bool dma = k <= 8 && E % 32 == 0 && E <= 256 &&
                      static_cast<int64_t>((T + 63) / 64) * 64 * E * 4 <= INT32_MAX;
     const int grid = dma ? (blocks < kRouteStreamGrid ? blocks : kRouteStreamGrid) : blocks;
     auto go = [&](auto kp, auto km) {
       constexpr int KP = decltype(kp)::value, KM = decltype(km)::value;
-      if (dma)
-        hipExtLaunchKernelGGL(k_route_lanes<KP, KM, true>, dim3(grid), dim3(256), 0, s, ev0, ev1,
-                              0, logits, T, E, k, topk_idx, gates, bad_flag, Tb);
-      else
-        hipExtLaunchKernelGGL(k_route_lanes<KP, KM, false>, dim3(blocks), dim3(256), 0, s, ev0, ev1,
-                              0, logits, T, E, k, topk_idx, gates, bad_flag, Tb);
+      if constexpr (KM <= 8) {
+        if (dma) {
+          hipExtLaunchKernelGGL(k_route_lanes<KP, KM, true>, dim3(grid), dim3(256), 0, s, ev0,
+                                ev1, 0, logits, T, E, k, topk_idx, gates, bad_flag, Tb);
+          return;
+        }
+      }
+      hipExtLaunchKernelGGL(k_route_lanes<KP, KM, false>, dim3(blocks), dim3(256), 0, s, ev0, ev1,
+                            0, logits, T, E, k, topk_idx, gates, bad_flag, Tb);
     };
     using std::integral_constant;
     if (k <= 2) go(integral_constant<int, 3>{}, integral_constant<int, 2>{});
@@ -1489,15 +1577,23 @@ hipError_t launch_permute(const int32_t* topk_idx, int T, int k, int32_t* bad_fl
 }
 
 hipError_t launch_permute_chunked(const int32_t* topk_idx, int T, int k, int32_t* bad_flag,
-                                  int32_t* chunk_base, int32_t* counter, const PermuteOut& o,
-                                  hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
+                                  int32_t* chunk_base, const PermuteOut& o, hipEvent_t ev0,
+                                  hipEvent_t ev1, hipStream_t s) {
   const int n = permute_chunks(T);
-  hipExtLaunchKernelGGL(k_perm_hist, dim3(n), dim3(kPermThreads), 0, s, ev0, nullptr, 0, topk_idx,
-                        T, k, bad_flag, chunk_base, counter, o);
+  hipExtLaunchKernelGGL(k_perm_count_batch, dim3(n, 1), dim3(256), 0, s, ev0, nullptr, 0, topk_idx,
+                        T, k, o.E, chunk_base);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipExtLaunchKernelGGL(k_perm_rank, dim3(n), dim3(kPermThreads), 0, s, nullptr, ev1, 0, topk_idx,
-                        T, k, o.E, chunk_base, o.perm, o.inv_perm);
+  hipLaunchKernelGGL(k_perm_plan, dim3(1), dim3(kPermThreads), 0, s, topk_idx, T, k, n, bad_flag,
+                     chunk_base, o);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (k <= 8)
+    hipExtLaunchKernelGGL(k_perm_rank<4>, dim3(n), dim3(kPermThreads), 0, s, nullptr, ev1, 0,
+                          topk_idx, T, k, o.E, chunk_base, o.perm, o.inv_perm);
+  else
+    hipExtLaunchKernelGGL(k_perm_rank<8>, dim3(n), dim3(kPermThreads), 0, s, nullptr, ev1, 0,
+                          topk_idx, T, k, o.E, chunk_base, o.perm, o.inv_perm);
   return hipGetLastError();
 }
 
@@ -1513,8 +1609,12 @@ hipError_t launch_permute_batch(const int32_t* topk_idx, int B, int T, int k,
                      bad_flag, chunk_base, o);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_perm_rank_batch, dim3(n, B), dim3(kPermThreads), 0, s, topk_idx, T, k, o.E,
-                     chunk_base, o.perm, o.inv_perm);
+  if (k <= 8)
+    hipLaunchKernelGGL(k_perm_rank_batch<4>, dim3(n, B), dim3(kPermThreads), 0, s, topk_idx, T, k,
+                       o.E, chunk_base, o.perm, o.inv_perm);
+  else
+    hipLaunchKernelGGL(k_perm_rank_batch<8>, dim3(n, B), dim3(kPermThreads), 0, s, topk_idx, T, k,
+                       o.E, chunk_base, o.perm, o.inv_perm);
   return hipGetLastError();
 }
 
@@ -1547,9 +1647,9 @@ namespace {
 
 constexpr int kNoAllocMaxTokens = 65535;
 constexpr int kNoAllocChunks = (kNoAllocMaxTokens + oled::kChunkTokens - 1) / oled::kChunkTokens;
-// int32 layout: [0] non-finite flag of the top-k launch, [1] completion
-// counter of the counting launch, [2..3] completion counter and flag of the
-// fused launch, [64, 64 + kNoAllocChunks * kMaxExperts) per-chunk counts.
+// int32 layout: [0] non-finite flag of the top-k launch, [1] unused, [2..3]
+// completion counter and flag of the fused launch, [64, 64 + kNoAllocChunks *
+// kMaxExperts) per-chunk counts.
 constexpr int kScratchHead = 64;
 constexpr int kScratchInts = kScratchHead + kNoAllocChunks * oled::kMaxExperts;
 constexpr int kMaxDevices = 64;
@@ -1638,7 +1738,7 @@ extern "C" oled_status oled_route_noalloc(const float* logits_dev, int32_t T, in
                                 nullptr, s);
     if (e == hipSuccess) {
       if (oled::permute_chunked(T))
-        e = oled::launch_permute_chunked(topk_idx_dev, T, k, sc, sc + kScratchHead, sc + 1, o,
+        e = oled::launch_permute_chunked(topk_idx_dev, T, k, sc, sc + kScratchHead, o,
                                          nullptr, nullptr, s);
       else
         e = oled::launch_permute(topk_idx_dev, T, k, sc, o, nullptr, nullptr, s);

@@ -164,7 +164,7 @@ hipError_t launch_permute(const int32_t*, int T, int k, int32_t*, const PermuteO
   publish_route(T, k, o);
   return hipSuccess;
 }
-hipError_t launch_permute_chunked(const int32_t*, int T, int k, int32_t*, int32_t*, int32_t*,
+hipError_t launch_permute_chunked(const int32_t*, int T, int k, int32_t*, int32_t*,
                                   const PermuteOut& o, hipEvent_t, hipEvent_t, hipStream_t) {
   publish_route(T, k, o);
   return hipSuccess;

@@ -75,8 +75,9 @@ def _check_block(got, b, lg_b, k, where):
 
 @pytest.mark.parametrize("B,T,E,k", [(4, 3000, 128, 8), (3, 100, 200, 3), (5, 513, 64, 6),
                                      (2, 1, 8, 2),
-                                     # streamed top-k (E a multiple of 32): one, three and
-                                     # eight 32-expert chunks, k = 16; register staging at E = 48
+                                     # streamed top-k (E a multiple of 32, k <= 8): one and
+                                     # eight 32-expert chunks; register staging at k = 16
+                                     # (E = 96) and at E = 48
                                      (2, 2500, 32, 4), (2, 1100, 96, 16), (2, 1500, 256, 8),
                                      (2, 1300, 48, 8)])
 def test_route_batch_against_oracle(B, T, E, k):
