@@ -272,7 +272,7 @@ struct ScoreArgs {
   uint64_t* key_out;      // [E] retention key of each expert (S under the priority policy)
   int parts;              // scoring workgroups: score_parts(T, k)
   unsigned long long* acc;  // [E] zero between launches (several parts only)
-  int32_t* acc_sync;        // [2] completion counter, bad flag; zero between launches
+  int32_t* acc_sync;        // [2]: unused, non-finite confidence flag; zero between layers
   int reject = 0;         // 1: commit nothing (R stays, staged misses return their slots);
                           // with T = 0 no route or confidence is read
 };
@@ -290,6 +290,8 @@ struct CombineArgs {
   void* y;
 };
 
+// K6; blocks of more than 8192 routes (a.parts > 1) take a second, one-workgroup
+// commit launch (ev1 is recorded after it).
 hipError_t launch_score_retain(const ScoreArgs& a, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s);
 
 // Layer-adaptive re-sizing of every layer's capacity from the smoothed
@@ -312,7 +314,7 @@ void set_noctx_error(const char* msg);
 hipError_t launch_coop_unstage(const CacheView& cv, int layer, int E, const ExpertMask& cpu,
                                hipStream_t s);
 
-// K5 and K6 in one launch (the layer's last).
+// K5 and K6 in one launch (the layer's last), plus the commit launch when a.parts > 1.
 hipError_t launch_combine_score(bool bf16, const CombineArgs& c, const ScoreArgs& a,
                                 hipEvent_t ev0, hipEvent_t ev1, hipStream_t s);
 

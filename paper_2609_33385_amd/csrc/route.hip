@@ -465,52 +465,64 @@ constexpr int kPermThreads = 1024;
 constexpr int kChunkWords = 16;               // bitmask words per expert per chunk
 static_assert(kChunkWords == 16, "the ranking's per-expert prefix is a 16-lane row scan");
 constexpr int kChunkTokens = kChunkWords * 32;
+// Per-expert token bitmasks of a chunk: rows of kMaskStride = 17 words (16
+// words of 32 tokens, one pad word). The lanes of a wavefront share a 32-token
+// word and scatter over experts; with 17-word rows they fall in distinct LDS
+// banks (with 16-word rows every expert's row began in one of two banks).
+constexpr int kMaskStride = kChunkWords + 1;
+constexpr int kMaskRows = kMaxExperts + 1;     // + a row that missing routes target
+constexpr int kMaskSpare = kMaxExperts * kMaskStride;
+constexpr int kRouteBits = 13;                 // chunk-local route index
+static_assert(kChunkTokens * kMaxTopK <= 1 << kRouteBits, "chunk-local routes fit 13 bits");
+static_assert(kPermThreads == 2 * kChunkTokens, "two threads per token of a chunk");
 
 constexpr int kFusedMaxRoutes = 1024;       // fused routing path: T * k routes kept in LDS
 constexpr int kLaneTokensMin = 1024;        // blocks of more tokens route one token per lane
 constexpr int kRouteStreamGrid = 512;       // DMA-streamed top-k: two workgroups per CU
 constexpr int kGateFullGrid = 256;          // gate GEMM workgroups that fill the compute units
 constexpr int kChunkedMinTokens = 1024;     // and permute over many workgroups
+constexpr int kMaxChunks = 128;             // chunked permutation: T <= 65535 tokens
+// chunks per planning thread: kMaxChunks over the fewest groups (E = 256 at kPermThreads)
+constexpr int kPlanPer = kMaxChunks / (kPermThreads / kMaxExperts);
 
 // Stable positions of the routes of tokens [t0, t1) (at most kChunkTokens):
 // a per-expert bitmask of the chunk's tokens that chose the expert (LDS
-// atomics), a running popcount prefix per 32-token word from the expert's
-// base s_run[e], and each route's position = that prefix + the tokens of its
-// word below it (positions outside [0, n_routes) are dropped). Advances s_run
-// past the chunk. Every thread of the workgroup takes part.
+// atomics into kMaskStride-word rows), a running popcount prefix per 32-token
+// word from the expert's base s_run[e], and each route's position = that
+// prefix + the tokens of its word below it (positions outside [0, n_routes)
+// are dropped). Advances s_run past the chunk. Every thread of the workgroup
+// takes part (any workgroup size).
 __device__ __forceinline__ void rank_chunk(const int32_t* idx, int t0, int t1, int k, int E,
                                            int n_routes,
                                            uint32_t* s_mask, int32_t* s_pre, int32_t* s_run,
                                            int32_t* __restrict__ perm,
                                            int32_t* __restrict__ inv_perm) {
   const int tid = threadIdx.x, nthr = blockDim.x;
-  for (int i = tid; i < E * kChunkWords; i += nthr) s_mask[i] = 0u;
+  for (int i = tid; i < kMaskRows * kMaskStride; i += nthr) s_mask[i] = 0u;
   __syncthreads();
   for (int r = t0 * k + tid; r < t1 * k; r += nthr) {
     const int e = idx[r];
     const int lt = r / k - t0;
-    atomicOr(&s_mask[e * kChunkWords + (lt >> 5)], 1u << (lt & 31));
+    atomicOr(&s_mask[e * kMaskStride + (lt >> 5)], 1u << (lt & 31));
   }
   __syncthreads();
-  // word w of expert e is lane w of a 16-lane row: the popcount prefix over
-  // the expert's words is a row scan (whole wavefronts take part)
   for (int i = tid; i < ((E * kChunkWords + 63) & ~63); i += nthr) {
-    const int e = i / kChunkWords;
-    const int c = e < E ? __popc(s_mask[i]) : 0;
+    const int e = i / kChunkWords, w = i & (kChunkWords - 1);
+    const int c = e < E ? __popc(s_mask[e * kMaskStride + w]) : 0;
     const int incl = row16_incl_scan(c);
     if (e < E) {
       const int run = s_run[e];
-      s_pre[i] = run + incl - c;
-      if (i % kChunkWords == kChunkWords - 1) s_run[e] = run + incl;
+      s_pre[e * kMaskStride + w] = run + incl - c;
+      if (w == kChunkWords - 1) s_run[e] = run + incl;
     }
   }
   __syncthreads();
   for (int r = t0 * k + tid; r < t1 * k; r += nthr) {
     const int e = idx[r];
     const int lt = r / k - t0;
-    const int w = lt >> 5;
-    const uint32_t below = s_mask[e * kChunkWords + w] & ((1u << (lt & 31)) - 1u);
-    const int pos = s_pre[e * kChunkWords + w] + __popc(below);
+    const int w = e * kMaskStride + (lt >> 5);
+    const uint32_t below = s_mask[w] & ((1u << (lt & 31)) - 1u);
+    const int pos = s_pre[w] + __popc(below);
     if (pos >= 0 && pos < n_routes) {
       perm[pos] = r;
       inv_perm[r] = pos;
@@ -545,8 +557,8 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
   __shared__ int32_t s_dshort[kMaxExperts];  // its short dense item, or -1
   __shared__ int32_t s_sexp[kMaxExperts];
   __shared__ int32_t s_sslot[kMaxExperts];
-  __shared__ uint32_t s_mask[kMaxExperts * kChunkWords];
-  __shared__ int32_t s_pre[kMaxExperts * kChunkWords];
+  __shared__ uint32_t s_mask[kMaskRows * kMaskStride];
+  __shared__ int32_t s_pre[kMaskRows * kMaskStride];
 
   const int tid = threadIdx.x;
   const int nthr = blockDim.x;
@@ -555,24 +567,26 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
   const bool cache = o.cv.hdr != nullptr;   // else routing and permutation only
   for (int e = tid; e < kMaxExperts; e += nthr) s_cnt[e] = 0;
   __syncthreads();
-  // Chunked: counts per chunk in chunk_base [n_chunks][E], from other
-  // workgroups. G threads per expert each take a contiguous run of chunks
-  // (short chains of dependent loads); their partial sums stay in s_pre
-  // (g * E + e), which the chunked path does not otherwise use, for the
-  // per-chunk bases at the end.
+  // Chunked: counts per chunk in chunk_base [n_chunks][E], from an earlier
+  // launch. G threads per expert each take a contiguous run of at most
+  // kPlanPer chunks, loaded at once into registers (kept for the per-chunk
+  // bases at the end); their partial sums stay in s_pre (g * E + e), which the
+  // chunked path does not otherwise use.
   const int G = chunk_base ? max(1, min(nthr / E, n_chunks)) : 1;
   const int per = chunk_base ? (n_chunks + G - 1) / G : 0;
+  const int my_g = chunk_base && tid < G * E ? tid / E : -1;
+  const int my_e = my_g >= 0 ? tid - my_g * E : 0;
+  const int ch_lo = my_g >= 0 ? my_g * per : 0;
+  const int ch_hi = my_g >= 0 ? min(n_chunks, ch_lo + per) : 0;
+  int cc[kPlanPer];
   if (chunk_base) {
-    for (int i = tid; i < G * E; i += nthr) {
-      const int g = i / E, e = i - g * E;
-      const int c1 = min(n_chunks, (g + 1) * per);
-      int c = 0;
-#pragma unroll 4
-      for (int ch = g * per; ch < c1; ++ch)
-        c += __hip_atomic_load(chunk_base + static_cast<size_t>(ch) * E + e, __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
-      s_pre[i] = c;
+    int c = 0;
+#pragma unroll
+    for (int q = 0; q < kPlanPer; ++q) {
+      cc[q] = ch_lo + q < ch_hi ? chunk_base[static_cast<size_t>(ch_lo + q) * E + my_e] : 0;
+      c += cc[q];
     }
+    if (my_g >= 0) s_pre[tid] = c;
     __syncthreads();
     for (int e = tid; e < E; e += nthr) {
       int c = 0;
@@ -760,24 +774,15 @@ __device__ __forceinline__ void permute_body(const int32_t* idx, int T, int k, i
   if (tid == 0) o.offsets[E] = s_off[E];
 
   if (chunk_base) {   // per-chunk bases for the ranking launch: exclusive scan over chunks
-    for (int i = tid; i < G * E; i += nthr) {
-      const int g = i / E, e = i - g * E;
-      int run = s_off[e];
-      for (int h = 0; h < g; ++h) run += s_pre[h * E + e];
-      const int c1 = min(n_chunks, (g + 1) * per);
-      for (int ch = g * per; ch < c1; ch += 4) {   // 4 counts read, then 4 bases written
-        int c[4];
+    if (my_g >= 0) {
+      int run = s_off[my_e];
+      for (int h = 0; h < my_g; ++h) run += s_pre[h * E + my_e];
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
-          c[u] = ch + u < c1 ? __hip_atomic_load(chunk_base + static_cast<size_t>(ch + u) * E + e,
-                                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
-                             : 0;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          if (ch + u < c1) chunk_base[static_cast<size_t>(ch + u) * E + e] = run;
-          run += c[u];
+      for (int q = 0; q < kPlanPer; ++q)
+        if (ch_lo + q < ch_hi) {
+          chunk_base[static_cast<size_t>(ch_lo + q) * E + my_e] = run;
+          run += cc[q];
         }
-      }
     }
   } else {
     for (int t0 = 0; t0 < T; t0 += kChunkTokens)
@@ -925,11 +930,6 @@ __global__ __launch_bounds__(kPermThreads) void k_perm_plan(const int32_t* __res
 // written in contiguous runs per expert (positions s_run[e] + rank) by
 // consecutive lanes instead of one scattered store per lane. Stores go
 // through buffer resources of T*k entries: positions outside are dropped.
-constexpr int kMaskStride = kChunkWords + 1;
-constexpr int kMaskRows = kMaxExperts + 1;     // + a row that missing routes target
-constexpr int kRouteBits = 13;                 // chunk-local route index
-static_assert(kChunkTokens * kMaxTopK <= 1 << kRouteBits, "chunk-local routes fit 13 bits");
-static_assert(kPermThreads == 2 * kChunkTokens, "two threads per token of a chunk");
 
 template <int KH>
 __device__ __forceinline__ void perm_rank_body(const int32_t* __restrict__ topk_idx, int T, int k,
@@ -967,10 +967,9 @@ __device__ __forceinline__ void perm_rank_body(const int32_t* __restrict__ topk_
   const int run = tid < E ? chunk_base[static_cast<size_t>(ch) * E + tid] : 0;
   const uint32_t bit = 1u << (lt & 31);
   const int wofs = lt >> 5;
-  const int spare = kMaxExperts * kMaskStride;
   int a[KH];
 #pragma unroll
-  for (int u = 0; u < KH; ++u) a[u] = ev[u] >= 0 && ev[u] < E ? ev[u] * kMaskStride + wofs : spare;
+  for (int u = 0; u < KH; ++u) a[u] = ev[u] >= 0 && ev[u] < E ? ev[u] * kMaskStride + wofs : kMaskSpare;
 
   for (int i = tid; i < kMaskRows * kMaskStride; i += kPermThreads) s_mask[i] = 0u;
   __syncthreads();
@@ -1019,7 +1018,7 @@ __device__ __forceinline__ void perm_rank_body(const int32_t* __restrict__ topk_
       __builtin_amdgcn_make_buffer_rsrc(inv_perm, 0, n_routes * 4, kRouteBufferFlags);
 #pragma unroll
   for (int u = 0; u < KH; ++u) {
-    const bool ok = a[u] != spare;
+    const bool ok = a[u] != kMaskSpare;
     const int e = ok ? ev[u] : 0;
     const int local = pv[u] + __popc(mv[u] & (bit - 1u));
     pv[u] = s_run[e] + local;
@@ -1580,6 +1579,7 @@ hipError_t launch_permute_chunked(const int32_t* topk_idx, int T, int k, int32_t
                                   int32_t* chunk_base, const PermuteOut& o, hipEvent_t ev0,
                                   hipEvent_t ev1, hipStream_t s) {
   const int n = permute_chunks(T);
+  if (n > kMaxChunks) return hipErrorInvalidValue;   // the planning keeps kPlanPer counts a thread
   hipExtLaunchKernelGGL(k_perm_count_batch, dim3(n, 1), dim3(256), 0, s, ev0, nullptr, 0, topk_idx,
                         T, k, o.E, chunk_base);
   hipError_t e = hipGetLastError();
@@ -1601,6 +1601,7 @@ hipError_t launch_permute_batch(const int32_t* topk_idx, int B, int T, int k,
                                 const int32_t* bad_flag, int32_t* chunk_base, const PermuteOut& o,
                                 hipStream_t s) {
   const int n = permute_chunks(T);
+  if (n > kMaxChunks) return hipErrorInvalidValue;   // the planning keeps kPlanPer counts a thread
   hipLaunchKernelGGL(k_perm_count_batch, dim3(n, B), dim3(256), 0, s, topk_idx, T, k, o.E,
                      chunk_base);
   hipError_t e = hipGetLastError();

@@ -301,14 +301,14 @@ __device__ __forceinline__ void combine_body(const CombineArgs& c, int t, int hb
 // Priority numerators and retention of one layer by the first a.parts
 // workgroups of a launch. One part: that workgroup sums every route and
 // commits. Several parts (large blocks): part p sums routes [p*n, (p+1)*n)
-// (n = kScoreRoutes) into LDS, adds its nonzero numerators to the device
-// accumulators with integer atomics (any order, same bits), and the last part
-// to finish (a fenced counter; nobody waits) reads the totals, re-arms the
-// accumulators and commits.
+// (n = kScoreRoutes) into LDS and adds its nonzero numerators to the device
+// accumulators with integer atomics (any order, same bits); a second launch
+// of one workgroup (k_score_commit) reads the totals, re-arms the
+// accumulators and commits. Two launches in stream order: no workgroup waits
+// on another and no device-scope fence orders the sums.
 __device__ __forceinline__ void score_part(const ScoreArgs& a, int part) {
   __shared__ unsigned long long s_S[kMaxExperts];
   __shared__ int32_t s_bad;
-  __shared__ int32_t s_last;
   __shared__ ScoreState st;
   const int tid = threadIdx.x, E = a.E;
   const int R = a.T * a.k;
@@ -328,19 +328,21 @@ __device__ __forceinline__ void score_part(const ScoreArgs& a, int part) {
   for (int e = tid; e < E; e += kThreads)
     if (s_S[e]) atomicAdd(&a.acc[e], s_S[e]);
   if (tid == 0 && s_bad) atomicOr(&a.acc_sync[1], 1);
-  __threadfence();   // this part's sums are visible device-wide
-  __syncthreads();
-  if (tid == 0) s_last = atomicAdd(&a.acc_sync[0], 1) == a.parts - 1;
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();   // see every other part's sums
-  for (int e = tid; e < E; e += kThreads) {
-    s_S[e] = __hip_atomic_load(&a.acc[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    a.acc[e] = 0ull;   // re-arm for the next launch (stream order)
+}
+
+// Several parts, second launch: the totals of every part, the accumulators
+// re-armed for the next layer (stream order), the commit.
+__global__ __launch_bounds__(kThreads) void k_score_commit(ScoreArgs a) {
+  __shared__ unsigned long long s_S[kMaxExperts];
+  __shared__ int32_t s_bad;
+  __shared__ ScoreState st;
+  const int tid = threadIdx.x, E = a.E;
+  for (int e = tid; e < kMaxExperts; e += kThreads) {
+    s_S[e] = e < E ? a.acc[e] : 0ull;
+    if (e < E) a.acc[e] = 0ull;
   }
   if (tid == 0) {
-    s_bad = __hip_atomic_load(&a.acc_sync[1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    a.acc_sync[0] = 0;
+    s_bad = a.acc_sync[1];
     a.acc_sync[1] = 0;
   }
   score_prefetch(a, st);
@@ -571,7 +573,13 @@ int score_parts(int T, int k) {
 
 hipError_t launch_score_retain(const ScoreArgs& a, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
   if (a.parts != score_parts(a.T, a.k)) return hipErrorInvalidValue;
-  hipExtLaunchKernelGGL(k_score_retain, dim3(a.parts), dim3(kThreads), 0, s, ev0, ev1, 0, a);
+  const bool split = a.parts > 1;
+  hipExtLaunchKernelGGL(k_score_retain, dim3(a.parts), dim3(kThreads), 0, s, ev0,
+                        split ? nullptr : ev1, 0, a);
+  if (!split) return hipGetLastError();
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipExtLaunchKernelGGL(k_score_commit, dim3(1), dim3(kThreads), 0, s, nullptr, ev1, 0, a);
   return hipGetLastError();
 }
 
@@ -579,10 +587,17 @@ hipError_t launch_combine_score(bool bf16, const CombineArgs& c, const ScoreArgs
                                 hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
   if (a.parts != score_parts(a.T, a.k)) return hipErrorInvalidValue;
   const int grid = a.parts + c.T * ((c.H + 1023) / 1024);
+  const bool split = a.parts > 1;
   if (bf16)
-    hipExtLaunchKernelGGL(k_combine_score<true>, dim3(grid), dim3(kThreads), 0, s, ev0, ev1, 0, c, a);
+    hipExtLaunchKernelGGL(k_combine_score<true>, dim3(grid), dim3(kThreads), 0, s, ev0,
+                          split ? nullptr : ev1, 0, c, a);
   else
-    hipExtLaunchKernelGGL(k_combine_score<false>, dim3(grid), dim3(kThreads), 0, s, ev0, ev1, 0, c, a);
+    hipExtLaunchKernelGGL(k_combine_score<false>, dim3(grid), dim3(kThreads), 0, s, ev0,
+                          split ? nullptr : ev1, 0, c, a);
+  if (!split) return hipGetLastError();
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipExtLaunchKernelGGL(k_score_commit, dim3(1), dim3(kThreads), 0, s, nullptr, ev1, 0, a);
   return hipGetLastError();
 }
 
