@@ -1074,28 +1074,76 @@ __global__ __launch_bounds__(256) void k_perm_count_batch(const int32_t* __restr
 }
 
 // Second: one workgroup per block turns its per-chunk counts into the
-// block's counts, offsets and per-chunk first positions (the planning step of
-// permute_body, without a cache). Per block b: routes at b*T*k, counts at
-// b*E, offsets at b*(E+1), non-finite flag at b.
+// block's counts, offsets and per-chunk first positions. Per block b: counts
+// at b*E, offsets at b*(E+1), non-finite flag at b. G threads per expert each
+// keep a contiguous run of at most kPlanPer chunk counts in registers: their
+// partial sums give the expert totals and the offsets (a DPP scan over the
+// experts, 4 per lane), then each run's first positions are written from the
+// registers. (The planning of permute_body without its cache, work-list and
+// record steps.)
 __global__ __launch_bounds__(kPermThreads) void k_perm_plan_batch(
-    const int32_t* __restrict__ topk_idx, int T, int k, int n_chunks,
-    const int32_t* __restrict__ bad_flag, int32_t* __restrict__ chunk_base, PermuteOut o) {
-  __shared__ int32_t s_free[kMaxExperts];
-  __shared__ int32_t s_ftop;
-  __shared__ uint32_t s_res[kMaxExperts / 32], s_pm[kMaxExperts / 32];
-  __shared__ int32_t s_slot[kMaxExperts];
-  const int b = blockIdx.x, E = o.E;
-  const size_t R = static_cast<size_t>(T) * k;
-  PermuteOut ob = o;
-  ob.counts += static_cast<size_t>(b) * E;
-  ob.offsets += static_cast<size_t>(b) * (E + 1);
-  ob.perm += b * R;
-  ob.inv_perm += b * R;
-  if (ob.bad_out) ob.bad_out += b;
-  if ((threadIdx.x >> 6) == 1) prefetch_state(ob.cv, E, 0, s_free, &s_ftop, s_res, s_pm, s_slot);
+    const int32_t* __restrict__ bad_flag, int n_chunks, int32_t* __restrict__ chunk_base,
+    PermuteOut o) {
+  __shared__ int32_t s_part[kPermThreads];
+  __shared__ int32_t s_cnt[kMaxExperts];
+  __shared__ int32_t s_off[kMaxExperts];
+  const int b = blockIdx.x, E = o.E, tid = threadIdx.x;
+  int32_t* cb = chunk_base + static_cast<size_t>(b) * n_chunks * E;
+  const int G = max(1, min(kPermThreads / E, n_chunks));
+  const int per = (n_chunks + G - 1) / G;
+  const int my_g = tid < G * E ? tid / E : -1;
+  const int my_e = my_g >= 0 ? tid - my_g * E : 0;
+  const int ch_lo = my_g >= 0 ? my_g * per : 0;
+  const int ch_hi = my_g >= 0 ? min(n_chunks, ch_lo + per) : 0;
+  int cc[kPlanPer];
+  int sum = 0;
+#pragma unroll
+  for (int q = 0; q < kPlanPer; ++q) {
+    cc[q] = ch_lo + q < ch_hi ? cb[static_cast<size_t>(ch_lo + q) * E + my_e] : 0;
+    sum += cc[q];
+  }
+  if (my_g >= 0) s_part[tid] = sum;
   __syncthreads();
-  permute_body(topk_idx + b * R, T, k, bad_flag[b], ob, s_free, &s_ftop, s_res, s_pm, s_slot,
-               chunk_base + static_cast<size_t>(b) * n_chunks * E, n_chunks);
+  for (int e = tid; e < E; e += kPermThreads) {
+    int c = 0;
+    for (int g = 0; g < G; ++g) c += s_part[g * E + e];
+    s_cnt[e] = c;
+  }
+  __syncthreads();
+  if (tid < 64) {
+    int c[4], tot = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = 4 * tid + q;
+      c[q] = e < E ? s_cnt[e] : 0;
+      tot += c[q];
+    }
+    const int incl = wave_incl_scan(tot);
+    int run = incl - tot;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = 4 * tid + q;
+      if (e < E) {
+        s_off[e] = run;
+        o.counts[static_cast<size_t>(b) * E + e] = c[q];
+        o.offsets[static_cast<size_t>(b) * (E + 1) + e] = run;
+      }
+      run += c[q];
+    }
+    if (tid == 63) o.offsets[static_cast<size_t>(b) * (E + 1) + E] = incl;
+    if (tid == 0 && o.bad_out) o.bad_out[b] = bad_flag[b] ? 1 : 0;
+  }
+  __syncthreads();
+  if (my_g >= 0) {
+    int run = s_off[my_e];
+    for (int h = 0; h < my_g; ++h) run += s_part[h * E + my_e];
+#pragma unroll
+    for (int q = 0; q < kPlanPer; ++q)
+      if (ch_lo + q < ch_hi) {
+        cb[static_cast<size_t>(ch_lo + q) * E + my_e] = run;
+        run += cc[q];
+      }
+  }
 }
 
 // Third: workgroup (c, b) ranks chunk c of block b from its first positions.
@@ -1606,8 +1654,8 @@ hipError_t launch_permute_batch(const int32_t* topk_idx, int B, int T, int k,
                      chunk_base);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_perm_plan_batch, dim3(B), dim3(kPermThreads), 0, s, topk_idx, T, k, n,
-                     bad_flag, chunk_base, o);
+  hipLaunchKernelGGL(k_perm_plan_batch, dim3(B), dim3(kPermThreads), 0, s, bad_flag, n,
+                     chunk_base, o);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (k <= 8)
