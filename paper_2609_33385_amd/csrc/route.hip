@@ -498,7 +498,7 @@ __device__ __forceinline__ void rank_chunk(const int32_t* idx, int t0, int t1, i
                                            int32_t* __restrict__ perm,
                                            int32_t* __restrict__ inv_perm) {
   const int tid = threadIdx.x, nthr = blockDim.x;
-  for (int i = tid; i < kMaskRows * kMaskStride; i += nthr) s_mask[i] = 0u;
+  for (int i = tid; i < E * kMaskStride; i += nthr) s_mask[i] = 0u;
   __syncthreads();
   for (int r = t0 * k + tid; r < t1 * k; r += nthr) {
     const int e = idx[r];
@@ -918,19 +918,16 @@ __global__ __launch_bounds__(kPermThreads) void k_perm_plan(const int32_t* __res
   permute_body(topk_idx, T, k, bad, o, s_free, &s_ftop, s_res, s_pm, s_slot, chunk_base, n_chunks);
 }
 
-// Large blocks, second launch: workgroup c ranks the routes of chunk c from
+// Large blocks, third launch: workgroup c ranks the routes of chunk c from
 // its first positions per expert (chunk_base[c][e]). Thread i takes token
-// i / 2 of the chunk and half (i % 2) of its routes, loaded once into
-// registers. The per-expert token bitmasks sit in rows of kMaskStride = 17
-// words (16 words of 32 tokens, one pad word): the lanes of a wavefront, one
-// 32-token word apart in token order and scattered over experts, then fall in
-// distinct LDS banks (with 16-word rows every expert row began in one of two
-// banks). Each route's rank among the chunk's routes to its expert also
-// places it in a counting sort of the chunk by expert in LDS, so perm is
-// written in contiguous runs per expert (positions s_run[e] + rank) by
-// consecutive lanes instead of one scattered store per lane. Stores go
+// i / 2 of the chunk and half (i % 2) of its routes (at most KH), loaded once
+// into registers, so the lanes of a wavefront share one 32-token word; the
+// per-expert token bitmasks sit in kMaskStride-word rows. Each route's rank
+// among the chunk's routes to its expert also places it in a counting sort of
+// the chunk by expert in LDS, so perm is written in contiguous runs per expert
+// (positions s_run[e] + rank) by consecutive lanes instead of one scattered
+// store per lane. perm (and inv_perm, except on the 16-byte path) is stored
 // through buffer resources of T*k entries: positions outside are dropped.
-
 template <int KH>
 __device__ __forceinline__ void perm_rank_body(const int32_t* __restrict__ topk_idx, int T, int k,
                                                int E, const int32_t* __restrict__ chunk_base,
@@ -971,10 +968,20 @@ __device__ __forceinline__ void perm_rank_body(const int32_t* __restrict__ topk_
 #pragma unroll
   for (int u = 0; u < KH; ++u) a[u] = ev[u] >= 0 && ev[u] < E ? ev[u] * kMaskStride + wofs : kMaskSpare;
 
-  for (int i = tid; i < kMaskRows * kMaskStride; i += kPermThreads) s_mask[i] = 0u;
+  for (int i = tid; i < E * kMaskStride; i += kPermThreads) s_mask[i] = 0u;
+  if (tid < kMaskStride) s_mask[kMaskSpare + tid] = 0u;
   __syncthreads();
+  // token t takes its slots in the order (u + t) mod KH: the tokens of a
+  // 32-token word (one wavefront) often share their best experts, and an LDS
+  // atomic serialises the lanes that hit one address
 #pragma unroll
-  for (int u = 0; u < KH; ++u) atomicOr(&s_mask[a[u]], bit);
+  for (int u = 0; u < KH; ++u) {
+    const int q = (u + lt) & (KH - 1);
+    int aq = a[0];
+#pragma unroll
+    for (int v = 1; v < KH; ++v) aq = q == v ? a[v] : aq;
+    atomicOr(&s_mask[aq], bit);
+  }
   if (tid < E) s_run[tid] = run;
   __syncthreads();
   // word w of expert e is lane w of a 16-lane row: the chunk-local prefix of
