@@ -126,6 +126,40 @@ def test_route_batch_nonfinite_flags():
         _check_block(got, b, lg[b], k, f"block {b} beside a bad one")
 
 
+def test_route_batch_unaligned_route_arrays():
+    """topk_idx and inv_perm 4 bytes off a 16-byte boundary: at k = 8 the
+    counting and ranking launches then take their 4-byte paths instead of the
+    16-byte loads and stores; every output equals the aligned call's."""
+    B, T, E, k = 2, 1500, 128, 8
+    _say(f"[batch] unaligned route arrays B={B} T={T} E={E} k={k}")
+    lg = _logits(B, T, E, 77)
+    ref = _route_batch(lg, k)
+    s = torch.cuda.current_stream()
+    R = T * k
+    raw = {name: torch.full((B * R + 1,), -7, dtype=torch.int32, device="cuda")
+           for name in ("topk_idx", "inv_perm")}
+    dev = dict(topk_idx=raw["topk_idx"][1:],
+               gates=torch.full((B * R,), -1.0, dtype=torch.float32, device="cuda"),
+               counts=torch.full((B * E,), -7, dtype=torch.int32, device="cuda"),
+               offsets=torch.full((B * (E + 1),), -7, dtype=torch.int32, device="cuda"),
+               perm=torch.full((B * R,), -7, dtype=torch.int32, device="cuda"),
+               inv_perm=raw["inv_perm"][1:],
+               nonfinite=torch.full((B,), 9, dtype=torch.int32, device="cuda"))
+    assert dev["topk_idx"].data_ptr() % 16 == 4 and dev["inv_perm"].data_ptr() % 16 == 4
+    ws = torch.empty(oled.oled_route_batch_workspace(B, T, E), dtype=torch.uint8, device="cuda")
+    st = oled.oled_route_batch(torch.from_numpy(lg).cuda(), B, T, E, k, dev["topk_idx"],
+                               dev["gates"], dev["counts"], dev["offsets"], dev["perm"],
+                               dev["inv_perm"], dev["nonfinite"], ws, s)
+    assert st == oled.OLED_OK, oled.last_error(None)
+    torch.cuda.synchronize()
+    got = {key: v.cpu().numpy() for key, v in dev.items()}
+    for key in ("topk_idx", "counts", "offsets", "perm", "inv_perm", "nonfinite"):
+        np.testing.assert_array_equal(got[key].reshape(-1), ref[key].reshape(-1), err_msg=key)
+    np.testing.assert_array_equal(got["gates"].view(np.uint32),
+                                  ref["gates"].reshape(-1).view(np.uint32))
+    assert raw["topk_idx"][0].item() == -7 and raw["inv_perm"][0].item() == -7
+
+
 @pytest.mark.parametrize("B,T,E,k", [(3, 3000, 128, 8), (2, 20000, 64, 8), (4, 37, 16, 4)])
 def test_priority_batch_against_oracle(B, T, E, k):
     _say(f"[batch] priority B={B} T={T} E={E} k={k}")
